@@ -1,0 +1,492 @@
+"""CPU oracle for the DQT linear train step (Direct Quantized Training,
+arXiv 2412.04787).
+
+TEST INFRASTRUCTURE, NOT PRODUCT CODE.  Only ``tests/``,
+``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of ``bench.py`` may
+import or call anything in ``oracle/``.  The HIP library never calls it, and
+this module imports nothing from the HIP package: the two share no code,
+tables or constants.
+
+Everything here is plain numpy, written for readability, not speed.  Exact
+integer work is done in int64 (or in float64 where every partial sum is an
+integer far below 2**53, which makes float64 exact).  Real-valued sums are
+float64.  Where the method itself fixes an fp32 operation (the per-token
+activation scale, the SR step size, the update delta), the oracle performs that
+same single fp32 operation with numpy ``float32`` scalars/arrays, which round
+to nearest-even with no fused multiply-add.
+
+Paper map (section / equation of the DQT paper):
+  * Sec. 3.1, Eq. 1 ........ stochastic rounding SR(x)           -> sr_update
+  * Sec. 3.2, Eq. 2-4 ...... AbsMean init quantisation            -> absmean_init
+  * Sec. 3.2 (BitNet 8-bit activations, forward with W~) ......... -> act_quant,
+                                                                      linear_fwd
+  * Sec. 3.2 (backprop to the gradient of W~, no STE on weights) -> linear_bwd
+  * Sec. 3.2, Eq. 5 ........ direct update W^ = SR(W')            -> sr_update
+  * Sec. 5.2 ............... fraction of weights changed per step -> n_changed
+
+Readings of points the paper leaves open (each is listed in the design doc):
+  R1  SR acts in grid units: with W~ = q * alpha (alpha = 1/s, Eq. 3) and
+      W' = W~ - lr * grad, the updated code is SR(W' / alpha).  This is what
+      the worked example of Sec. 5 (a value -1 + 0.02 goes to 0 with
+      probability 2%) requires.
+  R2  Ternary grid is {-1, 0, 1}; n-bit grid is [qmin, qmax] given by the
+      caller (Eq. 3 gives -2^(n-1) .. 2^(n-1)-1; 8-bit configs may use
+      -127..127).
+  R3  alpha is fixed at initialisation and never recomputed (Eq. 2-4 are
+      skipped during training, Sec. 3.2).
+  R4  Activations: per-token absmax to int8 with the constant 127, eps 1e-5
+      and clamp to [-128, 127]; or to OCP e4m3 with the constant 448.
+  R5  The backward treats activation quantisation as pass-through and uses
+      the dequantised activation X~ (in the environment dtype) for dW.
+  R6  The optimiser target is the plain step W' = W~ - lr * grad.
+  R7  Random bits: Philox4x32-10 with the counter layout of ``rng_u32``;
+      Bernoulli(p) is realised as U < ceil(p * 2**32) with U uniform on
+      [0, 2**32).
+  R8  A non-finite gradient entry leaves its weight unchanged and is counted.
+"""
+
+from __future__ import annotations
+
+import numpy as np
+
+# ---------------------------------------------------------------------------
+# Number formats.  Each converter is written from the format's definition:
+# enumerate / bracket the representable values and pick the nearest one, ties
+# to the value whose last significand bit is 0.
+# ---------------------------------------------------------------------------
+
+
+def bf16_round(x) -> np.ndarray:
+    """fp32 -> bf16 bit pattern (uint16), round to nearest, ties to even.
+
+    bf16 keeps the sign, the 8 exponent bits and the top 7 fraction bits of an
+    fp32 value.  For a finite input the two candidates are the value with the
+    low 16 bits cleared (toward zero) and the next bf16 value away from zero;
+    the nearer one wins, and on a tie the one with an even last bit.
+    Only finite inputs are expected here.
+    """
+    x = np.asarray(x, dtype=np.float32)
+    bits = x.view(np.uint32).astype(np.uint64)
+    toward_zero = (bits >> np.uint64(16))  # bf16 pattern, magnitude rounded down
+    away = toward_zero + np.uint64(1)      # next magnitude up (carries into exp)
+    v_tz = (toward_zero << np.uint64(16)).astype(np.uint32).view(np.float32).astype(np.float64)
+    v_aw = (away << np.uint64(16)).astype(np.uint32).view(np.float32).astype(np.float64)
+    xv = x.astype(np.float64)
+    d_tz = np.abs(xv - v_tz)
+    d_aw = np.abs(v_aw - xv)
+    pick_away = (d_aw < d_tz) | ((d_aw == d_tz) & ((toward_zero & np.uint64(1)) == np.uint64(1)))
+    out = np.where(pick_away, away, toward_zero)
+    return out.astype(np.uint16)
+
+
+def bf16_to_f32(b) -> np.ndarray:
+    """bf16 bit pattern (uint16) -> fp32 value (exact)."""
+    b = np.asarray(b, dtype=np.uint16).astype(np.uint32)
+    return (b << np.uint32(16)).view(np.float32)
+
+
+def _e4m3_table() -> np.ndarray:
+    """Value of every OCP E4M3 ('fn') code, NaN for the two NaN codes.
+
+    Layout: 1 sign bit, 4 exponent bits (bias 7), 3 fraction bits.
+    exponent 0 is subnormal: value = frac/8 * 2**(1-7).
+    S.1111.111 is NaN; there are no infinities, so the largest finite
+    magnitude is 1.75 * 2**8 = 448.
+    """
+    vals = np.empty(256, dtype=np.float64)
+    for code in range(256):
+        sign = -1.0 if code & 0x80 else 1.0
+        e = (code >> 3) & 0xF
+        f = code & 0x7
+        if e == 0xF and f == 0x7:
+            vals[code] = np.nan
+        elif e == 0:
+            vals[code] = sign * (f / 8.0) * 2.0 ** (1 - 7)
+        else:
+            vals[code] = sign * (1.0 + f / 8.0) * 2.0 ** (e - 7)
+    return vals
+
+
+E4M3_VALUES = _e4m3_table()
+E4M3_MAX = 448.0
+
+
+def e4m3_encode(x) -> np.ndarray:
+    """fp32 -> OCP E4M3 code (uint8): round to nearest, ties to even fraction,
+    saturating to +-448.  The sign bit is kept (so -0.0 -> 0x80).
+
+    Brute force: for each magnitude, find the nearest of the 127 non-negative
+    finite codes (0x00..0x7E, increasing in value), ties to the even code.
+    """
+    x = np.asarray(x, dtype=np.float32).astype(np.float64)
+    sign = np.signbit(x)
+    a = np.minimum(np.abs(x), E4M3_MAX)
+    pos = E4M3_VALUES[:0x7F]                        # 0x00 .. 0x7E, sorted
+    hi = np.searchsorted(pos, a, side="left")       # first code with value >= a
+    hi = np.clip(hi, 0, 0x7E)
+    lo = np.clip(hi - 1, 0, 0x7E)
+    d_lo = np.abs(a - pos[lo])
+    d_hi = np.abs(pos[hi] - a)
+    pick_hi = (d_hi < d_lo) | ((d_hi == d_lo) & (hi % 2 == 0))
+    code = np.where(pick_hi, hi, lo).astype(np.uint8)
+    return np.where(sign, code | np.uint8(0x80), code).astype(np.uint8)
+
+
+def e4m3_decode(code) -> np.ndarray:
+    """OCP E4M3 code -> float64 value (exact)."""
+    return E4M3_VALUES[np.asarray(code, dtype=np.uint8)]
+
+
+# ---------------------------------------------------------------------------
+# Weight storage: packed ternary codes.
+# ---------------------------------------------------------------------------
+
+
+def pack_ternary(q: np.ndarray) -> np.ndarray:
+    """int8 ternary [d_out, d_in] -> packed uint8 [d_out, d_in/4].
+
+    Weight (n, k) is stored as the 2-bit code q + 1 in byte k // 4 of row n,
+    at bit offset 2 * (k % 4).
+    """
+    q = np.asarray(q)
+    d_out, d_in = q.shape
+    assert d_in % 4 == 0
+    codes = (q.astype(np.int64) + 1).reshape(d_out, d_in // 4, 4)
+    assert codes.min() >= 0 and codes.max() <= 2
+    packed = np.zeros((d_out, d_in // 4), dtype=np.int64)
+    for j in range(4):
+        packed |= codes[:, :, j] << (2 * j)
+    return packed.astype(np.uint8)
+
+
+def unpack_ternary(packed: np.ndarray, d_in: int) -> np.ndarray:
+    """Inverse of pack_ternary: packed uint8 [d_out, d_in/4] -> int8 [d_out, d_in]."""
+    packed = np.asarray(packed, dtype=np.uint8).astype(np.int64)
+    d_out = packed.shape[0]
+    out = np.empty((d_out, d_in // 4, 4), dtype=np.int64)
+    for j in range(4):
+        out[:, :, j] = ((packed >> (2 * j)) & 3) - 1
+    return out.reshape(d_out, d_in).astype(np.int8)
+
+
+# ---------------------------------------------------------------------------
+# Sec. 3.2, Eq. 2-4: AbsMean initial quantisation (one-time, not per step).
+# ---------------------------------------------------------------------------
+
+
+def absmean(W) -> float:
+    """Eq. 2: the mean absolute value over every element of the tensor (fp64)."""
+    W = np.asarray(W, dtype=np.float64)
+    return float(np.mean(np.abs(W)))
+
+
+def absmean_init(W0, qmin: int, qmax: int):
+    """Eq. 3-4: s = Q_p / AbsMean(W);  q = Clip(Round(W * s), Q_n, Q_p).
+
+    Returns the integer codes q (int8) and the dequantisation scale
+    alpha = 1/s = AbsMean(W) / Q_p rounded once to fp32, so that the quantised
+    weight of Eq. 4 is q * alpha.  Round() is half-to-even (``np.rint``).
+    The products W * s are formed in fp64.
+    """
+    am = absmean(W0)
+    s = qmax / am
+    q = np.clip(np.rint(np.asarray(W0, dtype=np.float64) * s), qmin, qmax)
+    alpha = np.float32(am / qmax)
+    return q.astype(np.int8), alpha
+
+
+# ---------------------------------------------------------------------------
+# Sec. 3.2: 8-bit activation quantisation (BitNet convention, reading R4).
+# ---------------------------------------------------------------------------
+
+ACT_EPS = np.float32(1e-5)
+
+
+def act_quant(X, kind: str):
+    """Per-token absmax quantisation of X [M, K] (fp32 values).
+
+    g_m   = max(max_k |x_mk|, 1e-5)                 (fp32)
+    int8: inv_m = 127 / g_m ; Xq = clamp(rint(x * inv_m), -128, 127)
+          d_m   = g_m / 127
+    e4m3: inv_m = 448 / g_m ; Xq = e4m3(x * inv_m) ; d_m = g_m / 448
+    Each division and the product x * inv_m is one correctly rounded fp32
+    operation.  Returns (Xq, d) with Xq int8 or uint8 (e4m3 codes) and d fp32.
+    """
+    X = np.asarray(X, dtype=np.float32)
+    M = X.shape[0]
+    g = np.empty(M, dtype=np.float32)
+    for m in range(M):
+        row_max = np.float32(np.max(np.abs(X[m]))) if X.shape[1] else np.float32(0)
+        g[m] = max(row_max, ACT_EPS)
+    if kind == "i8":
+        qmax_act = np.float32(127.0)
+    elif kind == "e4m3":
+        qmax_act = np.float32(448.0)
+    else:
+        raise ValueError(kind)
+    inv = (qmax_act / g).astype(np.float32)            # fp32 division
+    d = (g / qmax_act).astype(np.float32)              # fp32 division
+    scaled = (X * inv[:, None]).astype(np.float32)     # one fp32 multiply
+    if kind == "i8":
+        Xq = np.clip(np.rint(scaled), -128, 127).astype(np.int8)
+    else:
+        Xq = e4m3_encode(scaled)
+    return Xq, d
+
+
+def act_values(Xq, kind: str) -> np.ndarray:
+    """Integer / e4m3 activation codes as exact float64 values."""
+    if kind == "i8":
+        return np.asarray(Xq, dtype=np.int8).astype(np.float64)
+    return e4m3_decode(Xq)
+
+
+def act_dequant(Xq, d, kind: str, xt: str) -> np.ndarray:
+    """X~[m, k] = Xq[m, k] * d_m as one fp32 multiply, then cast to the
+    environment dtype xt ('f32' or 'bf16').  Returned as float64 values."""
+    v = act_values(Xq, kind).astype(np.float32)
+    xt32 = (v * np.asarray(d, dtype=np.float32)[:, None]).astype(np.float32)
+    if xt == "f32":
+        return xt32.astype(np.float64)
+    if xt == "bf16":
+        return bf16_to_f32(bf16_round(xt32)).astype(np.float64)
+    raise ValueError(xt)
+
+
+def cast_out(y32: np.ndarray, out: str) -> np.ndarray:
+    """Cast fp32 results to the output dtype; returns fp32 (bf16 values widened)."""
+    y32 = np.asarray(y32, dtype=np.float32)
+    if out == "f32":
+        return y32
+    if out == "bf16":
+        return bf16_to_f32(bf16_round(y32))
+    raise ValueError(out)
+
+
+# ---------------------------------------------------------------------------
+# Sec. 3.2: forward with the quantised weights and quantised activations.
+# ---------------------------------------------------------------------------
+
+
+def linear_fwd(Xq, d, kind: str, q, alpha, out: str = "f32"):
+    """Y = X~ W~^T with X~ = Xq * d_m and W~ = q * alpha (nn.Linear layout:
+    q is [d_out, d_in], Y is [M, d_out]).
+
+    acc[m, n] = sum_k Xq[m, k] * q[n, k] is formed exactly (every product and
+    partial sum is an integer, or for e4m3 a multiple of 2**-9, well inside
+    float64's 53-bit significand, so a float64 matmul is exact in any order).
+    Then f_m = fl32(d_m * alpha) and y = fl32(fl32(acc) * f_m), cast to `out`.
+    """
+    a = act_values(Xq, kind)
+    w = np.asarray(q, dtype=np.int8).astype(np.float64)
+    acc = a @ w.T
+    if kind == "i8":
+        assert np.all(np.abs(acc) < 2.0 ** 31)
+    f = (np.asarray(d, dtype=np.float32) * np.float32(alpha)).astype(np.float32)
+    y32 = (acc.astype(np.float32) * f[:, None]).astype(np.float32)
+    return cast_out(y32, out), acc
+
+
+# ---------------------------------------------------------------------------
+# Sec. 3.2: backward.  No straight-through estimator on the weights: the
+# gradient is taken with respect to W~ itself; activation quantisation is
+# treated as pass-through (reading R5).
+# ---------------------------------------------------------------------------
+
+
+def linear_bwd(dY, q, alpha, Xq, d, kind: str, xt: str, dx_out: str = "f32"):
+    """dX = dY W~ = alpha * (dY @ q)          [M, d_in]
+    dW = dY^T X~                              [d_out, d_in], fp32
+
+    Sums in float64; dX is cast to `dx_out`, dW rounded once to fp32.
+    Returns (dX, dW, dX64, dW64) where the *64 arrays are the unrounded sums.
+    """
+    dY = np.asarray(dY, dtype=np.float64)
+    w = np.asarray(q, dtype=np.int8).astype(np.float64)
+    xt_vals = act_dequant(Xq, d, kind, xt)
+    dX64 = float(alpha) * (dY @ w)
+    dW64 = dY.T @ xt_vals
+    dX = cast_out(dX64.astype(np.float32), dx_out)
+    dW = dW64.astype(np.float32)
+    return dX, dW, dX64, dW64
+
+
+# ---------------------------------------------------------------------------
+# Random bits: Philox4x32-10 (Salmon, Moraes, Dror, Shaw, "Parallel random
+# numbers: as easy as 1, 2, 3", SC'11).  Counter-based: the output depends
+# only on (counter, key), so there is no state to carry between steps.
+# ---------------------------------------------------------------------------
+
+PHILOX_M0 = 0xD2511F53
+PHILOX_M1 = 0xCD9E8D57
+PHILOX_W0 = 0x9E3779B9   # key schedule increments (golden ratio, sqrt(3)-1)
+PHILOX_W1 = 0xBB67AE85
+_MASK32 = np.uint64(0xFFFFFFFF)
+
+
+def philox4x32_10(ctr, key):
+    """Philox4x32 with 10 rounds, vectorised over numpy arrays.
+
+    ctr: 4 arrays (or scalars) of uint32 words c0..c3;  key: 2 words k0, k1.
+    One round: multiply c0 by M0 and c2 by M1 into 64-bit products, then
+      (c0, c1, c2, c3) <- (hi(M1*c2) ^ c1 ^ k0, lo(M1*c2),
+                           hi(M0*c0) ^ c3 ^ k1, lo(M0*c0));
+    between rounds the key is bumped by (W0, W1) modulo 2**32.
+    """
+    c = [np.asarray(v, dtype=np.uint64) & _MASK32 for v in ctr]
+    k0 = np.asarray(key[0], dtype=np.uint64) & _MASK32
+    k1 = np.asarray(key[1], dtype=np.uint64) & _MASK32
+    m0 = np.uint64(PHILOX_M0)
+    m1 = np.uint64(PHILOX_M1)
+    for rnd in range(10):
+        if rnd > 0:
+            k0 = (k0 + np.uint64(PHILOX_W0)) & _MASK32
+            k1 = (k1 + np.uint64(PHILOX_W1)) & _MASK32
+        p0 = c[0] * m0
+        p1 = c[2] * m1
+        c = [
+            ((p1 >> np.uint64(32)) ^ c[1] ^ k0) & _MASK32,
+            p1 & _MASK32,
+            ((p0 >> np.uint64(32)) ^ c[3] ^ k1) & _MASK32,
+            p0 & _MASK32,
+        ]
+    return [v.astype(np.uint32) for v in c]
+
+
+def _half16(seed: int, step: int, tensor_id: int, idx: np.ndarray, dom: int) -> np.ndarray:
+    """16-bit draw for each element index in idx from stream `dom` (0 or 1).
+
+    Counter = (lo32(i >> 3), hi32(i >> 3) | dom << 31, step, tensor_id),
+    key = (lo32(seed), hi32(seed)).  One Philox call serves 8 consecutive
+    elements: element i takes output word (i & 7) >> 1, its low 16 bits when
+    i is even and its high 16 bits when i is odd.
+    """
+    idx = np.asarray(idx, dtype=np.uint64)
+    # one Philox call per distinct block of 8 elements
+    blk, inv = np.unique(idx >> np.uint64(3), return_inverse=True)
+    inv = inv.ravel()
+    c0 = blk & _MASK32
+    c1 = (blk >> np.uint64(32)) | np.uint64(dom << 31)
+    c2 = np.full_like(blk, np.uint64(step & 0xFFFFFFFF))
+    c3 = np.full_like(blk, np.uint64(tensor_id & 0xFFFFFFFF))
+    seed = int(seed) & 0xFFFFFFFFFFFFFFFF
+    words = philox4x32_10((c0, c1, c2, c3), (seed & 0xFFFFFFFF, seed >> 32))
+    words = np.stack(words).astype(np.uint64)           # [4, n_blocks]
+    w_sel = ((idx & np.uint64(7)) >> np.uint64(1)).astype(np.int64)
+    word = words[w_sel, inv]
+    shift = (idx & np.uint64(1)) * np.uint64(16)
+    return ((word >> shift) & np.uint64(0xFFFF)).astype(np.uint32)
+
+
+def rng_u32(seed: int, step: int, tensor_id: int, idx) -> np.ndarray:
+    """U(i) = (P16(i) << 16) | S16(i): a 32-bit uniform draw per element,
+    P16 from stream 0 and S16 from stream 1 (reading R7)."""
+    idx = np.atleast_1d(np.asarray(idx, dtype=np.uint64))
+    p = _half16(seed, step, tensor_id, idx, 0)
+    s = _half16(seed, step, tensor_id, idx, 1)
+    return ((p.astype(np.uint64) << np.uint64(16)) | s.astype(np.uint64)).astype(np.uint32)
+
+
+# ---------------------------------------------------------------------------
+# Sec. 3.1 Eq. 1 and Sec. 3.2 Eq. 5: direct stochastic-rounding update.
+# ---------------------------------------------------------------------------
+
+
+def sr_step_size(lr, alpha) -> np.float32:
+    """c = fl32(lr / alpha): the learning rate expressed in grid units."""
+    return np.float32(np.float32(lr) / np.float32(alpha))
+
+
+def sr_update(q, g, lr, alpha, qmin: int, qmax: int, seed: int, step: int,
+              tensor_id: int, idx=None):
+    """Eq. 5 in grid units (reading R1): q^ = Clip(SR(q + delta), qmin, qmax)
+    with delta = -fl32(c * g) and c = fl32(lr / alpha).
+
+    Eq. 1: with x = q + delta, SR(x) is floor(x) with probability
+    ceil(x) - x, else ceil(x).  q is an integer, so floor/ceil of x are q plus
+    floor/ceil of delta, and the probabilities are formed from delta alone
+    (which keeps them exact):
+      delta >= 0:  x rounds up   to q + floor(delta) + 1  w.p. delta - floor(delta)
+      delta <  0:  x rounds down to q + ceil(delta)  - 1  w.p. ceil(delta) - delta
+    A Bernoulli(p) event is U < ceil(p * 2**32) with U = rng_u32(...) (R7).
+
+    q, g: flat arrays of the same length.  idx: flat element indices (default
+    0..n-1) used to key the random draws.  Returns (q_new int64, n_changed,
+    n_nonfinite).
+    """
+    q = np.asarray(q).astype(np.int64).ravel()
+    g = np.asarray(g, dtype=np.float32).ravel()
+    if idx is None:
+        idx = np.arange(q.size, dtype=np.uint64)
+    c = sr_step_size(lr, alpha)
+    finite = np.isfinite(g)
+    with np.errstate(over="ignore", invalid="ignore"):
+        delta32 = -(c * np.where(finite, g, np.float32(0))).astype(np.float32)
+    delta = delta32.astype(np.float64)
+    U = rng_u32(seed, step, tensor_id, idx).astype(np.float64)
+
+    new = np.empty_like(q)
+    big = ~np.isfinite(delta)                 # |c*g| overflowed fp32
+    d_ok = np.where(big, 0.0, delta)
+    up_side = d_ok >= 0
+    fl = np.floor(d_ok)
+    ce = np.ceil(d_ok)
+    p = np.where(up_side, d_ok - fl, ce - d_ok)          # exact in float64
+    thresh = np.ceil(p * 2.0 ** 32)
+    event = U < thresh
+    base = np.where(up_side, fl, ce)
+    move = base + np.where(event, np.where(up_side, 1.0, -1.0), 0.0)
+    x_new = q.astype(np.float64) + move
+    x_new = np.where(big, np.where(delta > 0, np.inf, -np.inf), x_new)
+    new = np.clip(x_new, qmin, qmax).astype(np.int64)
+    new = np.where(finite, new, q)
+    n_changed = int(np.count_nonzero(new != q))
+    n_nonfinite = int(np.count_nonzero(~finite))
+    return new, n_changed, n_nonfinite
+
+
+def sr_change_probability(q, g, lr, alpha, qmin: int, qmax: int) -> np.ndarray:
+    """Per-element probability that the SR update changes the code (used for
+    the Poisson-binomial check of n_changed).  Probabilities are taken at the
+    2**-32 resolution of R7."""
+    q = np.asarray(q).astype(np.int64).ravel()
+    g = np.asarray(g, dtype=np.float32).ravel()
+    c = sr_step_size(lr, alpha)
+    delta = (-(c * g)).astype(np.float32).astype(np.float64)
+    fl = np.floor(delta)
+    frac = delta - fl
+    p_hi = np.ceil(frac * 2.0 ** 32) / 2.0 ** 32        # P(x -> q + fl + 1)
+    lo_val = np.clip(q + fl, qmin, qmax)
+    hi_val = np.clip(q + fl + 1, qmin, qmax)
+    return np.where(lo_val != q, 1.0 - p_hi, 0.0) + np.where(hi_val != q, p_hi, 0.0)
+
+
+def linear_train_step(X, dY, q, alpha, qmin, qmax, *, act: str, xt: str,
+                      y_out: str, dx_out: str, lr, seed, step, tensor_id):
+    """One full DQT linear step: act-quant, forward, backward, SR update.
+
+    Returns a dict of every intermediate, for comparison with the HIP path.
+    """
+    Xq, d = act_quant(X, act)
+    Y, acc = linear_fwd(Xq, d, act, q, alpha, y_out)
+    dX, dW, _, _ = linear_bwd(dY, q, alpha, Xq, d, act, xt, dx_out)
+    q_new, n_changed, n_nonfinite = sr_update(q, dW, lr, alpha, qmin, qmax,
+                                              seed, step, tensor_id)
+    return dict(Xq=Xq, d=d, Y=Y, acc=acc, dX=dX, dW=dW,
+                q_new=q_new.reshape(np.asarray(q).shape), n_changed=n_changed,
+                n_nonfinite=n_nonfinite)
+
+
+def gemm_abs_bound(A, B) -> np.ndarray:
+    """|A| @ |B| in float64: the sum of absolute terms of each output of A @ B,
+    used to scale componentwise tolerances."""
+    return np.abs(np.asarray(A, dtype=np.float64)) @ np.abs(np.asarray(B, dtype=np.float64))
+
+
+__all__ = [
+    "bf16_round", "bf16_to_f32", "E4M3_VALUES", "e4m3_encode", "e4m3_decode",
+    "pack_ternary", "unpack_ternary", "absmean", "absmean_init", "act_quant",
+    "act_values", "act_dequant", "cast_out", "linear_fwd", "linear_bwd",
+    "philox4x32_10", "rng_u32", "sr_step_size", "sr_update",
+    "sr_change_probability", "linear_train_step", "gemm_abs_bound",
+]
