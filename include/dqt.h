@@ -1,0 +1,218 @@
+/*
+ * dqt.h -- C ABI of libdqt, the training step of a DQT linear layer on
+ * AMD MI355X (gfx950).
+ *
+ * Direct Quantized Training (Zhao et al., "Direct Quantized Training of
+ * Language Models with Stochastic Rounding", arXiv 2412.04787) keeps every
+ * weight matrix on an n-bit integer grid for the whole of training: the
+ * weight is W~ = q * alpha with integer codes q in [qmin, qmax] and one fp32
+ * scale per tensor (Sec. 3.2, Eq. 2-4; alpha = 1/s of Eq. 3, fixed after
+ * initialisation).  A step is
+ *   1. quantise the activations to 8 bits per token       (Sec. 3.2, BitNet),
+ *   2. forward  Y  = X~ W~^T                               (Sec. 3.2),
+ *   3. backward dX = dY W~ and dW = dY^T X~                (Sec. 3.2, no STE),
+ *   4. direct update q <- Clip(SR(q - lr * dW / alpha))    (Sec. 3.1 Eq. 1,
+ *                                                           Sec. 3.2 Eq. 5).
+ *
+ * Conventions for every entry point:
+ *  - Tensor pointers are DEVICE pointers unless marked "host".  The caller
+ *    owns every buffer; the library never allocates or frees memory on these
+ *    calls and holds no mutable global state, so calls on different streams
+ *    or devices may run concurrently (as long as their buffers differ).
+ *  - Layouts are row-major.  W is [d_out, d_in] (nn.Linear); X is [M, d_in];
+ *    Y and dY are [M, d_out].  M is the number of tokens.
+ *  - `stream` is a hipStream_t (NULL = the legacy default stream).  Every
+ *    device entry point is asynchronous on that stream.
+ *  - All arguments are checked before anything is enqueued; on an error
+ *    nothing is launched and the status says why.  A launch failure reported
+ *    by the runtime returns DQT_ERR_HIP.  Faults during execution surface at
+ *    the caller's next synchronisation.  Nothing throws or aborts.
+ *  - Shapes: d_in and d_out are multiples of 16 and at least 16; M >= 0 (any
+ *    value, M = 0 is a no-op except that dW is then written as zeros).
+ *    Base pointers must be 16-byte aligned.
+ *  - Non-finite values in X or dY are not checked.
+ */
+#ifndef DQT_H
+#define DQT_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  DQT_OK = 0,
+  DQT_ERR_NULL = 1,        /* a required pointer is NULL                      */
+  DQT_ERR_SHAPE = 2,       /* a dimension is negative, too small or unaligned */
+  DQT_ERR_ALIGN = 3,       /* a base pointer is not 16-byte aligned           */
+  DQT_ERR_DTYPE = 4,       /* a dtype is not allowed in that position         */
+  DQT_ERR_RANGE = 5,       /* qmin/qmax/alpha/lr out of range                 */
+  DQT_ERR_WORKSPACE = 6,   /* workspace missing or smaller than required      */
+  DQT_ERR_UNSUPPORTED = 7, /* a valid but unimplemented combination          */
+  DQT_ERR_HIP = 8          /* the HIP runtime reported an error               */
+} dqt_status;
+
+typedef enum {
+  DQT_F32 = 0,        /* IEEE binary32                                        */
+  DQT_BF16 = 1,       /* bfloat16                                             */
+  DQT_I8 = 2,         /* int8                                                 */
+  DQT_FP8E4M3 = 3,    /* OCP E4M3 ("fn": bias 7, max 448, no inf)             */
+  DQT_TERNARY2 = 4    /* packed 2-bit ternary weight codes, see dqt_weight    */
+} dqt_dtype;
+
+/*
+ * Weight descriptor (Sec. 3.2).
+ *   wfmt = DQT_TERNARY2: q in {-1, 0, 1}; weight (n, k) is stored as the
+ *          2-bit code q + 1 in byte n * (d_in / 4) + k / 4, bit offset
+ *          2 * (k % 4).  Code 3 is never written and must not appear.
+ *          Requires qmin = -1, qmax = 1.
+ *   wfmt = DQT_I8: one int8 code per weight, [d_out, d_in] row-major.
+ *          Requires -128 <= qmin < qmax <= 127 (Eq. 3 gives -2^(n-1) ..
+ *          2^(n-1) - 1; a symmetric -127..127 grid is also allowed).
+ *   alpha: dequantisation scale, the weight's real value is q * alpha
+ *          (alpha = 1/s, Eq. 3).  Finite and > 0.  Fixed for the life of the
+ *          tensor: the library never recomputes it (Sec. 3.2 skips Eq. 2-4
+ *          after initialisation).
+ *   tensor_id: separates the random streams of different tensors in
+ *          dqt_sr_update.
+ */
+typedef struct {
+  int32_t d_out;
+  int32_t d_in;
+  int32_t wfmt;       /* dqt_dtype: DQT_TERNARY2 or DQT_I8 */
+  int32_t qmin;
+  int32_t qmax;
+  float alpha;
+  uint32_t tensor_id;
+  uint32_t reserved;  /* must be 0 */
+} dqt_weight;
+
+/*
+ * Per-token activation quantisation (Sec. 3.2: inputs and activations are
+ * quantised to 8 bits following BitNet).  For each row m of X [M, K]:
+ *   g_m = max(max_k |x_mk|, 1e-5)
+ *   act_q = DQT_I8:      Xq = clamp(rint(x * fl(127/g_m)), -128, 127),
+ *                        xdq[m] = fl(g_m / 127)
+ *   act_q = DQT_FP8E4M3: Xq = e4m3_rne_saturate(x * fl(448/g_m)),
+ *                        xdq[m] = fl(g_m / 448)
+ * Each product and quotient is one correctly rounded fp32 operation.
+ *   X:   [M, K], x_t = DQT_F32 or DQT_BF16.   (input)
+ *   Xq:  [M, K] int8 or e4m3 bytes.           (output)
+ *   xdq: [M] fp32 dequantisation scales.      (output)
+ * K must be a multiple of 16.
+ */
+dqt_status dqt_act_quant(const void* X, int32_t x_t, int64_t M, int32_t K,
+                         int32_t act_q, void* Xq, float* xdq, void* stream);
+
+/*
+ * Forward of a DQT linear (Sec. 3.2):  Y = X~ W~^T, i.e.
+ *   acc[m, n] = sum_k Xq[m, k] * q[n, k]     (int32, exact, for int8 codes;
+ *                                             fp32 MFMA sum for e4m3 codes)
+ *   Y[m, n]   = fl(fl(acc) * fl(xdq[m] * alpha)), cast to y_t (RNE).
+ *   w, Wq: weight descriptor (host) and codes (device).
+ *   X:     [M, d_in] (x_t = DQT_F32/DQT_BF16), or NULL when Xq/xdq already
+ *          hold this input's quantised form (several linears sharing one
+ *          input quantise it once with dqt_act_quant).
+ *   act_q: DQT_I8 or DQT_FP8E4M3 (e4m3 needs wfmt = DQT_TERNARY2).
+ *   Xq, xdq: [M, d_in] codes and [M] scales; written when X != NULL, read
+ *          otherwise.  Keep them for dqt_linear_bwd.
+ *   Y:     [M, d_out], y_t = DQT_F32 or DQT_BF16.  (output)
+ */
+dqt_status dqt_linear_fwd(const dqt_weight* w, const void* Wq,
+                          const void* X, int32_t x_t, int64_t M, int32_t act_q,
+                          void* Xq, float* xdq,
+                          void* Y, int32_t y_t, void* stream);
+
+/* Bytes of device workspace dqt_linear_bwd needs for this weight and M
+ * (0 if none).  Depends only on (d_out, d_in, M). */
+size_t dqt_linear_bwd_workspace(const dqt_weight* w, int64_t M);
+
+/*
+ * Backward of a DQT linear (Sec. 3.2).  The gradient is taken with respect to
+ * the quantised weight W~ itself (no straight-through estimator on weights);
+ * the activation quantiser is treated as the identity (BitNet convention):
+ *   dX[m, k] = alpha * sum_n dY[m, n] * q[n, k]          cast to dx_t
+ *   dW[n, k] = sum_m dY[m, n] * X~[m, k]                 fp32
+ * with X~[m, k] = cast_xt(fl(value(Xq[m, k]) * xdq[m])), the dequantised
+ * activation in the environment dtype xt_t (DQT_F32 or DQT_BF16).
+ * Products of bf16 operands are summed in fp32 by the matrix cores; with
+ * xt_t = DQT_F32 the operands are fp32 (dY must then be DQT_F32).
+ *   dY: [M, d_out], dy_t = DQT_F32 or DQT_BF16.
+ *   dX: [M, d_in] or NULL (skipped); dx_t = DQT_F32 or DQT_BF16.
+ *   dW: [d_out, d_in] fp32 or NULL (skipped); overwritten, never accumulated.
+ *   ws, ws_bytes: device workspace of at least dqt_linear_bwd_workspace()
+ *   bytes (may be NULL if that is 0).  Results do not depend on timing: the
+ *   split reduction over tokens is summed in a fixed order.
+ */
+dqt_status dqt_linear_bwd(const dqt_weight* w, const void* Wq,
+                          const void* Xq, int32_t act_q, const float* xdq,
+                          const void* dY, int32_t dy_t, int64_t M, int32_t xt_t,
+                          void* dX, int32_t dx_t, float* dW,
+                          void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Direct stochastic-rounding update (Sec. 3.1 Eq. 1 and Sec. 3.2 Eq. 5),
+ * in place on Wq.  In grid units the optimiser target W' = W~ - lr * dW is
+ * x = q + delta with delta = -fl(c * dW), c = fl(lr / alpha) (formed once on
+ * the host).  Eq. 1 rounds x to floor(x) with probability ceil(x) - x and to
+ * ceil(x) otherwise; the result is clipped to [qmin, qmax] and stored back.
+ * Random bits for element i = n * d_in + k (32 bits, exact 2^-32
+ * resolution): U(i) = P16(i) << 16 | S16(i), where P16/S16 are 16-bit halves
+ * of Philox4x32-10 (Salmon et al., SC'11) with key (lo32(seed), hi32(seed))
+ * and counter (lo32(i >> 3), hi32(i >> 3) | s << 31, step, tensor_id),
+ * s = 0 for P16 and 1 for S16; element i takes output word (i & 7) >> 1, low
+ * half for even i, high half for odd i.  The move away from q's side
+ * happens iff U < ceil(p * 2^32) where p is the distance of x from the grid
+ * point on q's side.
+ *   dW:  [d_out, d_in] fp32.  A non-finite entry leaves its weight unchanged
+ *        and is counted in counters[1].
+ *   lr:  finite, >= 0.
+ *   counters: NULL, or device uint64[2] to which the number of changed
+ *        weights and of non-finite gradient entries are ADDED.
+ * Each thread owns whole bytes of Wq, so the update has no write races and
+ * is bit-reproducible for a given (seed, step, tensor_id).
+ */
+dqt_status dqt_sr_update(const dqt_weight* w, void* Wq, const float* dW,
+                         float lr, uint64_t seed, uint32_t step,
+                         unsigned long long* counters, void* stream);
+
+/*
+ * Helpers (not on the timed path).
+ */
+
+/* The 32-bit draws U(i), i = i0 .. i0 + n - 1, of dqt_sr_update, written to
+ * device out[n].  For checking the random stream. */
+dqt_status dqt_debug_rng(uint64_t seed, uint32_t step, uint32_t tensor_id,
+                         uint64_t i0, int64_t n, uint32_t* out, void* stream);
+
+/* AbsMean initial quantisation on the host (Sec. 3.2, Eq. 2-4):
+ *   AbsMean = mean |W0| (sum in fp64, index order), s = qmax / AbsMean,
+ *   q = clip(rint(W0 * s), qmin, qmax) with the product in fp64,
+ *   alpha = fl32(AbsMean / qmax).
+ * W0: host fp32 [n]; q: host int8 [n] (output); alpha: host (output).
+ * Returns DQT_ERR_RANGE when AbsMean is 0 or not finite. */
+dqt_status dqt_absmean_init(const float* W0, int64_t n, int32_t qmin,
+                            int32_t qmax, int8_t* q, float* alpha);
+
+/* Host packing of ternary codes into the DQT_TERNARY2 layout and back.
+ * q: host int8 [rows, cols] in {-1, 0, 1}; packed: host uint8 [rows, cols/4];
+ * cols must be a multiple of 4.  pack returns DQT_ERR_RANGE (and stops) on a
+ * value outside {-1, 0, 1}. */
+dqt_status dqt_pack_ternary(const int8_t* q, int64_t rows, int64_t cols,
+                            uint8_t* packed);
+dqt_status dqt_unpack_ternary(const uint8_t* packed, int64_t rows,
+                              int64_t cols, int8_t* q);
+
+/* Human-readable name of a status code (static storage). */
+const char* dqt_status_string(int32_t status);
+
+/* Library version as MAJOR * 10000 + MINOR * 100 + PATCH. */
+int32_t dqt_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DQT_H */

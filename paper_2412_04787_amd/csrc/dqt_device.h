@@ -1,0 +1,97 @@
+// Device-side helpers shared by the libdqt kernels (gfx950 only).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace dqt {
+
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+typedef int i32x8 __attribute__((ext_vector_type(8)));
+typedef int i32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+
+constexpr int kWave = 64;
+
+// ---------------------------------------------------------------- bf16
+// fp32 -> bf16 bits, round to nearest even (finite inputs).
+__device__ __forceinline__ uint32_t f32_to_bf16_bits(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return u >> 16;
+}
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  return f32_to_bf16_bits(lo) | (f32_to_bf16_bits(hi) << 16);
+}
+__device__ __forceinline__ float bf16_bits_to_f32(uint32_t b) {
+  return __uint_as_float(b << 16);
+}
+
+// ---------------------------------------------------------------- e4m3
+// OCP E4M3 ("fn"): 1 sign, 4 exponent (bias 7), 3 fraction bits, max 448.
+// Round to nearest even, saturate to +-448, keep the sign of zero.
+__device__ __forceinline__ uint32_t f32_to_e4m3(float v) {
+  const uint32_t sign = (__float_as_uint(v) >> 24) & 0x80u;
+  const float a = fabsf(v);
+  uint32_t code;
+  if (!(a < 448.0f)) {
+    code = 0x7Eu;
+  } else if (a < 0.015625f) {                  // below 2^-6: subnormal grid 2^-9
+    code = (uint32_t)rintf(a * 512.0f);        // exact scaling, ties to even
+  } else {
+    const uint32_t ab = __float_as_uint(a);
+    const uint32_t r = ab + 0x7FFFFu + ((ab >> 20) & 1u);  // RNE to 3 fraction bits
+    code = (r >> 20) - (120u << 3);                       // exponent bias 127 -> 7
+    code = code > 0x7Eu ? 0x7Eu : code;
+  }
+  return code | sign;
+}
+
+// E4M3 byte -> fp32 (exact).  NaN codes are not produced by this library.
+__device__ __forceinline__ float e4m3_to_f32(uint32_t c) {
+  const uint32_t e = (c >> 3) & 0xFu, m = c & 7u;
+  float mag;
+  if (e == 0) {
+    mag = (float)m * 0.001953125f;             // m * 2^-9
+  } else {
+    mag = __uint_as_float(((e + 120u) << 23) | (m << 20));
+  }
+  return (c & 0x80u) ? -mag : mag;
+}
+
+// ---------------------------------------------------------------- ternary
+// Four 2-bit codes of one byte, one per output byte (bits 0-1 of each).
+__device__ __forceinline__ uint32_t spread_codes(uint32_t b) {
+  return (b & 3u) | ((b << 6) & 0x300u) | ((b << 12) & 0x30000u) | ((b << 18) & 0x3000000u);
+}
+// Code (0, 1, 2) -> int8 (-1, 0, 1), four at a time, via byte permute.
+__device__ __forceinline__ uint32_t codes_to_i8x4(uint32_t spread) {
+  return __builtin_amdgcn_perm(0u, 0x000100FFu, spread);
+}
+// Code (0, 1, 2) -> e4m3 (-1.0, 0, +1.0) bytes (0xB8, 0x00, 0x38).
+__device__ __forceinline__ uint32_t codes_to_e4m3x4(uint32_t spread) {
+  return __builtin_amdgcn_perm(0u, 0x003800B8u, spread);
+}
+// Code (0, 1, 2) -> bf16 bits of -1, 0, +1.
+__device__ __forceinline__ uint32_t code_to_bf16_bits(uint32_t code) {
+  return (uint32_t)((0x00003F800000BF80ull >> (16u * code)) & 0xFFFFu);
+}
+__device__ __forceinline__ float code_to_f32(uint32_t code) {
+  return (float)((int)code - 1);
+}
+
+// ---------------------------------------------------------------- waves
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v = fmaxf(v, __shfl_xor(v, off, kWave));
+  return v;
+}
+__device__ __forceinline__ unsigned long long wave_sum_u64(unsigned long long v) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, kWave);
+  return v;
+}
+
+}  // namespace dqt

@@ -1,0 +1,192 @@
+"""ctypes binding of libdqt.so: the C ABI of include/dqt.h, one Python function
+per entry point with the same name.  Argument marshalling only: torch tensors
+are passed as device pointers on torch's current stream, every step of the
+path runs in the library's HIP kernels, and a missing or unloadable library
+raises immediately (there is no fallback).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libdqt.so")
+
+# dqt_status
+DQT_OK, DQT_ERR_NULL, DQT_ERR_SHAPE, DQT_ERR_ALIGN, DQT_ERR_DTYPE = 0, 1, 2, 3, 4
+DQT_ERR_RANGE, DQT_ERR_WORKSPACE, DQT_ERR_UNSUPPORTED, DQT_ERR_HIP = 5, 6, 7, 8
+# dqt_dtype
+DQT_F32, DQT_BF16, DQT_I8, DQT_FP8E4M3, DQT_TERNARY2 = 0, 1, 2, 3, 4
+
+EXPORTS = (
+    "dqt_act_quant", "dqt_linear_fwd", "dqt_linear_bwd_workspace", "dqt_linear_bwd",
+    "dqt_sr_update", "dqt_debug_rng", "dqt_absmean_init", "dqt_pack_ternary",
+    "dqt_unpack_ternary", "dqt_status_string", "dqt_version",
+)
+
+
+class DqtWeight(ctypes.Structure):
+    _fields_ = [
+        ("d_out", ctypes.c_int32), ("d_in", ctypes.c_int32), ("wfmt", ctypes.c_int32),
+        ("qmin", ctypes.c_int32), ("qmax", ctypes.c_int32), ("alpha", ctypes.c_float),
+        ("tensor_id", ctypes.c_uint32), ("reserved", ctypes.c_uint32),
+    ]
+
+
+def weight(d_out: int, d_in: int, wfmt: int, qmin: int, qmax: int, alpha: float,
+           tensor_id: int = 0) -> DqtWeight:
+    return DqtWeight(d_out, d_in, wfmt, qmin, qmax, float(alpha), tensor_id, 0)
+
+
+class DqtError(RuntimeError):
+    def __init__(self, fn: str, status: int):
+        self.status = status
+        super().__init__(f"{fn}: {status_string(status)}")
+
+
+_lib = None
+
+_vp, _i32, _i64, _u32, _u64, _f32 = (ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64,
+                                     ctypes.c_uint32, ctypes.c_uint64, ctypes.c_float)
+_wp = ctypes.POINTER(DqtWeight)
+
+_SIGS = {
+    "dqt_act_quant": (_i32, [_vp, _i32, _i64, _i32, _i32, _vp, _vp, _vp]),
+    "dqt_linear_fwd": (_i32, [_wp, _vp, _vp, _i32, _i64, _i32, _vp, _vp, _vp, _i32, _vp]),
+    "dqt_linear_bwd_workspace": (ctypes.c_size_t, [_wp, _i64]),
+    "dqt_linear_bwd": (_i32, [_wp, _vp, _vp, _i32, _vp, _vp, _i32, _i64, _i32, _vp, _i32, _vp,
+                              _vp, ctypes.c_size_t, _vp]),
+    "dqt_sr_update": (_i32, [_wp, _vp, _vp, _f32, _u64, _u32, _vp, _vp]),
+    "dqt_debug_rng": (_i32, [_u64, _u32, _u32, _u64, _i64, _vp, _vp]),
+    "dqt_absmean_init": (_i32, [_vp, _i64, _i32, _i32, _vp, _vp]),
+    "dqt_pack_ternary": (_i32, [_vp, _i64, _i64, _vp]),
+    "dqt_unpack_ternary": (_i32, [_vp, _i64, _i64, _vp]),
+    "dqt_status_string": (ctypes.c_char_p, [_i32]),
+    "dqt_version": (_i32, []),
+}
+
+
+def load(path: str = LIB_PATH):
+    """Load libdqt.so (once).  Raises if it is missing: there is no fallback."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build it with "
+                           "`python -m paper_2412_04787_amd.build_lib`")
+    lib = ctypes.CDLL(path)
+    for name, (res, args) in _SIGS.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    _lib = lib
+    return lib
+
+
+def _check(fn: str, st: int):
+    if st != DQT_OK:
+        raise DqtError(fn, st)
+
+
+def status_string(st: int) -> str:
+    return load().dqt_status_string(st).decode()
+
+
+def version() -> int:
+    return load().dqt_version()
+
+
+# ----------------------------------------------------------------- tensors
+
+def _torch():
+    import torch
+    return torch
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream=None):
+    torch = _torch()
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def dtype_code(t) -> int:
+    torch = _torch()
+    return {torch.float32: DQT_F32, torch.bfloat16: DQT_BF16, torch.int8: DQT_I8,
+            torch.float8_e4m3fn: DQT_FP8E4M3, torch.uint8: DQT_FP8E4M3}[t.dtype]
+
+
+def dqt_act_quant(X, act_q: int, Xq, xdq, stream=None):
+    M, K = X.shape
+    _check("dqt_act_quant", load().dqt_act_quant(_ptr(X), dtype_code(X), M, K, act_q, _ptr(Xq),
+                                                 _ptr(xdq), _stream(stream)))
+
+
+def dqt_linear_fwd(w: DqtWeight, Wq, X, M: int, act_q: int, Xq, xdq, Y, stream=None,
+                   x_t: int | None = None):
+    """X may be None when Xq / xdq already hold the quantised input."""
+    if x_t is None:
+        x_t = dtype_code(X) if X is not None else DQT_F32
+    _check("dqt_linear_fwd", load().dqt_linear_fwd(ctypes.byref(w), _ptr(Wq), _ptr(X), x_t, M,
+                                                   act_q, _ptr(Xq), _ptr(xdq), _ptr(Y),
+                                                   dtype_code(Y), _stream(stream)))
+
+
+def dqt_linear_bwd_workspace(w: DqtWeight, M: int) -> int:
+    return int(load().dqt_linear_bwd_workspace(ctypes.byref(w), M))
+
+
+def dqt_linear_bwd(w: DqtWeight, Wq, Xq, act_q: int, xdq, dY, M: int, xt_t: int, dX, dW,
+                   ws=None, stream=None, dy_t: int | None = None, dx_t: int | None = None):
+    dy_t = dtype_code(dY) if dy_t is None else dy_t
+    dx_t = (dtype_code(dX) if dX is not None else DQT_F32) if dx_t is None else dx_t
+    ws_bytes = 0 if ws is None else ws.numel() * ws.element_size()
+    _check("dqt_linear_bwd", load().dqt_linear_bwd(ctypes.byref(w), _ptr(Wq), _ptr(Xq), act_q,
+                                                   _ptr(xdq), _ptr(dY), dy_t, M, xt_t, _ptr(dX),
+                                                   dx_t, _ptr(dW), _ptr(ws), ws_bytes,
+                                                   _stream(stream)))
+
+
+def dqt_sr_update(w: DqtWeight, Wq, dW, lr: float, seed: int, step: int, counters=None,
+                  stream=None):
+    _check("dqt_sr_update", load().dqt_sr_update(ctypes.byref(w), _ptr(Wq), _ptr(dW), lr, seed,
+                                                 step, _ptr(counters), _stream(stream)))
+
+
+def dqt_debug_rng(seed: int, step: int, tensor_id: int, i0: int, out, stream=None):
+    _check("dqt_debug_rng", load().dqt_debug_rng(seed, step, tensor_id, i0, out.numel(),
+                                                 _ptr(out), _stream(stream)))
+
+
+# ----------------------------------------------------------------- host helpers
+
+def dqt_absmean_init(W0: np.ndarray, qmin: int, qmax: int):
+    W0 = np.ascontiguousarray(W0, dtype=np.float32)
+    q = np.empty(W0.shape, dtype=np.int8)
+    alpha = ctypes.c_float()
+    _check("dqt_absmean_init", load().dqt_absmean_init(W0.ctypes.data, W0.size, qmin, qmax,
+                                                       q.ctypes.data, ctypes.byref(alpha)))
+    return q, np.float32(alpha.value)
+
+
+def dqt_pack_ternary(q: np.ndarray) -> np.ndarray:
+    q = np.ascontiguousarray(q, dtype=np.int8)
+    rows, cols = q.shape
+    packed = np.empty((rows, cols // 4), dtype=np.uint8)
+    _check("dqt_pack_ternary", load().dqt_pack_ternary(q.ctypes.data, rows, cols,
+                                                       packed.ctypes.data))
+    return packed
+
+
+def dqt_unpack_ternary(packed: np.ndarray, cols: int) -> np.ndarray:
+    packed = np.ascontiguousarray(packed, dtype=np.uint8)
+    rows = packed.shape[0]
+    q = np.empty((rows, cols), dtype=np.int8)
+    _check("dqt_unpack_ternary", load().dqt_unpack_ternary(packed.ctypes.data, rows, cols,
+                                                           q.ctypes.data))
+    return q
