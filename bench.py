@@ -82,8 +82,10 @@ class Block:
             self.X[name] = torch.from_numpy(W.input_draw(wl, name)).to(bf).to(dev)
             self.Xq[name] = torch.empty((M, wl.input_width(name)), dtype=qdt, device=dev)
             self.xdq[name] = torch.empty((M,), dtype=torch.float32, device=dev)
-        ws = max(dqt.dqt_linear_bwd_workspace(w, M) for w in self.weights)
-        self.ws = torch.empty((max(ws // 4, 4),), dtype=torch.float32, device=dev)
+        # one workspace serves every call: calls on one stream run in order
+        ws = max(max(dqt.dqt_linear_bwd_workspace(w, M), dqt.dqt_linear_fwd_workspace(w))
+                 for w in self.weights)
+        self.ws = dqt.workspace(ws, dev)
         self.counters = torch.zeros((2,), dtype=torch.int64, device=dev)
 
 
@@ -98,11 +100,11 @@ def run_step(blk, dqt, step, stream, rec):
     for li, lin in enumerate(wl.linears):
         rec("fwd", li, lambda li=li, lin=lin: dqt.dqt_linear_fwd(
             blk.weights[li], blk.codes[li], None, M, blk.act, blk.Xq[lin.input],
-            blk.xdq[lin.input], blk.Y[li], stream))
+            blk.xdq[lin.input], blk.Y[li], blk.ws, stream))
     for li, lin in enumerate(wl.linears):
         rec("bwd_dx", li, lambda li=li, lin=lin: dqt.dqt_linear_bwd(
             blk.weights[li], blk.codes[li], blk.Xq[lin.input], blk.act, blk.xdq[lin.input],
-            blk.dY[li], M, blk.xt, blk.dX[li], None, None, stream))
+            blk.dY[li], M, blk.xt, blk.dX[li], None, blk.ws, stream))
         rec("bwd_dw", li, lambda li=li, lin=lin: dqt.dqt_linear_bwd(
             blk.weights[li], blk.codes[li], blk.Xq[lin.input], blk.act, blk.xdq[lin.input],
             blk.dY[li], M, blk.xt, None, blk.dW[li], blk.ws, stream))

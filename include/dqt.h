@@ -106,6 +106,11 @@ typedef struct {
 dqt_status dqt_act_quant(const void* X, int32_t x_t, int64_t M, int32_t K,
                          int32_t act_q, void* Xq, float* xdq, void* stream);
 
+/* Bytes of device workspace dqt_linear_fwd needs for this weight (0 if
+ * none): ternary weights are unpacked once per call into d_out * d_in
+ * operand bytes.  Depends only on the descriptor. */
+size_t dqt_linear_fwd_workspace(const dqt_weight* w);
+
 /*
  * Forward of a DQT linear (Sec. 3.2):  Y = X~ W~^T, i.e.
  *   acc[m, n] = sum_k Xq[m, k] * q[n, k]     (int32, exact, for int8 codes;
@@ -119,14 +124,19 @@ dqt_status dqt_act_quant(const void* X, int32_t x_t, int64_t M, int32_t K,
  *   Xq, xdq: [M, d_in] codes and [M] scales; written when X != NULL, read
  *          otherwise.  Keep them for dqt_linear_bwd.
  *   Y:     [M, d_out], y_t = DQT_F32 or DQT_BF16.  (output)
+ *   ws, ws_bytes: device workspace of at least dqt_linear_fwd_workspace()
+ *          bytes (may be NULL when that is 0).
  */
 dqt_status dqt_linear_fwd(const dqt_weight* w, const void* Wq,
                           const void* X, int32_t x_t, int64_t M, int32_t act_q,
                           void* Xq, float* xdq,
-                          void* Y, int32_t y_t, void* stream);
+                          void* Y, int32_t y_t,
+                          void* ws, size_t ws_bytes, void* stream);
 
-/* Bytes of device workspace dqt_linear_bwd needs for this weight and M
- * (0 if none).  Depends only on (d_out, d_in, M). */
+/* Bytes of device workspace dqt_linear_bwd needs for this weight and M.
+ * Depends only on (d_out, d_in, M) and covers every dtype combination:
+ * fp32 split-reduction partials, the weights unpacked to bf16 (dX) and the
+ * dequantised activation X~ in bf16 (dW). */
 size_t dqt_linear_bwd_workspace(const dqt_weight* w, int64_t M);
 
 /*
@@ -143,8 +153,8 @@ size_t dqt_linear_bwd_workspace(const dqt_weight* w, int64_t M);
  *   dX: [M, d_in] or NULL (skipped); dx_t = DQT_F32 or DQT_BF16.
  *   dW: [d_out, d_in] fp32 or NULL (skipped); overwritten, never accumulated.
  *   ws, ws_bytes: device workspace of at least dqt_linear_bwd_workspace()
- *   bytes (may be NULL if that is 0).  Results do not depend on timing: the
- *   split reduction over tokens is summed in a fixed order.
+ *   bytes.  Results do not depend on timing: the split reduction over tokens
+ *   is summed in a fixed order.
  */
 dqt_status dqt_linear_bwd(const dqt_weight* w, const void* Wq,
                           const void* Xq, int32_t act_q, const float* xdq,

@@ -68,9 +68,14 @@ dqt_status dqt_act_quant(const void* X, int32_t x_t, int64_t M, int32_t K, int32
                                         static_cast<hipStream_t>(stream)));
 }
 
+size_t dqt_linear_fwd_workspace(const dqt_weight* w) {
+  if (check_weight(w) != DQT_OK) return 0;
+  return dqt::fwd_workspace_bytes(w->wfmt == DQT_TERNARY2, w->d_out, w->d_in);
+}
+
 dqt_status dqt_linear_fwd(const dqt_weight* w, const void* Wq, const void* X, int32_t x_t,
                           int64_t M, int32_t act_q, void* Xq, float* xdq, void* Y, int32_t y_t,
-                          void* stream) {
+                          void* ws, size_t ws_bytes, void* stream) {
   dqt_status st = check_weight(w);
   if (st != DQT_OK) return st;
   if (M < 0) return DQT_ERR_SHAPE;
@@ -83,6 +88,9 @@ dqt_status dqt_linear_fwd(const dqt_weight* w, const void* Wq, const void* X, in
   if (!aligned16(Wq) || !aligned16(Xq) || !aligned16(xdq) || !aligned16(Y) ||
       (X != nullptr && !aligned16(X)))
     return DQT_ERR_ALIGN;
+  const size_t need = dqt_linear_fwd_workspace(w);
+  if (need > 0 && (ws == nullptr || ws_bytes < need)) return DQT_ERR_WORKSPACE;
+  if (need > 0 && !aligned16(ws)) return DQT_ERR_ALIGN;
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (X != nullptr) {
     st = from_hip(dqt::launch_act_quant(X, x_t == DQT_BF16, M, w->d_in, act_q == DQT_FP8E4M3, Xq,
@@ -97,18 +105,41 @@ dqt_status dqt_linear_fwd(const dqt_weight* w, const void* Wq, const void* X, in
   a.M = M;
   a.d_in = w->d_in;
   a.d_out = w->d_out;
+  a.ws = ws;
   a.alpha = w->alpha;
   a.w_ternary = w->wfmt == DQT_TERNARY2;
   a.act_e4m3 = act_q == DQT_FP8E4M3;
   a.y_bf16 = y_t == DQT_BF16;
-  return from_hip(dqt::launch_fwd(a, s));
+  return from_hip(dqt::launch_fwd_v2(a, s));
+}
+
+// Backward workspace layout (each region 256-byte aligned):
+//   [fp32 split partials: splits * d_out * d_in]   (when splits > 1)
+//   [bf16 weights: d_out * d_in]                   (bf16-environment dX)
+//   [bf16 X~: M * d_in]                            (bf16-environment dW)
+struct BwdLayout {
+  int64_t splits;
+  size_t part, q, xt, total;
+};
+static size_t align256(size_t n) { return (n + 255) / 256 * 256; }
+static BwdLayout bwd_layout(const dqt_weight* w, int64_t M) {
+  BwdLayout L;
+  int wj;
+  int64_t s_v2;
+  dqt::plan_dw_v2(w->d_out, w->d_in, M, &wj, &s_v2);
+  const int64_t s_f32 = dqt::dw_splits_f32(w->d_out, w->d_in, M);
+  L.splits = s_v2 > s_f32 ? s_v2 : s_f32;
+  const size_t wn = (size_t)w->d_out * (size_t)w->d_in;
+  L.part = L.splits > 1 ? align256((size_t)L.splits * wn * sizeof(float)) : 0;
+  L.q = align256(wn * 2);
+  L.xt = align256((size_t)M * (size_t)w->d_in * 2);
+  L.total = L.part + L.q + L.xt;
+  return L;
 }
 
 size_t dqt_linear_bwd_workspace(const dqt_weight* w, int64_t M) {
   if (check_weight(w) != DQT_OK || M < 0) return 0;
-  const int64_t splits = dqt::dw_splits(w->d_out, w->d_in, M);
-  if (splits <= 1) return 0;
-  return (size_t)splits * (size_t)w->d_out * (size_t)w->d_in * sizeof(float);
+  return bwd_layout(w, M).total;
 }
 
 dqt_status dqt_linear_bwd(const dqt_weight* w, const void* Wq, const void* Xq, int32_t act_q,
@@ -123,12 +154,12 @@ dqt_status dqt_linear_bwd(const dqt_weight* w, const void* Wq, const void* Xq, i
   if (dX != nullptr && !is_float_type(dx_t)) return DQT_ERR_DTYPE;
   if (dW != nullptr && dy_t != xt_t) return DQT_ERR_UNSUPPORTED;
   if (dX == nullptr && dW == nullptr) return DQT_OK;
-  const int64_t splits = dqt::dw_splits(w->d_out, w->d_in, M);
-  const size_t need = dqt_linear_bwd_workspace(w, M);
+  const BwdLayout L = bwd_layout(w, M);
+  if (ws == nullptr || ws_bytes < L.total) return DQT_ERR_WORKSPACE;
+  if (!aligned16(ws)) return DQT_ERR_ALIGN;
+  uint8_t* wsb = static_cast<uint8_t*>(ws);
   if (dW != nullptr) {
     if (!aligned16(dW)) return DQT_ERR_ALIGN;
-    if (need > 0 && (ws == nullptr || ws_bytes < need)) return DQT_ERR_WORKSPACE;
-    if (need > 0 && !aligned16(ws)) return DQT_ERR_ALIGN;
     if (M > 0 && (Xq == nullptr || xdq == nullptr)) return DQT_ERR_NULL;
   }
   if (M > 0) {
@@ -154,7 +185,7 @@ dqt_status dqt_linear_bwd(const dqt_weight* w, const void* Wq, const void* Xq, i
     a.w_ternary = w->wfmt == DQT_TERNARY2;
     a.dy_bf16 = dy_t == DQT_BF16;
     a.dx_bf16 = dx_t == DQT_BF16;
-    st = from_hip(dqt::launch_dx(a, s));
+    st = from_hip(a.dy_bf16 ? dqt::launch_dx_v2(a, wsb + L.part, s) : dqt::launch_dx_f32(a, s));
     if (st != DQT_OK) return st;
   }
   if (dW != nullptr) {
@@ -163,14 +194,14 @@ dqt_status dqt_linear_bwd(const dqt_weight* w, const void* Wq, const void* Xq, i
     a.Xq = Xq;
     a.xdq = xdq;
     a.dW = dW;
-    a.ws = static_cast<float*>(ws);
+    a.ws = reinterpret_cast<float*>(wsb);
     a.M = M;
     a.d_in = w->d_in;
     a.d_out = w->d_out;
-    a.splits = splits;
+    a.splits = L.splits;
     a.act_e4m3 = act_q == DQT_FP8E4M3;
     a.xt_bf16 = xt_t == DQT_BF16;
-    st = from_hip(dqt::launch_dw(a, s));
+    st = from_hip(a.xt_bf16 ? dqt::launch_dw_v2(a, wsb + L.part + L.q, s) : dqt::launch_dw_f32(a, s));
   }
   return st;
 }

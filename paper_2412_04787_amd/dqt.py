@@ -21,7 +21,8 @@ DQT_ERR_RANGE, DQT_ERR_WORKSPACE, DQT_ERR_UNSUPPORTED, DQT_ERR_HIP = 5, 6, 7, 8
 DQT_F32, DQT_BF16, DQT_I8, DQT_FP8E4M3, DQT_TERNARY2 = 0, 1, 2, 3, 4
 
 EXPORTS = (
-    "dqt_act_quant", "dqt_linear_fwd", "dqt_linear_bwd_workspace", "dqt_linear_bwd",
+    "dqt_act_quant", "dqt_linear_fwd_workspace", "dqt_linear_fwd", "dqt_linear_bwd_workspace",
+    "dqt_linear_bwd",
     "dqt_sr_update", "dqt_debug_rng", "dqt_absmean_init", "dqt_pack_ternary",
     "dqt_unpack_ternary", "dqt_status_string", "dqt_version",
 )
@@ -54,7 +55,9 @@ _wp = ctypes.POINTER(DqtWeight)
 
 _SIGS = {
     "dqt_act_quant": (_i32, [_vp, _i32, _i64, _i32, _i32, _vp, _vp, _vp]),
-    "dqt_linear_fwd": (_i32, [_wp, _vp, _vp, _i32, _i64, _i32, _vp, _vp, _vp, _i32, _vp]),
+    "dqt_linear_fwd_workspace": (ctypes.c_size_t, [_wp]),
+    "dqt_linear_fwd": (_i32, [_wp, _vp, _vp, _i32, _i64, _i32, _vp, _vp, _vp, _i32, _vp,
+                              ctypes.c_size_t, _vp]),
     "dqt_linear_bwd_workspace": (ctypes.c_size_t, [_wp, _i64]),
     "dqt_linear_bwd": (_i32, [_wp, _vp, _vp, _i32, _vp, _vp, _i32, _i64, _i32, _vp, _i32, _vp,
                               _vp, ctypes.c_size_t, _vp]),
@@ -127,14 +130,28 @@ def dqt_act_quant(X, act_q: int, Xq, xdq, stream=None):
                                                  _ptr(xdq), _stream(stream)))
 
 
-def dqt_linear_fwd(w: DqtWeight, Wq, X, M: int, act_q: int, Xq, xdq, Y, stream=None,
+def dqt_linear_fwd_workspace(w: DqtWeight) -> int:
+    return int(load().dqt_linear_fwd_workspace(ctypes.byref(w)))
+
+
+def dqt_linear_fwd(w: DqtWeight, Wq, X, M: int, act_q: int, Xq, xdq, Y, ws=None, stream=None,
                    x_t: int | None = None):
     """X may be None when Xq / xdq already hold the quantised input."""
     if x_t is None:
         x_t = dtype_code(X) if X is not None else DQT_F32
+    ws_bytes = 0 if ws is None else ws.numel() * ws.element_size()
     _check("dqt_linear_fwd", load().dqt_linear_fwd(ctypes.byref(w), _ptr(Wq), _ptr(X), x_t, M,
                                                    act_q, _ptr(Xq), _ptr(xdq), _ptr(Y),
-                                                   dtype_code(Y), _stream(stream)))
+                                                   dtype_code(Y), _ptr(ws), ws_bytes,
+                                                   _stream(stream)))
+
+
+def workspace(nbytes: int, device="cuda:0"):
+    """A device buffer of at least nbytes (16-byte aligned), or None for 0."""
+    if nbytes == 0:
+        return None
+    torch = _torch()
+    return torch.empty(((nbytes + 15) // 16 * 4,), dtype=torch.float32, device=device)
 
 
 def dqt_linear_bwd_workspace(w: DqtWeight, M: int) -> int:

@@ -66,7 +66,8 @@ def run_fwd(w, Wq, X_dev, act: str, y_out: str):
     Xq = torch.empty((M, K), dtype=torch.int8 if act == "i8" else torch.uint8, device=DEV)
     xdq = torch.empty((max(M, 1),), dtype=torch.float32, device=DEV)
     Y = torch.empty((M, w.d_out), dtype=torch_float(y_out), device=DEV)
-    dqt.dqt_linear_fwd(w, Wq, X_dev, M, act_code(act), Xq, xdq, Y)
+    ws = dqt.workspace(dqt.dqt_linear_fwd_workspace(w))
+    dqt.dqt_linear_fwd(w, Wq, X_dev, M, act_code(act), Xq, xdq, Y, ws)
     return Xq, xdq, Y
 
 
@@ -75,8 +76,7 @@ def run_bwd(w, Wq, Xq, act: str, xdq, dY_dev, xt: str, dx_out: str | None = "f32
     M = dY_dev.shape[0]
     dX = None if dx_out is None else torch.empty((M, w.d_in), dtype=torch_float(dx_out), device=DEV)
     dW = torch.empty((w.d_out, w.d_in), dtype=torch.float32, device=DEV) if want_dw else None
-    nbytes = dqt.dqt_linear_bwd_workspace(w, M)
-    ws = torch.empty((max(nbytes // 4, 4),), dtype=torch.float32, device=DEV) if nbytes else None
+    ws = dqt.workspace(dqt.dqt_linear_bwd_workspace(w, M))
     dqt.dqt_linear_bwd(w, Wq, Xq, act_code(act), xdq, dY_dev, M, float_code(xt), dX, dW, ws)
     return dX, dW
 

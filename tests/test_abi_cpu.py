@@ -100,7 +100,7 @@ def test_bad_weight_descriptor_rejected(kw, status):
     st = lib.dqt_sr_update(ctypes.byref(w), FAKE, FAKE, 1e-3, 0, 1, None, None)
     assert st == status
     st = lib.dqt_linear_fwd(ctypes.byref(w), FAKE, FAKE, dqt.DQT_F32, 16, dqt.DQT_I8, FAKE, FAKE,
-                            FAKE, dqt.DQT_F32, None)
+                            FAKE, dqt.DQT_F32, FAKE, 1 << 30, None)
     assert st == status
 
 
@@ -109,26 +109,35 @@ def test_call_level_checks():
     w = _w()
     bw = ctypes.byref(w)
     # fwd
+    BIG = 1 << 30
     assert lib.dqt_linear_fwd(bw, FAKE, FAKE, dqt.DQT_F32, -1, dqt.DQT_I8, FAKE, FAKE, FAKE,
-                              dqt.DQT_F32, None) == dqt.DQT_ERR_SHAPE
+                              dqt.DQT_F32, FAKE, BIG, None) == dqt.DQT_ERR_SHAPE
     assert lib.dqt_linear_fwd(bw, None, FAKE, dqt.DQT_F32, 16, dqt.DQT_I8, FAKE, FAKE, FAKE,
-                              dqt.DQT_F32, None) == dqt.DQT_ERR_NULL
+                              dqt.DQT_F32, FAKE, BIG, None) == dqt.DQT_ERR_NULL
     assert lib.dqt_linear_fwd(bw, FAKE, FAKE, dqt.DQT_F32, 16, dqt.DQT_I8, FAKE, UNALIGNED, FAKE,
-                              dqt.DQT_F32, None) == dqt.DQT_ERR_ALIGN
+                              dqt.DQT_F32, FAKE, BIG, None) == dqt.DQT_ERR_ALIGN
     assert lib.dqt_linear_fwd(bw, FAKE, FAKE, dqt.DQT_I8, 16, dqt.DQT_I8, FAKE, FAKE, FAKE,
-                              dqt.DQT_F32, None) == dqt.DQT_ERR_DTYPE
+                              dqt.DQT_F32, FAKE, BIG, None) == dqt.DQT_ERR_DTYPE
     assert lib.dqt_linear_fwd(bw, FAKE, FAKE, dqt.DQT_F32, 16, dqt.DQT_F32, FAKE, FAKE, FAKE,
-                              dqt.DQT_F32, None) == dqt.DQT_ERR_DTYPE
+                              dqt.DQT_F32, FAKE, BIG, None) == dqt.DQT_ERR_DTYPE
+    need_f = lib.dqt_linear_fwd_workspace(bw)
+    assert need_f == 64 * 64
+    assert lib.dqt_linear_fwd(bw, FAKE, FAKE, dqt.DQT_F32, 16, dqt.DQT_I8, FAKE, FAKE, FAKE,
+                              dqt.DQT_F32, FAKE, need_f - 1, None) == dqt.DQT_ERR_WORKSPACE
+    assert lib.dqt_linear_fwd(bw, FAKE, FAKE, dqt.DQT_F32, 16, dqt.DQT_I8, FAKE, FAKE, FAKE,
+                              dqt.DQT_F32, None, 0, None) == dqt.DQT_ERR_WORKSPACE
     w8 = _w(wfmt=dqt.DQT_I8, qmin=-127, qmax=127)
+    assert lib.dqt_linear_fwd_workspace(ctypes.byref(w8)) == 0
     assert lib.dqt_linear_fwd(ctypes.byref(w8), FAKE, FAKE, dqt.DQT_F32, 16, dqt.DQT_FP8E4M3,
-                              FAKE, FAKE, FAKE, dqt.DQT_F32, None) == dqt.DQT_ERR_UNSUPPORTED
+                              FAKE, FAKE, FAKE, dqt.DQT_F32, None, 0, None) == dqt.DQT_ERR_UNSUPPORTED
     # M = 0 is a no-op that launches nothing
     assert lib.dqt_linear_fwd(bw, None, None, dqt.DQT_F32, 0, dqt.DQT_I8, None, None, None,
-                              dqt.DQT_F32, None) == dqt.DQT_OK
+                              dqt.DQT_F32, None, 0, None) == dqt.DQT_OK
     # bwd
     big = _w(d_out=768, d_in=768)
     need = lib.dqt_linear_bwd_workspace(ctypes.byref(big), 8192)
-    assert need > 0 and need % (768 * 768 * 4) == 0
+    # bf16 weights + bf16 X~ + split partials
+    assert need >= 768 * 768 * 2 + 8192 * 768 * 2
     assert lib.dqt_linear_bwd(ctypes.byref(big), FAKE, FAKE, dqt.DQT_I8, FAKE, FAKE, dqt.DQT_BF16,
                               8192, dqt.DQT_BF16, None, dqt.DQT_F32, FAKE, None, 0,
                               None) == dqt.DQT_ERR_WORKSPACE
@@ -140,7 +149,7 @@ def test_call_level_checks():
                               None) == dqt.DQT_ERR_UNSUPPORTED
     assert lib.dqt_linear_bwd(bw, FAKE, FAKE, dqt.DQT_I8, FAKE, FAKE, dqt.DQT_F32, 16,
                               dqt.DQT_F32, None, dqt.DQT_F32, None, None, 0, None) == dqt.DQT_OK
-    assert lib.dqt_linear_bwd_workspace(ctypes.byref(_w()), 512) == 0
+    assert lib.dqt_linear_bwd_workspace(ctypes.byref(_w()), 512) >= 64 * 64 * 2 + 512 * 64 * 2
     # sr
     assert lib.dqt_sr_update(bw, FAKE, None, 1e-3, 0, 1, None, None) == dqt.DQT_ERR_NULL
     assert lib.dqt_sr_update(bw, FAKE, FAKE, -1.0, 0, 1, None, None) == dqt.DQT_ERR_RANGE

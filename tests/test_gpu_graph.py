@@ -19,8 +19,8 @@ def test_graph_replays_match_eager(lib):
     X = torch.from_numpy(W.draw_normal((M, d_in), 1.0, 5, 97, 2)).to(torch.bfloat16).to(DEV)
     dY = torch.from_numpy(W.draw_normal((M, d_out), 1e-2, 5, 97, 3)).to(torch.bfloat16).to(DEV)
     Wq0 = weight_codes_dev(q, "ternary")
-    nws = dqt.dqt_linear_bwd_workspace(w, M)
-    ws = torch.empty((max(nws // 4, 4),), dtype=torch.float32, device=DEV)
+    ws = dqt.workspace(dqt.dqt_linear_bwd_workspace(w, M))
+    fws = dqt.workspace(dqt.dqt_linear_fwd_workspace(w))
 
     def make_bufs():
         return dict(Wq=Wq0.clone(), Xq=torch.empty((M, d_in), dtype=torch.int8, device=DEV),
@@ -31,7 +31,7 @@ def test_graph_replays_match_eager(lib):
                     cnt=torch.zeros((2,), dtype=torch.int64, device=DEV))
 
     def step(b):
-        dqt.dqt_linear_fwd(w, b["Wq"], X, M, dqt.DQT_I8, b["Xq"], b["xdq"], b["Y"])
+        dqt.dqt_linear_fwd(w, b["Wq"], X, M, dqt.DQT_I8, b["Xq"], b["xdq"], b["Y"], fws)
         dqt.dqt_linear_bwd(w, b["Wq"], b["Xq"], dqt.DQT_I8, b["xdq"], dY, M, dqt.DQT_BF16,
                            b["dX"], b["dW"], ws)
         dqt.dqt_sr_update(w, b["Wq"], b["dW"], 1e-2, 11, 1, b["cnt"])

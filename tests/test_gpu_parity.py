@@ -145,7 +145,12 @@ def test_backward_empty_tokens_writes_zero_dw(lib):
     dY = torch.empty((0, 48), dtype=torch.float32, device=DEV)
     Xq = torch.empty((0, 32), dtype=torch.int8, device=DEV)
     xdq = torch.empty((1,), dtype=torch.float32, device=DEV)
-    dqt.dqt_linear_bwd(w, Wq, Xq, dqt.DQT_I8, xdq, dY, 0, dqt.DQT_F32, None, dW)
+    for xt in (dqt.DQT_F32, dqt.DQT_BF16):
+        dW.fill_(7.0)
+        dYt = dY if xt == dqt.DQT_F32 else dY.to(torch.bfloat16)
+        ws = dqt.workspace(dqt.dqt_linear_bwd_workspace(w, 0))
+        dqt.dqt_linear_bwd(w, Wq, Xq, dqt.DQT_I8, xdq, dYt, 0, xt, None, dW, ws)
+        assert torch.count_nonzero(dW).item() == 0
     assert torch.count_nonzero(dW).item() == 0
 
 
