@@ -82,53 +82,51 @@ class Block:
             self.X[name] = torch.from_numpy(W.input_draw(wl, name)).to(bf).to(dev)
             self.Xq[name] = torch.empty((M, wl.input_width(name)), dtype=qdt, device=dev)
             self.xdq[name] = torch.empty((M,), dtype=torch.float32, device=dev)
+        ents = []
+        for li, lin in enumerate(wl.linears):
+            ents.append(dict(w=self.weights[li], Wq=self.codes[li], Xq=self.Xq[lin.input],
+                             xdq=self.xdq[lin.input], Y=self.Y[li], dY=self.dY[li],
+                             dX=self.dX[li], dW=self.dW[li]))
+        self.io_all = dqt.linear_io(ents)
+        self.io_dx = dqt.linear_io([dict(e, dW=None) for e in ents])
+        self.io_dw = dqt.linear_io([dict(e, dX=None) for e in ents])
+        self.y_t = dqt.DQT_BF16 if wl.y_out == "bf16" else dqt.DQT_F32
+        self.dy_t = dqt.DQT_BF16 if wl.dy_dtype == "bf16" else dqt.DQT_F32
+        self.dx_t = dqt.DQT_BF16 if wl.dx_out == "bf16" else dqt.DQT_F32
         # one workspace serves every call: calls on one stream run in order
-        ws = max(max(dqt.dqt_linear_bwd_workspace(w, M), dqt.dqt_linear_fwd_workspace(w))
-                 for w in self.weights)
+        ws = max(dqt.dqt_linear_bwd_batch_workspace(self.io_all, M),
+                 dqt.dqt_linear_fwd_batch_workspace(self.io_all))
         self.ws = dqt.workspace(ws, dev)
         self.counters = torch.zeros((2,), dtype=torch.int64, device=dev)
 
 
 def run_step(blk, dqt, step, stream, rec):
-    """Enqueue one train step.  rec(kind, index, fn) brackets each call with
-    events when timing, or just calls fn."""
+    """Enqueue one train step: act-quant per distinct input, then one batched
+    call per stage over all linears.  rec(kind, fn) runs fn (or records it
+    into a graph)."""
     wl = blk.wl
     M = wl.M
     for name in wl.inputs:
-        rec("act_quant", name, lambda name=name: dqt.dqt_act_quant(
+        rec("act_quant", lambda name=name: dqt.dqt_act_quant(
             blk.X[name], blk.act, blk.Xq[name], blk.xdq[name], stream))
-    for li, lin in enumerate(wl.linears):
-        rec("fwd", li, lambda li=li, lin=lin: dqt.dqt_linear_fwd(
-            blk.weights[li], blk.codes[li], None, M, blk.act, blk.Xq[lin.input],
-            blk.xdq[lin.input], blk.Y[li], blk.ws, stream))
-    for li, lin in enumerate(wl.linears):
-        rec("bwd_dx", li, lambda li=li, lin=lin: dqt.dqt_linear_bwd(
-            blk.weights[li], blk.codes[li], blk.Xq[lin.input], blk.act, blk.xdq[lin.input],
-            blk.dY[li], M, blk.xt, blk.dX[li], None, blk.ws, stream))
-        rec("bwd_dw", li, lambda li=li, lin=lin: dqt.dqt_linear_bwd(
-            blk.weights[li], blk.codes[li], blk.Xq[lin.input], blk.act, blk.xdq[lin.input],
-            blk.dY[li], M, blk.xt, None, blk.dW[li], blk.ws, stream))
-    for li in range(len(wl.linears)):
-        rec("sr", li, lambda li=li: dqt.dqt_sr_update(
-            blk.weights[li], blk.codes[li], blk.dW[li], wl.lr, wl.seed, step, blk.counters,
-            stream))
+    rec("fwd", lambda: dqt.dqt_linear_fwd_batch(blk.io_all, M, blk.act, blk.y_t, blk.ws, stream))
+    rec("bwd_dx", lambda: dqt.dqt_linear_bwd_batch(blk.io_dx, M, blk.act, blk.dy_t, blk.xt,
+                                                   blk.dx_t, blk.ws, stream))
+    rec("bwd_dw", lambda: dqt.dqt_linear_bwd_batch(blk.io_dw, M, blk.act, blk.dy_t, blk.xt,
+                                                   blk.dx_t, blk.ws, stream))
+    rec("sr", lambda: dqt.dqt_sr_update_batch(blk.io_all, wl.lr, wl.seed, step, blk.counters,
+                                              stream))
 
 
 def algorithmic_units(wl):
-    """Flops of each GEMM call and bytes of each streaming call, per launch."""
+    """Per step: flops of each GEMM stage, bytes of each streaming stage."""
     M = wl.M
-    units = {}
-    for li, lin in enumerate(wl.linears):
-        f = 2 * M * lin.d_in * lin.d_out
-        units[("fwd", li)] = f
-        units[("bwd_dx", li)] = f
-        units[("bwd_dw", li)] = f
-        code_b = lin.d_in * lin.d_out * (0.25 if wl.wfmt == "ternary" else 1.0)
-        units[("sr", li)] = 2 * code_b + 4 * lin.d_in * lin.d_out
+    f = sum(2 * M * l.d_in * l.d_out for l in wl.linears)
+    code_b = 0.25 if wl.wfmt == "ternary" else 1.0
+    sr_bytes = sum((2 * code_b + 4) * l.d_in * l.d_out for l in wl.linears)
     xb = 2 if wl.x_dtype == "bf16" else 4
-    for name in wl.inputs:
-        units[("act_quant", name)] = M * wl.input_width(name) * (xb + 1) + 4 * M
-    return units
+    act_bytes = sum(M * wl.input_width(n) * (xb + 1) + 4 * M for n in wl.inputs)
+    return {"fwd": f, "bwd_dx": f, "bwd_dw": f, "sr": sr_bytes, "act_quant": act_bytes}
 
 
 def cpu_baseline(wl, tokens: int):
@@ -216,7 +214,7 @@ def main():
     blk = Block(wl, torch, dqt, W)
     units = algorithmic_units(wl)
 
-    def plain(kind, idx, fn):
+    def plain(kind, fn):
         fn()
 
     for s in range(args.warmup):
@@ -255,9 +253,9 @@ def main():
     for kind in kinds:
         calls = []
 
-        def only(k, idx, fn, kind=kind, calls=calls):
+        def only(k, fn, kind=kind, calls=calls):
             if k == kind:
-                calls.append(idx)
+                calls.append(k)
                 fn()
 
         g = torch.cuda.CUDAGraph()
@@ -272,7 +270,7 @@ def main():
         e1.record(stream)
         torch.cuda.synchronize()
         per_kind_ms[kind] = e0.elapsed_time(e1)
-        per_kind_units[kind] = args.steps * sum(units[(kind, i)] for i in calls)
+        per_kind_units[kind] = args.steps * units[kind]
         per_kind_n[kind] = args.steps * len(calls)
         del g
 
@@ -285,7 +283,7 @@ def main():
     for kind in per_kind_ms:
         t = per_kind_ms[kind] / args.steps
         u = per_kind_units[kind] / args.steps
-        entry = {"ms_per_step": round(t, 4), "launches_per_step": per_kind_n[kind] // args.steps}
+        entry = {"ms_per_step": round(t, 4), "calls_per_step": per_kind_n[kind] // args.steps}
         if kind in gemm_dtype:
             tf = u / (t * 1e-3) / 1e12
             entry.update({"tflops": round(tf, 1), "dtype": gemm_dtype[kind],

@@ -189,6 +189,58 @@ dqt_status dqt_sr_update(const dqt_weight* w, void* Wq, const float* dW,
                          unsigned long long* counters, void* stream);
 
 /*
+ * Batches.  One call runs the same step for up to DQT_MAX_BATCH linears that
+ * share the token count M and the dtypes (e.g. the seven linears of a
+ * transformer block), as one launch per stage, so that the tiles of every
+ * linear fill the GPU together.  Results are those of the single-linear calls
+ * above; only the split of the dW reduction over tokens (a fixed function of
+ * the batch's shapes) may differ, which changes dW by fp32 rounding only.
+ * Linears may share Xq/xdq (the same input); the activation X~ is then
+ * formed once.  All weights of a batch must have the same wfmt.
+ */
+#define DQT_MAX_BATCH 8
+
+typedef struct {
+  const dqt_weight* w;  /* descriptor (host pointer)                          */
+  void* Wq;             /* codes (device); dqt_sr_update_batch updates them    */
+  const void* Xq;       /* [M, d_in] quantised input (dqt_act_quant)           */
+  const float* xdq;     /* [M] its per-token scales                            */
+  void* Y;              /* forward output [M, d_out]                           */
+  const void* dY;       /* upstream gradient [M, d_out]                        */
+  void* dX;             /* input gradient [M, d_in], or NULL to skip           */
+  float* dW;            /* weight gradient [d_out, d_in] fp32, or NULL to skip */
+} dqt_linear_io;
+
+/* Workspace bytes of dqt_linear_fwd_batch (0 if none); depends only on the
+ * descriptors. */
+size_t dqt_linear_fwd_batch_workspace(int32_t n, const dqt_linear_io* io);
+
+/* Forward of n linears (see dqt_linear_fwd; inputs already quantised).
+ * Uses w, Wq, Xq, xdq, Y of each entry. */
+dqt_status dqt_linear_fwd_batch(int32_t n, const dqt_linear_io* io, int64_t M,
+                                int32_t act_q, int32_t y_t,
+                                void* ws, size_t ws_bytes, void* stream);
+
+/* Workspace bytes of dqt_linear_bwd_batch; depends only on the descriptors'
+ * shapes and M. */
+size_t dqt_linear_bwd_batch_workspace(int32_t n, const dqt_linear_io* io,
+                                      int64_t M);
+
+/* Backward of n linears (see dqt_linear_bwd).  Uses w, Wq, Xq, xdq, dY, dX,
+ * dW of each entry; dX and dW may be NULL per entry. */
+dqt_status dqt_linear_bwd_batch(int32_t n, const dqt_linear_io* io, int64_t M,
+                                int32_t act_q, int32_t dy_t, int32_t xt_t,
+                                int32_t dx_t, void* ws, size_t ws_bytes,
+                                void* stream);
+
+/* Direct SR update of n weight tensors in one launch (see dqt_sr_update);
+ * uses w, Wq, dW of each entry.  Each tensor draws from its own stream
+ * (tensor_id); counters, when given, receive the totals over all tensors. */
+dqt_status dqt_sr_update_batch(int32_t n, const dqt_linear_io* io, float lr,
+                               uint64_t seed, uint32_t step,
+                               unsigned long long* counters, void* stream);
+
+/*
  * Helpers (not on the timed path).
  */
 

@@ -68,9 +68,209 @@ dqt_status dqt_act_quant(const void* X, int32_t x_t, int64_t M, int32_t K, int32
                                         static_cast<hipStream_t>(stream)));
 }
 
+// ----------------------------------------------------------------- batches
+
+namespace {
+
+// Checks shared by every batch call; fills the launcher's view of the batch.
+dqt_status check_batch(int32_t n, const dqt_linear_io* io, dqt::LinearIO* L, int32_t* wfmt) {
+  if (n < 1 || n > DQT_MAX_BATCH) return DQT_ERR_SHAPE;
+  if (io == nullptr) return DQT_ERR_NULL;
+  for (int l = 0; l < n; ++l) {
+    const dqt_status st = check_weight(io[l].w);
+    if (st != DQT_OK) return st;
+    if (l == 0) *wfmt = io[l].w->wfmt;
+    else if (io[l].w->wfmt != *wfmt) return DQT_ERR_UNSUPPORTED;
+    L[l] = dqt::LinearIO{};
+    L[l].d_in = io[l].w->d_in;
+    L[l].d_out = io[l].w->d_out;
+    L[l].alpha = io[l].w->alpha;
+    L[l].Wq = io[l].Wq;
+    L[l].Xq = io[l].Xq;
+    L[l].xdq = io[l].xdq;
+    L[l].Y = io[l].Y;
+    L[l].dY = io[l].dY;
+    L[l].dX = io[l].dX;
+    L[l].dW = io[l].dW;
+  }
+  return DQT_OK;
+}
+
+}  // namespace
+
+size_t dqt_linear_fwd_batch_workspace(int32_t n, const dqt_linear_io* io) {
+  dqt::LinearIO L[DQT_MAX_BATCH];
+  int32_t wfmt;
+  if (check_batch(n, io, L, &wfmt) != DQT_OK) return 0;
+  return dqt::fwd_batch_workspace(n, L, wfmt == DQT_TERNARY2, nullptr);
+}
+
+dqt_status dqt_linear_fwd_batch(int32_t n, const dqt_linear_io* io, int64_t M, int32_t act_q,
+                                int32_t y_t, void* ws, size_t ws_bytes, void* stream) {
+  dqt::LinearIO L[DQT_MAX_BATCH];
+  int32_t wfmt;
+  dqt_status st = check_batch(n, io, L, &wfmt);
+  if (st != DQT_OK) return st;
+  if (M < 0) return DQT_ERR_SHAPE;
+  if (act_q != DQT_I8 && act_q != DQT_FP8E4M3) return DQT_ERR_DTYPE;
+  if (!is_float_type(y_t)) return DQT_ERR_DTYPE;
+  if (act_q == DQT_FP8E4M3 && wfmt != DQT_TERNARY2) return DQT_ERR_UNSUPPORTED;
+  if (M == 0) return DQT_OK;
+  for (int l = 0; l < n; ++l) {
+    if (io[l].Wq == nullptr || io[l].Xq == nullptr || io[l].xdq == nullptr || io[l].Y == nullptr)
+      return DQT_ERR_NULL;
+    if (!aligned16(io[l].Wq) || !aligned16(io[l].Xq) || !aligned16(io[l].xdq) || !aligned16(io[l].Y))
+      return DQT_ERR_ALIGN;
+  }
+  const size_t need = dqt::fwd_batch_workspace(n, L, wfmt == DQT_TERNARY2, nullptr);
+  if (need > 0 && (ws == nullptr || ws_bytes < need)) return DQT_ERR_WORKSPACE;
+  if (need > 0 && !aligned16(ws)) return DQT_ERR_ALIGN;
+  dqt::BatchCfg c{n, M, wfmt == DQT_TERNARY2, act_q == DQT_FP8E4M3, y_t == DQT_BF16};
+  return from_hip(dqt::launch_fwd_batch(c, L, static_cast<uint8_t*>(ws), static_cast<hipStream_t>(stream)));
+}
+
+size_t dqt_linear_bwd_batch_workspace(int32_t n, const dqt_linear_io* io, int64_t M) {
+  dqt::LinearIO L[DQT_MAX_BATCH];
+  int32_t wfmt;
+  if (check_batch(n, io, L, &wfmt) != DQT_OK || M < 0) return 0;
+  return dqt::plan_bwd_batch(n, L, M).total;
+}
+
+dqt_status dqt_linear_bwd_batch(int32_t n, const dqt_linear_io* io, int64_t M, int32_t act_q,
+                                int32_t dy_t, int32_t xt_t, int32_t dx_t, void* ws,
+                                size_t ws_bytes, void* stream) {
+  dqt::LinearIO L[DQT_MAX_BATCH];
+  int32_t wfmt;
+  dqt_status st = check_batch(n, io, L, &wfmt);
+  if (st != DQT_OK) return st;
+  if (M < 0) return DQT_ERR_SHAPE;
+  if (act_q != DQT_I8 && act_q != DQT_FP8E4M3) return DQT_ERR_DTYPE;
+  if (!is_float_type(dy_t) || !is_float_type(xt_t) || !is_float_type(dx_t)) return DQT_ERR_DTYPE;
+  bool any_dx = false, any_dw = false;
+  for (int l = 0; l < n; ++l) {
+    any_dx |= io[l].dX != nullptr;
+    any_dw |= io[l].dW != nullptr;
+  }
+  if (any_dw && dy_t != xt_t) return DQT_ERR_UNSUPPORTED;
+  if (!any_dx && !any_dw) return DQT_OK;
+  const dqt::BwdPlan P = dqt::plan_bwd_batch(n, L, M);
+  if (ws == nullptr || ws_bytes < P.total) return DQT_ERR_WORKSPACE;
+  if (!aligned16(ws)) return DQT_ERR_ALIGN;
+  for (int l = 0; l < n; ++l) {
+    if (io[l].dW != nullptr) {
+      if (!aligned16(io[l].dW)) return DQT_ERR_ALIGN;
+      if (M > 0 && (io[l].Xq == nullptr || io[l].xdq == nullptr)) return DQT_ERR_NULL;
+    }
+    if ((io[l].dX != nullptr || io[l].dW != nullptr) && M > 0) {
+      if (io[l].dY == nullptr) return DQT_ERR_NULL;
+      if (!aligned16(io[l].dY)) return DQT_ERR_ALIGN;
+    }
+    if (io[l].Xq != nullptr && !aligned16(io[l].Xq)) return DQT_ERR_ALIGN;
+    if (io[l].xdq != nullptr && !aligned16(io[l].xdq)) return DQT_ERR_ALIGN;
+    if (io[l].dX != nullptr) {
+      if (M > 0 && io[l].Wq == nullptr) return DQT_ERR_NULL;
+      if (!aligned16(io[l].dX) || (io[l].Wq != nullptr && !aligned16(io[l].Wq))) return DQT_ERR_ALIGN;
+    }
+  }
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  uint8_t* wsb = static_cast<uint8_t*>(ws);
+  dqt::LinearIO sub[DQT_MAX_BATCH];
+  // dX for the linears that want it
+  int nx = 0;
+  dqt::BwdPlan Px = P;
+  for (int l = 0; l < n; ++l)
+    if (io[l].dX != nullptr) {
+      Px.q_off[nx] = P.q_off[l];
+      sub[nx++] = L[l];
+    }
+  if (nx > 0 && M > 0) {
+    if (dy_t == DQT_BF16) {
+      dqt::BatchCfg c{nx, M, wfmt == DQT_TERNARY2, act_q == DQT_FP8E4M3, dx_t == DQT_BF16};
+      st = from_hip(dqt::launch_dx_batch(c, sub, wsb, Px, s));
+    } else {
+      for (int l = 0; l < nx && st == DQT_OK; ++l) {
+        dqt::DxArgs a;
+        a.dY = sub[l].dY;
+        a.Wq = sub[l].Wq;
+        a.dX = sub[l].dX;
+        a.M = M;
+        a.d_in = sub[l].d_in;
+        a.d_out = sub[l].d_out;
+        a.alpha = sub[l].alpha;
+        a.w_ternary = wfmt == DQT_TERNARY2;
+        a.dy_bf16 = false;
+        a.dx_bf16 = dx_t == DQT_BF16;
+        st = from_hip(dqt::launch_dx_f32(a, s));
+      }
+    }
+    if (st != DQT_OK) return st;
+  }
+  // dW for the linears that want it
+  int nw = 0;
+  dqt::BwdPlan Pw = P;
+  for (int l = 0; l < n; ++l)
+    if (io[l].dW != nullptr) {
+      Pw.xt_off[nw] = P.xt_off[l];
+      Pw.part_off[nw] = P.part_off[l];
+      sub[nw++] = L[l];
+    }
+  if (nw > 0) {
+    if (xt_t == DQT_BF16) {
+      dqt::BatchCfg c{nw, M, wfmt == DQT_TERNARY2, act_q == DQT_FP8E4M3, false};
+      st = from_hip(dqt::launch_dw_batch(c, sub, wsb, Pw, s));
+    } else {
+      for (int l = 0; l < nw && st == DQT_OK; ++l) {
+        dqt::DwArgs a;
+        a.dY = sub[l].dY;
+        a.Xq = sub[l].Xq;
+        a.xdq = sub[l].xdq;
+        a.dW = sub[l].dW;
+        a.ws = reinterpret_cast<float*>(wsb + Pw.part_off[l]);
+        a.M = M;
+        a.d_in = sub[l].d_in;
+        a.d_out = sub[l].d_out;
+        a.splits = 0;
+        a.act_e4m3 = act_q == DQT_FP8E4M3;
+        a.xt_bf16 = false;
+        st = from_hip(dqt::launch_dw_f32(a, s));
+      }
+    }
+  }
+  return st;
+}
+
+dqt_status dqt_sr_update_batch(int32_t n, const dqt_linear_io* io, float lr, uint64_t seed,
+                               uint32_t step, unsigned long long* counters, void* stream) {
+  dqt::LinearIO L[DQT_MAX_BATCH];
+  int32_t wfmt;
+  dqt_status st = check_batch(n, io, L, &wfmt);
+  if (st != DQT_OK) return st;
+  if (counters != nullptr && (reinterpret_cast<uintptr_t>(counters) & 7u) != 0) return DQT_ERR_ALIGN;
+  if (!(isfinite(lr) && lr >= 0.0f)) return DQT_ERR_RANGE;
+  dqt::SRTensor t[DQT_MAX_BATCH];
+  for (int l = 0; l < n; ++l) {
+    if (io[l].Wq == nullptr || io[l].dW == nullptr) return DQT_ERR_NULL;
+    if (!aligned16(io[l].Wq) || !aligned16(io[l].dW)) return DQT_ERR_ALIGN;
+    const float c = lr / io[l].w->alpha;   // one correctly rounded fp32 division
+    if (!isfinite(c)) return DQT_ERR_RANGE;
+    t[l].wq = static_cast<uint8_t*>(io[l].Wq);
+    t[l].grad = io[l].dW;
+    t[l].nweights = (int64_t)io[l].w->d_out * (int64_t)io[l].w->d_in;
+    t[l].c = c;
+    t[l].qmin = io[l].w->qmin;
+    t[l].qmax = io[l].w->qmax;
+    t[l].tensor_id = io[l].w->tensor_id;
+  }
+  return from_hip(dqt::launch_sr_update(wfmt == DQT_TERNARY2, n, t, seed, step, counters,
+                                        static_cast<hipStream_t>(stream)));
+}
+
+// ---------------------------------------------------------- single linears
+
 size_t dqt_linear_fwd_workspace(const dqt_weight* w) {
-  if (check_weight(w) != DQT_OK) return 0;
-  return dqt::fwd_workspace_bytes(w->wfmt == DQT_TERNARY2, w->d_out, w->d_in);
+  dqt_linear_io io{};
+  io.w = w;
+  return dqt_linear_fwd_batch_workspace(1, &io);
 }
 
 dqt_status dqt_linear_fwd(const dqt_weight* w, const void* Wq, const void* X, int32_t x_t,
@@ -91,135 +291,49 @@ dqt_status dqt_linear_fwd(const dqt_weight* w, const void* Wq, const void* X, in
   const size_t need = dqt_linear_fwd_workspace(w);
   if (need > 0 && (ws == nullptr || ws_bytes < need)) return DQT_ERR_WORKSPACE;
   if (need > 0 && !aligned16(ws)) return DQT_ERR_ALIGN;
-  hipStream_t s = static_cast<hipStream_t>(stream);
   if (X != nullptr) {
     st = from_hip(dqt::launch_act_quant(X, x_t == DQT_BF16, M, w->d_in, act_q == DQT_FP8E4M3, Xq,
-                                        xdq, s));
+                                        xdq, static_cast<hipStream_t>(stream)));
     if (st != DQT_OK) return st;
   }
-  dqt::FwdArgs a;
-  a.Xq = Xq;
-  a.xdq = xdq;
-  a.Wq = Wq;
-  a.Y = Y;
-  a.M = M;
-  a.d_in = w->d_in;
-  a.d_out = w->d_out;
-  a.ws = ws;
-  a.alpha = w->alpha;
-  a.w_ternary = w->wfmt == DQT_TERNARY2;
-  a.act_e4m3 = act_q == DQT_FP8E4M3;
-  a.y_bf16 = y_t == DQT_BF16;
-  return from_hip(dqt::launch_fwd_v2(a, s));
-}
-
-// Backward workspace layout (each region 256-byte aligned):
-//   [fp32 split partials: splits * d_out * d_in]   (when splits > 1)
-//   [bf16 weights: d_out * d_in]                   (bf16-environment dX)
-//   [bf16 X~: M * d_in]                            (bf16-environment dW)
-struct BwdLayout {
-  int64_t splits;
-  size_t part, q, xt, total;
-};
-static size_t align256(size_t n) { return (n + 255) / 256 * 256; }
-static BwdLayout bwd_layout(const dqt_weight* w, int64_t M) {
-  BwdLayout L;
-  int wj;
-  int64_t s_v2;
-  dqt::plan_dw_v2(w->d_out, w->d_in, M, &wj, &s_v2);
-  const int64_t s_f32 = dqt::dw_splits_f32(w->d_out, w->d_in, M);
-  L.splits = s_v2 > s_f32 ? s_v2 : s_f32;
-  const size_t wn = (size_t)w->d_out * (size_t)w->d_in;
-  L.part = L.splits > 1 ? align256((size_t)L.splits * wn * sizeof(float)) : 0;
-  L.q = align256(wn * 2);
-  L.xt = align256((size_t)M * (size_t)w->d_in * 2);
-  L.total = L.part + L.q + L.xt;
-  return L;
+  dqt_linear_io io{};
+  io.w = w;
+  io.Wq = const_cast<void*>(Wq);
+  io.Xq = Xq;
+  io.xdq = xdq;
+  io.Y = Y;
+  return dqt_linear_fwd_batch(1, &io, M, act_q, y_t, ws, ws_bytes, stream);
 }
 
 size_t dqt_linear_bwd_workspace(const dqt_weight* w, int64_t M) {
-  if (check_weight(w) != DQT_OK || M < 0) return 0;
-  return bwd_layout(w, M).total;
+  dqt_linear_io io{};
+  io.w = w;
+  return dqt_linear_bwd_batch_workspace(1, &io, M);
 }
 
 dqt_status dqt_linear_bwd(const dqt_weight* w, const void* Wq, const void* Xq, int32_t act_q,
                           const float* xdq, const void* dY, int32_t dy_t, int64_t M,
                           int32_t xt_t, void* dX, int32_t dx_t, float* dW, void* ws,
                           size_t ws_bytes, void* stream) {
-  dqt_status st = check_weight(w);
-  if (st != DQT_OK) return st;
-  if (M < 0) return DQT_ERR_SHAPE;
-  if (act_q != DQT_I8 && act_q != DQT_FP8E4M3) return DQT_ERR_DTYPE;
-  if (!is_float_type(dy_t) || !is_float_type(xt_t)) return DQT_ERR_DTYPE;
-  if (dX != nullptr && !is_float_type(dx_t)) return DQT_ERR_DTYPE;
-  if (dW != nullptr && dy_t != xt_t) return DQT_ERR_UNSUPPORTED;
-  if (dX == nullptr && dW == nullptr) return DQT_OK;
-  const BwdLayout L = bwd_layout(w, M);
-  if (ws == nullptr || ws_bytes < L.total) return DQT_ERR_WORKSPACE;
-  if (!aligned16(ws)) return DQT_ERR_ALIGN;
-  uint8_t* wsb = static_cast<uint8_t*>(ws);
-  if (dW != nullptr) {
-    if (!aligned16(dW)) return DQT_ERR_ALIGN;
-    if (M > 0 && (Xq == nullptr || xdq == nullptr)) return DQT_ERR_NULL;
-  }
-  if (M > 0) {
-    if (dY == nullptr) return DQT_ERR_NULL;
-    if (!aligned16(dY)) return DQT_ERR_ALIGN;
-    if (Xq != nullptr && !aligned16(Xq)) return DQT_ERR_ALIGN;
-    if (xdq != nullptr && !aligned16(xdq)) return DQT_ERR_ALIGN;
-  }
-  if (dX != nullptr) {
-    if (M > 0 && Wq == nullptr) return DQT_ERR_NULL;
-    if (!aligned16(dX) || (Wq != nullptr && !aligned16(Wq))) return DQT_ERR_ALIGN;
-  }
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  if (dX != nullptr && M > 0) {
-    dqt::DxArgs a;
-    a.dY = dY;
-    a.Wq = Wq;
-    a.dX = dX;
-    a.M = M;
-    a.d_in = w->d_in;
-    a.d_out = w->d_out;
-    a.alpha = w->alpha;
-    a.w_ternary = w->wfmt == DQT_TERNARY2;
-    a.dy_bf16 = dy_t == DQT_BF16;
-    a.dx_bf16 = dx_t == DQT_BF16;
-    st = from_hip(a.dy_bf16 ? dqt::launch_dx_v2(a, wsb + L.part, s) : dqt::launch_dx_f32(a, s));
-    if (st != DQT_OK) return st;
-  }
-  if (dW != nullptr) {
-    dqt::DwArgs a;
-    a.dY = dY;
-    a.Xq = Xq;
-    a.xdq = xdq;
-    a.dW = dW;
-    a.ws = reinterpret_cast<float*>(wsb);
-    a.M = M;
-    a.d_in = w->d_in;
-    a.d_out = w->d_out;
-    a.splits = L.splits;
-    a.act_e4m3 = act_q == DQT_FP8E4M3;
-    a.xt_bf16 = xt_t == DQT_BF16;
-    st = from_hip(a.xt_bf16 ? dqt::launch_dw_v2(a, wsb + L.part + L.q, s) : dqt::launch_dw_f32(a, s));
-  }
-  return st;
+  dqt_linear_io io{};
+  io.w = w;
+  io.Wq = const_cast<void*>(Wq);
+  io.Xq = Xq;
+  io.xdq = xdq;
+  io.dY = dY;
+  io.dX = dX;
+  io.dW = dW;
+  if (dX == nullptr && !is_float_type(dx_t)) dx_t = DQT_F32;   // unused
+  return dqt_linear_bwd_batch(1, &io, M, act_q, dy_t, xt_t, dx_t, ws, ws_bytes, stream);
 }
 
 dqt_status dqt_sr_update(const dqt_weight* w, void* Wq, const float* dW, float lr, uint64_t seed,
                          uint32_t step, unsigned long long* counters, void* stream) {
-  dqt_status st = check_weight(w);
-  if (st != DQT_OK) return st;
-  if (Wq == nullptr || dW == nullptr) return DQT_ERR_NULL;
-  if (!aligned16(Wq) || !aligned16(dW)) return DQT_ERR_ALIGN;
-  if (counters != nullptr && (reinterpret_cast<uintptr_t>(counters) & 7u) != 0) return DQT_ERR_ALIGN;
-  if (!(isfinite(lr) && lr >= 0.0f)) return DQT_ERR_RANGE;
-  const float c = lr / w->alpha;  // one correctly rounded fp32 division
-  if (!isfinite(c)) return DQT_ERR_RANGE;
-  const int64_t n = (int64_t)w->d_out * (int64_t)w->d_in;
-  return from_hip(dqt::launch_sr_update(w->wfmt == DQT_TERNARY2, static_cast<uint8_t*>(Wq), dW, n,
-                                        c, w->qmin, w->qmax, seed, step, w->tensor_id, counters,
-                                        static_cast<hipStream_t>(stream)));
+  dqt_linear_io io{};
+  io.w = w;
+  io.Wq = Wq;
+  io.dW = const_cast<float*>(dW);
+  return dqt_sr_update_batch(1, &io, lr, seed, step, counters, stream);
 }
 
 dqt_status dqt_debug_rng(uint64_t seed, uint32_t step, uint32_t tensor_id, uint64_t i0, int64_t n,

@@ -9,17 +9,6 @@
 
 namespace dqt {
 
-struct FwdArgs {
-  const void* Xq;       // [M, d_in] int8 or e4m3
-  const float* xdq;     // [M]
-  const void* Wq;       // packed ternary or int8 codes
-  void* Y;              // [M, d_out]
-  int64_t M, d_in, d_out;
-  void* ws;             // unpacked weight rows (ternary weights only)
-  float alpha;
-  bool w_ternary, act_e4m3, y_bf16;
-};
-
 struct DxArgs {
   const void* dY;       // [M, d_out]
   const void* Wq;
@@ -41,20 +30,55 @@ struct DwArgs {
 
 hipError_t launch_act_quant(const void* X, bool x_bf16, int64_t M, int K, bool e4m3, void* Xq,
                             float* xdq, hipStream_t stream);
-// int8 / e4m3 / bf16 matrix-core kernels
-size_t fwd_workspace_bytes(bool ternary, int64_t d_out, int64_t d_in);
-hipError_t launch_fwd_v2(const FwdArgs& a, hipStream_t stream);
-hipError_t launch_dx_v2(const DxArgs& a, void* ws_q, hipStream_t stream);
-hipError_t launch_dw_v2(const DwArgs& a, void* ws_xt, hipStream_t stream);
-void plan_dw_v2(int64_t d_out, int64_t d_in, int64_t M, int* wj, int64_t* splits);
+// int8 / e4m3 / bf16 matrix-core kernels, batched: up to kMaxBatch linears
+// (same dtypes, same token count M) per launch.
+constexpr int kMaxBatch = 8;
+struct LinearIO {
+  int64_t d_in, d_out;
+  float alpha;
+  const void* Wq;       // codes
+  const void* Xq;       // [M, d_in] quantised input
+  const float* xdq;     // [M]
+  void* Y;              // [M, d_out]
+  const void* dY;       // [M, d_out]
+  void* dX;             // [M, d_in]
+  float* dW;            // [d_out, d_in]
+};
+struct BatchCfg {
+  int n;
+  int64_t M;
+  bool w_ternary, act_e4m3, out_bf16;
+};
+struct BwdPlan {
+  int64_t splits;
+  int wj;
+  size_t q_off[kMaxBatch], xt_off[kMaxBatch], part_off[kMaxBatch];
+  size_t total;
+};
+size_t fwd_batch_workspace(int n, const LinearIO* io, bool ternary, size_t* offs);
+hipError_t launch_fwd_batch(const BatchCfg& c, const LinearIO* io, uint8_t* ws, hipStream_t stream);
+BwdPlan plan_bwd_batch(int n, const LinearIO* io, int64_t M);
+hipError_t launch_dx_batch(const BatchCfg& c, const LinearIO* io, uint8_t* ws, const BwdPlan& P,
+                           hipStream_t stream);
+hipError_t launch_dw_batch(const BatchCfg& c, const LinearIO* io, uint8_t* ws, const BwdPlan& P,
+                           hipStream_t stream);
 // fp32-environment kernels
 hipError_t launch_dx_f32(const DxArgs& a, hipStream_t stream);
 hipError_t launch_dw_f32(const DwArgs& a, hipStream_t stream);
 int64_t dw_splits_f32(int64_t d_out, int64_t d_in, int64_t M);
 hipError_t launch_split_reduce(const float* ws, int splits, int64_t n, float* out, hipStream_t stream);
-hipError_t launch_sr_update(bool ternary, uint8_t* wq, const float* grad, int64_t nweights,
-                            float c, int qmin, int qmax, uint64_t seed, uint32_t step,
-                            uint32_t tensor_id, unsigned long long* counters, hipStream_t stream);
+// Direct SR update of up to kMaxBatch weight tensors (same code format) in
+// one launch.
+struct SRTensor {
+  uint8_t* wq;          // codes, updated in place
+  const float* grad;    // dW
+  int64_t nweights;     // multiple of 16
+  float c;              // fl32(lr / alpha)
+  int qmin, qmax;
+  uint32_t tensor_id;
+};
+hipError_t launch_sr_update(bool ternary, int n, const SRTensor* t, uint64_t seed, uint32_t step,
+                            unsigned long long* counters, hipStream_t stream);
 hipError_t launch_debug_rng(uint64_t seed, uint32_t step, uint32_t tensor_id, uint64_t i0,
                             int64_t n, uint32_t* out, hipStream_t stream);
 

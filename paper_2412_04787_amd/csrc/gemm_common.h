@@ -11,18 +11,33 @@ template <Mfma K> struct AccT { using type = f32x16; };
 template <> struct AccT<Mfma::I8> { using type = i32x16; };
 
 // ------------------------------------------------------------- epilogues
-// (i, j) -> value written.  acc is int32 (I8) or fp32.
+// An epilogue maps the accumulator of output (i, j) to the value stored:
+//   scale(i)  per-row factor (1 when unused), applied as fl(acc * scale)
+//   row(i)    address of output row i; out_bf16 selects the stored dtype.
+// The fp32 result is rounded once to bf16 (RNE) when out_bf16 is set.
 struct EpiFwd {          // y = fl(fl(acc) * fl(xdq[i] * alpha))
   void* y; int64_t ld; bool bf16; const float* xdq; float alpha;
+  static constexpr bool kRowScale = true;
+  __device__ float scale(int64_t i) const { return xdq[i] * alpha; }
+  __device__ bool out_bf16() const { return bf16; }
+  __device__ uint8_t* row(int64_t i, int) const {
+    return static_cast<uint8_t*>(y) + i * ld * (bf16 ? 2 : 4);
+  }
+  // scalar path used by the fp32-environment kernels
   __device__ void put(int64_t i, int64_t j, float acc) const {
-    const float f = xdq[i] * alpha;
-    const float v = acc * f;
+    const float v = acc * scale(i);
     if (bf16) reinterpret_cast<uint16_t*>(y)[i * ld + j] = (uint16_t)f32_to_bf16_bits(v);
     else reinterpret_cast<float*>(y)[i * ld + j] = v;
   }
 };
 struct EpiScale {        // y = fl(alpha * acc)
   void* y; int64_t ld; bool bf16; float alpha;
+  static constexpr bool kRowScale = false;
+  __device__ float scale(int64_t) const { return alpha; }
+  __device__ bool out_bf16() const { return bf16; }
+  __device__ uint8_t* row(int64_t i, int) const {
+    return static_cast<uint8_t*>(y) + i * ld * (bf16 ? 2 : 4);
+  }
   __device__ void put(int64_t i, int64_t j, float acc) const {
     const float v = alpha * acc;
     if (bf16) reinterpret_cast<uint16_t*>(y)[i * ld + j] = (uint16_t)f32_to_bf16_bits(v);
@@ -31,10 +46,15 @@ struct EpiScale {        // y = fl(alpha * acc)
 };
 struct EpiPartial {      // fp32 partial sums, one slab per split
   float* y; int64_t ld; int64_t slab;
+  static constexpr bool kRowScale = false;
+  __device__ float scale(int64_t) const { return 1.0f; }
+  __device__ bool out_bf16() const { return false; }
+  __device__ uint8_t* row(int64_t i, int split) const {
+    return reinterpret_cast<uint8_t*>(y + (int64_t)split * slab + i * ld);
+  }
   __device__ void put(int64_t i, int64_t j, float acc) const {
     y[(int64_t)blockIdx.z * slab + i * ld + j] = acc;
   }
 };
-
 
 }  // namespace dqt

@@ -131,9 +131,25 @@ struct Plan {
   }
 };
 
+// One GEMM problem of a grouped launch, with its tile grid (nbx x nby x
+// nbz tiles: column tiles, row tiles, reduction splits) and the index of its
+// first tile in the launch.
+template <class Epi>
+struct Prob {
+  Opnd A, B;
+  Epi epi;
+  int64_t I, J, R, split_len;
+  int32_t nbx, nby, nbz, tile0;
+};
+constexpr int MAXG = 8;
+template <class Epi>
+struct Group {
+  Prob<Epi> p[MAXG];
+  int32_t ng;
+};
+
 template <int ELEM, int MA, int MB, int WJ, class Epi>
-__global__ __launch_bounds__(NTH) void gemm_v2_kernel(Opnd A, Opnd B, Epi epi, int64_t I,
-                                                         int64_t J, int64_t R, int64_t split_len) {
+__global__ __launch_bounds__(NTH) void gemm_v2_kernel(const Group<Epi> grp) {
   using C = Cfg<ELEM, MA, MB, WJ>;
   __shared__ __attribute__((aligned(1024))) uint8_t smem_generic[C::LDS];
   lds_u8* smem = (lds_u8*)smem_generic;
@@ -143,9 +159,32 @@ __global__ __launch_bounds__(NTH) void gemm_v2_kernel(Opnd A, Opnd B, Epi epi, i
   const int wave = tid >> 6;
   const int wi = wave >> 1, wj = wave & 1;
   const int h = lane >> 5;
-  const int64_t i0 = (int64_t)blockIdx.y * C::TRA;
-  const int64_t j0 = (int64_t)blockIdx.x * C::TRB;
-  const int64_t r_begin = (int64_t)blockIdx.z * split_len;
+  // Workgroups are dispatched round-robin over the 8 XCDs (hardware id w
+  // runs on XCD w mod 8, each XCD with its own L2).  Give every XCD a
+  // contiguous run of tiles -- problem, then split, then row tile, then
+  // column tile -- so that blocks sharing operand tiles share an L2.
+  int g = 0, bx, by, bz;
+  {
+    const int nb = gridDim.x;
+    const int w = blockIdx.x;
+    const int xcd = w & 7, k = w >> 3;
+    const int per = nb >> 3, rem = nb & 7;
+    const int L = xcd * per + (xcd < rem ? xcd : rem) + k;
+    while (g + 1 < grp.ng && L >= grp.p[g + 1].tile0) ++g;
+    const int local = L - grp.p[g].tile0;
+    const int nbx = grp.p[g].nbx, nby = grp.p[g].nby;
+    bx = local % nbx;
+    by = (local / nbx) % nby;
+    bz = local / (nbx * nby);
+  }
+  const Opnd A = grp.p[g].A;
+  const Opnd B = grp.p[g].B;
+  const Epi epi = grp.p[g].epi;
+  const int64_t I = grp.p[g].I, J = grp.p[g].J, R = grp.p[g].R;
+  const int64_t split_len = grp.p[g].split_len;
+  const int64_t i0 = (int64_t)by * C::TRA;
+  const int64_t j0 = (int64_t)bx * C::TRB;
+  const int64_t r_begin = (int64_t)bz * split_len;
   int64_t r_end = r_begin + split_len;
   if (r_end > R) r_end = R;
   const int64_t rlen = r_end > r_begin ? r_end - r_begin : 0;
@@ -156,26 +195,33 @@ __global__ __launch_bounds__(NTH) void gemm_v2_kernel(Opnd A, Opnd B, Epi epi, i
   Plan<MB, C::TRB, C::EB> pb;
   pa.init(A, i0, r_begin);
   pb.init(B, j0, r_begin);
+  // wave-uniform LDS offset of this wave's DMA chunks (kept in an SGPR)
+  const int wave_u = __builtin_amdgcn_readfirstlane(wave);
 
+  // Issue the DMA of stage s (its slot is s mod STAGES).  The per-thread
+  // source pointers advance by one step per call, so stages are issued in
+  // order 0, 1, 2, ...
   auto issue = [&](int s) {
-    lds_u8* la = smem + (s % STAGES) * C::STAGE;
+    lds_u8* la = smem + (s % STAGES) * C::STAGE + wave_u * 1024;
     lds_u8* lb = la + C::A_BYTES;
     const bool last = tail && s == nsteps - 1;
-    const int64_t rbase = (int64_t)s * C::BK;
+    if (!last) {
 #pragma unroll
-    for (int q = 0; q < C::NLA; ++q) {
-      const uint8_t* g = pa.g[q] + (int64_t)s * pa.inc;
-      if (last && rbase + pa.rk[q] >= rlen) g = pa.safe[q];
-      dma16(g, la + (q * 4 + wave) * 1024);
-    }
+      for (int q = 0; q < C::NLA; ++q) dma16(pa.g[q] + (int64_t)s * pa.inc, la + q * 4096);
 #pragma unroll
-    for (int q = 0; q < C::NLB; ++q) {
-      const uint8_t* g = pb.g[q] + (int64_t)s * pb.inc;
-      if (last && rbase + pb.rk[q] >= rlen) g = pb.safe[q];
-      dma16(g, lb + (q * 4 + wave) * 1024);
+      for (int q = 0; q < C::NLB; ++q) dma16(pb.g[q] + (int64_t)s * pb.inc, lb + q * 4096);
+    } else {
+      const int64_t rbase = (int64_t)s * C::BK;
+#pragma unroll
+      for (int q = 0; q < C::NLA; ++q)
+        dma16(rbase + pa.rk[q] >= rlen ? pa.safe[q] : pa.g[q] + (int64_t)s * pa.inc, la + q * 4096);
+#pragma unroll
+      for (int q = 0; q < C::NLB; ++q)
+        dma16(rbase + pb.rk[q] >= rlen ? pb.safe[q] : pb.g[q] + (int64_t)s * pb.inc, lb + q * 4096);
     }
   };
-  // zero the chunks this lane loaded past the end of the reduction
+  // zero the chunks this lane loaded past the end of the reduction (the
+  // lane's own DMA for stage s has completed)
   auto zero_tail = [&](int s) {
     lds_u8* la = smem + (s % STAGES) * C::STAGE;
     lds_u8* lb = la + C::A_BYTES;
@@ -202,72 +248,79 @@ __global__ __launch_bounds__(NTH) void gemm_v2_kernel(Opnd A, Opnd B, Epi epi, i
   const int frow = lane & 31;
   const int t4 = (lane >> 2) & 3, u4 = lane & 3, ch = (lane >> 4) & 1;
 
-  auto frag_kc = [&](const lds_u8* base, int row, int kk) -> i32x4 {
-    const int c = (2 * kk + h) ^ ((row >> 2) & 3);
-    return *(const __attribute__((address_space(3))) i32x4*)(base + row * 64 + 16 * c);
-  };
-  // K-major fragments: two transposing reads give reduction slots 0-3 and
-  // 4-7 of the lane's column.  Issued as inline asm: the compiler would
-  // otherwise order every such read after all outstanding DMA (vmcnt(0)),
-  // serialising the ring; the vmcnt waits and barrier above already order the
-  // DMA before these reads, and tr_wait() below orders the reads before use.
-  auto frag_km = [&](const lds_u8* base, int col0, int kk, u32x2& lo, u32x2& hi) {
-    const int col = col0 + 16 * ch + 4 * u4;
-    const int region = col >> 6;
-    const int seg = ((col & 63) >> 4) ^ t4;
-    const uint32_t a0 = (uint32_t)(uintptr_t)(base + region * 4096 + (16 * kk + 8 * h + t4) * 128 +
-                                              32 * seg + 8 * u4);
-    asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(lo) : "v"(a0));
-    asm volatile("ds_read_b64_tr_b16 %0, %1 offset:512" : "=v"(hi) : "v"(a0));
-  };
-
-  const int npre = nsteps < STAGES - 1 ? nsteps : STAGES - 1;
-  for (int s = 0; s < npre; ++s) issue(s);
-
-  constexpr int LPS = C::NLA + C::NLB;   // DMA instructions per thread per stage
-  for (int it = 0; it < nsteps; ++it) {
-    const int ahead = nsteps - 1 - it < STAGES - 2 ? nsteps - 1 - it : STAGES - 2;
-    if (ahead >= 2) wait_vm<2 * LPS>();
-    else if (ahead == 1) wait_vm<LPS>();
-    else wait_vm<0>();
-    if (tail && it == nsteps - 1) zero_tail(it);
-    block_barrier();
-    if (it + STAGES - 1 < nsteps) issue(it + STAGES - 1);
-
-    const lds_u8* la = smem + (it % STAGES) * C::STAGE;
-    const lds_u8* lb = la + C::A_BYTES;
+  // Fragments of one step: fa/fb for K-contiguous operands (ds_read_b128,
+  // tracked by the compiler), ka/kb halves for K-major operands (transposing
+  // reads issued as inline asm: the compiler would otherwise order every such
+  // read after all outstanding DMA, vmcnt(0), serialising the ring; the vmcnt
+  // waits and barriers order the DMA before these reads, and frag_wait()
+  // orders the reads before use).
+  struct Frags {
     i32x4 fa[2][2], fb[WJ][2];
-    u32x2 ta_lo[2][2], ta_hi[2][2], tb_lo[WJ][2], tb_hi[WJ][2];
+    u32x2 ka[2][2][2], kb[WJ][2][2];
+  };
+  auto read_frags = [&](int s, Frags& F) {
+    const lds_u8* la = smem + (s % STAGES) * C::STAGE;
+    const lds_u8* lb = la + C::A_BYTES;
 #pragma unroll
     for (int t = 0; t < 2; ++t)
 #pragma unroll
       for (int kk = 0; kk < 2; ++kk) {
-        if constexpr (MA == KC) fa[t][kk] = frag_kc(la, wi * 64 + t * 32 + frow, kk);
-        else frag_km(la, wi * 64 + t * 32, kk, ta_lo[t][kk], ta_hi[t][kk]);
+        if constexpr (MA == KC) {
+          const int row = wi * 64 + t * 32 + frow;
+          const int c = (2 * kk + h) ^ ((row >> 2) & 3);
+          F.fa[t][kk] = *(const __attribute__((address_space(3))) i32x4*)(la + row * 64 + 16 * c);
+        } else {
+          const int col = wi * 64 + t * 32 + 16 * ch + 4 * u4;
+          const int seg = ((col & 63) >> 4) ^ t4;
+          const uint32_t a0 = (uint32_t)(uintptr_t)(la + (col >> 6) * 4096 +
+                                                    (16 * kk + 8 * h + t4) * 128 + 32 * seg + 8 * u4);
+          asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(F.ka[t][kk][0]) : "v"(a0));
+          asm volatile("ds_read_b64_tr_b16 %0, %1 offset:512" : "=v"(F.ka[t][kk][1]) : "v"(a0));
+        }
       }
 #pragma unroll
     for (int t = 0; t < WJ; ++t)
 #pragma unroll
       for (int kk = 0; kk < 2; ++kk) {
-        if constexpr (MB == KC) fb[t][kk] = frag_kc(lb, wj * 32 * WJ + t * 32 + frow, kk);
-        else frag_km(lb, wj * 32 * WJ + t * 32, kk, tb_lo[t][kk], tb_hi[t][kk]);
+        if constexpr (MB == KC) {
+          const int row = wj * 32 * WJ + t * 32 + frow;
+          const int c = (2 * kk + h) ^ ((row >> 2) & 3);
+          F.fb[t][kk] = *(const __attribute__((address_space(3))) i32x4*)(lb + row * 64 + 16 * c);
+        } else {
+          const int col = wj * 32 * WJ + t * 32 + 16 * ch + 4 * u4;
+          const int seg = ((col & 63) >> 4) ^ t4;
+          const uint32_t a0 = (uint32_t)(uintptr_t)(lb + (col >> 6) * 4096 +
+                                                    (16 * kk + 8 * h + t4) * 128 + 32 * seg + 8 * u4);
+          asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(F.kb[t][kk][0]) : "v"(a0));
+          asm volatile("ds_read_b64_tr_b16 %0, %1 offset:512" : "=v"(F.kb[t][kk][1]) : "v"(a0));
+        }
       }
+  };
+  // wait for this wave's outstanding LDS reads; ties the K-major halves so
+  // that no use is scheduled before the wait
+  auto frag_wait = [&](Frags& F) {
     if constexpr (MA == KM) {
-      tr_wait4(ta_lo[0][0], ta_hi[0][0], ta_lo[0][1], ta_hi[0][1]);
-      tr_wait4(ta_lo[1][0], ta_hi[1][0], ta_lo[1][1], ta_hi[1][1]);
 #pragma unroll
       for (int t = 0; t < 2; ++t)
-#pragma unroll
-        for (int kk = 0; kk < 2; ++kk) fa[t][kk] = join(ta_lo[t][kk], ta_hi[t][kk]);
+        tr_wait4(F.ka[t][0][0], F.ka[t][0][1], F.ka[t][1][0], F.ka[t][1][1]);
     }
     if constexpr (MB == KM) {
 #pragma unroll
-      for (int t = 0; t < WJ; ++t) tr_wait4(tb_lo[t][0], tb_hi[t][0], tb_lo[t][1], tb_hi[t][1]);
-#pragma unroll
       for (int t = 0; t < WJ; ++t)
-#pragma unroll
-        for (int kk = 0; kk < 2; ++kk) fb[t][kk] = join(tb_lo[t][kk], tb_hi[t][kk]);
+        tr_wait4(F.kb[t][0][0], F.kb[t][0][1], F.kb[t][1][0], F.kb[t][1][1]);
     }
+    if constexpr (MA == KC && MB == KC) __builtin_amdgcn_s_waitcnt((15) | (3 << 14) | (7 << 4) | (0 << 8));
+  };
+  auto mfma_step = [&](Frags& F) {
+    i32x4 fa[2][2], fb[WJ][2];
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk) fa[t][kk] = MA == KC ? F.fa[t][kk] : join(F.ka[t][kk][0], F.ka[t][kk][1]);
+#pragma unroll
+    for (int t = 0; t < WJ; ++t)
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk) fb[t][kk] = MB == KC ? F.fb[t][kk] : join(F.kb[t][kk][0], F.kb[t][kk][1]);
 #pragma unroll
     for (int ta = 0; ta < 2; ++ta) {
 #pragma unroll
@@ -287,31 +340,109 @@ __global__ __launch_bounds__(NTH) void gemm_v2_kernel(Opnd A, Opnd B, Epi epi, i
                             fa[ta][1][0], fa[ta][1][1], fa[ta][1][2], fa[ta][1][3]};
           const i32x8 bv = {fb[tb][0][0], fb[tb][0][1], fb[tb][0][2], fb[tb][0][3],
                             fb[tb][1][0], fb[tb][1][1], fb[tb][1][2], fb[tb][1][3]};
+          // both operands e4m3 (format 0), unit E8M0 scales (127 = 2^0)
           acc[ta][tb] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(av, bv, acc[ta][tb], 0, 0, 0,
                                                                         127, 0, 127);
         }
       }
     }
-  }
+  };
 
-  // epilogue: lane (j = lane mod 32, h) of block (ta, tb) holds rows
-  // 8 (r / 4) + 4 h + (r mod 4), r = 0..15
+  // Pipeline.  The ring holds STAGES steps.  Before the loop: DMA of stages
+  // 0 .. STAGES-1, then step 0's fragments.  Iteration `it`: wait for stage
+  // it+1's DMA, barrier (every wave has its step-it fragments in registers,
+  // so slot it mod STAGES is free), DMA stage it+STAGES into that slot, read
+  // step it+1's fragments, run step it's MFMAs while those reads land.
+  constexpr int LPS = C::NLA + C::NLB;   // DMA instructions per thread per stage
+  const int npre = nsteps < STAGES ? nsteps : STAGES;
+  for (int s = 0; s < npre; ++s) issue(s);
+  auto wait_stages = [&](int pending) {   // allow `pending` later stages in flight
+    if (pending >= 3) wait_vm<3 * LPS>();
+    else if (pending == 2) wait_vm<2 * LPS>();
+    else if (pending == 1) wait_vm<LPS>();
+    else wait_vm<0>();
+  };
+  Frags F0, F1;
+  if (nsteps > 0) {
+    wait_stages(npre - 1);
+    if (tail && nsteps == 1) zero_tail(0);
+    block_barrier();
+    read_frags(0, F0);
+    frag_wait(F0);
+  }
+  auto iteration = [&](int it, Frags& cur, Frags& nxt) {
+    if (it + 1 < nsteps) {
+      const int issued_last = (it - 1 + STAGES < nsteps - 1) ? it - 1 + STAGES : nsteps - 1;
+      wait_stages(issued_last - (it + 1));
+      if (tail && it + 1 == nsteps - 1) zero_tail(it + 1);
+    }
+    block_barrier();
+    if (it + STAGES < nsteps) issue(it + STAGES);
+    if (it + 1 < nsteps) read_frags(it + 1, nxt);
+    mfma_step(cur);
+    if (it + 1 < nsteps) frag_wait(nxt);
+  };
+  int it = 0;
+  for (; it + 1 < nsteps; it += 2) {
+    iteration(it, F0, F1);
+    iteration(it + 1, F1, F0);
+  }
+  if (it < nsteps) iteration(it, F0, F1);
+
+  // Epilogue.  Lane (j = lane mod 32, h) of MFMA block (ta, tb) holds column
+  // j of rows 8 (r / 4) + 4 h + (r mod 4), r = 0..15.  Each wave stages its
+  // 32 x (32 WJ) result rows for one ta as fp32 in its own LDS region (the
+  // ring is drained first), then writes whole 16-byte chunks of output rows.
+  block_barrier();
+  constexpr int COLS = 32 * WJ;
+  constexpr int PITCHW = COLS + 4;                 // fp32 words per staged row
+  lds_u8* stage = smem + wave * (32 * PITCHW * 4);
+  const bool obf = epi.out_bf16();
+  const int ebytes = obf ? 2 : 4;
+  const int cpr = COLS * ebytes / 16;              // 16-byte output chunks per row
+  const int epc = 16 / ebytes;                     // elements per chunk
 #pragma unroll
   for (int ta = 0; ta < 2; ++ta) {
+    const int64_t ibase = i0 + wi * 64 + ta * 32;
+    float sc[16];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      int64_t i = ibase + 8 * (r >> 2) + 4 * h + (r & 3);
+      if (i > I - 1) i = I - 1;
+      sc[r] = Epi::kRowScale ? epi.scale(i) : epi.scale(0);
+    }
 #pragma unroll
     for (int tb = 0; tb < WJ; ++tb) {
-      const int64_t j = j0 + wj * 32 * WJ + tb * 32 + (lane & 31);
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int64_t i = i0 + wi * 64 + ta * 32 + 8 * (r >> 2) + 4 * h + (r & 3);
-        if (i < I && j < J) {
-          float v;
-          if constexpr (ELEM == EI8) v = (float)acc[ta][tb][r];
-          else v = acc[ta][tb][r];
-          epi.put(i, j, v);
+        float v;
+        if constexpr (ELEM == EI8) v = (float)acc[ta][tb][r];
+        else v = acc[ta][tb][r];
+        v = v * sc[r];
+        const int rr = 8 * (r >> 2) + 4 * h + (r & 3);
+        *(__attribute__((address_space(3))) float*)(stage + (rr * PITCHW + tb * 32 + (lane & 31)) * 4) = v;
+      }
+    }
+    __asm__ volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    const int64_t jbase = j0 + wj * COLS;
+    for (int c = lane; c < 32 * cpr; c += 64) {
+      const int rr = c / cpr, cc = c - rr * cpr;
+      const int64_t i = ibase + rr;
+      const int64_t j = jbase + cc * epc;
+      if (i < I && j < J) {
+        const lds_u8* src = stage + (rr * PITCHW + cc * epc) * 4;
+        uint8_t* dst = epi.row(i, bz) + j * ebytes;
+        if (obf) {
+          const f32x4 a = *(const __attribute__((address_space(3))) f32x4*)src;
+          const f32x4 b = *(const __attribute__((address_space(3))) f32x4*)(src + 16);
+          *reinterpret_cast<uint4*>(dst) = make_uint4(pack_bf16x2(a[0], a[1]), pack_bf16x2(a[2], a[3]),
+                                                      pack_bf16x2(b[0], b[1]), pack_bf16x2(b[2], b[3]));
+        } else {
+          *reinterpret_cast<f32x4*>(dst) = *(const __attribute__((address_space(3))) f32x4*)src;
         }
       }
     }
+    __asm__ volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
   }
 }
 
@@ -322,224 +453,328 @@ __global__ __launch_bounds__(NTH) void gemm_v2_kernel(Opnd A, Opnd B, Epi epi, i
 namespace dqt {
 namespace v2 {
 
+// Up to MAXG independent element ranges handled by one launch.  Segment s
+// owns blocks [b0[s], b0[s+1]); each thread of a block handles one 16-element
+// chunk; chunks past n16[s] do nothing.
+struct SegTab {
+  const void* src[MAXG];
+  void* dst[MAXG];
+  const float* scale[MAXG];   // per-row scales (activation dequantisation)
+  int64_t n16[MAXG];
+  int32_t k16[MAXG];          // 16-element chunks per row (activation dequantisation)
+  int32_t b0[MAXG + 1];
+  int32_t n;
+};
+
+__device__ __forceinline__ int seg_of_block(const SegTab& t) {
+  int s = 0;
+  while (s + 1 < t.n && (int)blockIdx.x >= t.b0[s + 1]) ++s;
+  return s;
+}
+
 // Packed ternary codes -> one operand byte (int8 or e4m3) or one bf16 per
-// weight, same [d_out][d_in] row-major order.  Thread -> 16 weights.
+// weight, same [d_out][d_in] row-major order.
 template <int OUT>   // 0: int8, 1: e4m3, 2: bf16
-__global__ __launch_bounds__(256) void unpack_ternary_kernel(const uint32_t* __restrict__ src,
-                                                             int64_t n16, uint8_t* __restrict__ dst) {
-  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < n16; t += stride) {
-    const uint32_t w = src[t];
-    if constexpr (OUT < 2) {
-      uint32_t o[4];
+__global__ __launch_bounds__(256) void unpack_ternary_kernel(const SegTab tab) {
+  const int s = seg_of_block(tab);
+  const int64_t t = (int64_t)(blockIdx.x - tab.b0[s]) * 256 + threadIdx.x;
+  if (t >= tab.n16[s]) return;
+  const uint32_t w = static_cast<const uint32_t*>(tab.src[s])[t];
+  if constexpr (OUT < 2) {
+    uint32_t o[4];
 #pragma unroll
-      for (int b = 0; b < 4; ++b) {
-        const uint32_t sp = spread_codes((w >> (8 * b)) & 0xFFu);
-        o[b] = OUT == 1 ? codes_to_e4m3x4(sp) : codes_to_i8x4(sp);
-      }
-      reinterpret_cast<uint4*>(dst)[t] = make_uint4(o[0], o[1], o[2], o[3]);
-    } else {
-      uint32_t o[8];
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const uint32_t c = (w >> (4 * j)) & 0xFu;
-        o[j] = code_to_bf16_bits(c & 3u) | (code_to_bf16_bits(c >> 2) << 16);
-      }
-      uint4* d = reinterpret_cast<uint4*>(dst) + 2 * t;
-      d[0] = make_uint4(o[0], o[1], o[2], o[3]);
-      d[1] = make_uint4(o[4], o[5], o[6], o[7]);
+    for (int b = 0; b < 4; ++b) {
+      const uint32_t sp = spread_codes((w >> (8 * b)) & 0xFFu);
+      o[b] = OUT == 1 ? codes_to_e4m3x4(sp) : codes_to_i8x4(sp);
     }
-  }
-}
-
-// int8 codes -> bf16 (|q| <= 128 is exact in bf16).  Thread -> 16 weights.
-__global__ __launch_bounds__(256) void int8_to_bf16_kernel(const uint4* __restrict__ src, int64_t n16,
-                                                           uint4* __restrict__ dst) {
-  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < n16; t += stride) {
-    const uint4 v = src[t];
-    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+    static_cast<uint4*>(tab.dst[s])[t] = make_uint4(o[0], o[1], o[2], o[3]);
+  } else {
     uint32_t o[8];
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
-      const uint32_t two = w[j >> 1] >> (16 * (j & 1));
-      const float lo = (float)(int)(int8_t)(two & 0xFFu);
-      const float hi = (float)(int)(int8_t)((two >> 8) & 0xFFu);
-      o[j] = (__float_as_uint(lo) >> 16) | (__float_as_uint(hi) & 0xFFFF0000u);
+      const uint32_t c = (w >> (4 * j)) & 0xFu;
+      o[j] = code_to_bf16_bits(c & 3u) | (code_to_bf16_bits(c >> 2) << 16);
     }
-    dst[2 * t] = make_uint4(o[0], o[1], o[2], o[3]);
-    dst[2 * t + 1] = make_uint4(o[4], o[5], o[6], o[7]);
+    uint4* d = static_cast<uint4*>(tab.dst[s]) + 2 * t;
+    d[0] = make_uint4(o[0], o[1], o[2], o[3]);
+    d[1] = make_uint4(o[4], o[5], o[6], o[7]);
   }
 }
 
-// X~[m, k] = bf16(fl(value(Xq[m, k]) * xdq[m])).  Thread -> 16 elements of one row.
+// int8 codes -> bf16 (|q| <= 128 is exact in bf16).
+__global__ __launch_bounds__(256) void int8_to_bf16_kernel(const SegTab tab) {
+  const int s = seg_of_block(tab);
+  const int64_t t = (int64_t)(blockIdx.x - tab.b0[s]) * 256 + threadIdx.x;
+  if (t >= tab.n16[s]) return;
+  const uint4 v = static_cast<const uint4*>(tab.src[s])[t];
+  const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+  uint32_t o[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const uint32_t two = w[j >> 1] >> (16 * (j & 1));
+    const float lo = (float)(int)(int8_t)(two & 0xFFu);
+    const float hi = (float)(int)(int8_t)((two >> 8) & 0xFFu);
+    o[j] = (__float_as_uint(lo) >> 16) | (__float_as_uint(hi) & 0xFFFF0000u);
+  }
+  uint4* d = static_cast<uint4*>(tab.dst[s]) + 2 * t;
+  d[0] = make_uint4(o[0], o[1], o[2], o[3]);
+  d[1] = make_uint4(o[4], o[5], o[6], o[7]);
+}
+
+// X~[m, k] = bf16(fl(value(Xq[m, k]) * xdq[m])).
 template <bool E4M3>
-__global__ __launch_bounds__(256) void dequant_act_kernel(const uint4* __restrict__ xq,
-                                                          const float* __restrict__ xdq, int64_t n16,
-                                                          int k16, uint4* __restrict__ xt) {
-  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < n16; t += stride) {
-    const float d = xdq[t / k16];
-    const uint4 v = xq[t];
-    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
-    uint32_t o[8];
+__global__ __launch_bounds__(256) void dequant_act_kernel(const SegTab tab) {
+  const int s = seg_of_block(tab);
+  const int64_t t = (int64_t)(blockIdx.x - tab.b0[s]) * 256 + threadIdx.x;
+  if (t >= tab.n16[s]) return;
+  const float d = tab.scale[s][t / tab.k16[s]];
+  const uint4 v = static_cast<const uint4*>(tab.src[s])[t];
+  const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+  uint32_t o[8];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const uint32_t two = w[j >> 1] >> (16 * (j & 1));
-      float a, b;
-      if constexpr (E4M3) {
-        a = e4m3_to_f32(two & 0xFFu);
-        b = e4m3_to_f32((two >> 8) & 0xFFu);
-      } else {
-        a = (float)(int)(int8_t)(two & 0xFFu);
-        b = (float)(int)(int8_t)((two >> 8) & 0xFFu);
-      }
-      o[j] = pack_bf16x2(a * d, b * d);
+  for (int j = 0; j < 8; ++j) {
+    const uint32_t two = w[j >> 1] >> (16 * (j & 1));
+    float a, b;
+    if constexpr (E4M3) {
+      a = e4m3_to_f32(two & 0xFFu);
+      b = e4m3_to_f32((two >> 8) & 0xFFu);
+    } else {
+      a = (float)(int)(int8_t)(two & 0xFFu);
+      b = (float)(int)(int8_t)((two >> 8) & 0xFFu);
     }
-    xt[2 * t] = make_uint4(o[0], o[1], o[2], o[3]);
-    xt[2 * t + 1] = make_uint4(o[4], o[5], o[6], o[7]);
+    o[j] = pack_bf16x2(a * d, b * d);
   }
+  uint4* dst = static_cast<uint4*>(tab.dst[s]) + 2 * t;
+  dst[0] = make_uint4(o[0], o[1], o[2], o[3]);
+  dst[1] = make_uint4(o[4], o[5], o[6], o[7]);
 }
 
-static dim3 stream_grid(int64_t n) {
-  int64_t b = (n + 255) / 256;
-  if (b > 256 * 16) b = 256 * 16;
-  if (b < 1) b = 1;
-  return dim3((unsigned)b);
+// Fill in tile grids and offsets, then launch one grid over every tile of
+// every problem of the group.
+template <int ELEM, int MA, int MB, class Epi>
+static void launch_group(int wj, Group<Epi>& grp, hipStream_t s) {
+  const int64_t trb = 64 * wj;
+  int32_t tiles = 0;
+  for (int g = 0; g < grp.ng; ++g) {
+    Prob<Epi>& p = grp.p[g];
+    p.nbx = (int32_t)((p.J + trb - 1) / trb);
+    p.nby = (int32_t)((p.I + 127) / 128);
+    p.tile0 = tiles;
+    tiles += p.nbx * p.nby * p.nbz;
+  }
+  if (tiles == 0) return;
+  if (wj == 3)
+    hipLaunchKernelGGL((gemm_v2_kernel<ELEM, MA, MB, 3, Epi>), dim3((unsigned)tiles), dim3(NTH), 0, s, grp);
+  else
+    hipLaunchKernelGGL((gemm_v2_kernel<ELEM, MA, MB, 2, Epi>), dim3((unsigned)tiles), dim3(NTH), 0, s, grp);
 }
 
-// Tile choice: 128 x 128 (WJ = 2) or 128 x 192 (WJ = 3), whichever needs
-// fewer rounds of 256 CUs times tile area -- the matrix-core time when every
-// CU runs its blocks back to back.
-static int pick_wj(int64_t I, int64_t J, int64_t splits) {
+// Tile width for a group: 128 x 128 (WJ = 2) or 128 x 192 (WJ = 3),
+// whichever needs fewer rounds of 256 CUs times tile area.
+static int pick_wj_group(int n, const int64_t* I, const int64_t* J, const int64_t* splits) {
   int best = 2;
   double best_t = 1e300;
   for (int wj = 2; wj <= 3; ++wj) {
     const int64_t trb = 64 * wj;
-    const int64_t blocks = ((I + 127) / 128) * ((J + trb - 1) / trb) * splits;
+    int64_t blocks = 0;
+    for (int g = 0; g < n; ++g) blocks += ((I[g] + 127) / 128) * ((J[g] + trb - 1) / trb) * splits[g];
     const double t = (double)((blocks + 255) / 256) * (double)(128 * trb);
     if (t < best_t * 0.999) { best_t = t; best = wj; }
   }
   return best;
 }
 
-template <int ELEM, int MA, int MB, class Epi>
-static void launch_core(int wj, Opnd A, Opnd B, Epi epi, int64_t I, int64_t J, int64_t R,
-                        int64_t splits, int64_t split_len, hipStream_t s) {
-  const int64_t trb = 64 * wj;
-  const dim3 grid((unsigned)((J + trb - 1) / trb), (unsigned)((I + 127) / 128), (unsigned)splits);
-  if (wj == 3)
-    hipLaunchKernelGGL((gemm_v2_kernel<ELEM, MA, MB, 3, Epi>), grid, dim3(NTH), 0, s, A, B, epi, I,
-                       J, R, split_len);
-  else
-    hipLaunchKernelGGL((gemm_v2_kernel<ELEM, MA, MB, 2, Epi>), grid, dim3(NTH), 0, s, A, B, epi, I,
-                       J, R, split_len);
+static int32_t seal(SegTab& t) {
+  int32_t b = 0;
+  for (int s = 0; s < t.n; ++s) {
+    t.b0[s] = b;
+    b += (int32_t)((t.n16[s] + 255) / 256);
+  }
+  t.b0[t.n] = b;
+  return b;
 }
 
 }  // namespace v2
 
-size_t fwd_workspace_bytes(bool ternary, int64_t d_out, int64_t d_in) {
-  return ternary ? (size_t)((d_out * d_in + 255) / 256 * 256) : 0;
-}
+using namespace v2;
 
-hipError_t launch_fwd_v2(const FwdArgs& a, hipStream_t stream) {
-  using namespace v2;
-  const int64_t I = a.M, J = a.d_out, R = a.d_in;
-  if (I == 0) return hipSuccess;
-  const uint8_t* wrows = static_cast<const uint8_t*>(a.Wq);
-  if (a.w_ternary) {
-    const int64_t n16 = J * R / 16;
-    if (a.act_e4m3)
-      hipLaunchKernelGGL(unpack_ternary_kernel<1>, stream_grid(n16), dim3(256), 0, stream,
-                         static_cast<const uint32_t*>(a.Wq), n16, static_cast<uint8_t*>(a.ws));
-    else
-      hipLaunchKernelGGL(unpack_ternary_kernel<0>, stream_grid(n16), dim3(256), 0, stream,
-                         static_cast<const uint32_t*>(a.Wq), n16, static_cast<uint8_t*>(a.ws));
-    wrows = static_cast<const uint8_t*>(a.ws);
+static size_t align256(size_t n) { return (n + 255) / 256 * 256; }
+
+size_t fwd_batch_workspace(int n, const LinearIO* io, bool ternary, size_t* offs) {
+  size_t total = 0;
+  for (int l = 0; l < n; ++l) {
+    if (offs) offs[l] = total;
+    if (ternary) total += align256((size_t)(io[l].d_out * io[l].d_in));
   }
-  Opnd A{static_cast<const uint8_t*>(a.Xq), R, I};
-  Opnd B{wrows, R, J};
-  EpiFwd epi{a.Y, J, a.y_bf16, a.xdq, a.alpha};
-  const int wj = pick_wj(I, J, 1);
-  if (a.act_e4m3)
-    launch_core<EF8, KC, KC>(wj, A, B, epi, I, J, R, 1, R, stream);
-  else
-    launch_core<EI8, KC, KC>(wj, A, B, epi, I, J, R, 1, R, stream);
+  return total;
+}
+
+hipError_t launch_fwd_batch(const BatchCfg& c, const LinearIO* io, uint8_t* ws, hipStream_t stream) {
+  if (c.M == 0 || c.n == 0) return hipSuccess;
+  size_t offs[kMaxBatch];
+  fwd_batch_workspace(c.n, io, c.w_ternary, offs);
+  if (c.w_ternary) {
+    SegTab tab{};
+    tab.n = c.n;
+    for (int l = 0; l < c.n; ++l) {
+      tab.src[l] = io[l].Wq;
+      tab.dst[l] = ws + offs[l];
+      tab.n16[l] = io[l].d_out * io[l].d_in / 16;
+    }
+    const int32_t blocks = seal(tab);
+    if (c.act_e4m3)
+      hipLaunchKernelGGL(unpack_ternary_kernel<1>, dim3(blocks), dim3(256), 0, stream, tab);
+    else
+      hipLaunchKernelGGL(unpack_ternary_kernel<0>, dim3(blocks), dim3(256), 0, stream, tab);
+  }
+  Group<EpiFwd> grp{};
+  grp.ng = c.n;
+  int64_t I[kMaxBatch], J[kMaxBatch], S[kMaxBatch];
+  for (int l = 0; l < c.n; ++l) {
+    Prob<EpiFwd>& p = grp.p[l];
+    const uint8_t* rows = c.w_ternary ? ws + offs[l] : static_cast<const uint8_t*>(io[l].Wq);
+    p.A = Opnd{static_cast<const uint8_t*>(io[l].Xq), io[l].d_in, c.M};
+    p.B = Opnd{rows, io[l].d_in, io[l].d_out};
+    p.epi = EpiFwd{io[l].Y, io[l].d_out, c.out_bf16, io[l].xdq, io[l].alpha};
+    p.I = c.M;
+    p.J = io[l].d_out;
+    p.R = io[l].d_in;
+    p.split_len = io[l].d_in;
+    p.nbz = 1;
+    I[l] = p.I; J[l] = p.J; S[l] = 1;
+  }
+  const int wj = pick_wj_group(c.n, I, J, S);
+  if (c.act_e4m3) launch_group<EF8, KC, KC>(wj, grp, stream);
+  else launch_group<EI8, KC, KC>(wj, grp, stream);
   return hipGetLastError();
 }
 
-hipError_t launch_dx_v2(const DxArgs& a, void* ws_q, hipStream_t stream) {
-  using namespace v2;
-  // dX[m, k] = alpha sum_n dY[m, n] q[n, k]: I = M, J = d_in, R = d_out
-  const int64_t I = a.M, J = a.d_in, R = a.d_out;
-  if (I == 0) return hipSuccess;
-  const int64_t n16 = R * J / 16;
-  if (a.w_ternary)
-    hipLaunchKernelGGL(unpack_ternary_kernel<2>, stream_grid(n16), dim3(256), 0, stream,
-                       static_cast<const uint32_t*>(a.Wq), n16, static_cast<uint8_t*>(ws_q));
-  else
-    hipLaunchKernelGGL(int8_to_bf16_kernel, stream_grid(n16), dim3(256), 0, stream,
-                       static_cast<const uint4*>(a.Wq), n16, static_cast<uint4*>(ws_q));
-  Opnd A{static_cast<const uint8_t*>(a.dY), R * 2, I};
-  Opnd B{static_cast<const uint8_t*>(ws_q), J * 2, J};
-  EpiScale epi{a.dX, J, a.dx_bf16, a.alpha};
-  launch_core<EBF16, KC, KM>(pick_wj(I, J, 1), A, B, epi, I, J, R, 1, R, stream);
-  return hipGetLastError();
-}
-
-// Split count and tile for dW = dY^T X~ (reduction over M tokens): choose the
-// pair that minimises matrix-core rounds plus the fp32 partial traffic.
-void plan_dw_v2(int64_t d_out, int64_t d_in, int64_t M, int* wj_out, int64_t* splits_out) {
+// Backward plan for a batch in the bf16 environment: tile width, one split
+// count for every dW product of the batch, and the workspace layout
+//   per linear: [bf16 weights d_out x d_in][bf16 X~ M x d_in][fp32 partials]
+// (partials sized for the larger of this plan's and the fp32 kernels' split).
+BwdPlan plan_bwd_batch(int n, const LinearIO* io, int64_t M) {
+  BwdPlan P{};
   double best = 1e300;
-  int bw = 2;
-  int64_t bs = 1;
   for (int wj = 2; wj <= 3; ++wj) {
     const int64_t trb = 64 * wj;
-    const int64_t tiles = ((d_out + 127) / 128) * ((d_in + trb - 1) / trb);
     for (int64_t s = 1; s <= 32; ++s) {
       if (s > 1 && M / s < 256) break;
-      const int64_t blocks = tiles * s;
+      int64_t blocks = 0;
+      double part_bytes = 0;
+      for (int l = 0; l < n; ++l) {
+        blocks += ((io[l].d_out + 127) / 128) * ((io[l].d_in + trb - 1) / trb) * s;
+        if (s > 1) part_bytes += (2.0 * s + 1.0) * (double)(io[l].d_out * io[l].d_in * 4);
+      }
       const double rounds = (double)((blocks + 255) / 256);
-      const double steps = (double)((M + s - 1) / s + 31) / 32.0;
-      // per-block MFMA time: 2 * 128 * trb * 32 flops per step at ~9.8 TFLOP/s per CU
-      const double t_mfma = rounds * steps * (2.0 * 128 * trb * 32) / 9.8e12;
-      const double t_part = s > 1 ? (2.0 * s + 1.0) * (double)(d_out * d_in * 4) / 5.0e12 : 0.0;
-      const double t = t_mfma + t_part;
-      if (t < best * 0.999) { best = t; bw = wj; bs = s; }
+      const double steps = (double)(((M + s - 1) / s + 31) / 32);
+      const double t = rounds * steps * (2.0 * 128 * trb * 32) / 9.8e12 + part_bytes / 5.0e12;
+      if (t < best * 0.999) { best = t; P.wj = wj; P.splits = s; }
     }
   }
-  *wj_out = bw;
-  *splits_out = bs;
+  size_t off = 0;
+  for (int l = 0; l < n; ++l) {
+    const size_t wn = (size_t)(io[l].d_out * io[l].d_in);
+    const int64_t s32 = dw_splits_f32(io[l].d_out, io[l].d_in, M);
+    const int64_t sp = P.splits > s32 ? P.splits : s32;
+    P.q_off[l] = off;
+    off += align256(wn * 2);
+    P.xt_off[l] = off;
+    off += align256((size_t)M * (size_t)io[l].d_in * 2);
+    P.part_off[l] = off;
+    off += sp > 1 ? align256((size_t)sp * wn * 4) : 0;
+  }
+  P.total = off;
+  return P;
 }
 
-hipError_t launch_dw_v2(const DwArgs& a, void* ws_xt, hipStream_t stream) {
-  using namespace v2;
-  // dW[n, k] = sum_m dY[m, n] X~[m, k]: I = d_out, J = d_in, R = M
-  const int64_t I = a.d_out, J = a.d_in, R = a.M;
-  int wj;
-  int64_t splits;
-  plan_dw_v2(I, J, R, &wj, &splits);
-  if (R > 0) {
-    const int64_t n16 = R * J / 16;
-    if (a.act_e4m3)
-      hipLaunchKernelGGL(dequant_act_kernel<true>, stream_grid(n16), dim3(256), 0, stream,
-                         static_cast<const uint4*>(a.Xq), a.xdq, n16, (int)(J / 16),
-                         static_cast<uint4*>(ws_xt));
-    else
-      hipLaunchKernelGGL(dequant_act_kernel<false>, stream_grid(n16), dim3(256), 0, stream,
-                         static_cast<const uint4*>(a.Xq), a.xdq, n16, (int)(J / 16),
-                         static_cast<uint4*>(ws_xt));
+hipError_t launch_dx_batch(const BatchCfg& c, const LinearIO* io, uint8_t* ws, const BwdPlan& P,
+                           hipStream_t stream) {
+  if (c.M == 0 || c.n == 0) return hipSuccess;
+  SegTab tab{};
+  tab.n = c.n;
+  for (int l = 0; l < c.n; ++l) {
+    tab.src[l] = io[l].Wq;
+    tab.dst[l] = ws + P.q_off[l];
+    tab.n16[l] = io[l].d_out * io[l].d_in / 16;
   }
-  int64_t len = splits > 1 ? (R + splits - 1) / splits : (R > 0 ? R : 1);
+  const int32_t blocks = seal(tab);
+  if (c.w_ternary)
+    hipLaunchKernelGGL(unpack_ternary_kernel<2>, dim3(blocks), dim3(256), 0, stream, tab);
+  else
+    hipLaunchKernelGGL(int8_to_bf16_kernel, dim3(blocks), dim3(256), 0, stream, tab);
+  // dX[m, k] = alpha sum_n dY[m, n] q[n, k]: I = M, J = d_in, R = d_out
+  Group<EpiScale> grp{};
+  grp.ng = c.n;
+  int64_t I[kMaxBatch], J[kMaxBatch], S[kMaxBatch];
+  for (int l = 0; l < c.n; ++l) {
+    Prob<EpiScale>& p = grp.p[l];
+    p.A = Opnd{static_cast<const uint8_t*>(io[l].dY), io[l].d_out * 2, c.M};
+    p.B = Opnd{ws + P.q_off[l], io[l].d_in * 2, io[l].d_in};
+    p.epi = EpiScale{io[l].dX, io[l].d_in, c.out_bf16, io[l].alpha};
+    p.I = c.M;
+    p.J = io[l].d_in;
+    p.R = io[l].d_out;
+    p.split_len = io[l].d_out;
+    p.nbz = 1;
+    I[l] = p.I; J[l] = p.J; S[l] = 1;
+  }
+  launch_group<EBF16, KC, KM>(pick_wj_group(c.n, I, J, S), grp, stream);
+  return hipGetLastError();
+}
+
+hipError_t launch_dw_batch(const BatchCfg& c, const LinearIO* io, uint8_t* ws, const BwdPlan& P,
+                           hipStream_t stream) {
+  if (c.n == 0) return hipSuccess;
+  // X~ once per distinct quantised input
+  int first[kMaxBatch];
+  SegTab tab{};
+  for (int l = 0; l < c.n; ++l) {
+    first[l] = l;
+    for (int m = 0; m < l; ++m)
+      if (io[m].Xq == io[l].Xq && io[m].d_in == io[l].d_in) { first[l] = first[m]; break; }
+    if (first[l] == l && c.M > 0) {
+      const int s = tab.n++;
+      tab.src[s] = io[l].Xq;
+      tab.dst[s] = ws + P.xt_off[l];
+      tab.scale[s] = io[l].xdq;
+      tab.n16[s] = c.M * io[l].d_in / 16;
+      tab.k16[s] = (int32_t)(io[l].d_in / 16);
+    }
+  }
+  if (tab.n > 0) {
+    const int32_t blocks = seal(tab);
+    if (c.act_e4m3)
+      hipLaunchKernelGGL(dequant_act_kernel<true>, dim3(blocks), dim3(256), 0, stream, tab);
+    else
+      hipLaunchKernelGGL(dequant_act_kernel<false>, dim3(blocks), dim3(256), 0, stream, tab);
+  }
+  // dW[n, k] = sum_m dY[m, n] X~[m, k]: I = d_out, J = d_in, R = M
+  const int64_t splits = P.splits;
+  int64_t len = splits > 1 ? (c.M + splits - 1) / splits : (c.M > 0 ? c.M : 1);
   len = (len + 31) / 32 * 32;
-  float* target = splits > 1 ? a.ws : a.dW;
-  Opnd A{static_cast<const uint8_t*>(a.dY), I * 2, I};
-  Opnd B{static_cast<const uint8_t*>(ws_xt), J * 2, J};
-  EpiPartial epi{target, J, I * J};
-  launch_core<EBF16, KM, KM>(wj, A, B, epi, I, J, R, splits, len, stream);
+  Group<EpiPartial> grp{};
+  grp.ng = c.n;
+  for (int l = 0; l < c.n; ++l) {
+    Prob<EpiPartial>& p = grp.p[l];
+    const int64_t I = io[l].d_out, J = io[l].d_in;
+    p.A = Opnd{static_cast<const uint8_t*>(io[l].dY), I * 2, I};
+    p.B = Opnd{ws + P.xt_off[first[l]], J * 2, J};
+    float* target = splits > 1 ? reinterpret_cast<float*>(ws + P.part_off[l]) : io[l].dW;
+    p.epi = EpiPartial{target, J, I * J};
+    p.I = I;
+    p.J = J;
+    p.R = c.M;
+    p.split_len = len;
+    p.nbz = (int32_t)splits;
+  }
+  launch_group<EBF16, KM, KM>(P.wj, grp, stream);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || splits == 1) return e;
-  return launch_split_reduce(a.ws, (int)splits, I * J, a.dW, stream);
+  for (int l = 0; l < c.n && e == hipSuccess; ++l)
+    e = launch_split_reduce(reinterpret_cast<const float*>(ws + P.part_off[l]), (int)splits,
+                            io[l].d_out * io[l].d_in, io[l].dW, stream);
+  return e;
 }
 
 }  // namespace dqt

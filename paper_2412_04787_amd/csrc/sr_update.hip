@@ -75,27 +75,50 @@ __device__ __forceinline__ int sr_tie(int q, float g, uint32_t s16, const SRArgs
   return min(max(v, a.qmin), a.qmax);
 }
 
+constexpr int kMaxSR = kMaxBatch;
+// Up to kMaxSR tensors in one launch; tensor s owns blocks [b0[s], b0[s+1]).
+struct SRTab {
+  uint8_t* wq[kMaxSR];
+  const float* grad[kMaxSR];
+  int64_t nchunks[kMaxSR];
+  float c[kMaxSR], L[kMaxSR];
+  int qmin[kMaxSR], qmax[kMaxSR];
+  uint32_t tid[kMaxSR];
+  int32_t b0[kMaxSR + 1];
+  int32_t n;
+  uint32_t k0, k1, step;
+};
+
 template <bool TERNARY>
-__global__ __launch_bounds__(256) void sr_update_kernel(uint8_t* __restrict__ wq,
-                                                        const float* __restrict__ grad,
-                                                        int64_t nchunks, SRArgs a,
+__global__ __launch_bounds__(256) void sr_update_kernel(const SRTab tab,
                                                         unsigned long long* __restrict__ counters) {
+  int sidx = 0;
+  while (sidx + 1 < tab.n && (int)blockIdx.x >= tab.b0[sidx + 1]) ++sidx;
+  SRArgs a;
+  a.c = tab.c[sidx];
+  a.L = tab.L[sidx];
+  a.qmin = tab.qmin[sidx];
+  a.qmax = tab.qmax[sidx];
+  a.k0 = tab.k0;
+  a.k1 = tab.k1;
+  a.step = tab.step;
+  a.tid = tab.tid[sidx];
+  uint8_t* __restrict__ wq = tab.wq[sidx];
+  const float* __restrict__ grad = tab.grad[sidx];
   unsigned long long changed = 0, nonfin = 0;
-  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < nchunks; t += stride) {
+  const int64_t t = (int64_t)(blockIdx.x - tab.b0[sidx]) * blockDim.x + threadIdx.x;
+  if (t < tab.nchunks[sidx]) {
     const f32x4* gp = reinterpret_cast<const f32x4*>(grad + t * 16);
     f32x4 gv[4];
 #pragma unroll
     for (int u = 0; u < 4; ++u) gv[u] = __builtin_nontemporal_load(gp + u);
     int q[16];
-    uint32_t packed = 0;
-    uint4 packed8 = make_uint4(0, 0, 0, 0);
     if constexpr (TERNARY) {
-      packed = reinterpret_cast<const uint32_t*>(wq)[t];
+      const uint32_t packed = reinterpret_cast<const uint32_t*>(wq)[t];
 #pragma unroll
       for (int j = 0; j < 16; ++j) q[j] = (int)((packed >> (2 * j)) & 3u) - 1;
     } else {
-      packed8 = reinterpret_cast<const uint4*>(wq)[t];
+      const uint4 packed8 = reinterpret_cast<const uint4*>(wq)[t];
       const uint32_t w4[4] = {packed8.x, packed8.y, packed8.z, packed8.w};
 #pragma unroll
       for (int j = 0; j < 16; ++j) q[j] = (int)(int8_t)(w4[j >> 2] >> (8 * (j & 3)));
@@ -114,7 +137,7 @@ __global__ __launch_bounds__(256) void sr_update_kernel(uint8_t* __restrict__ wq
       ties |= (tie ? 1u : 0u) << j;
       nonfin += nf ? 1 : 0;
     }
-    if (ties) {  // probability ~2^-16 per element: recompute with stream 1
+    if (ties) {  // probability ~2^-16 per element: decide with stream 1
       const uint4 s0 = philox_block(blk, 1u, a.step, a.tid, a.k0, a.k1);
       const uint4 s1 = philox_block(blk + 1, 1u, a.step, a.tid, a.k0, a.k1);
 #pragma unroll
@@ -162,30 +185,32 @@ __global__ __launch_bounds__(256) void debug_rng_kernel(uint32_t* __restrict__ o
   }
 }
 
-hipError_t launch_sr_update(bool ternary, uint8_t* wq, const float* grad, int64_t nweights,
-                            float c, int qmin, int qmax, uint64_t seed, uint32_t step,
-                            uint32_t tensor_id, unsigned long long* counters, hipStream_t stream) {
-  const int64_t nchunks = nweights / 16;
-  if (nchunks == 0) return hipSuccess;
-  SRArgs a;
-  a.c = c;
-  a.L = (float)(qmax - qmin + 1);
-  a.qmin = qmin;
-  a.qmax = qmax;
-  a.k0 = (uint32_t)seed;
-  a.k1 = (uint32_t)(seed >> 32);
-  a.step = step;
-  a.tid = tensor_id;
-  const int threads = 256;
-  int64_t blocks = (nchunks + threads - 1) / threads;
-  const int64_t cap = 256 * 32;  // 32 blocks per CU: enough loads in flight
-  if (blocks > cap) blocks = cap;
+hipError_t launch_sr_update(bool ternary, int n, const SRTensor* t, uint64_t seed, uint32_t step,
+                            unsigned long long* counters, hipStream_t stream) {
+  SRTab tab{};
+  tab.n = n;
+  tab.k0 = (uint32_t)seed;
+  tab.k1 = (uint32_t)(seed >> 32);
+  tab.step = step;
+  int32_t blocks = 0;
+  for (int s = 0; s < n; ++s) {
+    tab.wq[s] = t[s].wq;
+    tab.grad[s] = t[s].grad;
+    tab.nchunks[s] = t[s].nweights / 16;
+    tab.c[s] = t[s].c;
+    tab.L[s] = (float)(t[s].qmax - t[s].qmin + 1);
+    tab.qmin[s] = t[s].qmin;
+    tab.qmax[s] = t[s].qmax;
+    tab.tid[s] = t[s].tensor_id;
+    tab.b0[s] = blocks;
+    blocks += (int32_t)((tab.nchunks[s] + 255) / 256);
+  }
+  tab.b0[n] = blocks;
+  if (blocks == 0) return hipSuccess;
   if (ternary)
-    hipLaunchKernelGGL(sr_update_kernel<true>, dim3((unsigned)blocks), dim3(threads), 0, stream,
-                       wq, grad, nchunks, a, counters);
+    hipLaunchKernelGGL(sr_update_kernel<true>, dim3((unsigned)blocks), dim3(256), 0, stream, tab, counters);
   else
-    hipLaunchKernelGGL(sr_update_kernel<false>, dim3((unsigned)blocks), dim3(threads), 0, stream,
-                       wq, grad, nchunks, a, counters);
+    hipLaunchKernelGGL(sr_update_kernel<false>, dim3((unsigned)blocks), dim3(256), 0, stream, tab, counters);
   return hipGetLastError();
 }
 

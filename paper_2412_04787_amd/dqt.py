@@ -22,7 +22,8 @@ DQT_F32, DQT_BF16, DQT_I8, DQT_FP8E4M3, DQT_TERNARY2 = 0, 1, 2, 3, 4
 
 EXPORTS = (
     "dqt_act_quant", "dqt_linear_fwd_workspace", "dqt_linear_fwd", "dqt_linear_bwd_workspace",
-    "dqt_linear_bwd",
+    "dqt_linear_bwd", "dqt_linear_fwd_batch_workspace", "dqt_linear_fwd_batch",
+    "dqt_linear_bwd_batch_workspace", "dqt_linear_bwd_batch", "dqt_sr_update_batch",
     "dqt_sr_update", "dqt_debug_rng", "dqt_absmean_init", "dqt_pack_ternary",
     "dqt_unpack_ternary", "dqt_status_string", "dqt_version",
 )
@@ -33,6 +34,17 @@ class DqtWeight(ctypes.Structure):
         ("d_out", ctypes.c_int32), ("d_in", ctypes.c_int32), ("wfmt", ctypes.c_int32),
         ("qmin", ctypes.c_int32), ("qmax", ctypes.c_int32), ("alpha", ctypes.c_float),
         ("tensor_id", ctypes.c_uint32), ("reserved", ctypes.c_uint32),
+    ]
+
+
+MAX_BATCH = 8
+
+
+class DqtLinearIO(ctypes.Structure):
+    _fields_ = [
+        ("w", ctypes.POINTER(DqtWeight)), ("Wq", ctypes.c_void_p), ("Xq", ctypes.c_void_p),
+        ("xdq", ctypes.c_void_p), ("Y", ctypes.c_void_p), ("dY", ctypes.c_void_p),
+        ("dX", ctypes.c_void_p), ("dW", ctypes.c_void_p),
     ]
 
 
@@ -62,6 +74,12 @@ _SIGS = {
     "dqt_linear_bwd": (_i32, [_wp, _vp, _vp, _i32, _vp, _vp, _i32, _i64, _i32, _vp, _i32, _vp,
                               _vp, ctypes.c_size_t, _vp]),
     "dqt_sr_update": (_i32, [_wp, _vp, _vp, _f32, _u64, _u32, _vp, _vp]),
+    "dqt_linear_fwd_batch_workspace": (ctypes.c_size_t, [_i32, _vp]),
+    "dqt_linear_fwd_batch": (_i32, [_i32, _vp, _i64, _i32, _i32, _vp, ctypes.c_size_t, _vp]),
+    "dqt_linear_bwd_batch_workspace": (ctypes.c_size_t, [_i32, _vp, _i64]),
+    "dqt_linear_bwd_batch": (_i32, [_i32, _vp, _i64, _i32, _i32, _i32, _i32, _vp,
+                                    ctypes.c_size_t, _vp]),
+    "dqt_sr_update_batch": (_i32, [_i32, _vp, _f32, _u64, _u32, _vp, _vp]),
     "dqt_debug_rng": (_i32, [_u64, _u32, _u32, _u64, _i64, _vp, _vp]),
     "dqt_absmean_init": (_i32, [_vp, _i64, _i32, _i32, _vp, _vp]),
     "dqt_pack_ternary": (_i32, [_vp, _i64, _i64, _vp]),
@@ -178,6 +196,52 @@ def dqt_sr_update(w: DqtWeight, Wq, dW, lr: float, seed: int, step: int, counter
 def dqt_debug_rng(seed: int, step: int, tensor_id: int, i0: int, out, stream=None):
     _check("dqt_debug_rng", load().dqt_debug_rng(seed, step, tensor_id, i0, out.numel(),
                                                  _ptr(out), _stream(stream)))
+
+
+# ----------------------------------------------------------------- batches
+
+def linear_io(entries):
+    """entries: list of dicts with keys w (DqtWeight), Wq, Xq, xdq, Y, dY, dX, dW
+    (tensors or None).  Returns a ctypes array of dqt_linear_io; the weight
+    descriptors are kept alive on the array."""
+    arr = (DqtLinearIO * len(entries))()
+    keep = []
+    for k, e in enumerate(entries):
+        w = e["w"]
+        keep.append(w)
+        arr[k].w = ctypes.pointer(w)
+        for f in ("Wq", "Xq", "xdq", "Y", "dY", "dX", "dW"):
+            t = e.get(f)
+            setattr(arr[k], f, None if t is None else t.data_ptr())
+    arr._keep = keep
+    return arr
+
+
+def dqt_linear_fwd_batch_workspace(io) -> int:
+    return int(load().dqt_linear_fwd_batch_workspace(len(io), io))
+
+
+def dqt_linear_fwd_batch(io, M: int, act_q: int, y_t: int, ws=None, stream=None):
+    ws_bytes = 0 if ws is None else ws.numel() * ws.element_size()
+    _check("dqt_linear_fwd_batch", load().dqt_linear_fwd_batch(len(io), io, M, act_q, y_t, _ptr(ws),
+                                                               ws_bytes, _stream(stream)))
+
+
+def dqt_linear_bwd_batch_workspace(io, M: int) -> int:
+    return int(load().dqt_linear_bwd_batch_workspace(len(io), io, M))
+
+
+def dqt_linear_bwd_batch(io, M: int, act_q: int, dy_t: int, xt_t: int, dx_t: int, ws=None,
+                         stream=None):
+    ws_bytes = 0 if ws is None else ws.numel() * ws.element_size()
+    _check("dqt_linear_bwd_batch", load().dqt_linear_bwd_batch(len(io), io, M, act_q, dy_t, xt_t,
+                                                               dx_t, _ptr(ws), ws_bytes,
+                                                               _stream(stream)))
+
+
+def dqt_sr_update_batch(io, lr: float, seed: int, step: int, counters=None, stream=None):
+    _check("dqt_sr_update_batch", load().dqt_sr_update_batch(len(io), io, lr, seed, step,
+                                                             _ptr(counters), _stream(stream)))
 
 
 # ----------------------------------------------------------------- host helpers
