@@ -51,7 +51,7 @@ struct BatchCfg {
 };
 struct BwdPlan {
   int64_t splits;
-  int wj;
+  int wi, wj;       // dW block tile (64 wi) x (64 wj)
   size_t q_off[kMaxBatch], xt_off[kMaxBatch], part_off[kMaxBatch];
   size_t total;
 };

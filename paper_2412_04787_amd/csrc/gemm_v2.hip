@@ -11,8 +11,8 @@
 // one row straight from a row-major [R][rows] tile -- the dW = dY^T X~ and
 // dX = dY Q products need no register transposes.
 //
-// Block: 256 threads = 2 x 2 waves; a wave owns 64 x (32 WJ) of C as 2 x WJ
-// MFMA 32x32 blocks; the block tile is 128 x (64 WJ).  Step: 64 bytes of
+// Block: 256 threads = 2 x 2 waves; a wave owns (32 WI) x (32 WJ) of C as
+// WI x WJ MFMA 32x32 blocks; the block tile is (64 WI) x (64 WJ).  Step: 64 bytes of
 // reduction per tile row (64 int8/e4m3 or 32 bf16 elements).
 //
 // LDS layouts (per stage, per operand), chosen so that every fragment read is
@@ -23,6 +23,9 @@
 //     32-byte segment s of row k sits at position s ^ (k & 3).
 // The DMA writes 64 consecutive 16-byte chunks per wave instruction, so each
 // lane loads the global chunk that belongs at its LDS position.
+#include <algorithm>
+#include <type_traits>
+
 #include "gemm_common.h"
 
 namespace dqt {
@@ -38,9 +41,9 @@ constexpr int STAGES = 4;
 enum Elem { EI8 = 0, EF8 = 1, EBF16 = 2 };
 enum Mode { KC = 0, KM = 1 };
 
-template <int ELEM, int MA, int MB, int WJ>
+template <int ELEM, int MA, int MB, int WI, int WJ>
 struct Cfg {
-  static constexpr int TRA = 128;              // tile rows of A (I)
+  static constexpr int TRA = 64 * WI;          // tile rows of A (I)
   static constexpr int TRB = 64 * WJ;          // tile rows of B (J)
   static constexpr int EB = ELEM == EBF16 ? 2 : 1;
   static constexpr int BK = 64 / EB;           // reduction elements per step
@@ -50,6 +53,7 @@ struct Cfg {
   static constexpr int NLB = TRB / 64;
   static constexpr int STAGE = A_BYTES + B_BYTES;
   static constexpr int LDS = STAGE * STAGES;
+  static_assert(LDS <= 160 * 1024, "LDS budget");
   static_assert(ELEM == EBF16 || (MA == KC && MB == KC), "K-major operands are bf16 only");
 };
 
@@ -148,10 +152,11 @@ struct Group {
   int32_t ng;
 };
 
-template <int ELEM, int MA, int MB, int WJ, class Epi>
+template <int ELEM, int MA, int MB, int WI, int WJ, class Epi>
 __global__ __launch_bounds__(NTH) void gemm_v2_kernel(const Group<Epi> grp) {
-  using C = Cfg<ELEM, MA, MB, WJ>;
+  using C = Cfg<ELEM, MA, MB, WI, WJ>;
   __shared__ __attribute__((aligned(1024))) uint8_t smem_generic[C::LDS];
+  __shared__ float row_scale[Epi::kRowScale ? C::TRA : 1];
   lds_u8* smem = (lds_u8*)smem_generic;
 
   const int tid = threadIdx.x;
@@ -197,6 +202,18 @@ __global__ __launch_bounds__(NTH) void gemm_v2_kernel(const Group<Epi> grp) {
   pb.init(B, j0, r_begin);
   // wave-uniform LDS offset of this wave's DMA chunks (kept in an SGPR)
   const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+  // per-row output scales of this tile: loaded before the first DMA (so the
+  // in-order load counter retires them with stage 0) and staged in LDS
+  // before the first barrier
+  static_assert(C::TRA <= NTH, "one row scale per thread");
+  float my_scale = 0.0f;
+  if constexpr (Epi::kRowScale) {
+    if (tid < C::TRA) {
+      int64_t i = i0 + tid;
+      if (i > I - 1) i = I - 1;
+      my_scale = epi.scale(i);
+    }
+  }
 
   // Issue the DMA of stage s (its slot is s mod STAGES).  The per-thread
   // source pointers advance by one step per call, so stages are issued in
@@ -236,9 +253,9 @@ __global__ __launch_bounds__(NTH) void gemm_v2_kernel(const Group<Epi> grp) {
   };
 
   using AccV = typename AccT<ELEM == EI8 ? Mfma::I8 : Mfma::BF16>::type;
-  AccV acc[2][WJ];
+  AccV acc[WI][WJ];
 #pragma unroll
-  for (int a = 0; a < 2; ++a)
+  for (int a = 0; a < WI; ++a)
 #pragma unroll
     for (int b = 0; b < WJ; ++b)
 #pragma unroll
@@ -255,22 +272,22 @@ __global__ __launch_bounds__(NTH) void gemm_v2_kernel(const Group<Epi> grp) {
   // waits and barriers order the DMA before these reads, and frag_wait()
   // orders the reads before use).
   struct Frags {
-    i32x4 fa[2][2], fb[WJ][2];
-    u32x2 ka[2][2][2], kb[WJ][2][2];
+    i32x4 fa[WI][2], fb[WJ][2];
+    u32x2 ka[WI][2][2], kb[WJ][2][2];
   };
   auto read_frags = [&](int s, Frags& F) {
     const lds_u8* la = smem + (s % STAGES) * C::STAGE;
     const lds_u8* lb = la + C::A_BYTES;
 #pragma unroll
-    for (int t = 0; t < 2; ++t)
+    for (int t = 0; t < WI; ++t)
 #pragma unroll
       for (int kk = 0; kk < 2; ++kk) {
         if constexpr (MA == KC) {
-          const int row = wi * 64 + t * 32 + frow;
+          const int row = wi * 32 * WI + t * 32 + frow;
           const int c = (2 * kk + h) ^ ((row >> 2) & 3);
           F.fa[t][kk] = *(const __attribute__((address_space(3))) i32x4*)(la + row * 64 + 16 * c);
         } else {
-          const int col = wi * 64 + t * 32 + 16 * ch + 4 * u4;
+          const int col = wi * 32 * WI + t * 32 + 16 * ch + 4 * u4;
           const int seg = ((col & 63) >> 4) ^ t4;
           const uint32_t a0 = (uint32_t)(uintptr_t)(la + (col >> 6) * 4096 +
                                                     (16 * kk + 8 * h + t4) * 128 + 32 * seg + 8 * u4);
@@ -301,7 +318,7 @@ __global__ __launch_bounds__(NTH) void gemm_v2_kernel(const Group<Epi> grp) {
   auto frag_wait = [&](Frags& F) {
     if constexpr (MA == KM) {
 #pragma unroll
-      for (int t = 0; t < 2; ++t)
+      for (int t = 0; t < WI; ++t)
         tr_wait4(F.ka[t][0][0], F.ka[t][0][1], F.ka[t][1][0], F.ka[t][1][1]);
     }
     if constexpr (MB == KM) {
@@ -312,9 +329,9 @@ __global__ __launch_bounds__(NTH) void gemm_v2_kernel(const Group<Epi> grp) {
     if constexpr (MA == KC && MB == KC) __builtin_amdgcn_s_waitcnt((15) | (3 << 14) | (7 << 4) | (0 << 8));
   };
   auto mfma_step = [&](Frags& F) {
-    i32x4 fa[2][2], fb[WJ][2];
+    i32x4 fa[WI][2], fb[WJ][2];
 #pragma unroll
-    for (int t = 0; t < 2; ++t)
+    for (int t = 0; t < WI; ++t)
 #pragma unroll
       for (int kk = 0; kk < 2; ++kk) fa[t][kk] = MA == KC ? F.fa[t][kk] : join(F.ka[t][kk][0], F.ka[t][kk][1]);
 #pragma unroll
@@ -322,7 +339,7 @@ __global__ __launch_bounds__(NTH) void gemm_v2_kernel(const Group<Epi> grp) {
 #pragma unroll
       for (int kk = 0; kk < 2; ++kk) fb[t][kk] = MB == KC ? F.fb[t][kk] : join(F.kb[t][kk][0], F.kb[t][kk][1]);
 #pragma unroll
-    for (int ta = 0; ta < 2; ++ta) {
+    for (int ta = 0; ta < WI; ++ta) {
 #pragma unroll
       for (int tb = 0; tb < WJ; ++tb) {
         if constexpr (ELEM == EI8) {
@@ -366,6 +383,11 @@ __global__ __launch_bounds__(NTH) void gemm_v2_kernel(const Group<Epi> grp) {
   if (nsteps > 0) {
     wait_stages(npre - 1);
     if (tail && nsteps == 1) zero_tail(0);
+  }
+  if constexpr (Epi::kRowScale) {
+    if (tid < C::TRA) row_scale[tid] = my_scale;
+  }
+  if (nsteps > 0) {
     block_barrier();
     read_frags(0, F0);
     frag_wait(F0);
@@ -398,19 +420,14 @@ __global__ __launch_bounds__(NTH) void gemm_v2_kernel(const Group<Epi> grp) {
   constexpr int PITCHW = COLS + 4;                 // fp32 words per staged row
   lds_u8* stage = smem + wave * (32 * PITCHW * 4);
   const bool obf = epi.out_bf16();
-  const int ebytes = obf ? 2 : 4;
-  const int cpr = COLS * ebytes / 16;              // 16-byte output chunks per row
-  const int epc = 16 / ebytes;                     // elements per chunk
 #pragma unroll
-  for (int ta = 0; ta < 2; ++ta) {
-    const int64_t ibase = i0 + wi * 64 + ta * 32;
+  for (int ta = 0; ta < WI; ++ta) {
+    const int64_t ibase = i0 + wi * 32 * WI + ta * 32;
     float sc[16];
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      int64_t i = ibase + 8 * (r >> 2) + 4 * h + (r & 3);
-      if (i > I - 1) i = I - 1;
-      sc[r] = Epi::kRowScale ? epi.scale(i) : epi.scale(0);
-    }
+    for (int r = 0; r < 16; ++r)
+      sc[r] = Epi::kRowScale ? row_scale[wi * 32 * WI + ta * 32 + 8 * (r >> 2) + 4 * h + (r & 3)]
+                             : epi.scale(0);
 #pragma unroll
     for (int tb = 0; tb < WJ; ++tb) {
 #pragma unroll
@@ -425,23 +442,33 @@ __global__ __launch_bounds__(NTH) void gemm_v2_kernel(const Group<Epi> grp) {
     }
     __asm__ volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
     const int64_t jbase = j0 + wj * COLS;
-    for (int c = lane; c < 32 * cpr; c += 64) {
-      const int rr = c / cpr, cc = c - rr * cpr;
-      const int64_t i = ibase + rr;
-      const int64_t j = jbase + cc * epc;
-      if (i < I && j < J) {
-        const lds_u8* src = stage + (rr * PITCHW + cc * epc) * 4;
-        uint8_t* dst = epi.row(i, bz) + j * ebytes;
-        if (obf) {
-          const f32x4 a = *(const __attribute__((address_space(3))) f32x4*)src;
-          const f32x4 b = *(const __attribute__((address_space(3))) f32x4*)(src + 16);
-          *reinterpret_cast<uint4*>(dst) = make_uint4(pack_bf16x2(a[0], a[1]), pack_bf16x2(a[2], a[3]),
-                                                      pack_bf16x2(b[0], b[1]), pack_bf16x2(b[2], b[3]));
-        } else {
-          *reinterpret_cast<f32x4*>(dst) = *(const __attribute__((address_space(3))) f32x4*)src;
+    // read back whole 16-byte output chunks of rows (8 bf16 or 4 fp32)
+    auto store_rows = [&](auto ebytes_tag) {
+      constexpr int EBY = decltype(ebytes_tag)::value;
+      constexpr int EPC = 16 / EBY;              // elements per chunk
+      constexpr int CPR = COLS / EPC;            // chunks per row
+#pragma unroll
+      for (int c0 = 0; c0 < 32 * CPR; c0 += 64) {
+        const int c = c0 + lane;
+        const int rr = c / CPR, cc = c % CPR;
+        const int64_t i = ibase + rr;
+        const int64_t j = jbase + cc * EPC;
+        if (i < I && j < J) {
+          const lds_u8* src = stage + (rr * PITCHW + cc * EPC) * 4;
+          uint8_t* dst = epi.row(i, bz) + j * EBY;
+          if constexpr (EBY == 2) {
+            const f32x4 a = *(const __attribute__((address_space(3))) f32x4*)src;
+            const f32x4 b = *(const __attribute__((address_space(3))) f32x4*)(src + 16);
+            *reinterpret_cast<uint4*>(dst) = make_uint4(pack_bf16x2(a[0], a[1]), pack_bf16x2(a[2], a[3]),
+                                                        pack_bf16x2(b[0], b[1]), pack_bf16x2(b[2], b[3]));
+          } else {
+            *reinterpret_cast<f32x4*>(dst) = *(const __attribute__((address_space(3))) f32x4*)src;
+          }
         }
       }
-    }
+    };
+    if (obf) store_rows(std::integral_constant<int, 2>{});
+    else store_rows(std::integral_constant<int, 4>{});
     __asm__ volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
   }
 }
@@ -549,37 +576,55 @@ __global__ __launch_bounds__(256) void dequant_act_kernel(const SegTab tab) {
   dst[1] = make_uint4(o[4], o[5], o[6], o[7]);
 }
 
+// Block tile shapes: (WI, WJ) -> (64 WI) x (64 WJ).
+struct Tile {
+  int wi, wj;
+};
+// Relative cost per output element of each tile shape in the operand-delivery
+// bound regime the kernel runs in (bytes per flop shrink as the tile grows).
+static double tile_cost(Tile t) {
+  return 1.0 / (64.0 * t.wi) + 1.0 / (64.0 * t.wj);
+}
+
 // Fill in tile grids and offsets, then launch one grid over every tile of
 // every problem of the group.
-template <int ELEM, int MA, int MB, class Epi>
-static void launch_group(int wj, Group<Epi>& grp, hipStream_t s) {
-  const int64_t trb = 64 * wj;
+template <int ELEM, int MA, int MB, int WI, int WJ, class Epi>
+static void launch_group_t(Group<Epi>& grp, hipStream_t s) {
+  const int64_t tra = 64 * WI, trb = 64 * WJ;
   int32_t tiles = 0;
   for (int g = 0; g < grp.ng; ++g) {
     Prob<Epi>& p = grp.p[g];
     p.nbx = (int32_t)((p.J + trb - 1) / trb);
-    p.nby = (int32_t)((p.I + 127) / 128);
+    p.nby = (int32_t)((p.I + tra - 1) / tra);
     p.tile0 = tiles;
     tiles += p.nbx * p.nby * p.nbz;
   }
   if (tiles == 0) return;
-  if (wj == 3)
-    hipLaunchKernelGGL((gemm_v2_kernel<ELEM, MA, MB, 3, Epi>), dim3((unsigned)tiles), dim3(NTH), 0, s, grp);
-  else
-    hipLaunchKernelGGL((gemm_v2_kernel<ELEM, MA, MB, 2, Epi>), dim3((unsigned)tiles), dim3(NTH), 0, s, grp);
+  hipLaunchKernelGGL((gemm_v2_kernel<ELEM, MA, MB, WI, WJ, Epi>), dim3((unsigned)tiles), dim3(NTH), 0,
+                     s, grp);
+}
+template <int ELEM, int MA, int MB, class Epi>
+static void launch_group(Tile t, Group<Epi>& grp, hipStream_t s) {
+  if (t.wi == 4 && t.wj == 4) launch_group_t<ELEM, MA, MB, 4, 4, Epi>(grp, s);
+  else if (t.wi == 4 && t.wj == 2) launch_group_t<ELEM, MA, MB, 4, 2, Epi>(grp, s);
+  else if (t.wi == 2 && t.wj == 4) launch_group_t<ELEM, MA, MB, 2, 4, Epi>(grp, s);
+  else launch_group_t<ELEM, MA, MB, 2, 2, Epi>(grp, s);
 }
 
-// Tile width for a group: 128 x 128 (WJ = 2) or 128 x 192 (WJ = 3),
-// whichever needs fewer rounds of 256 CUs times tile area.
-static int pick_wj_group(int n, const int64_t* I, const int64_t* J, const int64_t* splits) {
-  int best = 2;
+// Tile shape for a group: the one with the least (rounds of 256 CUs) x
+// (tile area) x (cost per element); blocks of the larger tiles run one per CU.
+static Tile pick_tile(int n, const int64_t* I, const int64_t* J, const int64_t* splits) {
+  static const Tile cands[] = {{2, 2}, {4, 2}, {2, 4}, {4, 4}};
+  Tile best = cands[0];
   double best_t = 1e300;
-  for (int wj = 2; wj <= 3; ++wj) {
-    const int64_t trb = 64 * wj;
+  for (const Tile& t : cands) {
+    const int64_t tra = 64 * t.wi, trb = 64 * t.wj;
     int64_t blocks = 0;
-    for (int g = 0; g < n; ++g) blocks += ((I[g] + 127) / 128) * ((J[g] + trb - 1) / trb) * splits[g];
-    const double t = (double)((blocks + 255) / 256) * (double)(128 * trb);
-    if (t < best_t * 0.999) { best_t = t; best = wj; }
+    for (int g = 0; g < n; ++g) blocks += ((I[g] + tra - 1) / tra) * ((J[g] + trb - 1) / trb) * splits[g];
+    const int per_cu = (t.wi * t.wj <= 4) ? 2 : 1;       // co-resident blocks per CU (LDS)
+    const double rounds = (double)((blocks + 256 * per_cu - 1) / (256 * per_cu));
+    const double tm = rounds * (double)(tra * trb) * per_cu * tile_cost(t);
+    if (tm < best_t * 0.999) { best_t = tm; best = t; }
   }
   return best;
 }
@@ -643,9 +688,9 @@ hipError_t launch_fwd_batch(const BatchCfg& c, const LinearIO* io, uint8_t* ws, 
     p.nbz = 1;
     I[l] = p.I; J[l] = p.J; S[l] = 1;
   }
-  const int wj = pick_wj_group(c.n, I, J, S);
-  if (c.act_e4m3) launch_group<EF8, KC, KC>(wj, grp, stream);
-  else launch_group<EI8, KC, KC>(wj, grp, stream);
+  const Tile tile = pick_tile(c.n, I, J, S);
+  if (c.act_e4m3) launch_group<EF8, KC, KC>(tile, grp, stream);
+  else launch_group<EI8, KC, KC>(tile, grp, stream);
   return hipGetLastError();
 }
 
@@ -656,20 +701,26 @@ hipError_t launch_fwd_batch(const BatchCfg& c, const LinearIO* io, uint8_t* ws, 
 BwdPlan plan_bwd_batch(int n, const LinearIO* io, int64_t M) {
   BwdPlan P{};
   double best = 1e300;
-  for (int wj = 2; wj <= 3; ++wj) {
-    const int64_t trb = 64 * wj;
+  static const Tile cands[] = {{2, 2}, {4, 2}, {2, 4}, {4, 4}};
+  for (const Tile& t : cands) {
+    const int64_t tra = 64 * t.wi, trb = 64 * t.wj;
+    const int per_cu = (t.wi * t.wj <= 4) ? 2 : 1;
     for (int64_t s = 1; s <= 32; ++s) {
       if (s > 1 && M / s < 256) break;
       int64_t blocks = 0;
       double part_bytes = 0;
       for (int l = 0; l < n; ++l) {
-        blocks += ((io[l].d_out + 127) / 128) * ((io[l].d_in + trb - 1) / trb) * s;
+        blocks += ((io[l].d_out + tra - 1) / tra) * ((io[l].d_in + trb - 1) / trb) * s;
         if (s > 1) part_bytes += (2.0 * s + 1.0) * (double)(io[l].d_out * io[l].d_in * 4);
       }
-      const double rounds = (double)((blocks + 255) / 256);
+      const double rounds = (double)((blocks + 256 * per_cu - 1) / (256 * per_cu));
       const double steps = (double)(((M + s - 1) / s + 31) / 32);
-      const double t = rounds * steps * (2.0 * 128 * trb * 32) / 9.8e12 + part_bytes / 5.0e12;
-      if (t < best * 0.999) { best = t; P.wj = wj; P.splits = s; }
+      // per step a block moves (tra + trb) * 64 bytes of operands at ~20 B/clk
+      // per CU and runs 2 * tra * trb * 32 flops at ~4 Kflop/clk per CU
+      const double clk = std::max((double)(tra + trb) * 64.0 / 20.0 * per_cu,
+                                  2.0 * tra * trb * 32 / 4096.0 * per_cu);
+      const double t_us = rounds * steps * clk / 2400.0 + part_bytes / 5.0e6;
+      if (t_us < best * 0.999) { best = t_us; P.wi = t.wi; P.wj = t.wj; P.splits = s; }
     }
   }
   size_t off = 0;
@@ -719,7 +770,7 @@ hipError_t launch_dx_batch(const BatchCfg& c, const LinearIO* io, uint8_t* ws, c
     p.nbz = 1;
     I[l] = p.I; J[l] = p.J; S[l] = 1;
   }
-  launch_group<EBF16, KC, KM>(pick_wj_group(c.n, I, J, S), grp, stream);
+  launch_group<EBF16, KC, KM>(pick_tile(c.n, I, J, S), grp, stream);
   return hipGetLastError();
 }
 
@@ -768,7 +819,7 @@ hipError_t launch_dw_batch(const BatchCfg& c, const LinearIO* io, uint8_t* ws, c
     p.split_len = len;
     p.nbz = (int32_t)splits;
   }
-  launch_group<EBF16, KM, KM>(P.wj, grp, stream);
+  launch_group<EBF16, KM, KM>(Tile{P.wi, P.wj}, grp, stream);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || splits == 1) return e;
   for (int l = 0; l < c.n && e == hipSuccess; ++l)
