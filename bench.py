@@ -45,6 +45,9 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-tokens", type=int, default=4096,
                    help="tokens of the oracle's bounded sample")
+    p.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                   help="first run three plain device copies of MIB MiB, so that hardware "
+                        "byte counters can be scaled against a kernel of known traffic")
     return p.parse_args()
 
 
@@ -211,6 +214,14 @@ def main():
     dqt.load()
     wl = W.WORKLOADS[args.workload]
     torch.cuda.set_device(0)
+    if args.copy_calibration > 0:
+        n = args.copy_calibration << 20
+        src = torch.ones((n,), dtype=torch.uint8, device="cuda:0")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     blk = Block(wl, torch, dqt, W)
     units = algorithmic_units(wl)
 
