@@ -143,7 +143,7 @@ struct Prob {
   Opnd A, B;
   Epi epi;
   int64_t I, J, R, split_len;
-  int32_t nbx, nby, nbz, tile0;
+  int32_t nbx, nby, nbz, ntiles;
 };
 constexpr int MAXG = 8;
 template <class Epi>
@@ -165,18 +165,24 @@ __global__ __launch_bounds__(NTH) void gemm_v2_kernel(const Group<Epi> grp) {
   const int wi = wave >> 1, wj = wave & 1;
   const int h = lane >> 5;
   // Workgroups are dispatched round-robin over the 8 XCDs (hardware id w
-  // runs on XCD w mod 8, each XCD with its own L2).  Give every XCD a
-  // contiguous run of tiles -- problem, then split, then row tile, then
-  // column tile -- so that blocks sharing operand tiles share an L2.
+  // runs on XCD w mod 8, each XCD with its own L2), and in order of w within
+  // an XCD.  XCD x takes a contiguous 1/8 of every problem's tiles, so that
+  // the XCDs get equal work and tiles sharing operand panels share an L2;
+  // problems are sorted longest reduction first, so the long tiles start
+  // first.  The grid is padded to a multiple of 8 x the largest per-XCD
+  // count; padding blocks have no tile and leave at once.
   int g = 0, bx, by, bz;
   {
-    const int nb = gridDim.x;
-    const int w = blockIdx.x;
-    const int xcd = w & 7, k = w >> 3;
-    const int per = nb >> 3, rem = nb & 7;
-    const int L = xcd * per + (xcd < rem ? xcd : rem) + k;
-    while (g + 1 < grp.ng && L >= grp.p[g + 1].tile0) ++g;
-    const int local = L - grp.p[g].tile0;
+    const int x = blockIdx.x & 7;
+    int k = blockIdx.x >> 3;
+    int local = -1;
+    for (; g < grp.ng; ++g) {
+      const int n = grp.p[g].ntiles;
+      const int s0 = (x * n) >> 3, cnt = (((x + 1) * n) >> 3) - s0;
+      if (k < cnt) { local = s0 + k; break; }
+      k -= cnt;
+    }
+    if (local < 0) return;
     const int nbx = grp.p[g].nbx, nby = grp.p[g].nby;
     bx = local % nbx;
     by = (local / nbx) % nby;
@@ -586,22 +592,37 @@ static double tile_cost(Tile t) {
   return 1.0 / (64.0 * t.wi) + 1.0 / (64.0 * t.wj);
 }
 
-// Fill in tile grids and offsets, then launch one grid over every tile of
-// every problem of the group.
+// Fill in tile grids, sort the problems by reduction steps per tile
+// (longest first) and launch one grid over every tile of every problem.
 template <int ELEM, int MA, int MB, int WI, int WJ, class Epi>
 static void launch_group_t(Group<Epi>& grp, hipStream_t s) {
-  const int64_t tra = 64 * WI, trb = 64 * WJ;
-  int32_t tiles = 0;
+  using C = Cfg<ELEM, MA, MB, WI, WJ>;
+  const int64_t tra = C::TRA, trb = C::TRB;
+  int64_t steps[MAXG];
   for (int g = 0; g < grp.ng; ++g) {
     Prob<Epi>& p = grp.p[g];
     p.nbx = (int32_t)((p.J + trb - 1) / trb);
     p.nby = (int32_t)((p.I + tra - 1) / tra);
-    p.tile0 = tiles;
-    tiles += p.nbx * p.nby * p.nbz;
+    p.ntiles = p.nbx * p.nby * p.nbz;
+    steps[g] = (std::min(p.split_len, p.R) + C::BK - 1) / C::BK;
   }
-  if (tiles == 0) return;
-  hipLaunchKernelGGL((gemm_v2_kernel<ELEM, MA, MB, WI, WJ, Epi>), dim3((unsigned)tiles), dim3(NTH), 0,
-                     s, grp);
+  for (int a = 1; a < grp.ng; ++a)          // stable insertion sort, descending
+    for (int b = a; b > 0 && steps[b] > steps[b - 1]; --b) {
+      std::swap(steps[b], steps[b - 1]);
+      std::swap(grp.p[b], grp.p[b - 1]);
+    }
+  int32_t per_xcd = 0;
+  for (int x = 0; x < 8; ++x) {
+    int32_t c = 0;
+    for (int g = 0; g < grp.ng; ++g) {
+      const int32_t n = grp.p[g].ntiles;
+      c += ((x + 1) * n >> 3) - (x * n >> 3);
+    }
+    per_xcd = std::max(per_xcd, c);
+  }
+  if (per_xcd == 0) return;
+  hipLaunchKernelGGL((gemm_v2_kernel<ELEM, MA, MB, WI, WJ, Epi>), dim3((unsigned)(8 * per_xcd)), dim3(NTH),
+                     0, s, grp);
 }
 template <int ELEM, int MA, int MB, class Epi>
 static void launch_group(Tile t, Group<Epi>& grp, hipStream_t s) {
