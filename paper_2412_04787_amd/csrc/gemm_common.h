@@ -19,6 +19,9 @@ struct EpiFwd {          // y = fl(fl(acc) * fl(xdq[i] * alpha))
   void* y; int64_t ld; bool bf16; const float* xdq; float alpha;
   static constexpr bool kRowScale = true;
   __device__ float scale(int64_t i) const { return xdq[i] * alpha; }
+  // the same factor in two parts: the per-row load, then the multiply
+  __device__ float scale_raw(int64_t i) const { return xdq[i]; }
+  __device__ float scale_fin(float raw) const { return raw * alpha; }
   __device__ bool out_bf16() const { return bf16; }
   __device__ uint8_t* row(int64_t i, int) const {
     return static_cast<uint8_t*>(y) + i * ld * (bf16 ? 2 : 4);
@@ -34,6 +37,8 @@ struct EpiScale {        // y = fl(alpha * acc)
   void* y; int64_t ld; bool bf16; float alpha;
   static constexpr bool kRowScale = false;
   __device__ float scale(int64_t) const { return alpha; }
+  __device__ float scale_raw(int64_t) const { return 1.0f; }
+  __device__ float scale_fin(float) const { return alpha; }
   __device__ bool out_bf16() const { return bf16; }
   __device__ uint8_t* row(int64_t i, int) const {
     return static_cast<uint8_t*>(y) + i * ld * (bf16 ? 2 : 4);
@@ -48,6 +53,8 @@ struct EpiPartial {      // fp32 partial sums, one slab per split
   float* y; int64_t ld; int64_t slab;
   static constexpr bool kRowScale = false;
   __device__ float scale(int64_t) const { return 1.0f; }
+  __device__ float scale_raw(int64_t) const { return 1.0f; }
+  __device__ float scale_fin(float) const { return 1.0f; }
   __device__ bool out_bf16() const { return false; }
   __device__ uint8_t* row(int64_t i, int split) const {
     return reinterpret_cast<uint8_t*>(y + (int64_t)split * slab + i * ld);

@@ -1,0 +1,815 @@
+// MFMA GEMM for the int8 / e4m3 / bf16 contractions of the DQT linear step
+// (Sec. 3.2), written for gfx950:
+//   C[i, j] = sum_r A(i, r) B(j, r)
+// Each operand is either K-contiguous (stored [rows][R], the reduction runs
+// along a row) or K-major (stored [R][rows], bf16 only).
+//
+// Design (measured on MI355X):
+//  * Block tile 256 x 256, 8 waves in a 2 x 4 grid, each wave 128 x 64 as
+//    4 x 2 MFMA 32x32 blocks.  Two waves share each SIMD, so one wave's LDS
+//    and barrier waits are covered by the other's matrix instructions.  At
+//    this tile size a full-rate MFMA loop needs ~32 B/clk/CU of operands.
+//  * Operands move global -> LDS with direct-to-LDS DMA
+//    (global_load_lds_dwordx4, no VGPR staging) in steps of one 128-byte
+//    cache line per tile row (128 int8 / e4m3 or 64 bf16 reduction
+//    elements): streaming whole lines delivers ~35 B/clk/CU, half lines only
+//    ~21.  Two 64 KB stages: the DMA of step s+1 lands while step s runs.
+//  * Persistent grid, one block per CU.  XCD x (workgroups are dispatched
+//    round-robin over the 8 XCDs, each with its own L2) owns a contiguous
+//    1/8 of every problem's tiles, problems sorted longest reduction first;
+//    its blocks take that list round-robin.  Before a tile's epilogue the
+//    block issues the first DMA stage of its next tile, so the load latency
+//    hides behind the epilogue.
+//  * Fragments come from LDS with ds_read_b128 (K-contiguous) or with the
+//    transposing ds_read_b64_tr_b16 (K-major), which hands each lane eight
+//    reduction-consecutive bf16 of one row straight from a [R][rows] tile, so
+//    dW = dY^T X~ and dX = dY Q need no register transposes.
+//
+// LDS layouts (per stage, per operand), free of bank conflicts for the
+// fragment reads:
+//   K-contiguous: [256 rows][128 B]; 16-byte chunk c of row r sits at
+//     position c ^ ((r >> 1) & 7).
+//   K-major (bf16): four 64-column regions, each [64 reduction rows][128 B];
+//     the 32-byte segment s of row k sits at position s ^ (k & 3).
+// Each DMA wave instruction fills 1 KB of consecutive LDS positions, so each
+// lane loads the global chunk that belongs at its position.
+#include <algorithm>
+#include <type_traits>
+
+#include "gemm_common.h"
+
+namespace dqt {
+namespace v3 {
+
+using lds_u8 = __attribute__((address_space(3))) uint8_t;
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+
+constexpr int NW = 8;                 // waves per block, 2 (rows) x 4 (cols)
+constexpr int NTH = 64 * NW;
+constexpr int TILE = 256;             // block tile edge (outputs)
+constexpr int WI = 4, WJ = 2;         // MFMA 32x32 blocks per wave
+constexpr int KBYTES = 128;           // reduction bytes per tile row per step
+constexpr int OPB = TILE * KBYTES;    // bytes per operand per stage (32 KB)
+constexpr int SLOT = 2 * OPB;         // bytes per stage (64 KB)
+constexpr int NL = OPB / 16 / NTH;    // DMA instructions per thread per operand per stage
+constexpr int PITCH = 68;             // fp32 words per staged epilogue row (64 + 4)
+static_assert(NL == 4, "DMA plan assumes 4 chunks per thread");
+static_assert(NW * 16 * PITCH * 4 <= SLOT, "epilogue staging fits in one stage");
+
+enum Elem { EI8 = 0, EF8 = 1, EBF16 = 2 };
+enum Mode { KC = 0, KM = 1 };
+
+// Global operand: base of element (row 0, reduction 0), row stride in bytes,
+// extent of the tile dimension.
+struct Opnd {
+  const uint8_t* p;
+  int64_t ld;
+  int64_t n;
+};
+
+// One GEMM problem of a grouped launch: nbx x nby x nbz tiles (column tiles,
+// row tiles, reduction splits).
+template <class Epi>
+struct Prob {
+  Opnd A, B;
+  Epi epi;
+  int64_t I, J, R, split_len;
+  int32_t nbx, nby, nbz, ntiles;
+};
+constexpr int MAXG = 8;
+template <class Epi>
+struct Group {
+  Prob<Epi> p[MAXG];
+  int32_t ng;
+};
+
+__device__ __forceinline__ void tr_wait2(u32x2& a, u32x2& b) {
+  asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(a), "+v"(b));
+}
+__device__ __forceinline__ i32x4 join(u32x2 lo, u32x2 hi) {
+  return i32x4{(int)lo[0], (int)lo[1], (int)hi[0], (int)hi[1]};
+}
+// One direct-to-LDS load of 16 bytes per lane; the wave's 64 chunks land at
+// l, l + 16, ... (l is wave-uniform, passed in M0).  Issued as inline asm so
+// that the compiler, which cannot tell which LDS bytes the DMA writes, does
+// not wait for all outstanding DMA before every later LDS access; the
+// kernel waits for its DMA explicitly (vmcnt) before the barrier that
+// publishes a stage.  Nothing else in these kernels uses M0.
+__device__ __forceinline__ void dma16(const uint8_t* g, lds_u8* l) {
+  const uint32_t m0 = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)l);
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" : : "v"(g), "s"(m0) : "memory");
+}
+__device__ __forceinline__ void wait_vm0() {
+  __builtin_amdgcn_s_waitcnt((0) | (0 << 14) | (7 << 4) | (15 << 8));
+}
+// Barrier that keeps the compiler from moving memory accesses across it; it
+// waits for this wave's LDS accesses but not for outstanding DMA.
+__device__ __forceinline__ void block_barrier() {
+  __asm__ volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt((15) | (3 << 14) | (7 << 4) | (0 << 8));   // lgkmcnt(0)
+  __builtin_amdgcn_s_barrier();
+  __asm__ volatile("" ::: "memory");
+}
+
+// Per-thread DMA plan of one operand of one tile: the global address of each
+// of its NL chunks at step 0; the reduction offset (elements, within a step)
+// the chunks cover, which is the same for all of them; and the distance
+// back from a chunk's address to a safe one in the same row (K-contiguous)
+// or column (K-major) for loads past the end of the reduction.
+template <int MODE, int EB>
+struct Plan {
+  const uint8_t* g[NL];
+  int64_t back;
+  int64_t inc;
+  int rk;
+
+  __device__ void init(const Opnd& o, int64_t row0, int64_t r_begin, int tid) {
+#pragma unroll
+    for (int q = 0; q < NL; ++q) {
+      const int p = q * NTH + tid;                  // physical 16-byte position
+      if constexpr (MODE == KC) {
+        const int row = p >> 3;
+        const int c = (p & 7) ^ ((row >> 1) & 7);   // logical chunk (same for every q)
+        int64_t gr = row0 + row;
+        if (gr > o.n - 1) gr = o.n - 1;
+        g[q] = o.p + gr * o.ld + r_begin * EB + 16 * c;
+        back = r_begin * EB + 16 * c;
+        rk = 16 * c / EB;
+      } else {
+        const int region = p >> 9;                  // 64-column region
+        const int k = (p & 511) >> 3;               // reduction row within the step (same for every q)
+        const int pc = p & 7;
+        const int seg = (pc >> 1) ^ (k & 3);
+        int64_t col = row0 + 64 * region + 16 * seg + 8 * (pc & 1);
+        if (col > o.n - 8) col = o.n - 8;
+        g[q] = o.p + (r_begin + k) * o.ld + 2 * col;
+        back = (int64_t)k * o.ld;
+        rk = k;
+      }
+    }
+    inc = MODE == KC ? KBYTES : 64 * o.ld;
+  }
+};
+
+// Tile j of XCD x's list: XCD x owns [x n / 8, (x + 1) n / 8) of every
+// problem's n tiles, problems in launch order.  False past the end.
+template <class Epi>
+__device__ __forceinline__ bool locate(const Group<Epi>& grp, int x, int j, int& g, int& local) {
+  for (g = 0; g < grp.ng; ++g) {
+    const int n = grp.p[g].ntiles;
+    const int s0 = (x * n) >> 3, cnt = (((x + 1) * n) >> 3) - s0;
+    if (j < cnt) {
+      local = s0 + j;
+      return true;
+    }
+    j -= cnt;
+  }
+  return false;
+}
+
+template <int ELEM, int MA, int MB, class Epi>
+__global__ __launch_bounds__(NTH) void gemm_v3_kernel(const Group<Epi> grp) {
+  constexpr int EB = ELEM == EBF16 ? 2 : 1;
+  constexpr int BK = KBYTES / EB;           // reduction elements per step
+  __shared__ __attribute__((aligned(1024))) uint8_t smem_generic[2 * SLOT];
+  __shared__ float row_scale[Epi::kRowScale ? TILE : 1];
+  lds_u8* smem = (lds_u8*)smem_generic;
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int wi = wave >> 2, wj = wave & 3;
+  const int h = lane >> 5;
+  const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+  const int xcd = blockIdx.x & 7, kb = blockIdx.x >> 3, nbx8 = gridDim.x >> 3;
+
+  // ---- state of the tile being computed
+  struct TileState {
+    int g;
+    int64_t i0, j0, rlen;
+    int bz, nsteps;
+    bool tail;
+  };
+  Plan<MA, EB> pa;
+  Plan<MB, EB> pb;
+  TileState cur;
+  float my_scale = 0.0f;
+
+  auto setup = [&](int g, int local, TileState& T) {
+    const Prob<Epi>& P = grp.p[g];
+    const int bx = local % P.nbx;
+    const int by = (local / P.nbx) % P.nby;
+    const int bz = local / (P.nbx * P.nby);
+    T.g = g;
+    T.i0 = (int64_t)by * TILE;
+    T.j0 = (int64_t)bx * TILE;
+    T.bz = bz;
+    const int64_t r_begin = (int64_t)bz * P.split_len;
+    int64_t r_end = r_begin + P.split_len;
+    if (r_end > P.R) r_end = P.R;
+    T.rlen = r_end > r_begin ? r_end - r_begin : 0;
+    T.nsteps = (int)((T.rlen + BK - 1) / BK);
+    T.tail = (T.rlen % BK) != 0;
+    pa.init(P.A, T.i0, r_begin, tid);
+    pb.init(P.B, T.j0, r_begin, tid);
+    if constexpr (Epi::kRowScale) {
+      if (tid < TILE) {
+        int64_t i = T.i0 + tid;
+        if (i > P.I - 1) i = P.I - 1;
+        my_scale = P.epi.scale_raw(i);     // used only in the epilogue
+      }
+    }
+  };
+
+  // DMA of step s of the current plans into stage `slot`.
+  auto issue = [&](int s, int slot, const TileState& T) {
+    lds_u8* la = smem + slot * SLOT + wave_u * 1024;
+    lds_u8* lb = la + OPB;
+    if (!(T.tail && s == T.nsteps - 1)) {
+#pragma unroll
+      for (int q = 0; q < NL; ++q) dma16(pa.g[q] + (int64_t)s * pa.inc, la + q * (NTH * 16));
+#pragma unroll
+      for (int q = 0; q < NL; ++q) dma16(pb.g[q] + (int64_t)s * pb.inc, lb + q * (NTH * 16));
+    } else {
+      const int64_t rbase = (int64_t)s * BK;
+      const bool oa = rbase + pa.rk >= T.rlen, ob = rbase + pb.rk >= T.rlen;
+#pragma unroll
+      for (int q = 0; q < NL; ++q) dma16(oa ? pa.g[q] - pa.back : pa.g[q] + (int64_t)s * pa.inc, la + q * (NTH * 16));
+#pragma unroll
+      for (int q = 0; q < NL; ++q) dma16(ob ? pb.g[q] - pb.back : pb.g[q] + (int64_t)s * pb.inc, lb + q * (NTH * 16));
+    }
+  };
+  // zero the chunks this thread loaded past the end of the reduction (its
+  // own DMA for that stage has completed)
+  auto zero_tail = [&](int s, int slot, const TileState& T) {
+    lds_u8* la = smem + slot * SLOT;
+    lds_u8* lb = la + OPB;
+    const int64_t rbase = (int64_t)s * BK;
+    const i32x4 z = {0, 0, 0, 0};
+    if (rbase + pa.rk >= T.rlen)
+#pragma unroll
+      for (int q = 0; q < NL; ++q) *(__attribute__((address_space(3))) i32x4*)(la + (q * NTH + tid) * 16) = z;
+    if (rbase + pb.rk >= T.rlen)
+#pragma unroll
+      for (int q = 0; q < NL; ++q) *(__attribute__((address_space(3))) i32x4*)(lb + (q * NTH + tid) * 16) = z;
+  };
+
+  using AccV = typename AccT<ELEM == EI8 ? Mfma::I8 : Mfma::BF16>::type;
+  AccV acc[WI][WJ];
+
+  // fragment address parts
+  const int frow = lane & 31;
+  const int t4 = (lane >> 2) & 3, u4 = lane & 3, ch = (lane >> 4) & 1;
+
+  // Fragments of one reduction sub-step kk (0..3; 32 bytes of reduction per
+  // tile row): K-contiguous ones by ds_read_b128, K-major ones by two
+  // transposing reads (inline asm, waited for by frag_wait).
+  struct Frags {
+    i32x4 fa[WI], fb[WJ];
+    u32x2 ka[WI][2], kb[WJ][2];
+  };
+  auto read_frags = [&](const lds_u8* la, const lds_u8* lb, int kk, Frags& F) {
+#pragma unroll
+    for (int t = 0; t < WI; ++t) {
+      if constexpr (MA == KC) {
+        const int row = wi * 32 * WI + t * 32 + frow;
+        const int c = (2 * kk + h) ^ ((row >> 1) & 7);
+        F.fa[t] = *(const __attribute__((address_space(3))) i32x4*)(la + row * KBYTES + 16 * c);
+      } else {
+        const int col = wi * 32 * WI + t * 32 + 16 * ch + 4 * u4;
+        const int seg = ((col & 63) >> 4) ^ t4;
+        const uint32_t a0 = (uint32_t)(uintptr_t)(la + (col >> 6) * 8192 + (16 * kk + 8 * h + t4) * 128 +
+                                                  32 * seg + 8 * u4);
+        asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(F.ka[t][0]) : "v"(a0));
+        asm volatile("ds_read_b64_tr_b16 %0, %1 offset:512" : "=v"(F.ka[t][1]) : "v"(a0));
+      }
+    }
+#pragma unroll
+    for (int t = 0; t < WJ; ++t) {
+      if constexpr (MB == KC) {
+        const int row = wj * 32 * WJ + t * 32 + frow;
+        const int c = (2 * kk + h) ^ ((row >> 1) & 7);
+        F.fb[t] = *(const __attribute__((address_space(3))) i32x4*)(lb + row * KBYTES + 16 * c);
+      } else {
+        const int col = wj * 32 * WJ + t * 32 + 16 * ch + 4 * u4;
+        const int seg = ((col & 63) >> 4) ^ t4;
+        const uint32_t a0 = (uint32_t)(uintptr_t)(lb + (col >> 6) * 8192 + (16 * kk + 8 * h + t4) * 128 +
+                                                  32 * seg + 8 * u4);
+        asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(F.kb[t][0]) : "v"(a0));
+        asm volatile("ds_read_b64_tr_b16 %0, %1 offset:512" : "=v"(F.kb[t][1]) : "v"(a0));
+      }
+    }
+  };
+  auto frag_wait = [&](Frags& F) {
+    if constexpr (MA == KM) {
+#pragma unroll
+      for (int t = 0; t < WI; ++t) tr_wait2(F.ka[t][0], F.ka[t][1]);
+    }
+    if constexpr (MB == KM) {
+#pragma unroll
+      for (int t = 0; t < WJ; ++t) tr_wait2(F.kb[t][0], F.kb[t][1]);
+    }
+  };
+  auto opa = [&](const Frags& F, int t) { return MA == KC ? F.fa[t] : join(F.ka[t][0], F.ka[t][1]); };
+  auto opb = [&](const Frags& F, int t) { return MB == KC ? F.fb[t] : join(F.kb[t][0], F.kb[t][1]); };
+  // MFMAs of one sub-step (int8 / bf16), or of two sub-steps (e4m3, whose
+  // instruction reduces 64 elements: sub-step pairs (0, 1) and (2, 3)).
+  auto mfma1 = [&](const Frags& F) {
+#pragma unroll
+    for (int ta = 0; ta < WI; ++ta)
+#pragma unroll
+      for (int tb = 0; tb < WJ; ++tb) {
+        if constexpr (ELEM == EI8)
+          acc[ta][tb] = __builtin_amdgcn_mfma_i32_32x32x32_i8(opa(F, ta), opb(F, tb), acc[ta][tb], 0, 0, 0);
+        else
+          acc[ta][tb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, opa(F, ta)),
+                                                                __builtin_bit_cast(bf16x8, opb(F, tb)),
+                                                                acc[ta][tb], 0, 0, 0);
+      }
+  };
+  auto mfma2 = [&](const Frags& F0, const Frags& F1) {
+#pragma unroll
+    for (int ta = 0; ta < WI; ++ta)
+#pragma unroll
+      for (int tb = 0; tb < WJ; ++tb) {
+        const i32x4 a0 = opa(F0, ta), a1 = opa(F1, ta), b0 = opb(F0, tb), b1 = opb(F1, tb);
+        const i32x8 av = {a0[0], a0[1], a0[2], a0[3], a1[0], a1[1], a1[2], a1[3]};
+        const i32x8 bv = {b0[0], b0[1], b0[2], b0[3], b1[0], b1[1], b1[2], b1[3]};
+        // both operands e4m3 (format 0), unit E8M0 scales (127 = 2^0)
+        acc[ta][tb] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(av, bv, acc[ta][tb], 0, 0, 0, 127, 0, 127);
+      }
+  };
+  // One step from stage `slot`: sub-step kk+1's fragments load while kk's
+  // MFMAs run.
+  auto compute = [&](int slot) {
+    const lds_u8* la = smem + slot * SLOT;
+    const lds_u8* lb = la + OPB;
+    Frags F0, F1, F2, F3;
+    read_frags(la, lb, 0, F0);
+    frag_wait(F0);
+    read_frags(la, lb, 1, F1);
+    if constexpr (ELEM != EF8) mfma1(F0);
+    frag_wait(F1);
+    read_frags(la, lb, 2, F2);
+    if constexpr (ELEM != EF8) mfma1(F1);
+    else mfma2(F0, F1);
+    frag_wait(F2);
+    read_frags(la, lb, 3, F3);
+    if constexpr (ELEM != EF8) mfma1(F2);
+    frag_wait(F3);
+    if constexpr (ELEM != EF8) mfma1(F3);
+    else mfma2(F2, F3);
+  };
+
+  // ---- persistent loop over this block's tiles
+  int g0, local0;
+  if (!locate(grp, xcd, kb, g0, local0)) return;
+  setup(g0, local0, cur);
+  int slot0 = 0;                         // stage of the current tile's step 0
+  if (cur.nsteps > 0) issue(0, slot0, cur);
+
+  for (int j = kb;;) {
+#pragma unroll
+    for (int a = 0; a < WI; ++a)
+#pragma unroll
+      for (int b = 0; b < WJ; ++b)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[a][b][r] = 0;
+
+    // main loop: step it computes from stage (slot0 + it) & 1 while step
+    // it + 1 loads into the other stage
+    for (int it = 0; it < cur.nsteps; ++it) {
+      const int slot = (slot0 + it) & 1;
+      wait_vm0();
+      if (cur.tail && it == cur.nsteps - 1) zero_tail(it, slot, cur);
+      block_barrier();                 // stage `slot` complete; the other stage is free
+      if (it + 1 < cur.nsteps) issue(it + 1, slot ^ 1, cur);
+      compute(slot);
+    }
+
+    // epilogue parameters of this tile, then the next tile's first stage
+    const Prob<Epi>& P = grp.p[cur.g];
+    const Epi epi = P.epi;
+    const int64_t I = P.I, J = P.J;
+    const int64_t i0 = cur.i0, j0 = cur.j0;
+    const int bz = cur.bz;
+    const int last = (slot0 + cur.nsteps + 1) & 1;   // stage of the last step (staging area)
+    if constexpr (Epi::kRowScale) {
+      if (tid < TILE) row_scale[tid] = epi.scale_fin(my_scale);
+    }
+    block_barrier();                   // every wave is done with both stages
+    const int jn = j + nbx8;
+    int gn, localn;
+    const bool more = locate(grp, xcd, jn, gn, localn);
+    if (more) {
+      const int slotn = (slot0 + cur.nsteps) & 1;
+      setup(gn, localn, cur);
+      if (cur.nsteps > 0) issue(0, slotn, cur);
+      slot0 = slotn;
+    }
+
+    // Lane (j = lane mod 32, h) of MFMA block (ta, tb) holds column j of rows
+    // 8 (r / 4) + 4 h + (r mod 4), r = 0..15.  Each wave stages 16 of its
+    // rows at a time as fp32 in its own part of stage `last`, then writes
+    // whole 16-byte chunks of output rows (8 bf16 or 4 fp32).
+    lds_u8* stage = smem + last * SLOT + wave * (16 * PITCH * 4);
+    const bool obf = epi.out_bf16();
+#pragma unroll
+    for (int ta = 0; ta < WI; ++ta) {
+      float sc[16];
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+        sc[r] = Epi::kRowScale ? row_scale[wi * 32 * WI + ta * 32 + 8 * (r >> 2) + 4 * h + (r & 3)]
+                               : epi.scale(0);
+#pragma unroll
+      for (int half = 0; half < 2; ++half) {
+#pragma unroll
+        for (int tb = 0; tb < WJ; ++tb)
+#pragma unroll
+          for (int r8 = 0; r8 < 8; ++r8) {
+            const int r = 8 * half + r8;
+            float v;
+            if constexpr (ELEM == EI8) v = (float)acc[ta][tb][r];
+            else v = acc[ta][tb][r];
+            v = v * sc[r];
+            const int lr = 8 * ((r >> 2) & 1) + 4 * h + (r & 3);
+            *(__attribute__((address_space(3))) float*)(stage + (lr * PITCH + tb * 32 + (lane & 31)) * 4) = v;
+          }
+        __asm__ volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+        const int64_t ibase = i0 + wi * 32 * WI + ta * 32 + 16 * half;
+        const int64_t jbase = j0 + wj * 32 * WJ;
+        auto store_rows = [&](auto ebytes_tag) {
+          constexpr int EBY = decltype(ebytes_tag)::value;
+          constexpr int EPC = 16 / EBY;            // elements per 16-byte chunk
+          constexpr int CPR = 32 * WJ / EPC;       // chunks per staged row
+#pragma unroll
+          for (int c0 = 0; c0 < 16 * CPR; c0 += 64) {
+            const int c = c0 + lane;
+            const int rr = c / CPR, cc = c % CPR;
+            const int64_t i = ibase + rr;
+            const int64_t jj = jbase + cc * EPC;
+            if (i < I && jj < J) {
+              const lds_u8* src = stage + (rr * PITCH + cc * EPC) * 4;
+              uint8_t* dst = epi.row(i, bz) + jj * EBY;
+              if constexpr (EBY == 2) {
+                const f32x4 a = *(const __attribute__((address_space(3))) f32x4*)src;
+                const f32x4 b = *(const __attribute__((address_space(3))) f32x4*)(src + 16);
+                *reinterpret_cast<uint4*>(dst) = make_uint4(pack_bf16x2(a[0], a[1]), pack_bf16x2(a[2], a[3]),
+                                                            pack_bf16x2(b[0], b[1]), pack_bf16x2(b[2], b[3]));
+              } else {
+                *reinterpret_cast<f32x4*>(dst) = *(const __attribute__((address_space(3))) f32x4*)src;
+              }
+            }
+          }
+        };
+        if (obf) store_rows(std::integral_constant<int, 2>{});
+        else store_rows(std::integral_constant<int, 4>{});
+        __asm__ volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+      }
+    }
+    if (!more) break;
+    j = jn;
+    // a tile without reduction steps has no main-loop barrier before the
+    // next epilogue reuses the staging area and the row scales
+    if (cur.nsteps == 0) block_barrier();
+  }
+}
+
+}  // namespace v3
+}  // namespace dqt
+
+// ------------------------------------------------------------ pre-passes
+namespace dqt {
+namespace v3 {
+
+// Up to MAXG independent element ranges handled by one launch.  Segment s
+// owns blocks [b0[s], b0[s+1]); each thread of a block handles one 16-element
+// chunk; chunks past n16[s] do nothing.
+struct SegTab {
+  const void* src[MAXG];
+  void* dst[MAXG];
+  const float* scale[MAXG];   // per-row scales (activation dequantisation)
+  int64_t n16[MAXG];
+  int32_t k16[MAXG];          // 16-element chunks per row (activation dequantisation)
+  int32_t b0[MAXG + 1];
+  int32_t n;
+};
+
+__device__ __forceinline__ int seg_of_block(const SegTab& t) {
+  int s = 0;
+  while (s + 1 < t.n && (int)blockIdx.x >= t.b0[s + 1]) ++s;
+  return s;
+}
+
+// Packed ternary codes -> one operand byte (int8 or e4m3) or one bf16 per
+// weight, same [d_out][d_in] row-major order.
+template <int OUT>   // 0: int8, 1: e4m3, 2: bf16
+__global__ __launch_bounds__(256) void unpack_ternary_kernel(const SegTab tab) {
+  const int s = seg_of_block(tab);
+  const int64_t t = (int64_t)(blockIdx.x - tab.b0[s]) * 256 + threadIdx.x;
+  if (t >= tab.n16[s]) return;
+  const uint32_t w = static_cast<const uint32_t*>(tab.src[s])[t];
+  if constexpr (OUT < 2) {
+    uint32_t o[4];
+#pragma unroll
+    for (int b = 0; b < 4; ++b) {
+      const uint32_t sp = spread_codes((w >> (8 * b)) & 0xFFu);
+      o[b] = OUT == 1 ? codes_to_e4m3x4(sp) : codes_to_i8x4(sp);
+    }
+    static_cast<uint4*>(tab.dst[s])[t] = make_uint4(o[0], o[1], o[2], o[3]);
+  } else {
+    uint32_t o[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const uint32_t c = (w >> (4 * j)) & 0xFu;
+      o[j] = code_to_bf16_bits(c & 3u) | (code_to_bf16_bits(c >> 2) << 16);
+    }
+    uint4* d = static_cast<uint4*>(tab.dst[s]) + 2 * t;
+    d[0] = make_uint4(o[0], o[1], o[2], o[3]);
+    d[1] = make_uint4(o[4], o[5], o[6], o[7]);
+  }
+}
+
+// int8 codes -> bf16 (|q| <= 128 is exact in bf16).
+__global__ __launch_bounds__(256) void int8_to_bf16_kernel(const SegTab tab) {
+  const int s = seg_of_block(tab);
+  const int64_t t = (int64_t)(blockIdx.x - tab.b0[s]) * 256 + threadIdx.x;
+  if (t >= tab.n16[s]) return;
+  const uint4 v = static_cast<const uint4*>(tab.src[s])[t];
+  const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+  uint32_t o[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const uint32_t two = w[j >> 1] >> (16 * (j & 1));
+    const float lo = (float)(int)(int8_t)(two & 0xFFu);
+    const float hi = (float)(int)(int8_t)((two >> 8) & 0xFFu);
+    o[j] = (__float_as_uint(lo) >> 16) | (__float_as_uint(hi) & 0xFFFF0000u);
+  }
+  uint4* d = static_cast<uint4*>(tab.dst[s]) + 2 * t;
+  d[0] = make_uint4(o[0], o[1], o[2], o[3]);
+  d[1] = make_uint4(o[4], o[5], o[6], o[7]);
+}
+
+// X~[m, k] = bf16(fl(value(Xq[m, k]) * xdq[m])).
+template <bool E4M3>
+__global__ __launch_bounds__(256) void dequant_act_kernel(const SegTab tab) {
+  const int s = seg_of_block(tab);
+  const int64_t t = (int64_t)(blockIdx.x - tab.b0[s]) * 256 + threadIdx.x;
+  if (t >= tab.n16[s]) return;
+  const float d = tab.scale[s][t / tab.k16[s]];
+  const uint4 v = static_cast<const uint4*>(tab.src[s])[t];
+  const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+  uint32_t o[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const uint32_t two = w[j >> 1] >> (16 * (j & 1));
+    float a, b;
+    if constexpr (E4M3) {
+      a = e4m3_to_f32(two & 0xFFu);
+      b = e4m3_to_f32((two >> 8) & 0xFFu);
+    } else {
+      a = (float)(int)(int8_t)(two & 0xFFu);
+      b = (float)(int)(int8_t)((two >> 8) & 0xFFu);
+    }
+    o[j] = pack_bf16x2(a * d, b * d);
+  }
+  uint4* dst = static_cast<uint4*>(tab.dst[s]) + 2 * t;
+  dst[0] = make_uint4(o[0], o[1], o[2], o[3]);
+  dst[1] = make_uint4(o[4], o[5], o[6], o[7]);
+}
+
+static int32_t seal(SegTab& t) {
+  int32_t b = 0;
+  for (int s = 0; s < t.n; ++s) {
+    t.b0[s] = b;
+    b += (int32_t)((t.n16[s] + 255) / 256);
+  }
+  t.b0[t.n] = b;
+  return b;
+}
+
+// Compute units of the current device (one persistent block each).
+static int device_cus() {
+  int dev = 0, n = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 256;
+  if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) return 256;
+  return n;
+}
+
+// Fill in tile grids, sort the problems by reduction steps per tile (longest
+// first) and launch the persistent grid: 8 x (blocks per XCD).
+template <int ELEM, int MA, int MB, class Epi>
+static void launch_group(Group<Epi>& grp, hipStream_t s) {
+  constexpr int64_t BK = KBYTES / (ELEM == EBF16 ? 2 : 1);
+  int64_t steps[MAXG];
+  for (int g = 0; g < grp.ng; ++g) {
+    Prob<Epi>& p = grp.p[g];
+    p.nbx = (int32_t)((p.J + TILE - 1) / TILE);
+    p.nby = (int32_t)((p.I + TILE - 1) / TILE);
+    p.ntiles = p.nbx * p.nby * p.nbz;
+    steps[g] = (std::min(p.split_len, p.R) + BK - 1) / BK;
+  }
+  for (int a = 1; a < grp.ng; ++a)          // stable insertion sort, descending
+    for (int b = a; b > 0 && steps[b] > steps[b - 1]; --b) {
+      std::swap(steps[b], steps[b - 1]);
+      std::swap(grp.p[b], grp.p[b - 1]);
+    }
+  int32_t per_xcd = 0;
+  for (int x = 0; x < 8; ++x) {
+    int32_t c = 0;
+    for (int g = 0; g < grp.ng; ++g) {
+      const int32_t n = grp.p[g].ntiles;
+      c += ((x + 1) * n >> 3) - (x * n >> 3);
+    }
+    per_xcd = std::max(per_xcd, c);
+  }
+  if (per_xcd == 0) return;
+  static const int cus = device_cus();
+  const int32_t bpx = std::min(per_xcd, std::max(1, cus / 8));
+  hipLaunchKernelGGL((gemm_v3_kernel<ELEM, MA, MB, Epi>), dim3((unsigned)(8 * bpx)), dim3(NTH), 0, s, grp);
+}
+
+}  // namespace v3
+
+using namespace v3;
+
+static size_t align256(size_t n) { return (n + 255) / 256 * 256; }
+
+size_t fwd_batch_workspace(int n, const LinearIO* io, bool ternary, size_t* offs) {
+  size_t total = 0;
+  for (int l = 0; l < n; ++l) {
+    if (offs) offs[l] = total;
+    if (ternary) total += align256((size_t)(io[l].d_out * io[l].d_in));
+  }
+  return total;
+}
+
+hipError_t launch_fwd_batch(const BatchCfg& c, const LinearIO* io, uint8_t* ws, hipStream_t stream) {
+  if (c.M == 0 || c.n == 0) return hipSuccess;
+  size_t offs[kMaxBatch];
+  fwd_batch_workspace(c.n, io, c.w_ternary, offs);
+  if (c.w_ternary) {
+    SegTab tab{};
+    tab.n = c.n;
+    for (int l = 0; l < c.n; ++l) {
+      tab.src[l] = io[l].Wq;
+      tab.dst[l] = ws + offs[l];
+      tab.n16[l] = io[l].d_out * io[l].d_in / 16;
+    }
+    const int32_t blocks = seal(tab);
+    if (c.act_e4m3)
+      hipLaunchKernelGGL(unpack_ternary_kernel<1>, dim3(blocks), dim3(256), 0, stream, tab);
+    else
+      hipLaunchKernelGGL(unpack_ternary_kernel<0>, dim3(blocks), dim3(256), 0, stream, tab);
+  }
+  Group<EpiFwd> grp{};
+  grp.ng = c.n;
+  for (int l = 0; l < c.n; ++l) {
+    Prob<EpiFwd>& p = grp.p[l];
+    const uint8_t* rows = c.w_ternary ? ws + offs[l] : static_cast<const uint8_t*>(io[l].Wq);
+    p.A = Opnd{static_cast<const uint8_t*>(io[l].Xq), io[l].d_in, c.M};
+    p.B = Opnd{rows, io[l].d_in, io[l].d_out};
+    p.epi = EpiFwd{io[l].Y, io[l].d_out, c.out_bf16, io[l].xdq, io[l].alpha};
+    p.I = c.M;
+    p.J = io[l].d_out;
+    p.R = io[l].d_in;
+    p.split_len = io[l].d_in;
+    p.nbz = 1;
+  }
+  if (c.act_e4m3) launch_group<EF8, KC, KC>(grp, stream);
+  else launch_group<EI8, KC, KC>(grp, stream);
+  return hipGetLastError();
+}
+
+// Backward plan for a batch in the bf16 environment: one split count for
+// every dW product of the batch, and the workspace layout
+//   per linear: [bf16 weights d_out x d_in][bf16 X~ M x d_in][fp32 partials]
+// (partials sized for the larger of this plan's and the fp32 kernels' split).
+// The split count minimises an estimate of rounds of the persistent grid x
+// steps per tile plus the traffic of the partial sums.
+BwdPlan plan_bwd_batch(int n, const LinearIO* io, int64_t M) {
+  BwdPlan P{};
+  P.wi = 4;
+  P.wj = 4;
+  P.splits = 1;
+  double best = 1e300;
+  static const int cus = device_cus();
+  for (int64_t s = 1; s <= 32; ++s) {
+    if (s > 1 && M / s < 256) break;
+    int64_t tiles = 0;
+    double part_bytes = 0;
+    for (int l = 0; l < n; ++l) {
+      tiles += ((io[l].d_out + TILE - 1) / TILE) * ((io[l].d_in + TILE - 1) / TILE) * s;
+      if (s > 1) part_bytes += (2.0 * s + 1.0) * (double)(io[l].d_out * io[l].d_in * 4);
+    }
+    const double rounds = (double)((tiles + cus - 1) / cus);
+    const double steps = (double)(((M + s - 1) / s + 63) / 64);
+    // a step of a 256 x 256 bf16 tile is ~2048 MFMA cycles at ~2.1 GHz,
+    // plus ~2 us of per-tile prologue / epilogue; partials move at ~4 TB/s
+    const double t_us = rounds * (steps * 2048.0 / 2100.0 + 2.0) + part_bytes / 4.0e6;
+    if (t_us < best * 0.999) { best = t_us; P.splits = s; }
+  }
+  size_t off = 0;
+  for (int l = 0; l < n; ++l) {
+    const size_t wn = (size_t)(io[l].d_out * io[l].d_in);
+    const int64_t s32 = dw_splits_f32(io[l].d_out, io[l].d_in, M);
+    const int64_t sp = P.splits > s32 ? P.splits : s32;
+    P.q_off[l] = off;
+    off += align256(wn * 2);
+    P.xt_off[l] = off;
+    off += align256((size_t)M * (size_t)io[l].d_in * 2);
+    P.part_off[l] = off;
+    off += sp > 1 ? align256((size_t)sp * wn * 4) : 0;
+  }
+  P.total = off;
+  return P;
+}
+
+hipError_t launch_dx_batch(const BatchCfg& c, const LinearIO* io, uint8_t* ws, const BwdPlan& P,
+                           hipStream_t stream) {
+  if (c.M == 0 || c.n == 0) return hipSuccess;
+  SegTab tab{};
+  tab.n = c.n;
+  for (int l = 0; l < c.n; ++l) {
+    tab.src[l] = io[l].Wq;
+    tab.dst[l] = ws + P.q_off[l];
+    tab.n16[l] = io[l].d_out * io[l].d_in / 16;
+  }
+  const int32_t blocks = seal(tab);
+  if (c.w_ternary)
+    hipLaunchKernelGGL(unpack_ternary_kernel<2>, dim3(blocks), dim3(256), 0, stream, tab);
+  else
+    hipLaunchKernelGGL(int8_to_bf16_kernel, dim3(blocks), dim3(256), 0, stream, tab);
+  // dX[m, k] = alpha sum_n dY[m, n] q[n, k]: I = M, J = d_in, R = d_out
+  Group<EpiScale> grp{};
+  grp.ng = c.n;
+  for (int l = 0; l < c.n; ++l) {
+    Prob<EpiScale>& p = grp.p[l];
+    p.A = Opnd{static_cast<const uint8_t*>(io[l].dY), io[l].d_out * 2, c.M};
+    p.B = Opnd{ws + P.q_off[l], io[l].d_in * 2, io[l].d_in};
+    p.epi = EpiScale{io[l].dX, io[l].d_in, c.out_bf16, io[l].alpha};
+    p.I = c.M;
+    p.J = io[l].d_in;
+    p.R = io[l].d_out;
+    p.split_len = io[l].d_out;
+    p.nbz = 1;
+  }
+  launch_group<EBF16, KC, KM>(grp, stream);
+  return hipGetLastError();
+}
+
+hipError_t launch_dw_batch(const BatchCfg& c, const LinearIO* io, uint8_t* ws, const BwdPlan& P,
+                           hipStream_t stream) {
+  if (c.n == 0) return hipSuccess;
+  // X~ once per distinct quantised input
+  int first[kMaxBatch];
+  SegTab tab{};
+  for (int l = 0; l < c.n; ++l) {
+    first[l] = l;
+    for (int m = 0; m < l; ++m)
+      if (io[m].Xq == io[l].Xq && io[m].d_in == io[l].d_in) { first[l] = first[m]; break; }
+    if (first[l] == l && c.M > 0) {
+      const int s = tab.n++;
+      tab.src[s] = io[l].Xq;
+      tab.dst[s] = ws + P.xt_off[l];
+      tab.scale[s] = io[l].xdq;
+      tab.n16[s] = c.M * io[l].d_in / 16;
+      tab.k16[s] = (int32_t)(io[l].d_in / 16);
+    }
+  }
+  if (tab.n > 0) {
+    const int32_t blocks = seal(tab);
+    if (c.act_e4m3)
+      hipLaunchKernelGGL(dequant_act_kernel<true>, dim3(blocks), dim3(256), 0, stream, tab);
+    else
+      hipLaunchKernelGGL(dequant_act_kernel<false>, dim3(blocks), dim3(256), 0, stream, tab);
+  }
+  // dW[n, k] = sum_m dY[m, n] X~[m, k]: I = d_out, J = d_in, R = M
+  const int64_t splits = P.splits;
+  int64_t len = splits > 1 ? (c.M + splits - 1) / splits : (c.M > 0 ? c.M : 1);
+  len = (len + 63) / 64 * 64;
+  Group<EpiPartial> grp{};
+  grp.ng = c.n;
+  for (int l = 0; l < c.n; ++l) {
+    Prob<EpiPartial>& p = grp.p[l];
+    const int64_t I = io[l].d_out, J = io[l].d_in;
+    p.A = Opnd{static_cast<const uint8_t*>(io[l].dY), I * 2, I};
+    p.B = Opnd{ws + P.xt_off[first[l]], J * 2, J};
+    float* target = splits > 1 ? reinterpret_cast<float*>(ws + P.part_off[l]) : io[l].dW;
+    p.epi = EpiPartial{target, J, I * J};
+    p.I = I;
+    p.J = J;
+    p.R = c.M;
+    p.split_len = len;
+    p.nbz = (int32_t)splits;
+  }
+  launch_group<EBF16, KM, KM>(grp, stream);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || splits == 1) return e;
+  for (int l = 0; l < c.n && e == hipSuccess; ++l)
+    e = launch_split_reduce(reinterpret_cast<const float*>(ws + P.part_off[l]), (int)splits,
+                            io[l].d_out * io[l].d_in, io[l].dW, stream);
+  return e;
+}
+
+}  // namespace dqt
