@@ -91,6 +91,8 @@ class Block:
                              xdq=self.xdq[lin.input], Y=self.Y[li], dY=self.dY[li],
                              dX=self.dX[li], dW=self.dW[li]))
         self.io_all = dqt.linear_io(ents)
+        self.act_io = dqt.act_io([(self.X[n], self.Xq[n], self.xdq[n]) for n in wl.inputs])
+        self.x_t = dqt.DQT_BF16 if wl.x_dtype == "bf16" else dqt.DQT_F32
         self.io_dx = dqt.linear_io([dict(e, dW=None) for e in ents])
         self.io_dw = dqt.linear_io([dict(e, dX=None) for e in ents])
         self.y_t = dqt.DQT_BF16 if wl.y_out == "bf16" else dqt.DQT_F32
@@ -104,14 +106,12 @@ class Block:
 
 
 def run_step(blk, dqt, step, stream, rec):
-    """Enqueue one train step: act-quant per distinct input, then one batched
-    call per stage over all linears.  rec(kind, fn) runs fn (or records it
+    """Enqueue one train step: one batched call per stage (act-quant of every
+    distinct input, forward, dX, dW, SR update) over all linears.  rec(kind, fn) runs fn (or records it
     into a graph)."""
     wl = blk.wl
     M = wl.M
-    for name in wl.inputs:
-        rec("act_quant", lambda name=name: dqt.dqt_act_quant(
-            blk.X[name], blk.act, blk.Xq[name], blk.xdq[name], stream))
+    rec("act_quant", lambda: dqt.dqt_act_quant_batch(blk.act_io, blk.x_t, M, blk.act, stream))
     rec("fwd", lambda: dqt.dqt_linear_fwd_batch(blk.io_all, M, blk.act, blk.y_t, blk.ws, stream))
     rec("bwd_dx", lambda: dqt.dqt_linear_bwd_batch(blk.io_dx, M, blk.act, blk.dy_t, blk.xt,
                                                    blk.dx_t, blk.ws, stream))

@@ -101,14 +101,15 @@ typedef struct {
  *   X:   [M, K], x_t = DQT_F32 or DQT_BF16.   (input)
  *   Xq:  [M, K] int8 or e4m3 bytes.           (output)
  *   xdq: [M] fp32 dequantisation scales.      (output)
- * K must be a multiple of 16.
+ * K must be a multiple of 16; M at most 2^28.
  */
 dqt_status dqt_act_quant(const void* X, int32_t x_t, int64_t M, int32_t K,
                          int32_t act_q, void* Xq, float* xdq, void* stream);
 
 /* Bytes of device workspace dqt_linear_fwd needs for this weight (0 if
- * none): ternary weights are unpacked once per call into d_out * d_in
- * operand bytes.  Depends only on the descriptor. */
+ * none).  Ternary codes feed the matrix cores packed when d_in is a multiple
+ * of 64 (workspace 0); otherwise they are unpacked once per call into
+ * d_out * d_in operand bytes.  Depends only on the descriptor. */
 size_t dqt_linear_fwd_workspace(const dqt_weight* w);
 
 /*
@@ -232,6 +233,19 @@ dqt_status dqt_linear_bwd_batch(int32_t n, const dqt_linear_io* io, int64_t M,
                                 int32_t act_q, int32_t dy_t, int32_t xt_t,
                                 int32_t dx_t, void* ws, size_t ws_bytes,
                                 void* stream);
+
+/* Activation quantisation (see dqt_act_quant) of n inputs with the same M
+ * and dtypes in one launch.  Entry s quantises X [M, K] into Xq and xdq. */
+typedef struct {
+  const void* X;        /* [M, K] input (device)                               */
+  void* Xq;             /* [M, K] codes (device, output)                       */
+  float* xdq;           /* [M] scales (device, output)                         */
+  int32_t K;            /* row length, a multiple of 16                        */
+  int32_t reserved;     /* must be 0                                           */
+} dqt_act_io;
+
+dqt_status dqt_act_quant_batch(int32_t n, const dqt_act_io* io, int32_t x_t,
+                               int64_t M, int32_t act_q, void* stream);
 
 /* Direct SR update of n weight tensors in one launch (see dqt_sr_update);
  * uses w, Wq, dW of each entry.  Each tensor draws from its own stream

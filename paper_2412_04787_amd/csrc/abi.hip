@@ -59,13 +59,31 @@ int32_t dqt_version(void) { return kVersion; }
 
 dqt_status dqt_act_quant(const void* X, int32_t x_t, int64_t M, int32_t K, int32_t act_q,
                          void* Xq, float* xdq, void* stream) {
-  if (M < 0 || K < 16 || (K % 16) != 0) return DQT_ERR_SHAPE;
+  if (M < 0 || M > (int64_t(1) << 28) || K < 16 || (K % 16) != 0) return DQT_ERR_SHAPE;
   if (!is_float_type(x_t) || (act_q != DQT_I8 && act_q != DQT_FP8E4M3)) return DQT_ERR_DTYPE;
   if (M == 0) return DQT_OK;
   if (X == nullptr || Xq == nullptr || xdq == nullptr) return DQT_ERR_NULL;
   if (!aligned16(X) || !aligned16(Xq) || !aligned16(xdq)) return DQT_ERR_ALIGN;
   return from_hip(dqt::launch_act_quant(X, x_t == DQT_BF16, M, K, act_q == DQT_FP8E4M3, Xq, xdq,
                                         static_cast<hipStream_t>(stream)));
+}
+
+dqt_status dqt_act_quant_batch(int32_t n, const dqt_act_io* io, int32_t x_t, int64_t M,
+                               int32_t act_q, void* stream) {
+  if (n < 0 || n > DQT_MAX_BATCH) return DQT_ERR_SHAPE;
+  if (n > 0 && io == nullptr) return DQT_ERR_NULL;
+  if (M < 0 || M > (int64_t(1) << 28)) return DQT_ERR_SHAPE;
+  if (!is_float_type(x_t) || (act_q != DQT_I8 && act_q != DQT_FP8E4M3)) return DQT_ERR_DTYPE;
+  dqt::ActIO a[dqt::kMaxBatch];
+  for (int s = 0; s < n; ++s) {
+    if (io[s].K < 16 || (io[s].K % 16) != 0 || io[s].reserved != 0) return DQT_ERR_SHAPE;
+    if (M > 0 && (io[s].X == nullptr || io[s].Xq == nullptr || io[s].xdq == nullptr)) return DQT_ERR_NULL;
+    if (!aligned16(io[s].X) || !aligned16(io[s].Xq) || !aligned16(io[s].xdq)) return DQT_ERR_ALIGN;
+    a[s] = dqt::ActIO{io[s].X, io[s].Xq, io[s].xdq, io[s].K};
+  }
+  if (M == 0 || n == 0) return DQT_OK;
+  return from_hip(dqt::launch_act_quant_batch(n, a, x_t == DQT_BF16, M, act_q == DQT_FP8E4M3,
+                                              static_cast<hipStream_t>(stream)));
 }
 
 // ----------------------------------------------------------------- batches

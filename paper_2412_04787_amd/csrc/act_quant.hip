@@ -2,12 +2,18 @@
 // are quantised to 8 bits following BitNet): absmax per row, then int8 or
 // OCP e4m3 codes plus one fp32 dequantisation scale per row.
 //
-// HBM-bound: reads the row (2 or 4 B/element) and writes 1 B/element.  One
-// wave per row; the row is read twice (max, then quantise) and the second
-// read is served by the L2/MALL because the wave's row was just streamed.
+// HBM-bound: reads the row (2 or 4 B/element) once and writes 1 B/element.
+// One wave per row.  Rows of up to 64 x 24 16-byte chunks are held in
+// registers between the absmax and the quantisation (the row is read from
+// memory once); longer rows are read twice, the second time from cache.
+// Up to kMaxBatch inputs (same M and dtypes) are quantised by one launch.
 #include "dqt_launch.h"
 
 namespace dqt {
+
+namespace {
+
+typedef int i32x4v __attribute__((ext_vector_type(4)));
 
 template <typename TX>
 struct RowChunk;  // 16-byte chunk of a row: 8 bf16 or 4 fp32 values
@@ -15,102 +21,183 @@ struct RowChunk;  // 16-byte chunk of a row: 8 bf16 or 4 fp32 values
 template <>
 struct RowChunk<uint16_t> {  // bf16 bits
   static constexpr int kElems = 8;
-  __device__ static void load(const uint16_t* p, float (&v)[8]) {
-    const uint4 u = *reinterpret_cast<const uint4*>(p);
-    const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+  __device__ static void decode(i32x4v u, float (&v)[8]) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      v[2 * i] = bf16_bits_to_f32(w[i] & 0xFFFFu);
-      v[2 * i + 1] = bf16_bits_to_f32(w[i] >> 16);
+      v[2 * i] = bf16_bits_to_f32((uint32_t)u[i] & 0xFFFFu);
+      v[2 * i + 1] = bf16_bits_to_f32((uint32_t)u[i] >> 16);
     }
   }
 };
 template <>
 struct RowChunk<float> {
   static constexpr int kElems = 4;
-  __device__ static void load(const float* p, float (&v)[4]) {
-    const f32x4 u = *reinterpret_cast<const f32x4*>(p);
+  __device__ static void decode(i32x4v u, float (&v)[4]) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) v[i] = u[i];
+    for (int i = 0; i < 4; ++i) v[i] = __int_as_float(u[i]);
   }
 };
 
-template <typename TX, bool E4M3>
-__global__ __launch_bounds__(256) void act_quant_kernel(const TX* __restrict__ X, int64_t M, int K,
-                                                        uint8_t* __restrict__ Xq,
-                                                        float* __restrict__ xdq) {
+struct ActTab {
+  const void* X[kMaxBatch];
+  uint8_t* Xq[kMaxBatch];
+  float* xdq[kMaxBatch];
+  int32_t K[kMaxBatch];
+  int32_t b0[kMaxBatch + 1];   // first block of each input (4 rows per block)
+  int32_t n;
+  int64_t M;
+};
+
+constexpr int kRowsPerBlock = 4;
+
+__device__ __forceinline__ int seg_of(const ActTab& t) {
+  int s = 0;
+  while (s + 1 < t.n && (int)blockIdx.x >= t.b0[s + 1]) ++s;
+  return s;
+}
+
+template <bool E4M3, int E>
+__device__ __forceinline__ void quantise_store(const float (&v)[E], float inv, uint8_t* dst) {
+  uint32_t out[E / 4];
+#pragma unroll
+  for (int w = 0; w < E / 4; ++w) {
+    uint32_t word = 0;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float s = v[4 * w + i] * inv;
+      uint32_t b;
+      if constexpr (E4M3) {
+        b = f32_to_e4m3(s);
+      } else {
+        const float r = fminf(fmaxf(rintf(s), -128.0f), 127.0f);
+        b = (uint32_t)(int)r & 0xFFu;
+      }
+      word |= b << (8 * i);
+    }
+    out[w] = word;
+  }
+  if constexpr (E == 8) {
+    *reinterpret_cast<uint2*>(dst) = make_uint2(out[0], out[1]);
+  } else {
+    *reinterpret_cast<uint32_t*>(dst) = out[0];
+  }
+}
+
+// NCH > 0: the lane's chunks lane, lane + 64, ... (at most NCH of them) stay
+// in registers.  NCH == 0: two passes over the row.
+template <typename TX, bool E4M3, int NCH>
+__global__ __launch_bounds__(256) void act_quant_kernel(const ActTab tab) {
   using C = RowChunk<TX>;
   constexpr int E = C::kElems;
+  const int s = seg_of(tab);
   const int lane = threadIdx.x & (kWave - 1);
-  const int64_t row = (int64_t)blockIdx.x * (blockDim.x / kWave) + (threadIdx.x / kWave);
-  if (row >= M) return;
-  const TX* xr = X + row * (int64_t)K;
-  uint8_t* qr = Xq + row * (int64_t)K;
+  const int64_t row = (int64_t)(blockIdx.x - tab.b0[s]) * kRowsPerBlock + (threadIdx.x / kWave);
+  if (row >= tab.M) return;
+  const int K = tab.K[s];
+  const TX* xr = static_cast<const TX*>(tab.X[s]) + row * (int64_t)K;
+  uint8_t* qr = tab.Xq[s] + row * (int64_t)K;
   const int nchunk = K / E;
+  const float qscale = E4M3 ? 448.0f : 127.0f;
 
   float amax = 0.0f;
-  for (int c = lane; c < nchunk; c += kWave) {
-    float v[E];
-    C::load(xr + c * E, v);
+  if constexpr (NCH > 0) {
+    i32x4v raw[NCH];
 #pragma unroll
-    for (int i = 0; i < E; ++i) amax = fmaxf(amax, fabsf(v[i]));
-  }
-  amax = wave_max(amax);
-  const float g = fmaxf(amax, 1e-5f);
-  const float qscale = E4M3 ? 448.0f : 127.0f;
-  const float inv = qscale / g;   // correctly rounded fp32 division
-  if (lane == 0) xdq[row] = g / qscale;
-
-  for (int c = lane; c < nchunk; c += kWave) {
-    float v[E];
-    C::load(xr + c * E, v);
-    uint32_t out[E / 4];
+    for (int c = 0; c < NCH; ++c) {
+      const int idx = lane + kWave * c;
+      if (idx < nchunk) {
+        raw[c] = __builtin_nontemporal_load(reinterpret_cast<const i32x4v*>(xr + idx * E));
+        float v[E];
+        C::decode(raw[c], v);
 #pragma unroll
-    for (int w = 0; w < E / 4; ++w) {
-      uint32_t word = 0;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const float s = v[4 * w + i] * inv;
-        uint32_t b;
-        if constexpr (E4M3) {
-          b = f32_to_e4m3(s);
-        } else {
-          const float r = fminf(fmaxf(rintf(s), -128.0f), 127.0f);
-          b = (uint32_t)(int)r & 0xFFu;
-        }
-        word |= b << (8 * i);
+        for (int i = 0; i < E; ++i) amax = fmaxf(amax, fabsf(v[i]));
       }
-      out[w] = word;
     }
-    if constexpr (E == 8) {
-      *reinterpret_cast<uint2*>(qr + c * E) = make_uint2(out[0], out[1]);
-    } else {
-      *reinterpret_cast<uint32_t*>(qr + c * E) = out[0];
+    amax = wave_max(amax);
+    const float g = fmaxf(amax, 1e-5f);
+    const float inv = qscale / g;   // correctly rounded fp32 division
+    if (lane == 0) tab.xdq[s][row] = g / qscale;
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+      const int idx = lane + kWave * c;
+      if (idx < nchunk) {
+        float v[E];
+        C::decode(raw[c], v);
+        quantise_store<E4M3, E>(v, inv, qr + idx * E);
+      }
+    }
+  } else {
+    for (int c = lane; c < nchunk; c += kWave) {
+      float v[E];
+      C::decode(*reinterpret_cast<const i32x4v*>(xr + c * E), v);
+#pragma unroll
+      for (int i = 0; i < E; ++i) amax = fmaxf(amax, fabsf(v[i]));
+    }
+    amax = wave_max(amax);
+    const float g = fmaxf(amax, 1e-5f);
+    const float inv = qscale / g;
+    if (lane == 0) tab.xdq[s][row] = g / qscale;
+    for (int c = lane; c < nchunk; c += kWave) {
+      float v[E];
+      C::decode(*reinterpret_cast<const i32x4v*>(xr + c * E), v);
+      quantise_store<E4M3, E>(v, inv, qr + c * E);
     }
   }
 }
 
-hipError_t launch_act_quant(const void* X, bool x_bf16, int64_t M, int K, bool e4m3, void* Xq,
-                            float* xdq, hipStream_t stream) {
-  if (M == 0) return hipSuccess;
-  const int rows_per_block = 4;
-  const dim3 grid((unsigned)((M + rows_per_block - 1) / rows_per_block));
-  const dim3 block(rows_per_block * kWave);
-  uint8_t* q = static_cast<uint8_t*>(Xq);
+template <typename TX, bool E4M3>
+void launch_t(const ActTab& tab, int nch, int32_t blocks, hipStream_t stream) {
+  const dim3 grid((unsigned)blocks), block(kRowsPerBlock * kWave);
+  switch (nch) {
+    case 1: hipLaunchKernelGGL((act_quant_kernel<TX, E4M3, 1>), grid, block, 0, stream, tab); break;
+    case 2: hipLaunchKernelGGL((act_quant_kernel<TX, E4M3, 2>), grid, block, 0, stream, tab); break;
+    case 4: hipLaunchKernelGGL((act_quant_kernel<TX, E4M3, 4>), grid, block, 0, stream, tab); break;
+    case 8: hipLaunchKernelGGL((act_quant_kernel<TX, E4M3, 8>), grid, block, 0, stream, tab); break;
+    case 16: hipLaunchKernelGGL((act_quant_kernel<TX, E4M3, 16>), grid, block, 0, stream, tab); break;
+    case 24: hipLaunchKernelGGL((act_quant_kernel<TX, E4M3, 24>), grid, block, 0, stream, tab); break;
+    default: hipLaunchKernelGGL((act_quant_kernel<TX, E4M3, 0>), grid, block, 0, stream, tab); break;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_act_quant_batch(int n, const ActIO* io, bool x_bf16, int64_t M, bool e4m3,
+                                  hipStream_t stream) {
+  if (M == 0 || n == 0) return hipSuccess;
+  ActTab tab{};
+  tab.n = n;
+  tab.M = M;
+  const int E = x_bf16 ? 8 : 4;
+  int32_t blocks = 0;
+  int max_per_lane = 0;
+  for (int s = 0; s < n; ++s) {
+    tab.X[s] = io[s].X;
+    tab.Xq[s] = static_cast<uint8_t*>(io[s].Xq);
+    tab.xdq[s] = io[s].xdq;
+    tab.K[s] = io[s].K;
+    tab.b0[s] = blocks;
+    blocks += (int32_t)((M + kRowsPerBlock - 1) / kRowsPerBlock);
+    const int per_lane = (io[s].K / E + kWave - 1) / kWave;
+    max_per_lane = per_lane > max_per_lane ? per_lane : max_per_lane;
+  }
+  tab.b0[n] = blocks;
+  int nch = 0;
+  for (int c : {1, 2, 4, 8, 16, 24})
+    if (max_per_lane <= c) { nch = c; break; }
   if (x_bf16) {
-    const uint16_t* x = static_cast<const uint16_t*>(X);
-    if (e4m3)
-      hipLaunchKernelGGL((act_quant_kernel<uint16_t, true>), grid, block, 0, stream, x, M, K, q, xdq);
-    else
-      hipLaunchKernelGGL((act_quant_kernel<uint16_t, false>), grid, block, 0, stream, x, M, K, q, xdq);
+    if (e4m3) launch_t<uint16_t, true>(tab, nch, blocks, stream);
+    else launch_t<uint16_t, false>(tab, nch, blocks, stream);
   } else {
-    const float* x = static_cast<const float*>(X);
-    if (e4m3)
-      hipLaunchKernelGGL((act_quant_kernel<float, true>), grid, block, 0, stream, x, M, K, q, xdq);
-    else
-      hipLaunchKernelGGL((act_quant_kernel<float, false>), grid, block, 0, stream, x, M, K, q, xdq);
+    if (e4m3) launch_t<float, true>(tab, nch, blocks, stream);
+    else launch_t<float, false>(tab, nch, blocks, stream);
   }
   return hipGetLastError();
+}
+
+hipError_t launch_act_quant(const void* X, bool x_bf16, int64_t M, int K, bool e4m3, void* Xq,
+                            float* xdq, hipStream_t stream) {
+  const ActIO io{X, Xq, xdq, K};
+  return launch_act_quant_batch(1, &io, x_bf16, M, e4m3, stream);
 }
 
 }  // namespace dqt

@@ -30,6 +30,15 @@ struct DwArgs {
 
 hipError_t launch_act_quant(const void* X, bool x_bf16, int64_t M, int K, bool e4m3, void* Xq,
                             float* xdq, hipStream_t stream);
+// up to kMaxBatch inputs with the same M and dtypes in one launch
+struct ActIO {
+  const void* X;        // [M, K]
+  void* Xq;             // [M, K] codes
+  float* xdq;           // [M]
+  int K;
+};
+hipError_t launch_act_quant_batch(int n, const ActIO* io, bool x_bf16, int64_t M, bool e4m3,
+                                  hipStream_t stream);
 // int8 / e4m3 / bf16 matrix-core kernels, batched: up to kMaxBatch linears
 // (same dtypes, same token count M) per launch.
 constexpr int kMaxBatch = 8;

@@ -50,14 +50,20 @@ constexpr int TILE = 256;             // block tile edge (outputs)
 constexpr int WI = 4, WJ = 2;         // MFMA 32x32 blocks per wave
 constexpr int KBYTES = 128;           // reduction bytes per tile row per step
 constexpr int OPB = TILE * KBYTES;    // bytes per operand per stage (32 KB)
-constexpr int SLOT = 2 * OPB;         // bytes per stage (64 KB)
 constexpr int NL = OPB / 16 / NTH;    // DMA instructions per thread per operand per stage
 constexpr int PITCH = 68;             // fp32 words per staged epilogue row (64 + 4)
+constexpr int PKB = 32;               // packed ternary bytes per tile row per step (128 codes)
 static_assert(NL == 4, "DMA plan assumes 4 chunks per thread");
-static_assert(NW * 16 * PITCH * 4 <= SLOT, "epilogue staging fits in one stage");
+static_assert(TILE * 2 == NTH, "packed plan: one 16-byte chunk per thread");
+static_assert(NW * 16 * PITCH * 4 <= OPB + TILE * PKB, "epilogue staging fits in one stage");
 
 enum Elem { EI8 = 0, EF8 = 1, EBF16 = 2 };
-enum Mode { KC = 0, KM = 1 };
+enum Mode { KC = 0, KM = 1, KCP = 2 };   // KCP: K-contiguous packed ternary codes (B only)
+
+// bytes per stage: A, then B (bf16 / 8-bit operand, or packed ternary codes)
+template <int MB>
+constexpr int slot_bytes() { return OPB + (MB == KCP ? TILE * PKB : OPB); }
+
 
 // Global operand: base of element (row 0, reduction 0), row stride in bytes,
 // extent of the tile dimension.
@@ -83,8 +89,13 @@ struct Group {
   int32_t ng;
 };
 
-__device__ __forceinline__ void tr_wait2(u32x2& a, u32x2& b) {
-  asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(a), "+v"(b));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+// Transposing LDS read: each lane receives four 16-bit values of one column
+// from four consecutive rows of a row-major tile (ds_read_b64_tr_b16).
+__device__ __forceinline__ u32x2 tr_read(const lds_u8* base, int off) {
+  const s16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (__attribute__((address_space(3))) s16x4*)(base + off));
+  return __builtin_bit_cast(u32x2, v);
 }
 __device__ __forceinline__ i32x4 join(u32x2 lo, u32x2 hi) {
   return i32x4{(int)lo[0], (int)lo[1], (int)hi[0], (int)hi[1]};
@@ -95,12 +106,28 @@ __device__ __forceinline__ i32x4 join(u32x2 lo, u32x2 hi) {
 // not wait for all outstanding DMA before every later LDS access; the
 // kernel waits for its DMA explicitly (vmcnt) before the barrier that
 // publishes a stage.  Nothing else in these kernels uses M0.
+// 16 packed ternary codes (code q + 1 at bits 2k, 2k+1) -> 16 operand bytes
+// in k order, via the byte lookup `lut` (code 0, 1, 2 -> lut bytes 0, 1, 2):
+// split the four codes of every byte into four byte planes, transpose the
+// 4 x 4 byte matrix, then look each code up.
+__device__ __forceinline__ i32x4 expand16(uint32_t x, uint32_t lut) {
+  const uint32_t e = x & 0x03030303u, f = (x >> 2) & 0x03030303u;
+  const uint32_t g = (x >> 4) & 0x03030303u, h = (x >> 6) & 0x03030303u;
+  const uint32_t efl = __builtin_amdgcn_perm(f, e, 0x05010400u), efh = __builtin_amdgcn_perm(f, e, 0x07030602u);
+  const uint32_t ghl = __builtin_amdgcn_perm(h, g, 0x05010400u), ghh = __builtin_amdgcn_perm(h, g, 0x07030602u);
+  const uint32_t d0 = __builtin_amdgcn_perm(ghl, efl, 0x05040100u), d1 = __builtin_amdgcn_perm(ghl, efl, 0x07060302u);
+  const uint32_t d2 = __builtin_amdgcn_perm(ghh, efh, 0x05040100u), d3 = __builtin_amdgcn_perm(ghh, efh, 0x07060302u);
+  return i32x4{(int)__builtin_amdgcn_perm(0u, lut, d0), (int)__builtin_amdgcn_perm(0u, lut, d1),
+               (int)__builtin_amdgcn_perm(0u, lut, d2), (int)__builtin_amdgcn_perm(0u, lut, d3)};
+}
 __device__ __forceinline__ void dma16(const uint8_t* g, lds_u8* l) {
   const uint32_t m0 = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)l);
   asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" : : "v"(g), "s"(m0) : "memory");
 }
-__device__ __forceinline__ void wait_vm0() {
-  __builtin_amdgcn_s_waitcnt((0) | (0 << 14) | (7 << 4) | (15 << 8));
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
 // Barrier that keeps the compiler from moving memory accesses across it; it
 // waits for this wave's LDS accesses but not for outstanding DMA.
@@ -127,7 +154,16 @@ struct Plan {
 #pragma unroll
     for (int q = 0; q < NL; ++q) {
       const int p = q * NTH + tid;                  // physical 16-byte position
-      if constexpr (MODE == KC) {
+      if constexpr (MODE == KCP) {
+        if (q > 0) break;                           // one chunk per thread
+        const int row = p >> 1;
+        const int c = (p & 1) ^ ((row >> 3) & 1);   // logical 16-byte chunk (64 codes)
+        int64_t gr = row0 + row;
+        if (gr > o.n - 1) gr = o.n - 1;
+        g[q] = o.p + gr * o.ld + r_begin / 4 + 16 * c;
+        back = r_begin / 4 + 16 * c;
+        rk = 64 * c;
+      } else if constexpr (MODE == KC) {
         const int row = p >> 3;
         const int c = (p & 7) ^ ((row >> 1) & 7);   // logical chunk (same for every q)
         int64_t gr = row0 + row;
@@ -147,7 +183,7 @@ struct Plan {
         rk = k;
       }
     }
-    inc = MODE == KC ? KBYTES : 64 * o.ld;
+    inc = MODE == KC ? KBYTES : MODE == KCP ? PKB : 64 * o.ld;
   }
 };
 
@@ -171,7 +207,12 @@ template <int ELEM, int MA, int MB, class Epi>
 __global__ __launch_bounds__(NTH) void gemm_v3_kernel(const Group<Epi> grp) {
   constexpr int EB = ELEM == EBF16 ? 2 : 1;
   constexpr int BK = KBYTES / EB;           // reduction elements per step
-  __shared__ __attribute__((aligned(1024))) uint8_t smem_generic[2 * SLOT];
+  constexpr int SLOTB = slot_bytes<MB>();
+  constexpr int NLB = MB == KCP ? 1 : NL;  // DMA chunks per thread for B
+  // as many stages as fit next to the row scales: 3 with packed B, else 2
+  constexpr int NS = 3 * SLOTB + TILE * 4 <= 160 * 1024 ? 3 : 2;
+  constexpr int LPS = NL + NLB;            // DMA instructions per thread per stage
+  __shared__ __attribute__((aligned(1024))) uint8_t smem_generic[NS * SLOTB];
   __shared__ float row_scale[Epi::kRowScale ? TILE : 1];
   lds_u8* smem = (lds_u8*)smem_generic;
 
@@ -223,33 +264,34 @@ __global__ __launch_bounds__(NTH) void gemm_v3_kernel(const Group<Epi> grp) {
 
   // DMA of step s of the current plans into stage `slot`.
   auto issue = [&](int s, int slot, const TileState& T) {
-    lds_u8* la = smem + slot * SLOT + wave_u * 1024;
+    lds_u8* la = smem + slot * SLOTB + wave_u * 1024;
     lds_u8* lb = la + OPB;
     if (!(T.tail && s == T.nsteps - 1)) {
 #pragma unroll
       for (int q = 0; q < NL; ++q) dma16(pa.g[q] + (int64_t)s * pa.inc, la + q * (NTH * 16));
 #pragma unroll
-      for (int q = 0; q < NL; ++q) dma16(pb.g[q] + (int64_t)s * pb.inc, lb + q * (NTH * 16));
+      for (int q = 0; q < NLB; ++q) dma16(pb.g[q] + (int64_t)s * pb.inc, lb + q * (NTH * 16));
     } else {
       const int64_t rbase = (int64_t)s * BK;
       const bool oa = rbase + pa.rk >= T.rlen, ob = rbase + pb.rk >= T.rlen;
 #pragma unroll
       for (int q = 0; q < NL; ++q) dma16(oa ? pa.g[q] - pa.back : pa.g[q] + (int64_t)s * pa.inc, la + q * (NTH * 16));
 #pragma unroll
-      for (int q = 0; q < NL; ++q) dma16(ob ? pb.g[q] - pb.back : pb.g[q] + (int64_t)s * pb.inc, lb + q * (NTH * 16));
+      for (int q = 0; q < NLB; ++q) dma16(ob ? pb.g[q] - pb.back : pb.g[q] + (int64_t)s * pb.inc, lb + q * (NTH * 16));
     }
   };
   // zero the chunks this thread loaded past the end of the reduction (its
   // own DMA for that stage has completed)
+  // (packed B codes past the end need no zeroing: they meet zeroed A)
   auto zero_tail = [&](int s, int slot, const TileState& T) {
-    lds_u8* la = smem + slot * SLOT;
+    lds_u8* la = smem + slot * SLOTB;
     lds_u8* lb = la + OPB;
     const int64_t rbase = (int64_t)s * BK;
     const i32x4 z = {0, 0, 0, 0};
     if (rbase + pa.rk >= T.rlen)
 #pragma unroll
       for (int q = 0; q < NL; ++q) *(__attribute__((address_space(3))) i32x4*)(la + (q * NTH + tid) * 16) = z;
-    if (rbase + pb.rk >= T.rlen)
+    if (MB != KCP && rbase + pb.rk >= T.rlen)
 #pragma unroll
       for (int q = 0; q < NL; ++q) *(__attribute__((address_space(3))) i32x4*)(lb + (q * NTH + tid) * 16) = z;
   };
@@ -267,6 +309,7 @@ __global__ __launch_bounds__(NTH) void gemm_v3_kernel(const Group<Epi> grp) {
   struct Frags {
     i32x4 fa[WI], fb[WJ];
     u32x2 ka[WI][2], kb[WJ][2];
+    uint32_t pb[WJ];          // packed codes (16 per lane), expanded at use
   };
   auto read_frags = [&](const lds_u8* la, const lds_u8* lb, int kk, Frags& F) {
 #pragma unroll
@@ -278,40 +321,36 @@ __global__ __launch_bounds__(NTH) void gemm_v3_kernel(const Group<Epi> grp) {
       } else {
         const int col = wi * 32 * WI + t * 32 + 16 * ch + 4 * u4;
         const int seg = ((col & 63) >> 4) ^ t4;
-        const uint32_t a0 = (uint32_t)(uintptr_t)(la + (col >> 6) * 8192 + (16 * kk + 8 * h + t4) * 128 +
-                                                  32 * seg + 8 * u4);
-        asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(F.ka[t][0]) : "v"(a0));
-        asm volatile("ds_read_b64_tr_b16 %0, %1 offset:512" : "=v"(F.ka[t][1]) : "v"(a0));
+        const int a0 = (col >> 6) * 8192 + (16 * kk + 8 * h + t4) * 128 + 32 * seg + 8 * u4;
+        F.ka[t][0] = tr_read(la, a0);
+        F.ka[t][1] = tr_read(la, a0 + 512);
       }
     }
 #pragma unroll
     for (int t = 0; t < WJ; ++t) {
-      if constexpr (MB == KC) {
+      if constexpr (MB == KCP) {
+        const int row = wj * 32 * WJ + t * 32 + frow;
+        const int w = 2 * kk + h;                  // 4-byte word of the row's 32 bytes
+        const int pos = 4 * ((w >> 2) ^ ((row >> 3) & 1)) + (w & 3);
+        F.pb[t] = *(const __attribute__((address_space(3))) uint32_t*)(lb + row * PKB + 4 * pos);
+      } else if constexpr (MB == KC) {
         const int row = wj * 32 * WJ + t * 32 + frow;
         const int c = (2 * kk + h) ^ ((row >> 1) & 7);
         F.fb[t] = *(const __attribute__((address_space(3))) i32x4*)(lb + row * KBYTES + 16 * c);
       } else {
         const int col = wj * 32 * WJ + t * 32 + 16 * ch + 4 * u4;
         const int seg = ((col & 63) >> 4) ^ t4;
-        const uint32_t a0 = (uint32_t)(uintptr_t)(lb + (col >> 6) * 8192 + (16 * kk + 8 * h + t4) * 128 +
-                                                  32 * seg + 8 * u4);
-        asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(F.kb[t][0]) : "v"(a0));
-        asm volatile("ds_read_b64_tr_b16 %0, %1 offset:512" : "=v"(F.kb[t][1]) : "v"(a0));
+        const int a0 = (col >> 6) * 8192 + (16 * kk + 8 * h + t4) * 128 + 32 * seg + 8 * u4;
+        F.kb[t][0] = tr_read(lb, a0);
+        F.kb[t][1] = tr_read(lb, a0 + 512);
       }
     }
   };
-  auto frag_wait = [&](Frags& F) {
-    if constexpr (MA == KM) {
-#pragma unroll
-      for (int t = 0; t < WI; ++t) tr_wait2(F.ka[t][0], F.ka[t][1]);
-    }
-    if constexpr (MB == KM) {
-#pragma unroll
-      for (int t = 0; t < WJ; ++t) tr_wait2(F.kb[t][0], F.kb[t][1]);
-    }
-  };
   auto opa = [&](const Frags& F, int t) { return MA == KC ? F.fa[t] : join(F.ka[t][0], F.ka[t][1]); };
-  auto opb = [&](const Frags& F, int t) { return MB == KC ? F.fb[t] : join(F.kb[t][0], F.kb[t][1]); };
+  auto opb = [&](const Frags& F, int t) {
+    if constexpr (MB == KCP) return expand16(F.pb[t], ELEM == EF8 ? 0x003800B8u : 0x000100FFu);
+    else return MB == KC ? F.fb[t] : join(F.kb[t][0], F.kb[t][1]);
+  };
   // MFMAs of one sub-step (int8 / bf16), or of two sub-steps (e4m3, whose
   // instruction reduces 64 elements: sub-step pairs (0, 1) and (2, 3)).
   auto mfma1 = [&](const Frags& F) {
@@ -339,34 +378,42 @@ __global__ __launch_bounds__(NTH) void gemm_v3_kernel(const Group<Epi> grp) {
         acc[ta][tb] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(av, bv, acc[ta][tb], 0, 0, 0, 127, 0, 127);
       }
   };
-  // One step from stage `slot`: sub-step kk+1's fragments load while kk's
-  // MFMAs run.
-  auto compute = [&](int slot) {
-    const lds_u8* la = smem + slot * SLOT;
-    const lds_u8* lb = la + OPB;
-    Frags F0, F1, F2, F3;
-    read_frags(la, lb, 0, F0);
-    frag_wait(F0);
-    read_frags(la, lb, 1, F1);
-    if constexpr (ELEM != EF8) mfma1(F0);
-    frag_wait(F1);
-    read_frags(la, lb, 2, F2);
-    if constexpr (ELEM != EF8) mfma1(F1);
-    else mfma2(F0, F1);
-    frag_wait(F2);
-    read_frags(la, lb, 3, F3);
-    if constexpr (ELEM != EF8) mfma1(F2);
-    frag_wait(F3);
-    if constexpr (ELEM != EF8) mfma1(F3);
-    else mfma2(F2, F3);
-  };
+  auto stage_ptr = [&](int slot) { return smem + slot * SLOTB; };
 
   // ---- persistent loop over this block's tiles
   int g0, local0;
   if (!locate(grp, xcd, kb, g0, local0)) return;
   setup(g0, local0, cur);
-  int slot0 = 0;                         // stage of the current tile's step 0
-  if (cur.nsteps > 0) issue(0, slot0, cur);
+  // Stage of step s of the current tile: (slot0 + s) mod NS.  Before a tile
+  // starts, its steps 0 .. NS-2 are in flight.
+  int slot0 = 0;
+  for (int s = 0; s < NS - 1 && s < cur.nsteps; ++s) issue(s, s, cur);
+
+  // One step from stage `slot`: sub-step kk+1's fragments load while kk's
+  // MFMAs run (e4m3: sub-steps are consumed in pairs).
+  auto compute = [&](int slot) {
+    const lds_u8* la = stage_ptr(slot);
+    const lds_u8* lb = la + OPB;
+    Frags F0, F1;
+    if constexpr (ELEM != EF8) {
+      read_frags(la, lb, 0, F0);
+      read_frags(la, lb, 1, F1);
+      mfma1(F0);
+      read_frags(la, lb, 2, F0);
+      mfma1(F1);
+      read_frags(la, lb, 3, F1);
+      mfma1(F0);
+      mfma1(F1);
+    } else {
+      Frags F2, F3;
+      read_frags(la, lb, 0, F0);
+      read_frags(la, lb, 1, F1);
+      read_frags(la, lb, 2, F2);
+      mfma2(F0, F1);
+      read_frags(la, lb, 3, F3);
+      mfma2(F2, F3);
+    }
+  };
 
   for (int j = kb;;) {
 #pragma unroll
@@ -376,14 +423,17 @@ __global__ __launch_bounds__(NTH) void gemm_v3_kernel(const Group<Epi> grp) {
 #pragma unroll
         for (int r = 0; r < 16; ++r) acc[a][b][r] = 0;
 
-    // main loop: step it computes from stage (slot0 + it) & 1 while step
-    // it + 1 loads into the other stage
+    // main loop: step it computes from stage (slot0 + it) mod NS while the
+    // next NS - 1 steps load into the other stages.  The first step of a
+    // tile waits for every load and store of this thread (the previous
+    // epilogue's stores were issued after this tile's first stages).
     for (int it = 0; it < cur.nsteps; ++it) {
-      const int slot = (slot0 + it) & 1;
-      wait_vm0();
+      const int slot = (slot0 + it) % NS;
+      if (NS == 2 || it == 0 || it + 1 == cur.nsteps) wait_vm<0>();
+      else wait_vm<LPS>();             // step it + 1 may still be in flight
       if (cur.tail && it == cur.nsteps - 1) zero_tail(it, slot, cur);
-      block_barrier();                 // stage `slot` complete; the other stage is free
-      if (it + 1 < cur.nsteps) issue(it + 1, slot ^ 1, cur);
+      block_barrier();                 // stage `slot` complete; step it - 1's stage is free
+      if (it + NS - 1 < cur.nsteps) issue(it + NS - 1, (slot + NS - 1) % NS, cur);
       compute(slot);
     }
 
@@ -393,18 +443,18 @@ __global__ __launch_bounds__(NTH) void gemm_v3_kernel(const Group<Epi> grp) {
     const int64_t I = P.I, J = P.J;
     const int64_t i0 = cur.i0, j0 = cur.j0;
     const int bz = cur.bz;
-    const int last = (slot0 + cur.nsteps + 1) & 1;   // stage of the last step (staging area)
+    const int last = (slot0 + cur.nsteps + NS - 1) % NS;   // stage of the last step (staging area)
     if constexpr (Epi::kRowScale) {
       if (tid < TILE) row_scale[tid] = epi.scale_fin(my_scale);
     }
-    block_barrier();                   // every wave is done with both stages
+    block_barrier();                   // every wave is done with every stage
     const int jn = j + nbx8;
     int gn, localn;
     const bool more = locate(grp, xcd, jn, gn, localn);
     if (more) {
-      const int slotn = (slot0 + cur.nsteps) & 1;
+      const int slotn = (last + 1) % NS;      // the next tile's stages avoid `last`
       setup(gn, localn, cur);
-      if (cur.nsteps > 0) issue(0, slotn, cur);
+      for (int s = 0; s < NS - 1 && s < cur.nsteps; ++s) issue(s, (slotn + s) % NS, cur);
       slot0 = slotn;
     }
 
@@ -412,7 +462,7 @@ __global__ __launch_bounds__(NTH) void gemm_v3_kernel(const Group<Epi> grp) {
     // 8 (r / 4) + 4 h + (r mod 4), r = 0..15.  Each wave stages 16 of its
     // rows at a time as fp32 in its own part of stage `last`, then writes
     // whole 16-byte chunks of output rows (8 bf16 or 4 fp32).
-    lds_u8* stage = smem + last * SLOT + wave * (16 * PITCH * 4);
+    lds_u8* stage = smem + last * SLOTB + wave * (16 * PITCH * 4);
     const bool obf = epi.out_bf16();
 #pragma unroll
     for (int ta = 0; ta < WI; ++ta) {
@@ -578,6 +628,33 @@ __global__ __launch_bounds__(256) void dequant_act_kernel(const SegTab tab) {
   dst[1] = make_uint4(o[4], o[5], o[6], o[7]);
 }
 
+// dW[l] = sum over splits of the fp32 partials of linear l, in split order
+// (deterministic), for every linear of a batch in one launch.
+struct RedTab {
+  const float* src[MAXG];     // [splits][n] partials
+  float* dst[MAXG];           // [n]
+  int64_t n4[MAXG];           // n / 4
+  int32_t b0[MAXG + 1];
+  int32_t n, splits;
+};
+__global__ __launch_bounds__(256) void split_reduce_batch_kernel(const RedTab tab) {
+  int s = 0;
+  while (s + 1 < tab.n && (int)blockIdx.x >= tab.b0[s + 1]) ++s;
+  const int64_t t = (int64_t)(blockIdx.x - tab.b0[s]) * 256 + threadIdx.x;
+  const int64_t n4 = tab.n4[s];
+  if (t >= n4) return;
+  const f32x4* src = reinterpret_cast<const f32x4*>(tab.src[s]);
+  f32x4 acc = __builtin_nontemporal_load(src + t);
+  for (int k = 1; k < tab.splits; ++k) {
+    const f32x4 v = __builtin_nontemporal_load(src + (int64_t)k * n4 + t);
+    acc[0] = acc[0] + v[0];
+    acc[1] = acc[1] + v[1];
+    acc[2] = acc[2] + v[2];
+    acc[3] = acc[3] + v[3];
+  }
+  reinterpret_cast<f32x4*>(tab.dst[s])[t] = acc;
+}
+
 static int32_t seal(SegTab& t) {
   int32_t b = 0;
   for (int s = 0; s < t.n; ++s) {
@@ -635,11 +712,21 @@ using namespace v3;
 
 static size_t align256(size_t n) { return (n + 255) / 256 * 256; }
 
+// Ternary weights reach the forward GEMM as packed codes when every d_in of
+// the batch is a multiple of 64 (16-byte aligned packed rows); otherwise
+// they are first unpacked into the workspace.
+static bool fwd_packed(int n, const LinearIO* io) {
+  for (int l = 0; l < n; ++l)
+    if (io[l].d_in % 64 != 0) return false;
+  return true;
+}
+
 size_t fwd_batch_workspace(int n, const LinearIO* io, bool ternary, size_t* offs) {
   size_t total = 0;
+  const bool unpack = ternary && !fwd_packed(n, io);
   for (int l = 0; l < n; ++l) {
     if (offs) offs[l] = total;
-    if (ternary) total += align256((size_t)(io[l].d_out * io[l].d_in));
+    if (unpack) total += align256((size_t)(io[l].d_out * io[l].d_in));
   }
   return total;
 }
@@ -648,7 +735,8 @@ hipError_t launch_fwd_batch(const BatchCfg& c, const LinearIO* io, uint8_t* ws, 
   if (c.M == 0 || c.n == 0) return hipSuccess;
   size_t offs[kMaxBatch];
   fwd_batch_workspace(c.n, io, c.w_ternary, offs);
-  if (c.w_ternary) {
+  const bool packed = c.w_ternary && fwd_packed(c.n, io);
+  if (c.w_ternary && !packed) {
     SegTab tab{};
     tab.n = c.n;
     for (int l = 0; l < c.n; ++l) {
@@ -666,9 +754,13 @@ hipError_t launch_fwd_batch(const BatchCfg& c, const LinearIO* io, uint8_t* ws, 
   grp.ng = c.n;
   for (int l = 0; l < c.n; ++l) {
     Prob<EpiFwd>& p = grp.p[l];
-    const uint8_t* rows = c.w_ternary ? ws + offs[l] : static_cast<const uint8_t*>(io[l].Wq);
     p.A = Opnd{static_cast<const uint8_t*>(io[l].Xq), io[l].d_in, c.M};
-    p.B = Opnd{rows, io[l].d_in, io[l].d_out};
+    if (packed)
+      p.B = Opnd{static_cast<const uint8_t*>(io[l].Wq), io[l].d_in / 4, io[l].d_out};
+    else if (c.w_ternary)
+      p.B = Opnd{ws + offs[l], io[l].d_in, io[l].d_out};
+    else
+      p.B = Opnd{static_cast<const uint8_t*>(io[l].Wq), io[l].d_in, io[l].d_out};
     p.epi = EpiFwd{io[l].Y, io[l].d_out, c.out_bf16, io[l].xdq, io[l].alpha};
     p.I = c.M;
     p.J = io[l].d_out;
@@ -676,8 +768,13 @@ hipError_t launch_fwd_batch(const BatchCfg& c, const LinearIO* io, uint8_t* ws, 
     p.split_len = io[l].d_in;
     p.nbz = 1;
   }
-  if (c.act_e4m3) launch_group<EF8, KC, KC>(grp, stream);
-  else launch_group<EI8, KC, KC>(grp, stream);
+  if (packed) {
+    if (c.act_e4m3) launch_group<EF8, KC, KCP>(grp, stream);
+    else launch_group<EI8, KC, KCP>(grp, stream);
+  } else {
+    if (c.act_e4m3) launch_group<EF8, KC, KC>(grp, stream);
+    else launch_group<EI8, KC, KC>(grp, stream);
+  }
   return hipGetLastError();
 }
 
@@ -806,10 +903,20 @@ hipError_t launch_dw_batch(const BatchCfg& c, const LinearIO* io, uint8_t* ws, c
   launch_group<EBF16, KM, KM>(grp, stream);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || splits == 1) return e;
-  for (int l = 0; l < c.n && e == hipSuccess; ++l)
-    e = launch_split_reduce(reinterpret_cast<const float*>(ws + P.part_off[l]), (int)splits,
-                            io[l].d_out * io[l].d_in, io[l].dW, stream);
-  return e;
+  RedTab red{};
+  red.n = c.n;
+  red.splits = (int32_t)splits;
+  int32_t blocks = 0;
+  for (int l = 0; l < c.n; ++l) {
+    red.src[l] = reinterpret_cast<const float*>(ws + P.part_off[l]);
+    red.dst[l] = io[l].dW;
+    red.n4[l] = io[l].d_out * io[l].d_in / 4;
+    red.b0[l] = blocks;
+    blocks += (int32_t)((red.n4[l] + 255) / 256);
+  }
+  red.b0[c.n] = blocks;
+  hipLaunchKernelGGL(split_reduce_batch_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, red);
+  return hipGetLastError();
 }
 
 }  // namespace dqt

@@ -21,7 +21,7 @@ DQT_ERR_RANGE, DQT_ERR_WORKSPACE, DQT_ERR_UNSUPPORTED, DQT_ERR_HIP = 5, 6, 7, 8
 DQT_F32, DQT_BF16, DQT_I8, DQT_FP8E4M3, DQT_TERNARY2 = 0, 1, 2, 3, 4
 
 EXPORTS = (
-    "dqt_act_quant", "dqt_linear_fwd_workspace", "dqt_linear_fwd", "dqt_linear_bwd_workspace",
+    "dqt_act_quant", "dqt_act_quant_batch", "dqt_linear_fwd_workspace", "dqt_linear_fwd", "dqt_linear_bwd_workspace",
     "dqt_linear_bwd", "dqt_linear_fwd_batch_workspace", "dqt_linear_fwd_batch",
     "dqt_linear_bwd_batch_workspace", "dqt_linear_bwd_batch", "dqt_sr_update_batch",
     "dqt_sr_update", "dqt_debug_rng", "dqt_absmean_init", "dqt_pack_ternary",
@@ -48,6 +48,11 @@ class DqtLinearIO(ctypes.Structure):
     ]
 
 
+class DqtActIO(ctypes.Structure):
+    _fields_ = [("X", ctypes.c_void_p), ("Xq", ctypes.c_void_p), ("xdq", ctypes.c_void_p),
+                ("K", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+
+
 def weight(d_out: int, d_in: int, wfmt: int, qmin: int, qmax: int, alpha: float,
            tensor_id: int = 0) -> DqtWeight:
     return DqtWeight(d_out, d_in, wfmt, qmin, qmax, float(alpha), tensor_id, 0)
@@ -67,6 +72,7 @@ _wp = ctypes.POINTER(DqtWeight)
 
 _SIGS = {
     "dqt_act_quant": (_i32, [_vp, _i32, _i64, _i32, _i32, _vp, _vp, _vp]),
+    "dqt_act_quant_batch": (_i32, [_i32, _vp, _i32, _i64, _i32, _vp]),
     "dqt_linear_fwd_workspace": (ctypes.c_size_t, [_wp]),
     "dqt_linear_fwd": (_i32, [_wp, _vp, _vp, _i32, _i64, _i32, _vp, _vp, _vp, _i32, _vp,
                               ctypes.c_size_t, _vp]),
@@ -215,6 +221,24 @@ def linear_io(entries):
             setattr(arr[k], f, None if t is None else t.data_ptr())
     arr._keep = keep
     return arr
+
+
+def act_io(entries):
+    """entries: list of (X, Xq, xdq) tensors with X [M, K].  Returns a ctypes
+    array of dqt_act_io."""
+    arr = (DqtActIO * len(entries))()
+    for k, (X, Xq, xdq) in enumerate(entries):
+        arr[k].X = X.data_ptr()
+        arr[k].Xq = Xq.data_ptr()
+        arr[k].xdq = xdq.data_ptr()
+        arr[k].K = X.shape[1]
+        arr[k].reserved = 0
+    return arr
+
+
+def dqt_act_quant_batch(io, x_t: int, M: int, act_q: int, stream=None):
+    _check("dqt_act_quant_batch", load().dqt_act_quant_batch(len(io), io, x_t, M, act_q,
+                                                             _stream(stream)))
 
 
 def dqt_linear_fwd_batch_workspace(io) -> int:

@@ -120,12 +120,15 @@ def test_call_level_checks():
                               dqt.DQT_F32, FAKE, BIG, None) == dqt.DQT_ERR_DTYPE
     assert lib.dqt_linear_fwd(bw, FAKE, FAKE, dqt.DQT_F32, 16, dqt.DQT_F32, FAKE, FAKE, FAKE,
                               dqt.DQT_F32, FAKE, BIG, None) == dqt.DQT_ERR_DTYPE
-    need_f = lib.dqt_linear_fwd_workspace(bw)
-    assert need_f == 64 * 64
-    assert lib.dqt_linear_fwd(bw, FAKE, FAKE, dqt.DQT_F32, 16, dqt.DQT_I8, FAKE, FAKE, FAKE,
-                              dqt.DQT_F32, FAKE, need_f - 1, None) == dqt.DQT_ERR_WORKSPACE
-    assert lib.dqt_linear_fwd(bw, FAKE, FAKE, dqt.DQT_F32, 16, dqt.DQT_I8, FAKE, FAKE, FAKE,
-                              dqt.DQT_F32, None, 0, None) == dqt.DQT_ERR_WORKSPACE
+    # packed codes go straight to the GEMM when d_in is a multiple of 64
+    assert lib.dqt_linear_fwd_workspace(bw) == 0
+    w48 = _w(d_in=48)
+    need_f = lib.dqt_linear_fwd_workspace(ctypes.byref(w48))
+    assert need_f == 64 * 48
+    assert lib.dqt_linear_fwd(ctypes.byref(w48), FAKE, FAKE, dqt.DQT_F32, 16, dqt.DQT_I8, FAKE, FAKE,
+                              FAKE, dqt.DQT_F32, FAKE, need_f - 1, None) == dqt.DQT_ERR_WORKSPACE
+    assert lib.dqt_linear_fwd(ctypes.byref(w48), FAKE, FAKE, dqt.DQT_F32, 16, dqt.DQT_I8, FAKE, FAKE,
+                              FAKE, dqt.DQT_F32, None, 0, None) == dqt.DQT_ERR_WORKSPACE
     w8 = _w(wfmt=dqt.DQT_I8, qmin=-127, qmax=127)
     assert lib.dqt_linear_fwd_workspace(ctypes.byref(w8)) == 0
     assert lib.dqt_linear_fwd(ctypes.byref(w8), FAKE, FAKE, dqt.DQT_F32, 16, dqt.DQT_FP8E4M3,
@@ -162,6 +165,24 @@ def test_call_level_checks():
     assert lib.dqt_act_quant(FAKE, dqt.DQT_F32, 4, 20, dqt.DQT_I8, FAKE, FAKE,
                              None) == dqt.DQT_ERR_SHAPE
     assert lib.dqt_act_quant(FAKE, dqt.DQT_F32, 0, 32, dqt.DQT_I8, None, None, None) == dqt.DQT_OK
+    ents = (dqt.DqtActIO * 9)()
+    for e in ents:
+        e.X, e.Xq, e.xdq, e.K, e.reserved = 1 << 20, 1 << 20, 1 << 20, 64, 0
+    assert lib.dqt_act_quant_batch(9, ents, dqt.DQT_BF16, 16, dqt.DQT_I8, None) == dqt.DQT_ERR_SHAPE
+    assert lib.dqt_act_quant_batch(2, None, dqt.DQT_BF16, 16, dqt.DQT_I8, None) == dqt.DQT_ERR_NULL
+    assert lib.dqt_act_quant_batch(2, ents, dqt.DQT_I8, 16, dqt.DQT_I8, None) == dqt.DQT_ERR_DTYPE
+    ents[1].K = 20
+    assert lib.dqt_act_quant_batch(2, ents, dqt.DQT_BF16, 16, dqt.DQT_I8, None) == dqt.DQT_ERR_SHAPE
+    ents[1].K = 64
+    ents[1].Xq = None
+    assert lib.dqt_act_quant_batch(2, ents, dqt.DQT_BF16, 16, dqt.DQT_I8, None) == dqt.DQT_ERR_NULL
+    ents[1].Xq = (1 << 20) + 8
+    assert lib.dqt_act_quant_batch(2, ents, dqt.DQT_BF16, 16, dqt.DQT_I8, None) == dqt.DQT_ERR_ALIGN
+    assert lib.dqt_act_quant_batch(2, ents, dqt.DQT_BF16, 0, dqt.DQT_I8, None) == dqt.DQT_ERR_ALIGN
+    ents[1].Xq = 1 << 20
+    assert lib.dqt_act_quant_batch(2, ents, dqt.DQT_BF16, 0, dqt.DQT_I8, None) == dqt.DQT_OK
+    assert lib.dqt_act_quant_batch(2, ents, dqt.DQT_BF16, (1 << 28) + 1, dqt.DQT_I8,
+                                   None) == dqt.DQT_ERR_SHAPE
     assert lib.dqt_debug_rng(0, 1, 0, 0, -1, FAKE, None) == dqt.DQT_ERR_SHAPE
     assert lib.dqt_debug_rng(0, 1, 0, 0, 5, None, None) == dqt.DQT_ERR_NULL
 

@@ -38,7 +38,7 @@ def test_rng_stream_bit_exact(lib, seed, step, tid, i0, n):
 
 # ------------------------------------------------------------ act quant
 
-@pytest.mark.parametrize("M,K", [(1, 16), (37, 272), (513, 768), (64, 11008)])
+@pytest.mark.parametrize("M,K", [(1, 16), (37, 272), (513, 768), (64, 11008), (5, 20480)])
 @pytest.mark.parametrize("x_t", ["f32", "bf16"])
 @pytest.mark.parametrize("act", ["i8", "e4m3"])
 def test_act_quant_bit_exact(lib, M, K, x_t, act):
@@ -54,6 +54,28 @@ def test_act_quant_bit_exact(lib, M, K, x_t, act):
     want_q, want_d = O.act_quant(X_seen, act)
     assert np.array_equal(xdq.cpu().numpy(), want_d)
     assert np.array_equal(Xq.cpu().numpy(), want_q.view(np.uint8))
+
+
+@pytest.mark.parametrize("x_t", ["f32", "bf16"])
+@pytest.mark.parametrize("act", ["i8", "e4m3"])
+def test_act_quant_batch_matches_oracle(lib, x_t, act):
+    M = 257
+    Ks = [768, 2048, 272, 11008]
+    ents, seen = [], []
+    for i, K in enumerate(Ks):
+        X = draws((M, K), 1.0, 11, i, K)
+        X[7, :] = 0.0
+        X_dev, X_seen = to_dev(X, x_t)
+        Xq = torch.empty((M, K), dtype=torch.uint8, device=DEV)
+        xdq = torch.empty((M,), dtype=torch.float32, device=DEV)
+        ents.append((X_dev, Xq, xdq))
+        seen.append(X_seen)
+    io = dqt.act_io(ents)
+    dqt.dqt_act_quant_batch(io, dqt.dtype_code(ents[0][0]), M, act_code(act))
+    for (X_dev, Xq, xdq), X_seen in zip(ents, seen):
+        want_q, want_d = O.act_quant(X_seen, act)
+        assert np.array_equal(xdq.cpu().numpy(), want_d)
+        assert np.array_equal(Xq.cpu().numpy(), want_q.view(np.uint8))
 
 
 # -------------------------------------------------------------- forward
