@@ -31,6 +31,12 @@
  *    value, M = 0 is a no-op except that dW is then written as zeros).
  *    Base pointers must be 16-byte aligned.
  *  - Non-finite values in X or dY are not checked.
+ *  - Workspaces (dqt_linear_fwd / dqt_linear_bwd and their batches) are
+ *    caller-owned device buffers of at least the size the matching
+ *    *_workspace() call returns.  Their first 256 bytes hold the library's
+ *    tile counters: they must be zero before a workspace's first use (e.g.
+ *    allocate it zero-filled) and every call leaves them zero.  Calls that
+ *    share a workspace must not run concurrently.
  */
 #ifndef DQT_H
 #define DQT_H
@@ -106,10 +112,11 @@ typedef struct {
 dqt_status dqt_act_quant(const void* X, int32_t x_t, int64_t M, int32_t K,
                          int32_t act_q, void* Xq, float* xdq, void* stream);
 
-/* Bytes of device workspace dqt_linear_fwd needs for this weight (0 if
- * none).  Ternary codes feed the matrix cores packed when d_in is a multiple
- * of 64 (workspace 0); otherwise they are unpacked once per call into
- * d_out * d_in operand bytes.  Depends only on the descriptor. */
+/* Bytes of device workspace dqt_linear_fwd needs for this weight: the 256
+ * counter bytes, plus, for ternary weights whose d_in is not a multiple of
+ * 64, d_out * d_in operand bytes they are unpacked into (with d_in a
+ * multiple of 64 the packed codes feed the matrix cores directly).  Depends
+ * only on the descriptor. */
 size_t dqt_linear_fwd_workspace(const dqt_weight* w);
 
 /*

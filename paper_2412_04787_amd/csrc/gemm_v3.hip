@@ -17,7 +17,9 @@
 //  * Persistent grid, one block per CU.  XCD x (workgroups are dispatched
 //    round-robin over the 8 XCDs, each with its own L2) owns a contiguous
 //    1/8 of every problem's tiles, problems sorted longest reduction first;
-//    its blocks take that list round-robin.  Before a tile's epilogue the
+//    its blocks take tiles from that list through an atomic counter, so a
+//    block that finishes early takes the next one (longest-first list
+//    scheduling).  Before a tile's epilogue the
 //    block issues the first DMA stage of its next tile, so the load latency
 //    hides behind the epilogue.
 //  * Fragments come from LDS with ds_read_b128 (K-contiguous) or with the
@@ -87,6 +89,10 @@ template <class Epi>
 struct Group {
   Prob<Epi> p[MAXG];
   int32_t ng;
+  // tile counters: next[x] is the next tile of XCD x's list to hand out,
+  // done[x] counts XCD x's blocks that found the list empty (the last one
+  // resets both to zero for the next launch)
+  int* sched;
 };
 
 typedef short s16x4 __attribute__((ext_vector_type(4)));
@@ -191,6 +197,7 @@ struct Plan {
 // problem's n tiles, problems in launch order.  False past the end.
 template <class Epi>
 __device__ __forceinline__ bool locate(const Group<Epi>& grp, int x, int j, int& g, int& local) {
+  if (j < 0) return false;   // counters not zero at launch: do nothing rather than fault
   for (g = 0; g < grp.ng; ++g) {
     const int n = grp.p[g].ntiles;
     const int s0 = (x * n) >> 3, cnt = (((x + 1) * n) >> 3) - s0;
@@ -222,7 +229,7 @@ __global__ __launch_bounds__(NTH) void gemm_v3_kernel(const Group<Epi> grp) {
   const int wi = wave >> 2, wj = wave & 3;
   const int h = lane >> 5;
   const int wave_u = __builtin_amdgcn_readfirstlane(wave);
-  const int xcd = blockIdx.x & 7, kb = blockIdx.x >> 3, nbx8 = gridDim.x >> 3;
+  const int xcd = blockIdx.x & 7, nbx8 = gridDim.x >> 3;
 
   // ---- state of the tile being computed
   struct TileState {
@@ -381,8 +388,21 @@ __global__ __launch_bounds__(NTH) void gemm_v3_kernel(const Group<Epi> grp) {
   auto stage_ptr = [&](int slot) { return smem + slot * SLOTB; };
 
   // ---- persistent loop over this block's tiles
+  __shared__ int next_tile;
+  int* const next_ctr = grp.sched + xcd;
+  auto finish = [&]() {                 // this block found XCD xcd's list empty
+    if (tid == 0 && atomicAdd(grp.sched + 8 + xcd, 1) == nbx8 - 1) {
+      next_ctr[0] = 0;
+      grp.sched[8 + xcd] = 0;
+    }
+  };
+  if (tid == 0) next_tile = atomicAdd(next_ctr, 1);
+  __syncthreads();
   int g0, local0;
-  if (!locate(grp, xcd, kb, g0, local0)) return;
+  if (!locate(grp, xcd, next_tile, g0, local0)) {
+    finish();
+    return;
+  }
   setup(g0, local0, cur);
   // Stage of step s of the current tile: (slot0 + s) mod NS.  Before a tile
   // starts, its steps 0 .. NS-2 are in flight.
@@ -415,7 +435,8 @@ __global__ __launch_bounds__(NTH) void gemm_v3_kernel(const Group<Epi> grp) {
     }
   };
 
-  for (int j = kb;;) {
+  for (;;) {
+    int fetched = 0;                   // thread 0: index of the next tile
 #pragma unroll
     for (int a = 0; a < WI; ++a)
 #pragma unroll
@@ -434,6 +455,8 @@ __global__ __launch_bounds__(NTH) void gemm_v3_kernel(const Group<Epi> grp) {
       if (cur.tail && it == cur.nsteps - 1) zero_tail(it, slot, cur);
       block_barrier();                 // stage `slot` complete; step it - 1's stage is free
       if (it + NS - 1 < cur.nsteps) issue(it + NS - 1, (slot + NS - 1) % NS, cur);
+      // fetch the next tile early; its value is needed only at the epilogue
+      if (it == 0 && tid == 0) fetched = atomicAdd(next_ctr, 1);
       compute(slot);
     }
 
@@ -447,10 +470,10 @@ __global__ __launch_bounds__(NTH) void gemm_v3_kernel(const Group<Epi> grp) {
     if constexpr (Epi::kRowScale) {
       if (tid < TILE) row_scale[tid] = epi.scale_fin(my_scale);
     }
+    if (tid == 0) next_tile = cur.nsteps > 0 ? fetched : atomicAdd(next_ctr, 1);
     block_barrier();                   // every wave is done with every stage
-    const int jn = j + nbx8;
     int gn, localn;
-    const bool more = locate(grp, xcd, jn, gn, localn);
+    const bool more = locate(grp, xcd, next_tile, gn, localn);
     if (more) {
       const int slotn = (last + 1) % NS;      // the next tile's stages avoid `last`
       setup(gn, localn, cur);
@@ -518,11 +541,11 @@ __global__ __launch_bounds__(NTH) void gemm_v3_kernel(const Group<Epi> grp) {
       }
     }
     if (!more) break;
-    j = jn;
     // a tile without reduction steps has no main-loop barrier before the
     // next epilogue reuses the staging area and the row scales
     if (cur.nsteps == 0) block_barrier();
   }
+  finish();
 }
 
 }  // namespace v3
@@ -676,7 +699,8 @@ static int device_cus() {
 // Fill in tile grids, sort the problems by reduction steps per tile (longest
 // first) and launch the persistent grid: 8 x (blocks per XCD).
 template <int ELEM, int MA, int MB, class Epi>
-static void launch_group(Group<Epi>& grp, hipStream_t s) {
+static void launch_group(Group<Epi>& grp, uint8_t* ws, hipStream_t s) {
+  grp.sched = reinterpret_cast<int*>(ws);
   constexpr int64_t BK = KBYTES / (ELEM == EBF16 ? 2 : 1);
   int64_t steps[MAXG];
   for (int g = 0; g < grp.ng; ++g) {
@@ -722,7 +746,7 @@ static bool fwd_packed(int n, const LinearIO* io) {
 }
 
 size_t fwd_batch_workspace(int n, const LinearIO* io, bool ternary, size_t* offs) {
-  size_t total = 0;
+  size_t total = kSchedBytes;
   const bool unpack = ternary && !fwd_packed(n, io);
   for (int l = 0; l < n; ++l) {
     if (offs) offs[l] = total;
@@ -769,11 +793,11 @@ hipError_t launch_fwd_batch(const BatchCfg& c, const LinearIO* io, uint8_t* ws, 
     p.nbz = 1;
   }
   if (packed) {
-    if (c.act_e4m3) launch_group<EF8, KC, KCP>(grp, stream);
-    else launch_group<EI8, KC, KCP>(grp, stream);
+    if (c.act_e4m3) launch_group<EF8, KC, KCP>(grp, ws, stream);
+    else launch_group<EI8, KC, KCP>(grp, ws, stream);
   } else {
-    if (c.act_e4m3) launch_group<EF8, KC, KC>(grp, stream);
-    else launch_group<EI8, KC, KC>(grp, stream);
+    if (c.act_e4m3) launch_group<EF8, KC, KC>(grp, ws, stream);
+    else launch_group<EI8, KC, KC>(grp, ws, stream);
   }
   return hipGetLastError();
 }
@@ -806,7 +830,7 @@ BwdPlan plan_bwd_batch(int n, const LinearIO* io, int64_t M) {
     const double t_us = rounds * (steps * 2048.0 / 2100.0 + 2.0) + part_bytes / 4.0e6;
     if (t_us < best * 0.999) { best = t_us; P.splits = s; }
   }
-  size_t off = 0;
+  size_t off = kSchedBytes;
   for (int l = 0; l < n; ++l) {
     const size_t wn = (size_t)(io[l].d_out * io[l].d_in);
     const int64_t s32 = dw_splits_f32(io[l].d_out, io[l].d_in, M);
@@ -851,7 +875,7 @@ hipError_t launch_dx_batch(const BatchCfg& c, const LinearIO* io, uint8_t* ws, c
     p.split_len = io[l].d_out;
     p.nbz = 1;
   }
-  launch_group<EBF16, KC, KM>(grp, stream);
+  launch_group<EBF16, KC, KM>(grp, ws, stream);
   return hipGetLastError();
 }
 
@@ -900,7 +924,7 @@ hipError_t launch_dw_batch(const BatchCfg& c, const LinearIO* io, uint8_t* ws, c
     p.split_len = len;
     p.nbz = (int32_t)splits;
   }
-  launch_group<EBF16, KM, KM>(grp, stream);
+  launch_group<EBF16, KM, KM>(grp, ws, stream);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || splits == 1) return e;
   RedTab red{};

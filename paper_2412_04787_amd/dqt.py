@@ -171,11 +171,13 @@ def dqt_linear_fwd(w: DqtWeight, Wq, X, M: int, act_q: int, Xq, xdq, Y, ws=None,
 
 
 def workspace(nbytes: int, device="cuda:0"):
-    """A device buffer of at least nbytes (16-byte aligned), or None for 0."""
+    """A zero-filled device buffer of at least nbytes (16-byte aligned), or
+    None for 0.  (The GEMM calls keep tile counters in the first 256 bytes of
+    a workspace; they must start at zero and every call leaves them zero.)"""
     if nbytes == 0:
         return None
     torch = _torch()
-    return torch.empty(((nbytes + 15) // 16 * 4,), dtype=torch.float32, device=device)
+    return torch.zeros(((nbytes + 15) // 16 * 4,), dtype=torch.float32, device=device)
 
 
 def dqt_linear_bwd_workspace(w: DqtWeight, M: int) -> int:

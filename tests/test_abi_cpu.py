@@ -120,17 +120,18 @@ def test_call_level_checks():
                               dqt.DQT_F32, FAKE, BIG, None) == dqt.DQT_ERR_DTYPE
     assert lib.dqt_linear_fwd(bw, FAKE, FAKE, dqt.DQT_F32, 16, dqt.DQT_F32, FAKE, FAKE, FAKE,
                               dqt.DQT_F32, FAKE, BIG, None) == dqt.DQT_ERR_DTYPE
-    # packed codes go straight to the GEMM when d_in is a multiple of 64
-    assert lib.dqt_linear_fwd_workspace(bw) == 0
+    # 256 counter bytes; packed codes go straight to the GEMM when d_in is a
+    # multiple of 64, else they are unpacked into the workspace
+    assert lib.dqt_linear_fwd_workspace(bw) == 256
     w48 = _w(d_in=48)
     need_f = lib.dqt_linear_fwd_workspace(ctypes.byref(w48))
-    assert need_f == 64 * 48
+    assert need_f == 256 + 64 * 48
     assert lib.dqt_linear_fwd(ctypes.byref(w48), FAKE, FAKE, dqt.DQT_F32, 16, dqt.DQT_I8, FAKE, FAKE,
                               FAKE, dqt.DQT_F32, FAKE, need_f - 1, None) == dqt.DQT_ERR_WORKSPACE
     assert lib.dqt_linear_fwd(ctypes.byref(w48), FAKE, FAKE, dqt.DQT_F32, 16, dqt.DQT_I8, FAKE, FAKE,
                               FAKE, dqt.DQT_F32, None, 0, None) == dqt.DQT_ERR_WORKSPACE
     w8 = _w(wfmt=dqt.DQT_I8, qmin=-127, qmax=127)
-    assert lib.dqt_linear_fwd_workspace(ctypes.byref(w8)) == 0
+    assert lib.dqt_linear_fwd_workspace(ctypes.byref(w8)) == 256
     assert lib.dqt_linear_fwd(ctypes.byref(w8), FAKE, FAKE, dqt.DQT_F32, 16, dqt.DQT_FP8E4M3,
                               FAKE, FAKE, FAKE, dqt.DQT_F32, None, 0, None) == dqt.DQT_ERR_UNSUPPORTED
     # M = 0 is a no-op that launches nothing

@@ -8,7 +8,8 @@ import torch
 from oracle import dqt_oracle as O
 from paper_2412_04787_amd import dqt, workloads as W
 
-from gpu_util import DEV, gemm_close, log, make_weight, to_dev, weight_codes_dev, weight_codes_host
+from gpu_util import (DEV, gemm_close, log, make_weight, run_fwd, to_dev, weight_codes_dev,
+                      weight_codes_host)
 
 pytestmark = pytest.mark.gpu
 SEED = 4321
@@ -121,3 +122,29 @@ def test_batch_rejects_mixed_formats_and_sizes(lib):
     with pytest.raises(dqt.DqtError) as e:
         dqt.dqt_sr_update_batch(io9, 1e-3, 0, 1)
     assert e.value.status == dqt.DQT_ERR_SHAPE
+
+
+def test_tile_counters_return_to_zero(lib):
+    """The persistent GEMM's tile counters (first 256 bytes of the workspace)
+    are zero again after every call, so one workspace serves call after call
+    and graph replay after replay."""
+    M = 1000
+    ents = []
+    for li, (d_in, d_out) in enumerate([(256, 512), (512, 256), (256, 256)]):
+        q = W.draw_ternary((d_out, d_in), 5, 97, li)
+        w = make_weight(d_out, d_in, "ternary", -1, 1, 0.02, li)
+        X_dev, _ = to_dev(W.draw_normal((M, d_in), 1.0, 5, 97, 10 + li), "bf16")
+        dY_dev, _ = to_dev(W.draw_normal((M, d_out), 1e-2, 5, 97, 20 + li), "bf16")
+        Xq, xdq, _ = run_fwd(w, weight_codes_dev(q, "ternary"), X_dev, "i8", "bf16")
+        ents.append(dict(w=w, Wq=weight_codes_dev(q, "ternary"), Xq=Xq, xdq=xdq,
+                         Y=torch.empty((M, d_out), dtype=torch.bfloat16, device=DEV), dY=dY_dev,
+                         dX=torch.empty((M, d_in), dtype=torch.bfloat16, device=DEV),
+                         dW=torch.empty((d_out, d_in), dtype=torch.float32, device=DEV)))
+    io = dqt.linear_io(ents)
+    ws = dqt.workspace(max(dqt.dqt_linear_fwd_batch_workspace(io),
+                           dqt.dqt_linear_bwd_batch_workspace(io, M)))
+    for rep in range(3):
+        dqt.dqt_linear_fwd_batch(io, M, dqt.DQT_I8, dqt.DQT_BF16, ws)
+        dqt.dqt_linear_bwd_batch(io, M, dqt.DQT_I8, dqt.DQT_BF16, dqt.DQT_BF16, dqt.DQT_BF16, ws)
+        torch.cuda.synchronize()
+        assert torch.count_nonzero(ws[:64]).item() == 0, rep
