@@ -50,21 +50,34 @@ constexpr int NW = 8;                 // waves per block, 2 (rows) x 4 (cols)
 constexpr int NTH = 64 * NW;
 constexpr int TILE = 256;             // block tile edge (outputs)
 constexpr int WI = 4, WJ = 2;         // MFMA 32x32 blocks per wave
-constexpr int KBYTES = 128;           // reduction bytes per tile row per step
-constexpr int OPB = TILE * KBYTES;    // bytes per operand per stage (32 KB)
-constexpr int NL = OPB / 16 / NTH;    // DMA instructions per thread per operand per stage
 constexpr int PITCH = 68;             // fp32 words per staged epilogue row (64 + 4)
 constexpr int PKB = 32;               // packed ternary bytes per tile row per step (128 codes)
-static_assert(NL == 4, "DMA plan assumes 4 chunks per thread");
 static_assert(TILE * 2 == NTH, "packed plan: one 16-byte chunk per thread");
-static_assert(NW * 16 * PITCH * 4 <= OPB + TILE * PKB, "epilogue staging fits in one stage");
+
+// Step geometry for KB reduction bytes per tile row per step (128: one cache
+// line; 64: half a line, used with more stages in flight).  K-contiguous
+// tiles are [256 rows][KB bytes]; K-major (bf16) tiles are KB / 2 reduction
+// rows of 256 columns, stored as four 64-column regions.
+template <int KB>
+struct Geo {
+  static_assert(KB == 128 || KB == 64, "step of 64 or 128 bytes");
+  static constexpr int OPB = TILE * KB;       // bytes per operand per stage
+  static constexpr int NL = OPB / 16 / NTH;   // DMA chunks per thread per operand
+  static constexpr int CPR = KB / 16;         // K-contiguous 16-byte chunks per row
+  static constexpr int KR = KB / 2;           // K-major rows per step
+  static constexpr int NKK = KB / 32;         // MFMA sub-steps per step
+  // K-contiguous swizzle: chunk c of row r sits at c ^ swz(r) (conflict-free
+  // ds_read_b128 for 8 or 4 chunks per row)
+  __device__ static int swz(int r) { return CPR == 8 ? (r >> 1) & 7 : (r >> 2) & 3; }
+};
+
 
 enum Elem { EI8 = 0, EF8 = 1, EBF16 = 2 };
 enum Mode { KC = 0, KM = 1, KCP = 2 };   // KCP: K-contiguous packed ternary codes (B only)
 
 // bytes per stage: A, then B (bf16 / 8-bit operand, or packed ternary codes)
-template <int MB>
-constexpr int slot_bytes() { return OPB + (MB == KCP ? TILE * PKB : OPB); }
+template <int MB, int KB>
+constexpr int slot_bytes() { return Geo<KB>::OPB + (MB == KCP ? TILE * PKB : Geo<KB>::OPB); }
 
 
 // Global operand: base of element (row 0, reduction 0), row stride in bytes,
@@ -149,8 +162,10 @@ __device__ __forceinline__ void block_barrier() {
 // the chunks cover, which is the same for all of them; and the distance
 // back from a chunk's address to a safe one in the same row (K-contiguous)
 // or column (K-major) for loads past the end of the reduction.
-template <int MODE, int EB>
+template <int MODE, int EB, int KB>
 struct Plan {
+  using G = Geo<KB>;
+  static constexpr int NL = G::NL;
   const uint8_t* g[NL];
   int64_t back;
   int64_t inc;
@@ -170,16 +185,16 @@ struct Plan {
         back = r_begin / 4 + 16 * c;
         rk = 64 * c;
       } else if constexpr (MODE == KC) {
-        const int row = p >> 3;
-        const int c = (p & 7) ^ ((row >> 1) & 7);   // logical chunk (same for every q)
+        const int row = p / G::CPR;
+        const int c = (p % G::CPR) ^ G::swz(row);   // logical chunk (same for every q)
         int64_t gr = row0 + row;
         if (gr > o.n - 1) gr = o.n - 1;
         g[q] = o.p + gr * o.ld + r_begin * EB + 16 * c;
         back = r_begin * EB + 16 * c;
         rk = 16 * c / EB;
       } else {
-        const int region = p >> 9;                  // 64-column region
-        const int k = (p & 511) >> 3;               // reduction row within the step (same for every q)
+        const int region = p / (G::KR * 8);         // 64-column region
+        const int k = (p % (G::KR * 8)) >> 3;       // reduction row within the step (same for every q)
         const int pc = p & 7;
         const int seg = (pc >> 1) ^ (k & 3);
         int64_t col = row0 + 64 * region + 16 * seg + 8 * (pc & 1);
@@ -189,7 +204,7 @@ struct Plan {
         rk = k;
       }
     }
-    inc = MODE == KC ? KBYTES : MODE == KCP ? PKB : 64 * o.ld;
+    inc = MODE == KC ? KB : MODE == KCP ? PKB : G::KR * o.ld;
   }
 };
 
@@ -210,14 +225,21 @@ __device__ __forceinline__ bool locate(const Group<Epi>& grp, int x, int j, int&
   return false;
 }
 
-template <int ELEM, int MA, int MB, class Epi>
+template <int ELEM, int MA, int MB, int KB, class Epi>
 __global__ __launch_bounds__(NTH) void gemm_v3_kernel(const Group<Epi> grp) {
+  using G = Geo<KB>;
+  static_assert(MB != KCP || KB == 128, "packed codes use 128-byte steps");
   constexpr int EB = ELEM == EBF16 ? 2 : 1;
-  constexpr int BK = KBYTES / EB;           // reduction elements per step
-  constexpr int SLOTB = slot_bytes<MB>();
+  constexpr int BK = KB / EB;               // reduction elements per step
+  constexpr int OPB = G::OPB;
+  constexpr int NL = G::NL;
+  constexpr int SLOTB = slot_bytes<MB, KB>();
   constexpr int NLB = MB == KCP ? 1 : NL;  // DMA chunks per thread for B
-  // as many stages as fit next to the row scales: 3 with packed B, else 2
-  constexpr int NS = 3 * SLOTB + TILE * 4 <= 160 * 1024 ? 3 : 2;
+  // as many stages as fit next to the row scales (at most 4)
+  constexpr int NS = 4 * SLOTB + TILE * 4 <= 160 * 1024 ? 4 : 3 * SLOTB + TILE * 4 <= 160 * 1024 ? 3 : 2;
+  // epilogue rows staged per pass: 16, or 8 when a stage is smaller
+  constexpr int RP = NW * 16 * PITCH * 4 <= SLOTB ? 16 : 8;
+  static_assert(NW * RP * PITCH * 4 <= SLOTB, "epilogue staging fits in one stage");
   constexpr int LPS = NL + NLB;            // DMA instructions per thread per stage
   __shared__ __attribute__((aligned(1024))) uint8_t smem_generic[NS * SLOTB];
   __shared__ float row_scale[Epi::kRowScale ? TILE : 1];
@@ -238,8 +260,8 @@ __global__ __launch_bounds__(NTH) void gemm_v3_kernel(const Group<Epi> grp) {
     int bz, nsteps;
     bool tail;
   };
-  Plan<MA, EB> pa;
-  Plan<MB, EB> pb;
+  Plan<MA, EB, KB> pa;
+  Plan<MB, EB, KB> pb;
   TileState cur;
   float my_scale = 0.0f;
 
@@ -323,12 +345,12 @@ __global__ __launch_bounds__(NTH) void gemm_v3_kernel(const Group<Epi> grp) {
     for (int t = 0; t < WI; ++t) {
       if constexpr (MA == KC) {
         const int row = wi * 32 * WI + t * 32 + frow;
-        const int c = (2 * kk + h) ^ ((row >> 1) & 7);
-        F.fa[t] = *(const __attribute__((address_space(3))) i32x4*)(la + row * KBYTES + 16 * c);
+        const int c = (2 * kk + h) ^ G::swz(row);
+        F.fa[t] = *(const __attribute__((address_space(3))) i32x4*)(la + row * KB + 16 * c);
       } else {
         const int col = wi * 32 * WI + t * 32 + 16 * ch + 4 * u4;
         const int seg = ((col & 63) >> 4) ^ t4;
-        const int a0 = (col >> 6) * 8192 + (16 * kk + 8 * h + t4) * 128 + 32 * seg + 8 * u4;
+        const int a0 = (col >> 6) * (G::KR * 128) + (16 * kk + 8 * h + t4) * 128 + 32 * seg + 8 * u4;
         F.ka[t][0] = tr_read(la, a0);
         F.ka[t][1] = tr_read(la, a0 + 512);
       }
@@ -342,12 +364,12 @@ __global__ __launch_bounds__(NTH) void gemm_v3_kernel(const Group<Epi> grp) {
         F.pb[t] = *(const __attribute__((address_space(3))) uint32_t*)(lb + row * PKB + 4 * pos);
       } else if constexpr (MB == KC) {
         const int row = wj * 32 * WJ + t * 32 + frow;
-        const int c = (2 * kk + h) ^ ((row >> 1) & 7);
-        F.fb[t] = *(const __attribute__((address_space(3))) i32x4*)(lb + row * KBYTES + 16 * c);
+        const int c = (2 * kk + h) ^ G::swz(row);
+        F.fb[t] = *(const __attribute__((address_space(3))) i32x4*)(lb + row * KB + 16 * c);
       } else {
         const int col = wj * 32 * WJ + t * 32 + 16 * ch + 4 * u4;
         const int seg = ((col & 63) >> 4) ^ t4;
-        const int a0 = (col >> 6) * 8192 + (16 * kk + 8 * h + t4) * 128 + 32 * seg + 8 * u4;
+        const int a0 = (col >> 6) * (G::KR * 128) + (16 * kk + 8 * h + t4) * 128 + 32 * seg + 8 * u4;
         F.kb[t][0] = tr_read(lb, a0);
         F.kb[t][1] = tr_read(lb, a0 + 512);
       }
@@ -419,19 +441,25 @@ __global__ __launch_bounds__(NTH) void gemm_v3_kernel(const Group<Epi> grp) {
       read_frags(la, lb, 0, F0);
       read_frags(la, lb, 1, F1);
       mfma1(F0);
-      read_frags(la, lb, 2, F0);
-      mfma1(F1);
-      read_frags(la, lb, 3, F1);
-      mfma1(F0);
+      if constexpr (G::NKK == 4) {
+        read_frags(la, lb, 2, F0);
+        mfma1(F1);
+        read_frags(la, lb, 3, F1);
+        mfma1(F0);
+      }
       mfma1(F1);
     } else {
-      Frags F2, F3;
       read_frags(la, lb, 0, F0);
       read_frags(la, lb, 1, F1);
-      read_frags(la, lb, 2, F2);
-      mfma2(F0, F1);
-      read_frags(la, lb, 3, F3);
-      mfma2(F2, F3);
+      if constexpr (G::NKK == 4) {
+        Frags F2, F3;
+        read_frags(la, lb, 2, F2);
+        mfma2(F0, F1);
+        read_frags(la, lb, 3, F3);
+        mfma2(F2, F3);
+      } else {
+        mfma2(F0, F1);
+      }
     }
   };
 
@@ -485,7 +513,7 @@ __global__ __launch_bounds__(NTH) void gemm_v3_kernel(const Group<Epi> grp) {
     // 8 (r / 4) + 4 h + (r mod 4), r = 0..15.  Each wave stages 16 of its
     // rows at a time as fp32 in its own part of stage `last`, then writes
     // whole 16-byte chunks of output rows (8 bf16 or 4 fp32).
-    lds_u8* stage = smem + last * SLOTB + wave * (16 * PITCH * 4);
+    lds_u8* stage = smem + last * SLOTB + wave * (RP * PITCH * 4);
     const bool obf = epi.out_bf16();
 #pragma unroll
     for (int ta = 0; ta < WI; ++ta) {
@@ -494,29 +522,31 @@ __global__ __launch_bounds__(NTH) void gemm_v3_kernel(const Group<Epi> grp) {
       for (int r = 0; r < 16; ++r)
         sc[r] = Epi::kRowScale ? row_scale[wi * 32 * WI + ta * 32 + 8 * (r >> 2) + 4 * h + (r & 3)]
                                : epi.scale(0);
+      // pass `pass` stages the block's rows [RP pass, RP pass + RP), i.e.
+      // accumulator entries r = RP/2 pass .. RP/2 pass + RP/2 - 1
 #pragma unroll
-      for (int half = 0; half < 2; ++half) {
+      for (int pass = 0; pass < 32 / RP; ++pass) {
 #pragma unroll
         for (int tb = 0; tb < WJ; ++tb)
 #pragma unroll
-          for (int r8 = 0; r8 < 8; ++r8) {
-            const int r = 8 * half + r8;
+          for (int rr = 0; rr < RP / 2; ++rr) {
+            const int r = RP / 2 * pass + rr;
             float v;
             if constexpr (ELEM == EI8) v = (float)acc[ta][tb][r];
             else v = acc[ta][tb][r];
             v = v * sc[r];
-            const int lr = 8 * ((r >> 2) & 1) + 4 * h + (r & 3);
+            const int lr = 8 * ((r >> 2) % (RP / 8)) + 4 * h + (r & 3);
             *(__attribute__((address_space(3))) float*)(stage + (lr * PITCH + tb * 32 + (lane & 31)) * 4) = v;
           }
         __asm__ volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-        const int64_t ibase = i0 + wi * 32 * WI + ta * 32 + 16 * half;
+        const int64_t ibase = i0 + wi * 32 * WI + ta * 32 + RP * pass;
         const int64_t jbase = j0 + wj * 32 * WJ;
         auto store_rows = [&](auto ebytes_tag) {
           constexpr int EBY = decltype(ebytes_tag)::value;
           constexpr int EPC = 16 / EBY;            // elements per 16-byte chunk
           constexpr int CPR = 32 * WJ / EPC;       // chunks per staged row
 #pragma unroll
-          for (int c0 = 0; c0 < 16 * CPR; c0 += 64) {
+          for (int c0 = 0; c0 < RP * CPR; c0 += 64) {
             const int c = c0 + lane;
             const int rr = c / CPR, cc = c % CPR;
             const int64_t i = ibase + rr;
@@ -698,10 +728,10 @@ static int device_cus() {
 
 // Fill in tile grids, sort the problems by reduction steps per tile (longest
 // first) and launch the persistent grid: 8 x (blocks per XCD).
-template <int ELEM, int MA, int MB, class Epi>
+template <int ELEM, int MA, int MB, int KB, class Epi>
 static void launch_group(Group<Epi>& grp, uint8_t* ws, hipStream_t s) {
   grp.sched = reinterpret_cast<int*>(ws);
-  constexpr int64_t BK = KBYTES / (ELEM == EBF16 ? 2 : 1);
+  constexpr int64_t BK = KB / (ELEM == EBF16 ? 2 : 1);
   int64_t steps[MAXG];
   for (int g = 0; g < grp.ng; ++g) {
     Prob<Epi>& p = grp.p[g];
@@ -727,12 +757,22 @@ static void launch_group(Group<Epi>& grp, uint8_t* ws, hipStream_t s) {
   if (per_xcd == 0) return;
   static const int cus = device_cus();
   const int32_t bpx = std::min(per_xcd, std::max(1, cus / 8));
-  hipLaunchKernelGGL((gemm_v3_kernel<ELEM, MA, MB, Epi>), dim3((unsigned)(8 * bpx)), dim3(NTH), 0, s, grp);
+  hipLaunchKernelGGL((gemm_v3_kernel<ELEM, MA, MB, KB, Epi>), dim3((unsigned)(8 * bpx)), dim3(NTH), 0, s, grp);
 }
 
 }  // namespace v3
 
 using namespace v3;
+
+// reduction bytes per step of the unpacked 8-bit forward and of the bf16
+// backward products (128: full lines, two stages; 64: half lines, four
+// stages in flight -- measured equal on the LLaMA-block shapes)
+#ifndef KB_FWD
+#define KB_FWD 128
+#endif
+#ifndef KB_BWD
+#define KB_BWD 128
+#endif
 
 static size_t align256(size_t n) { return (n + 255) / 256 * 256; }
 
@@ -793,11 +833,11 @@ hipError_t launch_fwd_batch(const BatchCfg& c, const LinearIO* io, uint8_t* ws, 
     p.nbz = 1;
   }
   if (packed) {
-    if (c.act_e4m3) launch_group<EF8, KC, KCP>(grp, ws, stream);
-    else launch_group<EI8, KC, KCP>(grp, ws, stream);
+    if (c.act_e4m3) launch_group<EF8, KC, KCP, 128>(grp, ws, stream);
+    else launch_group<EI8, KC, KCP, 128>(grp, ws, stream);
   } else {
-    if (c.act_e4m3) launch_group<EF8, KC, KC>(grp, ws, stream);
-    else launch_group<EI8, KC, KC>(grp, ws, stream);
+    if (c.act_e4m3) launch_group<EF8, KC, KC, KB_FWD>(grp, ws, stream);
+    else launch_group<EI8, KC, KC, KB_FWD>(grp, ws, stream);
   }
   return hipGetLastError();
 }
@@ -875,7 +915,7 @@ hipError_t launch_dx_batch(const BatchCfg& c, const LinearIO* io, uint8_t* ws, c
     p.split_len = io[l].d_out;
     p.nbz = 1;
   }
-  launch_group<EBF16, KC, KM>(grp, ws, stream);
+  launch_group<EBF16, KC, KM, KB_BWD>(grp, ws, stream);
   return hipGetLastError();
 }
 
@@ -924,7 +964,7 @@ hipError_t launch_dw_batch(const BatchCfg& c, const LinearIO* io, uint8_t* ws, c
     p.split_len = len;
     p.nbz = (int32_t)splits;
   }
-  launch_group<EBF16, KM, KM>(grp, ws, stream);
+  launch_group<EBF16, KM, KM, KB_BWD>(grp, ws, stream);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || splits == 1) return e;
   RedTab red{};
