@@ -43,7 +43,7 @@ def parse():
     p.add_argument("--warmup", type=int, default=5)
     p.add_argument("--workload", default="llama_h768")
     p.add_argument("--no-cpu-baseline", action="store_true")
-    p.add_argument("--cpu-tokens", type=int, default=4096,
+    p.add_argument("--cpu-tokens", type=int, default=8192,
                    help="tokens of the oracle's bounded sample")
     p.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                    help="first run three plain device copies of MIB MiB, so that hardware "
@@ -132,9 +132,10 @@ def algorithmic_units(wl):
     return {"fwd": f, "bwd_dx": f, "bwd_dw": f, "sr": sr_bytes, "act_quant": act_bytes}
 
 
-def cpu_baseline(wl, tokens: int):
+def cpu_baseline(wl, tokens: int, min_seconds: float = 10.0):
     """The oracle (untuned) on a bounded sample of the workload: one train step
-    of every linear over the first `tokens` tokens."""
+    of every linear over the first `tokens` tokens, repeated until at least
+    `min_seconds` of oracle time have accumulated (at most 5 repetitions)."""
     from threadpoolctl import threadpool_info
 
     from oracle import dqt_oracle as O
@@ -142,8 +143,7 @@ def cpu_baseline(wl, tokens: int):
 
     tokens = min(tokens, wl.M)
     X = {n: W.input_draw(wl, n)[:tokens] for n in wl.inputs}
-    flops = 0
-    elapsed = 0.0
+    prepared = []
     for li, lin in enumerate(wl.linears):
         W0, qdraw = W.weight_draws(wl, li)
         if wl.init == "uniform":
@@ -155,21 +155,28 @@ def cpu_baseline(wl, tokens: int):
         if wl.x_dtype == "bf16":
             x = O.bf16_to_f32(O.bf16_round(x))
             dY = O.bf16_to_f32(O.bf16_round(dY))
-        t0 = time.perf_counter()
-        O.linear_train_step(x, dY, q, alpha, wl.qmin, wl.qmax, act=wl.act, xt=wl.xt,
-                            y_out=wl.y_out, dx_out=wl.dx_out, lr=wl.lr, seed=wl.seed,
-                            step=1, tensor_id=li)
-        elapsed += time.perf_counter() - t0
-        flops += 6 * tokens * lin.d_in * lin.d_out
+        prepared.append((li, lin, x, dY, q, alpha))
+    flops = 0
+    elapsed = 0.0
+    reps = 0
+    while reps < 5 and (reps == 0 or elapsed < min_seconds):
+        for li, lin, x, dY, q, alpha in prepared:
+            t0 = time.perf_counter()
+            O.linear_train_step(x, dY, q, alpha, wl.qmin, wl.qmax, act=wl.act, xt=wl.xt,
+                                y_out=wl.y_out, dx_out=wl.dx_out, lr=wl.lr, seed=wl.seed,
+                                step=1, tensor_id=li)
+            elapsed += time.perf_counter() - t0
+            flops += 6 * tokens * lin.d_in * lin.d_out
+        reps += 1
     threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
     return {
         "value": flops / elapsed / 1e12,
         "unit": "TFLOP/s",
         "cores": int(threads),
         "kind": "oracle",
-        "sample": f"one train step (act-quant, fwd, dX, dW, SR) of all {len(wl.linears)} "
-                  f"linears of {wl.name} over the first {tokens} of {wl.M} tokens; "
-                  f"{elapsed:.1f} s; host os.cpu_count()={os.cpu_count()}",
+        "sample": f"{reps} x one train step (act-quant, fwd, dX, dW, SR) of all "
+                  f"{len(wl.linears)} linears of {wl.name} over the first {tokens} of {wl.M} "
+                  f"tokens; {elapsed:.1f} s of oracle time; host os.cpu_count()={os.cpu_count()}",
     }
 
 
