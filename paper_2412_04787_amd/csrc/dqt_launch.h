@@ -42,8 +42,10 @@ hipError_t launch_act_quant_batch(int n, const ActIO* io, bool x_bf16, int64_t M
 // int8 / e4m3 / bf16 matrix-core kernels, batched: up to kMaxBatch linears
 // (same dtypes, same token count M) per launch.
 constexpr int kMaxBatch = 8;
-// The first kSchedBytes of every GEMM workspace hold the tile counters of the
-// persistent GEMM (zero before the first call; every call leaves them zero).
+// The first kSchedBytes of every GEMM workspace are the persistent GEMM's:
+// bytes 0-63 hold its tile counters (zero before the first call; every call
+// leaves them zero), bytes 128-143 absorb epilogue stores of chunks outside
+// the output.
 constexpr size_t kSchedBytes = 256;
 struct LinearIO {
   int64_t d_in, d_out;

@@ -148,6 +148,17 @@ __device__ __forceinline__ void wait_vm() {
   static_assert(N >= 0 && N < 64, "vmcnt range");
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
+// wait until at most n (wave-uniform, 0 <= n <= N) vector memory operations
+// of this wave are outstanding
+template <int N>
+__device__ __forceinline__ void wait_vm_le(int n) {
+  if constexpr (N == 0) {
+    wait_vm<0>();
+  } else {
+    if (n >= N) wait_vm<N>();
+    else wait_vm_le<N - 1>(n);
+  }
+}
 // Barrier that keeps the compiler from moving memory accesses across it; it
 // waits for this wave's LDS accesses but not for outstanding DMA.
 __device__ __forceinline__ void block_barrier() {
@@ -463,6 +474,13 @@ __global__ __launch_bounds__(NTH) void gemm_v3_kernel(const Group<Epi> grp) {
     }
   };
 
+  // vector stores one thread issues in an epilogue (every chunk is stored;
+  // chunks outside the output go to a dummy slot in the workspace)
+  constexpr int kStoresBf16 = WI * 32 * (32 * WJ * 2 / 16) / 64;
+  constexpr int kStoresF32 = WI * 32 * (32 * WJ * 4 / 16) / 64;
+  static_assert(kStoresF32 + 2 * LPS < 64, "vmcnt range");
+  uint8_t* const dummy = reinterpret_cast<uint8_t*>(grp.sched) + 128;
+  bool first_tile = true, obf_prev = false;
   for (;;) {
     int fetched = 0;                   // thread 0: index of the next tile
 #pragma unroll
@@ -478,8 +496,19 @@ __global__ __launch_bounds__(NTH) void gemm_v3_kernel(const Group<Epi> grp) {
     // epilogue's stores were issued after this tile's first stages).
     for (int it = 0; it < cur.nsteps; ++it) {
       const int slot = (slot0 + it) % NS;
-      if (NS == 2 || it == 0 || it + 1 == cur.nsteps) wait_vm<0>();
-      else wait_vm<LPS>();             // step it + 1 may still be in flight
+      if (it == 0) {
+        // step 0's loads were issued before the previous epilogue's stores
+        // (a fixed number per thread), which may stay in flight, as may the
+        // tile's later prefetched steps
+        const int ahead = (cur.nsteps < NS - 1 ? cur.nsteps : NS - 1) - 1;
+        const int n = ahead * LPS + (first_tile ? 0 : obf_prev ? kStoresBf16 : kStoresF32);
+        wait_vm_le<kStoresF32 + 2 * LPS>(__builtin_amdgcn_readfirstlane(n));
+        first_tile = false;
+      } else if (NS == 2 || it + 1 == cur.nsteps) {
+        wait_vm<0>();
+      } else {
+        wait_vm<LPS>();                // step it + 1 may still be in flight
+      }
       if (cur.tail && it == cur.nsteps - 1) zero_tail(it, slot, cur);
       block_barrier();                 // stage `slot` complete; step it - 1's stage is free
       if (it + NS - 1 < cur.nsteps) issue(it + NS - 1, (slot + NS - 1) % NS, cur);
@@ -551,9 +580,10 @@ __global__ __launch_bounds__(NTH) void gemm_v3_kernel(const Group<Epi> grp) {
             const int rr = c / CPR, cc = c % CPR;
             const int64_t i = ibase + rr;
             const int64_t jj = jbase + cc * EPC;
-            if (i < I && jj < J) {
+            {
+              const bool inside = i < I && jj < J;
               const lds_u8* src = stage + (rr * PITCH + cc * EPC) * 4;
-              uint8_t* dst = epi.row(i, bz) + jj * EBY;
+              uint8_t* dst = inside ? epi.row(i, bz) + jj * EBY : dummy;
               if constexpr (EBY == 2) {
                 const f32x4 a = *(const __attribute__((address_space(3))) f32x4*)src;
                 const f32x4 b = *(const __attribute__((address_space(3))) f32x4*)(src + 16);
@@ -567,6 +597,7 @@ __global__ __launch_bounds__(NTH) void gemm_v3_kernel(const Group<Epi> grp) {
         };
         if (obf) store_rows(std::integral_constant<int, 2>{});
         else store_rows(std::integral_constant<int, 4>{});
+        obf_prev = obf;
         __asm__ volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
       }
     }
