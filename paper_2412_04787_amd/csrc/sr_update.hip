@@ -10,6 +10,13 @@
 
 namespace dqt {
 
+// a ^ b ^ k in one instruction (k is wave-uniform).
+__device__ __forceinline__ uint32_t xor3(uint32_t a, uint32_t b, uint32_t k) {
+  uint32_t r;
+  asm("v_bitop3_b32 %0, %1, %2, %3 bitop3:0x96" : "=v"(r) : "v"(a), "v"(b), "s"(k));
+  return r;
+}
+
 // Philox4x32 with 10 rounds (Salmon, Moraes, Dror, Shaw, SC'11).  The key is
 // uniform across the grid, so its schedule stays in scalar registers.
 __device__ __forceinline__ uint4 philox10(uint4 c, uint32_t k0, uint32_t k1) {
@@ -17,8 +24,8 @@ __device__ __forceinline__ uint4 philox10(uint4 c, uint32_t k0, uint32_t k1) {
   for (int r = 0; r < 10; ++r) {
     const uint64_t p0 = (uint64_t)0xD2511F53u * c.x;
     const uint64_t p1 = (uint64_t)0xCD9E8D57u * c.z;
-    c = make_uint4((uint32_t)(p1 >> 32) ^ c.y ^ k0, (uint32_t)p1,
-                   (uint32_t)(p0 >> 32) ^ c.w ^ k1, (uint32_t)p0);
+    c = make_uint4(xor3((uint32_t)(p1 >> 32), c.y, k0), (uint32_t)p1,
+                   xor3((uint32_t)(p0 >> 32), c.w, k1), (uint32_t)p0);
     k0 += 0x9E3779B9u;
     k1 += 0xBB67AE85u;
   }
@@ -43,10 +50,10 @@ struct SRArgs {
   uint32_t k0, k1, step, tid;
 };
 
-// One element.  Returns the new code; sets `tie` when the primary 16-bit draw
-// equals the top 16 bits of the threshold (the secondary draw decides).
-// x = q + delta; n = trunc(delta); r = delta - n (exact); the move to the far
-// side (q + n + sign(r)) happens iff U < T = ceil(|r| * 2^32).
+// One element, the full rule.  Returns the new code; sets `tie` when the
+// primary 16-bit draw equals the top 16 bits of the threshold (the secondary
+// draw decides).  x = q + delta; n = trunc(delta); r = delta - n (exact); the
+// move to the far side (q + n + sign(r)) happens iff U < T = ceil(|r| * 2^32).
 __device__ __forceinline__ int sr_one(int q, float g, uint32_t p16, const SRArgs& a,
                                       bool& tie, bool& nonfinite) {
   nonfinite = (__float_as_uint(g) & 0x7F800000u) == 0x7F800000u;
@@ -75,8 +82,29 @@ __device__ __forceinline__ int sr_tie(int q, float g, uint32_t s16, const SRArgs
   return min(max(v, a.qmin), a.qmax);
 }
 
+// The same rule in fewer instructions, for finite gradients and no tie:
+//  * delta = med3(-c * g, -L, L); n = (int)delta truncates toward zero;
+//  * |r| = fract(|delta|) (exact: |delta| - floor(|delta|));
+//  * with P = (p16 << 16) | 0xFFFF, p16 < (T >> 16) iff P < T, and
+//    p16 == (T >> 16) iff (P - T) mod 2^32 <= 0xFFFF, so the running minimum
+//    of P - T flags every element the secondary draw may have to decide.
+// `code` is q plus a per-format offset and [lo, hi] the offset range.
+__device__ __forceinline__ int sr_fast(int code, float g, uint32_t P, float nc, float L, int lo,
+                                       int hi, uint32_t& tiemin) {
+  const float delta = __builtin_amdgcn_fmed3f(nc * g, -L, L);
+  const int n = (int)delta;
+  const float ar = __builtin_amdgcn_fractf(fabsf(delta));
+  const uint32_t T = (uint32_t)ceilf(ar * 4294967296.0f);
+  tiemin = min(tiemin, P - T);
+  const int sgn = ((int)__float_as_uint(delta) >> 31) | 1;
+  const int v = code + n + (P < T ? sgn : 0);
+  return min(max(v, lo), hi);
+}
+
 constexpr int kMaxSR = kMaxBatch;
-// Up to kMaxSR tensors in one launch; tensor s owns blocks [b0[s], b0[s+1]).
+constexpr int kChunksPerTile = 256;   // one 16-weight chunk per thread
+// Up to kMaxSR tensors in one launch; tensor s owns the tiles [b0[s], b0[s+1])
+// of 256 chunks each (its last tile may be partial).
 struct SRTab {
   uint8_t* wq[kMaxSR];
   const float* grad[kMaxSR];
@@ -84,90 +112,162 @@ struct SRTab {
   float c[kMaxSR], L[kMaxSR];
   int qmin[kMaxSR], qmax[kMaxSR];
   uint32_t tid[kMaxSR];
-  int32_t b0[kMaxSR + 1];
+  int64_t b0[kMaxSR + 1];
   int32_t n;
   uint32_t k0, k1, step;
 };
 
+// Persistent kernel: block b takes tiles b, b + grid, ...; thread t of a tile
+// owns chunk t of 16 consecutive weights (64 bytes of gradient, 4 or 16 bytes
+// of codes, so no two lanes touch the same byte).  The change and non-finite
+// counts are reduced per block and added with one atomic each.
 template <bool TERNARY>
 __global__ __launch_bounds__(256) void sr_update_kernel(const SRTab tab,
                                                         unsigned long long* __restrict__ counters) {
-  int sidx = 0;
-  while (sidx + 1 < tab.n && (int)blockIdx.x >= tab.b0[sidx + 1]) ++sidx;
-  SRArgs a;
-  a.c = tab.c[sidx];
-  a.L = tab.L[sidx];
-  a.qmin = tab.qmin[sidx];
-  a.qmax = tab.qmax[sidx];
-  a.k0 = tab.k0;
-  a.k1 = tab.k1;
-  a.step = tab.step;
-  a.tid = tab.tid[sidx];
-  uint8_t* __restrict__ wq = tab.wq[sidx];
-  const float* __restrict__ grad = tab.grad[sidx];
+  __shared__ unsigned long long red[2][256 / kWave];
   unsigned long long changed = 0, nonfin = 0;
-  const int64_t t = (int64_t)(blockIdx.x - tab.b0[sidx]) * blockDim.x + threadIdx.x;
-  if (t < tab.nchunks[sidx]) {
-    const f32x4* gp = reinterpret_cast<const f32x4*>(grad + t * 16);
-    f32x4 gv[4];
+  const int64_t ntiles = tab.b0[tab.n];
+  // Software pipeline: the next tile's gradient and codes are requested
+  // before the current tile is computed, so loads stay in flight meanwhile.
+  int sidx = 0;
+  f32x4 ng[4];
+  uint32_t nw[4];
+  int64_t nt = 0;
+  int ns = 0;
+  auto fetch = [&](int64_t tl) {
+    while (sidx + 1 < tab.n && tl >= tab.b0[sidx + 1]) ++sidx;   // tiles ascend
+    ns = sidx;
+    nt = (tl - tab.b0[sidx]) * kChunksPerTile + threadIdx.x;
+    if (nt < tab.nchunks[sidx]) {
+      const f32x4* gp = reinterpret_cast<const f32x4*>(tab.grad[sidx] + nt * 16);
 #pragma unroll
-    for (int u = 0; u < 4; ++u) gv[u] = __builtin_nontemporal_load(gp + u);
-    int q[16];
-    if constexpr (TERNARY) {
-      const uint32_t packed = reinterpret_cast<const uint32_t*>(wq)[t];
-#pragma unroll
-      for (int j = 0; j < 16; ++j) q[j] = (int)((packed >> (2 * j)) & 3u) - 1;
-    } else {
-      const uint4 packed8 = reinterpret_cast<const uint4*>(wq)[t];
-      const uint32_t w4[4] = {packed8.x, packed8.y, packed8.z, packed8.w};
-#pragma unroll
-      for (int j = 0; j < 16; ++j) q[j] = (int)(int8_t)(w4[j >> 2] >> (8 * (j & 3)));
+      for (int u = 0; u < 4; ++u) ng[u] = __builtin_nontemporal_load(gp + u);
+      if constexpr (TERNARY) {
+        nw[0] = reinterpret_cast<const uint32_t*>(tab.wq[sidx])[nt];
+      } else {
+        const uint4 w = reinterpret_cast<const uint4*>(tab.wq[sidx])[nt];
+        nw[0] = w.x; nw[1] = w.y; nw[2] = w.z; nw[3] = w.w;
+      }
     }
+  };
+  int64_t tile = blockIdx.x;
+  if (tile < ntiles) fetch(tile);
+  for (; tile < ntiles; tile += gridDim.x) {
+    const int cs = ns;
+    const int64_t t = nt;
+    f32x4 gv[4];
+    uint32_t win[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      gv[u] = ng[u];
+      win[u] = nw[u];
+    }
+    if (tile + gridDim.x < ntiles) fetch(tile + gridDim.x);
+    if (t >= tab.nchunks[cs]) continue;
+    SRArgs a;
+    a.c = tab.c[cs];
+    a.L = tab.L[cs];
+    a.qmin = tab.qmin[cs];
+    a.qmax = tab.qmax[cs];
+    a.k0 = tab.k0;
+    a.k1 = tab.k1;
+    a.step = tab.step;
+    a.tid = tab.tid[cs];
+    uint8_t* __restrict__ wq = tab.wq[cs];
     const uint64_t blk = (uint64_t)t * 2;
     const uint4 r0 = philox_block(blk, 0u, a.step, a.tid, a.k0, a.k1);
     const uint4 r1 = philox_block(blk + 1, 0u, a.step, a.tid, a.k0, a.k1);
-    int nq[16];
-    uint32_t ties = 0;
+    const uint32_t rw[8] = {r0.x, r0.y, r0.z, r0.w, r1.x, r1.y, r1.z, r1.w};
+
+    // finite check: a product chain stays finite unless some g is inf/NaN
+    // (or a product overflows, which only sends the chunk to the full rule)
+    float probe = 0.0f;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      probe = __builtin_fmaf(gv[u][0], gv[u][1], probe);
+      probe = __builtin_fmaf(gv[u][2], gv[u][3], probe);
+    }
+    uint32_t tiemin = 0xFFFFFFFFu;
+    const float nc = -a.c;
+    uint32_t wout[4] = {0, 0, 0, 0};
 #pragma unroll
     for (int j = 0; j < 16; ++j) {
       const float g = gv[j >> 2][j & 3];
-      const uint32_t p16 = half16(j < 8 ? r0 : r1, j & 7);
-      bool tie, nf;
-      nq[j] = sr_one(q[j], g, p16, a, tie, nf);
-      ties |= (tie ? 1u : 0u) << j;
-      nonfin += nf ? 1 : 0;
-    }
-    if (ties) {  // probability ~2^-16 per element: decide with stream 1
-      const uint4 s0 = philox_block(blk, 1u, a.step, a.tid, a.k0, a.k1);
-      const uint4 s1 = philox_block(blk + 1, 1u, a.step, a.tid, a.k0, a.k1);
-#pragma unroll
-      for (int j = 0; j < 16; ++j) {
-        if (ties & (1u << j)) {
-          const float g = gv[j >> 2][j & 3];
-          nq[j] = sr_tie(q[j], g, half16(j < 8 ? s0 : s1, j & 7), a);
-        }
+      const uint32_t word = rw[j >> 1];
+      const uint32_t P = (j & 1) ? (word | 0xFFFFu) : ((word << 16) | 0xFFFFu);
+      if constexpr (TERNARY) {
+        const int code = (int)((win[0] >> (2 * j)) & 3u);
+        const int v = sr_fast(code, g, P, nc, a.L, a.qmin + 1, a.qmax + 1, tiemin);
+        wout[0] |= (uint32_t)v << (2 * j);
+      } else {
+        const int code = (int)(int8_t)(win[j >> 2] >> (8 * (j & 3)));
+        const int v = sr_fast(code, g, P, nc, a.L, a.qmin, a.qmax, tiemin);
+        wout[j >> 2] |= ((uint32_t)v & 0xFFu) << (8 * (j & 3));
       }
     }
+    if (tiemin <= 0xFFFFu || !__builtin_isfinite(probe)) {
+      // rare (about 16 / 65536 per chunk, or a non-finite gradient): full rule
+      int q[16], nq[16];
 #pragma unroll
-    for (int j = 0; j < 16; ++j) changed += (nq[j] != q[j]) ? 1 : 0;
+      for (int j = 0; j < 16; ++j)
+        q[j] = TERNARY ? (int)((win[0] >> (2 * j)) & 3u) - 1
+                       : (int)(int8_t)(win[j >> 2] >> (8 * (j & 3)));
+      uint32_t ties = 0;
+#pragma unroll
+      for (int j = 0; j < 16; ++j) {
+        bool tie, nf;
+        nq[j] = sr_one(q[j], gv[j >> 2][j & 3], half16(j < 8 ? r0 : r1, j & 7), a, tie, nf);
+        ties |= (tie ? 1u : 0u) << j;
+        nonfin += nf ? 1 : 0;
+      }
+      if (ties) {
+        const uint4 s0 = philox_block(blk, 1u, a.step, a.tid, a.k0, a.k1);
+        const uint4 s1 = philox_block(blk + 1, 1u, a.step, a.tid, a.k0, a.k1);
+#pragma unroll
+        for (int j = 0; j < 16; ++j)
+          if (ties & (1u << j))
+            nq[j] = sr_tie(q[j], gv[j >> 2][j & 3], half16(j < 8 ? s0 : s1, j & 7), a);
+      }
+#pragma unroll
+      for (int w = 0; w < 4; ++w) wout[w] = 0;
+#pragma unroll
+      for (int j = 0; j < 16; ++j) {
+        if constexpr (TERNARY) wout[0] |= (uint32_t)(nq[j] + 1) << (2 * j);
+        else wout[j >> 2] |= ((uint32_t)nq[j] & 0xFFu) << (8 * (j & 3));
+      }
+    }
+    // changed codes: count differing 2-bit fields or bytes
     if constexpr (TERNARY) {
-      uint32_t out = 0;
-#pragma unroll
-      for (int j = 0; j < 16; ++j) out |= (uint32_t)(nq[j] + 1) << (2 * j);
-      reinterpret_cast<uint32_t*>(wq)[t] = out;
+      const uint32_t x = wout[0] ^ win[0];
+      changed += __builtin_popcount((x | (x >> 1)) & 0x55555555u);
+      reinterpret_cast<uint32_t*>(wq)[t] = wout[0];
     } else {
-      uint32_t o[4] = {0, 0, 0, 0};
 #pragma unroll
-      for (int j = 0; j < 16; ++j) o[j >> 2] |= ((uint32_t)nq[j] & 0xFFu) << (8 * (j & 3));
-      reinterpret_cast<uint4*>(wq)[t] = make_uint4(o[0], o[1], o[2], o[3]);
+      for (int w = 0; w < 4; ++w) {
+        const uint32_t x = wout[w] ^ win[w];
+        changed += __builtin_popcount((((x & 0x7F7F7F7Fu) + 0x7F7F7F7Fu) | x) & 0x80808080u);
+      }
+      reinterpret_cast<uint4*>(wq)[t] = make_uint4(wout[0], wout[1], wout[2], wout[3]);
     }
   }
   if (counters != nullptr) {
     changed = wave_sum_u64(changed);
     nonfin = wave_sum_u64(nonfin);
+    const int w = threadIdx.x / kWave;
     if ((threadIdx.x & (kWave - 1)) == 0) {
-      if (changed) atomicAdd(counters + 0, changed);
-      if (nonfin) atomicAdd(counters + 1, nonfin);
+      red[0][w] = changed;
+      red[1][w] = nonfin;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      unsigned long long c = 0, f = 0;
+#pragma unroll
+      for (int i = 0; i < 256 / kWave; ++i) {
+        c += red[0][i];
+        f += red[1][i];
+      }
+      if (c) atomicAdd(counters + 0, c);
+      if (f) atomicAdd(counters + 1, f);
     }
   }
 }
@@ -185,6 +285,17 @@ __global__ __launch_bounds__(256) void debug_rng_kernel(uint32_t* __restrict__ o
   }
 }
 
+// Blocks of `threads` threads of `fn` resident on the current device at once.
+static int occupancy_blocks(const void* fn, int threads) {
+  int dev = 0, cus = 0, per_cu = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
+    cus = 256;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, threads, 0) != hipSuccess || per_cu <= 0)
+    per_cu = 4;
+  return cus * per_cu;
+}
+
 hipError_t launch_sr_update(bool ternary, int n, const SRTensor* t, uint64_t seed, uint32_t step,
                             unsigned long long* counters, hipStream_t stream) {
   SRTab tab{};
@@ -192,7 +303,7 @@ hipError_t launch_sr_update(bool ternary, int n, const SRTensor* t, uint64_t see
   tab.k0 = (uint32_t)seed;
   tab.k1 = (uint32_t)(seed >> 32);
   tab.step = step;
-  int32_t blocks = 0;
+  int64_t tiles = 0;
   for (int s = 0; s < n; ++s) {
     tab.wq[s] = t[s].wq;
     tab.grad[s] = t[s].grad;
@@ -202,15 +313,21 @@ hipError_t launch_sr_update(bool ternary, int n, const SRTensor* t, uint64_t see
     tab.qmin[s] = t[s].qmin;
     tab.qmax[s] = t[s].qmax;
     tab.tid[s] = t[s].tensor_id;
-    tab.b0[s] = blocks;
-    blocks += (int32_t)((tab.nchunks[s] + 255) / 256);
+    tab.b0[s] = tiles;
+    tiles += (tab.nchunks[s] + kChunksPerTile - 1) / kChunksPerTile;
   }
-  tab.b0[n] = blocks;
-  if (blocks == 0) return hipSuccess;
+  tab.b0[n] = tiles;
+  if (tiles == 0) return hipSuccess;
+  // as many blocks as fit on the device at once; each loops over tiles
+  static const int resident[2] = {
+      occupancy_blocks(reinterpret_cast<const void*>(sr_update_kernel<false>), 256),
+      occupancy_blocks(reinterpret_cast<const void*>(sr_update_kernel<true>), 256)};
+  const int64_t cap = resident[ternary ? 1 : 0];
+  const unsigned blocks = (unsigned)(tiles < cap ? tiles : cap);
   if (ternary)
-    hipLaunchKernelGGL(sr_update_kernel<true>, dim3((unsigned)blocks), dim3(256), 0, stream, tab, counters);
+    hipLaunchKernelGGL(sr_update_kernel<true>, dim3(blocks), dim3(256), 0, stream, tab, counters);
   else
-    hipLaunchKernelGGL(sr_update_kernel<false>, dim3((unsigned)blocks), dim3(256), 0, stream, tab, counters);
+    hipLaunchKernelGGL(sr_update_kernel<false>, dim3(blocks), dim3(256), 0, stream, tab, counters);
   return hipGetLastError();
 }
 

@@ -270,6 +270,39 @@ def test_sr_worked_example_on_gpu(lib):
     assert np.array_equal(got.ravel()[idx.astype(np.int64)], want)
 
 
+@pytest.mark.parametrize("wfmt,qmin,qmax,alpha", [("ternary", -1, 1, 0.016),
+                                                  ("i8", -128, 127, 2e-4)])
+def test_sr_update_large_sampled(lib, wfmt, qmin, qmax, alpha):
+    """16M weights: several 4096-weight tiles per block of the persistent
+    grid.  Bit-exact on a sample (every weight of the first and last tiles and
+    of 150k random positions), counters against the host's own count."""
+    d_out, d_in = 4096, 4096
+    n = d_out * d_in
+    log(f"sr_update large {wfmt} {d_out}x{d_in}")
+    q = _weights(d_out, d_in, wfmt, qmin, qmax, 4096, 7)
+    g = draws((d_out, d_in), 1.0, 11, wfmt == "ternary")
+    flat = g.reshape(-1)
+    flat[3::7919] *= 1e4
+    flat[17::100_003] = np.nan
+    flat[29::100_019] = np.inf
+    n_nonfinite = int(np.count_nonzero(~np.isfinite(flat)))
+    lr = 3e-4 if wfmt == "ternary" else 1e-3
+    w = make_weight(d_out, d_in, wfmt, qmin, qmax, alpha, tensor_id=6)
+    Wq = weight_codes_dev(q, wfmt)
+    counters = torch.zeros((2,), dtype=torch.int64, device=DEV)
+    dqt.dqt_sr_update(w, Wq, torch.from_numpy(g).to(DEV), lr, 77, 5, counters)
+    got = weight_codes_host(Wq, wfmt, d_in).ravel()
+    rng = np.random.default_rng(5)
+    idx = np.unique(np.concatenate([np.arange(4096), np.arange(n - 4096, n),
+                                    rng.choice(n, 150_000, replace=False)])).astype(np.uint64)
+    ii = idx.astype(np.int64)
+    want, _, _ = O.sr_update(q.ravel()[ii], flat[ii], lr, alpha, qmin, qmax, 77, 5, 6, idx=idx)
+    assert np.array_equal(got[ii], want)
+    c = counters.cpu().numpy()
+    assert int(c[0]) == int(np.count_nonzero(got != q.ravel()))
+    assert int(c[1]) == n_nonfinite
+
+
 # ------------------------------------------------------- full train step
 
 def _full_step(wl, li, M=None, sample_rows=None, sample_cols=None):
