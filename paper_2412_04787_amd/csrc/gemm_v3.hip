@@ -46,13 +46,19 @@ namespace v3 {
 using lds_u8 = __attribute__((address_space(3))) uint8_t;
 typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
 
-constexpr int NW = 8;                 // waves per block, 2 (rows) x 4 (cols)
+#ifndef GEMM_NW
+#define GEMM_NW 8
+#endif
+constexpr int NW = GEMM_NW;           // waves per block: 8 (2 x 4 grid) or 4 (2 x 2)
+static_assert(NW == 8 || NW == 4, "8 or 4 waves");
 constexpr int NTH = 64 * NW;
+constexpr int NTD = NTH;             // threads issuing global -> LDS copies
 constexpr int TILE = 256;             // block tile edge (outputs)
-constexpr int WI = 4, WJ = 2;         // MFMA 32x32 blocks per wave
-constexpr int PITCH = 68;             // fp32 words per staged epilogue row (64 + 4)
+constexpr int WI = 4;                 // MFMA 32x32 blocks per wave along rows
+constexpr int WJ = NW == 8 ? 2 : 4;   // ... and along columns
+constexpr int WGC = TILE / (32 * WJ); // waves per row of the wave grid
+constexpr int PITCH = 32 * WJ + 4;    // fp32 words per staged epilogue row
 constexpr int PKB = 32;               // packed ternary bytes per tile row per step (128 codes)
-static_assert(TILE * 2 == NTH, "packed plan: one 16-byte chunk per thread");
 
 // Step geometry for KB reduction bytes per tile row per step (128: one cache
 // line; 64: half a line, used with more stages in flight).  K-contiguous
@@ -62,7 +68,7 @@ template <int KB>
 struct Geo {
   static_assert(KB == 128 || KB == 64, "step of 64 or 128 bytes");
   static constexpr int OPB = TILE * KB;       // bytes per operand per stage
-  static constexpr int NL = OPB / 16 / NTH;   // DMA chunks per thread per operand
+  static constexpr int NL = OPB / 16 / NTD;   // DMA chunks per DMA thread per operand
   static constexpr int CPR = KB / 16;         // K-contiguous 16-byte chunks per row
   static constexpr int KR = KB / 2;           // K-major rows per step
   static constexpr int NKK = KB / 32;         // MFMA sub-steps per step
@@ -168,6 +174,14 @@ __device__ __forceinline__ void block_barrier() {
   __asm__ volatile("" ::: "memory");
 }
 
+// The value x, hidden from the optimiser: per-lane indices derived from it
+// are recomputed where they are used instead of being hoisted out of the
+// tile loop, where they would hold registers across the main loop.
+__device__ __forceinline__ int opaque(int x) {
+  __asm__ volatile("" : "+v"(x));
+  return x;
+}
+
 // Per-thread DMA plan of one operand of one tile: the global address of each
 // of its NL chunks at step 0; the reduction offset (elements, within a step)
 // the chunks cover, which is the same for all of them; and the distance
@@ -176,18 +190,25 @@ __device__ __forceinline__ void block_barrier() {
 template <int MODE, int EB, int KB>
 struct Plan {
   using G = Geo<KB>;
-  static constexpr int NL = G::NL;
+  static constexpr int NL = MODE == KCP ? TILE * PKB / 16 / NTD : G::NL;
+  // K-major: a thread's chunks cover two reduction rows, k and k + KSTEP,
+  // when one wave instruction's 8 rows repeat within a region (4 waves)
+  static constexpr int KSTEP = MODE == KM && NTD < G::KR * 8 ? NTD / 8 : 0;
+  static_assert(KSTEP == 0 || G::KR * 8 == 2 * NTD, "K-major chunks cover at most two reduction rows");
   const uint8_t* g[NL];
   int64_t back;
   int64_t inc;
   int rk;
+  // reduction offset of chunk q (elements within the step) and the distance
+  // back from it to a safe address
+  __device__ int rk_of(int q) const { return rk + (KSTEP && (q & 1) ? KSTEP : 0); }
+  __device__ int64_t back_of(int q, int64_t ld) const { return back + (KSTEP && (q & 1) ? KSTEP * ld : 0); }
 
   __device__ void init(const Opnd& o, int64_t row0, int64_t r_begin, int tid) {
 #pragma unroll
     for (int q = 0; q < NL; ++q) {
-      const int p = q * NTH + tid;                  // physical 16-byte position
+      const int p = q * NTD + tid;                  // physical 16-byte position
       if constexpr (MODE == KCP) {
-        if (q > 0) break;                           // one chunk per thread
         const int row = p >> 1;
         const int c = (p & 1) ^ ((row >> 3) & 1);   // logical 16-byte chunk (64 codes)
         int64_t gr = row0 + row;
@@ -205,14 +226,16 @@ struct Plan {
         rk = 16 * c / EB;
       } else {
         const int region = p / (G::KR * 8);         // 64-column region
-        const int k = (p % (G::KR * 8)) >> 3;       // reduction row within the step (same for every q)
+        const int k = (p % (G::KR * 8)) >> 3;       // reduction row within the step
         const int pc = p & 7;
         const int seg = (pc >> 1) ^ (k & 3);
         int64_t col = row0 + 64 * region + 16 * seg + 8 * (pc & 1);
         if (col > o.n - 8) col = o.n - 8;
         g[q] = o.p + (r_begin + k) * o.ld + 2 * col;
-        back = (int64_t)k * o.ld;
-        rk = k;
+        if (q == 0) {                               // chunks q > 0: rk_of / back_of
+          back = (int64_t)k * o.ld;
+          rk = k;
+        }
       }
     }
     inc = MODE == KC ? KB : MODE == KCP ? PKB : G::KR * o.ld;
@@ -245,7 +268,7 @@ __global__ __launch_bounds__(NTH) void gemm_v3_kernel(const Group<Epi> grp) {
   constexpr int OPB = G::OPB;
   constexpr int NL = G::NL;
   constexpr int SLOTB = slot_bytes<MB, KB>();
-  constexpr int NLB = MB == KCP ? 1 : NL;  // DMA chunks per thread for B
+  constexpr int NLB = Plan<MB, EB, KB>::NL;  // DMA chunks per thread for B
   // as many stages as fit next to the row scales (at most 4)
   constexpr int NS = 4 * SLOTB + TILE * 4 <= 160 * 1024 ? 4 : 3 * SLOTB + TILE * 4 <= 160 * 1024 ? 3 : 2;
   // epilogue rows staged per pass: 16, or 8 when a stage is smaller
@@ -259,7 +282,7 @@ __global__ __launch_bounds__(NTH) void gemm_v3_kernel(const Group<Epi> grp) {
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
-  const int wi = wave >> 2, wj = wave & 3;
+  const int wi = wave / WGC, wj = wave % WGC;
   const int h = lane >> 5;
   const int wave_u = __builtin_amdgcn_readfirstlane(wave);
   const int xcd = blockIdx.x & 7, nbx8 = gridDim.x >> 3;
@@ -291,8 +314,9 @@ __global__ __launch_bounds__(NTH) void gemm_v3_kernel(const Group<Epi> grp) {
     T.rlen = r_end > r_begin ? r_end - r_begin : 0;
     T.nsteps = (int)((T.rlen + BK - 1) / BK);
     T.tail = (T.rlen % BK) != 0;
-    pa.init(P.A, T.i0, r_begin, tid);
-    pb.init(P.B, T.j0, r_begin, tid);
+    const int tid_s = opaque(tid);
+    pa.init(P.A, T.i0, r_begin, tid_s);
+    pb.init(P.B, T.j0, r_begin, tid_s);
     if constexpr (Epi::kRowScale) {
       if (tid < TILE) {
         int64_t i = T.i0 + tid;
@@ -308,32 +332,40 @@ __global__ __launch_bounds__(NTH) void gemm_v3_kernel(const Group<Epi> grp) {
     lds_u8* lb = la + OPB;
     if (!(T.tail && s == T.nsteps - 1)) {
 #pragma unroll
-      for (int q = 0; q < NL; ++q) dma16(pa.g[q] + (int64_t)s * pa.inc, la + q * (NTH * 16));
+      for (int q = 0; q < NL; ++q) dma16(pa.g[q] + (int64_t)s * pa.inc, la + q * (NTD * 16));
 #pragma unroll
-      for (int q = 0; q < NLB; ++q) dma16(pb.g[q] + (int64_t)s * pb.inc, lb + q * (NTH * 16));
+      for (int q = 0; q < NLB; ++q) dma16(pb.g[q] + (int64_t)s * pb.inc, lb + q * (NTD * 16));
     } else {
       const int64_t rbase = (int64_t)s * BK;
-      const bool oa = rbase + pa.rk >= T.rlen, ob = rbase + pb.rk >= T.rlen;
+      const Prob<Epi>& P = grp.p[T.g];
 #pragma unroll
-      for (int q = 0; q < NL; ++q) dma16(oa ? pa.g[q] - pa.back : pa.g[q] + (int64_t)s * pa.inc, la + q * (NTH * 16));
+      for (int q = 0; q < NL; ++q) {
+        const bool o = rbase + pa.rk_of(q) >= T.rlen;
+        dma16(o ? pa.g[q] - pa.back_of(q, P.A.ld) : pa.g[q] + (int64_t)s * pa.inc, la + q * (NTD * 16));
+      }
 #pragma unroll
-      for (int q = 0; q < NLB; ++q) dma16(ob ? pb.g[q] - pb.back : pb.g[q] + (int64_t)s * pb.inc, lb + q * (NTH * 16));
+      for (int q = 0; q < NLB; ++q) {
+        const bool o = rbase + pb.rk_of(q) >= T.rlen;
+        dma16(o ? pb.g[q] - pb.back_of(q, P.B.ld) : pb.g[q] + (int64_t)s * pb.inc, lb + q * (NTD * 16));
+      }
     }
   };
   // zero the chunks this thread loaded past the end of the reduction (its
   // own DMA for that stage has completed)
   // (packed B codes past the end need no zeroing: they meet zeroed A)
   auto zero_tail = [&](int s, int slot, const TileState& T) {
+    const int dtid = tid;
     lds_u8* la = smem + slot * SLOTB;
     lds_u8* lb = la + OPB;
     const int64_t rbase = (int64_t)s * BK;
     const i32x4 z = {0, 0, 0, 0};
-    if (rbase + pa.rk >= T.rlen)
 #pragma unroll
-      for (int q = 0; q < NL; ++q) *(__attribute__((address_space(3))) i32x4*)(la + (q * NTH + tid) * 16) = z;
-    if (MB != KCP && rbase + pb.rk >= T.rlen)
+    for (int q = 0; q < NL; ++q)
+      if (rbase + pa.rk_of(q) >= T.rlen) *(__attribute__((address_space(3))) i32x4*)(la + (q * NTD + dtid) * 16) = z;
+    if constexpr (MB != KCP)
 #pragma unroll
-      for (int q = 0; q < NL; ++q) *(__attribute__((address_space(3))) i32x4*)(lb + (q * NTH + tid) * 16) = z;
+      for (int q = 0; q < NL; ++q)
+        if (rbase + pb.rk_of(q) >= T.rlen) *(__attribute__((address_space(3))) i32x4*)(lb + (q * NTD + dtid) * 16) = z;
   };
 
   using AccV = typename AccT<ELEM == EI8 ? Mfma::I8 : Mfma::BF16>::type;
@@ -447,19 +479,30 @@ __global__ __launch_bounds__(NTH) void gemm_v3_kernel(const Group<Epi> grp) {
   auto compute = [&](int slot) {
     const lds_u8* la = stage_ptr(slot);
     const lds_u8* lb = la + OPB;
+    // (scheduling barriers keep each group of reads ahead of the MFMAs that
+    // precede their use; left alone, the compiler sinks every read next to
+    // its first use and exposes the LDS latency)
     Frags F0, F1;
     if constexpr (ELEM != EF8) {
       read_frags(la, lb, 0, F0);
       read_frags(la, lb, 1, F1);
+      __builtin_amdgcn_sched_barrier(0);
       mfma1(F0);
+      __builtin_amdgcn_sched_barrier(0);
       if constexpr (G::NKK == 4) {
         read_frags(la, lb, 2, F0);
+        __builtin_amdgcn_sched_barrier(0);
         mfma1(F1);
+        __builtin_amdgcn_sched_barrier(0);
         read_frags(la, lb, 3, F1);
+        __builtin_amdgcn_sched_barrier(0);
         mfma1(F0);
+        __builtin_amdgcn_sched_barrier(0);
       }
       mfma1(F1);
     } else {
+      // (e4m3 keeps the compiler's own order: a pair of sub-steps per
+      // instruction leaves no registers for a further pair in flight)
       read_frags(la, lb, 0, F0);
       read_frags(la, lb, 1, F1);
       if constexpr (G::NKK == 4) {
@@ -478,7 +521,11 @@ __global__ __launch_bounds__(NTH) void gemm_v3_kernel(const Group<Epi> grp) {
   // chunks outside the output go to a dummy slot in the workspace)
   constexpr int kStoresBf16 = WI * 32 * (32 * WJ * 2 / 16) / 64;
   constexpr int kStoresF32 = WI * 32 * (32 * WJ * 4 / 16) / 64;
-  static_assert(kStoresF32 + 2 * LPS < 64, "vmcnt range");
+  // the wave's vmcnt counts at most 63 operations in flight (the wave waits
+  // at issue beyond that), so "at most 63 newer" is a correct, if
+  // conservative, wait when more were issued
+  constexpr int kVmMax = 63;
+  static_assert(NS * LPS < kVmMax, "vmcnt range");
   uint8_t* const dummy = reinterpret_cast<uint8_t*>(grp.sched) + 128;
   bool first_tile = true, obf_prev = false;
   for (;;) {
@@ -501,13 +548,15 @@ __global__ __launch_bounds__(NTH) void gemm_v3_kernel(const Group<Epi> grp) {
         // (a fixed number per thread), which may stay in flight, as may the
         // tile's later prefetched steps
         const int ahead = (cur.nsteps < NS - 1 ? cur.nsteps : NS - 1) - 1;
-        const int n = ahead * LPS + (first_tile ? 0 : obf_prev ? kStoresBf16 : kStoresF32);
-        wait_vm_le<kStoresF32 + 2 * LPS>(__builtin_amdgcn_readfirstlane(n));
+        int n = ahead * LPS + (first_tile ? 0 : obf_prev ? kStoresBf16 : kStoresF32);
+        if (n > kVmMax) n = kVmMax;
+        wait_vm_le<kVmMax>(__builtin_amdgcn_readfirstlane(n));
         first_tile = false;
-      } else if (NS == 2 || it + 1 == cur.nsteps) {
-        wait_vm<0>();
       } else {
-        wait_vm<LPS>();                // step it + 1 may still be in flight
+        // copies of steps it + 1 .. it + NS - 2 (those issued) may stay in flight
+        const int newer = cur.nsteps - 1 - it < NS - 2 ? cur.nsteps - 1 - it : NS - 2;
+        if constexpr (NS == 2) wait_vm<0>();
+        else wait_vm_le<(NS - 2) * LPS>(__builtin_amdgcn_readfirstlane(newer * LPS));
       }
       if (cur.tail && it == cur.nsteps - 1) zero_tail(it, slot, cur);
       block_barrier();                 // stage `slot` complete; step it - 1's stage is free
@@ -542,6 +591,7 @@ __global__ __launch_bounds__(NTH) void gemm_v3_kernel(const Group<Epi> grp) {
     // 8 (r / 4) + 4 h + (r mod 4), r = 0..15.  Each wave stages 16 of its
     // rows at a time as fp32 in its own part of stage `last`, then writes
     // whole 16-byte chunks of output rows (8 bf16 or 4 fp32).
+    const int lane_e = opaque(lane), h_e = lane_e >> 5;
     lds_u8* stage = smem + last * SLOTB + wave * (RP * PITCH * 4);
     const bool obf = epi.out_bf16();
 #pragma unroll
@@ -549,7 +599,7 @@ __global__ __launch_bounds__(NTH) void gemm_v3_kernel(const Group<Epi> grp) {
       float sc[16];
 #pragma unroll
       for (int r = 0; r < 16; ++r)
-        sc[r] = Epi::kRowScale ? row_scale[wi * 32 * WI + ta * 32 + 8 * (r >> 2) + 4 * h + (r & 3)]
+        sc[r] = Epi::kRowScale ? row_scale[wi * 32 * WI + ta * 32 + 8 * (r >> 2) + 4 * h_e + (r & 3)]
                                : epi.scale(0);
       // pass `pass` stages the block's rows [RP pass, RP pass + RP), i.e.
       // accumulator entries r = RP/2 pass .. RP/2 pass + RP/2 - 1
@@ -564,8 +614,8 @@ __global__ __launch_bounds__(NTH) void gemm_v3_kernel(const Group<Epi> grp) {
             if constexpr (ELEM == EI8) v = (float)acc[ta][tb][r];
             else v = acc[ta][tb][r];
             v = v * sc[r];
-            const int lr = 8 * ((r >> 2) % (RP / 8)) + 4 * h + (r & 3);
-            *(__attribute__((address_space(3))) float*)(stage + (lr * PITCH + tb * 32 + (lane & 31)) * 4) = v;
+            const int lr = 8 * ((r >> 2) % (RP / 8)) + 4 * h_e + (r & 3);
+            *(__attribute__((address_space(3))) float*)(stage + (lr * PITCH + tb * 32 + (lane_e & 31)) * 4) = v;
           }
         __asm__ volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
         const int64_t ibase = i0 + wi * 32 * WI + ta * 32 + RP * pass;
@@ -576,7 +626,7 @@ __global__ __launch_bounds__(NTH) void gemm_v3_kernel(const Group<Epi> grp) {
           constexpr int CPR = 32 * WJ / EPC;       // chunks per staged row
 #pragma unroll
           for (int c0 = 0; c0 < RP * CPR; c0 += 64) {
-            const int c = c0 + lane;
+            const int c = c0 + lane_e;
             const int rr = c / CPR, cc = c % CPR;
             const int64_t i = ibase + rr;
             const int64_t jj = jbase + cc * EPC;
