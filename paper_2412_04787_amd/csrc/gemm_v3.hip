@@ -58,7 +58,10 @@ constexpr int WI = 4;                 // MFMA 32x32 blocks per wave along rows
 constexpr int WJ = NW == 8 ? 2 : 4;   // ... and along columns
 constexpr int WGC = TILE / (32 * WJ); // waves per row of the wave grid
 constexpr int PITCH = 32 * WJ + 4;    // fp32 words per staged epilogue row
-constexpr int PKB = 32;               // packed ternary bytes per tile row per step (128 codes)
+// packed ternary codes per tile row per step: one code per reduction element,
+// four per byte (32 bytes for an 8-bit step of 128, 16 for a bf16 step of 64)
+template <int KB, int EB>
+constexpr int pkb() { return KB / EB / 4; }
 
 // Step geometry for KB reduction bytes per tile row per step (128: one cache
 // line; 64: half a line, used with more stages in flight).  K-contiguous
@@ -82,8 +85,8 @@ enum Elem { EI8 = 0, EF8 = 1, EBF16 = 2 };
 enum Mode { KC = 0, KM = 1, KCP = 2 };   // KCP: K-contiguous packed ternary codes (B only)
 
 // bytes per stage: A, then B (bf16 / 8-bit operand, or packed ternary codes)
-template <int MB, int KB>
-constexpr int slot_bytes() { return Geo<KB>::OPB + (MB == KCP ? TILE * PKB : Geo<KB>::OPB); }
+template <int MB, int KB, int EB>
+constexpr int slot_bytes() { return Geo<KB>::OPB + (MB == KCP ? TILE * pkb<KB, EB>() : Geo<KB>::OPB); }
 
 
 // Global operand: base of element (row 0, reduction 0), row stride in bytes,
@@ -190,7 +193,10 @@ __device__ __forceinline__ int opaque(int x) {
 template <int MODE, int EB, int KB>
 struct Plan {
   using G = Geo<KB>;
-  static constexpr int NL = MODE == KCP ? TILE * PKB / 16 / NTD : G::NL;
+  static constexpr int PK = pkb<KB, EB>();
+  static constexpr int CH = TILE * PK / 16;   // packed 16-byte chunks per stage
+  // packed codes: all threads (32-byte rows), or the first CH threads (16-byte rows)
+  static constexpr int NL = MODE == KCP ? (CH >= NTD ? CH / NTD : 1) : G::NL;
   // K-major: a thread's chunks cover two reduction rows, k and k + KSTEP,
   // when one wave instruction's 8 rows repeat within a region (4 waves)
   static constexpr int KSTEP = MODE == KM && NTD < G::KR * 8 ? NTD / 8 : 0;
@@ -209,8 +215,10 @@ struct Plan {
     for (int q = 0; q < NL; ++q) {
       const int p = q * NTD + tid;                  // physical 16-byte position
       if constexpr (MODE == KCP) {
-        const int row = p >> 1;
-        const int c = (p & 1) ^ ((row >> 3) & 1);   // logical 16-byte chunk (64 codes)
+        // 32-byte rows: two chunks, swapped on odd groups of 8 rows; 16-byte
+        // rows (bf16 steps): one chunk, whose halves the packing arranges
+        const int row = PK == 32 ? p >> 1 : p;
+        const int c = PK == 32 ? (p & 1) ^ ((row >> 3) & 1) : 0;   // logical 16-byte chunk (64 codes)
         int64_t gr = row0 + row;
         if (gr > o.n - 1) gr = o.n - 1;
         g[q] = o.p + gr * o.ld + r_begin / 4 + 16 * c;
@@ -238,7 +246,7 @@ struct Plan {
         }
       }
     }
-    inc = MODE == KC ? KB : MODE == KCP ? PKB : G::KR * o.ld;
+    inc = MODE == KC ? KB : MODE == KCP ? PK : G::KR * o.ld;
   }
 };
 
@@ -267,16 +275,20 @@ __global__ __launch_bounds__(NTH) void gemm_v3_kernel(const Group<Epi> grp) {
   constexpr int BK = KB / EB;               // reduction elements per step
   constexpr int OPB = G::OPB;
   constexpr int NL = G::NL;
-  constexpr int SLOTB = slot_bytes<MB, KB>();
+  constexpr int SLOTB = slot_bytes<MB, KB, EB>();
+  constexpr int PKB = pkb<KB, EB>();
   constexpr int NLB = Plan<MB, EB, KB>::NL;  // DMA chunks per thread for B
   // as many stages as fit next to the row scales (at most 4)
   constexpr int NS = 4 * SLOTB + TILE * 4 <= 160 * 1024 ? 4 : 3 * SLOTB + TILE * 4 <= 160 * 1024 ? 3 : 2;
   // epilogue rows staged per pass: 16, or 8 when a stage is smaller
   constexpr int RP = NW * 16 * PITCH * 4 <= SLOTB ? 16 : 8;
   static_assert(NW * RP * PITCH * 4 <= SLOTB, "epilogue staging fits in one stage");
-  constexpr int LPS = NL + NLB;            // DMA instructions per thread per stage
+  constexpr int LPS = NL + NLB;            // DMA instructions per thread per stage (at most)
+  // bf16 operand from packed codes: two codes (a nibble) -> two bf16 by table
+  constexpr bool kLutB = MB == KCP && ELEM == EBF16;
   __shared__ __attribute__((aligned(1024))) uint8_t smem_generic[NS * SLOTB];
   __shared__ float row_scale[Epi::kRowScale ? TILE : 1];
+  __shared__ uint32_t code_lut[kLutB ? 16 : 1];
   lds_u8* smem = (lds_u8*)smem_generic;
 
   const int tid = threadIdx.x;
@@ -285,6 +297,17 @@ __global__ __launch_bounds__(NTH) void gemm_v3_kernel(const Group<Epi> grp) {
   const int wi = wave / WGC, wj = wave % WGC;
   const int h = lane >> 5;
   const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+  // packed B rows of 16 bytes need only the first CH threads' copies
+  constexpr int kChB = Plan<MB, EB, KB>::CH;
+  const bool b_copies = MB != KCP || kChB >= NTD || wave_u * 64 < kChB;
+  const int lps = NL + (b_copies ? NLB : 0);   // this wave's copies per stage
+  if constexpr (kLutB) {
+    if (tid < 16) {   // entry n: codes (n & 3, n >> 2) -> bf16 (code - 1), low half first
+      const uint32_t lo = (uint32_t)((0x00003F800000BF80ull >> (16u * (tid & 3))) & 0xFFFFu);
+      const uint32_t hi = (uint32_t)((0x00003F800000BF80ull >> (16u * (tid >> 2))) & 0xFFFFu);
+      code_lut[tid] = lo | (hi << 16);
+    }
+  }
   const int xcd = blockIdx.x & 7, nbx8 = gridDim.x >> 3;
 
   // ---- state of the tile being computed
@@ -333,8 +356,9 @@ __global__ __launch_bounds__(NTH) void gemm_v3_kernel(const Group<Epi> grp) {
     if (!(T.tail && s == T.nsteps - 1)) {
 #pragma unroll
       for (int q = 0; q < NL; ++q) dma16(pa.g[q] + (int64_t)s * pa.inc, la + q * (NTD * 16));
+      if (b_copies)
 #pragma unroll
-      for (int q = 0; q < NLB; ++q) dma16(pb.g[q] + (int64_t)s * pb.inc, lb + q * (NTD * 16));
+        for (int q = 0; q < NLB; ++q) dma16(pb.g[q] + (int64_t)s * pb.inc, lb + q * (NTD * 16));
     } else {
       const int64_t rbase = (int64_t)s * BK;
       const Prob<Epi>& P = grp.p[T.g];
@@ -343,11 +367,12 @@ __global__ __launch_bounds__(NTH) void gemm_v3_kernel(const Group<Epi> grp) {
         const bool o = rbase + pa.rk_of(q) >= T.rlen;
         dma16(o ? pa.g[q] - pa.back_of(q, P.A.ld) : pa.g[q] + (int64_t)s * pa.inc, la + q * (NTD * 16));
       }
+      if (b_copies)
 #pragma unroll
-      for (int q = 0; q < NLB; ++q) {
-        const bool o = rbase + pb.rk_of(q) >= T.rlen;
-        dma16(o ? pb.g[q] - pb.back_of(q, P.B.ld) : pb.g[q] + (int64_t)s * pb.inc, lb + q * (NTD * 16));
-      }
+        for (int q = 0; q < NLB; ++q) {
+          const bool o = rbase + pb.rk_of(q) >= T.rlen;
+          dma16(o ? pb.g[q] - pb.back_of(q, P.B.ld) : pb.g[q] + (int64_t)s * pb.inc, lb + q * (NTD * 16));
+        }
     }
   };
   // zero the chunks this thread loaded past the end of the reduction (its
@@ -383,7 +408,9 @@ __global__ __launch_bounds__(NTH) void gemm_v3_kernel(const Group<Epi> grp) {
     u32x2 ka[WI][2], kb[WJ][2];
     uint32_t pb[WJ];          // packed codes (16 per lane), expanded at use
   };
-  auto read_frags = [&](const lds_u8* la, const lds_u8* lb, int kk, Frags& F) {
+  // pk: bf16 steps from packed codes, this lane's 64 bits of each B row
+  // (sub-step kk in bits 16 kk .. 16 kk + 15, read once per step)
+  auto read_frags = [&](const lds_u8* la, const lds_u8* lb, int kk, Frags& F, const u32x2* pk) {
 #pragma unroll
     for (int t = 0; t < WI; ++t) {
       if constexpr (MA == KC) {
@@ -400,7 +427,11 @@ __global__ __launch_bounds__(NTH) void gemm_v3_kernel(const Group<Epi> grp) {
     }
 #pragma unroll
     for (int t = 0; t < WJ; ++t) {
-      if constexpr (MB == KCP) {
+      if constexpr (kLutB) {
+        const uint32_t x16 = (pk[t][kk >> 1] >> (16 * (kk & 1))) & 0xFFFFu;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) F.fb[t][i] = (int)code_lut[(x16 >> (4 * i)) & 0xFu];
+      } else if constexpr (MB == KCP) {
         const int row = wj * 32 * WJ + t * 32 + frow;
         const int w = 2 * kk + h;                  // 4-byte word of the row's 32 bytes
         const int pos = 4 * ((w >> 2) ^ ((row >> 3) & 1)) + (w & 3);
@@ -420,7 +451,8 @@ __global__ __launch_bounds__(NTH) void gemm_v3_kernel(const Group<Epi> grp) {
   };
   auto opa = [&](const Frags& F, int t) { return MA == KC ? F.fa[t] : join(F.ka[t][0], F.ka[t][1]); };
   auto opb = [&](const Frags& F, int t) {
-    if constexpr (MB == KCP) return expand16(F.pb[t], ELEM == EF8 ? 0x003800B8u : 0x000100FFu);
+    if constexpr (kLutB) return F.fb[t];
+    else if constexpr (MB == KCP) return expand16(F.pb[t], ELEM == EF8 ? 0x003800B8u : 0x000100FFu);
     else return MB == KC ? F.fb[t] : join(F.kb[t][0], F.kb[t][1]);
   };
   // MFMAs of one sub-step (int8 / bf16), or of two sub-steps (e4m3, whose
@@ -482,19 +514,28 @@ __global__ __launch_bounds__(NTH) void gemm_v3_kernel(const Group<Epi> grp) {
     // (scheduling barriers keep each group of reads ahead of the MFMAs that
     // precede their use; left alone, the compiler sinks every read next to
     // its first use and exposes the LDS latency)
+    u32x2 pk[WJ];
+    if constexpr (kLutB) {
+#pragma unroll
+      for (int t = 0; t < WJ; ++t) {
+        // the packing swaps the two 8-byte halves of rows with bit 4 set
+        const int row = wj * 32 * WJ + t * 32 + frow;
+        pk[t] = *(const __attribute__((address_space(3))) u32x2*)(lb + row * 16 + 8 * (h ^ ((row >> 4) & 1)));
+      }
+    }
     Frags F0, F1;
     if constexpr (ELEM != EF8) {
-      read_frags(la, lb, 0, F0);
-      read_frags(la, lb, 1, F1);
+      read_frags(la, lb, 0, F0, pk);
+      read_frags(la, lb, 1, F1, pk);
       __builtin_amdgcn_sched_barrier(0);
       mfma1(F0);
       __builtin_amdgcn_sched_barrier(0);
       if constexpr (G::NKK == 4) {
-        read_frags(la, lb, 2, F0);
+        read_frags(la, lb, 2, F0, pk);
         __builtin_amdgcn_sched_barrier(0);
         mfma1(F1);
         __builtin_amdgcn_sched_barrier(0);
-        read_frags(la, lb, 3, F1);
+        read_frags(la, lb, 3, F1, pk);
         __builtin_amdgcn_sched_barrier(0);
         mfma1(F0);
         __builtin_amdgcn_sched_barrier(0);
@@ -503,13 +544,13 @@ __global__ __launch_bounds__(NTH) void gemm_v3_kernel(const Group<Epi> grp) {
     } else {
       // (e4m3 keeps the compiler's own order: a pair of sub-steps per
       // instruction leaves no registers for a further pair in flight)
-      read_frags(la, lb, 0, F0);
-      read_frags(la, lb, 1, F1);
+      read_frags(la, lb, 0, F0, pk);
+      read_frags(la, lb, 1, F1, pk);
       if constexpr (G::NKK == 4) {
         Frags F2, F3;
-        read_frags(la, lb, 2, F2);
+        read_frags(la, lb, 2, F2, pk);
         mfma2(F0, F1);
-        read_frags(la, lb, 3, F3);
+        read_frags(la, lb, 3, F3, pk);
         mfma2(F2, F3);
       } else {
         mfma2(F0, F1);
@@ -548,7 +589,7 @@ __global__ __launch_bounds__(NTH) void gemm_v3_kernel(const Group<Epi> grp) {
         // (a fixed number per thread), which may stay in flight, as may the
         // tile's later prefetched steps
         const int ahead = (cur.nsteps < NS - 1 ? cur.nsteps : NS - 1) - 1;
-        int n = ahead * LPS + (first_tile ? 0 : obf_prev ? kStoresBf16 : kStoresF32);
+        int n = ahead * lps + (first_tile ? 0 : obf_prev ? kStoresBf16 : kStoresF32);
         if (n > kVmMax) n = kVmMax;
         wait_vm_le<kVmMax>(__builtin_amdgcn_readfirstlane(n));
         first_tile = false;
@@ -556,7 +597,7 @@ __global__ __launch_bounds__(NTH) void gemm_v3_kernel(const Group<Epi> grp) {
         // copies of steps it + 1 .. it + NS - 2 (those issued) may stay in flight
         const int newer = cur.nsteps - 1 - it < NS - 2 ? cur.nsteps - 1 - it : NS - 2;
         if constexpr (NS == 2) wait_vm<0>();
-        else wait_vm_le<(NS - 2) * LPS>(__builtin_amdgcn_readfirstlane(newer * LPS));
+        else wait_vm_le<(NS - 2) * LPS>(__builtin_amdgcn_readfirstlane(newer * lps));
       }
       if (cur.tail && it == cur.nsteps - 1) zero_tail(it, slot, cur);
       block_barrier();                 // stage `slot` complete; step it - 1's stage is free
@@ -683,6 +724,56 @@ __device__ __forceinline__ int seg_of_block(const SegTab& t) {
   int s = 0;
   while (s + 1 < t.n && (int)blockIdx.x >= t.b0[s + 1]) ++s;
   return s;
+}
+
+// Packed ternary codes q [d_out][d_in / 4 bytes] -> the B operand of dX in
+// packed form: row k (input feature) holds the codes of column k of q in
+// steps of 64 output features, 16 bytes per step (ld = 16 ceil(d_out / 64)).
+// Within a step, codes n = 64 st + 16 kk + 8 h + e go to 16-bit word kk of
+// the 8-byte half h (e at bits 2 e), the halves swapped when bit 4 of k is
+// set (the GEMM reads a lane's half with one 8-byte LDS read, free of bank
+// conflicts).  Past d_out the code is 1 (zero).
+struct TpTab {
+  const uint8_t* src[MAXG];
+  uint8_t* dst[MAXG];
+  int32_t d_out[MAXG], d_in[MAXG];
+  int32_t b0[MAXG + 1];
+  int32_t n;
+};
+
+__global__ __launch_bounds__(256) void pack_codes_t_kernel(const TpTab tab) {
+  int s = 0;
+  while (s + 1 < tab.n && (int)blockIdx.x >= tab.b0[s + 1]) ++s;
+  const int d_out = tab.d_out[s], d_in = tab.d_in[s];
+  const int n16 = d_in / 16, nst = (d_out + 63) / 64;
+  const int64_t t = (int64_t)(blockIdx.x - tab.b0[s]) * 256 + threadIdx.x;
+  if (t >= (int64_t)n16 * nst) return;
+  const int j16 = (int)(t % n16), st = (int)(t / n16);   // 16 input features, one step
+  const uint8_t* src = tab.src[s] + 4 * j16;
+  const int ldw = d_in / 4;
+  uint32_t out[16][4];
+#pragma unroll
+  for (int jj = 0; jj < 16; ++jj)
+#pragma unroll
+    for (int w = 0; w < 4; ++w) out[jj][w] = 0;
+#pragma unroll
+  for (int e = 0; e < 64; ++e) {
+    const int r = st * 64 + e;
+    const uint32_t w = r < d_out ? *reinterpret_cast<const uint32_t*>(src + (int64_t)r * ldw) : 0x55555555u;
+    const int kk = e >> 4, hh = (e >> 3) & 1, ee = e & 7;
+    const int word = 2 * hh + (kk >> 1);                  // dword of the 16 bytes
+    const int shift = 16 * (kk & 1) + 2 * ee;
+#pragma unroll
+    for (int jj = 0; jj < 16; ++jj) out[jj][word] |= ((w >> (2 * jj)) & 3u) << shift;
+  }
+  const int ldq = 16 * nst;
+  const bool swap = (j16 & 1) != 0;                        // bit 4 of k = 16 j16 + jj
+#pragma unroll
+  for (int jj = 0; jj < 16; ++jj) {
+    const uint4 v = swap ? make_uint4(out[jj][2], out[jj][3], out[jj][0], out[jj][1])
+                         : make_uint4(out[jj][0], out[jj][1], out[jj][2], out[jj][3]);
+    *reinterpret_cast<uint4*>(tab.dst[s] + (int64_t)(16 * j16 + jj) * ldq + 16 * st) = v;
+  }
 }
 
 // Packed ternary codes -> one operand byte (int8 or e4m3) or one bf16 per
@@ -854,6 +945,9 @@ using namespace v3;
 #ifndef KB_BWD
 #define KB_BWD 128
 #endif
+#ifndef DX_PACKED_B
+#define DX_PACKED_B 0
+#endif
 
 static size_t align256(size_t n) { return (n + 255) / 256 * 256; }
 
@@ -970,25 +1064,12 @@ BwdPlan plan_bwd_batch(int n, const LinearIO* io, int64_t M) {
 hipError_t launch_dx_batch(const BatchCfg& c, const LinearIO* io, uint8_t* ws, const BwdPlan& P,
                            hipStream_t stream) {
   if (c.M == 0 || c.n == 0) return hipSuccess;
-  SegTab tab{};
-  tab.n = c.n;
-  for (int l = 0; l < c.n; ++l) {
-    tab.src[l] = io[l].Wq;
-    tab.dst[l] = ws + P.q_off[l];
-    tab.n16[l] = io[l].d_out * io[l].d_in / 16;
-  }
-  const int32_t blocks = seal(tab);
-  if (c.w_ternary)
-    hipLaunchKernelGGL(unpack_ternary_kernel<2>, dim3(blocks), dim3(256), 0, stream, tab);
-  else
-    hipLaunchKernelGGL(int8_to_bf16_kernel, dim3(blocks), dim3(256), 0, stream, tab);
   // dX[m, k] = alpha sum_n dY[m, n] q[n, k]: I = M, J = d_in, R = d_out
   Group<EpiScale> grp{};
   grp.ng = c.n;
   for (int l = 0; l < c.n; ++l) {
     Prob<EpiScale>& p = grp.p[l];
     p.A = Opnd{static_cast<const uint8_t*>(io[l].dY), io[l].d_out * 2, c.M};
-    p.B = Opnd{ws + P.q_off[l], io[l].d_in * 2, io[l].d_in};
     p.epi = EpiScale{io[l].dX, io[l].d_in, c.out_bf16, io[l].alpha};
     p.I = c.M;
     p.J = io[l].d_in;
@@ -996,6 +1077,40 @@ hipError_t launch_dx_batch(const BatchCfg& c, const LinearIO* io, uint8_t* ws, c
     p.split_len = io[l].d_out;
     p.nbz = 1;
   }
+  if (c.w_ternary && DX_PACKED_B) {
+    // codes stay packed: transposed into 16-byte steps, expanded in the GEMM
+    // (fewer bytes per step, but the table expansion costs more than the
+    // copies it saves in the current main loop)
+    TpTab tab{};
+    tab.n = c.n;
+    int32_t blocks = 0;
+    for (int l = 0; l < c.n; ++l) {
+      tab.src[l] = static_cast<const uint8_t*>(io[l].Wq);
+      tab.dst[l] = ws + P.q_off[l];
+      tab.d_out[l] = (int32_t)io[l].d_out;
+      tab.d_in[l] = (int32_t)io[l].d_in;
+      tab.b0[l] = blocks;
+      blocks += (int32_t)(((io[l].d_in / 16) * ((io[l].d_out + 63) / 64) + 255) / 256);
+      grp.p[l].B = Opnd{ws + P.q_off[l], 16 * ((io[l].d_out + 63) / 64), io[l].d_in};
+    }
+    tab.b0[c.n] = blocks;
+    hipLaunchKernelGGL(pack_codes_t_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, tab);
+    launch_group<EBF16, KC, KCP, 128>(grp, ws, stream);
+    return hipGetLastError();
+  }
+  SegTab tab{};
+  tab.n = c.n;
+  for (int l = 0; l < c.n; ++l) {
+    tab.src[l] = io[l].Wq;
+    tab.dst[l] = ws + P.q_off[l];
+    tab.n16[l] = io[l].d_out * io[l].d_in / 16;
+    grp.p[l].B = Opnd{ws + P.q_off[l], io[l].d_in * 2, io[l].d_in};
+  }
+  const int32_t blocks = seal(tab);
+  if (c.w_ternary)
+    hipLaunchKernelGGL(unpack_ternary_kernel<2>, dim3(blocks), dim3(256), 0, stream, tab);
+  else
+    hipLaunchKernelGGL(int8_to_bf16_kernel, dim3(blocks), dim3(256), 0, stream, tab);
   launch_group<EBF16, KC, KM, KB_BWD>(grp, ws, stream);
   return hipGetLastError();
 }
