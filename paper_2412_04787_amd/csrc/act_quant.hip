@@ -105,13 +105,16 @@ __global__ __launch_bounds__(256) void act_quant_kernel(const ActTab tab) {
 #pragma unroll
     for (int c = 0; c < NCH; ++c) {
       const int idx = lane + kWave * c;
-      if (idx < nchunk) {
-        raw[c] = __builtin_nontemporal_load(reinterpret_cast<const i32x4v*>(xr + idx * E));
-        float v[E];
-        C::decode(raw[c], v);
+      raw[c] = __builtin_nontemporal_load(reinterpret_cast<const i32x4v*>(xr + (idx < nchunk ? idx : nchunk - 1) * E));
+    }
 #pragma unroll
-        for (int i = 0; i < E; ++i) amax = fmaxf(amax, fabsf(v[i]));
-      }
+    for (int c = 0; c < NCH; ++c) {
+      float v[E];
+      C::decode(raw[c], v);
+      float m = 0.0f;
+#pragma unroll
+      for (int i = 0; i < E; ++i) m = fmaxf(m, fabsf(v[i]));
+      amax = lane + kWave * c < nchunk ? fmaxf(amax, m) : amax;
     }
     amax = wave_max(amax);
     const float g = fmaxf(amax, 1e-5f);
@@ -145,6 +148,78 @@ __global__ __launch_bounds__(256) void act_quant_kernel(const ActTab tab) {
   }
 }
 
+// Rows of up to 16 x 16 chunks: 16 lanes per row, 4 rows per wave, 16 rows
+// per block.  A row's chunks are lane, lane + 16, ... (each load instruction
+// reads 256 contiguous bytes of 4 rows) and stay in registers; the row max
+// is formed by rotations within the 16-lane DPP row, without LDS.
+__device__ __forceinline__ float row16_max(float v) {
+  v = fmaxf(v, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x128, 0xF, 0xF, false)));
+  v = fmaxf(v, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x124, 0xF, 0xF, false)));
+  v = fmaxf(v, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x122, 0xF, 0xF, false)));
+  v = fmaxf(v, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x121, 0xF, 0xF, false)));
+  return v;
+}
+constexpr int kRows16 = 16;   // rows per block of the 16-lane kernel
+
+template <typename TX, bool E4M3, int NCH>
+__global__ __launch_bounds__(256) void act_quant16_kernel(const ActTab tab) {
+  using C = RowChunk<TX>;
+  constexpr int E = C::kElems;
+  const int s = seg_of(tab);
+  const int lane = threadIdx.x & (kWave - 1);
+  const int l16 = lane & 15;
+  const int64_t row = (int64_t)(blockIdx.x - tab.b0[s]) * kRows16 + (threadIdx.x >> 4);
+  const bool valid = row < tab.M;
+  const int K = tab.K[s];
+  const TX* xr = static_cast<const TX*>(tab.X[s]) + (valid ? row : 0) * (int64_t)K;
+  uint8_t* qr = tab.Xq[s] + row * (int64_t)K;
+  const int nchunk = K / E;
+  const float qscale = E4M3 ? 448.0f : 127.0f;
+  // every lane loads all NCH chunks (past the row end it reloads the last
+  // one), so the loads issue back to back; those chunks do not count
+  i32x4v raw[NCH];
+  float amax = 0.0f;
+#pragma unroll
+  for (int c = 0; c < NCH; ++c) {
+    const int idx = l16 + 16 * c;
+    raw[c] = __builtin_nontemporal_load(reinterpret_cast<const i32x4v*>(xr + (idx < nchunk ? idx : nchunk - 1) * E));
+  }
+#pragma unroll
+  for (int c = 0; c < NCH; ++c) {
+    float v[E];
+    C::decode(raw[c], v);
+    float m = 0.0f;
+#pragma unroll
+    for (int i = 0; i < E; ++i) m = fmaxf(m, fabsf(v[i]));
+    amax = l16 + 16 * c < nchunk ? fmaxf(amax, m) : amax;
+  }
+  amax = row16_max(amax);
+  const float g = fmaxf(amax, 1e-5f);
+  const float inv = qscale / g;   // correctly rounded fp32 division
+  if (valid && l16 == 0) tab.xdq[s][row] = g / qscale;
+#pragma unroll
+  for (int c = 0; c < NCH; ++c) {
+    const int idx = l16 + 16 * c;
+    if (valid && idx < nchunk) {
+      float v[E];
+      C::decode(raw[c], v);
+      quantise_store<E4M3, E>(v, inv, qr + idx * E);
+    }
+  }
+}
+
+template <typename TX, bool E4M3>
+void launch16_t(const ActTab& tab, int nch, int32_t blocks, hipStream_t stream) {
+  const dim3 grid((unsigned)blocks), block(256);
+  switch (nch) {
+    case 1: hipLaunchKernelGGL((act_quant16_kernel<TX, E4M3, 1>), grid, block, 0, stream, tab); break;
+    case 2: hipLaunchKernelGGL((act_quant16_kernel<TX, E4M3, 2>), grid, block, 0, stream, tab); break;
+    case 4: hipLaunchKernelGGL((act_quant16_kernel<TX, E4M3, 4>), grid, block, 0, stream, tab); break;
+    case 8: hipLaunchKernelGGL((act_quant16_kernel<TX, E4M3, 8>), grid, block, 0, stream, tab); break;
+    default: hipLaunchKernelGGL((act_quant16_kernel<TX, E4M3, 16>), grid, block, 0, stream, tab); break;
+  }
+}
+
 template <typename TX, bool E4M3>
 void launch_t(const ActTab& tab, int nch, int32_t blocks, hipStream_t stream) {
   const dim3 grid((unsigned)blocks), block(kRowsPerBlock * kWave);
@@ -161,35 +236,64 @@ void launch_t(const ActTab& tab, int nch, int32_t blocks, hipStream_t stream) {
 
 }  // namespace
 
+// Kernel variant of a row of `chunks` 16-byte chunks: 16 lanes per row with
+// NCH chunks per lane (code 16 + NCH), or a whole wave per row with NCH
+// chunks per lane (code 64 + NCH; NCH 0: two passes over the row).
+static int act_variant(int chunks) {
+  if (chunks <= 16 * 16) {
+    const int per = (chunks + 15) / 16;
+    for (int c : {1, 2, 4, 8, 16})
+      if (per <= c) return 16 + c;
+  }
+  const int per = (chunks + kWave - 1) / kWave;
+  for (int c : {1, 2, 4, 8, 16, 24})
+    if (per <= c) return 64 + c;
+  return 64;
+}
+
 hipError_t launch_act_quant_batch(int n, const ActIO* io, bool x_bf16, int64_t M, bool e4m3,
                                   hipStream_t stream) {
   if (M == 0 || n == 0) return hipSuccess;
-  ActTab tab{};
-  tab.n = n;
-  tab.M = M;
   const int E = x_bf16 ? 8 : 4;
-  int32_t blocks = 0;
-  int max_per_lane = 0;
-  for (int s = 0; s < n; ++s) {
-    tab.X[s] = io[s].X;
-    tab.Xq[s] = static_cast<uint8_t*>(io[s].Xq);
-    tab.xdq[s] = io[s].xdq;
-    tab.K[s] = io[s].K;
-    tab.b0[s] = blocks;
-    blocks += (int32_t)((M + kRowsPerBlock - 1) / kRowsPerBlock);
-    const int per_lane = (io[s].K / E + kWave - 1) / kWave;
-    max_per_lane = per_lane > max_per_lane ? per_lane : max_per_lane;
-  }
-  tab.b0[n] = blocks;
-  int nch = 0;
-  for (int c : {1, 2, 4, 8, 16, 24})
-    if (max_per_lane <= c) { nch = c; break; }
-  if (x_bf16) {
-    if (e4m3) launch_t<uint16_t, true>(tab, nch, blocks, stream);
-    else launch_t<uint16_t, false>(tab, nch, blocks, stream);
-  } else {
-    if (e4m3) launch_t<float, true>(tab, nch, blocks, stream);
-    else launch_t<float, false>(tab, nch, blocks, stream);
+  // one launch per kernel variant among the inputs (rows of one length share one)
+  bool done[kMaxBatch] = {};
+  for (int s0 = 0; s0 < n; ++s0) {
+    if (done[s0]) continue;
+    const int var = act_variant(io[s0].K / E);
+    ActTab tab{};
+    tab.M = M;
+    const int rows_per_block = var < 64 ? kRows16 : kRowsPerBlock;
+    int32_t blocks = 0;
+    for (int s = s0; s < n; ++s) {
+      if (done[s] || act_variant(io[s].K / E) != var) continue;
+      done[s] = true;
+      const int t = tab.n++;
+      tab.X[t] = io[s].X;
+      tab.Xq[t] = static_cast<uint8_t*>(io[s].Xq);
+      tab.xdq[t] = io[s].xdq;
+      tab.K[t] = io[s].K;
+      tab.b0[t] = blocks;
+      blocks += (int32_t)((M + rows_per_block - 1) / rows_per_block);
+    }
+    tab.b0[tab.n] = blocks;
+    const int nch = var < 64 ? var - 16 : var - 64;
+    if (var < 64) {
+      if (x_bf16) {
+        if (e4m3) launch16_t<uint16_t, true>(tab, nch, blocks, stream);
+        else launch16_t<uint16_t, false>(tab, nch, blocks, stream);
+      } else {
+        if (e4m3) launch16_t<float, true>(tab, nch, blocks, stream);
+        else launch16_t<float, false>(tab, nch, blocks, stream);
+      }
+    } else {
+      if (x_bf16) {
+        if (e4m3) launch_t<uint16_t, true>(tab, nch, blocks, stream);
+        else launch_t<uint16_t, false>(tab, nch, blocks, stream);
+      } else {
+        if (e4m3) launch_t<float, true>(tab, nch, blocks, stream);
+        else launch_t<float, false>(tab, nch, blocks, stream);
+      }
+    }
   }
   return hipGetLastError();
 }
