@@ -121,16 +121,51 @@ struct SRTab {
 // owns chunk t of 16 consecutive weights (64 bytes of gradient, 4 or 16 bytes
 // of codes, so no two lanes touch the same byte).  The change and non-finite
 // counts are reduced per block and added with one atomic each.
-template <bool TERNARY>
+// Code words of CW weights: 2-bit ternary codes (CW / 4 bytes) or int8
+// codes (CW bytes), as 32-bit words w[0 .. CW / 4 - 1] (ternary: w[0] holds
+// 2 CW bits).
+template <bool TERNARY, int CW>
+struct CodeIO {
+  static constexpr int NWORD = TERNARY ? 1 : CW / 4;
+  __device__ static void load(const uint8_t* wq, int64_t t, uint32_t (&w)[4]) {
+    if constexpr (TERNARY && CW == 16) {
+      w[0] = reinterpret_cast<const uint32_t*>(wq)[t];
+    } else if constexpr (TERNARY) {
+      w[0] = reinterpret_cast<const uint16_t*>(wq)[t];
+    } else if constexpr (CW == 16) {
+      const uint4 v = reinterpret_cast<const uint4*>(wq)[t];
+      w[0] = v.x; w[1] = v.y; w[2] = v.z; w[3] = v.w;
+    } else {
+      const uint2 v = reinterpret_cast<const uint2*>(wq)[t];
+      w[0] = v.x; w[1] = v.y;
+    }
+  }
+  __device__ static void store(uint8_t* wq, int64_t t, const uint32_t (&w)[4]) {
+    if constexpr (TERNARY && CW == 16) reinterpret_cast<uint32_t*>(wq)[t] = w[0];
+    else if constexpr (TERNARY) reinterpret_cast<uint16_t*>(wq)[t] = (uint16_t)w[0];
+    else if constexpr (CW == 16) reinterpret_cast<uint4*>(wq)[t] = make_uint4(w[0], w[1], w[2], w[3]);
+    else reinterpret_cast<uint2*>(wq)[t] = make_uint2(w[0], w[1]);
+  }
+};
+
+// Persistent kernel: block b takes tiles b, b + grid, ...; thread t of a tile
+// owns chunk t of CW consecutive weights (4 CW bytes of gradient, CW / 4 or
+// CW bytes of codes, so no two lanes touch the same byte).  The change and
+// non-finite counts are reduced per block and added with one atomic each.
+template <bool TERNARY, int CW>
 __global__ __launch_bounds__(256) void sr_update_kernel(const SRTab tab,
                                                         unsigned long long* __restrict__ counters) {
+  static_assert(CW == 8 || CW == 16, "8 or 16 weights per lane");
+  using CIO = CodeIO<TERNARY, CW>;
+  constexpr int NG = CW / 4;               // gradient f32x4 per chunk
+  constexpr int NB = CW / 8;               // Philox blocks per chunk
   __shared__ unsigned long long red[2][256 / kWave];
   unsigned long long changed = 0, nonfin = 0;
   const int64_t ntiles = tab.b0[tab.n];
   // Software pipeline: the next tile's gradient and codes are requested
   // before the current tile is computed, so loads stay in flight meanwhile.
   int sidx = 0;
-  f32x4 ng[4];
+  f32x4 ng[NG];
   uint32_t nw[4];
   int64_t nt = 0;
   int ns = 0;
@@ -139,15 +174,10 @@ __global__ __launch_bounds__(256) void sr_update_kernel(const SRTab tab,
     ns = sidx;
     nt = (tl - tab.b0[sidx]) * kChunksPerTile + threadIdx.x;
     if (nt < tab.nchunks[sidx]) {
-      const f32x4* gp = reinterpret_cast<const f32x4*>(tab.grad[sidx] + nt * 16);
+      const f32x4* gp = reinterpret_cast<const f32x4*>(tab.grad[sidx] + nt * CW);
 #pragma unroll
-      for (int u = 0; u < 4; ++u) ng[u] = __builtin_nontemporal_load(gp + u);
-      if constexpr (TERNARY) {
-        nw[0] = reinterpret_cast<const uint32_t*>(tab.wq[sidx])[nt];
-      } else {
-        const uint4 w = reinterpret_cast<const uint4*>(tab.wq[sidx])[nt];
-        nw[0] = w.x; nw[1] = w.y; nw[2] = w.z; nw[3] = w.w;
-      }
+      for (int u = 0; u < NG; ++u) ng[u] = __builtin_nontemporal_load(gp + u);
+      CIO::load(tab.wq[sidx], nt, nw);
     }
   };
   int64_t tile = blockIdx.x;
@@ -155,13 +185,12 @@ __global__ __launch_bounds__(256) void sr_update_kernel(const SRTab tab,
   for (; tile < ntiles; tile += gridDim.x) {
     const int cs = ns;
     const int64_t t = nt;
-    f32x4 gv[4];
+    f32x4 gv[NG];
     uint32_t win[4];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      gv[u] = ng[u];
-      win[u] = nw[u];
-    }
+    for (int u = 0; u < NG; ++u) gv[u] = ng[u];
+#pragma unroll
+    for (int u = 0; u < CIO::NWORD; ++u) win[u] = nw[u];
     if (tile + gridDim.x < ntiles) fetch(tile + gridDim.x);
     if (t >= tab.nchunks[cs]) continue;
     SRArgs a;
@@ -174,16 +203,16 @@ __global__ __launch_bounds__(256) void sr_update_kernel(const SRTab tab,
     a.step = tab.step;
     a.tid = tab.tid[cs];
     uint8_t* __restrict__ wq = tab.wq[cs];
-    const uint64_t blk = (uint64_t)t * 2;
-    const uint4 r0 = philox_block(blk, 0u, a.step, a.tid, a.k0, a.k1);
-    const uint4 r1 = philox_block(blk + 1, 0u, a.step, a.tid, a.k0, a.k1);
-    const uint32_t rw[8] = {r0.x, r0.y, r0.z, r0.w, r1.x, r1.y, r1.z, r1.w};
+    const uint64_t blk = (uint64_t)t * NB;   // Philox block of the chunk's first weight
+    uint4 r[NB];
+#pragma unroll
+    for (int b = 0; b < NB; ++b) r[b] = philox_block(blk + b, 0u, a.step, a.tid, a.k0, a.k1);
 
     // finite check: a product chain stays finite unless some g is inf/NaN
     // (or a product overflows, which only sends the chunk to the full rule)
     float probe = 0.0f;
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
+    for (int u = 0; u < NG; ++u) {
       probe = __builtin_fmaf(gv[u][0], gv[u][1], probe);
       probe = __builtin_fmaf(gv[u][2], gv[u][3], probe);
     }
@@ -191,9 +220,10 @@ __global__ __launch_bounds__(256) void sr_update_kernel(const SRTab tab,
     const float nc = -a.c;
     uint32_t wout[4] = {0, 0, 0, 0};
 #pragma unroll
-    for (int j = 0; j < 16; ++j) {
+    for (int j = 0; j < CW; ++j) {
       const float g = gv[j >> 2][j & 3];
-      const uint32_t word = rw[j >> 1];
+      const uint4& rb = r[j >> 3];
+      const uint32_t word = ((j >> 1) & 3) == 0 ? rb.x : ((j >> 1) & 3) == 1 ? rb.y : ((j >> 1) & 3) == 2 ? rb.z : rb.w;
       const uint32_t P = (j & 1) ? (word | 0xFFFFu) : ((word << 16) | 0xFFFFu);
       if constexpr (TERNARY) {
         const int code = (int)((win[0] >> (2 * j)) & 3u);
@@ -206,32 +236,33 @@ __global__ __launch_bounds__(256) void sr_update_kernel(const SRTab tab,
       }
     }
     if (tiemin <= 0xFFFFu || !__builtin_isfinite(probe)) {
-      // rare (about 16 / 65536 per chunk, or a non-finite gradient): full rule
-      int q[16], nq[16];
+      // rare (about CW / 65536 per chunk, or a non-finite gradient): full rule
+      int q[CW], nq[CW];
 #pragma unroll
-      for (int j = 0; j < 16; ++j)
+      for (int j = 0; j < CW; ++j)
         q[j] = TERNARY ? (int)((win[0] >> (2 * j)) & 3u) - 1
                        : (int)(int8_t)(win[j >> 2] >> (8 * (j & 3)));
       uint32_t ties = 0;
 #pragma unroll
-      for (int j = 0; j < 16; ++j) {
+      for (int j = 0; j < CW; ++j) {
         bool tie, nf;
-        nq[j] = sr_one(q[j], gv[j >> 2][j & 3], half16(j < 8 ? r0 : r1, j & 7), a, tie, nf);
+        nq[j] = sr_one(q[j], gv[j >> 2][j & 3], half16(r[j >> 3], j & 7), a, tie, nf);
         ties |= (tie ? 1u : 0u) << j;
         nonfin += nf ? 1 : 0;
       }
       if (ties) {
-        const uint4 s0 = philox_block(blk, 1u, a.step, a.tid, a.k0, a.k1);
-        const uint4 s1 = philox_block(blk + 1, 1u, a.step, a.tid, a.k0, a.k1);
 #pragma unroll
-        for (int j = 0; j < 16; ++j)
-          if (ties & (1u << j))
-            nq[j] = sr_tie(q[j], gv[j >> 2][j & 3], half16(j < 8 ? s0 : s1, j & 7), a);
+        for (int b = 0; b < NB; ++b) {
+          const uint4 sb = philox_block(blk + b, 1u, a.step, a.tid, a.k0, a.k1);
+#pragma unroll
+          for (int j = 8 * b; j < 8 * b + 8; ++j)
+            if (ties & (1u << j)) nq[j] = sr_tie(q[j], gv[j >> 2][j & 3], half16(sb, j & 7), a);
+        }
       }
 #pragma unroll
       for (int w = 0; w < 4; ++w) wout[w] = 0;
 #pragma unroll
-      for (int j = 0; j < 16; ++j) {
+      for (int j = 0; j < CW; ++j) {
         if constexpr (TERNARY) wout[0] |= (uint32_t)(nq[j] + 1) << (2 * j);
         else wout[j >> 2] |= ((uint32_t)nq[j] & 0xFFu) << (8 * (j & 3));
       }
@@ -240,15 +271,14 @@ __global__ __launch_bounds__(256) void sr_update_kernel(const SRTab tab,
     if constexpr (TERNARY) {
       const uint32_t x = wout[0] ^ win[0];
       changed += __builtin_popcount((x | (x >> 1)) & 0x55555555u);
-      reinterpret_cast<uint32_t*>(wq)[t] = wout[0];
     } else {
 #pragma unroll
-      for (int w = 0; w < 4; ++w) {
+      for (int w = 0; w < CIO::NWORD; ++w) {
         const uint32_t x = wout[w] ^ win[w];
         changed += __builtin_popcount((((x & 0x7F7F7F7Fu) + 0x7F7F7F7Fu) | x) & 0x80808080u);
       }
-      reinterpret_cast<uint4*>(wq)[t] = make_uint4(wout[0], wout[1], wout[2], wout[3]);
     }
+    CIO::store(wq, t, wout);
   }
   if (counters != nullptr) {
     changed = wave_sum_u64(changed);
@@ -296,6 +326,11 @@ static int occupancy_blocks(const void* fn, int threads) {
   return cus * per_cu;
 }
 
+#ifndef SR_CW
+#define SR_CW 8
+#endif
+constexpr int kCW = SR_CW;   // weights per lane
+
 hipError_t launch_sr_update(bool ternary, int n, const SRTensor* t, uint64_t seed, uint32_t step,
                             unsigned long long* counters, hipStream_t stream) {
   SRTab tab{};
@@ -307,7 +342,7 @@ hipError_t launch_sr_update(bool ternary, int n, const SRTensor* t, uint64_t see
   for (int s = 0; s < n; ++s) {
     tab.wq[s] = t[s].wq;
     tab.grad[s] = t[s].grad;
-    tab.nchunks[s] = t[s].nweights / 16;
+    tab.nchunks[s] = t[s].nweights / kCW;
     tab.c[s] = t[s].c;
     tab.L[s] = (float)(t[s].qmax - t[s].qmin + 1);
     tab.qmin[s] = t[s].qmin;
@@ -320,14 +355,14 @@ hipError_t launch_sr_update(bool ternary, int n, const SRTensor* t, uint64_t see
   if (tiles == 0) return hipSuccess;
   // as many blocks as fit on the device at once; each loops over tiles
   static const int resident[2] = {
-      occupancy_blocks(reinterpret_cast<const void*>(sr_update_kernel<false>), 256),
-      occupancy_blocks(reinterpret_cast<const void*>(sr_update_kernel<true>), 256)};
+      occupancy_blocks(reinterpret_cast<const void*>(sr_update_kernel<false, kCW>), 256),
+      occupancy_blocks(reinterpret_cast<const void*>(sr_update_kernel<true, kCW>), 256)};
   const int64_t cap = resident[ternary ? 1 : 0];
   const unsigned blocks = (unsigned)(tiles < cap ? tiles : cap);
   if (ternary)
-    hipLaunchKernelGGL(sr_update_kernel<true>, dim3(blocks), dim3(256), 0, stream, tab, counters);
+    hipLaunchKernelGGL((sr_update_kernel<true, kCW>), dim3(blocks), dim3(256), 0, stream, tab, counters);
   else
-    hipLaunchKernelGGL(sr_update_kernel<false>, dim3(blocks), dim3(256), 0, stream, tab, counters);
+    hipLaunchKernelGGL((sr_update_kernel<false, kCW>), dim3(blocks), dim3(256), 0, stream, tab, counters);
   return hipGetLastError();
 }
 
