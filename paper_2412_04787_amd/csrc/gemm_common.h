@@ -26,6 +26,7 @@ struct EpiFwd {          // y = fl(fl(acc) * fl(xdq[i] * alpha))
   __device__ uint8_t* row(int64_t i, int) const {
     return static_cast<uint8_t*>(y) + i * ld * (bf16 ? 2 : 4);
   }
+  __device__ int64_t row_bytes() const { return ld * (bf16 ? 2 : 4); }
   // scalar path used by the fp32-environment kernels
   __device__ void put(int64_t i, int64_t j, float acc) const {
     const float v = acc * scale(i);
@@ -43,6 +44,7 @@ struct EpiScale {        // y = fl(alpha * acc)
   __device__ uint8_t* row(int64_t i, int) const {
     return static_cast<uint8_t*>(y) + i * ld * (bf16 ? 2 : 4);
   }
+  __device__ int64_t row_bytes() const { return ld * (bf16 ? 2 : 4); }
   __device__ void put(int64_t i, int64_t j, float acc) const {
     const float v = alpha * acc;
     if (bf16) reinterpret_cast<uint16_t*>(y)[i * ld + j] = (uint16_t)f32_to_bf16_bits(v);
@@ -59,6 +61,7 @@ struct EpiPartial {      // fp32 partial sums, one slab per split
   __device__ uint8_t* row(int64_t i, int split) const {
     return reinterpret_cast<uint8_t*>(y + (int64_t)split * slab + i * ld);
   }
+  __device__ int64_t row_bytes() const { return ld * 4; }
   __device__ void put(int64_t i, int64_t j, float acc) const {
     y[(int64_t)blockIdx.z * slab + i * ld + j] = acc;
   }

@@ -57,7 +57,6 @@ constexpr int TILE = 256;             // block tile edge (outputs)
 constexpr int WI = 4;                 // MFMA 32x32 blocks per wave along rows
 constexpr int WJ = NW == 8 ? 2 : 4;   // ... and along columns
 constexpr int WGC = TILE / (32 * WJ); // waves per row of the wave grid
-constexpr int PITCH = 32 * WJ + 4;    // fp32 words per staged epilogue row
 // packed ternary codes per tile row per step: one code per reduction element,
 // four per byte (32 bytes for an 8-bit step of 128, 16 for a bf16 step of 64)
 template <int KB, int EB>
@@ -280,9 +279,7 @@ __global__ __launch_bounds__(NTH) void gemm_v3_kernel(const Group<Epi> grp) {
   constexpr int NLB = Plan<MB, EB, KB>::NL;  // DMA chunks per thread for B
   // as many stages as fit next to the row scales (at most 4)
   constexpr int NS = 4 * SLOTB + TILE * 4 <= 160 * 1024 ? 4 : 3 * SLOTB + TILE * 4 <= 160 * 1024 ? 3 : 2;
-  // epilogue rows staged per pass: 16, or 8 when a stage is smaller
-  constexpr int RP = NW * 16 * PITCH * 4 <= SLOTB ? 16 : 8;
-  static_assert(NW * RP * PITCH * 4 <= SLOTB, "epilogue staging fits in one stage");
+  static_assert(NW * 32 * 128 <= SLOTB, "epilogue staging (32 rows of 128 bytes per wave) fits in one stage");
   constexpr int LPS = NL + NLB;            // DMA instructions per thread per stage (at most)
   // bf16 operand from packed codes: two codes (a nibble) -> two bf16 by table
   constexpr bool kLutB = MB == KCP && ELEM == EBF16;
@@ -463,10 +460,10 @@ __global__ __launch_bounds__(NTH) void gemm_v3_kernel(const Group<Epi> grp) {
 #pragma unroll
       for (int tb = 0; tb < WJ; ++tb) {
         if constexpr (ELEM == EI8)
-          acc[ta][tb] = __builtin_amdgcn_mfma_i32_32x32x32_i8(opa(F, ta), opb(F, tb), acc[ta][tb], 0, 0, 0);
+          acc[ta][tb] = __builtin_amdgcn_mfma_i32_32x32x32_i8(opb(F, tb), opa(F, ta), acc[ta][tb], 0, 0, 0);
         else
-          acc[ta][tb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, opa(F, ta)),
-                                                                __builtin_bit_cast(bf16x8, opb(F, tb)),
+          acc[ta][tb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, opb(F, tb)),
+                                                                __builtin_bit_cast(bf16x8, opa(F, ta)),
                                                                 acc[ta][tb], 0, 0, 0);
       }
   };
@@ -479,7 +476,7 @@ __global__ __launch_bounds__(NTH) void gemm_v3_kernel(const Group<Epi> grp) {
         const i32x8 av = {a0[0], a0[1], a0[2], a0[3], a1[0], a1[1], a1[2], a1[3]};
         const i32x8 bv = {b0[0], b0[1], b0[2], b0[3], b1[0], b1[1], b1[2], b1[3]};
         // both operands e4m3 (format 0), unit E8M0 scales (127 = 2^0)
-        acc[ta][tb] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(av, bv, acc[ta][tb], 0, 0, 0, 127, 0, 127);
+        acc[ta][tb] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(bv, av, acc[ta][tb], 0, 0, 0, 127, 0, 127);
       }
   };
   auto stage_ptr = [&](int slot) { return smem + slot * SLOTB; };
@@ -628,70 +625,85 @@ __global__ __launch_bounds__(NTH) void gemm_v3_kernel(const Group<Epi> grp) {
       slot0 = slotn;
     }
 
-    // Lane (j = lane mod 32, h) of MFMA block (ta, tb) holds column j of rows
-    // 8 (r / 4) + 4 h + (r mod 4), r = 0..15.  Each wave stages 16 of its
-    // rows at a time as fp32 in its own part of stage `last`, then writes
-    // whole 16-byte chunks of output rows (8 bf16 or 4 fp32).
-    const int lane_e = opaque(lane), h_e = lane_e >> 5;
-    lds_u8* stage = smem + last * SLOTB + wave * (RP * PITCH * 4);
+    // The MFMAs take the B fragment as their first operand, so lane
+    // (j = lane mod 32, h) of block (ta, tb) holds row 32 ta + j, columns
+    // 32 tb + 8 (r / 4) + 4 h + (r mod 4), r = 0..15: four consecutive
+    // columns per group of four entries.  Each wave stages 32 rows of 128
+    // bytes at a time in its own part of stage `last` (bf16: both column
+    // blocks of a pair; fp32: one column block), 16-byte chunk c of row
+    // r at chunk c ^ ((r >> 1) & 7), then writes whole 16-byte chunks of
+    // output rows.
+    const int lane_e = opaque(lane), h_e = lane_e >> 5, j_e = lane_e & 31;
+    lds_u8* stage = smem + last * SLOTB + wave * (32 * 128);
     const bool obf = epi.out_bf16();
-#pragma unroll
-    for (int ta = 0; ta < WI; ++ta) {
-      float sc[16];
-#pragma unroll
-      for (int r = 0; r < 16; ++r)
-        sc[r] = Epi::kRowScale ? row_scale[wi * 32 * WI + ta * 32 + 8 * (r >> 2) + 4 * h_e + (r & 3)]
-                               : epi.scale(0);
-      // pass `pass` stages the block's rows [RP pass, RP pass + RP), i.e.
-      // accumulator entries r = RP/2 pass .. RP/2 pass + RP/2 - 1
-#pragma unroll
-      for (int pass = 0; pass < 32 / RP; ++pass) {
-#pragma unroll
-        for (int tb = 0; tb < WJ; ++tb)
-#pragma unroll
-          for (int rr = 0; rr < RP / 2; ++rr) {
-            const int r = RP / 2 * pass + rr;
-            float v;
-            if constexpr (ELEM == EI8) v = (float)acc[ta][tb][r];
-            else v = acc[ta][tb][r];
-            v = v * sc[r];
-            const int lr = 8 * ((r >> 2) % (RP / 8)) + 4 * h_e + (r & 3);
-            *(__attribute__((address_space(3))) float*)(stage + (lr * PITCH + tb * 32 + (lane_e & 31)) * 4) = v;
-          }
+    const int sw_w = (j_e >> 1) & 7;
+    const int rd_row = lane_e >> 3, rd_chunk = lane_e & 7;
+    // one row block (32 rows of the wave): its values in LDS, then its rows
+    auto epi_block = [&](int ta, auto ebytes_tag) {
+      constexpr int EBY = decltype(ebytes_tag)::value;
+      const float sc = Epi::kRowScale ? row_scale[wi * 32 * WI + ta * 32 + j_e] : epi.scale(0);
+      auto value = [&](int tb, int r) {
+        float v;
+        if constexpr (ELEM == EI8) v = (float)acc[ta][tb][r];
+        else v = acc[ta][tb][r];
+        return v * sc;
+      };
+      // stores the staged 32 x 128 bytes: columns from `col0` (elements)
+      // (every lane stores every time, chunks outside the output to a dummy
+      // slot, so the number of stores in flight is known)
+      auto store_staged = [&](int col0) {
         __asm__ volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-        const int64_t ibase = i0 + wi * 32 * WI + ta * 32 + RP * pass;
-        const int64_t jbase = j0 + wj * 32 * WJ;
-        auto store_rows = [&](auto ebytes_tag) {
-          constexpr int EBY = decltype(ebytes_tag)::value;
-          constexpr int EPC = 16 / EBY;            // elements per 16-byte chunk
-          constexpr int CPR = 32 * WJ / EPC;       // chunks per staged row
+        const int64_t jj = j0 + wj * 32 * WJ + col0 + rd_chunk * (16 / EBY);
+        const int rows_left = (int)__builtin_amdgcn_readfirstlane(
+            (int)(I - (i0 + wi * 32 * WI + ta * 32) < 32 ? I - (i0 + wi * 32 * WI + ta * 32) : 32));
+        uint8_t* const p0 = epi.row(i0 + wi * 32 * WI + ta * 32 + rd_row, bz) + jj * EBY;
+        const int64_t rstride = 8 * epi.row_bytes();
+        const bool col_ok = jj < J;
 #pragma unroll
-          for (int c0 = 0; c0 < RP * CPR; c0 += 64) {
-            const int c = c0 + lane_e;
-            const int rr = c / CPR, cc = c % CPR;
-            const int64_t i = ibase + rr;
-            const int64_t jj = jbase + cc * EPC;
-            {
-              const bool inside = i < I && jj < J;
-              const lds_u8* src = stage + (rr * PITCH + cc * EPC) * 4;
-              uint8_t* dst = inside ? epi.row(i, bz) + jj * EBY : dummy;
-              if constexpr (EBY == 2) {
-                const f32x4 a = *(const __attribute__((address_space(3))) f32x4*)src;
-                const f32x4 b = *(const __attribute__((address_space(3))) f32x4*)(src + 16);
-                *reinterpret_cast<uint4*>(dst) = make_uint4(pack_bf16x2(a[0], a[1]), pack_bf16x2(a[2], a[3]),
-                                                            pack_bf16x2(b[0], b[1]), pack_bf16x2(b[2], b[3]));
-              } else {
-                *reinterpret_cast<f32x4*>(dst) = *(const __attribute__((address_space(3))) f32x4*)src;
-              }
+        for (int u = 0; u < 4; ++u) {
+          const int row = rd_row + 8 * u;
+          const i32x4 d = *(const __attribute__((address_space(3))) i32x4*)(
+              stage + row * 128 + ((rd_chunk ^ ((row >> 1) & 7)) << 4));
+          uint8_t* dst = (col_ok && row < rows_left) ? p0 + u * rstride : dummy;
+          *reinterpret_cast<i32x4*>(dst) = d;
+        }
+        __asm__ volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+      };
+      if constexpr (EBY == 2) {
+#pragma unroll
+        for (int tp = 0; tp < WJ / 2; ++tp) {
+#pragma unroll
+          for (int t2 = 0; t2 < 2; ++t2)
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+              const int tb = 2 * tp + t2;
+              const u32x2 w = {pack_bf16x2(value(tb, 4 * k), value(tb, 4 * k + 1)),
+                               pack_bf16x2(value(tb, 4 * k + 2), value(tb, 4 * k + 3))};
+              *(__attribute__((address_space(3))) u32x2*)(
+                  stage + j_e * 128 + (((4 * t2 + k) ^ sw_w) << 4) + 8 * h_e) = w;
             }
+          store_staged(64 * tp);
+        }
+      } else {
+#pragma unroll
+        for (int tb = 0; tb < WJ; ++tb) {
+#pragma unroll
+          for (int k = 0; k < 4; ++k) {
+            const f32x4 w = {value(tb, 4 * k), value(tb, 4 * k + 1), value(tb, 4 * k + 2), value(tb, 4 * k + 3)};
+            *(__attribute__((address_space(3))) f32x4*)(stage + j_e * 128 + (((2 * k + h_e) ^ sw_w) << 4)) = w;
           }
-        };
-        if (obf) store_rows(std::integral_constant<int, 2>{});
-        else store_rows(std::integral_constant<int, 4>{});
-        obf_prev = obf;
-        __asm__ volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+          store_staged(32 * tb);
+        }
       }
+    };
+    if (obf) {
+#pragma unroll
+      for (int ta = 0; ta < WI; ++ta) epi_block(ta, std::integral_constant<int, 2>{});
+    } else {
+#pragma unroll
+      for (int ta = 0; ta < WI; ++ta) epi_block(ta, std::integral_constant<int, 4>{});
     }
+    obf_prev = obf;
     if (!more) break;
     // a tile without reduction steps has no main-loop barrier before the
     // next epilogue reuses the staging area and the row scales
