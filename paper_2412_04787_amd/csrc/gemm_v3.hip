@@ -281,6 +281,9 @@ __global__ __launch_bounds__(NTH) void gemm_v3_kernel(const Group<Epi> grp) {
   constexpr int NS = 4 * SLOTB + TILE * 4 <= 160 * 1024 ? 4 : 3 * SLOTB + TILE * 4 <= 160 * 1024 ? 3 : 2;
   static_assert(NW * 32 * 128 <= SLOTB, "epilogue staging (32 rows of 128 bytes per wave) fits in one stage");
   constexpr int LPS = NL + NLB;            // DMA instructions per thread per stage (at most)
+  // (measured faster for the int8 forward and for dX; the e4m3 forward and
+  // dW keep the burst after the barrier)
+  constexpr bool kSplitCopies = ELEM == EI8 || (ELEM == EBF16 && !std::is_same<Epi, EpiPartial>::value);
   // bf16 operand from packed codes: two codes (a nibble) -> two bf16 by table
   constexpr bool kLutB = MB == KCP && ELEM == EBF16;
   __shared__ __attribute__((aligned(1024))) uint8_t smem_generic[NS * SLOTB];
@@ -505,7 +508,7 @@ __global__ __launch_bounds__(NTH) void gemm_v3_kernel(const Group<Epi> grp) {
 
   // One step from stage `slot`: sub-step kk+1's fragments load while kk's
   // MFMAs run (e4m3: sub-steps are consumed in pairs).
-  auto compute = [&](int slot) {
+  auto compute = [&](int slot, auto&& mid) {
     const lds_u8* la = stage_ptr(slot);
     const lds_u8* lb = la + OPB;
     // (scheduling barriers keep each group of reads ahead of the MFMAs that
@@ -527,6 +530,8 @@ __global__ __launch_bounds__(NTH) void gemm_v3_kernel(const Group<Epi> grp) {
       __builtin_amdgcn_sched_barrier(0);
       mfma1(F0);
       __builtin_amdgcn_sched_barrier(0);
+      mid();
+      __builtin_amdgcn_sched_barrier(0);
       if constexpr (G::NKK == 4) {
         read_frags(la, lb, 2, F0, pk);
         __builtin_amdgcn_sched_barrier(0);
@@ -547,10 +552,12 @@ __global__ __launch_bounds__(NTH) void gemm_v3_kernel(const Group<Epi> grp) {
         Frags F2, F3;
         read_frags(la, lb, 2, F2, pk);
         mfma2(F0, F1);
+        mid();
         read_frags(la, lb, 3, F3, pk);
         mfma2(F2, F3);
       } else {
         mfma2(F0, F1);
+        mid();
       }
     }
   };
@@ -598,10 +605,17 @@ __global__ __launch_bounds__(NTH) void gemm_v3_kernel(const Group<Epi> grp) {
       }
       if (cur.tail && it == cur.nsteps - 1) zero_tail(it, slot, cur);
       block_barrier();                 // stage `slot` complete; step it - 1's stage is free
-      if (it + NS - 1 < cur.nsteps) issue(it + NS - 1, (slot + NS - 1) % NS, cur);
+      // The two waves of a SIMD take turns: the first half of the waves
+      // issues its copies right after the barrier, the other half after its
+      // first group of MFMAs, so each SIMD has one wave issuing MFMAs while
+      // the other waits for its copies to be taken.
+      const bool copy_now = !kSplitCopies || wave_u < NW / 2;
+      if (copy_now && it + NS - 1 < cur.nsteps) issue(it + NS - 1, (slot + NS - 1) % NS, cur);
       // fetch the next tile early; its value is needed only at the epilogue
       if (it == 0 && tid == 0) fetched = atomicAdd(next_ctr, 1);
-      compute(slot);
+      compute(slot, [&]() {
+        if (!copy_now && it + NS - 1 < cur.nsteps) issue(it + NS - 1, (slot + NS - 1) % NS, cur);
+      });
     }
 
     // epilogue parameters of this tile, then the next tile's first stage
