@@ -802,53 +802,79 @@ __global__ __launch_bounds__(256) void pack_codes_t_kernel(const TpTab tab) {
   }
 }
 
-// Packed ternary codes -> one operand byte (int8 or e4m3) or one bf16 per
-// weight, same [d_out][d_in] row-major order.
-template <int OUT>   // 0: int8, 1: e4m3, 2: bf16
+// Packed ternary codes -> one operand byte (int8 or e4m3) per weight, same
+// [d_out][d_in] row-major order.
+template <int OUT>   // 0: int8, 1: e4m3
 __global__ __launch_bounds__(256) void unpack_ternary_kernel(const SegTab tab) {
   const int s = seg_of_block(tab);
   const int64_t t = (int64_t)(blockIdx.x - tab.b0[s]) * 256 + threadIdx.x;
   if (t >= tab.n16[s]) return;
   const uint32_t w = static_cast<const uint32_t*>(tab.src[s])[t];
-  if constexpr (OUT < 2) {
-    uint32_t o[4];
+  uint32_t o[4];
 #pragma unroll
-    for (int b = 0; b < 4; ++b) {
-      const uint32_t sp = spread_codes((w >> (8 * b)) & 0xFFu);
-      o[b] = OUT == 1 ? codes_to_e4m3x4(sp) : codes_to_i8x4(sp);
-    }
-    static_cast<uint4*>(tab.dst[s])[t] = make_uint4(o[0], o[1], o[2], o[3]);
-  } else {
-    uint32_t o[8];
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const uint32_t c = (w >> (4 * j)) & 0xFu;
-      o[j] = code_to_bf16_bits(c & 3u) | (code_to_bf16_bits(c >> 2) << 16);
-    }
-    uint4* d = static_cast<uint4*>(tab.dst[s]) + 2 * t;
-    d[0] = make_uint4(o[0], o[1], o[2], o[3]);
-    d[1] = make_uint4(o[4], o[5], o[6], o[7]);
+  for (int b = 0; b < 4; ++b) {
+    const uint32_t sp = spread_codes((w >> (8 * b)) & 0xFFu);
+    o[b] = OUT == 1 ? codes_to_e4m3x4(sp) : codes_to_i8x4(sp);
   }
+  static_cast<uint4*>(tab.dst[s])[t] = make_uint4(o[0], o[1], o[2], o[3]);
 }
 
 // int8 codes -> bf16 (|q| <= 128 is exact in bf16).
-__global__ __launch_bounds__(256) void int8_to_bf16_kernel(const SegTab tab) {
-  const int s = seg_of_block(tab);
-  const int64_t t = (int64_t)(blockIdx.x - tab.b0[s]) * 256 + threadIdx.x;
-  if (t >= tab.n16[s]) return;
-  const uint4 v = static_cast<const uint4*>(tab.src[s])[t];
-  const uint32_t w[4] = {v.x, v.y, v.z, v.w};
-  uint32_t o[8];
+// Weights q [d_out][d_in] (packed ternary codes, or int8) -> the B operand of
+// dX with the reduction contiguous: W~T[k][n] = bf16(q[n][k]), rows of d_out
+// elements.  One 64 x 64 tile per block, transposed through LDS.
+struct TrTab {
+  const uint8_t* src[MAXG];
+  uint16_t* dst[MAXG];
+  int32_t d_out[MAXG], d_in[MAXG];
+  int32_t tn[MAXG];           // tiles along n (d_out / 64, rounded up)
+  int32_t b0[MAXG + 1];
+  int32_t n;
+};
+template <bool TERN>
+__global__ __launch_bounds__(256) void unpack_t_kernel(const TrTab tab) {
+  int s = 0;
+  while (s + 1 < tab.n && (int)blockIdx.x >= tab.b0[s + 1]) ++s;
+  const int tile = (int)blockIdx.x - tab.b0[s];
+  const int n0 = (tile % tab.tn[s]) * 64, k0 = (tile / tab.tn[s]) * 64;
+  const int d_out = tab.d_out[s], d_in = tab.d_in[s];
+  __shared__ __attribute__((aligned(16))) uint16_t t_lds[64][72];   // [k][n]
+  const int t = threadIdx.x;
+  {
+    // thread t: row n0 + t / 4, reduction elements k0 + 16 (t mod 4) .. + 15
+    const int nl = t >> 2, kl = (t & 3) * 16;
+    const int n = n0 + nl, k = k0 + kl;
+    uint16_t v[16];
+    if (n < d_out && k < d_in) {
+      if constexpr (TERN) {
+        const uint32_t w = *reinterpret_cast<const uint32_t*>(tab.src[s] + (int64_t)n * (d_in / 4) + k / 4);
 #pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    const uint32_t two = w[j >> 1] >> (16 * (j & 1));
-    const float lo = (float)(int)(int8_t)(two & 0xFFu);
-    const float hi = (float)(int)(int8_t)((two >> 8) & 0xFFu);
-    o[j] = (__float_as_uint(lo) >> 16) | (__float_as_uint(hi) & 0xFFFF0000u);
+        for (int e = 0; e < 16; ++e) v[e] = (uint16_t)code_to_bf16_bits((w >> (2 * e)) & 3u);
+      } else {
+        const uint4 w4 = *reinterpret_cast<const uint4*>(tab.src[s] + (int64_t)n * d_in + k);
+        const uint32_t w[4] = {w4.x, w4.y, w4.z, w4.w};
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const float f = (float)(int)(int8_t)((w[e >> 2] >> (8 * (e & 3))) & 0xFFu);
+          v[e] = (uint16_t)(__float_as_uint(f) >> 16);   // exact: |q| <= 128
+        }
+      }
+    } else {
+#pragma unroll
+      for (int e = 0; e < 16; ++e) v[e] = 0;
+    }
+#pragma unroll
+    for (int e = 0; e < 16; ++e) t_lds[kl + e][nl] = v[e];
   }
-  uint4* d = static_cast<uint4*>(tab.dst[s]) + 2 * t;
-  d[0] = make_uint4(o[0], o[1], o[2], o[3]);
-  d[1] = make_uint4(o[4], o[5], o[6], o[7]);
+  __syncthreads();
+#pragma unroll
+  for (int c = t; c < 64 * 8; c += 256) {
+    const int kl = c >> 3, ch = c & 7;
+    const int k = k0 + kl, n = n0 + ch * 8;
+    if (k < d_in && n < d_out)
+      *reinterpret_cast<uint4*>(tab.dst[s] + (int64_t)k * d_out + n) =
+          *reinterpret_cast<const uint4*>(&t_lds[kl][ch * 8]);
+  }
 }
 
 // X~[m, k] = bf16(fl(value(Xq[m, k]) * xdq[m])).
@@ -1124,20 +1150,27 @@ hipError_t launch_dx_batch(const BatchCfg& c, const LinearIO* io, uint8_t* ws, c
     launch_group<EBF16, KC, KCP, 128>(grp, ws, stream);
     return hipGetLastError();
   }
-  SegTab tab{};
+  // bf16 weights transposed (reduction contiguous), so both operands are
+  // read without the transposing LDS reads
+  TrTab tab{};
   tab.n = c.n;
+  int32_t blocks = 0;
   for (int l = 0; l < c.n; ++l) {
-    tab.src[l] = io[l].Wq;
-    tab.dst[l] = ws + P.q_off[l];
-    tab.n16[l] = io[l].d_out * io[l].d_in / 16;
-    grp.p[l].B = Opnd{ws + P.q_off[l], io[l].d_in * 2, io[l].d_in};
+    tab.src[l] = static_cast<const uint8_t*>(io[l].Wq);
+    tab.dst[l] = reinterpret_cast<uint16_t*>(ws + P.q_off[l]);
+    tab.d_out[l] = (int32_t)io[l].d_out;
+    tab.d_in[l] = (int32_t)io[l].d_in;
+    tab.tn[l] = (int32_t)((io[l].d_out + 63) / 64);
+    tab.b0[l] = blocks;
+    blocks += tab.tn[l] * (int32_t)((io[l].d_in + 63) / 64);
+    grp.p[l].B = Opnd{ws + P.q_off[l], io[l].d_out * 2, io[l].d_in};
   }
-  const int32_t blocks = seal(tab);
+  tab.b0[c.n] = blocks;
   if (c.w_ternary)
-    hipLaunchKernelGGL(unpack_ternary_kernel<2>, dim3(blocks), dim3(256), 0, stream, tab);
+    hipLaunchKernelGGL(unpack_t_kernel<true>, dim3(blocks), dim3(256), 0, stream, tab);
   else
-    hipLaunchKernelGGL(int8_to_bf16_kernel, dim3(blocks), dim3(256), 0, stream, tab);
-  launch_group<EBF16, KC, KM, KB_BWD>(grp, ws, stream);
+    hipLaunchKernelGGL(unpack_t_kernel<false>, dim3(blocks), dim3(256), 0, stream, tab);
+  launch_group<EBF16, KC, KC, KB_BWD>(grp, ws, stream);
   return hipGetLastError();
 }
 
