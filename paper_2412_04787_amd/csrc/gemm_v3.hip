@@ -877,32 +877,70 @@ __global__ __launch_bounds__(256) void unpack_t_kernel(const TrTab tab) {
   }
 }
 
-// X~[m, k] = bf16(fl(value(Xq[m, k]) * xdq[m])).
+// X~T[k, m] = bf16(fl(value(Xq[m, k]) * xdq[m])): the dequantised
+// activations transposed (the reduction of dW, over tokens, contiguous).
+// One 64 x 64 tile per block, transposed through LDS.
+struct DqTab {
+  const uint8_t* src[MAXG];   // Xq [M][K]
+  uint16_t* dst[MAXG];        // X~T [K][Mp]
+  const float* scale[MAXG];   // xdq [M]
+  int32_t K[MAXG];
+  int32_t tm[MAXG];           // tiles along m
+  int32_t b0[MAXG + 1];
+  int32_t n;
+  int64_t M, Mp;              // tokens, and the row stride of X~T (a multiple of 64)
+};
 template <bool E4M3>
-__global__ __launch_bounds__(256) void dequant_act_kernel(const SegTab tab) {
-  const int s = seg_of_block(tab);
-  const int64_t t = (int64_t)(blockIdx.x - tab.b0[s]) * 256 + threadIdx.x;
-  if (t >= tab.n16[s]) return;
-  const float d = tab.scale[s][t / tab.k16[s]];
-  const uint4 v = static_cast<const uint4*>(tab.src[s])[t];
-  const uint32_t w[4] = {v.x, v.y, v.z, v.w};
-  uint32_t o[8];
+__global__ __launch_bounds__(256) void dequant_t_kernel(const DqTab tab) {
+  int s = 0;
+  while (s + 1 < tab.n && (int)blockIdx.x >= tab.b0[s + 1]) ++s;
+  const int tile = (int)blockIdx.x - tab.b0[s];
+  const int64_t M = tab.M;
+  const int K = tab.K[s];
+  const int64_t m0 = (int64_t)(tile % tab.tm[s]) * 64;
+  const int k0 = (tile / tab.tm[s]) * 64;
+  __shared__ __attribute__((aligned(16))) uint16_t t_lds[64][72];   // [k][m]
+  const int t = threadIdx.x;
+  {
+    // thread t: token m0 + t / 4, features k0 + 16 (t mod 4) .. + 15
+    const int ml = t >> 2, kl = (t & 3) * 16;
+    const int64_t m = m0 + ml;
+    const int k = k0 + kl;
+    uint32_t o[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    if (m < M && k < K) {
+      const float d = tab.scale[s][m];
+      const uint4 v = *reinterpret_cast<const uint4*>(tab.src[s] + m * K + k);
+      const uint32_t w[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    const uint32_t two = w[j >> 1] >> (16 * (j & 1));
-    float a, b;
-    if constexpr (E4M3) {
-      a = e4m3_to_f32(two & 0xFFu);
-      b = e4m3_to_f32((two >> 8) & 0xFFu);
-    } else {
-      a = (float)(int)(int8_t)(two & 0xFFu);
-      b = (float)(int)(int8_t)((two >> 8) & 0xFFu);
+      for (int j = 0; j < 8; ++j) {
+        const uint32_t two = w[j >> 1] >> (16 * (j & 1));
+        float a, b;
+        if constexpr (E4M3) {
+          a = e4m3_to_f32(two & 0xFFu);
+          b = e4m3_to_f32((two >> 8) & 0xFFu);
+        } else {
+          a = (float)(int)(int8_t)(two & 0xFFu);
+          b = (float)(int)(int8_t)((two >> 8) & 0xFFu);
+        }
+        o[j] = pack_bf16x2(a * d, b * d);
+      }
     }
-    o[j] = pack_bf16x2(a * d, b * d);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      t_lds[kl + 2 * j][ml] = (uint16_t)(o[j] & 0xFFFFu);
+      t_lds[kl + 2 * j + 1][ml] = (uint16_t)(o[j] >> 16);
+    }
   }
-  uint4* dst = static_cast<uint4*>(tab.dst[s]) + 2 * t;
-  dst[0] = make_uint4(o[0], o[1], o[2], o[3]);
-  dst[1] = make_uint4(o[4], o[5], o[6], o[7]);
+  __syncthreads();
+#pragma unroll
+  for (int c = t; c < 64 * 8; c += 256) {
+    const int kl = c >> 3, ch = c & 7;
+    const int k = k0 + kl;
+    const int64_t m = m0 + ch * 8;
+    if (k < K && m < M)
+      *reinterpret_cast<uint4*>(tab.dst[s] + (int64_t)k * tab.Mp + m) =
+          *reinterpret_cast<const uint4*>(&t_lds[kl][ch * 8]);
+  }
 }
 
 // dW[l] = sum over splits of the fp32 partials of linear l, in split order
@@ -1071,10 +1109,13 @@ hipError_t launch_fwd_batch(const BatchCfg& c, const LinearIO* io, uint8_t* ws, 
 
 // Backward plan for a batch in the bf16 environment: one split count for
 // every dW product of the batch, and the workspace layout
-//   per linear: [bf16 weights d_out x d_in][bf16 X~ M x d_in][fp32 partials]
+//   per linear: [bf16 weights d_in x d_out][bf16 X~T d_in x Mp][fp32 partials]
+// (Mp: M rounded up to a multiple of 64, the row stride of X~T)
 // (partials sized for the larger of this plan's and the fp32 kernels' split).
 // The split count minimises an estimate of rounds of the persistent grid x
 // steps per tile plus the traffic of the partial sums.
+static int64_t xt_stride(int64_t M) { return (M + 63) / 64 * 64; }
+
 BwdPlan plan_bwd_batch(int n, const LinearIO* io, int64_t M) {
   BwdPlan P{};
   P.wi = 4;
@@ -1105,7 +1146,7 @@ BwdPlan plan_bwd_batch(int n, const LinearIO* io, int64_t M) {
     P.q_off[l] = off;
     off += align256(wn * 2);
     P.xt_off[l] = off;
-    off += align256((size_t)M * (size_t)io[l].d_in * 2);
+    off += align256((size_t)xt_stride(M) * (size_t)io[l].d_in * 2);
     P.part_off[l] = off;
     off += sp > 1 ? align256((size_t)sp * wn * 4) : 0;
   }
@@ -1177,30 +1218,35 @@ hipError_t launch_dx_batch(const BatchCfg& c, const LinearIO* io, uint8_t* ws, c
 hipError_t launch_dw_batch(const BatchCfg& c, const LinearIO* io, uint8_t* ws, const BwdPlan& P,
                            hipStream_t stream) {
   if (c.n == 0) return hipSuccess;
-  // X~ once per distinct quantised input
+  // X~T once per distinct quantised input
   int first[kMaxBatch];
-  SegTab tab{};
+  DqTab tab{};
+  tab.M = c.M;
+  tab.Mp = xt_stride(c.M);
+  int32_t blocks = 0;
   for (int l = 0; l < c.n; ++l) {
     first[l] = l;
     for (int m = 0; m < l; ++m)
       if (io[m].Xq == io[l].Xq && io[m].d_in == io[l].d_in) { first[l] = first[m]; break; }
     if (first[l] == l && c.M > 0) {
       const int s = tab.n++;
-      tab.src[s] = io[l].Xq;
-      tab.dst[s] = ws + P.xt_off[l];
+      tab.src[s] = static_cast<const uint8_t*>(io[l].Xq);
+      tab.dst[s] = reinterpret_cast<uint16_t*>(ws + P.xt_off[l]);
       tab.scale[s] = io[l].xdq;
-      tab.n16[s] = c.M * io[l].d_in / 16;
-      tab.k16[s] = (int32_t)(io[l].d_in / 16);
+      tab.K[s] = (int32_t)io[l].d_in;
+      tab.tm[s] = (int32_t)((c.M + 63) / 64);
+      tab.b0[s] = blocks;
+      blocks += tab.tm[s] * (int32_t)((io[l].d_in + 63) / 64);
     }
   }
+  tab.b0[tab.n] = blocks;
   if (tab.n > 0) {
-    const int32_t blocks = seal(tab);
     if (c.act_e4m3)
-      hipLaunchKernelGGL(dequant_act_kernel<true>, dim3(blocks), dim3(256), 0, stream, tab);
+      hipLaunchKernelGGL(dequant_t_kernel<true>, dim3(blocks), dim3(256), 0, stream, tab);
     else
-      hipLaunchKernelGGL(dequant_act_kernel<false>, dim3(blocks), dim3(256), 0, stream, tab);
+      hipLaunchKernelGGL(dequant_t_kernel<false>, dim3(blocks), dim3(256), 0, stream, tab);
   }
-  // dW[n, k] = sum_m dY[m, n] X~[m, k]: I = d_out, J = d_in, R = M
+  // dW[n, k] = sum_m dY[m, n] X~T[k, m]: I = d_out, J = d_in, R = M
   const int64_t splits = P.splits;
   int64_t len = splits > 1 ? (c.M + splits - 1) / splits : (c.M > 0 ? c.M : 1);
   len = (len + 63) / 64 * 64;
@@ -1210,7 +1256,7 @@ hipError_t launch_dw_batch(const BatchCfg& c, const LinearIO* io, uint8_t* ws, c
     Prob<EpiPartial>& p = grp.p[l];
     const int64_t I = io[l].d_out, J = io[l].d_in;
     p.A = Opnd{static_cast<const uint8_t*>(io[l].dY), I * 2, I};
-    p.B = Opnd{ws + P.xt_off[first[l]], J * 2, J};
+    p.B = Opnd{ws + P.xt_off[first[l]], xt_stride(c.M) * 2, J};
     float* target = splits > 1 ? reinterpret_cast<float*>(ws + P.part_off[l]) : io[l].dW;
     p.epi = EpiPartial{target, J, I * J};
     p.I = I;
@@ -1219,13 +1265,13 @@ hipError_t launch_dw_batch(const BatchCfg& c, const LinearIO* io, uint8_t* ws, c
     p.split_len = len;
     p.nbz = (int32_t)splits;
   }
-  launch_group<EBF16, KM, KM, KB_BWD>(grp, ws, stream);
+  launch_group<EBF16, KM, KC, KB_BWD>(grp, ws, stream);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || splits == 1) return e;
   RedTab red{};
   red.n = c.n;
   red.splits = (int32_t)splits;
-  int32_t blocks = 0;
+  blocks = 0;
   for (int l = 0; l < c.n; ++l) {
     red.src[l] = reinterpret_cast<const float*>(ws + P.part_off[l]);
     red.dst[l] = io[l].dW;
