@@ -105,18 +105,24 @@ class Block:
         self.counters = torch.zeros((2,), dtype=torch.int64, device=dev)
 
 
-def run_step(blk, dqt, step, stream, rec):
+def run_step(blk, dqt, step, stream, rec, split_bwd=False):
     """Enqueue one train step: one batched call per stage (act-quant of every
-    distinct input, forward, dX, dW, SR update) over all linears.  rec(kind, fn) runs fn (or records it
-    into a graph)."""
+    distinct input, forward, backward (dX and dW in one call, which may run
+    them side by side), SR update) over all linears.  With split_bwd the
+    backward is two calls, dX then dW, so each can be timed on its own.
+    rec(kind, fn) runs fn (or records it into a graph)."""
     wl = blk.wl
     M = wl.M
     rec("act_quant", lambda: dqt.dqt_act_quant_batch(blk.act_io, blk.x_t, M, blk.act, stream))
     rec("fwd", lambda: dqt.dqt_linear_fwd_batch(blk.io_all, M, blk.act, blk.y_t, blk.ws, stream))
-    rec("bwd_dx", lambda: dqt.dqt_linear_bwd_batch(blk.io_dx, M, blk.act, blk.dy_t, blk.xt,
-                                                   blk.dx_t, blk.ws, stream))
-    rec("bwd_dw", lambda: dqt.dqt_linear_bwd_batch(blk.io_dw, M, blk.act, blk.dy_t, blk.xt,
-                                                   blk.dx_t, blk.ws, stream))
+    if split_bwd:
+        rec("bwd_dx", lambda: dqt.dqt_linear_bwd_batch(blk.io_dx, M, blk.act, blk.dy_t, blk.xt,
+                                                       blk.dx_t, blk.ws, stream))
+        rec("bwd_dw", lambda: dqt.dqt_linear_bwd_batch(blk.io_dw, M, blk.act, blk.dy_t, blk.xt,
+                                                       blk.dx_t, blk.ws, stream))
+    else:
+        rec("bwd", lambda: dqt.dqt_linear_bwd_batch(blk.io_all, M, blk.act, blk.dy_t, blk.xt,
+                                                    blk.dx_t, blk.ws, stream))
     rec("sr", lambda: dqt.dqt_sr_update_batch(blk.io_all, wl.lr, wl.seed, step, blk.counters,
                                               stream))
 
@@ -278,7 +284,7 @@ def main():
 
         g = torch.cuda.CUDAGraph()
         with torch.cuda.graph(g):
-            run_step(blk, dqt, 1, None, only)
+            run_step(blk, dqt, 1, None, only, split_bwd=True)
         torch.cuda.synchronize()
         e0 = torch.cuda.Event(enable_timing=True)
         e1 = torch.cuda.Event(enable_timing=True)
