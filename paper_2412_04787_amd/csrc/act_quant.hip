@@ -43,7 +43,8 @@ struct ActTab {
   uint8_t* Xq[kMaxBatch];
   float* xdq[kMaxBatch];
   int32_t K[kMaxBatch];
-  int32_t b0[kMaxBatch + 1];   // first block of each input (4 rows per block)
+  int32_t nch[kMaxBatch];      // 16-lane kernel: chunks per lane of each input
+  int32_t b0[kMaxBatch + 1];   // first block of each input
   int32_t n;
   int64_t M;
 };
@@ -162,10 +163,9 @@ __device__ __forceinline__ float row16_max(float v) {
 constexpr int kRows16 = 16;   // rows per block of the 16-lane kernel
 
 template <typename TX, bool E4M3, int NCH>
-__global__ __launch_bounds__(256) void act_quant16_kernel(const ActTab tab) {
+__device__ __forceinline__ void act_quant16_rows(const ActTab& tab, int s) {
   using C = RowChunk<TX>;
   constexpr int E = C::kElems;
-  const int s = seg_of(tab);
   const int lane = threadIdx.x & (kWave - 1);
   const int l16 = lane & 15;
   const int64_t row = (int64_t)(blockIdx.x - tab.b0[s]) * kRows16 + (threadIdx.x >> 4);
@@ -208,16 +208,23 @@ __global__ __launch_bounds__(256) void act_quant16_kernel(const ActTab tab) {
   }
 }
 
+// Inputs of any row length up to 256 chunks in one launch: each block runs
+// the variant of its input (a uniform branch), 16 rows per block.
 template <typename TX, bool E4M3>
-void launch16_t(const ActTab& tab, int nch, int32_t blocks, hipStream_t stream) {
-  const dim3 grid((unsigned)blocks), block(256);
-  switch (nch) {
-    case 1: hipLaunchKernelGGL((act_quant16_kernel<TX, E4M3, 1>), grid, block, 0, stream, tab); break;
-    case 2: hipLaunchKernelGGL((act_quant16_kernel<TX, E4M3, 2>), grid, block, 0, stream, tab); break;
-    case 4: hipLaunchKernelGGL((act_quant16_kernel<TX, E4M3, 4>), grid, block, 0, stream, tab); break;
-    case 8: hipLaunchKernelGGL((act_quant16_kernel<TX, E4M3, 8>), grid, block, 0, stream, tab); break;
-    default: hipLaunchKernelGGL((act_quant16_kernel<TX, E4M3, 16>), grid, block, 0, stream, tab); break;
+__global__ __launch_bounds__(256) void act_quant16_kernel(const ActTab tab) {
+  const int s = seg_of(tab);
+  switch (tab.nch[s]) {
+    case 1: act_quant16_rows<TX, E4M3, 1>(tab, s); break;
+    case 2: act_quant16_rows<TX, E4M3, 2>(tab, s); break;
+    case 4: act_quant16_rows<TX, E4M3, 4>(tab, s); break;
+    case 8: act_quant16_rows<TX, E4M3, 8>(tab, s); break;
+    default: act_quant16_rows<TX, E4M3, 16>(tab, s); break;
   }
+}
+
+template <typename TX, bool E4M3>
+void launch16_t(const ActTab& tab, int32_t blocks, hipStream_t stream) {
+  hipLaunchKernelGGL((act_quant16_kernel<TX, E4M3>), dim3((unsigned)blocks), dim3(256), 0, stream, tab);
 }
 
 template <typename TX, bool E4M3>
@@ -255,37 +262,42 @@ hipError_t launch_act_quant_batch(int n, const ActIO* io, bool x_bf16, int64_t M
                                   hipStream_t stream) {
   if (M == 0 || n == 0) return hipSuccess;
   const int E = x_bf16 ? 8 : 4;
-  // one launch per kernel variant among the inputs (rows of one length share one)
+  // one launch for every input of at most 256 chunks per row (16 lanes per
+  // row, the chunk count per lane chosen per input), one per variant of the
+  // whole-wave kernel for longer rows
   bool done[kMaxBatch] = {};
   for (int s0 = 0; s0 < n; ++s0) {
     if (done[s0]) continue;
     const int var = act_variant(io[s0].K / E);
+    const bool v16 = var < 64;
     ActTab tab{};
     tab.M = M;
-    const int rows_per_block = var < 64 ? kRows16 : kRowsPerBlock;
+    const int rows_per_block = v16 ? kRows16 : kRowsPerBlock;
     int32_t blocks = 0;
     for (int s = s0; s < n; ++s) {
-      if (done[s] || act_variant(io[s].K / E) != var) continue;
+      const int vs = act_variant(io[s].K / E);
+      if (done[s] || (v16 ? vs >= 64 : vs != var)) continue;
       done[s] = true;
       const int t = tab.n++;
       tab.X[t] = io[s].X;
       tab.Xq[t] = static_cast<uint8_t*>(io[s].Xq);
       tab.xdq[t] = io[s].xdq;
       tab.K[t] = io[s].K;
+      tab.nch[t] = v16 ? vs - 16 : 0;
       tab.b0[t] = blocks;
       blocks += (int32_t)((M + rows_per_block - 1) / rows_per_block);
     }
     tab.b0[tab.n] = blocks;
-    const int nch = var < 64 ? var - 16 : var - 64;
-    if (var < 64) {
+    if (v16) {
       if (x_bf16) {
-        if (e4m3) launch16_t<uint16_t, true>(tab, nch, blocks, stream);
-        else launch16_t<uint16_t, false>(tab, nch, blocks, stream);
+        if (e4m3) launch16_t<uint16_t, true>(tab, blocks, stream);
+        else launch16_t<uint16_t, false>(tab, blocks, stream);
       } else {
-        if (e4m3) launch16_t<float, true>(tab, nch, blocks, stream);
-        else launch16_t<float, false>(tab, nch, blocks, stream);
+        if (e4m3) launch16_t<float, true>(tab, blocks, stream);
+        else launch16_t<float, false>(tab, blocks, stream);
       }
     } else {
+      const int nch = var - 64;
       if (x_bf16) {
         if (e4m3) launch_t<uint16_t, true>(tab, nch, blocks, stream);
         else launch_t<uint16_t, false>(tab, nch, blocks, stream);
