@@ -281,9 +281,9 @@ __global__ __launch_bounds__(NTH) void gemm_v3_kernel(const Group<Epi> grp) {
   constexpr int NS = 4 * SLOTB + TILE * 4 <= 160 * 1024 ? 4 : 3 * SLOTB + TILE * 4 <= 160 * 1024 ? 3 : 2;
   static_assert(NW * 32 * 128 <= SLOTB, "epilogue staging (32 rows of 128 bytes per wave) fits in one stage");
   constexpr int LPS = NL + NLB;            // DMA instructions per thread per stage (at most)
-  // (measured faster for the int8 forward and for dX; the e4m3 forward and
-  // dW keep the burst after the barrier)
-  constexpr bool kSplitCopies = ELEM == EI8 || (ELEM == EBF16 && !std::is_same<Epi, EpiPartial>::value);
+  // (measured faster for the int8 forward, dX and dW; the e4m3 forward keeps
+  // the burst after the barrier)
+  constexpr bool kSplitCopies = ELEM != EF8;
   // bf16 operand from packed codes: two codes (a nibble) -> two bf16 by table
   constexpr bool kLutB = MB == KCP && ELEM == EBF16;
   __shared__ __attribute__((aligned(1024))) uint8_t smem_generic[NS * SLOTB];
