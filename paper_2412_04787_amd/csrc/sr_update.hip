@@ -3,9 +3,9 @@
 //
 // Memory-bound streaming kernel: per weight it reads the packed code and the
 // fp32 gradient and writes the code back (4.5 B/weight for 2-bit ternary
-// codes, 6 B/weight for int8 codes).  Each lane owns 16 consecutive weights:
-// 64 contiguous bytes of gradient, and 4 (ternary) or 16 (int8) whole bytes of
-// codes, so no two lanes ever touch the same byte.
+// codes, 6 B/weight for int8 codes).  Each lane owns 8 consecutive weights
+// (one Philox block): 32 contiguous bytes of gradient, and 2 (ternary) or 8
+// (int8) whole bytes of codes, so no two lanes ever touch the same byte.
 #include "dqt_launch.h"
 
 namespace dqt {
@@ -86,23 +86,30 @@ __device__ __forceinline__ int sr_tie(int q, float g, uint32_t s16, const SRArgs
 //  * delta = med3(-c * g, -L, L); n = (int)delta truncates toward zero;
 //  * |r| = fract(|delta|) (exact: |delta| - floor(|delta|));
 //  * with P = (p16 << 16) | 0xFFFF, p16 < (T >> 16) iff P < T, and
-//    p16 == (T >> 16) iff (P - T) mod 2^32 <= 0xFFFF, so the running minimum
-//    of P - T flags every element the secondary draw may have to decide.
-// `code` is q plus a per-format offset and [lo, hi] the offset range.
+//    p16 == (T >> 16) iff (P - T) mod 2^32 <= 0xFFFF;
+//  * F = floor(|r| 2^32) (the conversion truncates) is T or T - 1, and
+//    P < F decides as P < T does whenever (P - F) mod 2^32 > 0xFFFF: the two
+//    differ only at P = F = T - 1, and P - T = 0xFFFF (T's low half zero, so
+//    no draw is below T) is decided P >= T by both.  So the running minimum
+//    of P - F flags every element the secondary draw may have to decide.
+// `code` is q plus a per-format offset and [lo, hi] the offset range (one
+// median-of-three clamps).
 __device__ __forceinline__ int sr_fast(int code, float g, uint32_t P, float nc, float L, int lo,
                                        int hi, uint32_t& tiemin) {
   const float delta = __builtin_amdgcn_fmed3f(nc * g, -L, L);
   const int n = (int)delta;
   const float ar = __builtin_amdgcn_fractf(fabsf(delta));
-  const uint32_t T = (uint32_t)ceilf(ar * 4294967296.0f);
-  tiemin = min(tiemin, P - T);
+  const uint32_t F = (uint32_t)(ar * 4294967296.0f);
+  tiemin = min(tiemin, P - F);
   const int sgn = ((int)__float_as_uint(delta) >> 31) | 1;
-  const int v = code + n + (P < T ? sgn : 0);
-  return min(max(v, lo), hi);
+  const int v = code + n + (P < F ? sgn : 0);
+  int r;
+  asm("v_med3_i32 %0, %1, %2, %3" : "=v"(r) : "v"(v), "v"(lo), "v"(hi));
+  return r;
 }
 
 constexpr int kMaxSR = kMaxBatch;
-constexpr int kChunksPerTile = 256;   // one 16-weight chunk per thread
+constexpr int kChunksPerTile = 256;   // one chunk of weights per thread
 // Up to kMaxSR tensors in one launch; tensor s owns the tiles [b0[s], b0[s+1])
 // of 256 chunks each (its last tile may be partial).
 struct SRTab {
@@ -117,10 +124,6 @@ struct SRTab {
   uint32_t k0, k1, step;
 };
 
-// Persistent kernel: block b takes tiles b, b + grid, ...; thread t of a tile
-// owns chunk t of 16 consecutive weights (64 bytes of gradient, 4 or 16 bytes
-// of codes, so no two lanes touch the same byte).  The change and non-finite
-// counts are reduced per block and added with one atomic each.
 // Code words of CW weights: 2-bit ternary codes (CW / 4 bytes) or int8
 // codes (CW bytes), as 32-bit words w[0 .. CW / 4 - 1] (ternary: w[0] holds
 // 2 CW bits).
