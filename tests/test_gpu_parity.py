@@ -59,8 +59,11 @@ def test_act_quant_bit_exact(lib, M, K, x_t, act):
 @pytest.mark.parametrize("x_t", ["f32", "bf16"])
 @pytest.mark.parametrize("act", ["i8", "e4m3"])
 def test_act_quant_batch_matches_oracle(lib, x_t, act):
+    """Inputs of six row lengths in one call: rows of up to 256 chunks share
+    one launch whose blocks run 1, 4, 8 or 16 chunks per lane (by input),
+    longer rows take the whole-wave kernel."""
     M = 257
-    Ks = [768, 2048, 272, 11008]
+    Ks = [768, 2048, 272, 11008, 16, 512]
     ents, seen = [], []
     for i, K in enumerate(Ks):
         X = draws((M, K), 1.0, 11, i, K)
