@@ -193,6 +193,14 @@ dqt_status dqt_linear_bwd_batch(int32_t n, const dqt_linear_io* io, int64_t M, i
   hipStream_t s = static_cast<hipStream_t>(stream);
   uint8_t* wsb = static_cast<uint8_t*>(ws);
   dqt::LinearIO sub[DQT_MAX_BATCH];
+  // every linear wants both gradients on the bf16 matrix-core path: one
+  // launch holds the tiles of both products
+  bool both = M > 0 && dy_t == DQT_BF16 && xt_t == DQT_BF16;
+  for (int l = 0; l < n; ++l) both &= io[l].dX != nullptr && io[l].dW != nullptr;
+  if (both) {
+    dqt::BatchCfg c{n, M, wfmt == DQT_TERNARY2, act_q == DQT_FP8E4M3, dx_t == DQT_BF16};
+    return from_hip(dqt::launch_dxdw_batch(c, L, wsb, P, s));
+  }
   // dX for the linears that want it
   int nx = 0;
   dqt::BwdPlan Px = P;

@@ -64,7 +64,8 @@ struct BatchCfg {
   bool w_ternary, act_e4m3, out_bf16;
 };
 struct BwdPlan {
-  int64_t splits;
+  int64_t splits;        // dW batch splits when dW runs in a launch of its own
+  int64_t splits_dual;   // ... and when it shares one launch with dX
   int wi, wj;       // dW block tile (64 wi) x (64 wj)
   size_t q_off[kMaxBatch], xt_off[kMaxBatch], part_off[kMaxBatch];
   size_t total;
@@ -76,6 +77,9 @@ hipError_t launch_dx_batch(const BatchCfg& c, const LinearIO* io, uint8_t* ws, c
                            hipStream_t stream);
 hipError_t launch_dw_batch(const BatchCfg& c, const LinearIO* io, uint8_t* ws, const BwdPlan& P,
                            hipStream_t stream);
+// dX and dW of every linear of the batch in one launch (bf16 operands).
+hipError_t launch_dxdw_batch(const BatchCfg& c, const LinearIO* io, uint8_t* ws, const BwdPlan& P,
+                             hipStream_t stream);
 // fp32-environment kernels
 hipError_t launch_dx_f32(const DxArgs& a, hipStream_t stream);
 hipError_t launch_dw_f32(const DwArgs& a, hipStream_t stream);

@@ -266,19 +266,36 @@ __device__ __forceinline__ bool locate(const Group<Epi>& grp, int x, int j, int&
   return false;
 }
 
+using lds_f32 = __attribute__((address_space(3))) float;
+using lds_u32 = __attribute__((address_space(3))) uint32_t;
+using lds_i32 = __attribute__((address_space(3))) int;
+
+// Stage geometry of one instantiation: bytes per stage and stages in flight.
+template <int ELEM, int MB, int KB>
+struct StageGeo {
+  static constexpr int EB = ELEM == EBF16 ? 2 : 1;
+  static constexpr int SLOTB = slot_bytes<MB, KB, EB>();
+  // as many stages as fit next to the row scales (at most 4)
+  static constexpr int NS = 4 * SLOTB + TILE * 4 <= 160 * 1024 ? 4 : 3 * SLOTB + TILE * 4 <= 160 * 1024 ? 3 : 2;
+  static constexpr int kBytes = NS * SLOTB;
+};
+
+// The persistent grouped GEMM over the tiles of `grp`, with its LDS passed
+// in (stages, 256 row factors, a 16-entry code table, the next-tile slot),
+// so that two groups can run one after the other in one launch.
 template <int ELEM, int MA, int MB, int KB, class Epi>
-__global__ __launch_bounds__(NTH) void gemm_v3_kernel(const Group<Epi> grp) {
+__device__ __forceinline__ void gemm_v3_body(const Group<Epi>& grp, lds_u8* smem, lds_f32* row_scale,
+                                             lds_u32* code_lut, lds_i32* next_tile_p) {
   using G = Geo<KB>;
   static_assert(MB != KCP || KB == 128, "packed codes use 128-byte steps");
   constexpr int EB = ELEM == EBF16 ? 2 : 1;
   constexpr int BK = KB / EB;               // reduction elements per step
   constexpr int OPB = G::OPB;
   constexpr int NL = G::NL;
-  constexpr int SLOTB = slot_bytes<MB, KB, EB>();
+  constexpr int SLOTB = StageGeo<ELEM, MB, KB>::SLOTB;
   constexpr int PKB = pkb<KB, EB>();
   constexpr int NLB = Plan<MB, EB, KB>::NL;  // DMA chunks per thread for B
-  // as many stages as fit next to the row scales (at most 4)
-  constexpr int NS = 4 * SLOTB + TILE * 4 <= 160 * 1024 ? 4 : 3 * SLOTB + TILE * 4 <= 160 * 1024 ? 3 : 2;
+  constexpr int NS = StageGeo<ELEM, MB, KB>::NS;
   static_assert(NW * 32 * 128 <= SLOTB, "epilogue staging (32 rows of 128 bytes per wave) fits in one stage");
   constexpr int LPS = NL + NLB;            // DMA instructions per thread per stage (at most)
   // (measured faster for the int8 forward, dX and dW; the e4m3 forward keeps
@@ -286,10 +303,6 @@ __global__ __launch_bounds__(NTH) void gemm_v3_kernel(const Group<Epi> grp) {
   constexpr bool kSplitCopies = ELEM != EF8;
   // bf16 operand from packed codes: two codes (a nibble) -> two bf16 by table
   constexpr bool kLutB = MB == KCP && ELEM == EBF16;
-  __shared__ __attribute__((aligned(1024))) uint8_t smem_generic[NS * SLOTB];
-  __shared__ float row_scale[Epi::kRowScale ? TILE : 1];
-  __shared__ uint32_t code_lut[kLutB ? 16 : 1];
-  lds_u8* smem = (lds_u8*)smem_generic;
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -485,7 +498,7 @@ __global__ __launch_bounds__(NTH) void gemm_v3_kernel(const Group<Epi> grp) {
   auto stage_ptr = [&](int slot) { return smem + slot * SLOTB; };
 
   // ---- persistent loop over this block's tiles
-  __shared__ int next_tile;
+  lds_i32& next_tile = *next_tile_p;
   int* const next_ctr = grp.sched + xcd;
   auto finish = [&]() {                 // this block found XCD xcd's list empty
     if (tid == 0 && atomicAdd(grp.sched + 8 + xcd, 1) == nbx8 - 1) {
@@ -724,6 +737,33 @@ __global__ __launch_bounds__(NTH) void gemm_v3_kernel(const Group<Epi> grp) {
     if (cur.nsteps == 0) block_barrier();
   }
   finish();
+}
+
+template <int ELEM, int MA, int MB, int KB, class Epi>
+__global__ __launch_bounds__(NTH) void gemm_v3_kernel(const Group<Epi> grp) {
+  __shared__ __attribute__((aligned(1024))) uint8_t stages[StageGeo<ELEM, MB, KB>::kBytes];
+  __shared__ float row_scale[TILE];
+  __shared__ uint32_t code_lut[16];
+  __shared__ int next_tile;
+  gemm_v3_body<ELEM, MA, MB, KB, Epi>(grp, (lds_u8*)stages, (lds_f32*)row_scale, (lds_u32*)code_lut,
+                                       (lds_i32*)&next_tile);
+}
+
+// Two groups in one launch: every block takes tiles of the first group until
+// its lists are empty, then tiles of the second, so blocks left without a
+// tile of the first start on the second at once.
+template <int E1, int MA1, int MB1, int KB1, class Epi1, int E2, int MA2, int MB2, int KB2, class Epi2>
+__global__ __launch_bounds__(NTH) void gemm_v3_dual_kernel(const Group<Epi1> g1, const Group<Epi2> g2) {
+  constexpr int B1 = StageGeo<E1, MB1, KB1>::kBytes, B2 = StageGeo<E2, MB2, KB2>::kBytes;
+  __shared__ __attribute__((aligned(1024))) uint8_t stages[B1 > B2 ? B1 : B2];
+  __shared__ float row_scale[TILE];
+  __shared__ uint32_t code_lut[16];
+  __shared__ int next_tile;
+  gemm_v3_body<E1, MA1, MB1, KB1, Epi1>(g1, (lds_u8*)stages, (lds_f32*)row_scale, (lds_u32*)code_lut,
+                                         (lds_i32*)&next_tile);
+  __syncthreads();
+  gemm_v3_body<E2, MA2, MB2, KB2, Epi2>(g2, (lds_u8*)stages, (lds_f32*)row_scale, (lds_u32*)code_lut,
+                                         (lds_i32*)&next_tile);
 }
 
 }  // namespace v3
@@ -988,11 +1028,12 @@ static int device_cus() {
   return n;
 }
 
-// Fill in tile grids, sort the problems by reduction steps per tile (longest
-// first) and launch the persistent grid: 8 x (blocks per XCD).
-template <int ELEM, int MA, int MB, int KB, class Epi>
-static void launch_group(Group<Epi>& grp, uint8_t* ws, hipStream_t s) {
-  grp.sched = reinterpret_cast<int*>(ws);
+// Tile counts and longest-first order of a group; `slot` picks its 64 bytes
+// of tile counters among the workspace's first 128.  Returns the most tiles
+// any XCD's list holds.
+template <int ELEM, int KB, class Epi>
+static int32_t prep_group(Group<Epi>& grp, uint8_t* ws, int slot) {
+  grp.sched = reinterpret_cast<int*>(ws + 64 * slot);
   constexpr int64_t BK = KB / (ELEM == EBF16 ? 2 : 1);
   int64_t steps[MAXG];
   for (int g = 0; g < grp.ng; ++g) {
@@ -1016,10 +1057,31 @@ static void launch_group(Group<Epi>& grp, uint8_t* ws, hipStream_t s) {
     }
     per_xcd = std::max(per_xcd, c);
   }
+  return per_xcd;
+}
+
+// Persistent grid over one group: 8 x (blocks per XCD), one block per
+// compute unit at most.
+template <int ELEM, int MA, int MB, int KB, class Epi>
+static void launch_group(Group<Epi>& grp, uint8_t* ws, hipStream_t s) {
+  const int32_t per_xcd = prep_group<ELEM, KB>(grp, ws, 0);
   if (per_xcd == 0) return;
   static const int cus = device_cus();
   const int32_t bpx = std::min(per_xcd, std::max(1, cus / 8));
   hipLaunchKernelGGL((gemm_v3_kernel<ELEM, MA, MB, KB, Epi>), dim3((unsigned)(8 * bpx)), dim3(NTH), 0, s, grp);
+}
+
+// Groups g1 then g2 in one launch (tile counters in slots 1 and 0).
+template <int E1, int MA1, int MB1, int KB1, class Epi1, int E2, int MA2, int MB2, int KB2, class Epi2>
+static void launch_dual(Group<Epi1>& g1, Group<Epi2>& g2, uint8_t* ws, hipStream_t s) {
+  const int32_t p1 = prep_group<E1, KB1>(g1, ws, 1);
+  const int32_t p2 = prep_group<E2, KB2>(g2, ws, 0);
+  const int32_t per_xcd = std::max(p1, p2);
+  if (per_xcd == 0) return;
+  static const int cus = device_cus();
+  const int32_t bpx = std::min(per_xcd, std::max(1, cus / 8));
+  hipLaunchKernelGGL((gemm_v3_dual_kernel<E1, MA1, MB1, KB1, Epi1, E2, MA2, MB2, KB2, Epi2>),
+                     dim3((unsigned)(8 * bpx)), dim3(NTH), 0, s, g1, g2);
 }
 
 }  // namespace v3
@@ -1121,28 +1183,40 @@ BwdPlan plan_bwd_batch(int n, const LinearIO* io, int64_t M) {
   P.wi = 4;
   P.wj = 4;
   P.splits = 1;
-  double best = 1e300;
+  P.splits_dual = 1;
   static const int cus = device_cus();
+  // a step of a 256 x 256 bf16 tile is ~2048 MFMA cycles at ~2.1 GHz, plus
+  // ~2 us of per-tile prologue / epilogue; partials move at ~4 TB/s
+  constexpr double kStepUs = 2048.0 / 2100.0, kTileUs = 2.0;
+  auto tiles_of = [](int64_t I, int64_t J) { return ((I + TILE - 1) / TILE) * ((J + TILE - 1) / TILE); };
+  double dx_us = 0;     // dX work of the whole batch, summed over its tiles
+  for (int l = 0; l < n; ++l)
+    dx_us += (double)tiles_of(M, io[l].d_in) * ((double)((io[l].d_out + 63) / 64) * kStepUs + kTileUs);
+  double best = 1e300, best_dual = 1e300;
   for (int64_t s = 1; s <= 32; ++s) {
     if (s > 1 && M / s < 256) break;
     int64_t tiles = 0;
     double part_bytes = 0;
     for (int l = 0; l < n; ++l) {
-      tiles += ((io[l].d_out + TILE - 1) / TILE) * ((io[l].d_in + TILE - 1) / TILE) * s;
+      tiles += tiles_of(io[l].d_out, io[l].d_in) * s;
       if (s > 1) part_bytes += (2.0 * s + 1.0) * (double)(io[l].d_out * io[l].d_in * 4);
     }
     const double rounds = (double)((tiles + cus - 1) / cus);
-    const double steps = (double)(((M + s - 1) / s + 63) / 64);
-    // a step of a 256 x 256 bf16 tile is ~2048 MFMA cycles at ~2.1 GHz,
-    // plus ~2 us of per-tile prologue / epilogue; partials move at ~4 TB/s
-    const double t_us = rounds * (steps * 2048.0 / 2100.0 + 2.0) + part_bytes / 4.0e6;
+    const double tile_us = (double)(((M + s - 1) / s + 63) / 64) * kStepUs + kTileUs;
+    // dW alone: whole rounds of equal tiles
+    const double t_us = rounds * tile_us + part_bytes / 4.0e6;
     if (t_us < best * 0.999) { best = t_us; P.splits = s; }
+    // dW then dX in one launch: the dW rounds, or the total work spread
+    // over every compute unit, whichever is longer
+    const double t_dual = std::max(rounds * tile_us, ((double)tiles * tile_us + dx_us) / cus) +
+                          part_bytes / 4.0e6;
+    if (t_dual < best_dual * 0.999) { best_dual = t_dual; P.splits_dual = s; }
   }
   size_t off = kSchedBytes;
   for (int l = 0; l < n; ++l) {
     const size_t wn = (size_t)(io[l].d_out * io[l].d_in);
     const int64_t s32 = dw_splits_f32(io[l].d_out, io[l].d_in, M);
-    const int64_t sp = P.splits > s32 ? P.splits : s32;
+    const int64_t sp = std::max(std::max(P.splits, P.splits_dual), s32);
     P.q_off[l] = off;
     off += align256(wn * 2);
     P.xt_off[l] = off;
@@ -1154,11 +1228,11 @@ BwdPlan plan_bwd_batch(int n, const LinearIO* io, int64_t M) {
   return P;
 }
 
-hipError_t launch_dx_batch(const BatchCfg& c, const LinearIO* io, uint8_t* ws, const BwdPlan& P,
-                           hipStream_t stream) {
-  if (c.M == 0 || c.n == 0) return hipSuccess;
-  // dX[m, k] = alpha sum_n dY[m, n] q[n, k]: I = M, J = d_in, R = d_out
-  Group<EpiScale> grp{};
+// dX[m, k] = alpha sum_n dY[m, n] q[n, k]: I = M, J = d_in, R = d_out.
+// Fills the problems of the group and launches the pre-pass that writes its
+// B operand into the workspace.
+static void prep_dx(const BatchCfg& c, const LinearIO* io, uint8_t* ws, const BwdPlan& P,
+                    hipStream_t stream, Group<EpiScale>& grp) {
   grp.ng = c.n;
   for (int l = 0; l < c.n; ++l) {
     Prob<EpiScale>& p = grp.p[l];
@@ -1188,8 +1262,7 @@ hipError_t launch_dx_batch(const BatchCfg& c, const LinearIO* io, uint8_t* ws, c
     }
     tab.b0[c.n] = blocks;
     hipLaunchKernelGGL(pack_codes_t_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, tab);
-    launch_group<EBF16, KC, KCP, 128>(grp, ws, stream);
-    return hipGetLastError();
+    return;
   }
   // bf16 weights transposed (reduction contiguous), so both operands are
   // read without the transposing LDS reads
@@ -1211,14 +1284,23 @@ hipError_t launch_dx_batch(const BatchCfg& c, const LinearIO* io, uint8_t* ws, c
     hipLaunchKernelGGL(unpack_t_kernel<true>, dim3(blocks), dim3(256), 0, stream, tab);
   else
     hipLaunchKernelGGL(unpack_t_kernel<false>, dim3(blocks), dim3(256), 0, stream, tab);
-  launch_group<EBF16, KC, KC, KB_BWD>(grp, ws, stream);
+}
+
+hipError_t launch_dx_batch(const BatchCfg& c, const LinearIO* io, uint8_t* ws, const BwdPlan& P,
+                           hipStream_t stream) {
+  if (c.M == 0 || c.n == 0) return hipSuccess;
+  Group<EpiScale> grp{};
+  prep_dx(c, io, ws, P, stream, grp);
+  if (c.w_ternary && DX_PACKED_B) launch_group<EBF16, KC, KCP, 128>(grp, ws, stream);
+  else launch_group<EBF16, KC, KC, KB_BWD>(grp, ws, stream);
   return hipGetLastError();
 }
 
-hipError_t launch_dw_batch(const BatchCfg& c, const LinearIO* io, uint8_t* ws, const BwdPlan& P,
-                           hipStream_t stream) {
-  if (c.n == 0) return hipSuccess;
-  // X~T once per distinct quantised input
+// dW[n, k] = sum_m dY[m, n] X~T[k, m]: I = d_out, J = d_in, R = M.
+// Launches the pre-pass that writes X~T once per distinct quantised input
+// and fills the problems of the group (split over the batch as planned).
+static void prep_dw(const BatchCfg& c, const LinearIO* io, uint8_t* ws, const BwdPlan& P,
+                    hipStream_t stream, Group<EpiPartial>& grp) {
   int first[kMaxBatch];
   DqTab tab{};
   tab.M = c.M;
@@ -1246,11 +1328,9 @@ hipError_t launch_dw_batch(const BatchCfg& c, const LinearIO* io, uint8_t* ws, c
     else
       hipLaunchKernelGGL(dequant_t_kernel<false>, dim3(blocks), dim3(256), 0, stream, tab);
   }
-  // dW[n, k] = sum_m dY[m, n] X~T[k, m]: I = d_out, J = d_in, R = M
   const int64_t splits = P.splits;
   int64_t len = splits > 1 ? (c.M + splits - 1) / splits : (c.M > 0 ? c.M : 1);
   len = (len + 63) / 64 * 64;
-  Group<EpiPartial> grp{};
   grp.ng = c.n;
   for (int l = 0; l < c.n; ++l) {
     Prob<EpiPartial>& p = grp.p[l];
@@ -1265,13 +1345,16 @@ hipError_t launch_dw_batch(const BatchCfg& c, const LinearIO* io, uint8_t* ws, c
     p.split_len = len;
     p.nbz = (int32_t)splits;
   }
-  launch_group<EBF16, KM, KC, KB_BWD>(grp, ws, stream);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess || splits == 1) return e;
+}
+
+// Sum of the batch-split dW partials into dW.
+static hipError_t reduce_dw(const BatchCfg& c, const LinearIO* io, uint8_t* ws, const BwdPlan& P,
+                            hipStream_t stream) {
+  if (P.splits == 1) return hipSuccess;
   RedTab red{};
   red.n = c.n;
-  red.splits = (int32_t)splits;
-  blocks = 0;
+  red.splits = (int32_t)P.splits;
+  int32_t blocks = 0;
   for (int l = 0; l < c.n; ++l) {
     red.src[l] = reinterpret_cast<const float*>(ws + P.part_off[l]);
     red.dst[l] = io[l].dW;
@@ -1282,6 +1365,39 @@ hipError_t launch_dw_batch(const BatchCfg& c, const LinearIO* io, uint8_t* ws, c
   red.b0[c.n] = blocks;
   hipLaunchKernelGGL(split_reduce_batch_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, red);
   return hipGetLastError();
+}
+
+hipError_t launch_dw_batch(const BatchCfg& c, const LinearIO* io, uint8_t* ws, const BwdPlan& P,
+                           hipStream_t stream) {
+  if (c.n == 0) return hipSuccess;
+  Group<EpiPartial> grp{};
+  prep_dw(c, io, ws, P, stream, grp);
+  launch_group<EBF16, KM, KC, KB_BWD>(grp, ws, stream);
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  return reduce_dw(c, io, ws, P, stream);
+}
+
+// dW and dX of a batch in one persistent launch: dW's tiles first (the
+// longer reduction), then dX's, so compute units that draw no dW tile, or
+// finish theirs early, go on with dX at once.
+hipError_t launch_dxdw_batch(const BatchCfg& c, const LinearIO* io, uint8_t* ws, const BwdPlan& P,
+                             hipStream_t stream) {
+  if (c.n == 0) return hipSuccess;
+  if (c.M == 0 || (c.w_ternary && DX_PACKED_B)) {
+    const hipError_t e = launch_dx_batch(c, io, ws, P, stream);
+    return e != hipSuccess ? e : launch_dw_batch(c, io, ws, P, stream);
+  }
+  Group<EpiScale> gx{};
+  Group<EpiPartial> gw{};
+  BwdPlan Q = P;
+  Q.splits = P.splits_dual;
+  prep_dx(c, io, ws, Q, stream, gx);
+  prep_dw(c, io, ws, Q, stream, gw);
+  launch_dual<EBF16, KM, KC, KB_BWD, EpiPartial, EBF16, KC, KC, KB_BWD, EpiScale>(gw, gx, ws, stream);
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  return reduce_dw(c, io, ws, Q, stream);
 }
 
 }  // namespace dqt

@@ -22,6 +22,9 @@ BATCHES = [
     (300, [(64, 80, 0), (80, 64, 1), (64, 64, 0)], "ternary", -1, 1, "i8", "f32"),
     (2048, [(768, 768, 0)] * 3 + [(768, 768, 1), (768, 2048, 2), (768, 2048, 2), (2048, 768, 3)],
      "ternary", -1, 1, "i8", "bf16"),
+    # two dW tiles over a long batch: dW split over the batch (partials and
+    # their reduction) inside the launch it shares with dX
+    (4096, [(256, 256, 0), (256, 128, 0)], "ternary", -1, 1, "i8", "bf16"),
 ]
 
 
@@ -125,7 +128,8 @@ def test_batch_rejects_mixed_formats_and_sizes(lib):
 
 
 def test_tile_counters_return_to_zero(lib):
-    """The persistent GEMM's tile counters (first 64 bytes of the workspace)
+    """The persistent GEMM's tile counters (first 128 bytes of the workspace:
+    one 64-byte set per group of a launch, two when dW and dX share a launch)
     are zero again after every call, so one workspace serves call after call
     and graph replay after replay."""
     M = 1000
@@ -147,4 +151,4 @@ def test_tile_counters_return_to_zero(lib):
         dqt.dqt_linear_fwd_batch(io, M, dqt.DQT_I8, dqt.DQT_BF16, ws)
         dqt.dqt_linear_bwd_batch(io, M, dqt.DQT_I8, dqt.DQT_BF16, dqt.DQT_BF16, dqt.DQT_BF16, ws)
         torch.cuda.synchronize()
-        assert torch.count_nonzero(ws[:16]).item() == 0, rep     # 16 int32 counters
+        assert torch.count_nonzero(ws[:32]).item() == 0, rep     # 2 x 16 int32 counters
