@@ -135,7 +135,8 @@ def algorithmic_units(wl):
     sr_bytes = sum((2 * code_b + 4) * l.d_in * l.d_out for l in wl.linears)
     xb = 2 if wl.x_dtype == "bf16" else 4
     act_bytes = sum(M * wl.input_width(n) * (xb + 1) + 4 * M for n in wl.inputs)
-    return {"fwd": f, "bwd_dx": f, "bwd_dw": f, "sr": sr_bytes, "act_quant": act_bytes}
+    return {"fwd": f, "bwd": 2 * f, "bwd_dx": f, "bwd_dw": f, "sr": sr_bytes,
+            "act_quant": act_bytes}
 
 
 def cpu_baseline(wl, tokens: int, min_seconds: float = 10.0):
@@ -271,8 +272,10 @@ def main():
     ms_per_step = total_ms / args.steps
 
     # Per-call-kind durations: a graph holding one step's calls of one kind,
-    # replayed back to back between two events on the same stream.
-    kinds = ["act_quant", "fwd", "bwd_dx", "bwd_dw", "sr"]
+    # replayed back to back between two events on the same stream.  The
+    # step's own calls first; then dX and dW each in a call of its own.
+    step_kinds = ["act_quant", "fwd", "bwd", "sr"]
+    kinds = step_kinds + ["bwd_dx", "bwd_dw"]
     per_kind_ms, per_kind_units, per_kind_n = {}, {}, {}
     for kind in kinds:
         calls = []
@@ -284,7 +287,7 @@ def main():
 
         g = torch.cuda.CUDAGraph()
         with torch.cuda.graph(g):
-            run_step(blk, dqt, 1, None, only, split_bwd=True)
+            run_step(blk, dqt, 1, None, only, split_bwd=kind not in step_kinds)
         torch.cuda.synchronize()
         e0 = torch.cuda.Event(enable_timing=True)
         e1 = torch.cuda.Event(enable_timing=True)
@@ -301,6 +304,7 @@ def main():
     flops = wl.train_flops
     value = flops / (ms_per_step * 1e-3) / 1e12
     gemm_dtype = {"fwd": "fp8" if wl.act == "e4m3" else "i8",
+                  "bwd": "bf16" if wl.dy_dtype == "bf16" and wl.xt == "bf16" else "f32",
                   "bwd_dx": "bf16" if wl.dy_dtype == "bf16" else "f32",
                   "bwd_dw": "bf16" if wl.xt == "bf16" else "f32"}
     breakdown = {}
@@ -318,7 +322,7 @@ def main():
         breakdown[kind] = entry
 
     # the dominant kernel class: largest share of the step
-    dom = max(per_kind_ms, key=lambda k: per_kind_ms[k])
+    dom = max(step_kinds, key=lambda k: per_kind_ms[k])
     dom_avg_ms = per_kind_ms[dom] / per_kind_n[dom]
     dom_units = per_kind_units[dom] / per_kind_n[dom]
     if dom in gemm_dtype:
@@ -337,7 +341,7 @@ def main():
     sr_t = per_kind_ms.get("sr", 0.0) / args.steps
     sr_gbs = per_kind_units.get("sr", 0.0) / args.steps / (sr_t * 1e-3) / 1e9 if sr_t else None
     mfma_frac = sum(per_kind_units[k] / args.steps / (PEAK_TFLOPS[gemm_dtype[k]] * 1e12)
-                    for k in gemm_dtype) / (ms_per_step * 1e-3)
+                    for k in ("fwd", "bwd_dx", "bwd_dw")) / (ms_per_step * 1e-3)
 
     out = {
         "metric": "DQT linear train-step TFLOP/s (fwd+bwd) + SR-update GB/s, % of MI355X peak",
