@@ -43,6 +43,10 @@ def parse():
     p.add_argument("--warmup", type=int, default=5)
     p.add_argument("--workload", default="llama_h768")
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--sr", choices=("fused", "separate"), default=None,
+                   help="fused: the SR update consumes dW inside the backward call (dW is "
+                        "never stored; bf16 environment only, the default there); separate: "
+                        "backward writes dW, then the SR update call")
     p.add_argument("--cpu-tokens", type=int, default=8192,
                    help="tokens of the oracle's bounded sample")
     p.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -91,6 +95,7 @@ class Block:
                              xdq=self.xdq[lin.input], Y=self.Y[li], dY=self.dY[li],
                              dX=self.dX[li], dW=self.dW[li]))
         self.io_all = dqt.linear_io(ents)
+        self.io_fused = dqt.linear_io([dict(e, dW=None) for e in ents])
         self.act_io = dqt.act_io([(self.X[n], self.Xq[n], self.xdq[n]) for n in wl.inputs])
         self.x_t = dqt.DQT_BF16 if wl.x_dtype == "bf16" else dqt.DQT_F32
         self.io_dx = dqt.linear_io([dict(e, dW=None) for e in ents])
@@ -105,16 +110,22 @@ class Block:
         self.counters = torch.zeros((2,), dtype=torch.int64, device=dev)
 
 
-def run_step(blk, dqt, step, stream, rec, split_bwd=False):
+def run_step(blk, dqt, step, stream, rec, split_bwd=False, sr="separate"):
     """Enqueue one train step: one batched call per stage (act-quant of every
     distinct input, forward, backward (dX and dW in one call, which may run
-    them side by side), SR update) over all linears.  With split_bwd the
-    backward is two calls, dX then dW, so each can be timed on its own.
-    rec(kind, fn) runs fn (or records it into a graph)."""
+    them side by side), SR update) over all linears.  With sr == "fused" the
+    backward and the SR update are one call (dW consumed where it is formed).
+    With split_bwd the backward is two calls, dX then dW, so each can be
+    timed on its own.  rec(kind, fn) runs fn (or records it into a graph)."""
     wl = blk.wl
     M = wl.M
     rec("act_quant", lambda: dqt.dqt_act_quant_batch(blk.act_io, blk.x_t, M, blk.act, stream))
     rec("fwd", lambda: dqt.dqt_linear_fwd_batch(blk.io_all, M, blk.act, blk.y_t, blk.ws, stream))
+    if sr == "fused" and not split_bwd:
+        rec("bwd_sr", lambda: dqt.dqt_linear_bwd_sr_batch(blk.io_fused, M, blk.act, blk.dy_t,
+                                                          blk.xt, blk.dx_t, wl.lr, wl.seed, step,
+                                                          blk.counters, blk.ws, stream))
+        return
     if split_bwd:
         rec("bwd_dx", lambda: dqt.dqt_linear_bwd_batch(blk.io_dx, M, blk.act, blk.dy_t, blk.xt,
                                                        blk.dx_t, blk.ws, stream))
@@ -135,7 +146,7 @@ def algorithmic_units(wl):
     sr_bytes = sum((2 * code_b + 4) * l.d_in * l.d_out for l in wl.linears)
     xb = 2 if wl.x_dtype == "bf16" else 4
     act_bytes = sum(M * wl.input_width(n) * (xb + 1) + 4 * M for n in wl.inputs)
-    return {"fwd": f, "bwd": 2 * f, "bwd_dx": f, "bwd_dw": f, "sr": sr_bytes,
+    return {"fwd": f, "bwd": 2 * f, "bwd_sr": 2 * f, "bwd_dx": f, "bwd_dw": f, "sr": sr_bytes,
             "act_quant": act_bytes}
 
 
@@ -236,6 +247,8 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
+    if args.sr is None:
+        args.sr = "fused" if wl.xt == "bf16" and wl.dy_dtype == "bf16" else "separate"
     blk = Block(wl, torch, dqt, W)
     units = algorithmic_units(wl)
 
@@ -243,7 +256,7 @@ def main():
         fn()
 
     for s in range(args.warmup):
-        run_step(blk, dqt, 1000 + s, None, plain)
+        run_step(blk, dqt, 1000 + s, None, plain, sr=args.sr)
     torch.cuda.synchronize()
 
     # One step is ~40 kernel launches; on its own the host would need longer
@@ -252,7 +265,7 @@ def main():
     # the step runs in every replay.
     step_graph = torch.cuda.CUDAGraph()
     with torch.cuda.graph(step_graph):
-        run_step(blk, dqt, 1, None, plain)
+        run_step(blk, dqt, 1, None, plain, sr=args.sr)
     torch.cuda.synchronize()
     step_graph.replay()
     torch.cuda.synchronize()
@@ -274,8 +287,8 @@ def main():
     # Per-call-kind durations: a graph holding one step's calls of one kind,
     # replayed back to back between two events on the same stream.  The
     # step's own calls first; then dX and dW each in a call of its own.
-    step_kinds = ["act_quant", "fwd", "bwd", "sr"]
-    kinds = step_kinds + ["bwd_dx", "bwd_dw"]
+    step_kinds = ["act_quant", "fwd"] + (["bwd_sr"] if args.sr == "fused" else ["bwd", "sr"])
+    kinds = step_kinds + (["bwd", "sr"] if args.sr == "fused" else []) + ["bwd_dx", "bwd_dw"]
     per_kind_ms, per_kind_units, per_kind_n = {}, {}, {}
     for kind in kinds:
         calls = []
@@ -287,7 +300,8 @@ def main():
 
         g = torch.cuda.CUDAGraph()
         with torch.cuda.graph(g):
-            run_step(blk, dqt, 1, None, only, split_bwd=kind not in step_kinds)
+            run_step(blk, dqt, 1, None, only, split_bwd=kind in ("bwd_dx", "bwd_dw"),
+                     sr="fused" if kind == "bwd_sr" else "separate")
         torch.cuda.synchronize()
         e0 = torch.cuda.Event(enable_timing=True)
         e1 = torch.cuda.Event(enable_timing=True)
@@ -305,6 +319,7 @@ def main():
     value = flops / (ms_per_step * 1e-3) / 1e12
     gemm_dtype = {"fwd": "fp8" if wl.act == "e4m3" else "i8",
                   "bwd": "bf16" if wl.dy_dtype == "bf16" and wl.xt == "bf16" else "f32",
+                  "bwd_sr": "bf16",
                   "bwd_dx": "bf16" if wl.dy_dtype == "bf16" else "f32",
                   "bwd_dw": "bf16" if wl.xt == "bf16" else "f32"}
     breakdown = {}
@@ -363,6 +378,7 @@ def main():
                         f"{wl.linears[6].d_out}; {wl.M} tokens; {wl.wfmt} weights; "
                         f"{wl.act} activations; {wl.xt} environment; lr {wl.lr}",
             "tokens": wl.M, "linears": len(wl.linears), "weights": wl.n_weights,
+            "sr_update": "fused into the dW product" if args.sr == "fused" else "separate call",
             "parallelism": "single GPU",
         },
         "sr_update_gbs": round(sr_gbs, 1) if sr_gbs else None,

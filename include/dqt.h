@@ -262,6 +262,30 @@ dqt_status dqt_sr_update_batch(int32_t n, const dqt_linear_io* io, float lr,
                                unsigned long long* counters, void* stream);
 
 /*
+ * Backward and direct SR update of n linears in one call (Sec. 3.2: the
+ * update of Eq. 5 consumes dW of the backward), with dW never written to
+ * memory: the dW product's epilogue updates the 8 codes of each group of 8
+ * consecutive weights of a row as it forms their gradients (or, when the
+ * dW reduction over tokens is split, the kernel that sums the partials
+ * does).  The codes and counters equal those of dqt_linear_bwd_batch
+ * writing dW followed by dqt_sr_update_batch on that dW, bit for bit; dX is
+ * formed from the codes as they were before the update.
+ *   io: uses w, Wq (updated in place), Xq, xdq, dY, dX of each entry; dX may
+ *       be NULL per entry; every dW must be NULL (DQT_ERR_UNSUPPORTED
+ *       otherwise: use the two calls to keep dW).
+ *   dy_t, xt_t: DQT_BF16 only (the matrix-core path); other values return
+ *       DQT_ERR_UNSUPPORTED.  dx_t: DQT_F32 or DQT_BF16.
+ *   lr, seed, step, counters: as dqt_sr_update_batch.
+ *   ws, ws_bytes: at least dqt_linear_bwd_batch_workspace(n, io, M) bytes.
+ *   M = 0: dW is zero, which moves no weight; nothing is launched.
+ */
+dqt_status dqt_linear_bwd_sr_batch(int32_t n, const dqt_linear_io* io, int64_t M,
+                                   int32_t act_q, int32_t dy_t, int32_t xt_t,
+                                   int32_t dx_t, float lr, uint64_t seed,
+                                   uint32_t step, unsigned long long* counters,
+                                   void* ws, size_t ws_bytes, void* stream);
+
+/*
  * Helpers (not on the timed path).
  */
 

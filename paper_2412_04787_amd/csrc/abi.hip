@@ -265,6 +265,69 @@ dqt_status dqt_linear_bwd_batch(int32_t n, const dqt_linear_io* io, int64_t M, i
   return st;
 }
 
+dqt_status dqt_linear_bwd_sr_batch(int32_t n, const dqt_linear_io* io, int64_t M, int32_t act_q,
+                                   int32_t dy_t, int32_t xt_t, int32_t dx_t, float lr,
+                                   uint64_t seed, uint32_t step, unsigned long long* counters,
+                                   void* ws, size_t ws_bytes, void* stream) {
+  dqt::LinearIO L[DQT_MAX_BATCH];
+  int32_t wfmt;
+  dqt_status st = check_batch(n, io, L, &wfmt);
+  if (st != DQT_OK) return st;
+  if (M < 0) return DQT_ERR_SHAPE;
+  if (act_q != DQT_I8 && act_q != DQT_FP8E4M3) return DQT_ERR_DTYPE;
+  if (!is_float_type(dy_t) || !is_float_type(xt_t) || !is_float_type(dx_t)) return DQT_ERR_DTYPE;
+  if (dy_t != DQT_BF16 || xt_t != DQT_BF16) return DQT_ERR_UNSUPPORTED;
+  if (counters != nullptr && (reinterpret_cast<uintptr_t>(counters) & 7u) != 0) return DQT_ERR_ALIGN;
+  if (!(isfinite(lr) && lr >= 0.0f)) return DQT_ERR_RANGE;
+  dqt::SRTensor t[DQT_MAX_BATCH];
+  int nx = 0;
+  for (int l = 0; l < n; ++l) {
+    if (io[l].dW != nullptr) return DQT_ERR_UNSUPPORTED;
+    if (io[l].Wq == nullptr) return DQT_ERR_NULL;
+    if (!aligned16(io[l].Wq)) return DQT_ERR_ALIGN;
+    if (M > 0) {
+      if (io[l].Xq == nullptr || io[l].xdq == nullptr || io[l].dY == nullptr) return DQT_ERR_NULL;
+      if (!aligned16(io[l].Xq) || !aligned16(io[l].xdq) || !aligned16(io[l].dY)) return DQT_ERR_ALIGN;
+    }
+    if (io[l].dX != nullptr) {
+      if (!aligned16(io[l].dX)) return DQT_ERR_ALIGN;
+      ++nx;
+    }
+    const float c = lr / io[l].w->alpha;   // one correctly rounded fp32 division
+    if (!isfinite(c)) return DQT_ERR_RANGE;
+    t[l].wq = static_cast<uint8_t*>(io[l].Wq);
+    t[l].grad = nullptr;
+    t[l].nweights = (int64_t)io[l].w->d_out * (int64_t)io[l].w->d_in;
+    t[l].c = c;
+    t[l].qmin = io[l].w->qmin;
+    t[l].qmax = io[l].w->qmax;
+    t[l].tensor_id = io[l].w->tensor_id;
+  }
+  const dqt::BwdPlan P = dqt::plan_bwd_batch(n, L, M);
+  if (ws == nullptr || ws_bytes < P.total) return DQT_ERR_WORKSPACE;
+  if (!aligned16(ws)) return DQT_ERR_ALIGN;
+  if (M == 0) return DQT_OK;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  uint8_t* wsb = static_cast<uint8_t*>(ws);
+  const dqt::BatchCfg c{n, M, wfmt == DQT_TERNARY2, act_q == DQT_FP8E4M3, dx_t == DQT_BF16};
+  if (nx > 0 && nx < n) {
+    // dX of the linears that want it first (it reads the codes before the
+    // update), then dW and the update of every linear
+    dqt::LinearIO sub[DQT_MAX_BATCH];
+    dqt::BwdPlan Px = P;
+    int k = 0;
+    for (int l = 0; l < n; ++l)
+      if (io[l].dX != nullptr) {
+        Px.q_off[k] = P.q_off[l];
+        sub[k++] = L[l];
+      }
+    const dqt::BatchCfg cx{nx, M, c.w_ternary, c.act_e4m3, c.out_bf16};
+    st = from_hip(dqt::launch_dx_batch(cx, sub, wsb, Px, s));
+    if (st != DQT_OK) return st;
+  }
+  return from_hip(dqt::launch_bwd_sr_batch(c, L, t, seed, step, counters, nx == n, wsb, P, s));
+}
+
 dqt_status dqt_sr_update_batch(int32_t n, const dqt_linear_io* io, float lr, uint64_t seed,
                                uint32_t step, unsigned long long* counters, void* stream) {
   dqt::LinearIO L[DQT_MAX_BATCH];

@@ -80,6 +80,13 @@ hipError_t launch_dw_batch(const BatchCfg& c, const LinearIO* io, uint8_t* ws, c
 // dX and dW of every linear of the batch in one launch (bf16 operands).
 hipError_t launch_dxdw_batch(const BatchCfg& c, const LinearIO* io, uint8_t* ws, const BwdPlan& P,
                              hipStream_t stream);
+struct SRTensor;
+// dW of every linear of the batch consumed by the SR update of its codes
+// (dW is not stored), with dX of every linear in the same launch when
+// with_dx (bf16 operands).
+hipError_t launch_bwd_sr_batch(const BatchCfg& c, const LinearIO* io, const SRTensor* t, uint64_t seed,
+                               uint32_t step, unsigned long long* counters, bool with_dx, uint8_t* ws,
+                               const BwdPlan& P, hipStream_t stream);
 // fp32-environment kernels
 hipError_t launch_dx_f32(const DxArgs& a, hipStream_t stream);
 hipError_t launch_dw_f32(const DwArgs& a, hipStream_t stream);

@@ -18,6 +18,8 @@ template <> struct AccT<Mfma::I8> { using type = i32x16; };
 struct EpiFwd {          // y = fl(fl(acc) * fl(xdq[i] * alpha))
   void* y; int64_t ld; bool bf16; const float* xdq; float alpha;
   static constexpr bool kRowScale = true;
+  static constexpr bool kSR = false;
+  static constexpr bool kTern = false;
   __device__ float scale(int64_t i) const { return xdq[i] * alpha; }
   // the same factor in two parts: the per-row load, then the multiply
   __device__ float scale_raw(int64_t i) const { return xdq[i]; }
@@ -37,6 +39,8 @@ struct EpiFwd {          // y = fl(fl(acc) * fl(xdq[i] * alpha))
 struct EpiScale {        // y = fl(alpha * acc)
   void* y; int64_t ld; bool bf16; float alpha;
   static constexpr bool kRowScale = false;
+  static constexpr bool kSR = false;
+  static constexpr bool kTern = false;
   __device__ float scale(int64_t) const { return alpha; }
   __device__ float scale_raw(int64_t) const { return 1.0f; }
   __device__ float scale_fin(float) const { return alpha; }
@@ -54,6 +58,8 @@ struct EpiScale {        // y = fl(alpha * acc)
 struct EpiPartial {      // fp32 partial sums, one slab per split
   float* y; int64_t ld; int64_t slab;
   static constexpr bool kRowScale = false;
+  static constexpr bool kSR = false;
+  static constexpr bool kTern = false;
   __device__ float scale(int64_t) const { return 1.0f; }
   __device__ float scale_raw(int64_t) const { return 1.0f; }
   __device__ float scale_fin(float) const { return 1.0f; }
@@ -65,6 +71,30 @@ struct EpiPartial {      // fp32 partial sums, one slab per split
   __device__ void put(int64_t i, int64_t j, float acc) const {
     y[(int64_t)blockIdx.z * slab + i * ld + j] = acc;
   }
+};
+
+// dW consumed where it is formed: each group of 8 consecutive dW entries of
+// a row goes through the direct SR update of its 8 codes (Sec. 3.2 Eq. 5)
+// and dW itself is never stored.  TERN: 2-bit ternary codes (2 bytes per 8
+// weights), else int8 codes (8 bytes).
+template <bool TERN>
+struct EpiSR {
+  uint8_t* wq;          // codes [d_out][d_in], updated in place
+  int64_t ldc;          // bytes per code row (d_in / 4 or d_in)
+  int64_t d_in;         // weights per row: the flat index of (n, k) is n d_in + k
+  float c, L;           // fl32(lr / alpha); |delta| clamp qmax - qmin + 1
+  int qmin, qmax;
+  uint32_t k0, k1, step, tid;   // Philox key (seed), step, tensor id
+  unsigned long long* counters; // nullable: changed, non-finite (accumulated)
+  static constexpr bool kRowScale = false;
+  static constexpr bool kSR = true;
+  static constexpr bool kTern = TERN;
+  __device__ float scale(int64_t) const { return 1.0f; }
+  __device__ float scale_raw(int64_t) const { return 1.0f; }
+  __device__ float scale_fin(float) const { return 1.0f; }
+  __device__ bool out_bf16() const { return false; }
+  __device__ uint8_t* row(int64_t i, int) const { return wq + i * ldc; }
+  __device__ int64_t row_bytes() const { return ldc; }
 };
 
 }  // namespace dqt

@@ -39,6 +39,7 @@
 #include <type_traits>
 
 #include "gemm_common.h"
+#include "sr_rule.h"
 
 namespace dqt {
 namespace v3 {
@@ -579,13 +580,25 @@ __device__ __forceinline__ void gemm_v3_body(const Group<Epi>& grp, lds_u8* smem
   // chunks outside the output go to a dummy slot in the workspace)
   constexpr int kStoresBf16 = WI * 32 * (32 * WJ * 2 / 16) / 64;
   constexpr int kStoresF32 = WI * 32 * (32 * WJ * 4 / 16) / 64;
+  constexpr int kStoresSR = WI * WJ * 2;      // two 8-weight code chunks per 32 x 32 block
   // the wave's vmcnt counts at most 63 operations in flight (the wave waits
   // at issue beyond that), so "at most 63 newer" is a correct, if
   // conservative, wait when more were issued
   constexpr int kVmMax = 63;
   static_assert(NS * LPS < kVmMax, "vmcnt range");
   uint8_t* const dummy = reinterpret_cast<uint8_t*>(grp.sched) + 128;
-  bool first_tile = true, obf_prev = false;
+  bool first_tile = true;
+  int stores_prev = 0;                 // stores per thread of the previous epilogue
+  // SR epilogue: changed and non-finite counts of each wave, kept in LDS
+  // (the row-scale area, which that epilogue does not use) so that nothing
+  // extra stays live in registers across the main loop
+  lds_u32* const sr_cnt = (lds_u32*)row_scale;
+  if constexpr (Epi::kSR) {
+    if (lane == 0) {
+      sr_cnt[2 * wave_u] = 0;
+      sr_cnt[2 * wave_u + 1] = 0;
+    }
+  }
   for (;;) {
     int fetched = 0;                   // thread 0: index of the next tile
 #pragma unroll
@@ -606,7 +619,7 @@ __device__ __forceinline__ void gemm_v3_body(const Group<Epi>& grp, lds_u8* smem
         // (a fixed number per thread), which may stay in flight, as may the
         // tile's later prefetched steps
         const int ahead = (cur.nsteps < NS - 1 ? cur.nsteps : NS - 1) - 1;
-        int n = ahead * lps + (first_tile ? 0 : obf_prev ? kStoresBf16 : kStoresF32);
+        int n = ahead * lps + (first_tile ? 0 : stores_prev);
         if (n > kVmMax) n = kVmMax;
         wait_vm_le<kVmMax>(__builtin_amdgcn_readfirstlane(n));
         first_tile = false;
@@ -641,10 +654,48 @@ __device__ __forceinline__ void gemm_v3_body(const Group<Epi>& grp, lds_u8* smem
     if constexpr (Epi::kRowScale) {
       if (tid < TILE) row_scale[tid] = epi.scale_fin(my_scale);
     }
+    // SR epilogue: this lane's code chunks, rows sr_r + 16 u of each 32-row
+    // block and columns 8 sr_c .. 8 sr_c + 7 of each 32-column block (8
+    // weights per chunk: one Philox block, since d_in is a multiple of 8).
+    // Loaded here, after the main loop, and waited for before the next
+    // tile's copies are issued, so the wait drains nothing else.
+    const int sr_r = lane >> 2, sr_c = lane & 3;
+    // ternary: both chunks of a 32 x 32 block in one register (u = 0 low
+    // half); int8: two words per chunk
+    [[maybe_unused]] uint32_t srt[Epi::kSR ? WI : 1][Epi::kSR ? WJ : 1];
+    [[maybe_unused]] uint32_t sr8[Epi::kSR && !Epi::kTern ? WI : 1][Epi::kSR && !Epi::kTern ? WJ : 1][2][2];
+    auto sr_pos = [&](int ta, int tb, int u, int64_t& n, int64_t& k) {
+      n = i0 + wi * 32 * WI + ta * 32 + sr_r + 16 * u;
+      k = j0 + wj * 32 * WJ + tb * 32 + 8 * sr_c;
+      return n < I && k < J;
+    };
+    if constexpr (Epi::kSR) {
+#pragma unroll
+      for (int ta = 0; ta < WI; ++ta)
+#pragma unroll
+        for (int tb = 0; tb < WJ; ++tb)
+#pragma unroll
+          for (int u = 0; u < 2; ++u) {
+            int64_t n, k;
+            const bool ok = sr_pos(ta, tb, u, n, k);
+            if constexpr (Epi::kTern) {
+              const uint8_t* src = ok ? epi.wq + n * epi.ldc + (k >> 2) : dummy;
+              const uint32_t v = *reinterpret_cast<const uint16_t*>(src);
+              if (u == 0) srt[ta][tb] = v;
+              else srt[ta][tb] |= v << 16;
+            } else {
+              const uint8_t* src = ok ? epi.wq + n * epi.ldc + k : dummy;
+              const uint2 v = *reinterpret_cast<const uint2*>(src);
+              sr8[ta][tb][u][0] = v.x;
+              sr8[ta][tb][u][1] = v.y;
+            }
+          }
+    }
     if (tid == 0) next_tile = cur.nsteps > 0 ? fetched : atomicAdd(next_ctr, 1);
     block_barrier();                   // every wave is done with every stage
     int gn, localn;
     const bool more = locate(grp, xcd, next_tile, gn, localn);
+    if constexpr (Epi::kSR) wait_vm<0>();   // the codes (nothing else is in flight)
     if (more) {
       const int slotn = (last + 1) % NS;      // the next tile's stages avoid `last`
       setup(gn, localn, cur);
@@ -723,18 +774,115 @@ __device__ __forceinline__ void gemm_v3_body(const Group<Epi>& grp, lds_u8* smem
         }
       }
     };
-    if (obf) {
+    if constexpr (Epi::kSR) {
+      // each 32 x 32 block of dW staged in LDS as fp32, then read back as
+      // two chunks of 8 consecutive entries of a row per lane, which update
+      // their 8 codes; out-of-range chunks count nothing and store their
+      // codes to the dummy slot (a fixed number of stores per thread)
+      SRArgs sa;
+      sa.c = epi.c;
+      sa.L = epi.L;
+      sa.qmin = epi.qmin;
+      sa.qmax = epi.qmax;
+      sa.k0 = epi.k0;
+      sa.k1 = epi.k1;
+      sa.step = epi.step;
+      sa.tid = epi.tid;
+      uint32_t tc = 0, tn = 0;   // this tile's counts
+      // 32 rows x 64 columns (both column blocks of a row block) per wave:
+      // two 32 x 128-byte areas, laid out as the fp32 staging above
+      static_assert(NW * 32 * 256 <= SLOTB, "SR staging (32 rows of 256 bytes per wave) fits in one stage");
+      lds_u8* const st2 = smem + last * SLOTB + wave * (32 * 256);
 #pragma unroll
-      for (int ta = 0; ta < WI; ++ta) epi_block(ta, std::integral_constant<int, 2>{});
+      for (int ta = 0; ta < WI; ++ta) {
+#pragma unroll
+        for (int tb = 0; tb < WJ; ++tb)
+#pragma unroll
+          for (int k = 0; k < 4; ++k) {
+            const f32x4 w = {(float)acc[ta][tb][4 * k], (float)acc[ta][tb][4 * k + 1],
+                             (float)acc[ta][tb][4 * k + 2], (float)acc[ta][tb][4 * k + 3]};
+            *(__attribute__((address_space(3))) f32x4*)(st2 + tb * (32 * 128) + j_e * 128 +
+                                                          (((2 * k + h_e) ^ sw_w) << 4)) = w;
+          }
+        __asm__ volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+        // the row block's 2 WJ chunks from LDS, one at a time (not
+        // unrolled: short code, few live registers)
+#pragma unroll 1
+        for (int cq = 0; cq < 2 * WJ; ++cq) {
+          const int tb = cq >> 1, u = cq & 1;
+          const int row = sr_r + 16 * u;
+          const int sw = (row >> 1) & 7;
+          const lds_u8* sb = st2 + tb * (32 * 128) + row * 128;
+          f32x4 gv[2];
+          gv[0] = *(const __attribute__((address_space(3))) f32x4*)(sb + (((2 * sr_c) ^ sw) << 4));
+          gv[1] = *(const __attribute__((address_space(3))) f32x4*)(sb + (((2 * sr_c + 1) ^ sw) << 4));
+          int64_t n, k;
+          const bool ok = sr_pos(ta, tb, u, n, k);
+          uint32_t win[4] = {0u, 0u, 0u, 0u};
+          if constexpr (Epi::kTern) {
+            uint32_t w2 = srt[ta][0];
+#pragma unroll
+            for (int t = 1; t < WJ; ++t) w2 = tb == t ? srt[ta][t] : w2;
+            win[0] = (w2 >> (16 * u)) & 0xFFFFu;
+          } else {
+            uint32_t x0 = sr8[ta][0][0][0], x1 = sr8[ta][0][0][1];
+#pragma unroll
+            for (int t = 0; t < WJ; ++t)
+#pragma unroll
+              for (int v = 0; v < 2; ++v)
+                if (cq == 2 * t + v) {
+                  x0 = sr8[ta][t][v][0];
+                  x1 = sr8[ta][t][v][1];
+                }
+            win[0] = x0;
+            win[1] = x1;
+          }
+          uint32_t wout[4];
+          uint32_t ch = 0, nf = 0;
+          sr_chunk<Epi::kTern, 8>(win, gv, (uint64_t)(n * epi.d_in + k) >> 3, sa, wout, ch, nf);
+          if (ok) {
+            tc += ch;
+            tn += nf;
+          }
+          if constexpr (Epi::kTern) {
+            uint8_t* dst = ok ? epi.wq + n * epi.ldc + (k >> 2) : dummy;
+            *reinterpret_cast<uint16_t*>(dst) = (uint16_t)wout[0];
+          } else {
+            uint8_t* dst = ok ? epi.wq + n * epi.ldc + k : dummy;
+            *reinterpret_cast<uint2*>(dst) = make_uint2(wout[0], wout[1]);
+          }
+        }
+        __asm__ volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+      }
+      tc = wave_sum_u32(tc);
+      tn = wave_sum_u32(tn);
+      if (lane == 0) {
+        sr_cnt[2 * wave_u] += tc;
+        sr_cnt[2 * wave_u + 1] += tn;
+      }
+      stores_prev = kStoresSR;
     } else {
+      if (obf) {
 #pragma unroll
-      for (int ta = 0; ta < WI; ++ta) epi_block(ta, std::integral_constant<int, 4>{});
+        for (int ta = 0; ta < WI; ++ta) epi_block(ta, std::integral_constant<int, 2>{});
+      } else {
+#pragma unroll
+        for (int ta = 0; ta < WI; ++ta) epi_block(ta, std::integral_constant<int, 4>{});
+      }
+      stores_prev = obf ? kStoresBf16 : kStoresF32;
     }
-    obf_prev = obf;
     if (!more) break;
     // a tile without reduction steps has no main-loop barrier before the
     // next epilogue reuses the staging area and the row scales
     if (cur.nsteps == 0) block_barrier();
+  }
+  if constexpr (Epi::kSR) {
+    unsigned long long* const cnt = grp.p[0].epi.counters;
+    if (cnt != nullptr && lane == 0) {
+      const unsigned long long c = sr_cnt[2 * wave_u], f = sr_cnt[2 * wave_u + 1];
+      if (c) atomicAdd(cnt, c);
+      if (f) atomicAdd(cnt + 1, f);
+    }
   }
   finish();
 }
@@ -1008,6 +1156,73 @@ __global__ __launch_bounds__(256) void split_reduce_batch_kernel(const RedTab ta
     acc[3] = acc[3] + v[3];
   }
   reinterpret_cast<f32x4*>(tab.dst[s])[t] = acc;
+}
+
+// The split-K sum of dW (the same order as split_reduce_batch_kernel, so the
+// same dW bits) consumed by the SR update of the codes, 8 weights per
+// thread; dW is never stored.
+struct RedSRTab {
+  const float* src[MAXG];     // [splits][n] partials
+  uint8_t* wq[MAXG];          // codes, updated in place
+  int64_t n8[MAXG];           // n / 8
+  float c[MAXG], L[MAXG];
+  int32_t qmin[MAXG], qmax[MAXG];
+  uint32_t tid[MAXG];
+  int32_t b0[MAXG + 1];
+  int32_t n, splits;
+  uint32_t k0, k1, step;
+  unsigned long long* counters;
+};
+template <bool TERN>
+__global__ __launch_bounds__(256) void split_reduce_sr_kernel(const RedSRTab tab) {
+  int s = 0;
+  while (s + 1 < tab.n && (int)blockIdx.x >= tab.b0[s + 1]) ++s;
+  const int64_t t = (int64_t)(blockIdx.x - tab.b0[s]) * 256 + threadIdx.x;
+  uint32_t ch = 0, nf = 0;
+  if (t < tab.n8[s]) {
+    const int64_t n4 = 2 * tab.n8[s];
+    const f32x4* src = reinterpret_cast<const f32x4*>(tab.src[s]);
+    f32x4 gv[2];
+    gv[0] = __builtin_nontemporal_load(src + 2 * t);
+    gv[1] = __builtin_nontemporal_load(src + 2 * t + 1);
+    for (int k = 1; k < tab.splits; ++k) {
+#pragma unroll
+      for (int e = 0; e < 2; ++e) {
+        const f32x4 v = __builtin_nontemporal_load(src + (int64_t)k * n4 + 2 * t + e);
+        gv[e][0] = gv[e][0] + v[0];
+        gv[e][1] = gv[e][1] + v[1];
+        gv[e][2] = gv[e][2] + v[2];
+        gv[e][3] = gv[e][3] + v[3];
+      }
+    }
+    SRArgs a;
+    a.c = tab.c[s];
+    a.L = tab.L[s];
+    a.qmin = tab.qmin[s];
+    a.qmax = tab.qmax[s];
+    a.k0 = tab.k0;
+    a.k1 = tab.k1;
+    a.step = tab.step;
+    a.tid = tab.tid[s];
+    uint32_t win[4] = {0u, 0u, 0u, 0u}, wout[4];
+    if constexpr (TERN) {
+      win[0] = reinterpret_cast<const uint16_t*>(tab.wq[s])[t];
+    } else {
+      const uint2 v = reinterpret_cast<const uint2*>(tab.wq[s])[t];
+      win[0] = v.x;
+      win[1] = v.y;
+    }
+    sr_chunk<TERN, 8>(win, gv, (uint64_t)t, a, wout, ch, nf);
+    if constexpr (TERN) reinterpret_cast<uint16_t*>(tab.wq[s])[t] = (uint16_t)wout[0];
+    else reinterpret_cast<uint2*>(tab.wq[s])[t] = make_uint2(wout[0], wout[1]);
+  }
+  if (tab.counters != nullptr) {
+    const unsigned long long c = wave_sum_u64(ch), f = wave_sum_u64(nf);
+    if ((threadIdx.x & (kWave - 1)) == 0) {
+      if (c) atomicAdd(tab.counters, c);
+      if (f) atomicAdd(tab.counters + 1, f);
+    }
+  }
 }
 
 static int32_t seal(SegTab& t) {
@@ -1296,12 +1511,10 @@ hipError_t launch_dx_batch(const BatchCfg& c, const LinearIO* io, uint8_t* ws, c
   return hipGetLastError();
 }
 
-// dW[n, k] = sum_m dY[m, n] X~T[k, m]: I = d_out, J = d_in, R = M.
-// Launches the pre-pass that writes X~T once per distinct quantised input
-// and fills the problems of the group (split over the batch as planned).
-static void prep_dw(const BatchCfg& c, const LinearIO* io, uint8_t* ws, const BwdPlan& P,
-                    hipStream_t stream, Group<EpiPartial>& grp) {
-  int first[kMaxBatch];
+// X~T once per distinct quantised input (the dequantising transpose
+// pre-pass); first[l] is the linear whose X~T linear l reads.
+static void prep_xt(const BatchCfg& c, const LinearIO* io, uint8_t* ws, const BwdPlan& P,
+                    hipStream_t stream, int* first) {
   DqTab tab{};
   tab.M = c.M;
   tab.Mp = xt_stride(c.M);
@@ -1328,23 +1541,41 @@ static void prep_dw(const BatchCfg& c, const LinearIO* io, uint8_t* ws, const Bw
     else
       hipLaunchKernelGGL(dequant_t_kernel<false>, dim3(blocks), dim3(256), 0, stream, tab);
   }
+}
+
+// dW[n, k] = sum_m dY[m, n] X~T[k, m]: I = d_out, J = d_in, R = M, split over
+// the batch into P.splits parts; make(l) gives linear l's epilogue.
+template <class Epi, class MakeEpi>
+static void fill_dw(const BatchCfg& c, const LinearIO* io, uint8_t* ws, const BwdPlan& P,
+                    const int* first, Group<Epi>& grp, MakeEpi make) {
   const int64_t splits = P.splits;
   int64_t len = splits > 1 ? (c.M + splits - 1) / splits : (c.M > 0 ? c.M : 1);
   len = (len + 63) / 64 * 64;
   grp.ng = c.n;
   for (int l = 0; l < c.n; ++l) {
-    Prob<EpiPartial>& p = grp.p[l];
+    Prob<Epi>& p = grp.p[l];
     const int64_t I = io[l].d_out, J = io[l].d_in;
     p.A = Opnd{static_cast<const uint8_t*>(io[l].dY), I * 2, I};
     p.B = Opnd{ws + P.xt_off[first[l]], xt_stride(c.M) * 2, J};
-    float* target = splits > 1 ? reinterpret_cast<float*>(ws + P.part_off[l]) : io[l].dW;
-    p.epi = EpiPartial{target, J, I * J};
+    p.epi = make(l);
     p.I = I;
     p.J = J;
     p.R = c.M;
     p.split_len = len;
     p.nbz = (int32_t)splits;
   }
+}
+
+// dW into dW (one split) or into the workspace partials (several).
+static void prep_dw(const BatchCfg& c, const LinearIO* io, uint8_t* ws, const BwdPlan& P,
+                    hipStream_t stream, Group<EpiPartial>& grp) {
+  int first[kMaxBatch];
+  prep_xt(c, io, ws, P, stream, first);
+  fill_dw(c, io, ws, P, first, grp, [&](int l) {
+    const int64_t I = io[l].d_out, J = io[l].d_in;
+    float* target = P.splits > 1 ? reinterpret_cast<float*>(ws + P.part_off[l]) : io[l].dW;
+    return EpiPartial{target, J, I * J};
+  });
 }
 
 // Sum of the batch-split dW partials into dW.
@@ -1398,6 +1629,105 @@ hipError_t launch_dxdw_batch(const BatchCfg& c, const LinearIO* io, uint8_t* ws,
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   return reduce_dw(c, io, ws, Q, stream);
+}
+
+// Partials of a batch-split dW summed and consumed by the SR update.
+static hipError_t reduce_sr(const BatchCfg& c, const LinearIO* io, const SRTensor* t, uint64_t seed,
+                            uint32_t step, unsigned long long* counters, uint8_t* ws,
+                            const BwdPlan& P, hipStream_t stream) {
+  RedSRTab red{};
+  red.n = c.n;
+  red.splits = (int32_t)P.splits;
+  red.k0 = (uint32_t)seed;
+  red.k1 = (uint32_t)(seed >> 32);
+  red.step = step;
+  red.counters = counters;
+  int32_t blocks = 0;
+  for (int l = 0; l < c.n; ++l) {
+    red.src[l] = reinterpret_cast<const float*>(ws + P.part_off[l]);
+    red.wq[l] = t[l].wq;
+    red.n8[l] = io[l].d_out * io[l].d_in / 8;
+    red.c[l] = t[l].c;
+    red.L[l] = (float)(t[l].qmax - t[l].qmin + 1);
+    red.qmin[l] = t[l].qmin;
+    red.qmax[l] = t[l].qmax;
+    red.tid[l] = t[l].tensor_id;
+    red.b0[l] = blocks;
+    blocks += (int32_t)((red.n8[l] + 255) / 256);
+  }
+  red.b0[c.n] = blocks;
+  if (c.w_ternary)
+    hipLaunchKernelGGL(split_reduce_sr_kernel<true>, dim3((unsigned)blocks), dim3(256), 0, stream, red);
+  else
+    hipLaunchKernelGGL(split_reduce_sr_kernel<false>, dim3((unsigned)blocks), dim3(256), 0, stream, red);
+  return hipGetLastError();
+}
+
+// dW of every linear consumed by the SR update of its codes in the GEMM
+// epilogue (one split) or in the reduction of the partials (several), with
+// dX of every linear in the same launch when with_dx.
+template <bool TERN>
+static void launch_dw_sr_group(const BatchCfg& c, const LinearIO* io, const SRTensor* t, uint64_t seed,
+                               uint32_t step, unsigned long long* counters, uint8_t* ws,
+                               const BwdPlan& P, const int* first, Group<EpiScale>* gx,
+                               hipStream_t stream) {
+  Group<EpiSR<TERN>> gw{};
+  fill_dw(c, io, ws, P, first, gw, [&](int l) {
+    EpiSR<TERN> e;
+    e.wq = t[l].wq;
+    e.ldc = TERN ? io[l].d_in / 4 : io[l].d_in;
+    e.d_in = io[l].d_in;
+    e.c = t[l].c;
+    e.L = (float)(t[l].qmax - t[l].qmin + 1);
+    e.qmin = t[l].qmin;
+    e.qmax = t[l].qmax;
+    e.k0 = (uint32_t)seed;
+    e.k1 = (uint32_t)(seed >> 32);
+    e.step = step;
+    e.tid = t[l].tensor_id;
+    e.counters = counters;
+    return e;
+  });
+  if (gx != nullptr)
+    launch_dual<EBF16, KM, KC, KB_BWD, EpiSR<TERN>, EBF16, KC, KC, KB_BWD, EpiScale>(gw, *gx, ws, stream);
+  else
+    launch_group<EBF16, KM, KC, KB_BWD, EpiSR<TERN>>(gw, ws, stream);
+}
+
+hipError_t launch_bwd_sr_batch(const BatchCfg& c, const LinearIO* io, const SRTensor* t, uint64_t seed,
+                               uint32_t step, unsigned long long* counters, bool with_dx, uint8_t* ws,
+                               const BwdPlan& P, hipStream_t stream) {
+  if (c.n == 0 || c.M == 0) return hipSuccess;
+  if (with_dx && c.w_ternary && DX_PACKED_B) {
+    const hipError_t e = launch_dx_batch(c, io, ws, P, stream);
+    if (e != hipSuccess) return e;
+    with_dx = false;
+  }
+  BwdPlan Q = P;
+  Q.splits = with_dx ? P.splits_dual : P.splits;
+  Group<EpiScale> gx{};
+  if (with_dx) prep_dx(c, io, ws, Q, stream, gx);
+  int first[kMaxBatch];
+  prep_xt(c, io, ws, Q, stream, first);
+  if (Q.splits == 1) {
+    if (c.w_ternary)
+      launch_dw_sr_group<true>(c, io, t, seed, step, counters, ws, Q, first, with_dx ? &gx : nullptr, stream);
+    else
+      launch_dw_sr_group<false>(c, io, t, seed, step, counters, ws, Q, first, with_dx ? &gx : nullptr, stream);
+    return hipGetLastError();
+  }
+  Group<EpiPartial> gw{};
+  fill_dw(c, io, ws, Q, first, gw, [&](int l) {
+    const int64_t I = io[l].d_out, J = io[l].d_in;
+    return EpiPartial{reinterpret_cast<float*>(ws + Q.part_off[l]), J, I * J};
+  });
+  if (with_dx)
+    launch_dual<EBF16, KM, KC, KB_BWD, EpiPartial, EBF16, KC, KC, KB_BWD, EpiScale>(gw, gx, ws, stream);
+  else
+    launch_group<EBF16, KM, KC, KB_BWD, EpiPartial>(gw, ws, stream);
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  return reduce_sr(c, io, t, seed, step, counters, ws, Q, stream);
 }
 
 }  // namespace dqt

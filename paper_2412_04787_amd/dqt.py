@@ -23,7 +23,8 @@ DQT_F32, DQT_BF16, DQT_I8, DQT_FP8E4M3, DQT_TERNARY2 = 0, 1, 2, 3, 4
 EXPORTS = (
     "dqt_act_quant", "dqt_act_quant_batch", "dqt_linear_fwd_workspace", "dqt_linear_fwd", "dqt_linear_bwd_workspace",
     "dqt_linear_bwd", "dqt_linear_fwd_batch_workspace", "dqt_linear_fwd_batch",
-    "dqt_linear_bwd_batch_workspace", "dqt_linear_bwd_batch", "dqt_sr_update_batch",
+    "dqt_linear_bwd_batch_workspace", "dqt_linear_bwd_batch", "dqt_linear_bwd_sr_batch",
+    "dqt_sr_update_batch",
     "dqt_sr_update", "dqt_debug_rng", "dqt_absmean_init", "dqt_pack_ternary",
     "dqt_unpack_ternary", "dqt_status_string", "dqt_version",
 )
@@ -85,6 +86,8 @@ _SIGS = {
     "dqt_linear_bwd_batch_workspace": (ctypes.c_size_t, [_i32, _vp, _i64]),
     "dqt_linear_bwd_batch": (_i32, [_i32, _vp, _i64, _i32, _i32, _i32, _i32, _vp,
                                     ctypes.c_size_t, _vp]),
+    "dqt_linear_bwd_sr_batch": (_i32, [_i32, _vp, _i64, _i32, _i32, _i32, _i32, _f32, _u64, _u32,
+                                       _vp, _vp, ctypes.c_size_t, _vp]),
     "dqt_sr_update_batch": (_i32, [_i32, _vp, _f32, _u64, _u32, _vp, _vp]),
     "dqt_debug_rng": (_i32, [_u64, _u32, _u32, _u64, _i64, _vp, _vp]),
     "dqt_absmean_init": (_i32, [_vp, _i64, _i32, _i32, _vp, _vp]),
@@ -263,6 +266,14 @@ def dqt_linear_bwd_batch(io, M: int, act_q: int, dy_t: int, xt_t: int, dx_t: int
     _check("dqt_linear_bwd_batch", load().dqt_linear_bwd_batch(len(io), io, M, act_q, dy_t, xt_t,
                                                                dx_t, _ptr(ws), ws_bytes,
                                                                _stream(stream)))
+
+
+def dqt_linear_bwd_sr_batch(io, M: int, act_q: int, dy_t: int, xt_t: int, dx_t: int, lr: float,
+                            seed: int, step: int, counters=None, ws=None, stream=None):
+    ws_bytes = 0 if ws is None else ws.numel() * ws.element_size()
+    _check("dqt_linear_bwd_sr_batch",
+           load().dqt_linear_bwd_sr_batch(len(io), io, M, act_q, dy_t, xt_t, dx_t, lr, seed, step,
+                                          _ptr(counters), _ptr(ws), ws_bytes, _stream(stream)))
 
 
 def dqt_sr_update_batch(io, lr: float, seed: int, step: int, counters=None, stream=None):
