@@ -23,6 +23,7 @@ Paper map (section / equation of the DQT paper):
   * Sec. 3.2 (backprop to the gradient of W~, no STE on weights) -> linear_bwd
   * Sec. 3.2, Eq. 5 ........ direct update W^ = SR(W')            -> sr_update
   * Sec. 5.2 ............... fraction of weights changed per step -> n_changed
+  * Sec. 4.1 (AdamW modified with SR; reading R11) ............... -> adamw_sr_update
 
 Readings of points the paper leaves open (each is listed in the design doc):
   R1  SR acts in grid units: with W~ = q * alpha (alpha = 1/s, Eq. 3) and
@@ -43,6 +44,16 @@ Readings of points the paper leaves open (each is listed in the design doc):
       Bernoulli(p) is realised as U < ceil(p * 2**32) with U uniform on
       [0, 2**32).
   R8  A non-finite gradient entry leaves its weight unchanged and is counted.
+  R11 AdamW with SR (Sec. 4.1 names AdamW, modified to round stochastically,
+      and gives no further detail): the target W' is the AdamW step with
+      decoupled weight decay and bias correction,
+        m <- b1 m + (1 - b1) g,  v <- b2 v + (1 - b2) g^2,
+        W' = W~ (1 - lr wd) - lr * mhat / (sqrt(vhat) + eps),
+        mhat = m / (1 - b1^t),  vhat = v / (1 - b2^t),
+      taken in grid units (R1) and rounded by Eq. 1 with the draws of R7;
+      m and v are fp32.  The element-wise arithmetic is fixed in fp32 (see
+      ``adamw_sr_update``); a non-finite gradient entry, or a NaN step, leaves
+      the weight, m and v unchanged and is counted.
 """
 
 from __future__ import annotations
@@ -422,11 +433,20 @@ def sr_update(q, g, lr, alpha, qmin: int, qmax: int, seed: int, step: int,
     finite = np.isfinite(g)
     with np.errstate(over="ignore", invalid="ignore"):
         delta32 = -(c * np.where(finite, g, np.float32(0))).astype(np.float32)
-    delta = delta32.astype(np.float64)
-    U = rng_u32(seed, step, tensor_id, idx).astype(np.float64)
+    new = _sr_round(q, delta32, qmin, qmax, seed, step, tensor_id, idx)
+    new = np.where(finite, new, q)
+    n_changed = int(np.count_nonzero(new != q))
+    n_nonfinite = int(np.count_nonzero(~finite))
+    return new, n_changed, n_nonfinite
 
-    new = np.empty_like(q)
-    big = ~np.isfinite(delta)                 # |c*g| overflowed fp32
+
+def _sr_round(q, delta32, qmin: int, qmax: int, seed: int, step: int, tensor_id: int, idx):
+    """Eq. 1 on x = q + delta (grid units), clipped to [qmin, qmax]; delta
+    is an fp32 array (an infinite delta saturates).  Element idx[i] keys the
+    draw of element i (R7)."""
+    delta = np.asarray(delta32, dtype=np.float32).astype(np.float64)
+    U = rng_u32(seed, step, tensor_id, idx).astype(np.float64)
+    big = ~np.isfinite(delta)                 # the step overflowed fp32
     d_ok = np.where(big, 0.0, delta)
     up_side = d_ok >= 0
     fl = np.floor(d_ok)
@@ -438,11 +458,91 @@ def sr_update(q, g, lr, alpha, qmin: int, qmax: int, seed: int, step: int,
     move = base + np.where(event, np.where(up_side, 1.0, -1.0), 0.0)
     x_new = q.astype(np.float64) + move
     x_new = np.where(big, np.where(delta > 0, np.inf, -np.inf), x_new)
-    new = np.clip(x_new, qmin, qmax).astype(np.int64)
-    new = np.where(finite, new, q)
-    n_changed = int(np.count_nonzero(new != q))
-    n_nonfinite = int(np.count_nonzero(~finite))
-    return new, n_changed, n_nonfinite
+    return np.clip(x_new, qmin, qmax).astype(np.int64)
+
+
+# ---------------------------------------------------------------------------
+# Next row: AdamW with SR (Sec. 4.1; reading R11).
+# ---------------------------------------------------------------------------
+
+
+def pow_by_squaring(b: float, t: int) -> float:
+    """b**t in float64 by binary exponentiation (t >= 0): square the base
+    and multiply it in for every set bit of t, low bit first."""
+    r, x = 1.0, float(b)
+    while t > 0:
+        if t & 1:
+            r = r * x
+        x = x * x
+        t >>= 1
+    return r
+
+
+def adamw_scalars(lr, alpha, beta1, beta2, eps, weight_decay, t: int) -> dict:
+    """Per-call constants, each formed in float64 from the fp32 inputs and
+    rounded once to fp32:
+      b1, b2, eps        the inputs;
+      ob1 = 1 - b1, ob2 = 1 - b2;
+      k2 = 1 / sqrt(1 - b2^t)          (sqrt(vhat) = sqrt(v) * k2);
+      cu = lr / (alpha * (1 - b1^t))   (the bias-corrected step in grid units);
+      cd = lr * weight_decay           (the decoupled decay per step)."""
+    f = lambda x: np.float32(np.float64(x))
+    b1 = np.float64(np.float32(beta1))
+    b2 = np.float64(np.float32(beta2))
+    lr64 = np.float64(np.float32(lr))
+    a64 = np.float64(np.float32(alpha))
+    wd64 = np.float64(np.float32(weight_decay))
+    return dict(b1=f(b1), b2=f(b2), eps=np.float32(eps), ob1=f(1.0 - b1), ob2=f(1.0 - b2),
+                k2=f(1.0 / np.sqrt(1.0 - pow_by_squaring(b2, t))),
+                cu=f(lr64 / (a64 * (1.0 - pow_by_squaring(b1, t)))),
+                cd=f(lr64 * wd64))
+
+
+def adamw_target(q, g, m, v, k: dict):
+    """One AdamW step in grid units, element-wise in fp32 (round to nearest
+    even after every operation, no fused multiply-add; sqrt and division
+    correctly rounded):
+      m' = b1 m + ob1 g
+      v' = b2 v + (ob2 g) g
+      den = sqrt(v') k2 + eps
+      u = m' / den
+      delta = -(cu u + cd q)
+    Returns (delta, m', v') as fp32 arrays: x = q + delta is W' / alpha."""
+    f32 = np.float32
+    q = np.asarray(q).astype(np.int64).astype(f32)
+    g = np.asarray(g, dtype=f32)
+    m = np.asarray(m, dtype=f32)
+    v = np.asarray(v, dtype=f32)
+    with np.errstate(over="ignore", invalid="ignore", divide="ignore"):
+        m1 = (k["b1"] * m).astype(f32) + (k["ob1"] * g).astype(f32)
+        v1 = (k["b2"] * v).astype(f32) + ((k["ob2"] * g).astype(f32) * g).astype(f32)
+        den = (np.sqrt(v1.astype(f32)) * k["k2"]).astype(f32) + k["eps"]
+        u = (m1.astype(f32) / den.astype(f32)).astype(f32)
+        delta = -((k["cu"] * u).astype(f32) + (k["cd"] * q).astype(f32)).astype(f32)
+    return delta.astype(f32), m1.astype(f32), v1.astype(f32)
+
+
+def adamw_sr_update(q, g, m, v, lr, alpha, beta1, beta2, eps, weight_decay, qmin: int,
+                    qmax: int, seed: int, step: int, tensor_id: int, idx=None):
+    """AdamW with SR (R11): the AdamW target of ``adamw_target`` with
+    t = step, rounded by Eq. 1 (``_sr_round``, draws keyed as in R7 by
+    (seed, step, tensor_id, element)) and clipped to [qmin, qmax].  An element
+    whose gradient is non-finite or whose delta is NaN keeps q, m and v.
+    Returns (q_new int64, m_new, v_new, n_changed, n_nonfinite)."""
+    q = np.asarray(q).astype(np.int64).ravel()
+    g = np.asarray(g, dtype=np.float32).ravel()
+    m = np.asarray(m, dtype=np.float32).ravel()
+    v = np.asarray(v, dtype=np.float32).ravel()
+    if idx is None:
+        idx = np.arange(q.size, dtype=np.uint64)
+    k = adamw_scalars(lr, alpha, beta1, beta2, eps, weight_decay, step)
+    delta, m1, v1 = adamw_target(q, g, m, v, k)
+    ok = np.isfinite(g) & ~np.isnan(delta)
+    new = _sr_round(q, np.where(ok, delta, np.float32(0)), qmin, qmax, seed, step, tensor_id, idx)
+    new = np.where(ok, new, q)
+    m_new = np.where(ok, m1, m).astype(np.float32)
+    v_new = np.where(ok, v1, v).astype(np.float32)
+    return (new, m_new, v_new, int(np.count_nonzero(new != q)), int(np.count_nonzero(~ok)))
 
 
 def sr_change_probability(q, g, lr, alpha, qmin: int, qmax: int) -> np.ndarray:
