@@ -262,6 +262,50 @@ dqt_status dqt_sr_update_batch(int32_t n, const dqt_linear_io* io, float lr,
                                unsigned long long* counters, void* stream);
 
 /*
+ * AdamW with direct stochastic rounding.  The paper trains DQT with AdamW
+ * modified to round stochastically (Sec. 4.1): the optimiser's target W'
+ * (Sec. 3.2) is the AdamW step with decoupled weight decay and bias
+ * correction, and the new code is Clip(SR(W' / alpha)) (Eq. 1 and 5 in grid
+ * units, the draws of dqt_sr_update).  The paper gives no further detail;
+ * this library fixes, per element, in fp32 with round-to-nearest-even after
+ * every operation (no fused multiply-add; sqrt and division correctly
+ * rounded):
+ *   m' = b1 m + ob1 g,   v' = b2 v + (ob2 g) g,
+ *   u  = m' / (sqrt(v') k2 + eps),   delta = -(cu u + cd q),   x = q + delta,
+ * with per-call constants formed in double and rounded once to fp32:
+ *   b1 = beta1, b2 = beta2, ob1 = 1 - b1, ob2 = 1 - b2,
+ *   k2 = 1 / sqrt(1 - b2^t), cu = lr / (alpha (1 - b1^t)), cd = lr wd,
+ * t = step, b^t by binary exponentiation (low bit first) in double.
+ * An element whose gradient is non-finite or whose delta is NaN keeps its
+ * code, m and v and is counted in counters[1].
+ */
+typedef struct {
+  float lr;             /* >= 0, finite                                         */
+  float beta1, beta2;   /* in [0, 1)                                            */
+  float eps;            /* > 0, finite                                          */
+  float weight_decay;   /* >= 0, finite (decoupled: W' includes -lr wd W~)      */
+} dqt_adamw;
+
+/* One tensor.  Wq (codes), m and v ([d_out, d_in] fp32, both zero before
+ * the first step) are updated in place; dW: [d_out, d_in] fp32.  step >= 1
+ * is AdamW's t and keys the draws as in dqt_sr_update.  counters: NULL, or
+ * device uint64[2] to which the changed and non-finite counts are ADDED.
+ * Errors: DQT_ERR_NULL, DQT_ERR_ALIGN (16 bytes), DQT_ERR_RANGE (a
+ * hyper-parameter out of range, step 0, or a non-finite cu). */
+dqt_status dqt_adamw_sr_update(const dqt_weight* w, void* Wq, const float* dW,
+                               float* m, float* v, const dqt_adamw* hp,
+                               uint64_t seed, uint32_t step,
+                               unsigned long long* counters, void* stream);
+
+/* n tensors of one code format in one launch; uses w, Wq, dW of each entry
+ * of io, and m[l], v[l] (host arrays of n device pointers). */
+dqt_status dqt_adamw_sr_update_batch(int32_t n, const dqt_linear_io* io,
+                                     float* const* m, float* const* v,
+                                     const dqt_adamw* hp, uint64_t seed,
+                                     uint32_t step, unsigned long long* counters,
+                                     void* stream);
+
+/*
  * Backward and direct SR update of n linears in one call (Sec. 3.2: the
  * update of Eq. 5 consumes dW of the backward), with dW never written to
  * memory: the dW product's epilogue updates the 8 codes of each group of 8

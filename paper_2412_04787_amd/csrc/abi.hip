@@ -328,6 +328,60 @@ dqt_status dqt_linear_bwd_sr_batch(int32_t n, const dqt_linear_io* io, int64_t M
   return from_hip(dqt::launch_bwd_sr_batch(c, L, t, seed, step, counters, nx == n, wsb, P, s));
 }
 
+dqt_status dqt_adamw_sr_update_batch(int32_t n, const dqt_linear_io* io, float* const* m,
+                                     float* const* v, const dqt_adamw* hp, uint64_t seed,
+                                     uint32_t step, unsigned long long* counters, void* stream) {
+  dqt::LinearIO L[DQT_MAX_BATCH];
+  int32_t wfmt;
+  dqt_status st = check_batch(n, io, L, &wfmt);
+  if (st != DQT_OK) return st;
+  if (hp == nullptr || (n > 0 && (m == nullptr || v == nullptr))) return DQT_ERR_NULL;
+  if (counters != nullptr && (reinterpret_cast<uintptr_t>(counters) & 7u) != 0) return DQT_ERR_ALIGN;
+  if (!(isfinite(hp->lr) && hp->lr >= 0.0f)) return DQT_ERR_RANGE;
+  if (!(hp->beta1 >= 0.0f && hp->beta1 < 1.0f && hp->beta2 >= 0.0f && hp->beta2 < 1.0f))
+    return DQT_ERR_RANGE;
+  if (!(isfinite(hp->eps) && hp->eps > 0.0f)) return DQT_ERR_RANGE;
+  if (!(isfinite(hp->weight_decay) && hp->weight_decay >= 0.0f)) return DQT_ERR_RANGE;
+  if (step == 0) return DQT_ERR_RANGE;
+  dqt::AdamTensor t[DQT_MAX_BATCH];
+  for (int l = 0; l < n; ++l) {
+    if (io[l].Wq == nullptr || io[l].dW == nullptr || m[l] == nullptr || v[l] == nullptr)
+      return DQT_ERR_NULL;
+    if (!aligned16(io[l].Wq) || !aligned16(io[l].dW) || !aligned16(m[l]) || !aligned16(v[l]))
+      return DQT_ERR_ALIGN;
+    // the bias-corrected step in grid units must be finite
+    double b1t = 1.0, x = (double)hp->beta1;
+    for (uint32_t e = step; e > 0; e >>= 1) {
+      if (e & 1u) b1t *= x;
+      x *= x;
+    }
+    const double cu = (double)hp->lr / ((double)io[l].w->alpha * (1.0 - b1t));
+    if (!isfinite((float)cu)) return DQT_ERR_RANGE;
+    t[l].wq = static_cast<uint8_t*>(io[l].Wq);
+    t[l].grad = io[l].dW;
+    t[l].m = m[l];
+    t[l].v = v[l];
+    t[l].nweights = (int64_t)io[l].w->d_out * (int64_t)io[l].w->d_in;
+    t[l].alpha = io[l].w->alpha;
+    t[l].qmin = io[l].w->qmin;
+    t[l].qmax = io[l].w->qmax;
+    t[l].tensor_id = io[l].w->tensor_id;
+  }
+  const dqt::AdamHyper h{hp->lr, hp->beta1, hp->beta2, hp->eps, hp->weight_decay};
+  return from_hip(dqt::launch_adamw_sr(wfmt == DQT_TERNARY2, n, t, h, seed, step, counters,
+                                       static_cast<hipStream_t>(stream)));
+}
+
+dqt_status dqt_adamw_sr_update(const dqt_weight* w, void* Wq, const float* dW, float* m, float* v,
+                               const dqt_adamw* hp, uint64_t seed, uint32_t step,
+                               unsigned long long* counters, void* stream) {
+  dqt_linear_io io{};
+  io.w = w;
+  io.Wq = Wq;
+  io.dW = const_cast<float*>(dW);
+  return dqt_adamw_sr_update_batch(1, &io, &m, &v, hp, seed, step, counters, stream);
+}
+
 dqt_status dqt_sr_update_batch(int32_t n, const dqt_linear_io* io, float lr, uint64_t seed,
                                uint32_t step, unsigned long long* counters, void* stream) {
   dqt::LinearIO L[DQT_MAX_BATCH];

@@ -104,6 +104,23 @@ struct SRTensor {
 };
 hipError_t launch_sr_update(bool ternary, int n, const SRTensor* t, uint64_t seed, uint32_t step,
                             unsigned long long* counters, hipStream_t stream);
+// AdamW with SR (up to kMaxBatch tensors of one code format per launch).
+struct AdamTensor {
+  uint8_t* wq;          // codes, updated in place
+  const float* grad;    // dW
+  float* m;             // first moment, updated in place
+  float* v;             // second moment, updated in place
+  int64_t nweights;     // multiple of 8
+  float alpha;
+  int qmin, qmax;
+  uint32_t tensor_id;
+};
+struct AdamHyper {
+  float lr, beta1, beta2, eps, weight_decay;
+};
+hipError_t launch_adamw_sr(bool ternary, int n, const AdamTensor* t, const AdamHyper& hp,
+                           uint64_t seed, uint32_t step, unsigned long long* counters,
+                           hipStream_t stream);
 hipError_t launch_debug_rng(uint64_t seed, uint32_t step, uint32_t tensor_id, uint64_t i0,
                             int64_t n, uint32_t* out, hipStream_t stream);
 

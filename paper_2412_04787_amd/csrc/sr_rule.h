@@ -48,40 +48,48 @@ struct SRArgs {
   uint32_t k0, k1, step, tid;
 };
 
-// One element, the full rule.  Returns the new code; sets `tie` when the
-// primary 16-bit draw equals the top 16 bits of the threshold (the secondary
-// draw decides).  x = q + delta; n = trunc(delta); r = delta - n (exact); the
-// move to the far side (q + n + sign(r)) happens iff U < T = ceil(|r| * 2^32).
-__device__ __forceinline__ int sr_one(int q, float g, uint32_t p16, const SRArgs& a,
-                                      bool& tie, bool& nonfinite) {
-  nonfinite = (__float_as_uint(g) & 0x7F800000u) == 0x7F800000u;
-  float delta = -(a.c * g);
-  delta = fminf(fmaxf(delta, -a.L), a.L);
+// One element, the full rule, for a step delta in grid units (x = q +
+// delta; an infinite delta saturates).  Returns the new code; sets `tie`
+// when the primary 16-bit draw equals the top 16 bits of the threshold (the
+// secondary draw decides).  n = trunc(delta); r = delta - n (exact); the
+// move to the far side (q + n + sign(r)) happens iff U < T = ceil(|r| 2^32).
+__device__ __forceinline__ int sr_one_d(int q, float delta_raw, uint32_t p16, const SRArgs& a,
+                                        bool& tie) {
+  const float delta = fminf(fmaxf(delta_raw, -a.L), a.L);
   const float n = truncf(delta);
   const float r = delta - n;
   const uint32_t T = (uint32_t)ceilf(fabsf(r) * 4294967296.0f);
   const uint32_t thi = T >> 16;
-  tie = !nonfinite && (p16 == thi) && (T != 0u);
+  tie = (p16 == thi) && (T != 0u);
   const bool move = p16 < thi;
-  int v = q + (int)n + (move ? (r > 0.0f ? 1 : -1) : 0);
-  v = min(max(v, a.qmin), a.qmax);
+  const int v = q + (int)n + (move ? (r > 0.0f ? 1 : -1) : 0);
+  return min(max(v, a.qmin), a.qmax);
+}
+// The plain update's element: delta = -c g; a non-finite g keeps q.
+__device__ __forceinline__ int sr_one(int q, float g, uint32_t p16, const SRArgs& a,
+                                      bool& tie, bool& nonfinite) {
+  nonfinite = (__float_as_uint(g) & 0x7F800000u) == 0x7F800000u;
+  const int v = sr_one_d(q, -(a.c * g), p16, a, tie);
+  tie = tie && !nonfinite;
   return nonfinite ? q : v;
 }
 
 // Secondary decision for a tie element: move iff S16 < (T & 0xFFFF).
-__device__ __forceinline__ int sr_tie(int q, float g, uint32_t s16, const SRArgs& a) {
-  float delta = -(a.c * g);
-  delta = fminf(fmaxf(delta, -a.L), a.L);
+__device__ __forceinline__ int sr_tie_d(int q, float delta_raw, uint32_t s16, const SRArgs& a) {
+  const float delta = fminf(fmaxf(delta_raw, -a.L), a.L);
   const float n = truncf(delta);
   const float r = delta - n;
   const uint32_t T = (uint32_t)ceilf(fabsf(r) * 4294967296.0f);
   const bool move = s16 < (T & 0xFFFFu);
-  int v = q + (int)n + (move ? (r > 0.0f ? 1 : -1) : 0);
+  const int v = q + (int)n + (move ? (r > 0.0f ? 1 : -1) : 0);
   return min(max(v, a.qmin), a.qmax);
 }
+__device__ __forceinline__ int sr_tie(int q, float g, uint32_t s16, const SRArgs& a) {
+  return sr_tie_d(q, -(a.c * g), s16, a);
+}
 
-// The same rule in fewer instructions, for finite gradients and no tie:
-//  * delta = med3(-c * g, -L, L); n = (int)delta truncates toward zero;
+// The same rule in fewer instructions, for a finite delta and no tie:
+//  * delta = med3(delta, -L, L); n = (int)delta truncates toward zero;
 //  * |r| = fract(|delta|) (exact: |delta| - floor(|delta|));
 //  * with P = (p16 << 16) | 0xFFFF, p16 < (T >> 16) iff P < T, and
 //    p16 == (T >> 16) iff (P - T) mod 2^32 <= 0xFFFF;
@@ -92,9 +100,9 @@ __device__ __forceinline__ int sr_tie(int q, float g, uint32_t s16, const SRArgs
 //    of P - F flags every element the secondary draw may have to decide.
 // `code` is q plus a per-format offset and [lo, hi] the offset range (one
 // median-of-three clamps).
-__device__ __forceinline__ int sr_fast(int code, float g, uint32_t P, float nc, float L, int lo,
-                                       int hi, uint32_t& tiemin) {
-  const float delta = __builtin_amdgcn_fmed3f(nc * g, -L, L);
+__device__ __forceinline__ int sr_fast_d(int code, float delta_raw, uint32_t P, float L, int lo,
+                                         int hi, uint32_t& tiemin) {
+  const float delta = __builtin_amdgcn_fmed3f(delta_raw, -L, L);
   const int n = (int)delta;
   const float ar = __builtin_amdgcn_fractf(fabsf(delta));
   const uint32_t F = (uint32_t)(ar * 4294967296.0f);
@@ -104,6 +112,11 @@ __device__ __forceinline__ int sr_fast(int code, float g, uint32_t P, float nc, 
   int r;
   asm("v_med3_i32 %0, %1, %2, %3" : "=v"(r) : "v"(v), "v"(lo), "v"(hi));
   return r;
+}
+// The plain update (delta = -c g = nc g).
+__device__ __forceinline__ int sr_fast(int code, float g, uint32_t P, float nc, float L, int lo,
+                                       int hi, uint32_t& tiemin) {
+  return sr_fast_d(code, nc * g, P, L, lo, hi, tiemin);
 }
 
 // The update of one chunk of CW consecutive weights, elements
@@ -186,6 +199,69 @@ __device__ __forceinline__ void sr_chunk(const uint32_t (&win)[4], const f32x4 (
   } else {
 #pragma unroll
     for (int w = 0; w < CW / 4; ++w) {
+      const uint32_t x = wout[w] ^ win[w];
+      changed += __builtin_popcount((((x & 0x7F7F7F7Fu) + 0x7F7F7F7Fu) | x) & 0x80808080u);
+    }
+  }
+}
+
+// One chunk of 8 consecutive weights (elements 8 blk .. 8 blk + 7, one
+// Philox block) moved by given steps delta[j] in grid units; bit j of `bad`
+// keeps code j (counted as non-finite; its delta must be 0).  Codes as in
+// sr_chunk.
+template <bool TERNARY, class Count>
+__device__ __forceinline__ void sr_chunk_delta(const uint32_t (&win)[4], const float (&delta)[8], uint32_t bad,
+                                               uint64_t blk, const SRArgs& a, uint32_t (&wout)[4],
+                                               Count& changed, Count& nonfin) {
+  const uint4 r = philox_block(blk, 0u, a.step, a.tid, a.k0, a.k1);
+  auto q_of = [&](int j) {
+    return TERNARY ? (int)((win[0] >> (2 * j)) & 3u) - 1 : (int)(int8_t)(win[j >> 2] >> (8 * (j & 3)));
+  };
+  uint32_t tiemin = 0xFFFFFFFFu;
+#pragma unroll
+  for (int w = 0; w < 4; ++w) wout[w] = 0;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const uint32_t word = (j >> 1) == 0 ? r.x : (j >> 1) == 1 ? r.y : (j >> 1) == 2 ? r.z : r.w;
+    const uint32_t P = (j & 1) ? (word | 0xFFFFu) : ((word << 16) | 0xFFFFu);
+    if constexpr (TERNARY) {
+      const int code = (int)((win[0] >> (2 * j)) & 3u);
+      const int v = sr_fast_d(code, delta[j], P, a.L, a.qmin + 1, a.qmax + 1, tiemin);
+      wout[0] |= (uint32_t)v << (2 * j);
+    } else {
+      const int code = (int)(int8_t)(win[j >> 2] >> (8 * (j & 3)));
+      const int v = sr_fast_d(code, delta[j], P, a.L, a.qmin, a.qmax, tiemin);
+      wout[j >> 2] |= ((uint32_t)v & 0xFFu) << (8 * (j & 3));
+    }
+  }
+  if (tiemin <= 0xFFFFu) {
+    // rare: full rule (a kept element has delta 0, which the rule keeps)
+    uint32_t ties = 0;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      bool tie;
+      (void)sr_one_d(q_of(j), delta[j], half16(r, j), a, tie);
+      ties |= (tie ? 1u : 0u) << j;
+    }
+    const uint4 sb = ties ? philox_block(blk, 1u, a.step, a.tid, a.k0, a.k1) : make_uint4(0u, 0u, 0u, 0u);
+#pragma unroll
+    for (int w = 0; w < 4; ++w) wout[w] = 0;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      bool tie;
+      const int v = (ties >> j) & 1u ? sr_tie_d(q_of(j), delta[j], half16(sb, j), a)
+                                     : sr_one_d(q_of(j), delta[j], half16(r, j), a, tie);
+      if constexpr (TERNARY) wout[0] |= (uint32_t)(v + 1) << (2 * j);
+      else wout[j >> 2] |= ((uint32_t)v & 0xFFu) << (8 * (j & 3));
+    }
+  }
+  nonfin += __builtin_popcount(bad);
+  if constexpr (TERNARY) {
+    const uint32_t x = wout[0] ^ win[0];
+    changed += __builtin_popcount((x | (x >> 1)) & 0x55555555u);
+  } else {
+#pragma unroll
+    for (int w = 0; w < 2; ++w) {
       const uint32_t x = wout[w] ^ win[w];
       changed += __builtin_popcount((((x & 0x7F7F7F7Fu) + 0x7F7F7F7Fu) | x) & 0x80808080u);
     }

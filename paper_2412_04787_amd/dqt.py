@@ -24,7 +24,7 @@ EXPORTS = (
     "dqt_act_quant", "dqt_act_quant_batch", "dqt_linear_fwd_workspace", "dqt_linear_fwd", "dqt_linear_bwd_workspace",
     "dqt_linear_bwd", "dqt_linear_fwd_batch_workspace", "dqt_linear_fwd_batch",
     "dqt_linear_bwd_batch_workspace", "dqt_linear_bwd_batch", "dqt_linear_bwd_sr_batch",
-    "dqt_sr_update_batch",
+    "dqt_sr_update_batch", "dqt_adamw_sr_update", "dqt_adamw_sr_update_batch",
     "dqt_sr_update", "dqt_debug_rng", "dqt_absmean_init", "dqt_pack_ternary",
     "dqt_unpack_ternary", "dqt_status_string", "dqt_version",
 )
@@ -89,6 +89,8 @@ _SIGS = {
     "dqt_linear_bwd_sr_batch": (_i32, [_i32, _vp, _i64, _i32, _i32, _i32, _i32, _f32, _u64, _u32,
                                        _vp, _vp, ctypes.c_size_t, _vp]),
     "dqt_sr_update_batch": (_i32, [_i32, _vp, _f32, _u64, _u32, _vp, _vp]),
+    "dqt_adamw_sr_update": (_i32, [_wp, _vp, _vp, _vp, _vp, _vp, _u64, _u32, _vp, _vp]),
+    "dqt_adamw_sr_update_batch": (_i32, [_i32, _vp, _vp, _vp, _vp, _u64, _u32, _vp, _vp]),
     "dqt_debug_rng": (_i32, [_u64, _u32, _u32, _u64, _i64, _vp, _vp]),
     "dqt_absmean_init": (_i32, [_vp, _i64, _i32, _i32, _vp, _vp]),
     "dqt_pack_ternary": (_i32, [_vp, _i64, _i64, _vp]),
@@ -274,6 +276,35 @@ def dqt_linear_bwd_sr_batch(io, M: int, act_q: int, dy_t: int, xt_t: int, dx_t: 
     _check("dqt_linear_bwd_sr_batch",
            load().dqt_linear_bwd_sr_batch(len(io), io, M, act_q, dy_t, xt_t, dx_t, lr, seed, step,
                                           _ptr(counters), _ptr(ws), ws_bytes, _stream(stream)))
+
+
+class DqtAdamW(ctypes.Structure):
+    _fields_ = [("lr", ctypes.c_float), ("beta1", ctypes.c_float), ("beta2", ctypes.c_float),
+                ("eps", ctypes.c_float), ("weight_decay", ctypes.c_float)]
+
+
+def adamw(lr: float, beta1: float = 0.9, beta2: float = 0.999, eps: float = 1e-8,
+          weight_decay: float = 0.0) -> DqtAdamW:
+    return DqtAdamW(lr, beta1, beta2, eps, weight_decay)
+
+
+def dqt_adamw_sr_update(w, Wq, dW, m, v, hp: DqtAdamW, seed: int, step: int, counters=None,
+                        stream=None):
+    _check("dqt_adamw_sr_update",
+           load().dqt_adamw_sr_update(ctypes.byref(w), _ptr(Wq), _ptr(dW), _ptr(m), _ptr(v),
+                                      ctypes.byref(hp), seed, step, _ptr(counters),
+                                      _stream(stream)))
+
+
+def dqt_adamw_sr_update_batch(io, ms, vs, hp: DqtAdamW, seed: int, step: int, counters=None,
+                              stream=None):
+    """ms, vs: lists of fp32 device tensors (the moments of each entry of io)."""
+    n = len(io)
+    mp = (ctypes.c_void_p * n)(*[t.data_ptr() for t in ms])
+    vp = (ctypes.c_void_p * n)(*[t.data_ptr() for t in vs])
+    _check("dqt_adamw_sr_update_batch",
+           load().dqt_adamw_sr_update_batch(n, io, mp, vp, ctypes.byref(hp), seed, step,
+                                            _ptr(counters), _stream(stream)))
 
 
 def dqt_sr_update_batch(io, lr: float, seed: int, step: int, counters=None, stream=None):

@@ -194,3 +194,46 @@ def test_workspace_depends_on_shape_only():
     b = _w(d_out=2048, d_in=768, alpha=0.5)
     assert lib.dqt_linear_bwd_workspace(ctypes.byref(a), 8192) == \
         lib.dqt_linear_bwd_workspace(ctypes.byref(b), 8192)
+
+
+def test_adamw_sr_argument_checks():
+    """AdamW with SR: hyper-parameters, step and pointers are checked before
+    anything is launched."""
+    lib = dqt.load()
+    bw = ctypes.byref(_w())
+
+    def call(hp, step=1, m=FAKE, v=FAKE, wq=FAKE, dw=FAKE):
+        return lib.dqt_adamw_sr_update(bw, wq, dw, m, v, None if hp is None else ctypes.byref(hp),
+                                       0, step, None, None)
+
+    ok = dqt.adamw(1e-3)
+    assert call(None) == dqt.DQT_ERR_NULL
+    assert call(ok, step=0) == dqt.DQT_ERR_RANGE
+    assert call(dqt.adamw(1e-3, eps=0.0)) == dqt.DQT_ERR_RANGE
+    assert call(dqt.adamw(1e-3, beta1=1.0)) == dqt.DQT_ERR_RANGE
+    assert call(dqt.adamw(1e-3, beta2=-0.1)) == dqt.DQT_ERR_RANGE
+    assert call(dqt.adamw(-1e-3)) == dqt.DQT_ERR_RANGE
+    assert call(dqt.adamw(float("nan"))) == dqt.DQT_ERR_RANGE
+    assert call(dqt.adamw(1e-3, weight_decay=-1.0)) == dqt.DQT_ERR_RANGE
+    assert call(ok, m=None) == dqt.DQT_ERR_NULL
+    assert call(ok, v=UNALIGNED) == dqt.DQT_ERR_ALIGN
+    assert call(ok, wq=None) == dqt.DQT_ERR_NULL
+    # a step that overflows fp32 in grid units
+    tiny = ctypes.byref(_w(alpha=1e-38))
+    assert lib.dqt_adamw_sr_update(tiny, FAKE, FAKE, FAKE, FAKE, ctypes.byref(dqt.adamw(1e3)), 0, 1,
+                                   None, None) == dqt.DQT_ERR_RANGE
+
+
+def test_fused_bwd_sr_argument_checks_host():
+    """The fused backward + SR call rejects a dW pointer, the fp32
+    environment and a bad learning rate before launching anything."""
+    lib = dqt.load()
+    io = dqt.linear_io([dict(w=_w())])
+    io[0].Wq = io[0].Xq = io[0].xdq = io[0].dY = FAKE.value
+    io[0].dW = FAKE.value
+    bf, f32 = dqt.DQT_BF16, dqt.DQT_F32
+    args = lambda dy, lr: (1, io, 64, dqt.DQT_I8, dy, dy, bf, lr, 0, 1, None, FAKE, 1 << 30, None)
+    assert lib.dqt_linear_bwd_sr_batch(*args(bf, 1e-3)) == dqt.DQT_ERR_UNSUPPORTED
+    io[0].dW = None
+    assert lib.dqt_linear_bwd_sr_batch(*args(f32, 1e-3)) == dqt.DQT_ERR_UNSUPPORTED
+    assert lib.dqt_linear_bwd_sr_batch(*args(bf, -1.0)) == dqt.DQT_ERR_RANGE
