@@ -96,6 +96,9 @@ class Block:
                              dX=self.dX[li], dW=self.dW[li]))
         self.io_all = dqt.linear_io(ents)
         self.io_fused = dqt.linear_io([dict(e, dW=None) for e in ents])
+        # AdamW moments (only the adamw_sr breakdown entry uses them)
+        self.m = [torch.zeros_like(t) for t in self.dW]
+        self.v = [torch.zeros_like(t) for t in self.dW]
         self.act_io = dqt.act_io([(self.X[n], self.Xq[n], self.xdq[n]) for n in wl.inputs])
         self.x_t = dqt.DQT_BF16 if wl.x_dtype == "bf16" else dqt.DQT_F32
         self.io_dx = dqt.linear_io([dict(e, dW=None) for e in ents])
@@ -144,10 +147,12 @@ def algorithmic_units(wl):
     f = sum(2 * M * l.d_in * l.d_out for l in wl.linears)
     code_b = 0.25 if wl.wfmt == "ternary" else 1.0
     sr_bytes = sum((2 * code_b + 4) * l.d_in * l.d_out for l in wl.linears)
+    # AdamW with SR: read g, m, v and the code; write m, v and the code
+    adam_bytes = sum((2 * code_b + 20) * l.d_in * l.d_out for l in wl.linears)
     xb = 2 if wl.x_dtype == "bf16" else 4
     act_bytes = sum(M * wl.input_width(n) * (xb + 1) + 4 * M for n in wl.inputs)
     return {"fwd": f, "bwd": 2 * f, "bwd_sr": 2 * f, "bwd_dx": f, "bwd_dw": f, "sr": sr_bytes,
-            "act_quant": act_bytes}
+            "act_quant": act_bytes, "adamw_sr": adam_bytes}
 
 
 def cpu_baseline(wl, tokens: int, min_seconds: float = 10.0):
@@ -288,7 +293,9 @@ def main():
     # replayed back to back between two events on the same stream.  The
     # step's own calls first; then dX and dW each in a call of its own.
     step_kinds = ["act_quant", "fwd"] + (["bwd_sr"] if args.sr == "fused" else ["bwd", "sr"])
-    kinds = step_kinds + (["bwd", "sr"] if args.sr == "fused" else []) + ["bwd_dx", "bwd_dw"]
+    kinds = step_kinds + (["bwd", "sr"] if args.sr == "fused" else []) + ["bwd_dx", "bwd_dw",
+                                                                         "adamw_sr"]
+    adam_hp = dqt.adamw(wl.lr, 0.9, 0.95, 1e-8, 0.1)
     per_kind_ms, per_kind_units, per_kind_n = {}, {}, {}
     for kind in kinds:
         calls = []
@@ -300,8 +307,14 @@ def main():
 
         g = torch.cuda.CUDAGraph()
         with torch.cuda.graph(g):
-            run_step(blk, dqt, 1, None, only, split_bwd=kind in ("bwd_dx", "bwd_dw"),
-                     sr="fused" if kind == "bwd_sr" else "separate")
+            if kind == "adamw_sr":
+                # the AdamW variant of the update (not part of the step)
+                calls.append(kind)
+                dqt.dqt_adamw_sr_update_batch(blk.io_all, blk.m, blk.v, adam_hp, wl.seed, 1,
+                                              blk.counters, None)
+            else:
+                run_step(blk, dqt, 1, None, only, split_bwd=kind in ("bwd_dx", "bwd_dw"),
+                         sr="fused" if kind == "bwd_sr" else "separate")
         torch.cuda.synchronize()
         e0 = torch.cuda.Event(enable_timing=True)
         e1 = torch.cuda.Event(enable_timing=True)
