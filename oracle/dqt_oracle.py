@@ -24,6 +24,7 @@ Paper map (section / equation of the DQT paper):
   * Sec. 3.2, Eq. 5 ........ direct update W^ = SR(W')            -> sr_update
   * Sec. 5.2 ............... fraction of weights changed per step -> n_changed
   * Sec. 4.1 (AdamW modified with SR; reading R11) ............... -> adamw_sr_update
+  * Sec. 5 (rounding without SR; forcing the smallest 20 %; R12) -> update_variant
 
 Readings of points the paper leaves open (each is listed in the design doc):
   R1  SR acts in grid units: with W~ = q * alpha (alpha = 1/s, Eq. 3) and
@@ -54,6 +55,15 @@ Readings of points the paper leaves open (each is listed in the design doc):
       m and v are fp32.  The element-wise arithmetic is fixed in fp32 (see
       ``adamw_sr_update``); a non-finite gradient entry, or a NaN step, leaves
       the weight, m and v unchanged and is counted.
+  R12 Analysis variants of Sec. 5 (with alpha fixed, R3): the deterministic
+      control rounds x = q + delta to the nearest grid value (ties to even)
+      instead of stochastically; "the smallest 20 % of the updates" of a step
+      are ranked per tensor by |delta| (fp32 bit patterns as unsigned
+      integers, non-finite gradients ranked last): with k = floor(frac n) and
+      tau the k-th smallest key, the bottom set is {key <= tau} (ties at tau
+      may enlarge it).  Force-to-remain keeps the bottom codes; force-to-
+      update rounds x away from q (ceil for delta > 0, floor for delta < 0),
+      then clips; every other element takes the plain SR update.
 """
 
 from __future__ import annotations
@@ -590,3 +600,70 @@ __all__ = [
     "philox4x32_10", "rng_u32", "sr_step_size", "sr_update",
     "sr_change_probability", "linear_train_step", "gemm_abs_bound",
 ]
+
+
+# ---------------------------------------------------------------------------
+# Next row: the analysis variants of Sec. 5 (reading R12).
+# ---------------------------------------------------------------------------
+
+UPD_SR, UPD_NEAREST, UPD_FORCE_REMAIN, UPD_FORCE_CHANGE = 0, 1, 2, 3
+
+
+def delta_keys(g, lr, alpha) -> np.ndarray:
+    """Ranking keys of R12: the fp32 bit pattern of |delta| = |fl32(c g)| as
+    an unsigned integer (monotone in |delta|), 0xFFFFFFFF for a non-finite g."""
+    g = np.asarray(g, dtype=np.float32).ravel()
+    c = sr_step_size(lr, alpha)
+    finite = np.isfinite(g)
+    with np.errstate(over="ignore", invalid="ignore"):
+        mag = np.abs((c * np.where(finite, g, np.float32(0))).astype(np.float32))
+    keys = mag.astype(np.float32).view(np.uint32).copy()
+    keys[~finite] = np.uint32(0xFFFFFFFF)
+    return keys
+
+
+def bottom_threshold(keys, frac):
+    """tau = the k-th smallest key, k = floor(frac n) (frac as fp32, the
+    product in float64); None when k = 0."""
+    n = keys.size
+    k = int(np.floor(np.float64(np.float32(frac)) * n))
+    if k <= 0:
+        return None
+    return np.uint32(np.sort(keys)[k - 1])
+
+
+def update_variant(q, g, lr, alpha, qmin: int, qmax: int, seed: int, step: int, tensor_id: int,
+                   mode: int, frac: float = 0.2):
+    """The update of Sec. 3.2 Eq. 5 with the interventions of Sec. 5 (R12):
+    UPD_SR is ``sr_update``; UPD_NEAREST rounds x = q + delta to the nearest
+    grid value, ties to even; UPD_FORCE_REMAIN / UPD_FORCE_CHANGE keep, or
+    round away from q, the codes whose |delta| is in the bottom set of
+    ``bottom_threshold`` and give the rest the plain SR update (same draws).
+    A non-finite g keeps its code and is counted.  Returns (q_new,
+    n_changed, n_nonfinite)."""
+    q = np.asarray(q).astype(np.int64).ravel()
+    g = np.asarray(g, dtype=np.float32).ravel()
+    sr_new, _, nnf = sr_update(q, g, lr, alpha, qmin, qmax, seed, step, tensor_id)
+    finite = np.isfinite(g)
+    c = sr_step_size(lr, alpha)
+    with np.errstate(over="ignore", invalid="ignore"):
+        delta = (-(c * np.where(finite, g, np.float32(0)))).astype(np.float32).astype(np.float64)
+    if mode == UPD_SR:
+        new = sr_new
+    elif mode == UPD_NEAREST:
+        x = q.astype(np.float64) + delta               # exact: delta is fp32, q small
+        new = np.where(finite, np.clip(np.rint(x), qmin, qmax), q).astype(np.int64)
+    elif mode in (UPD_FORCE_REMAIN, UPD_FORCE_CHANGE):
+        keys = delta_keys(g, lr, alpha)
+        tau = bottom_threshold(keys, frac)
+        bottom = np.zeros(q.size, bool) if tau is None else ((keys <= tau) & finite)
+        if mode == UPD_FORCE_REMAIN:
+            forced = q
+        else:
+            away = np.where(delta > 0, np.ceil(delta), np.where(delta < 0, np.floor(delta), 0.0))
+            with np.errstate(invalid="ignore"):
+                forced = np.clip(q.astype(np.float64) + away, qmin, qmax).astype(np.int64)
+        new = np.where(bottom, forced, sr_new).astype(np.int64)
+    else:
+        raise ValueError(mode)
+    return new, int(np.count_nonzero(new != q)), nnf

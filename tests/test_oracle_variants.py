@@ -1,0 +1,106 @@
+"""Pins of the oracle's analysis variants of the update (Sec. 5; reading R12
+of the oracle): rounding to nearest against numpy's rint, the bottom-20 %
+threshold against a plain sort, the two interventions on the paper's own
+example, and every other element equal to the plain SR update."""
+import numpy as np
+import pytest
+
+from oracle import dqt_oracle as O
+
+
+def _case(n, seed, qmin=-1, qmax=1, scale=0.02):
+    rng = np.random.default_rng(seed)
+    q = rng.integers(qmin, qmax + 1, size=n).astype(np.int64)
+    g = rng.normal(0, scale, size=n).astype(np.float32)
+    return q, g
+
+
+def test_nearest_is_rint_of_the_target():
+    q, g = _case(50000, 1, -8, 7, scale=1.0)
+    lr, alpha = 0.3, 0.25
+    new, nch, _ = O.update_variant(q, g, lr, alpha, -8, 7, 0, 1, 0, O.UPD_NEAREST)
+    c = np.float32(np.float32(lr) / np.float32(alpha))
+    x = q + (-(c * g)).astype(np.float32).astype(np.float64)
+    assert np.array_equal(new, np.clip(np.rint(x), -8, 7).astype(np.int64))
+    # small updates never move (the failure the paper reports for it)
+    small = np.abs((c * g).astype(np.float32)) < 0.5
+    assert np.all(new[small] == q[small])
+    # deterministic: the seed does not matter
+    new2, *_ = O.update_variant(q, g, lr, alpha, -8, 7, 12345, 99, 7, O.UPD_NEAREST)
+    assert np.array_equal(new, new2)
+
+
+def test_nearest_ties_go_to_even():
+    q = np.array([0, 0, 1, -1, 0, 0], np.int64)
+    g = np.array([-0.5, 0.5, -0.5, 0.5, -1.5, 1.5], np.float32)   # c = 1: delta = -g
+    new, *_ = O.update_variant(q, g, 1.0, 1.0, -8, 7, 0, 1, 0, O.UPD_NEAREST)
+    assert new.tolist() == [0, 0, 2, -2, 2, -2]
+
+
+@pytest.mark.parametrize("n,frac", [(97, 0.2), (1000, 0.2), (4096, 0.5), (10, 0.05), (33, 1.0)])
+def test_bottom_threshold_is_the_kth_smallest(n, frac):
+    q, g = _case(n, n)
+    keys = O.delta_keys(g, 1e-2, 0.01)
+    tau = O.bottom_threshold(keys, frac)
+    k = int(np.floor(np.float64(np.float32(frac)) * n))
+    if k == 0:
+        assert tau is None
+        return
+    assert tau == sorted(int(x) for x in keys)[k - 1]
+    # tie-free data: exactly k elements are in the bottom set
+    if len(set(keys.tolist())) == n:
+        assert int(np.count_nonzero(keys <= tau)) == k
+    # keys order as |delta| does
+    mag = np.abs((np.float32(1.0) * g).astype(np.float32))
+    order = np.argsort(mag, kind="stable")
+    assert np.all(np.diff(keys[order].astype(np.int64)) >= 0)
+
+
+def test_paper_example_remain_and_update():
+    """A code at -1 moved by +0.02 whose update is among the smallest 20 %:
+    force-to-remain keeps -1, force-to-update gives 0 (Sec. 5)."""
+    n = 100
+    q = np.full(n, -1, np.int64)
+    g = np.linspace(-0.9, -0.02, n).astype(np.float32)     # delta = +0.02 .. +0.9 (c = 1)
+    g[0] = np.float32(-0.02)
+    g[-1] = np.float32(-0.9)
+    rem, *_ = O.update_variant(q, g, 1.0, 1.0, -1, 1, 0, 1, 0, O.UPD_FORCE_REMAIN, 0.2)
+    chg, *_ = O.update_variant(q, g, 1.0, 1.0, -1, 1, 0, 1, 0, O.UPD_FORCE_CHANGE, 0.2)
+    i = int(np.argmin(np.abs(g)))
+    assert abs(float(g[i])) < 0.03
+    assert rem[i] == -1 and chg[i] == 0
+    keys = O.delta_keys(g, 1.0, 1.0)
+    bottom = keys <= O.bottom_threshold(keys, 0.2)
+    assert int(bottom.sum()) == 20
+    assert np.all(rem[bottom] == -1) and np.all(chg[bottom] == 0)
+
+
+@pytest.mark.parametrize("mode", [O.UPD_FORCE_REMAIN, O.UPD_FORCE_CHANGE])
+def test_outside_the_bottom_set_is_the_plain_update(mode):
+    q, g = _case(30000, 3, -127, 127, scale=0.05)
+    g[[5, 77]] = [np.inf, np.nan]
+    lr, alpha = 1e-2, 0.004
+    new, nch, nnf = O.update_variant(q, g, lr, alpha, -127, 127, 8, 2, 5, mode, 0.2)
+    sr, _, nnf2 = O.sr_update(q, g, lr, alpha, -127, 127, 8, 2, 5)
+    keys = O.delta_keys(g, lr, alpha)
+    bottom = (keys <= O.bottom_threshold(keys, 0.2)) & np.isfinite(g)
+    assert np.array_equal(new[~bottom], sr[~bottom])
+    assert nnf == nnf2 == 2 and new[5] == q[5] and new[77] == q[77]
+    c = O.sr_step_size(lr, alpha)
+    delta = (-(c * g)).astype(np.float32)
+    if mode == O.UPD_FORCE_REMAIN:
+        assert np.all(new[bottom] == q[bottom])
+    else:
+        d = delta[bottom]
+        moved = new[bottom] - q[bottom]
+        free = (d != 0) & ~(((q[bottom] == 127) & (d > 0)) | ((q[bottom] == -127) & (d < 0)))
+        assert np.all(np.sign(moved[free]) == np.sign(d[free]))
+        assert np.all(moved[free] != 0)
+    assert nch == int(np.count_nonzero(new != q))
+
+
+def test_frac_zero_is_the_plain_update():
+    q, g = _case(5000, 4)
+    a, *_ = O.update_variant(q, g, 1e-2, 0.01, -1, 1, 3, 3, 3, O.UPD_FORCE_CHANGE, 0.0)
+    b, *_ = O.sr_update(q, g, 1e-2, 0.01, -1, 1, 3, 3, 3)
+    assert np.array_equal(a, b)
