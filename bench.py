@@ -152,7 +152,7 @@ def algorithmic_units(wl):
     xb = 2 if wl.x_dtype == "bf16" else 4
     act_bytes = sum(M * wl.input_width(n) * (xb + 1) + 4 * M for n in wl.inputs)
     return {"fwd": f, "bwd": 2 * f, "bwd_sr": 2 * f, "bwd_dx": f, "bwd_dw": f, "sr": sr_bytes,
-            "act_quant": act_bytes, "adamw_sr": adam_bytes}
+            "act_quant": act_bytes, "adamw_sr": adam_bytes, "upd_force": sr_bytes}
 
 
 def cpu_baseline(wl, tokens: int, min_seconds: float = 10.0):
@@ -294,7 +294,8 @@ def main():
     # step's own calls first; then dX and dW each in a call of its own.
     step_kinds = ["act_quant", "fwd"] + (["bwd_sr"] if args.sr == "fused" else ["bwd", "sr"])
     kinds = step_kinds + (["bwd", "sr"] if args.sr == "fused" else []) + ["bwd_dx", "bwd_dw",
-                                                                         "adamw_sr"]
+                                                                         "adamw_sr", "upd_force"]
+    var_ws = dqt.workspace(dqt.dqt_update_variant_workspace(len(wl.linears)))
     adam_hp = dqt.adamw(wl.lr, 0.9, 0.95, 1e-8, 0.1)
     per_kind_ms, per_kind_units, per_kind_n = {}, {}, {}
     for kind in kinds:
@@ -307,7 +308,12 @@ def main():
 
         g = torch.cuda.CUDAGraph()
         with torch.cuda.graph(g):
-            if kind == "adamw_sr":
+            if kind == "upd_force":
+                # force-to-update of the smallest 20 % (exact selection, then the update)
+                calls.append(kind)
+                dqt.dqt_update_variant_batch(blk.io_all, wl.lr, wl.seed, 1, dqt.DQT_UPD_FORCE_CHANGE,
+                                             0.2, blk.counters, var_ws)
+            elif kind == "adamw_sr":
                 # the AdamW variant of the update (not part of the step)
                 calls.append(kind)
                 dqt.dqt_adamw_sr_update_batch(blk.io_all, blk.m, blk.v, adam_hp, wl.seed, 1,

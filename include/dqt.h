@@ -262,6 +262,41 @@ dqt_status dqt_sr_update_batch(int32_t n, const dqt_linear_io* io, float lr,
                                unsigned long long* counters, void* stream);
 
 /*
+ * Analysis variants of the direct update (Sec. 5).  The paper contrasts SR
+ * with a deterministic rounding that drops small updates, and intervenes in
+ * the smallest 20 % of each step's updates, keeping those codes or forcing
+ * them to change.  With delta = -fl(fl(lr / alpha) * dW) as in
+ * dqt_sr_update and x = q + delta:
+ *   DQT_UPD_SR            the plain update (dqt_sr_update_batch);
+ *   DQT_UPD_NEAREST       x rounded to the nearest grid value, ties to even;
+ *   DQT_UPD_FORCE_REMAIN  codes in the bottom set keep their value,
+ *   DQT_UPD_FORCE_CHANGE  codes in the bottom set take x rounded away from q
+ *                         (ceil for delta > 0, floor for delta < 0);
+ *   every other code (and every code under DQT_UPD_SR) takes the plain
+ *   update with its draws, then all are clipped to [qmin, qmax].
+ * The bottom set of a tensor is {key <= tau}: key is the fp32 bit pattern of
+ * |fl(fl(lr / alpha) * dW)| as an unsigned integer (0xFFFFFFFF for a
+ * non-finite dW), tau the k-th smallest key, k = floor(frac * n) in double
+ * (n = d_out * d_in < 2^32; ties at tau may enlarge the set; k = 0 leaves it
+ * empty).  A non-finite dW keeps its code and is counted in counters[1].
+ *   frac: in [0, 1] (used by the two force modes).
+ *   ws, ws_bytes: dqt_update_variant_workspace(n) bytes for the force modes
+ *   (the exact selection's state); NULL / 0 allowed for the other modes.
+ * Uses w, Wq (updated in place) and dW of each entry of io.
+ */
+#define DQT_UPD_SR 0
+#define DQT_UPD_NEAREST 1
+#define DQT_UPD_FORCE_REMAIN 2
+#define DQT_UPD_FORCE_CHANGE 3
+
+size_t dqt_update_variant_workspace(int32_t n);
+
+dqt_status dqt_update_variant_batch(int32_t n, const dqt_linear_io* io, float lr,
+                                    uint64_t seed, uint32_t step, int32_t mode,
+                                    float frac, unsigned long long* counters,
+                                    void* ws, size_t ws_bytes, void* stream);
+
+/*
  * AdamW with direct stochastic rounding.  The paper trains DQT with AdamW
  * modified to round stochastically (Sec. 4.1): the optimiser's target W'
  * (Sec. 3.2) is the AdamW step with decoupled weight decay and bias

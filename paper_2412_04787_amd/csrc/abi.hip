@@ -328,6 +328,47 @@ dqt_status dqt_linear_bwd_sr_batch(int32_t n, const dqt_linear_io* io, int64_t M
   return from_hip(dqt::launch_bwd_sr_batch(c, L, t, seed, step, counters, nx == n, wsb, P, s));
 }
 
+size_t dqt_update_variant_workspace(int32_t n) {
+  if (n < 0 || n > DQT_MAX_BATCH) return 0;
+  return dqt::update_variant_workspace(n);
+}
+
+dqt_status dqt_update_variant_batch(int32_t n, const dqt_linear_io* io, float lr, uint64_t seed,
+                                    uint32_t step, int32_t mode, float frac,
+                                    unsigned long long* counters, void* ws, size_t ws_bytes,
+                                    void* stream) {
+  dqt::LinearIO L[DQT_MAX_BATCH];
+  int32_t wfmt;
+  dqt_status st = check_batch(n, io, L, &wfmt);
+  if (st != DQT_OK) return st;
+  if (mode < DQT_UPD_SR || mode > DQT_UPD_FORCE_CHANGE) return DQT_ERR_RANGE;
+  if (counters != nullptr && (reinterpret_cast<uintptr_t>(counters) & 7u) != 0) return DQT_ERR_ALIGN;
+  if (!(isfinite(lr) && lr >= 0.0f)) return DQT_ERR_RANGE;
+  const bool force = mode == DQT_UPD_FORCE_REMAIN || mode == DQT_UPD_FORCE_CHANGE;
+  if (force && !(frac >= 0.0f && frac <= 1.0f)) return DQT_ERR_RANGE;
+  dqt::SRTensor t[DQT_MAX_BATCH];
+  for (int l = 0; l < n; ++l) {
+    if (io[l].Wq == nullptr || io[l].dW == nullptr) return DQT_ERR_NULL;
+    if (!aligned16(io[l].Wq) || !aligned16(io[l].dW)) return DQT_ERR_ALIGN;
+    const float c = lr / io[l].w->alpha;
+    if (!isfinite(c)) return DQT_ERR_RANGE;
+    t[l].wq = static_cast<uint8_t*>(io[l].Wq);
+    t[l].grad = io[l].dW;
+    t[l].nweights = (int64_t)io[l].w->d_out * (int64_t)io[l].w->d_in;
+    if (force && t[l].nweights >= (int64_t(1) << 32)) return DQT_ERR_SHAPE;
+    t[l].c = c;
+    t[l].qmin = io[l].w->qmin;
+    t[l].qmax = io[l].w->qmax;
+    t[l].tensor_id = io[l].w->tensor_id;
+  }
+  if (force) {
+    if (ws == nullptr || ws_bytes < dqt::update_variant_workspace(n)) return DQT_ERR_WORKSPACE;
+    if (!aligned16(ws)) return DQT_ERR_ALIGN;
+  }
+  return from_hip(dqt::launch_update_variant(wfmt == DQT_TERNARY2, n, t, mode, frac, seed, step,
+                                             counters, ws, static_cast<hipStream_t>(stream)));
+}
+
 dqt_status dqt_adamw_sr_update_batch(int32_t n, const dqt_linear_io* io, float* const* m,
                                      float* const* v, const dqt_adamw* hp, uint64_t seed,
                                      uint32_t step, unsigned long long* counters, void* stream) {

@@ -104,6 +104,12 @@ struct SRTensor {
 };
 hipError_t launch_sr_update(bool ternary, int n, const SRTensor* t, uint64_t seed, uint32_t step,
                             unsigned long long* counters, hipStream_t stream);
+// Analysis variants of the update (mode 0 plain SR, 1 nearest, 2 force to
+// remain, 3 force to update the bottom `frac` of |delta|).
+size_t update_variant_workspace(int n);
+hipError_t launch_update_variant(bool ternary, int n, const SRTensor* t, int mode, float frac,
+                                 uint64_t seed, uint32_t step, unsigned long long* counters,
+                                 void* ws, hipStream_t stream);
 // AdamW with SR (up to kMaxBatch tensors of one code format per launch).
 struct AdamTensor {
   uint8_t* wq;          // codes, updated in place

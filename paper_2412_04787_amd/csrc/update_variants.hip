@@ -1,0 +1,304 @@
+// Analysis variants of the direct update (Sec. 5): rounding q + delta to
+// the nearest grid value instead of stochastically (the control that drops
+// small updates), and the two interventions on the smallest fraction of a
+// step's updates: keep those codes (force to remain), or round them away
+// from q (force to update); every other element takes the plain SR update
+// of Sec. 3.2 Eq. 5 with the same draws.
+//
+// The bottom set of a tensor is {key <= tau}: key is the fp32 bit pattern of
+// |delta| = |fl(c g)| read as an unsigned integer (monotone in |delta|;
+// 0xFFFFFFFF for a non-finite g) and tau the k-th smallest key, k =
+// floor(frac n).  tau is found exactly on the device by a radix select over
+// the keys: three passes of 11, 11 and 10 bits, each a histogram of the keys
+// that match the bits chosen so far, then a scan that picks the bin holding
+// the k-th key.  Each pass reads the gradient once (4 B per weight).
+#include <math.h>
+
+#include "sr_rule.h"
+
+namespace dqt {
+
+namespace {
+
+constexpr int kMaxV = kMaxBatch;
+constexpr int kHistBins = 2048;
+constexpr int kChunksPerThread = 4;               // 8 weights per chunk
+constexpr int kElemsPerBlock = 256 * 8 * kChunksPerThread;
+
+// Radix-select state of one tensor (in the caller's workspace).
+struct SelState {
+  uint32_t prefix, mask, krem, pad;
+  uint32_t hist[kHistBins];
+};
+
+struct VarTab {
+  uint8_t* wq[kMaxV];
+  const float* grad[kMaxV];
+  int64_t nweights[kMaxV];
+  int64_t b0[kMaxV + 1];         // blocks of kElemsPerBlock weights (selection passes)
+  int64_t t0[kMaxV + 1];         // tiles of 256 chunks (update)
+  float c[kMaxV], L[kMaxV];
+  int qmin[kMaxV], qmax[kMaxV];
+  uint32_t tid[kMaxV];
+  uint32_t k[kMaxV];             // bottom-set size; 0: empty
+  int32_t n, mode;
+  uint32_t k0, k1, step;
+};
+
+__device__ __forceinline__ uint32_t delta_key(float g, float c) {
+  return __builtin_isfinite(g) ? (__float_as_uint(c * g) & 0x7FFFFFFFu) : 0xFFFFFFFFu;
+}
+
+template <int N>
+__device__ __forceinline__ int seg_of(const int64_t (&b)[N], int n, int64_t x) {
+  int s = 0;
+  while (s + 1 < n && x >= b[s + 1]) ++s;
+  return s;
+}
+
+__global__ __launch_bounds__(256) void sel_init_kernel(const VarTab tab, SelState* __restrict__ st) {
+  SelState& S = st[blockIdx.x];
+  if (threadIdx.x == 0) {
+    S.prefix = 0;
+    S.mask = 0;
+    S.krem = tab.k[blockIdx.x];
+    S.pad = 0;
+  }
+  for (int i = threadIdx.x; i < kHistBins; i += 256) S.hist[i] = 0;
+}
+
+// Histogram of bits [shift, shift + nbits) of the keys that match the bits
+// chosen so far.  One block per kElemsPerBlock weights of one tensor.
+__global__ __launch_bounds__(256) void sel_hist_kernel(const VarTab tab, SelState* __restrict__ st,
+                                                       int shift, int nbins) {
+  __shared__ uint32_t h[kHistBins];
+  const int s = seg_of(tab.b0, tab.n, (int64_t)blockIdx.x);
+  for (int i = threadIdx.x; i < nbins; i += 256) h[i] = 0;
+  __syncthreads();
+  const SelState& S = st[s];
+  const uint32_t prefix = S.prefix, mask = S.mask;
+  if (tab.k[s] != 0) {
+    const int64_t base = (int64_t)(blockIdx.x - tab.b0[s]) * kElemsPerBlock;
+    const float c = tab.c[s];
+    const f32x4* g4 = reinterpret_cast<const f32x4*>(tab.grad[s]);
+#pragma unroll
+    for (int u = 0; u < kChunksPerThread; ++u) {
+      const int64_t e0 = base + ((int64_t)u * 256 + threadIdx.x) * 8;
+      if (e0 >= tab.nweights[s]) break;
+      const f32x4 a = g4[e0 / 4], b = g4[e0 / 4 + 1];
+      const float g[8] = {a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const uint32_t key = delta_key(g[j], c);
+        if ((key & mask) == prefix) atomicAdd(&h[(key >> shift) & (uint32_t)(nbins - 1)], 1u);
+      }
+    }
+  }
+  __syncthreads();
+  if (tab.k[s] != 0)
+    for (int i = threadIdx.x; i < nbins; i += 256)
+      if (h[i]) atomicAdd(&st[s].hist[i], h[i]);
+}
+
+// The bin holding the krem-th matching key: its bits join the prefix, krem
+// drops by the keys of the bins below it; the histogram is cleared.
+__global__ __launch_bounds__(256) void sel_pick_kernel(const VarTab tab, SelState* __restrict__ st,
+                                                       int shift, int nbins) {
+  __shared__ uint32_t part[256];
+  __shared__ uint32_t pick_bin, pick_below;
+  SelState& S = st[blockIdx.x];
+  if (tab.k[blockIdx.x] == 0) return;
+  const int per = nbins / 256;                   // 8 or 4 bins per thread
+  uint32_t sum = 0;
+  for (int i = 0; i < per; ++i) sum += S.hist[threadIdx.x * per + i];
+  part[threadIdx.x] = sum;
+  if (threadIdx.x == 0) {
+    pick_bin = (uint32_t)(nbins - 1);
+    pick_below = 0;
+  }
+  __syncthreads();
+  // exclusive prefix of the per-thread sums (Hillis-Steele in LDS)
+  for (int off = 1; off < 256; off <<= 1) {
+    const uint32_t v = threadIdx.x >= (unsigned)off ? part[threadIdx.x - off] : 0u;
+    __syncthreads();
+    part[threadIdx.x] += v;
+    __syncthreads();
+  }
+  const uint32_t krem = S.krem;
+  const uint32_t incl = part[threadIdx.x], excl = incl - sum;
+  if (excl < krem && krem <= incl) {             // exactly one thread
+    uint32_t cum = excl;
+    for (int i = 0; i < per; ++i) {
+      const uint32_t c = S.hist[threadIdx.x * per + i];
+      if (cum + c >= krem) {
+        pick_bin = (uint32_t)(threadIdx.x * per + i);
+        pick_below = cum;
+        break;
+      }
+      cum += c;
+    }
+  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < nbins; i += 256) S.hist[i] = 0;
+  if (threadIdx.x == 0) {
+    S.prefix |= pick_bin << shift;
+    S.mask |= (uint32_t)(nbins - 1) << shift;
+    S.krem = krem - pick_below;
+  }
+}
+
+// x = q + delta rounded to the nearest grid value, ties to even.
+__device__ __forceinline__ int nearest_code(int q, float g, float c, float L, int qmin, int qmax) {
+  const float delta = fminf(fmaxf(-(c * g), -L), L);
+  const float n = truncf(delta);
+  const float r = delta - n;                     // exact, |r| < 1
+  int v = q + (int)n;
+  const float ar = fabsf(r);
+  const int sgn = r > 0.0f ? 1 : -1;
+  if (ar > 0.5f || (ar == 0.5f && ((v + sgn) & 1) == 0)) v += sgn;
+  return min(max(v, qmin), qmax);
+}
+
+// x = q + delta rounded away from q (ceil for delta > 0, floor for < 0).
+__device__ __forceinline__ int away_code(int q, float g, float c, float L, int qmin, int qmax) {
+  const float delta = fminf(fmaxf(-(c * g), -L), L);
+  const float a = delta > 0.0f ? ceilf(delta) : floorf(delta);
+  return min(max(q + (int)a, qmin), qmax);
+}
+
+// The update: the plain SR chunk, then the variant's elements replaced.
+template <bool TERN>
+__global__ __launch_bounds__(256) void variant_update_kernel(const VarTab tab, const SelState* __restrict__ st,
+                                                             unsigned long long* __restrict__ counters) {
+  __shared__ unsigned long long red[2][256 / kWave];
+  unsigned long long changed = 0, nonfin = 0;
+  const int64_t ntiles = tab.t0[tab.n];
+  for (int64_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
+    const int s = seg_of(tab.t0, tab.n, tile);
+    const int64_t t = (tile - tab.t0[s]) * 256 + threadIdx.x;
+    if (t >= tab.nweights[s] / 8) continue;
+    const f32x4* gp = reinterpret_cast<const f32x4*>(tab.grad[s]) + 2 * t;
+    const f32x4 gv[2] = {__builtin_nontemporal_load(gp), __builtin_nontemporal_load(gp + 1)};
+    uint32_t win[4] = {0u, 0u, 0u, 0u};
+    if constexpr (TERN) {
+      win[0] = reinterpret_cast<const uint16_t*>(tab.wq[s])[t];
+    } else {
+      const uint2 w = reinterpret_cast<const uint2*>(tab.wq[s])[t];
+      win[0] = w.x;
+      win[1] = w.y;
+    }
+    SRArgs a;
+    a.c = tab.c[s];
+    a.L = tab.L[s];
+    a.qmin = tab.qmin[s];
+    a.qmax = tab.qmax[s];
+    a.k0 = tab.k0;
+    a.k1 = tab.k1;
+    a.step = tab.step;
+    a.tid = tab.tid[s];
+    uint32_t wout[4];
+    unsigned long long ch_sr = 0;
+    sr_chunk<TERN, 8>(win, gv, (uint64_t)t, a, wout, ch_sr, nonfin);
+    const bool sel = tab.mode >= 2 && tab.k[s] != 0;
+    const uint32_t tau = sel ? st[s].prefix : 0u;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const float g = gv[j >> 2][j & 3];
+      if (!__builtin_isfinite(g)) continue;      // kept by the SR chunk
+      const int q = TERN ? (int)((win[0] >> (2 * j)) & 3u) - 1 : (int)(int8_t)(win[j >> 2] >> (8 * (j & 3)));
+      int v;
+      if (tab.mode == 1) v = nearest_code(q, g, a.c, a.L, a.qmin, a.qmax);
+      else if (sel && delta_key(g, a.c) <= tau) v = tab.mode == 2 ? q : away_code(q, g, a.c, a.L, a.qmin, a.qmax);
+      else continue;
+      if constexpr (TERN) wout[0] = (wout[0] & ~(3u << (2 * j))) | ((uint32_t)(v + 1) << (2 * j));
+      else wout[j >> 2] = (wout[j >> 2] & ~(0xFFu << (8 * (j & 3)))) | (((uint32_t)v & 0xFFu) << (8 * (j & 3)));
+    }
+    if constexpr (TERN) {
+      const uint32_t x = wout[0] ^ win[0];
+      changed += __builtin_popcount((x | (x >> 1)) & 0x55555555u);
+      reinterpret_cast<uint16_t*>(tab.wq[s])[t] = (uint16_t)wout[0];
+    } else {
+#pragma unroll
+      for (int w = 0; w < 2; ++w) {
+        const uint32_t x = wout[w] ^ win[w];
+        changed += __builtin_popcount((((x & 0x7F7F7F7Fu) + 0x7F7F7F7Fu) | x) & 0x80808080u);
+      }
+      reinterpret_cast<uint2*>(tab.wq[s])[t] = make_uint2(wout[0], wout[1]);
+    }
+  }
+  if (counters != nullptr) {
+    changed = wave_sum_u64(changed);
+    nonfin = wave_sum_u64(nonfin);
+    const int w = threadIdx.x / kWave;
+    if ((threadIdx.x & (kWave - 1)) == 0) {
+      red[0][w] = changed;
+      red[1][w] = nonfin;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      unsigned long long c = 0, f = 0;
+#pragma unroll
+      for (int i = 0; i < 256 / kWave; ++i) {
+        c += red[0][i];
+        f += red[1][i];
+      }
+      if (c) atomicAdd(counters + 0, c);
+      if (f) atomicAdd(counters + 1, f);
+    }
+  }
+}
+
+}  // namespace
+
+size_t update_variant_workspace(int n) { return (size_t)n * sizeof(SelState); }
+
+hipError_t launch_update_variant(bool ternary, int n, const SRTensor* t, int mode, float frac,
+                                 uint64_t seed, uint32_t step, unsigned long long* counters,
+                                 void* ws, hipStream_t stream) {
+  VarTab tab{};
+  tab.n = n;
+  tab.mode = mode;
+  tab.k0 = (uint32_t)seed;
+  tab.k1 = (uint32_t)(seed >> 32);
+  tab.step = step;
+  int64_t blocks = 0, tiles = 0;
+  bool any_sel = false;
+  for (int s = 0; s < n; ++s) {
+    tab.wq[s] = t[s].wq;
+    tab.grad[s] = t[s].grad;
+    tab.nweights[s] = t[s].nweights;
+    tab.c[s] = t[s].c;
+    tab.L[s] = (float)(t[s].qmax - t[s].qmin + 1);
+    tab.qmin[s] = t[s].qmin;
+    tab.qmax[s] = t[s].qmax;
+    tab.tid[s] = t[s].tensor_id;
+    const double kk = mode >= 2 ? floor((double)frac * (double)t[s].nweights) : 0.0;
+    tab.k[s] = (uint32_t)kk;
+    any_sel |= tab.k[s] != 0;
+    tab.b0[s] = blocks;
+    blocks += (t[s].nweights + kElemsPerBlock - 1) / kElemsPerBlock;
+    tab.t0[s] = tiles;
+    tiles += (t[s].nweights / 8 + 255) / 256;
+  }
+  tab.b0[n] = blocks;
+  tab.t0[n] = tiles;
+  if (tiles == 0) return hipSuccess;
+  SelState* st = static_cast<SelState*>(ws);
+  if (any_sel) {
+    hipLaunchKernelGGL(sel_init_kernel, dim3((unsigned)n), dim3(256), 0, stream, tab, st);
+    const int shifts[3] = {21, 10, 0}, bins[3] = {2048, 2048, 1024};
+    for (int p = 0; p < 3; ++p) {
+      hipLaunchKernelGGL(sel_hist_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, tab, st, shifts[p],
+                         bins[p]);
+      hipLaunchKernelGGL(sel_pick_kernel, dim3((unsigned)n), dim3(256), 0, stream, tab, st, shifts[p], bins[p]);
+    }
+  }
+  const unsigned grid = (unsigned)(tiles < 4096 ? tiles : 4096);
+  if (ternary)
+    hipLaunchKernelGGL(variant_update_kernel<true>, dim3(grid), dim3(256), 0, stream, tab, st, counters);
+  else
+    hipLaunchKernelGGL(variant_update_kernel<false>, dim3(grid), dim3(256), 0, stream, tab, st, counters);
+  return hipGetLastError();
+}
+
+}  // namespace dqt

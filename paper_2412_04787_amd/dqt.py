@@ -25,6 +25,7 @@ EXPORTS = (
     "dqt_linear_bwd", "dqt_linear_fwd_batch_workspace", "dqt_linear_fwd_batch",
     "dqt_linear_bwd_batch_workspace", "dqt_linear_bwd_batch", "dqt_linear_bwd_sr_batch",
     "dqt_sr_update_batch", "dqt_adamw_sr_update", "dqt_adamw_sr_update_batch",
+    "dqt_update_variant_workspace", "dqt_update_variant_batch",
     "dqt_sr_update", "dqt_debug_rng", "dqt_absmean_init", "dqt_pack_ternary",
     "dqt_unpack_ternary", "dqt_status_string", "dqt_version",
 )
@@ -89,6 +90,9 @@ _SIGS = {
     "dqt_linear_bwd_sr_batch": (_i32, [_i32, _vp, _i64, _i32, _i32, _i32, _i32, _f32, _u64, _u32,
                                        _vp, _vp, ctypes.c_size_t, _vp]),
     "dqt_sr_update_batch": (_i32, [_i32, _vp, _f32, _u64, _u32, _vp, _vp]),
+    "dqt_update_variant_workspace": (ctypes.c_size_t, [_i32]),
+    "dqt_update_variant_batch": (_i32, [_i32, _vp, _f32, _u64, _u32, _i32, _f32, _vp, _vp,
+                                        ctypes.c_size_t, _vp]),
     "dqt_adamw_sr_update": (_i32, [_wp, _vp, _vp, _vp, _vp, _vp, _u64, _u32, _vp, _vp]),
     "dqt_adamw_sr_update_batch": (_i32, [_i32, _vp, _vp, _vp, _vp, _u64, _u32, _vp, _vp]),
     "dqt_debug_rng": (_i32, [_u64, _u32, _u32, _u64, _i64, _vp, _vp]),
@@ -216,7 +220,8 @@ def dqt_debug_rng(seed: int, step: int, tensor_id: int, i0: int, out, stream=Non
 def linear_io(entries):
     """entries: list of dicts with keys w (DqtWeight), Wq, Xq, xdq, Y, dY, dX, dW
     (tensors or None).  Returns a ctypes array of dqt_linear_io; the weight
-    descriptors are kept alive on the array."""
+    descriptors and the tensors are kept alive on the array (it holds raw
+    device pointers)."""
     arr = (DqtLinearIO * len(entries))()
     keep = []
     for k, e in enumerate(entries):
@@ -226,6 +231,8 @@ def linear_io(entries):
         for f in ("Wq", "Xq", "xdq", "Y", "dY", "dX", "dW"):
             t = e.get(f)
             setattr(arr[k], f, None if t is None else t.data_ptr())
+            if t is not None:
+                keep.append(t)
     arr._keep = keep
     return arr
 
@@ -276,6 +283,21 @@ def dqt_linear_bwd_sr_batch(io, M: int, act_q: int, dy_t: int, xt_t: int, dx_t: 
     _check("dqt_linear_bwd_sr_batch",
            load().dqt_linear_bwd_sr_batch(len(io), io, M, act_q, dy_t, xt_t, dx_t, lr, seed, step,
                                           _ptr(counters), _ptr(ws), ws_bytes, _stream(stream)))
+
+
+DQT_UPD_SR, DQT_UPD_NEAREST, DQT_UPD_FORCE_REMAIN, DQT_UPD_FORCE_CHANGE = 0, 1, 2, 3
+
+
+def dqt_update_variant_workspace(n: int) -> int:
+    return int(load().dqt_update_variant_workspace(n))
+
+
+def dqt_update_variant_batch(io, lr: float, seed: int, step: int, mode: int, frac: float = 0.2,
+                             counters=None, ws=None, stream=None):
+    ws_bytes = 0 if ws is None else ws.numel() * ws.element_size()
+    _check("dqt_update_variant_batch",
+           load().dqt_update_variant_batch(len(io), io, lr, seed, step, mode, frac, _ptr(counters),
+                                           _ptr(ws), ws_bytes, _stream(stream)))
 
 
 class DqtAdamW(ctypes.Structure):
