@@ -65,7 +65,8 @@ typedef enum {
   DQT_BF16 = 1,       /* bfloat16                                             */
   DQT_I8 = 2,         /* int8                                                 */
   DQT_FP8E4M3 = 3,    /* OCP E4M3 ("fn": bias 7, max 448, no inf)             */
-  DQT_TERNARY2 = 4    /* packed 2-bit ternary weight codes, see dqt_weight    */
+  DQT_TERNARY2 = 4,   /* packed 2-bit ternary weight codes, see dqt_weight    */
+  DQT_INT4 = 5        /* packed 4-bit weight codes, see dqt_weight            */
 } dqt_dtype;
 
 /*
@@ -77,6 +78,12 @@ typedef enum {
  *   wfmt = DQT_I8: one int8 code per weight, [d_out, d_in] row-major.
  *          Requires -128 <= qmin < qmax <= 127 (Eq. 3 gives -2^(n-1) ..
  *          2^(n-1) - 1; a symmetric -127..127 grid is also allowed).
+ *   wfmt = DQT_INT4: the n-bit grids of Eq. 3 for n <= 4 (n = 2, 3, 4:
+ *          -2..1, -4..3, -8..7) in 4-bit two's-complement nibbles: weight
+ *          (n, k) at byte n * (d_in / 2) + k / 2, low nibble for even k.
+ *          Requires -8 <= qmin < qmax <= 7.  The forward and dX expand the
+ *          nibbles to int8 / bf16 in the workspace; the updates work on the
+ *          nibbles in place.
  *   alpha: dequantisation scale, the weight's real value is q * alpha
  *          (alpha = 1/s, Eq. 3).  Finite and > 0.  Fixed for the life of the
  *          tensor: the library never recomputes it (Sec. 3.2 skips Eq. 2-4
@@ -87,7 +94,7 @@ typedef enum {
 typedef struct {
   int32_t d_out;
   int32_t d_in;
-  int32_t wfmt;       /* dqt_dtype: DQT_TERNARY2 or DQT_I8 */
+  int32_t wfmt;       /* dqt_dtype: DQT_TERNARY2, DQT_INT4 or DQT_I8 */
   int32_t qmin;
   int32_t qmax;
   float alpha;
@@ -390,6 +397,12 @@ dqt_status dqt_pack_ternary(const int8_t* q, int64_t rows, int64_t cols,
                             uint8_t* packed);
 dqt_status dqt_unpack_ternary(const uint8_t* packed, int64_t rows,
                               int64_t cols, int8_t* q);
+
+/* Host packing of codes in [-8, 7] into the DQT_INT4 layout and back.
+ * q: host int8 [rows, cols]; packed: host uint8 [rows, cols/2]; cols must be
+ * even.  pack returns DQT_ERR_RANGE (and stops) on a value outside [-8, 7]. */
+dqt_status dqt_pack_int4(const int8_t* q, int64_t rows, int64_t cols, uint8_t* packed);
+dqt_status dqt_unpack_int4(const uint8_t* packed, int64_t rows, int64_t cols, int8_t* q);
 
 /* Human-readable name of a status code (static storage). */
 const char* dqt_status_string(int32_t status);

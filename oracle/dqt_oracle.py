@@ -195,6 +195,25 @@ def unpack_ternary(packed: np.ndarray, d_in: int) -> np.ndarray:
 # ---------------------------------------------------------------------------
 
 
+def pack_int4(q: np.ndarray) -> np.ndarray:
+    """Codes in [-8, 7] [rows, cols] -> 4-bit two's-complement nibbles, two
+    per byte (weight k in the low nibble of byte k // 2 when k is even)."""
+    q = np.asarray(q).astype(np.int64)
+    assert q.ndim == 2 and q.shape[1] % 2 == 0 and q.min() >= -8 and q.max() <= 7
+    nib = (q & 0xF).astype(np.uint8)
+    return (nib[:, 0::2] | (nib[:, 1::2] << 4)).astype(np.uint8)
+
+
+def unpack_int4(packed: np.ndarray, d_in: int) -> np.ndarray:
+    p = np.asarray(packed, dtype=np.uint8)
+    lo = (p & 0xF).astype(np.int64)
+    hi = (p >> 4).astype(np.int64)
+    out = np.empty((p.shape[0], d_in), dtype=np.int64)
+    out[:, 0::2] = np.where(lo >= 8, lo - 16, lo)
+    out[:, 1::2] = np.where(hi >= 8, hi - 16, hi)
+    return out.astype(np.int8)
+
+
 def absmean(W) -> float:
     """Eq. 2: the mean absolute value over every element of the tensor (fp64)."""
     W = np.asarray(W, dtype=np.float64)

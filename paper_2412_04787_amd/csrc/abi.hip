@@ -25,12 +25,17 @@ dqt_status check_weight(const dqt_weight* w) {
     if (w->qmin != -1 || w->qmax != 1) return DQT_ERR_RANGE;
   } else if (w->wfmt == DQT_I8) {
     if (w->qmin < -128 || w->qmax > 127 || w->qmin >= w->qmax) return DQT_ERR_RANGE;
+  } else if (w->wfmt == DQT_INT4) {
+    if (w->qmin < -8 || w->qmax > 7 || w->qmin >= w->qmax) return DQT_ERR_RANGE;
   } else {
     return DQT_ERR_DTYPE;
   }
   if (!(isfinite(w->alpha) && w->alpha > 0.0f)) return DQT_ERR_RANGE;
   return DQT_OK;
 }
+
+// code format of the update kernels: 0 int8, 1 ternary 2-bit, 2 int4 nibbles
+int code_format(int32_t wfmt) { return wfmt == DQT_TERNARY2 ? 1 : wfmt == DQT_INT4 ? 2 : 0; }
 
 bool is_float_type(int32_t t) { return t == DQT_F32 || t == DQT_BF16; }
 
@@ -120,7 +125,7 @@ size_t dqt_linear_fwd_batch_workspace(int32_t n, const dqt_linear_io* io) {
   dqt::LinearIO L[DQT_MAX_BATCH];
   int32_t wfmt;
   if (check_batch(n, io, L, &wfmt) != DQT_OK) return 0;
-  return dqt::fwd_batch_workspace(n, L, wfmt == DQT_TERNARY2, nullptr);
+  return dqt::fwd_batch_workspace(n, L, code_format(wfmt), nullptr);
 }
 
 dqt_status dqt_linear_fwd_batch(int32_t n, const dqt_linear_io* io, int64_t M, int32_t act_q,
@@ -140,10 +145,11 @@ dqt_status dqt_linear_fwd_batch(int32_t n, const dqt_linear_io* io, int64_t M, i
     if (!aligned16(io[l].Wq) || !aligned16(io[l].Xq) || !aligned16(io[l].xdq) || !aligned16(io[l].Y))
       return DQT_ERR_ALIGN;
   }
-  const size_t need = dqt::fwd_batch_workspace(n, L, wfmt == DQT_TERNARY2, nullptr);
+  const size_t need = dqt::fwd_batch_workspace(n, L, code_format(wfmt), nullptr);
   if (need > 0 && (ws == nullptr || ws_bytes < need)) return DQT_ERR_WORKSPACE;
   if (need > 0 && !aligned16(ws)) return DQT_ERR_ALIGN;
   dqt::BatchCfg c{n, M, wfmt == DQT_TERNARY2, act_q == DQT_FP8E4M3, y_t == DQT_BF16};
+  c.w_int4 = wfmt == DQT_INT4;
   return from_hip(dqt::launch_fwd_batch(c, L, static_cast<uint8_t*>(ws), static_cast<hipStream_t>(stream)));
 }
 
@@ -199,6 +205,7 @@ dqt_status dqt_linear_bwd_batch(int32_t n, const dqt_linear_io* io, int64_t M, i
   for (int l = 0; l < n; ++l) both &= io[l].dX != nullptr && io[l].dW != nullptr;
   if (both) {
     dqt::BatchCfg c{n, M, wfmt == DQT_TERNARY2, act_q == DQT_FP8E4M3, dx_t == DQT_BF16};
+    c.w_int4 = wfmt == DQT_INT4;
     return from_hip(dqt::launch_dxdw_batch(c, L, wsb, P, s));
   }
   // dX for the linears that want it
@@ -212,12 +219,20 @@ dqt_status dqt_linear_bwd_batch(int32_t n, const dqt_linear_io* io, int64_t M, i
   if (nx > 0 && M > 0) {
     if (dy_t == DQT_BF16) {
       dqt::BatchCfg c{nx, M, wfmt == DQT_TERNARY2, act_q == DQT_FP8E4M3, dx_t == DQT_BF16};
+      c.w_int4 = wfmt == DQT_INT4;
       st = from_hip(dqt::launch_dx_batch(c, sub, wsb, Px, s));
     } else {
       for (int l = 0; l < nx && st == DQT_OK; ++l) {
         dqt::DxArgs a;
         a.dY = sub[l].dY;
         a.Wq = sub[l].Wq;
+        if (wfmt == DQT_INT4) {
+          // nibbles -> one int8 code per weight, in the weight area of the workspace
+          int8_t* q8 = reinterpret_cast<int8_t*>(wsb + Px.q_off[l]);
+          st = from_hip(dqt::launch_unpack_int4(sub[l].Wq, q8, sub[l].d_out * sub[l].d_in, s));
+          if (st != DQT_OK) break;
+          a.Wq = q8;
+        }
         a.dX = sub[l].dX;
         a.M = M;
         a.d_in = sub[l].d_in;
@@ -243,6 +258,7 @@ dqt_status dqt_linear_bwd_batch(int32_t n, const dqt_linear_io* io, int64_t M, i
   if (nw > 0) {
     if (xt_t == DQT_BF16) {
       dqt::BatchCfg c{nw, M, wfmt == DQT_TERNARY2, act_q == DQT_FP8E4M3, false};
+      c.w_int4 = wfmt == DQT_INT4;
       st = from_hip(dqt::launch_dw_batch(c, sub, wsb, Pw, s));
     } else {
       for (int l = 0; l < nw && st == DQT_OK; ++l) {
@@ -309,7 +325,8 @@ dqt_status dqt_linear_bwd_sr_batch(int32_t n, const dqt_linear_io* io, int64_t M
   if (M == 0) return DQT_OK;
   hipStream_t s = static_cast<hipStream_t>(stream);
   uint8_t* wsb = static_cast<uint8_t*>(ws);
-  const dqt::BatchCfg c{n, M, wfmt == DQT_TERNARY2, act_q == DQT_FP8E4M3, dx_t == DQT_BF16};
+  dqt::BatchCfg c{n, M, wfmt == DQT_TERNARY2, act_q == DQT_FP8E4M3, dx_t == DQT_BF16};
+  c.w_int4 = wfmt == DQT_INT4;
   if (nx > 0 && nx < n) {
     // dX of the linears that want it first (it reads the codes before the
     // update), then dW and the update of every linear
@@ -321,7 +338,8 @@ dqt_status dqt_linear_bwd_sr_batch(int32_t n, const dqt_linear_io* io, int64_t M
         Px.q_off[k] = P.q_off[l];
         sub[k++] = L[l];
       }
-    const dqt::BatchCfg cx{nx, M, c.w_ternary, c.act_e4m3, c.out_bf16};
+    dqt::BatchCfg cx{nx, M, c.w_ternary, c.act_e4m3, c.out_bf16};
+    cx.w_int4 = wfmt == DQT_INT4;
     st = from_hip(dqt::launch_dx_batch(cx, sub, wsb, Px, s));
     if (st != DQT_OK) return st;
   }
@@ -365,7 +383,7 @@ dqt_status dqt_update_variant_batch(int32_t n, const dqt_linear_io* io, float lr
     if (ws == nullptr || ws_bytes < dqt::update_variant_workspace(n)) return DQT_ERR_WORKSPACE;
     if (!aligned16(ws)) return DQT_ERR_ALIGN;
   }
-  return from_hip(dqt::launch_update_variant(wfmt == DQT_TERNARY2, n, t, mode, frac, seed, step,
+  return from_hip(dqt::launch_update_variant(code_format(wfmt), n, t, mode, frac, seed, step,
                                              counters, ws, static_cast<hipStream_t>(stream)));
 }
 
@@ -409,7 +427,7 @@ dqt_status dqt_adamw_sr_update_batch(int32_t n, const dqt_linear_io* io, float* 
     t[l].tensor_id = io[l].w->tensor_id;
   }
   const dqt::AdamHyper h{hp->lr, hp->beta1, hp->beta2, hp->eps, hp->weight_decay};
-  return from_hip(dqt::launch_adamw_sr(wfmt == DQT_TERNARY2, n, t, h, seed, step, counters,
+  return from_hip(dqt::launch_adamw_sr(code_format(wfmt), n, t, h, seed, step, counters,
                                        static_cast<hipStream_t>(stream)));
 }
 
@@ -445,7 +463,7 @@ dqt_status dqt_sr_update_batch(int32_t n, const dqt_linear_io* io, float lr, uin
     t[l].qmax = io[l].w->qmax;
     t[l].tensor_id = io[l].w->tensor_id;
   }
-  return from_hip(dqt::launch_sr_update(wfmt == DQT_TERNARY2, n, t, seed, step, counters,
+  return from_hip(dqt::launch_sr_update(code_format(wfmt), n, t, seed, step, counters,
                                         static_cast<hipStream_t>(stream)));
 }
 
@@ -575,6 +593,32 @@ dqt_status dqt_unpack_ternary(const uint8_t* packed, int64_t rows, int64_t cols,
     for (int64_t b = 0; b < pc; ++b)
       for (int j = 0; j < 4; ++j)
         q[r * cols + 4 * b + j] = (int8_t)((int)((packed[r * pc + b] >> (2 * j)) & 3u) - 1);
+  return DQT_OK;
+}
+
+dqt_status dqt_pack_int4(const int8_t* q, int64_t rows, int64_t cols, uint8_t* packed) {
+  if (q == nullptr || packed == nullptr) return DQT_ERR_NULL;
+  if (rows < 0 || cols < 0 || (cols % 2) != 0) return DQT_ERR_SHAPE;
+  const int64_t pc = cols / 2;
+  for (int64_t r = 0; r < rows; ++r)
+    for (int64_t b = 0; b < pc; ++b) {
+      const int lo = q[r * cols + 2 * b], hi = q[r * cols + 2 * b + 1];
+      if (lo < -8 || lo > 7 || hi < -8 || hi > 7) return DQT_ERR_RANGE;
+      packed[r * pc + b] = (uint8_t)(((uint32_t)lo & 0xFu) | (((uint32_t)hi & 0xFu) << 4));
+    }
+  return DQT_OK;
+}
+
+dqt_status dqt_unpack_int4(const uint8_t* packed, int64_t rows, int64_t cols, int8_t* q) {
+  if (q == nullptr || packed == nullptr) return DQT_ERR_NULL;
+  if (rows < 0 || cols < 0 || (cols % 2) != 0) return DQT_ERR_SHAPE;
+  const int64_t pc = cols / 2;
+  for (int64_t r = 0; r < rows; ++r)
+    for (int64_t b = 0; b < pc; ++b)
+      for (int j = 0; j < 2; ++j) {
+        const int v = (packed[r * pc + b] >> (4 * j)) & 0xF;
+        q[r * cols + 2 * b + j] = (int8_t)(v >= 8 ? v - 16 : v);
+      }
   return DQT_OK;
 }
 

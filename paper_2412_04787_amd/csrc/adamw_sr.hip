@@ -4,7 +4,8 @@
 //
 // Memory-bound streaming kernel: per weight it reads the fp32 gradient and
 // the two fp32 moments and the code, and writes the moments and the code
-// back (20.5 B/weight with 2-bit ternary codes, 22 B with int8 codes).  Each
+// back (20.5 B/weight with 2-bit ternary codes, 21 B with 4-bit and 22 B
+// with int8 codes).  Each
 // lane owns 8 consecutive weights (one Philox block), as the plain update.
 //
 // Per element, in fp32 with round-to-nearest-even after every operation (no
@@ -45,7 +46,7 @@ struct AdamTab {
 
 // Persistent kernel: block b takes tiles b, b + grid, ...; thread t of a tile
 // owns chunk t (8 weights).  Counts are reduced per block, one atomic each.
-template <bool TERN>
+template <int CF>
 __global__ __launch_bounds__(256) void adamw_sr_kernel(const AdamTab tab,
                                                        unsigned long long* __restrict__ counters) {
   __shared__ unsigned long long red[2][256 / kWave];
@@ -63,8 +64,10 @@ __global__ __launch_bounds__(256) void adamw_sr_kernel(const AdamTab tab,
     const f32x4 m4[2] = {__builtin_nontemporal_load(mp), __builtin_nontemporal_load(mp + 1)};
     const f32x4 v4[2] = {__builtin_nontemporal_load(vp), __builtin_nontemporal_load(vp + 1)};
     uint32_t win[4] = {0u, 0u, 0u, 0u};
-    if constexpr (TERN) {
+    if constexpr (CF == CF_T2) {
       win[0] = reinterpret_cast<const uint16_t*>(tab.wq[s])[t];
+    } else if constexpr (CF == CF_I4) {
+      win[0] = reinterpret_cast<const uint32_t*>(tab.wq[s])[t];
     } else {
       const uint2 w = reinterpret_cast<const uint2*>(tab.wq[s])[t];
       win[0] = w.x;
@@ -86,7 +89,7 @@ __global__ __launch_bounds__(256) void adamw_sr_kernel(const AdamTab tab,
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
       const float g = g4[j >> 2][j & 3], m = m4[j >> 2][j & 3], v = v4[j >> 2][j & 3];
-      const int q = TERN ? (int)((win[0] >> (2 * j)) & 3u) - 1 : (int)(int8_t)(win[j >> 2] >> (8 * (j & 3)));
+      const int q = CodeFmt<CF>::q_of(win, j);
       const float m1 = __fadd_rn(__fmul_rn(tab.b1, m), __fmul_rn(tab.ob1, g));
       const float v1 = __fadd_rn(__fmul_rn(tab.b2, v), __fmul_rn(__fmul_rn(tab.ob2, g), g));
       const float den = __fadd_rn(__fmul_rn(__fsqrt_rn(v1), tab.k2), tab.eps);
@@ -99,12 +102,13 @@ __global__ __launch_bounds__(256) void adamw_sr_kernel(const AdamTab tab,
       vo[j >> 2][j & 3] = keep ? v : v1;
     }
     uint32_t wout[4];
-    sr_chunk_delta<TERN>(win, delta, bad, (uint64_t)t, a, wout, changed, nonfin);
+    sr_chunk_delta<CF>(win, delta, bad, (uint64_t)t, a, wout, changed, nonfin);
     mp[0] = mo[0];
     mp[1] = mo[1];
     vp[0] = vo[0];
     vp[1] = vo[1];
-    if constexpr (TERN) reinterpret_cast<uint16_t*>(tab.wq[s])[t] = (uint16_t)wout[0];
+    if constexpr (CF == CF_T2) reinterpret_cast<uint16_t*>(tab.wq[s])[t] = (uint16_t)wout[0];
+    else if constexpr (CF == CF_I4) reinterpret_cast<uint32_t*>(tab.wq[s])[t] = wout[0];
     else reinterpret_cast<uint2*>(tab.wq[s])[t] = make_uint2(wout[0], wout[1]);
   }
   if (counters != nullptr) {
@@ -152,7 +156,7 @@ double pow_by_squaring(double b, uint32_t t) {
 
 }  // namespace
 
-hipError_t launch_adamw_sr(bool ternary, int n, const AdamTensor* t, const AdamHyper& hp,
+hipError_t launch_adamw_sr(int cf, int n, const AdamTensor* t, const AdamHyper& hp,
                            uint64_t seed, uint32_t step, unsigned long long* counters,
                            hipStream_t stream) {
   AdamTab tab{};
@@ -186,15 +190,18 @@ hipError_t launch_adamw_sr(bool ternary, int n, const AdamTensor* t, const AdamH
   }
   tab.b0[n] = tiles;
   if (tiles == 0) return hipSuccess;
-  static const int resident[2] = {
-      adam_resident_blocks(reinterpret_cast<const void*>(adamw_sr_kernel<false>)),
-      adam_resident_blocks(reinterpret_cast<const void*>(adamw_sr_kernel<true>))};
-  const int64_t cap = resident[ternary ? 1 : 0];
+  static const int resident[3] = {
+      adam_resident_blocks(reinterpret_cast<const void*>(adamw_sr_kernel<CF_I8>)),
+      adam_resident_blocks(reinterpret_cast<const void*>(adamw_sr_kernel<CF_T2>)),
+      adam_resident_blocks(reinterpret_cast<const void*>(adamw_sr_kernel<CF_I4>))};
+  const int64_t cap = resident[cf];
   const unsigned blocks = (unsigned)(tiles < cap ? tiles : cap);
-  if (ternary)
-    hipLaunchKernelGGL(adamw_sr_kernel<true>, dim3(blocks), dim3(256), 0, stream, tab, counters);
+  if (cf == CF_T2)
+    hipLaunchKernelGGL(adamw_sr_kernel<CF_T2>, dim3(blocks), dim3(256), 0, stream, tab, counters);
+  else if (cf == CF_I4)
+    hipLaunchKernelGGL(adamw_sr_kernel<CF_I4>, dim3(blocks), dim3(256), 0, stream, tab, counters);
   else
-    hipLaunchKernelGGL(adamw_sr_kernel<false>, dim3(blocks), dim3(256), 0, stream, tab, counters);
+    hipLaunchKernelGGL(adamw_sr_kernel<CF_I8>, dim3(blocks), dim3(256), 0, stream, tab, counters);
   return hipGetLastError();
 }
 

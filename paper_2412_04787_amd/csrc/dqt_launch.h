@@ -62,6 +62,7 @@ struct BatchCfg {
   int n;
   int64_t M;
   bool w_ternary, act_e4m3, out_bf16;
+  bool w_int4;          // 4-bit codes (two's-complement nibbles)
 };
 struct BwdPlan {
   int64_t splits;        // dW batch splits when dW runs in a launch of its own
@@ -70,7 +71,9 @@ struct BwdPlan {
   size_t q_off[kMaxBatch], xt_off[kMaxBatch], part_off[kMaxBatch];
   size_t total;
 };
-size_t fwd_batch_workspace(int n, const LinearIO* io, bool ternary, size_t* offs);
+size_t fwd_batch_workspace(int n, const LinearIO* io, int cf, size_t* offs);
+// int4 codes [n] -> int8 codes (one byte per weight), n a multiple of 16
+hipError_t launch_unpack_int4(const void* src, int8_t* dst, int64_t n, hipStream_t stream);
 hipError_t launch_fwd_batch(const BatchCfg& c, const LinearIO* io, uint8_t* ws, hipStream_t stream);
 BwdPlan plan_bwd_batch(int n, const LinearIO* io, int64_t M);
 hipError_t launch_dx_batch(const BatchCfg& c, const LinearIO* io, uint8_t* ws, const BwdPlan& P,
@@ -102,12 +105,13 @@ struct SRTensor {
   int qmin, qmax;
   uint32_t tensor_id;
 };
-hipError_t launch_sr_update(bool ternary, int n, const SRTensor* t, uint64_t seed, uint32_t step,
+// cf: code format, 0 int8, 1 ternary 2-bit, 2 int4 nibbles
+hipError_t launch_sr_update(int cf, int n, const SRTensor* t, uint64_t seed, uint32_t step,
                             unsigned long long* counters, hipStream_t stream);
 // Analysis variants of the update (mode 0 plain SR, 1 nearest, 2 force to
 // remain, 3 force to update the bottom `frac` of |delta|).
 size_t update_variant_workspace(int n);
-hipError_t launch_update_variant(bool ternary, int n, const SRTensor* t, int mode, float frac,
+hipError_t launch_update_variant(int cf, int n, const SRTensor* t, int mode, float frac,
                                  uint64_t seed, uint32_t step, unsigned long long* counters,
                                  void* ws, hipStream_t stream);
 // AdamW with SR (up to kMaxBatch tensors of one code format per launch).
@@ -124,7 +128,7 @@ struct AdamTensor {
 struct AdamHyper {
   float lr, beta1, beta2, eps, weight_decay;
 };
-hipError_t launch_adamw_sr(bool ternary, int n, const AdamTensor* t, const AdamHyper& hp,
+hipError_t launch_adamw_sr(int cf, int n, const AdamTensor* t, const AdamHyper& hp,
                            uint64_t seed, uint32_t step, unsigned long long* counters,
                            hipStream_t stream);
 hipError_t launch_debug_rng(uint64_t seed, uint32_t step, uint32_t tensor_id, uint64_t i0,

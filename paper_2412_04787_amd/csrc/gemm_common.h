@@ -20,6 +20,7 @@ struct EpiFwd {          // y = fl(fl(acc) * fl(xdq[i] * alpha))
   static constexpr bool kRowScale = true;
   static constexpr bool kSR = false;
   static constexpr bool kTern = false;
+  static constexpr int kCF = 0;
   __device__ float scale(int64_t i) const { return xdq[i] * alpha; }
   // the same factor in two parts: the per-row load, then the multiply
   __device__ float scale_raw(int64_t i) const { return xdq[i]; }
@@ -41,6 +42,7 @@ struct EpiScale {        // y = fl(alpha * acc)
   static constexpr bool kRowScale = false;
   static constexpr bool kSR = false;
   static constexpr bool kTern = false;
+  static constexpr int kCF = 0;
   __device__ float scale(int64_t) const { return alpha; }
   __device__ float scale_raw(int64_t) const { return 1.0f; }
   __device__ float scale_fin(float) const { return alpha; }
@@ -60,6 +62,7 @@ struct EpiPartial {      // fp32 partial sums, one slab per split
   static constexpr bool kRowScale = false;
   static constexpr bool kSR = false;
   static constexpr bool kTern = false;
+  static constexpr int kCF = 0;
   __device__ float scale(int64_t) const { return 1.0f; }
   __device__ float scale_raw(int64_t) const { return 1.0f; }
   __device__ float scale_fin(float) const { return 1.0f; }
@@ -75,12 +78,12 @@ struct EpiPartial {      // fp32 partial sums, one slab per split
 
 // dW consumed where it is formed: each group of 8 consecutive dW entries of
 // a row goes through the direct SR update of its 8 codes (Sec. 3.2 Eq. 5)
-// and dW itself is never stored.  TERN: 2-bit ternary codes (2 bytes per 8
-// weights), else int8 codes (8 bytes).
-template <bool TERN>
+// and dW itself is never stored.  CF: code format, 0 int8 codes (8 bytes
+// per 8 weights), 1 2-bit ternary codes (2 bytes), 2 int4 nibbles (4 bytes).
+template <int CF>
 struct EpiSR {
   uint8_t* wq;          // codes [d_out][d_in], updated in place
-  int64_t ldc;          // bytes per code row (d_in / 4 or d_in)
+  int64_t ldc;          // bytes per code row (d_in / 4, d_in / 2 or d_in)
   int64_t d_in;         // weights per row: the flat index of (n, k) is n d_in + k
   float c, L;           // fl32(lr / alpha); |delta| clamp qmax - qmin + 1
   int qmin, qmax;
@@ -88,7 +91,8 @@ struct EpiSR {
   unsigned long long* counters; // nullable: changed, non-finite (accumulated)
   static constexpr bool kRowScale = false;
   static constexpr bool kSR = true;
-  static constexpr bool kTern = TERN;
+  static constexpr bool kTern = CF == 1;
+  static constexpr int kCF = CF;
   __device__ float scale(int64_t) const { return 1.0f; }
   __device__ float scale_raw(int64_t) const { return 1.0f; }
   __device__ float scale_fin(float) const { return 1.0f; }

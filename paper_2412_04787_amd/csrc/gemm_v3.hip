@@ -683,6 +683,10 @@ __device__ __forceinline__ void gemm_v3_body(const Group<Epi>& grp, lds_u8* smem
               const uint32_t v = *reinterpret_cast<const uint16_t*>(src);
               if (u == 0) srt[ta][tb] = v;
               else srt[ta][tb] |= v << 16;
+            } else if constexpr (Epi::kCF == CF_I4) {
+              const uint8_t* src = ok ? epi.wq + n * epi.ldc + (k >> 1) : dummy;
+              sr8[ta][tb][u][0] = *reinterpret_cast<const uint32_t*>(src);
+              sr8[ta][tb][u][1] = 0;
             } else {
               const uint8_t* src = ok ? epi.wq + n * epi.ldc + k : dummy;
               const uint2 v = *reinterpret_cast<const uint2*>(src);
@@ -839,7 +843,7 @@ __device__ __forceinline__ void gemm_v3_body(const Group<Epi>& grp, lds_u8* smem
           }
           uint32_t wout[4];
           uint32_t ch = 0, nf = 0;
-          sr_chunk<Epi::kTern, 8>(win, gv, (uint64_t)(n * epi.d_in + k) >> 3, sa, wout, ch, nf);
+          sr_chunk<Epi::kCF, 8>(win, gv, (uint64_t)(n * epi.d_in + k) >> 3, sa, wout, ch, nf);
           if (ok) {
             tc += ch;
             tn += nf;
@@ -847,6 +851,9 @@ __device__ __forceinline__ void gemm_v3_body(const Group<Epi>& grp, lds_u8* smem
           if constexpr (Epi::kTern) {
             uint8_t* dst = ok ? epi.wq + n * epi.ldc + (k >> 2) : dummy;
             *reinterpret_cast<uint16_t*>(dst) = (uint16_t)wout[0];
+          } else if constexpr (Epi::kCF == CF_I4) {
+            uint8_t* dst = ok ? epi.wq + n * epi.ldc + (k >> 1) : dummy;
+            *reinterpret_cast<uint32_t*>(dst) = wout[0];
           } else {
             uint8_t* dst = ok ? epi.wq + n * epi.ldc + k : dummy;
             *reinterpret_cast<uint2*>(dst) = make_uint2(wout[0], wout[1]);
@@ -1007,6 +1014,23 @@ __global__ __launch_bounds__(256) void unpack_ternary_kernel(const SegTab tab) {
   static_cast<uint4*>(tab.dst[s])[t] = make_uint4(o[0], o[1], o[2], o[3]);
 }
 
+// int4 codes (two's-complement nibbles, weight k at bits 4 (k mod 2) of byte
+// k / 2) -> one int8 byte per weight, same order; 16 weights per thread.
+__global__ __launch_bounds__(256) void unpack_int4_kernel(const SegTab tab) {
+  const int s = seg_of_block(tab);
+  const int64_t t = (int64_t)(blockIdx.x - tab.b0[s]) * 256 + threadIdx.x;
+  if (t >= tab.n16[s]) return;
+  const uint2 w2 = static_cast<const uint2*>(tab.src[s])[t];
+  const uint32_t w[2] = {w2.x, w2.y};
+  uint32_t o[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+  for (int e = 0; e < 16; ++e) {
+    const int q = (int)(w[e >> 3] << (28 - 4 * (e & 7))) >> 28;
+    o[e >> 2] |= ((uint32_t)q & 0xFFu) << (8 * (e & 3));
+  }
+  static_cast<uint4*>(tab.dst[s])[t] = make_uint4(o[0], o[1], o[2], o[3]);
+}
+
 // int8 codes -> bf16 (|q| <= 128 is exact in bf16).
 // Weights q [d_out][d_in] (packed ternary codes, or int8) -> the B operand of
 // dX with the reduction contiguous: W~T[k][n] = bf16(q[n][k]), rows of d_out
@@ -1019,7 +1043,7 @@ struct TrTab {
   int32_t b0[MAXG + 1];
   int32_t n;
 };
-template <bool TERN>
+template <int CF>
 __global__ __launch_bounds__(256) void unpack_t_kernel(const TrTab tab) {
   int s = 0;
   while (s + 1 < tab.n && (int)blockIdx.x >= tab.b0[s + 1]) ++s;
@@ -1034,10 +1058,18 @@ __global__ __launch_bounds__(256) void unpack_t_kernel(const TrTab tab) {
     const int n = n0 + nl, k = k0 + kl;
     uint16_t v[16];
     if (n < d_out && k < d_in) {
-      if constexpr (TERN) {
+      if constexpr (CF == CF_T2) {
         const uint32_t w = *reinterpret_cast<const uint32_t*>(tab.src[s] + (int64_t)n * (d_in / 4) + k / 4);
 #pragma unroll
         for (int e = 0; e < 16; ++e) v[e] = (uint16_t)code_to_bf16_bits((w >> (2 * e)) & 3u);
+      } else if constexpr (CF == CF_I4) {
+        const uint2 w2 = *reinterpret_cast<const uint2*>(tab.src[s] + (int64_t)n * (d_in / 2) + k / 2);
+        const uint32_t w[2] = {w2.x, w2.y};
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const float f = (float)((int)(w[e >> 3] << (28 - 4 * (e & 7))) >> 28);
+          v[e] = (uint16_t)(__float_as_uint(f) >> 16);   // exact: |q| <= 8
+        }
       } else {
         const uint4 w4 = *reinterpret_cast<const uint4*>(tab.src[s] + (int64_t)n * d_in + k);
         const uint32_t w[4] = {w4.x, w4.y, w4.z, w4.w};
@@ -1173,7 +1205,7 @@ struct RedSRTab {
   uint32_t k0, k1, step;
   unsigned long long* counters;
 };
-template <bool TERN>
+template <int CF>
 __global__ __launch_bounds__(256) void split_reduce_sr_kernel(const RedSRTab tab) {
   int s = 0;
   while (s + 1 < tab.n && (int)blockIdx.x >= tab.b0[s + 1]) ++s;
@@ -1205,15 +1237,18 @@ __global__ __launch_bounds__(256) void split_reduce_sr_kernel(const RedSRTab tab
     a.step = tab.step;
     a.tid = tab.tid[s];
     uint32_t win[4] = {0u, 0u, 0u, 0u}, wout[4];
-    if constexpr (TERN) {
+    if constexpr (CF == CF_T2) {
       win[0] = reinterpret_cast<const uint16_t*>(tab.wq[s])[t];
+    } else if constexpr (CF == CF_I4) {
+      win[0] = reinterpret_cast<const uint32_t*>(tab.wq[s])[t];
     } else {
       const uint2 v = reinterpret_cast<const uint2*>(tab.wq[s])[t];
       win[0] = v.x;
       win[1] = v.y;
     }
-    sr_chunk<TERN, 8>(win, gv, (uint64_t)t, a, wout, ch, nf);
-    if constexpr (TERN) reinterpret_cast<uint16_t*>(tab.wq[s])[t] = (uint16_t)wout[0];
+    sr_chunk<CF, 8>(win, gv, (uint64_t)t, a, wout, ch, nf);
+    if constexpr (CF == CF_T2) reinterpret_cast<uint16_t*>(tab.wq[s])[t] = (uint16_t)wout[0];
+    else if constexpr (CF == CF_I4) reinterpret_cast<uint32_t*>(tab.wq[s])[t] = wout[0];
     else reinterpret_cast<uint2*>(tab.wq[s])[t] = make_uint2(wout[0], wout[1]);
   }
   if (tab.counters != nullptr) {
@@ -1318,6 +1353,18 @@ using namespace v3;
 
 static size_t align256(size_t n) { return (n + 255) / 256 * 256; }
 
+hipError_t launch_unpack_int4(const void* src, int8_t* dst, int64_t n, hipStream_t stream) {
+  if (n == 0) return hipSuccess;
+  SegTab tab{};
+  tab.n = 1;
+  tab.src[0] = src;
+  tab.dst[0] = dst;
+  tab.n16[0] = n / 16;
+  const int32_t blocks = seal(tab);
+  hipLaunchKernelGGL(unpack_int4_kernel, dim3(blocks), dim3(256), 0, stream, tab);
+  return hipGetLastError();
+}
+
 // Ternary weights reach the forward GEMM as packed codes when every d_in of
 // the batch is a multiple of 64 (16-byte aligned packed rows); otherwise
 // they are first unpacked into the workspace.
@@ -1327,9 +1374,9 @@ static bool fwd_packed(int n, const LinearIO* io) {
   return true;
 }
 
-size_t fwd_batch_workspace(int n, const LinearIO* io, bool ternary, size_t* offs) {
+size_t fwd_batch_workspace(int n, const LinearIO* io, int cf, size_t* offs) {
   size_t total = kSchedBytes;
-  const bool unpack = ternary && !fwd_packed(n, io);
+  const bool unpack = (cf == CF_T2 && !fwd_packed(n, io)) || cf == CF_I4;
   for (int l = 0; l < n; ++l) {
     if (offs) offs[l] = total;
     if (unpack) total += align256((size_t)(io[l].d_out * io[l].d_in));
@@ -1340,9 +1387,20 @@ size_t fwd_batch_workspace(int n, const LinearIO* io, bool ternary, size_t* offs
 hipError_t launch_fwd_batch(const BatchCfg& c, const LinearIO* io, uint8_t* ws, hipStream_t stream) {
   if (c.M == 0 || c.n == 0) return hipSuccess;
   size_t offs[kMaxBatch];
-  fwd_batch_workspace(c.n, io, c.w_ternary, offs);
+  fwd_batch_workspace(c.n, io, c.w_ternary ? CF_T2 : c.w_int4 ? CF_I4 : CF_I8, offs);
   const bool packed = c.w_ternary && fwd_packed(c.n, io);
-  if (c.w_ternary && !packed) {
+  const bool unpacked = (c.w_ternary && !packed) || c.w_int4;   // int8 copy in the workspace
+  if (c.w_int4) {
+    SegTab tab{};
+    tab.n = c.n;
+    for (int l = 0; l < c.n; ++l) {
+      tab.src[l] = io[l].Wq;
+      tab.dst[l] = ws + offs[l];
+      tab.n16[l] = io[l].d_out * io[l].d_in / 16;
+    }
+    const int32_t blocks = seal(tab);
+    hipLaunchKernelGGL(unpack_int4_kernel, dim3(blocks), dim3(256), 0, stream, tab);
+  } else if (c.w_ternary && !packed) {
     SegTab tab{};
     tab.n = c.n;
     for (int l = 0; l < c.n; ++l) {
@@ -1363,7 +1421,7 @@ hipError_t launch_fwd_batch(const BatchCfg& c, const LinearIO* io, uint8_t* ws, 
     p.A = Opnd{static_cast<const uint8_t*>(io[l].Xq), io[l].d_in, c.M};
     if (packed)
       p.B = Opnd{static_cast<const uint8_t*>(io[l].Wq), io[l].d_in / 4, io[l].d_out};
-    else if (c.w_ternary)
+    else if (unpacked)
       p.B = Opnd{ws + offs[l], io[l].d_in, io[l].d_out};
     else
       p.B = Opnd{static_cast<const uint8_t*>(io[l].Wq), io[l].d_in, io[l].d_out};
@@ -1496,9 +1554,11 @@ static void prep_dx(const BatchCfg& c, const LinearIO* io, uint8_t* ws, const Bw
   }
   tab.b0[c.n] = blocks;
   if (c.w_ternary)
-    hipLaunchKernelGGL(unpack_t_kernel<true>, dim3(blocks), dim3(256), 0, stream, tab);
+    hipLaunchKernelGGL(unpack_t_kernel<CF_T2>, dim3(blocks), dim3(256), 0, stream, tab);
+  else if (c.w_int4)
+    hipLaunchKernelGGL(unpack_t_kernel<CF_I4>, dim3(blocks), dim3(256), 0, stream, tab);
   else
-    hipLaunchKernelGGL(unpack_t_kernel<false>, dim3(blocks), dim3(256), 0, stream, tab);
+    hipLaunchKernelGGL(unpack_t_kernel<CF_I8>, dim3(blocks), dim3(256), 0, stream, tab);
 }
 
 hipError_t launch_dx_batch(const BatchCfg& c, const LinearIO* io, uint8_t* ws, const BwdPlan& P,
@@ -1657,25 +1717,27 @@ static hipError_t reduce_sr(const BatchCfg& c, const LinearIO* io, const SRTenso
   }
   red.b0[c.n] = blocks;
   if (c.w_ternary)
-    hipLaunchKernelGGL(split_reduce_sr_kernel<true>, dim3((unsigned)blocks), dim3(256), 0, stream, red);
+    hipLaunchKernelGGL(split_reduce_sr_kernel<CF_T2>, dim3((unsigned)blocks), dim3(256), 0, stream, red);
+  else if (c.w_int4)
+    hipLaunchKernelGGL(split_reduce_sr_kernel<CF_I4>, dim3((unsigned)blocks), dim3(256), 0, stream, red);
   else
-    hipLaunchKernelGGL(split_reduce_sr_kernel<false>, dim3((unsigned)blocks), dim3(256), 0, stream, red);
+    hipLaunchKernelGGL(split_reduce_sr_kernel<CF_I8>, dim3((unsigned)blocks), dim3(256), 0, stream, red);
   return hipGetLastError();
 }
 
 // dW of every linear consumed by the SR update of its codes in the GEMM
 // epilogue (one split) or in the reduction of the partials (several), with
 // dX of every linear in the same launch when with_dx.
-template <bool TERN>
+template <int CF>
 static void launch_dw_sr_group(const BatchCfg& c, const LinearIO* io, const SRTensor* t, uint64_t seed,
                                uint32_t step, unsigned long long* counters, uint8_t* ws,
                                const BwdPlan& P, const int* first, Group<EpiScale>* gx,
                                hipStream_t stream) {
-  Group<EpiSR<TERN>> gw{};
+  Group<EpiSR<CF>> gw{};
   fill_dw(c, io, ws, P, first, gw, [&](int l) {
-    EpiSR<TERN> e;
+    EpiSR<CF> e;
     e.wq = t[l].wq;
-    e.ldc = TERN ? io[l].d_in / 4 : io[l].d_in;
+    e.ldc = CF == CF_T2 ? io[l].d_in / 4 : CF == CF_I4 ? io[l].d_in / 2 : io[l].d_in;
     e.d_in = io[l].d_in;
     e.c = t[l].c;
     e.L = (float)(t[l].qmax - t[l].qmin + 1);
@@ -1689,9 +1751,9 @@ static void launch_dw_sr_group(const BatchCfg& c, const LinearIO* io, const SRTe
     return e;
   });
   if (gx != nullptr)
-    launch_dual<EBF16, KM, KC, KB_BWD, EpiSR<TERN>, EBF16, KC, KC, KB_BWD, EpiScale>(gw, *gx, ws, stream);
+    launch_dual<EBF16, KM, KC, KB_BWD, EpiSR<CF>, EBF16, KC, KC, KB_BWD, EpiScale>(gw, *gx, ws, stream);
   else
-    launch_group<EBF16, KM, KC, KB_BWD, EpiSR<TERN>>(gw, ws, stream);
+    launch_group<EBF16, KM, KC, KB_BWD, EpiSR<CF>>(gw, ws, stream);
 }
 
 hipError_t launch_bwd_sr_batch(const BatchCfg& c, const LinearIO* io, const SRTensor* t, uint64_t seed,
@@ -1710,10 +1772,10 @@ hipError_t launch_bwd_sr_batch(const BatchCfg& c, const LinearIO* io, const SRTe
   int first[kMaxBatch];
   prep_xt(c, io, ws, Q, stream, first);
   if (Q.splits == 1) {
-    if (c.w_ternary)
-      launch_dw_sr_group<true>(c, io, t, seed, step, counters, ws, Q, first, with_dx ? &gx : nullptr, stream);
-    else
-      launch_dw_sr_group<false>(c, io, t, seed, step, counters, ws, Q, first, with_dx ? &gx : nullptr, stream);
+    Group<EpiScale>* const pgx = with_dx ? &gx : nullptr;
+    if (c.w_ternary) launch_dw_sr_group<CF_T2>(c, io, t, seed, step, counters, ws, Q, first, pgx, stream);
+    else if (c.w_int4) launch_dw_sr_group<CF_I4>(c, io, t, seed, step, counters, ws, Q, first, pgx, stream);
+    else launch_dw_sr_group<CF_I8>(c, io, t, seed, step, counters, ws, Q, first, pgx, stream);
     return hipGetLastError();
   }
   Group<EpiPartial> gw{};

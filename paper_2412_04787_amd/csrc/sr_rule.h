@@ -119,14 +119,67 @@ __device__ __forceinline__ int sr_fast(int code, float g, uint32_t P, float nc, 
   return sr_fast_d(code, nc * g, P, L, lo, hi, tiemin);
 }
 
+// Code formats of the weights: CF_I8 one byte per weight (two's complement),
+// CF_T2 2-bit ternary (code q + 1 at bits 2k of the chunk's first word),
+// CF_I4 two's-complement nibbles (weight k at bits 4 (k mod 8) of word k / 8).
+// A chunk's codes sit in words w[0 .. 3]; `field` is what the fast rule
+// moves (q + off, clamped to [qmin + off, qmax + off]).
+constexpr int CF_I8 = 0, CF_T2 = 1, CF_I4 = 2;
+template <int CF>
+struct CodeFmt {
+  static constexpr int off = CF == CF_T2 ? 1 : 0;
+  __device__ static int field(const uint32_t (&w)[4], int j) {
+    if constexpr (CF == CF_T2) return (int)((w[0] >> (2 * j)) & 3u);
+    else if constexpr (CF == CF_I4) return (int)(w[j >> 3] << (28 - 4 * (j & 7))) >> 28;
+    else return (int)(int8_t)(w[j >> 2] >> (8 * (j & 3)));
+  }
+  __device__ static int q_of(const uint32_t (&w)[4], int j) { return field(w, j) - off; }
+  // ORs field v of weight j into zeroed words
+  __device__ static void put(uint32_t (&w)[4], int j, int v) {
+    if constexpr (CF == CF_T2) w[0] |= (uint32_t)v << (2 * j);
+    else if constexpr (CF == CF_I4) w[j >> 3] |= ((uint32_t)v & 0xFu) << (4 * (j & 7));
+    else w[j >> 2] |= ((uint32_t)v & 0xFFu) << (8 * (j & 3));
+  }
+  // replaces field j by v
+  __device__ static void set(uint32_t (&w)[4], int j, int v) {
+    if constexpr (CF == CF_T2) w[0] = (w[0] & ~(3u << (2 * j))) | ((uint32_t)v << (2 * j));
+    else if constexpr (CF == CF_I4)
+      w[j >> 3] = (w[j >> 3] & ~(0xFu << (4 * (j & 7)))) | (((uint32_t)v & 0xFu) << (4 * (j & 7)));
+    else w[j >> 2] = (w[j >> 2] & ~(0xFFu << (8 * (j & 3)))) | (((uint32_t)v & 0xFFu) << (8 * (j & 3)));
+  }
+  // number of weights whose code differs, over a chunk of CW weights
+  template <int CW>
+  __device__ static uint32_t changed(const uint32_t (&a)[4], const uint32_t (&b)[4]) {
+    uint32_t n = 0;
+    if constexpr (CF == CF_T2) {
+      const uint32_t x = a[0] ^ b[0];
+      n = __builtin_popcount((x | (x >> 1)) & 0x55555555u);
+    } else if constexpr (CF == CF_I4) {
+#pragma unroll
+      for (int w = 0; w < CW / 8; ++w) {
+        const uint32_t x = a[w] ^ b[w];
+        n += __builtin_popcount((x | (x >> 1) | (x >> 2) | (x >> 3)) & 0x11111111u);
+      }
+    } else {
+#pragma unroll
+      for (int w = 0; w < CW / 4; ++w) {
+        const uint32_t x = a[w] ^ b[w];
+        n += __builtin_popcount((((x & 0x7F7F7F7Fu) + 0x7F7F7F7Fu) | x) & 0x80808080u);
+      }
+    }
+    return n;
+  }
+};
+
 // The update of one chunk of CW consecutive weights, elements
 // 8 blk .. 8 blk + CW - 1 of their tensor (CW / 8 Philox blocks): codes `win`
-// (ternary: 2 CW bits in win[0]; int8: CW / 4 words), gradients gv.  Writes
-// the new codes to `wout` and adds the changed and non-finite counts.
-template <bool TERNARY, int CW, class Count>
+// (format CF), gradients gv.  Writes the new codes to `wout` and adds the
+// changed and non-finite counts.
+template <int CF, int CW, class Count>
 __device__ __forceinline__ void sr_chunk(const uint32_t (&win)[4], const f32x4 (&gv)[CW / 4], uint64_t blk,
                                          const SRArgs& a, uint32_t (&wout)[4], Count& changed,
                                          Count& nonfin) {
+  using F = CodeFmt<CF>;
   constexpr int NG = CW / 4, NB = CW / 8;
   uint4 r[NB];
 #pragma unroll
@@ -150,28 +203,18 @@ __device__ __forceinline__ void sr_chunk(const uint32_t (&win)[4], const f32x4 (
     const uint4& rb = r[j >> 3];
     const uint32_t word = ((j >> 1) & 3) == 0 ? rb.x : ((j >> 1) & 3) == 1 ? rb.y : ((j >> 1) & 3) == 2 ? rb.z : rb.w;
     const uint32_t P = (j & 1) ? (word | 0xFFFFu) : ((word << 16) | 0xFFFFu);
-    if constexpr (TERNARY) {
-      const int code = (int)((win[0] >> (2 * j)) & 3u);
-      const int v = sr_fast(code, g, P, nc, a.L, a.qmin + 1, a.qmax + 1, tiemin);
-      wout[0] |= (uint32_t)v << (2 * j);
-    } else {
-      const int code = (int)(int8_t)(win[j >> 2] >> (8 * (j & 3)));
-      const int v = sr_fast(code, g, P, nc, a.L, a.qmin, a.qmax, tiemin);
-      wout[j >> 2] |= ((uint32_t)v & 0xFFu) << (8 * (j & 3));
-    }
+    const int v = sr_fast(F::field(win, j), g, P, nc, a.L, a.qmin + F::off, a.qmax + F::off, tiemin);
+    F::put(wout, j, v);
   }
   if (tiemin <= 0xFFFFu || !__builtin_isfinite(probe)) {
     // rare (about CW / 65536 per chunk, or a non-finite gradient): full
     // rule, in two passes over the chunk (ties and non-finite entries, then
     // the codes), so no per-element arrays stay live
-    auto q_of = [&](int j) {
-      return TERNARY ? (int)((win[0] >> (2 * j)) & 3u) - 1 : (int)(int8_t)(win[j >> 2] >> (8 * (j & 3)));
-    };
     uint32_t ties = 0;
 #pragma unroll
     for (int j = 0; j < CW; ++j) {
       bool tie, nf;
-      (void)sr_one(q_of(j), gv[j >> 2][j & 3], half16(r[j >> 3], j & 7), a, tie, nf);
+      (void)sr_one(F::q_of(win, j), gv[j >> 2][j & 3], half16(r[j >> 3], j & 7), a, tie, nf);
       ties |= (tie ? 1u : 0u) << j;
       nonfin += nf ? 1 : 0;
     }
@@ -185,38 +228,25 @@ __device__ __forceinline__ void sr_chunk(const uint32_t (&win)[4], const f32x4 (
       for (int j = 8 * b; j < 8 * b + 8; ++j) {
         bool tie, nf;
         const int v = (tb >> (j & 7)) & 1u
-                          ? sr_tie(q_of(j), gv[j >> 2][j & 3], half16(sb, j & 7), a)
-                          : sr_one(q_of(j), gv[j >> 2][j & 3], half16(r[j >> 3], j & 7), a, tie, nf);
-        if constexpr (TERNARY) wout[0] |= (uint32_t)(v + 1) << (2 * j);
-        else wout[j >> 2] |= ((uint32_t)v & 0xFFu) << (8 * (j & 3));
+                          ? sr_tie(F::q_of(win, j), gv[j >> 2][j & 3], half16(sb, j & 7), a)
+                          : sr_one(F::q_of(win, j), gv[j >> 2][j & 3], half16(r[j >> 3], j & 7), a, tie, nf);
+        F::put(wout, j, v + F::off);
       }
     }
   }
-  // changed codes: count differing 2-bit fields or bytes
-  if constexpr (TERNARY) {
-    const uint32_t x = wout[0] ^ win[0];
-    changed += __builtin_popcount((x | (x >> 1)) & 0x55555555u);
-  } else {
-#pragma unroll
-    for (int w = 0; w < CW / 4; ++w) {
-      const uint32_t x = wout[w] ^ win[w];
-      changed += __builtin_popcount((((x & 0x7F7F7F7Fu) + 0x7F7F7F7Fu) | x) & 0x80808080u);
-    }
-  }
+  changed += F::template changed<CW>(wout, win);
 }
 
 // One chunk of 8 consecutive weights (elements 8 blk .. 8 blk + 7, one
 // Philox block) moved by given steps delta[j] in grid units; bit j of `bad`
 // keeps code j (counted as non-finite; its delta must be 0).  Codes as in
 // sr_chunk.
-template <bool TERNARY, class Count>
+template <int CF, class Count>
 __device__ __forceinline__ void sr_chunk_delta(const uint32_t (&win)[4], const float (&delta)[8], uint32_t bad,
                                                uint64_t blk, const SRArgs& a, uint32_t (&wout)[4],
                                                Count& changed, Count& nonfin) {
+  using F = CodeFmt<CF>;
   const uint4 r = philox_block(blk, 0u, a.step, a.tid, a.k0, a.k1);
-  auto q_of = [&](int j) {
-    return TERNARY ? (int)((win[0] >> (2 * j)) & 3u) - 1 : (int)(int8_t)(win[j >> 2] >> (8 * (j & 3)));
-  };
   uint32_t tiemin = 0xFFFFFFFFu;
 #pragma unroll
   for (int w = 0; w < 4; ++w) wout[w] = 0;
@@ -224,15 +254,8 @@ __device__ __forceinline__ void sr_chunk_delta(const uint32_t (&win)[4], const f
   for (int j = 0; j < 8; ++j) {
     const uint32_t word = (j >> 1) == 0 ? r.x : (j >> 1) == 1 ? r.y : (j >> 1) == 2 ? r.z : r.w;
     const uint32_t P = (j & 1) ? (word | 0xFFFFu) : ((word << 16) | 0xFFFFu);
-    if constexpr (TERNARY) {
-      const int code = (int)((win[0] >> (2 * j)) & 3u);
-      const int v = sr_fast_d(code, delta[j], P, a.L, a.qmin + 1, a.qmax + 1, tiemin);
-      wout[0] |= (uint32_t)v << (2 * j);
-    } else {
-      const int code = (int)(int8_t)(win[j >> 2] >> (8 * (j & 3)));
-      const int v = sr_fast_d(code, delta[j], P, a.L, a.qmin, a.qmax, tiemin);
-      wout[j >> 2] |= ((uint32_t)v & 0xFFu) << (8 * (j & 3));
-    }
+    const int v = sr_fast_d(F::field(win, j), delta[j], P, a.L, a.qmin + F::off, a.qmax + F::off, tiemin);
+    F::put(wout, j, v);
   }
   if (tiemin <= 0xFFFFu) {
     // rare: full rule (a kept element has delta 0, which the rule keeps)
@@ -240,7 +263,7 @@ __device__ __forceinline__ void sr_chunk_delta(const uint32_t (&win)[4], const f
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
       bool tie;
-      (void)sr_one_d(q_of(j), delta[j], half16(r, j), a, tie);
+      (void)sr_one_d(F::q_of(win, j), delta[j], half16(r, j), a, tie);
       ties |= (tie ? 1u : 0u) << j;
     }
     const uint4 sb = ties ? philox_block(blk, 1u, a.step, a.tid, a.k0, a.k1) : make_uint4(0u, 0u, 0u, 0u);
@@ -249,23 +272,13 @@ __device__ __forceinline__ void sr_chunk_delta(const uint32_t (&win)[4], const f
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
       bool tie;
-      const int v = (ties >> j) & 1u ? sr_tie_d(q_of(j), delta[j], half16(sb, j), a)
-                                     : sr_one_d(q_of(j), delta[j], half16(r, j), a, tie);
-      if constexpr (TERNARY) wout[0] |= (uint32_t)(v + 1) << (2 * j);
-      else wout[j >> 2] |= ((uint32_t)v & 0xFFu) << (8 * (j & 3));
+      const int v = (ties >> j) & 1u ? sr_tie_d(F::q_of(win, j), delta[j], half16(sb, j), a)
+                                     : sr_one_d(F::q_of(win, j), delta[j], half16(r, j), a, tie);
+      F::put(wout, j, v + F::off);
     }
   }
   nonfin += __builtin_popcount(bad);
-  if constexpr (TERNARY) {
-    const uint32_t x = wout[0] ^ win[0];
-    changed += __builtin_popcount((x | (x >> 1)) & 0x55555555u);
-  } else {
-#pragma unroll
-    for (int w = 0; w < 2; ++w) {
-      const uint32_t x = wout[w] ^ win[w];
-      changed += __builtin_popcount((((x & 0x7F7F7F7Fu) + 0x7F7F7F7Fu) | x) & 0x80808080u);
-    }
-  }
+  changed += F::template changed<8>(wout, win);
 }
 
 }  // namespace dqt

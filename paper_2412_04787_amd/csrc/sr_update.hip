@@ -26,30 +26,30 @@ struct SRTab {
   uint32_t k0, k1, step;
 };
 
-// Code words of CW weights: 2-bit ternary codes (CW / 4 bytes) or int8
-// codes (CW bytes), as 32-bit words w[0 .. CW / 4 - 1] (ternary: w[0] holds
-// 2 CW bits).
-template <bool TERNARY, int CW>
+// Code words of CW weights in format CF: 2-bit ternary codes (CW / 4
+// bytes, in w[0]), nibbles (CW / 2 bytes) or int8 codes (CW bytes).
+template <int CF, int CW>
 struct CodeIO {
-  static constexpr int NWORD = TERNARY ? 1 : CW / 4;
+  static constexpr int NBYTES = CF == CF_T2 ? CW / 4 : CF == CF_I4 ? CW / 2 : CW;
+  static constexpr int NWORD = NBYTES >= 4 ? NBYTES / 4 : 1;
   __device__ static void load(const uint8_t* wq, int64_t t, uint32_t (&w)[4]) {
-    if constexpr (TERNARY && CW == 16) {
-      w[0] = reinterpret_cast<const uint32_t*>(wq)[t];
-    } else if constexpr (TERNARY) {
+    if constexpr (NBYTES == 2) {
       w[0] = reinterpret_cast<const uint16_t*>(wq)[t];
-    } else if constexpr (CW == 16) {
-      const uint4 v = reinterpret_cast<const uint4*>(wq)[t];
-      w[0] = v.x; w[1] = v.y; w[2] = v.z; w[3] = v.w;
-    } else {
+    } else if constexpr (NBYTES == 4) {
+      w[0] = reinterpret_cast<const uint32_t*>(wq)[t];
+    } else if constexpr (NBYTES == 8) {
       const uint2 v = reinterpret_cast<const uint2*>(wq)[t];
       w[0] = v.x; w[1] = v.y;
+    } else {
+      const uint4 v = reinterpret_cast<const uint4*>(wq)[t];
+      w[0] = v.x; w[1] = v.y; w[2] = v.z; w[3] = v.w;
     }
   }
   __device__ static void store(uint8_t* wq, int64_t t, const uint32_t (&w)[4]) {
-    if constexpr (TERNARY && CW == 16) reinterpret_cast<uint32_t*>(wq)[t] = w[0];
-    else if constexpr (TERNARY) reinterpret_cast<uint16_t*>(wq)[t] = (uint16_t)w[0];
-    else if constexpr (CW == 16) reinterpret_cast<uint4*>(wq)[t] = make_uint4(w[0], w[1], w[2], w[3]);
-    else reinterpret_cast<uint2*>(wq)[t] = make_uint2(w[0], w[1]);
+    if constexpr (NBYTES == 2) reinterpret_cast<uint16_t*>(wq)[t] = (uint16_t)w[0];
+    else if constexpr (NBYTES == 4) reinterpret_cast<uint32_t*>(wq)[t] = w[0];
+    else if constexpr (NBYTES == 8) reinterpret_cast<uint2*>(wq)[t] = make_uint2(w[0], w[1]);
+    else reinterpret_cast<uint4*>(wq)[t] = make_uint4(w[0], w[1], w[2], w[3]);
   }
 };
 
@@ -57,11 +57,11 @@ struct CodeIO {
 // owns chunk t of CW consecutive weights (4 CW bytes of gradient, CW / 4 or
 // CW bytes of codes, so no two lanes touch the same byte).  The change and
 // non-finite counts are reduced per block and added with one atomic each.
-template <bool TERNARY, int CW>
+template <int CF, int CW>
 __global__ __launch_bounds__(256) void sr_update_kernel(const SRTab tab,
                                                         unsigned long long* __restrict__ counters) {
   static_assert(CW == 8 || CW == 16, "8 or 16 weights per lane");
-  using CIO = CodeIO<TERNARY, CW>;
+  using CIO = CodeIO<CF, CW>;
   constexpr int NG = CW / 4;               // gradient f32x4 per chunk
   constexpr int NB = CW / 8;               // Philox blocks per chunk
   __shared__ unsigned long long red[2][256 / kWave];
@@ -109,7 +109,7 @@ __global__ __launch_bounds__(256) void sr_update_kernel(const SRTab tab,
     a.tid = tab.tid[cs];
     uint8_t* __restrict__ wq = tab.wq[cs];
     uint32_t wout[4];
-    sr_chunk<TERNARY, CW>(win, gv, (uint64_t)t * NB, a, wout, changed, nonfin);
+    sr_chunk<CF, CW>(win, gv, (uint64_t)t * NB, a, wout, changed, nonfin);
     CIO::store(wq, t, wout);
   }
   if (counters != nullptr) {
@@ -163,7 +163,7 @@ static int occupancy_blocks(const void* fn, int threads) {
 #endif
 constexpr int kCW = SR_CW;   // weights per lane
 
-hipError_t launch_sr_update(bool ternary, int n, const SRTensor* t, uint64_t seed, uint32_t step,
+hipError_t launch_sr_update(int cf, int n, const SRTensor* t, uint64_t seed, uint32_t step,
                             unsigned long long* counters, hipStream_t stream) {
   SRTab tab{};
   tab.n = n;
@@ -186,15 +186,18 @@ hipError_t launch_sr_update(bool ternary, int n, const SRTensor* t, uint64_t see
   tab.b0[n] = tiles;
   if (tiles == 0) return hipSuccess;
   // as many blocks as fit on the device at once; each loops over tiles
-  static const int resident[2] = {
-      occupancy_blocks(reinterpret_cast<const void*>(sr_update_kernel<false, kCW>), 256),
-      occupancy_blocks(reinterpret_cast<const void*>(sr_update_kernel<true, kCW>), 256)};
-  const int64_t cap = resident[ternary ? 1 : 0];
+  static const int resident[3] = {
+      occupancy_blocks(reinterpret_cast<const void*>(sr_update_kernel<CF_I8, kCW>), 256),
+      occupancy_blocks(reinterpret_cast<const void*>(sr_update_kernel<CF_T2, kCW>), 256),
+      occupancy_blocks(reinterpret_cast<const void*>(sr_update_kernel<CF_I4, kCW>), 256)};
+  const int64_t cap = resident[cf];
   const unsigned blocks = (unsigned)(tiles < cap ? tiles : cap);
-  if (ternary)
-    hipLaunchKernelGGL((sr_update_kernel<true, kCW>), dim3(blocks), dim3(256), 0, stream, tab, counters);
+  if (cf == CF_T2)
+    hipLaunchKernelGGL((sr_update_kernel<CF_T2, kCW>), dim3(blocks), dim3(256), 0, stream, tab, counters);
+  else if (cf == CF_I4)
+    hipLaunchKernelGGL((sr_update_kernel<CF_I4, kCW>), dim3(blocks), dim3(256), 0, stream, tab, counters);
   else
-    hipLaunchKernelGGL((sr_update_kernel<false, kCW>), dim3(blocks), dim3(256), 0, stream, tab, counters);
+    hipLaunchKernelGGL((sr_update_kernel<CF_I8, kCW>), dim3(blocks), dim3(256), 0, stream, tab, counters);
   return hipGetLastError();
 }
 

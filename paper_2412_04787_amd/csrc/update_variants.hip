@@ -167,7 +167,7 @@ __device__ __forceinline__ int away_code(int q, float g, float c, float L, int q
 }
 
 // The update: the plain SR chunk, then the variant's elements replaced.
-template <bool TERN>
+template <int CF>
 __global__ __launch_bounds__(256) void variant_update_kernel(const VarTab tab, const SelState* __restrict__ st,
                                                              unsigned long long* __restrict__ counters) {
   __shared__ unsigned long long red[2][256 / kWave];
@@ -180,8 +180,10 @@ __global__ __launch_bounds__(256) void variant_update_kernel(const VarTab tab, c
     const f32x4* gp = reinterpret_cast<const f32x4*>(tab.grad[s]) + 2 * t;
     const f32x4 gv[2] = {__builtin_nontemporal_load(gp), __builtin_nontemporal_load(gp + 1)};
     uint32_t win[4] = {0u, 0u, 0u, 0u};
-    if constexpr (TERN) {
+    if constexpr (CF == CF_T2) {
       win[0] = reinterpret_cast<const uint16_t*>(tab.wq[s])[t];
+    } else if constexpr (CF == CF_I4) {
+      win[0] = reinterpret_cast<const uint32_t*>(tab.wq[s])[t];
     } else {
       const uint2 w = reinterpret_cast<const uint2*>(tab.wq[s])[t];
       win[0] = w.x;
@@ -198,33 +200,24 @@ __global__ __launch_bounds__(256) void variant_update_kernel(const VarTab tab, c
     a.tid = tab.tid[s];
     uint32_t wout[4];
     unsigned long long ch_sr = 0;
-    sr_chunk<TERN, 8>(win, gv, (uint64_t)t, a, wout, ch_sr, nonfin);
+    sr_chunk<CF, 8>(win, gv, (uint64_t)t, a, wout, ch_sr, nonfin);
     const bool sel = tab.mode >= 2 && tab.k[s] != 0;
     const uint32_t tau = sel ? st[s].prefix : 0u;
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
       const float g = gv[j >> 2][j & 3];
       if (!__builtin_isfinite(g)) continue;      // kept by the SR chunk
-      const int q = TERN ? (int)((win[0] >> (2 * j)) & 3u) - 1 : (int)(int8_t)(win[j >> 2] >> (8 * (j & 3)));
+      const int q = CodeFmt<CF>::q_of(win, j);
       int v;
       if (tab.mode == 1) v = nearest_code(q, g, a.c, a.L, a.qmin, a.qmax);
       else if (sel && delta_key(g, a.c) <= tau) v = tab.mode == 2 ? q : away_code(q, g, a.c, a.L, a.qmin, a.qmax);
       else continue;
-      if constexpr (TERN) wout[0] = (wout[0] & ~(3u << (2 * j))) | ((uint32_t)(v + 1) << (2 * j));
-      else wout[j >> 2] = (wout[j >> 2] & ~(0xFFu << (8 * (j & 3)))) | (((uint32_t)v & 0xFFu) << (8 * (j & 3)));
+      CodeFmt<CF>::set(wout, j, v + CodeFmt<CF>::off);
     }
-    if constexpr (TERN) {
-      const uint32_t x = wout[0] ^ win[0];
-      changed += __builtin_popcount((x | (x >> 1)) & 0x55555555u);
-      reinterpret_cast<uint16_t*>(tab.wq[s])[t] = (uint16_t)wout[0];
-    } else {
-#pragma unroll
-      for (int w = 0; w < 2; ++w) {
-        const uint32_t x = wout[w] ^ win[w];
-        changed += __builtin_popcount((((x & 0x7F7F7F7Fu) + 0x7F7F7F7Fu) | x) & 0x80808080u);
-      }
-      reinterpret_cast<uint2*>(tab.wq[s])[t] = make_uint2(wout[0], wout[1]);
-    }
+    changed += CodeFmt<CF>::template changed<8>(wout, win);
+    if constexpr (CF == CF_T2) reinterpret_cast<uint16_t*>(tab.wq[s])[t] = (uint16_t)wout[0];
+    else if constexpr (CF == CF_I4) reinterpret_cast<uint32_t*>(tab.wq[s])[t] = wout[0];
+    else reinterpret_cast<uint2*>(tab.wq[s])[t] = make_uint2(wout[0], wout[1]);
   }
   if (counters != nullptr) {
     changed = wave_sum_u64(changed);
@@ -252,7 +245,7 @@ __global__ __launch_bounds__(256) void variant_update_kernel(const VarTab tab, c
 
 size_t update_variant_workspace(int n) { return (size_t)n * sizeof(SelState); }
 
-hipError_t launch_update_variant(bool ternary, int n, const SRTensor* t, int mode, float frac,
+hipError_t launch_update_variant(int cf, int n, const SRTensor* t, int mode, float frac,
                                  uint64_t seed, uint32_t step, unsigned long long* counters,
                                  void* ws, hipStream_t stream) {
   VarTab tab{};
@@ -294,10 +287,12 @@ hipError_t launch_update_variant(bool ternary, int n, const SRTensor* t, int mod
     }
   }
   const unsigned grid = (unsigned)(tiles < 4096 ? tiles : 4096);
-  if (ternary)
-    hipLaunchKernelGGL(variant_update_kernel<true>, dim3(grid), dim3(256), 0, stream, tab, st, counters);
+  if (cf == CF_T2)
+    hipLaunchKernelGGL(variant_update_kernel<CF_T2>, dim3(grid), dim3(256), 0, stream, tab, st, counters);
+  else if (cf == CF_I4)
+    hipLaunchKernelGGL(variant_update_kernel<CF_I4>, dim3(grid), dim3(256), 0, stream, tab, st, counters);
   else
-    hipLaunchKernelGGL(variant_update_kernel<false>, dim3(grid), dim3(256), 0, stream, tab, st, counters);
+    hipLaunchKernelGGL(variant_update_kernel<CF_I8>, dim3(grid), dim3(256), 0, stream, tab, st, counters);
   return hipGetLastError();
 }
 

@@ -46,6 +46,8 @@ def weight_codes_dev(q: np.ndarray, wfmt: str):
     if wfmt == "ternary":
         packed = O.pack_ternary(q)
         return torch.from_numpy(packed).to(DEV)
+    if wfmt == "i4":
+        return torch.from_numpy(O.pack_int4(q)).to(DEV)
     return torch.from_numpy(np.ascontiguousarray(q, dtype=np.int8)).to(DEV)
 
 
@@ -53,11 +55,13 @@ def weight_codes_host(buf, wfmt: str, d_in: int) -> np.ndarray:
     a = buf.cpu().numpy()
     if wfmt == "ternary":
         return O.unpack_ternary(a, d_in)
+    if wfmt == "i4":
+        return O.unpack_int4(a.reshape(-1, d_in // 2), d_in)
     return a.astype(np.int8)
 
 
 def make_weight(d_out, d_in, wfmt, qmin, qmax, alpha, tensor_id=0):
-    code = dqt.DQT_TERNARY2 if wfmt == "ternary" else dqt.DQT_I8
+    code = {"ternary": dqt.DQT_TERNARY2, "i4": dqt.DQT_INT4}.get(wfmt, dqt.DQT_I8)
     return dqt.weight(d_out, d_in, code, qmin, qmax, float(alpha), tensor_id)
 
 

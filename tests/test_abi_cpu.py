@@ -237,3 +237,25 @@ def test_fused_bwd_sr_argument_checks_host():
     io[0].dW = None
     assert lib.dqt_linear_bwd_sr_batch(*args(f32, 1e-3)) == dqt.DQT_ERR_UNSUPPORTED
     assert lib.dqt_linear_bwd_sr_batch(*args(bf, -1.0)) == dqt.DQT_ERR_RANGE
+
+
+def test_int4_pack_matches_oracle_and_roundtrips():
+    rng = np.random.default_rng(3)
+    q = rng.integers(-8, 8, size=(5, 32)).astype(np.int8)
+    packed = dqt.dqt_pack_int4(q)
+    assert np.array_equal(packed, O.pack_int4(q))
+    assert np.array_equal(dqt.dqt_unpack_int4(packed, 32), q)
+    # layout: weight k in the low nibble of byte k // 2 when k is even
+    two = np.array([[-8, 7, 1, -1]], np.int8)
+    assert dqt.dqt_pack_int4(two).tolist() == [[0x78, 0xF1]]
+    with pytest.raises(dqt.DqtError):
+        dqt.dqt_pack_int4(np.array([[8, 0]], np.int8))
+    # descriptor checks: the 4-bit grid must lie in [-8, 7]
+    lib = dqt.load()
+    ok = _w(wfmt=dqt.DQT_INT4, qmin=-8, qmax=7)
+    assert lib.dqt_sr_update(ctypes.byref(ok), FAKE, None, 1e-3, 0, 1, None, None) == dqt.DQT_ERR_NULL
+    bad = _w(wfmt=dqt.DQT_INT4, qmin=-9, qmax=7)
+    assert lib.dqt_sr_update(ctypes.byref(bad), FAKE, FAKE, 1e-3, 0, 1, None, None) == dqt.DQT_ERR_RANGE
+    # e4m3 activations need ternary weights
+    assert lib.dqt_linear_fwd(ctypes.byref(ok), FAKE, FAKE, dqt.DQT_F32, 16, dqt.DQT_FP8E4M3, FAKE,
+                              FAKE, FAKE, dqt.DQT_F32, FAKE, 1 << 30, None) == dqt.DQT_ERR_UNSUPPORTED

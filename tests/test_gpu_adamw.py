@@ -23,6 +23,8 @@ CASES = [
     (64, 32, "i8", -8, 7, 0.05, dict(lr=0.5, beta1=0.5, beta2=0.6, eps=1e-3, weight_decay=0.3), 3),
     (2048, 2048, "ternary", -1, 1, 0.01, dict(lr=3e-4, beta1=0.9, beta2=0.95, eps=1e-8,
                                               weight_decay=0.01), 17),
+    (192, 160, "i4", -8, 7, 0.01, dict(lr=1e-2, beta1=0.9, beta2=0.99, eps=1e-8,
+                                        weight_decay=0.05), 4),
 ]
 
 

@@ -25,6 +25,9 @@ BATCHES = [
     # two dW tiles over a long batch: dW split over the batch (partials and
     # their reduction) inside the launch it shares with dX
     (4096, [(256, 256, 0), (256, 128, 0)], "ternary", -1, 1, "i8", "bf16"),
+    # 4-bit codes: forward, dX, dW and the SR update
+    (600, [(256, 128, 0), (128, 256, 1), (256, 256, 0)], "i4", -8, 7, "i8", "bf16"),
+    (300, [(64, 80, 0), (80, 64, 1)], "i4", -4, 3, "i8", "f32"),
 ]
 
 

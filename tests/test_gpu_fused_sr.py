@@ -36,6 +36,9 @@ CASES = [
     # weights stay and are counted
     (320, [(256, 256, 0, True), (256, 256, 1, True)], "ternary", -1, 1, "i8", 5e-3, (1, 7, 33)),
     (320, [(128, 256, 0, True)], "i8", -127, 127, "i8", 5e-3, (0, 5, 100)),
+    # 4-bit codes (ragged batch, dX for all; and a batch-split dW)
+    (1000, [(256, 384, 0, True), (384, 128, 1, True)], "i4", -8, 7, "i8", 2e-2, None),
+    (4096, [(256, 256, 0, True)], "i4", -4, 3, "i8", 2e-2, (0, 9, 3)),
 ]
 
 

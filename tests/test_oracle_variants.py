@@ -104,3 +104,13 @@ def test_frac_zero_is_the_plain_update():
     a, *_ = O.update_variant(q, g, 1e-2, 0.01, -1, 1, 3, 3, 3, O.UPD_FORCE_CHANGE, 0.0)
     b, *_ = O.sr_update(q, g, 1e-2, 0.01, -1, 1, 3, 3, 3)
     assert np.array_equal(a, b)
+
+
+def test_int4_packing_layout():
+    """4-bit codes: two's-complement nibbles, weight k in the low nibble of
+    byte k // 2 when k is even; every value of [-8, 7] round-trips."""
+    q = np.array([[-8, 7, 1, -1, 0, -2]], np.int64)
+    p = O.pack_int4(q)
+    assert p.tolist() == [[0x78, 0xF1, 0xE0]]
+    allv = np.arange(-8, 8).reshape(1, 16)
+    assert np.array_equal(O.unpack_int4(O.pack_int4(allv), 16), allv)
