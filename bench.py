@@ -65,7 +65,7 @@ class Block:
         bf = torch.bfloat16 if wl.x_dtype == "bf16" else torch.float32
         self.act = dqt.DQT_I8 if wl.act == "i8" else dqt.DQT_FP8E4M3
         self.xt = dqt.DQT_BF16 if wl.xt == "bf16" else dqt.DQT_F32
-        wfmt = dqt.DQT_TERNARY2 if wl.wfmt == "ternary" else dqt.DQT_I8
+        wfmt = {"ternary": dqt.DQT_TERNARY2, "i4": dqt.DQT_INT4}.get(wl.wfmt, dqt.DQT_I8)
         M = wl.M
         self.weights, self.codes, self.dY, self.Y, self.dX, self.dW = [], [], [], [], [], []
         for li, lin in enumerate(wl.linears):
@@ -73,7 +73,8 @@ class Block:
             q, alpha = dqt.dqt_absmean_init(W0, wl.qmin, wl.qmax)
             if wl.init == "uniform":   # codes drawn directly; scale from W0 (qmax = 1)
                 q = qdraw
-            codes = dqt.dqt_pack_ternary(q) if wl.wfmt == "ternary" else q
+            codes = (dqt.dqt_pack_ternary(q) if wl.wfmt == "ternary"
+                     else dqt.dqt_pack_int4(q) if wl.wfmt == "i4" else q)
             self.codes.append(torch.from_numpy(np.ascontiguousarray(codes)).to(dev))
             self.weights.append(dqt.weight(lin.d_out, lin.d_in, wfmt, wl.qmin, wl.qmax, alpha, li))
             dy = torch.from_numpy(W.grad_draw(wl, li)).to(bf).to(dev)
@@ -145,7 +146,7 @@ def algorithmic_units(wl):
     """Per step: flops of each GEMM stage, bytes of each streaming stage."""
     M = wl.M
     f = sum(2 * M * l.d_in * l.d_out for l in wl.linears)
-    code_b = 0.25 if wl.wfmt == "ternary" else 1.0
+    code_b = {"ternary": 0.25, "i4": 0.5}.get(wl.wfmt, 1.0)
     sr_bytes = sum((2 * code_b + 4) * l.d_in * l.d_out for l in wl.linears)
     # AdamW with SR: read g, m, v and the code; write m, v and the code
     adam_bytes = sum((2 * code_b + 20) * l.d_in * l.d_out for l in wl.linears)

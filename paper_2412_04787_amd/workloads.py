@@ -37,7 +37,7 @@ class Workload:
     wid: int
     M: int                      # tokens
     linears: tuple
-    wfmt: str                   # "ternary" (2-bit packed) or "i8"
+    wfmt: str                   # "ternary" (2-bit packed), "i4" (4-bit packed) or "i8"
     qmin: int
     qmax: int
     init: str                   # "uniform": q ~ U{-1,0,1}, scale from W0
@@ -119,6 +119,13 @@ WORKLOADS = {
         wfmt="ternary", qmin=-1, qmax=1, init="absmean", act="e4m3",
         x_dtype="bf16", dy_dtype="bf16", xt="bf16", y_out="bf16", dx_out="bf16",
         lr=1e-4),
+    # The hidden-2048 block with 4-bit weights (the n = 4 grid of Eq. 3,
+    # -8..7, packed two per byte).
+    "llama_h2048_int4": Workload(
+        name="llama_h2048_int4", wid=5, M=16384, linears=_llama_linears(2048, 5632),
+        wfmt="i4", qmin=-8, qmax=7, init="absmean", act="i8",
+        x_dtype="bf16", dy_dtype="bf16", xt="bf16", y_out="bf16", dx_out="bf16",
+        lr=3e-4),
 }
 
 # Stream ids: which tensor a draw belongs to.

@@ -387,7 +387,7 @@ def test_full_step_llama_h768(lib, li):
     _full_step(W.WORKLOADS["llama_h768"], li)
 
 
-@pytest.mark.parametrize("wname", ["llama_h2048", "llama_h4096"])
+@pytest.mark.parametrize("wname", ["llama_h2048", "llama_h4096", "llama_h2048_int4"])
 @pytest.mark.parametrize("li", [0, 4, 6])
 def test_full_step_large_sampled(lib, wname, li):
     wl = W.WORKLOADS[wname]
