@@ -3,9 +3,10 @@
 //
 // Memory-bound streaming kernel: per weight it reads the packed code and the
 // fp32 gradient and writes the code back (4.5 B/weight for 2-bit ternary
-// codes, 6 B/weight for int8 codes).  Each lane owns 8 consecutive weights
-// (one Philox block): 32 contiguous bytes of gradient, and 2 (ternary) or 8
-// (int8) whole bytes of codes, so no two lanes ever touch the same byte.
+// codes, 5 B for 4-bit, 6 B for int8).  Each lane owns 8 consecutive weights
+// (one Philox block): 32 contiguous bytes of gradient, and 2 (ternary), 4
+// (4-bit) or 8 (int8) whole bytes of codes, so no two lanes ever touch the
+// same byte.
 #include "sr_rule.h"
 
 namespace dqt {
