@@ -52,27 +52,49 @@ __global__ __launch_bounds__(256) void adamw_sr_kernel(const AdamTab tab,
   __shared__ unsigned long long red[2][256 / kWave];
   unsigned long long changed = 0, nonfin = 0;
   const int64_t ntiles = tab.b0[tab.n];
-  int s = 0;
+  // Software pipeline: the next tile's gradient, moments and codes are
+  // requested before the current tile is computed.
+  int sidx = 0, ns = 0;
+  int64_t nt = 0;
+  f32x4 ng[2], nm[2], nv[2];
+  uint32_t nw[2] = {0u, 0u};
+  auto fetch = [&](int64_t tl) {
+    while (sidx + 1 < tab.n && tl >= tab.b0[sidx + 1]) ++sidx;    // tiles ascend
+    ns = sidx;
+    nt = (tl - tab.b0[sidx]) * kAdamChunksPerTile + threadIdx.x;
+    if (nt < tab.nchunks[sidx]) {
+      const f32x4* gp = reinterpret_cast<const f32x4*>(tab.grad[sidx]) + 2 * nt;
+      const f32x4* mp = reinterpret_cast<const f32x4*>(tab.m[sidx]) + 2 * nt;
+      const f32x4* vp = reinterpret_cast<const f32x4*>(tab.v[sidx]) + 2 * nt;
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        ng[u] = __builtin_nontemporal_load(gp + u);
+        nm[u] = __builtin_nontemporal_load(mp + u);
+        nv[u] = __builtin_nontemporal_load(vp + u);
+      }
+      if constexpr (CF == CF_T2) {
+        nw[0] = reinterpret_cast<const uint16_t*>(tab.wq[sidx])[nt];
+      } else if constexpr (CF == CF_I4) {
+        nw[0] = reinterpret_cast<const uint32_t*>(tab.wq[sidx])[nt];
+      } else {
+        const uint2 w = reinterpret_cast<const uint2*>(tab.wq[sidx])[nt];
+        nw[0] = w.x;
+        nw[1] = w.y;
+      }
+    }
+  };
+  if ((int64_t)blockIdx.x < ntiles) fetch(blockIdx.x);
   for (int64_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
-    while (s + 1 < tab.n && tile >= tab.b0[s + 1]) ++s;    // tiles ascend
-    const int64_t t = (tile - tab.b0[s]) * kAdamChunksPerTile + threadIdx.x;
+    const int s = ns;
+    const int64_t t = nt;
+    const f32x4 g4[2] = {ng[0], ng[1]};
+    const f32x4 m4[2] = {nm[0], nm[1]};
+    const f32x4 v4[2] = {nv[0], nv[1]};
+    uint32_t win[4] = {nw[0], nw[1], 0u, 0u};
+    if (tile + gridDim.x < ntiles) fetch(tile + gridDim.x);
     if (t >= tab.nchunks[s]) continue;
-    const f32x4* gp = reinterpret_cast<const f32x4*>(tab.grad[s]) + 2 * t;
     f32x4* mp = reinterpret_cast<f32x4*>(tab.m[s]) + 2 * t;
     f32x4* vp = reinterpret_cast<f32x4*>(tab.v[s]) + 2 * t;
-    const f32x4 g4[2] = {__builtin_nontemporal_load(gp), __builtin_nontemporal_load(gp + 1)};
-    const f32x4 m4[2] = {__builtin_nontemporal_load(mp), __builtin_nontemporal_load(mp + 1)};
-    const f32x4 v4[2] = {__builtin_nontemporal_load(vp), __builtin_nontemporal_load(vp + 1)};
-    uint32_t win[4] = {0u, 0u, 0u, 0u};
-    if constexpr (CF == CF_T2) {
-      win[0] = reinterpret_cast<const uint16_t*>(tab.wq[s])[t];
-    } else if constexpr (CF == CF_I4) {
-      win[0] = reinterpret_cast<const uint32_t*>(tab.wq[s])[t];
-    } else {
-      const uint2 w = reinterpret_cast<const uint2*>(tab.wq[s])[t];
-      win[0] = w.x;
-      win[1] = w.y;
-    }
     SRArgs a;
     a.c = 0.0f;
     a.L = tab.L[s];
