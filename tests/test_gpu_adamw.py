@@ -95,3 +95,27 @@ def test_adamw_sr_batch_equals_single_calls(lib):
     for e, s in zip(ents, singles):
         assert torch.equal(e["Wq"], s["Wq"])
         assert torch.equal(e["m"], s["m"]) and torch.equal(e["v"], s["v"])
+
+
+def test_adamw_sr_at_a_large_step(lib):
+    """At a large step the bias corrections are 1 - b^t with b^t formed by
+    binary exponentiation on both sides: same codes, m and v as the oracle."""
+    d_out, d_in, alpha = 128, 256, 0.02
+    q = W.draw_ternary((d_out, d_in), SEED, 60, 1)
+    g = W.draw_normal((d_out, d_in), 1e-2, SEED, 60, 2).astype(np.float32)
+    m0 = W.draw_normal((d_out, d_in), 1e-3, SEED, 60, 3).astype(np.float32)
+    v0 = np.abs(W.draw_normal((d_out, d_in), 1e-4, SEED, 60, 4)).astype(np.float32)
+    w = make_weight(d_out, d_in, "ternary", -1, 1, alpha, tensor_id=1)
+    Wq = weight_codes_dev(q, "ternary")
+    m_d, v_d = torch.from_numpy(m0.copy()).to(DEV), torch.from_numpy(v0.copy()).to(DEV)
+    dW = torch.from_numpy(g).to(DEV)
+    step = 123457
+    hp = dict(lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=0.01)
+    dqt.dqt_adamw_sr_update(w, Wq, dW, m_d, v_d, dqt.adamw(**hp), SEED, step)
+    torch.cuda.synchronize()
+    want, mw, vw, _, _ = O.adamw_sr_update(q.ravel(), g.ravel(), m0.ravel(), v0.ravel(), hp["lr"],
+                                           alpha, hp["beta1"], hp["beta2"], hp["eps"],
+                                           hp["weight_decay"], -1, 1, SEED, step, 1)
+    assert np.array_equal(weight_codes_host(Wq, "ternary", d_in).ravel(), want)
+    assert np.array_equal(_bits(m_d.cpu().numpy().ravel()), _bits(mw))
+    assert np.array_equal(_bits(v_d.cpu().numpy().ravel()), _bits(vw))
