@@ -259,3 +259,25 @@ def test_int4_pack_matches_oracle_and_roundtrips():
     # e4m3 activations need ternary weights
     assert lib.dqt_linear_fwd(ctypes.byref(ok), FAKE, FAKE, dqt.DQT_F32, 16, dqt.DQT_FP8E4M3, FAKE,
                               FAKE, FAKE, dqt.DQT_F32, FAKE, 1 << 30, None) == dqt.DQT_ERR_UNSUPPORTED
+
+
+def test_new_batch_entry_points_take_one_to_eight_linears():
+    """Like the other linear batches, n outside 1..8 is rejected before
+    anything is enqueued, as is an unknown variant mode."""
+    lib = dqt.load()
+    bf = dqt.DQT_BF16
+    hp = ctypes.byref(dqt.adamw(1e-3))
+    empty = (dqt.DqtLinearIO * 1)()
+    assert lib.dqt_linear_bwd_sr_batch(0, empty, 64, dqt.DQT_I8, bf, bf, bf, 1e-3, 0, 1, None, FAKE,
+                                       1 << 30, None) == dqt.DQT_ERR_SHAPE
+    assert lib.dqt_adamw_sr_update_batch(0, empty, None, None, hp, 0, 1, None, None) == dqt.DQT_ERR_SHAPE
+    assert lib.dqt_update_variant_batch(0, empty, 1e-3, 0, 1, dqt.DQT_UPD_NEAREST, 0.2, None, None, 0,
+                                        None) == dqt.DQT_ERR_SHAPE
+    nine = dqt.linear_io([dict(w=_w())] * 9)
+    assert lib.dqt_linear_bwd_sr_batch(9, nine, 64, dqt.DQT_I8, bf, bf, bf, 1e-3, 0, 1, None, FAKE,
+                                       1 << 30, None) == dqt.DQT_ERR_SHAPE
+    assert lib.dqt_adamw_sr_update_batch(9, nine, None, None, hp, 0, 1, None, None) == dqt.DQT_ERR_SHAPE
+    assert lib.dqt_update_variant_batch(9, nine, 1e-3, 0, 1, 0, 0.2, None, None, 0,
+                                        None) == dqt.DQT_ERR_SHAPE
+    assert lib.dqt_update_variant_batch(1, dqt.linear_io([dict(w=_w())]), 1e-3, 0, 1, 7, 0.2, None,
+                                        None, 0, None) == dqt.DQT_ERR_RANGE

@@ -36,6 +36,10 @@ CASES = [
     # weights stay and are counted
     (320, [(256, 256, 0, True), (256, 256, 1, True)], "ternary", -1, 1, "i8", 5e-3, (1, 7, 33)),
     (320, [(128, 256, 0, True)], "i8", -127, 127, "i8", 5e-3, (0, 5, 100)),
+    # the largest batch (8 linears, three inputs)
+    (640, [(128, 128, 0, True), (128, 256, 0, True), (128, 64, 0, True), (256, 128, 1, True),
+           (64, 128, 2, True), (128, 192, 0, True), (256, 64, 1, False), (64, 64, 2, True)],
+     "ternary", -1, 1, "i8", 1e-2, None),
     # 4-bit codes (ragged batch, dX for all; and a batch-split dW)
     (1000, [(256, 384, 0, True), (384, 128, 1, True)], "i4", -8, 7, "i8", 2e-2, None),
     (4096, [(256, 256, 0, True)], "i4", -4, 3, "i8", 2e-2, (0, 9, 3)),
