@@ -6,12 +6,15 @@
 // of Sec. 3.2 Eq. 5 with the same draws.
 //
 // The bottom set of a tensor is {key <= tau}: key is the fp32 bit pattern of
-// |delta| = |fl(c g)| read as an unsigned integer (monotone in |delta|;
-// 0xFFFFFFFF for a non-finite g) and tau the k-th smallest key, k =
-// floor(frac n).  tau is found exactly on the device by a radix select over
-// the keys: three passes of 11, 11 and 10 bits, each a histogram of the keys
-// that match the bits chosen so far, then a scan that picks the bin holding
-// the k-th key.  Each pass reads the gradient once (4 B per weight).
+// |delta| = |fl(c g)| read as an unsigned integer (monotone in |delta|; a
+// non-finite g ranks above every finite one) and tau the k-th smallest key,
+// k = floor(frac n).  tau is found exactly on the device by a radix select
+// over the keys: bit 31 of a key is always 0 (a non-finite g takes
+// 0x7FFFFFFF, which selects the same bottom set as any key above all finite
+// ones), so three passes cover bits 30-20, 19-9 and 8-0, each a histogram
+// of the keys that match the bits chosen so far, then a scan that picks the
+// bin holding the k-th key.  Each pass reads the gradient once (4 B per
+// weight).
 #include <math.h>
 
 #include "sr_rule.h"
@@ -46,7 +49,7 @@ struct VarTab {
 };
 
 __device__ __forceinline__ uint32_t delta_key(float g, float c) {
-  return __builtin_isfinite(g) ? (__float_as_uint(c * g) & 0x7FFFFFFFu) : 0xFFFFFFFFu;
+  return __builtin_isfinite(g) ? (__float_as_uint(c * g) & 0x7FFFFFFFu) : 0x7FFFFFFFu;
 }
 
 template <int N>
@@ -108,7 +111,7 @@ __global__ __launch_bounds__(256) void sel_pick_kernel(const VarTab tab, SelStat
   __shared__ uint32_t pick_bin, pick_below;
   SelState& S = st[blockIdx.x];
   if (tab.k[blockIdx.x] == 0) return;
-  const int per = nbins / 256;                   // 8 or 4 bins per thread
+  const int per = nbins / 256;                   // 8 or 2 bins per thread
   uint32_t sum = 0;
   for (int i = 0; i < per; ++i) sum += S.hist[threadIdx.x * per + i];
   part[threadIdx.x] = sum;
@@ -279,7 +282,7 @@ hipError_t launch_update_variant(int cf, int n, const SRTensor* t, int mode, flo
   SelState* st = static_cast<SelState*>(ws);
   if (any_sel) {
     hipLaunchKernelGGL(sel_init_kernel, dim3((unsigned)n), dim3(256), 0, stream, tab, st);
-    const int shifts[3] = {21, 10, 0}, bins[3] = {2048, 2048, 1024};
+    const int shifts[3] = {20, 9, 0}, bins[3] = {2048, 2048, 512};
     for (int p = 0; p < 3; ++p) {
       hipLaunchKernelGGL(sel_hist_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, tab, st, shifts[p],
                          bins[p]);
