@@ -282,8 +282,8 @@ dqt_status dqt_sr_update_batch(int32_t n, const dqt_linear_io* io, float lr,
  *   every other code (and every code under DQT_UPD_SR) takes the plain
  *   update with its draws, then all are clipped to [qmin, qmax].
  * The bottom set of a tensor is {key <= tau}: key is the fp32 bit pattern of
- * |fl(fl(lr / alpha) * dW)| as an unsigned integer (0xFFFFFFFF for a
- * non-finite dW), tau the k-th smallest key, k = floor(frac * n) in double
+ * |fl(fl(lr / alpha) * dW)| as an unsigned integer (a non-finite dW ranks
+ * above every finite one), tau the k-th smallest key, k = floor(frac * n) in double
  * (n = d_out * d_in < 2^32; ties at tau may enlarge the set; k = 0 leaves it
  * empty).  A non-finite dW keeps its code and is counted in counters[1].
  *   frac: in [0, 1] (used by the two force modes).
