@@ -82,8 +82,8 @@ typedef enum {
  *          -2..1, -4..3, -8..7) in 4-bit two's-complement nibbles: weight
  *          (n, k) at byte n * (d_in / 2) + k / 2, low nibble for even k.
  *          Requires -8 <= qmin < qmax <= 7.  The forward and dX expand the
- *          nibbles to int8 / bf16 in the workspace; the updates work on the
- *          nibbles in place.
+ *          nibbles to int8 or e4m3 / bf16 in the workspace; the updates work
+ *          on the nibbles in place.
  *   alpha: dequantisation scale, the weight's real value is q * alpha
  *          (alpha = 1/s, Eq. 3).  Finite and > 0.  Fixed for the life of the
  *          tensor: the library never recomputes it (Sec. 3.2 skips Eq. 2-4
@@ -135,7 +135,8 @@ size_t dqt_linear_fwd_workspace(const dqt_weight* w);
  *   X:     [M, d_in] (x_t = DQT_F32/DQT_BF16), or NULL when Xq/xdq already
  *          hold this input's quantised form (several linears sharing one
  *          input quantise it once with dqt_act_quant).
- *   act_q: DQT_I8 or DQT_FP8E4M3 (e4m3 needs wfmt = DQT_TERNARY2).
+ *   act_q: DQT_I8 or DQT_FP8E4M3 (e4m3 needs wfmt = DQT_TERNARY2 or DQT_INT4,
+ *          whose values e4m3 holds exactly).
  *   Xq, xdq: [M, d_in] codes and [M] scales; written when X != NULL, read
  *          otherwise.  Keep them for dqt_linear_bwd.
  *   Y:     [M, d_out], y_t = DQT_F32 or DQT_BF16.  (output)

@@ -137,7 +137,8 @@ dqt_status dqt_linear_fwd_batch(int32_t n, const dqt_linear_io* io, int64_t M, i
   if (M < 0) return DQT_ERR_SHAPE;
   if (act_q != DQT_I8 && act_q != DQT_FP8E4M3) return DQT_ERR_DTYPE;
   if (!is_float_type(y_t)) return DQT_ERR_DTYPE;
-  if (act_q == DQT_FP8E4M3 && wfmt != DQT_TERNARY2) return DQT_ERR_UNSUPPORTED;
+  // e4m3 operands hold the weights exactly only for |q| <= 16 (ternary, 4-bit)
+  if (act_q == DQT_FP8E4M3 && wfmt == DQT_I8) return DQT_ERR_UNSUPPORTED;
   if (M == 0) return DQT_OK;
   for (int l = 0; l < n; ++l) {
     if (io[l].Wq == nullptr || io[l].Xq == nullptr || io[l].xdq == nullptr || io[l].Y == nullptr)
@@ -484,7 +485,7 @@ dqt_status dqt_linear_fwd(const dqt_weight* w, const void* Wq, const void* X, in
   if (act_q != DQT_I8 && act_q != DQT_FP8E4M3) return DQT_ERR_DTYPE;
   if (!is_float_type(y_t)) return DQT_ERR_DTYPE;
   if (X != nullptr && !is_float_type(x_t)) return DQT_ERR_DTYPE;
-  if (act_q == DQT_FP8E4M3 && w->wfmt != DQT_TERNARY2) return DQT_ERR_UNSUPPORTED;
+  if (act_q == DQT_FP8E4M3 && w->wfmt == DQT_I8) return DQT_ERR_UNSUPPORTED;
   if (M == 0) return DQT_OK;
   if (Wq == nullptr || Xq == nullptr || xdq == nullptr || Y == nullptr) return DQT_ERR_NULL;
   if (!aligned16(Wq) || !aligned16(Xq) || !aligned16(xdq) || !aligned16(Y) ||

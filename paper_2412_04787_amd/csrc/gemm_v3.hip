@@ -1015,7 +1015,9 @@ __global__ __launch_bounds__(256) void unpack_ternary_kernel(const SegTab tab) {
 }
 
 // int4 codes (two's-complement nibbles, weight k at bits 4 (k mod 2) of byte
-// k / 2) -> one int8 byte per weight, same order; 16 weights per thread.
+// k / 2) -> one operand byte per weight (int8, or e4m3, exact for |q| <= 8),
+// same order; 16 weights per thread.
+template <int OUT>   // 0: int8, 1: e4m3
 __global__ __launch_bounds__(256) void unpack_int4_kernel(const SegTab tab) {
   const int s = seg_of_block(tab);
   const int64_t t = (int64_t)(blockIdx.x - tab.b0[s]) * 256 + threadIdx.x;
@@ -1026,7 +1028,8 @@ __global__ __launch_bounds__(256) void unpack_int4_kernel(const SegTab tab) {
 #pragma unroll
   for (int e = 0; e < 16; ++e) {
     const int q = (int)(w[e >> 3] << (28 - 4 * (e & 7))) >> 28;
-    o[e >> 2] |= ((uint32_t)q & 0xFFu) << (8 * (e & 3));
+    const uint32_t b = OUT == 1 ? f32_to_e4m3((float)q) : ((uint32_t)q & 0xFFu);
+    o[e >> 2] |= b << (8 * (e & 3));
   }
   static_cast<uint4*>(tab.dst[s])[t] = make_uint4(o[0], o[1], o[2], o[3]);
 }
@@ -1361,7 +1364,7 @@ hipError_t launch_unpack_int4(const void* src, int8_t* dst, int64_t n, hipStream
   tab.dst[0] = dst;
   tab.n16[0] = n / 16;
   const int32_t blocks = seal(tab);
-  hipLaunchKernelGGL(unpack_int4_kernel, dim3(blocks), dim3(256), 0, stream, tab);
+  hipLaunchKernelGGL(unpack_int4_kernel<0>, dim3(blocks), dim3(256), 0, stream, tab);
   return hipGetLastError();
 }
 
@@ -1399,7 +1402,10 @@ hipError_t launch_fwd_batch(const BatchCfg& c, const LinearIO* io, uint8_t* ws, 
       tab.n16[l] = io[l].d_out * io[l].d_in / 16;
     }
     const int32_t blocks = seal(tab);
-    hipLaunchKernelGGL(unpack_int4_kernel, dim3(blocks), dim3(256), 0, stream, tab);
+    if (c.act_e4m3)
+      hipLaunchKernelGGL(unpack_int4_kernel<1>, dim3(blocks), dim3(256), 0, stream, tab);
+    else
+      hipLaunchKernelGGL(unpack_int4_kernel<0>, dim3(blocks), dim3(256), 0, stream, tab);
   } else if (c.w_ternary && !packed) {
     SegTab tab{};
     tab.n = c.n;

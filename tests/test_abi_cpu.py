@@ -256,8 +256,9 @@ def test_int4_pack_matches_oracle_and_roundtrips():
     assert lib.dqt_sr_update(ctypes.byref(ok), FAKE, None, 1e-3, 0, 1, None, None) == dqt.DQT_ERR_NULL
     bad = _w(wfmt=dqt.DQT_INT4, qmin=-9, qmax=7)
     assert lib.dqt_sr_update(ctypes.byref(bad), FAKE, FAKE, 1e-3, 0, 1, None, None) == dqt.DQT_ERR_RANGE
-    # e4m3 activations need ternary weights
-    assert lib.dqt_linear_fwd(ctypes.byref(ok), FAKE, FAKE, dqt.DQT_F32, 16, dqt.DQT_FP8E4M3, FAKE,
+    # e4m3 activations take ternary or 4-bit weights (exact in e4m3), not int8 codes
+    i8w = _w(wfmt=dqt.DQT_I8, qmin=-127, qmax=127)
+    assert lib.dqt_linear_fwd(ctypes.byref(i8w), FAKE, FAKE, dqt.DQT_F32, 16, dqt.DQT_FP8E4M3, FAKE,
                               FAKE, FAKE, dqt.DQT_F32, FAKE, 1 << 30, None) == dqt.DQT_ERR_UNSUPPORTED
 
 

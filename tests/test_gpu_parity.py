@@ -93,6 +93,7 @@ FWD_KINDS = [  # act, wfmt, qmin, qmax, x_t, y_out
     ("e4m3", "ternary", -1, 1, "f32", "bf16"),
     ("i8", "i4", -8, 7, "bf16", "bf16"),
     ("i8", "i4", -4, 3, "f32", "f32"),
+    ("e4m3", "i4", -8, 7, "bf16", "f32"),
 ]
 
 
@@ -139,6 +140,7 @@ BWD_KINDS = [  # act, wfmt, qmin, qmax, xt (= dY dtype), dx_out
     ("e4m3", "ternary", -1, 1, "f32", "f32"),
     ("i8", "i4", -8, 7, "bf16", "bf16"),
     ("i8", "i4", -2, 1, "f32", "f32"),
+    ("e4m3", "i4", -4, 3, "bf16", "bf16"),
 ]
 
 
