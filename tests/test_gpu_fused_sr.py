@@ -43,6 +43,8 @@ CASES = [
     # 4-bit codes (ragged batch, dX for all; and a batch-split dW)
     (1000, [(256, 384, 0, True), (384, 128, 1, True)], "i4", -8, 7, "i8", 2e-2, None),
     (4096, [(256, 256, 0, True)], "i4", -4, 3, "i8", 2e-2, (0, 9, 3)),
+    # 4-bit codes with e4m3 activations
+    (640, [(128, 256, 0, True), (256, 128, 1, True)], "i4", -8, 7, "e4m3", 2e-2, None),
 ]
 
 
