@@ -6,15 +6,20 @@ quantisation of each distinct layer input, the forward of every linear, both
 backward products (dX and dW) of every linear, and the direct SR update of
 every weight tensor -- all through the C ABI of libdqt on one HIP stream.
 
-Default workload: the seven linears of a LLaMA block at hidden 768 / FFN 2048
-(q, k, v, o 768x768; gate, up 768->2048; down 2048->768) over 8 x 1024 = 8192
-tokens, ternary weights, bf16 activations and gradients, lr 3e-4.
+Default workload: the seven linears of a LLaMA block at hidden 4096 / FFN
+11008 (q, k, v, o 4096x4096; gate, up 4096->11008; down 11008->4096) over
+8192 tokens, ternary weights, e4m3 activations, bf16 environment, lr 1e-4:
+the largest of the single-block workloads.
 
 Prints ONE JSON line.  `value` is step TFLOP/s (6 * M * d_in * d_out summed
 over the linears, divided by the measured step time).  The step is captured
-once as a HIP graph and replayed; per-kind durations (act-quant, forward, dX,
-dW, SR) come from HIP events around back-to-back replays of a graph holding one
-step's calls of that kind, on the same stream.
+once as a HIP graph; K replays are timed between two events (ms_per_step),
+with an event after every replay for the median and p10 / p90.  Per-kind
+durations (act-quant, forward, the backward calls, the SR update) come from
+HIP events around replays of a graph holding one step's calls of that kind,
+on the same stream; the SR update call rotates over enough copies of codes
+and gradients (more than 512 MB in all) that the 256 MB last-level cache
+cannot serve one call's data to the next.
 """
 from __future__ import annotations
 
@@ -41,14 +46,17 @@ def parse():
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=20)
     p.add_argument("--warmup", type=int, default=5)
-    p.add_argument("--workload", default="llama_h768")
+    p.add_argument("--workload", default="llama_h4096")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--sr", choices=("fused", "separate"), default=None,
                    help="fused: the SR update consumes dW inside the backward call (dW is "
                         "never stored; bf16 environment only, the default there); separate: "
                         "backward writes dW, then the SR update call")
-    p.add_argument("--cpu-tokens", type=int, default=8192,
-                   help="tokens of the oracle's bounded sample")
+    p.add_argument("--cpu-tokens", type=int, default=256,
+                   help="tokens of the oracle's GEMM slab (all cores); a slab of a quarter of "
+                        "that many tokens is timed on one thread")
+    p.add_argument("--cpu-sr-weights", type=int, default=16 << 20,
+                   help="weights of the oracle's SR sample")
     p.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                    help="first run three plain device copies of MIB MiB, so that hardware "
                         "byte counters can be scaled against a kernel of known traffic")
@@ -156,17 +164,11 @@ def algorithmic_units(wl):
             "act_quant": act_bytes, "adamw_sr": adam_bytes, "upd_force": sr_bytes}
 
 
-def cpu_baseline(wl, tokens: int, min_seconds: float = 10.0):
-    """The oracle (untuned) on a bounded sample of the workload: one train step
-    of every linear over the first `tokens` tokens, repeated until at least
-    `min_seconds` of oracle time have accumulated (at most 5 repetitions)."""
-    from threadpoolctl import threadpool_info
-
-    from oracle import dqt_oracle as O
-    from paper_2412_04787_amd import workloads as W
-
-    tokens = min(tokens, wl.M)
-    X = {n: W.input_draw(wl, n)[:tokens] for n in wl.inputs}
+def _oracle_slab(O, W, wl, tokens):
+    """The oracle's inputs for one slab of `tokens` tokens: per linear (lin,
+    x, dY, q, alpha) with the environment's bf16 rounding applied."""
+    # (the first `tokens` rows of each draw: the generator fills rows in order)
+    X = {n: W.input_draw(wl, n, M=tokens) for n in wl.inputs}
     prepared = []
     for li, lin in enumerate(wl.linears):
         W0, qdraw = W.weight_draws(wl, li)
@@ -174,33 +176,83 @@ def cpu_baseline(wl, tokens: int, min_seconds: float = 10.0):
             q, alpha = qdraw, np.float32(O.absmean(W0))
         else:
             q, alpha = O.absmean_init(W0, wl.qmin, wl.qmax)
-        dY = W.grad_draw(wl, li)[:tokens]
+        dY = W.grad_draw(wl, li, M=tokens)
         x = X[lin.input]
         if wl.x_dtype == "bf16":
             x = O.bf16_to_f32(O.bf16_round(x))
             dY = O.bf16_to_f32(O.bf16_round(dY))
         prepared.append((li, lin, x, dY, q, alpha))
-    flops = 0
-    elapsed = 0.0
-    reps = 0
-    while reps < 5 and (reps == 0 or elapsed < min_seconds):
-        for li, lin, x, dY, q, alpha in prepared:
-            t0 = time.perf_counter()
-            O.linear_train_step(x, dY, q, alpha, wl.qmin, wl.qmax, act=wl.act, xt=wl.xt,
-                                y_out=wl.y_out, dx_out=wl.dx_out, lr=wl.lr, seed=wl.seed,
-                                step=1, tensor_id=li)
-            elapsed += time.perf_counter() - t0
-            flops += 6 * tokens * lin.d_in * lin.d_out
-        reps += 1
+    return prepared
+
+
+def _time_oracle_gemms(O, wl, prepared):
+    """Seconds for act-quant, forward, dX and dW of every linear of a slab."""
+    t = 0.0
+    for li, lin, x, dY, q, alpha in prepared:
+        t0 = time.perf_counter()
+        Xq, d = O.act_quant(x, wl.act)
+        O.linear_fwd(Xq, d, wl.act, q, alpha, wl.y_out)
+        O.linear_bwd(dY, q, alpha, Xq, d, wl.act, wl.xt, wl.dx_out)
+        t += time.perf_counter() - t0
+    return t
+
+
+def cpu_baseline(wl, tokens: int, sr_weights: int):
+    """The oracle (untuned) timed on the host cores on a bounded sample of
+    the workload, extrapolated to one whole step:
+      * the GEMM part (act-quant, forward, dX, dW of every linear) on a slab
+        of the first `tokens` tokens with every BLAS thread, and on a slab of
+        tokens // 4 tokens on one thread; each scaled by M / slab tokens;
+      * the SR update on `sr_weights` weights (the same share of every
+        tensor, on its real gradient-sized draws), scaled by all weights /
+        sampled weights.
+    value = the step's flops / (GEMM time + SR time), all cores."""
+    from threadpoolctl import threadpool_info, threadpool_limits
+
+    from oracle import dqt_oracle as O
+    from paper_2412_04787_amd import workloads as W
+
+    tokens = max(16, min(tokens, wl.M))
+    tok1 = max(16, tokens // 4)
     threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    prepared = _oracle_slab(O, W, wl, tokens)
+    t_all = _time_oracle_gemms(O, wl, prepared)
+    small = [(li, lin, x[:tok1], dY[:tok1], q, a) for li, lin, x, dY, q, a in prepared]
+    with threadpool_limits(limits=1):
+        t_one = _time_oracle_gemms(O, wl, small)
+    # SR sample: the first rows of every tensor, in proportion to its size
+    share = min(1.0, sr_weights / wl.n_weights)
+    rng = np.random.default_rng(0)
+    t_sr, sampled = 0.0, 0
+    for li, lin, x, dY, q, alpha in prepared:
+        rows = max(1, int(round(share * lin.d_out)))
+        qs = np.ascontiguousarray(q[:rows])
+        g = (rng.standard_normal(qs.shape, dtype=np.float32) * np.float32(1e-2 * tokens ** 0.5))
+        t0 = time.perf_counter()
+        O.sr_update(qs.ravel(), g.ravel(), wl.lr, alpha, wl.qmin, wl.qmax, wl.seed, 1, li)
+        t_sr += time.perf_counter() - t0
+        sampled += qs.size
+    sr_full = t_sr * wl.n_weights / sampled
+    gemm_all = t_all * wl.M / tokens
+    gemm_one = t_one * wl.M / tok1
+    flops = wl.train_flops
     return {
-        "value": flops / elapsed / 1e12,
+        "value": flops / (gemm_all + sr_full) / 1e12,
         "unit": "TFLOP/s",
         "cores": int(threads),
         "kind": "oracle",
-        "sample": f"{reps} x one train step (act-quant, fwd, dX, dW, SR) of all "
-                  f"{len(wl.linears)} linears of {wl.name} over the first {tokens} of {wl.M} "
-                  f"tokens; {elapsed:.1f} s of oracle time; host os.cpu_count()={os.cpu_count()}",
+        "sample": (f"extrapolated: act-quant/fwd/dX/dW of all {len(wl.linears)} linears of "
+                   f"{wl.name} on the first {tokens} of {wl.M} tokens ({t_all:.1f} s on {threads} "
+                   f"BLAS threads, x {wl.M / tokens:g}) plus the SR update on {sampled} of "
+                   f"{wl.n_weights} weights ({t_sr:.1f} s on one thread, x "
+                   f"{wl.n_weights / sampled:.1f}); host os.cpu_count()={os.cpu_count()}"),
+        "step_s_all_cores": round(gemm_all + sr_full, 2),
+        "step_s_one_thread": round(gemm_one + sr_full, 2),
+        "one_thread_value": flops / (gemm_one + sr_full) / 1e12,
+        "one_thread_sample": f"GEMM part on the first {tok1} tokens ({t_one:.1f} s, x {wl.M / tok1:g})",
+        "sr_update_gbs_one_thread": round(
+            sum((2 * {"ternary": 0.25, "i4": 0.5}.get(wl.wfmt, 1.0) + 4) * l.d_in * l.d_out
+                for l in wl.linears) / sr_full / 1e9, 3),
     }
 
 
@@ -277,28 +329,43 @@ def main():
     torch.cuda.synchronize()
 
     stream = torch.cuda.current_stream()
-    start = torch.cuda.Event(enable_timing=True)
-    end = torch.cuda.Event(enable_timing=True)
+
+    def time_graph(g, reps):
+        """Replays g `reps` times on `stream`: (total ms, per-replay ms list)."""
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(reps + 1)]
+        torch.cuda.synchronize()
+        ev[0].record(stream)
+        for r in range(reps):
+            g.replay()
+            ev[r + 1].record(stream)
+        torch.cuda.synchronize()
+        per = [ev[r].elapsed_time(ev[r + 1]) for r in range(reps)]
+        return ev[0].elapsed_time(ev[reps]), per
+
+    # the timed region: exactly K replays of the whole step
     torch.cuda.synchronize()
     wall0 = time.perf_counter()
-    start.record(stream)
-    for _ in range(args.steps):
-        step_graph.replay()
-    end.record(stream)
-    torch.cuda.synchronize()
+    total_ms, per_step = time_graph(step_graph, args.steps)
     wall = time.perf_counter() - wall0
-    total_ms = start.elapsed_time(end)
     ms_per_step = total_ms / args.steps
+    pct = lambda v, q: float(np.percentile(np.asarray(v), q))
 
     # Per-call-kind durations: a graph holding one step's calls of one kind,
-    # replayed back to back between two events on the same stream.  The
-    # step's own calls first; then dX and dW each in a call of its own.
+    # replayed between events on the same stream.  The step's own calls
+    # first; then dX and dW each in a call of its own, the SR update call
+    # (over rotating buffer sets), AdamW with SR and an analysis variant.
     step_kinds = ["act_quant", "fwd"] + (["bwd_sr"] if args.sr == "fused" else ["bwd", "sr"])
     kinds = step_kinds + (["bwd", "sr"] if args.sr == "fused" else []) + ["bwd_dx", "bwd_dw",
                                                                          "adamw_sr", "upd_force"]
     var_ws = dqt.workspace(dqt.dqt_update_variant_workspace(len(wl.linears)))
     adam_hp = dqt.adamw(wl.lr, 0.9, 0.95, 1e-8, 0.1)
-    per_kind_ms, per_kind_units, per_kind_n = {}, {}, {}
+    # SR rotation: copies of the codes and of the gradient (the backward's dW,
+    # filled by the "bwd" kind, which runs before "sr") until more than
+    # 512 MB are in the rotation
+    set_bytes = units["sr"]
+    n_sets = max(2, int(np.ceil(600e6 / set_bytes)))
+    sr_sets = []
+    per_kind = {}
     for kind in kinds:
         calls = []
 
@@ -307,6 +374,18 @@ def main():
                 calls.append(k)
                 fn()
 
+        if kind == "sr" and not sr_sets:
+            torch.cuda.synchronize()
+            for si in range(n_sets):
+                if si == 0:
+                    sr_sets.append(blk.io_all)
+                    continue
+                ents = []
+                for li in range(len(wl.linears)):
+                    ents.append(dict(w=blk.weights[li], Wq=blk.codes[li].clone(),
+                                     dW=blk.dW[li].clone()))
+                sr_sets.append(dqt.linear_io(ents))
+            torch.cuda.synchronize()
         g = torch.cuda.CUDAGraph()
         with torch.cuda.graph(g):
             if kind == "upd_force":
@@ -319,20 +398,20 @@ def main():
                 calls.append(kind)
                 dqt.dqt_adamw_sr_update_batch(blk.io_all, blk.m, blk.v, adam_hp, wl.seed, 1,
                                               blk.counters, None)
+            elif kind == "sr":
+                for io in sr_sets:
+                    calls.append(kind)
+                    dqt.dqt_sr_update_batch(io, wl.lr, wl.seed, 1, blk.counters)
             else:
                 run_step(blk, dqt, 1, None, only, split_bwd=kind in ("bwd_dx", "bwd_dw"),
                          sr="fused" if kind == "bwd_sr" else "separate")
         torch.cuda.synchronize()
-        e0 = torch.cuda.Event(enable_timing=True)
-        e1 = torch.cuda.Event(enable_timing=True)
-        e0.record(stream)
-        for _ in range(args.steps):
-            g.replay()
-        e1.record(stream)
-        torch.cuda.synchronize()
-        per_kind_ms[kind] = e0.elapsed_time(e1)
-        per_kind_units[kind] = args.steps * units[kind]
-        per_kind_n[kind] = args.steps * len(calls)
+        g.replay()                      # one untimed replay
+        tot, per = time_graph(g, args.steps)
+        n_calls = len(calls)
+        per_kind[kind] = {"mean": tot / args.steps / n_calls, "calls": n_calls,
+                          "median": pct(per, 50) / n_calls, "p10": pct(per, 10) / n_calls,
+                          "p90": pct(per, 90) / n_calls}
         del g
 
     flops = wl.train_flops
@@ -343,10 +422,13 @@ def main():
                   "bwd_dx": "bf16" if wl.dy_dtype == "bf16" else "f32",
                   "bwd_dw": "bf16" if wl.xt == "bf16" else "f32"}
     breakdown = {}
-    for kind in per_kind_ms:
-        t = per_kind_ms[kind] / args.steps
-        u = per_kind_units[kind] / args.steps
-        entry = {"ms_per_step": round(t, 4), "calls_per_step": per_kind_n[kind] // args.steps}
+    for kind, tk in per_kind.items():
+        t = tk["median"]
+        u = units[kind]
+        entry = {"ms_per_call": round(t, 4), "p10_ms": round(tk["p10"], 4),
+                 "p90_ms": round(tk["p90"], 4), "calls_per_step": 1}
+        if kind == "sr":
+            entry["buffer_sets_rotated"] = tk["calls"]
         if kind in gemm_dtype:
             tf = u / (t * 1e-3) / 1e12
             entry.update({"tflops": round(tf, 1), "dtype": gemm_dtype[kind],
@@ -356,10 +438,11 @@ def main():
             entry.update({"gbs": round(gbs, 1), "frac_hbm": round(gbs / PEAK_HBM_GBS, 4)})
         breakdown[kind] = entry
 
-    # the dominant kernel class: largest share of the step
-    dom = max(step_kinds, key=lambda k: per_kind_ms[k])
-    dom_avg_ms = per_kind_ms[dom] / per_kind_n[dom]
-    dom_units = per_kind_units[dom] / per_kind_n[dom]
+    # the dominant call of the step: its share of the step is the largest;
+    # each such call is one GEMM launch (plus the tile-counter clear)
+    dom = max(step_kinds, key=lambda k: per_kind[k]["median"])
+    dom_avg_ms = per_kind[dom]["mean"]
+    dom_units = units[dom]
     if dom in gemm_dtype:
         achieved = dom_units / (dom_avg_ms * 1e-3) / 1e12
         peak = PEAK_TFLOPS[gemm_dtype[dom]]
@@ -369,13 +452,12 @@ def main():
         peak = PEAK_HBM_GBS
         roof = {"bound": "hbm", "unit": "GB/s"}
     traffic = read_traffic(dom, wl.name)
-    roof.update({"kernel": dom, "achieved": round(achieved, 2), "peak": peak,
-                 "frac": round(achieved / peak, 4), "traffic": traffic,
+    roof.update({"achieved": round(achieved, 2), "peak": peak,
+                 "frac": round(achieved / peak, 4), "traffic": traffic, "kernel": dom,
                  "avg_launch_ms": round(dom_avg_ms, 5), "units_per_launch": dom_units})
 
-    sr_t = per_kind_ms.get("sr", 0.0) / args.steps
-    sr_gbs = per_kind_units.get("sr", 0.0) / args.steps / (sr_t * 1e-3) / 1e9 if sr_t else None
-    mfma_frac = sum(per_kind_units[k] / args.steps / (PEAK_TFLOPS[gemm_dtype[k]] * 1e12)
+    sr = breakdown.get("sr")
+    mfma_frac = sum(units[k] / (PEAK_TFLOPS[gemm_dtype[k]] * 1e12)
                     for k in ("fwd", "bwd_dx", "bwd_dw")) / (ms_per_step * 1e-3)
 
     out = {
@@ -386,6 +468,9 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(ms_per_step, 4),
+        "ms_per_step_median": round(pct(per_step, 50), 4),
+        "ms_per_step_p10": round(pct(per_step, 10), 4),
+        "ms_per_step_p90": round(pct(per_step, 90), 4),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -401,8 +486,10 @@ def main():
             "sr_update": "fused into the dW product" if args.sr == "fused" else "separate call",
             "parallelism": "single GPU",
         },
-        "sr_update_gbs": round(sr_gbs, 1) if sr_gbs else None,
-        "sr_update_frac_hbm": round(sr_gbs / PEAK_HBM_GBS, 4) if sr_gbs else None,
+        "sr_update_gbs": sr["gbs"] if sr else None,
+        "sr_update_frac_hbm": sr["frac_hbm"] if sr else None,
+        "sr_update_note": (f"separate SR call, median over {args.steps} replays, rotating "
+                           f"{n_sets} buffer sets of {set_bytes / 1e6:.1f} MB") if sr else None,
         "gemm_frac_of_dtype_peak": round(mfma_frac, 4),
         "breakdown": breakdown,
         "wall_s_timed_region": round(wall, 3),
@@ -410,7 +497,7 @@ def main():
         "kernel_source_hash": kernel_source_hash(),
     }
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(wl, args.cpu_tokens)
+        out["cpu_baseline"] = cpu_baseline(wl, args.cpu_tokens, args.cpu_sr_weights)
     print(json.dumps(out), flush=True)
 
 

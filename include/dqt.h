@@ -33,9 +33,9 @@
  *  - Non-finite values in X or dY are not checked.
  *  - Workspaces (dqt_linear_fwd / dqt_linear_bwd and their batches) are
  *    caller-owned device buffers of at least the size the matching
- *    *_workspace() call returns.  Their first 256 bytes hold the library's
- *    tile counters: they must be zero before a workspace's first use (e.g.
- *    allocate it zero-filled) and every call leaves them zero.  Calls that
+ *    *_workspace() call returns.  Their contents on entry do not matter:
+ *    the first 256 bytes hold the library's tile counters, which every call
+ *    clears on its stream before the kernels that use them.  Calls that
  *    share a workspace must not run concurrently.
  */
 #ifndef DQT_H

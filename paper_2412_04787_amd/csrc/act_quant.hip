@@ -223,21 +223,21 @@ __global__ __launch_bounds__(256) void act_quant16_kernel(const ActTab tab) {
 }
 
 template <typename TX, bool E4M3>
-void launch16_t(const ActTab& tab, int32_t blocks, hipStream_t stream) {
-  hipLaunchKernelGGL((act_quant16_kernel<TX, E4M3>), dim3((unsigned)blocks), dim3(256), 0, stream, tab);
+hipError_t launch16_t(const ActTab& tab, int32_t blocks, hipStream_t stream) {
+  return launch_kernel(act_quant16_kernel<TX, E4M3>, dim3((unsigned)blocks), dim3(256), stream, tab);
 }
 
 template <typename TX, bool E4M3>
-void launch_t(const ActTab& tab, int nch, int32_t blocks, hipStream_t stream) {
+hipError_t launch_t(const ActTab& tab, int nch, int32_t blocks, hipStream_t stream) {
   const dim3 grid((unsigned)blocks), block(kRowsPerBlock * kWave);
   switch (nch) {
-    case 1: hipLaunchKernelGGL((act_quant_kernel<TX, E4M3, 1>), grid, block, 0, stream, tab); break;
-    case 2: hipLaunchKernelGGL((act_quant_kernel<TX, E4M3, 2>), grid, block, 0, stream, tab); break;
-    case 4: hipLaunchKernelGGL((act_quant_kernel<TX, E4M3, 4>), grid, block, 0, stream, tab); break;
-    case 8: hipLaunchKernelGGL((act_quant_kernel<TX, E4M3, 8>), grid, block, 0, stream, tab); break;
-    case 16: hipLaunchKernelGGL((act_quant_kernel<TX, E4M3, 16>), grid, block, 0, stream, tab); break;
-    case 24: hipLaunchKernelGGL((act_quant_kernel<TX, E4M3, 24>), grid, block, 0, stream, tab); break;
-    default: hipLaunchKernelGGL((act_quant_kernel<TX, E4M3, 0>), grid, block, 0, stream, tab); break;
+    case 1: return launch_kernel(act_quant_kernel<TX, E4M3, 1>, grid, block, stream, tab);
+    case 2: return launch_kernel(act_quant_kernel<TX, E4M3, 2>, grid, block, stream, tab);
+    case 4: return launch_kernel(act_quant_kernel<TX, E4M3, 4>, grid, block, stream, tab);
+    case 8: return launch_kernel(act_quant_kernel<TX, E4M3, 8>, grid, block, stream, tab);
+    case 16: return launch_kernel(act_quant_kernel<TX, E4M3, 16>, grid, block, stream, tab);
+    case 24: return launch_kernel(act_quant_kernel<TX, E4M3, 24>, grid, block, stream, tab);
+    default: return launch_kernel(act_quant_kernel<TX, E4M3, 0>, grid, block, stream, tab);
   }
 }
 
@@ -266,6 +266,7 @@ hipError_t launch_act_quant_batch(int n, const ActIO* io, bool x_bf16, int64_t M
   // row, the chunk count per lane chosen per input), one per variant of the
   // whole-wave kernel for longer rows
   bool done[kMaxBatch] = {};
+  LaunchStatus st;
   for (int s0 = 0; s0 < n; ++s0) {
     if (done[s0]) continue;
     const int var = act_variant(io[s0].K / E);
@@ -290,24 +291,24 @@ hipError_t launch_act_quant_batch(int n, const ActIO* io, bool x_bf16, int64_t M
     tab.b0[tab.n] = blocks;
     if (v16) {
       if (x_bf16) {
-        if (e4m3) launch16_t<uint16_t, true>(tab, blocks, stream);
-        else launch16_t<uint16_t, false>(tab, blocks, stream);
+        if (e4m3) st << launch16_t<uint16_t, true>(tab, blocks, stream);
+        else st << launch16_t<uint16_t, false>(tab, blocks, stream);
       } else {
-        if (e4m3) launch16_t<float, true>(tab, blocks, stream);
-        else launch16_t<float, false>(tab, blocks, stream);
+        if (e4m3) st << launch16_t<float, true>(tab, blocks, stream);
+        else st << launch16_t<float, false>(tab, blocks, stream);
       }
     } else {
       const int nch = var - 64;
       if (x_bf16) {
-        if (e4m3) launch_t<uint16_t, true>(tab, nch, blocks, stream);
-        else launch_t<uint16_t, false>(tab, nch, blocks, stream);
+        if (e4m3) st << launch_t<uint16_t, true>(tab, nch, blocks, stream);
+        else st << launch_t<uint16_t, false>(tab, nch, blocks, stream);
       } else {
-        if (e4m3) launch_t<float, true>(tab, nch, blocks, stream);
-        else launch_t<float, false>(tab, nch, blocks, stream);
+        if (e4m3) st << launch_t<float, true>(tab, nch, blocks, stream);
+        else st << launch_t<float, false>(tab, nch, blocks, stream);
       }
     }
   }
-  return hipGetLastError();
+  return st.e;
 }
 
 hipError_t launch_act_quant(const void* X, bool x_bf16, int64_t M, int K, bool e4m3, void* Xq,

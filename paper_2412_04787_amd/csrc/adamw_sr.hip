@@ -212,19 +212,14 @@ hipError_t launch_adamw_sr(int cf, int n, const AdamTensor* t, const AdamHyper& 
   }
   tab.b0[n] = tiles;
   if (tiles == 0) return hipSuccess;
-  static const int resident[3] = {
-      adam_resident_blocks(reinterpret_cast<const void*>(adamw_sr_kernel<CF_I8>)),
-      adam_resident_blocks(reinterpret_cast<const void*>(adamw_sr_kernel<CF_T2>)),
-      adam_resident_blocks(reinterpret_cast<const void*>(adamw_sr_kernel<CF_I4>))};
-  const int64_t cap = resident[cf];
+  const int64_t cap = adam_resident_blocks(
+      cf == CF_T2 ? reinterpret_cast<const void*>(adamw_sr_kernel<CF_T2>)
+                  : cf == CF_I4 ? reinterpret_cast<const void*>(adamw_sr_kernel<CF_I4>)
+                                : reinterpret_cast<const void*>(adamw_sr_kernel<CF_I8>));
   const unsigned blocks = (unsigned)(tiles < cap ? tiles : cap);
-  if (cf == CF_T2)
-    hipLaunchKernelGGL(adamw_sr_kernel<CF_T2>, dim3(blocks), dim3(256), 0, stream, tab, counters);
-  else if (cf == CF_I4)
-    hipLaunchKernelGGL(adamw_sr_kernel<CF_I4>, dim3(blocks), dim3(256), 0, stream, tab, counters);
-  else
-    hipLaunchKernelGGL(adamw_sr_kernel<CF_I8>, dim3(blocks), dim3(256), 0, stream, tab, counters);
-  return hipGetLastError();
+  if (cf == CF_T2) return launch_kernel(adamw_sr_kernel<CF_T2>, dim3(blocks), dim3(256), stream, tab, counters);
+  if (cf == CF_I4) return launch_kernel(adamw_sr_kernel<CF_I4>, dim3(blocks), dim3(256), stream, tab, counters);
+  return launch_kernel(adamw_sr_kernel<CF_I8>, dim3(blocks), dim3(256), stream, tab, counters);
 }
 
 }  // namespace dqt

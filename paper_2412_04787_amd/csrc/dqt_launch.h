@@ -5,9 +5,44 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <tuple>
+#include <type_traits>
+#include <utility>
+
 #include "dqt_device.h"
 
 namespace dqt {
+
+// Kernel launches return the status of that launch itself (hipLaunchKernel),
+// never an error some earlier runtime call left behind for hipGetLastError.
+template <class K, class T, size_t... I>
+hipError_t launch_argv(K k, dim3 grid, dim3 block, hipStream_t s, T& vals, std::index_sequence<I...>) {
+  void* argv[] = {static_cast<void*>(&std::get<I>(vals))...};
+  return hipLaunchKernel(reinterpret_cast<const void*>(k), grid, block, argv, 0, s);
+}
+template <class... P, class... A>
+hipError_t launch_kernel(void (*k)(P...), dim3 grid, dim3 block, hipStream_t s, A&&... a) {
+  static_assert(sizeof...(P) == sizeof...(A), "argument count");
+  std::tuple<std::decay_t<P>...> vals(std::forward<A>(a)...);
+  return launch_argv(k, grid, block, s, vals, std::index_sequence_for<P...>{});
+}
+// The first error of a sequence of launches.
+struct LaunchStatus {
+  hipError_t e = hipSuccess;
+  LaunchStatus& operator<<(hipError_t x) {
+    if (e == hipSuccess) e = x;
+    return *this;
+  }
+};
+
+// Compute units of the current device, queried on every call (nothing is
+// cached across calls or devices).
+inline int current_device_cus() {
+  int dev = 0, n = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 256;
+  if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) return 256;
+  return n;
+}
 
 struct DxArgs {
   const void* dY;       // [M, d_out]
@@ -43,9 +78,9 @@ hipError_t launch_act_quant_batch(int n, const ActIO* io, bool x_bf16, int64_t M
 // (same dtypes, same token count M) per launch.
 constexpr int kMaxBatch = 8;
 // The first kSchedBytes of every GEMM workspace are the persistent GEMM's:
-// bytes 0-63 hold its tile counters (zero before the first call; every call
-// leaves them zero), bytes 128-143 absorb epilogue stores of chunks outside
-// the output.
+// bytes 0-127 hold its tile counters (two 64-byte slots, cleared by a small
+// kernel before every launch), bytes 128-143 absorb epilogue stores of
+// chunks outside the output.
 constexpr size_t kSchedBytes = 256;
 struct LinearIO {
   int64_t d_in, d_out;

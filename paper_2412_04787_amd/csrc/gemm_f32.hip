@@ -227,9 +227,7 @@ hipError_t launch_split_reduce(const float* ws, int splits, int64_t n, float* ou
   int64_t blocks = (n4 + 255) / 256;
   if (blocks > 256 * 16) blocks = 256 * 16;
   if (blocks < 1) blocks = 1;
-  hipLaunchKernelGGL(split_reduce_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, ws, splits,
-                     n4, out);
-  return hipGetLastError();
+  return launch_kernel(split_reduce_kernel, dim3((unsigned)blocks), dim3(256), stream, ws, splits, n4, out);
 }
 
 hipError_t launch_dx_f32(const DxArgs& a, hipStream_t stream) {
@@ -240,14 +238,13 @@ hipError_t launch_dx_f32(const DxArgs& a, hipStream_t stream) {
   ContigSrc ya{static_cast<const uint8_t*>(a.dY), R * 4, I, R * 4};
   if (a.w_ternary) {
     QTernarySrc qb{static_cast<const uint8_t*>(a.Wq), J / 4, R, J};
-    hipLaunchKernelGGL((gemm_f32_kernel<ContigStager, TransF32Stager<QTernarySrc>, ContigSrc, QTernarySrc, EpiScale>),
-                       grid, block, 0, stream, ya, qb, epi, I, J, R, R);
+    return launch_kernel(gemm_f32_kernel<ContigStager, TransF32Stager<QTernarySrc>, ContigSrc, QTernarySrc, EpiScale>,
+                         grid, block, stream, ya, qb, epi, I, J, R, R);
   } else {
     QInt8Src qb{static_cast<const int8_t*>(a.Wq), J, R, J};
-    hipLaunchKernelGGL((gemm_f32_kernel<ContigStager, TransF32Stager<QInt8Src>, ContigSrc, QInt8Src, EpiScale>),
-                       grid, block, 0, stream, ya, qb, epi, I, J, R, R);
+    return launch_kernel(gemm_f32_kernel<ContigStager, TransF32Stager<QInt8Src>, ContigSrc, QInt8Src, EpiScale>,
+                         grid, block, stream, ya, qb, epi, I, J, R, R);
   }
-  return hipGetLastError();
 }
 
 int64_t dw_splits_f32(int64_t d_out, int64_t d_in, int64_t M) {
@@ -269,16 +266,16 @@ hipError_t launch_dw_f32(const DwArgs& a, hipStream_t stream) {
   float* target = splits > 1 ? a.ws : a.dW;
   EpiPartial epi{target, J, I * J};
   DyF32Src ya{static_cast<const float*>(a.dY), I, R, I};
+  hipError_t e;
   if (a.act_e4m3) {
     XtSrc<true> xb{static_cast<const uint8_t*>(a.Xq), a.xdq, J, R, J};
-    hipLaunchKernelGGL((gemm_f32_kernel<TransF32Stager<DyF32Src>, TransF32Stager<XtSrc<true>>, DyF32Src, XtSrc<true>, EpiPartial>),
-                       grid, block, 0, stream, ya, xb, epi, I, J, R, len);
+    e = launch_kernel(gemm_f32_kernel<TransF32Stager<DyF32Src>, TransF32Stager<XtSrc<true>>, DyF32Src, XtSrc<true>, EpiPartial>,
+                      grid, block, stream, ya, xb, epi, I, J, R, len);
   } else {
     XtSrc<false> xb{static_cast<const uint8_t*>(a.Xq), a.xdq, J, R, J};
-    hipLaunchKernelGGL((gemm_f32_kernel<TransF32Stager<DyF32Src>, TransF32Stager<XtSrc<false>>, DyF32Src, XtSrc<false>, EpiPartial>),
-                       grid, block, 0, stream, ya, xb, epi, I, J, R, len);
+    e = launch_kernel(gemm_f32_kernel<TransF32Stager<DyF32Src>, TransF32Stager<XtSrc<false>>, DyF32Src, XtSrc<false>, EpiPartial>,
+                      grid, block, stream, ya, xb, epi, I, J, R, len);
   }
-  hipError_t e = hipGetLastError();
   if (e != hipSuccess || splits == 1) return e;
   return launch_split_reduce(a.ws, (int)splits, I * J, a.dW, stream);
 }

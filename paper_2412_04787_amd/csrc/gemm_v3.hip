@@ -254,7 +254,6 @@ struct Plan {
 // problem's n tiles, problems in launch order.  False past the end.
 template <class Epi>
 __device__ __forceinline__ bool locate(const Group<Epi>& grp, int x, int j, int& g, int& local) {
-  if (j < 0) return false;   // counters not zero at launch: do nothing rather than fault
   for (g = 0; g < grp.ng; ++g) {
     const int n = grp.p[g].ntiles;
     const int s0 = (x * n) >> 3, cnt = (((x + 1) * n) >> 3) - s0;
@@ -322,7 +321,7 @@ __device__ __forceinline__ void gemm_v3_body(const Group<Epi>& grp, lds_u8* smem
       code_lut[tid] = lo | (hi << 16);
     }
   }
-  const int xcd = blockIdx.x & 7, nbx8 = gridDim.x >> 3;
+  const int xcd = blockIdx.x & 7;
 
   // ---- state of the tile being computed
   struct TileState {
@@ -498,22 +497,14 @@ __device__ __forceinline__ void gemm_v3_body(const Group<Epi>& grp, lds_u8* smem
   };
   auto stage_ptr = [&](int slot) { return smem + slot * SLOTB; };
 
-  // ---- persistent loop over this block's tiles
+  // ---- persistent loop over this block's tiles (the counters were cleared
+  // by sched_clear_kernel just before this launch)
   lds_i32& next_tile = *next_tile_p;
   int* const next_ctr = grp.sched + xcd;
-  auto finish = [&]() {                 // this block found XCD xcd's list empty
-    if (tid == 0 && atomicAdd(grp.sched + 8 + xcd, 1) == nbx8 - 1) {
-      next_ctr[0] = 0;
-      grp.sched[8 + xcd] = 0;
-    }
-  };
   if (tid == 0) next_tile = atomicAdd(next_ctr, 1);
   __syncthreads();
   int g0, local0;
-  if (!locate(grp, xcd, next_tile, g0, local0)) {
-    finish();
-    return;
-  }
+  if (!locate(grp, xcd, next_tile, g0, local0)) return;
   setup(g0, local0, cur);
   // Stage of step s of the current tile: (slot0 + s) mod NS.  Before a tile
   // starts, its steps 0 .. NS-2 are in flight.
@@ -891,7 +882,6 @@ __device__ __forceinline__ void gemm_v3_body(const Group<Epi>& grp, lds_u8* smem
       if (f) atomicAdd(cnt + 1, f);
     }
   }
-  finish();
 }
 
 template <int ELEM, int MA, int MB, int KB, class Epi>
@@ -1273,12 +1263,10 @@ static int32_t seal(SegTab& t) {
   return b;
 }
 
-// Compute units of the current device (one persistent block each).
-static int device_cus() {
-  int dev = 0, n = 0;
-  if (hipGetDevice(&dev) != hipSuccess) return 256;
-  if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) return 256;
-  return n;
+// Zeroes the persistent GEMM's tile counters (both 64-byte slots) before
+// its launch, so a workspace needs no particular contents.
+__global__ __launch_bounds__(64) void sched_clear_kernel(int* sched) {
+  if (threadIdx.x < 32) sched[threadIdx.x] = 0;
 }
 
 // Tile counts and longest-first order of a group; `slot` picks its 64 bytes
@@ -1316,25 +1304,29 @@ static int32_t prep_group(Group<Epi>& grp, uint8_t* ws, int slot) {
 // Persistent grid over one group: 8 x (blocks per XCD), one block per
 // compute unit at most.
 template <int ELEM, int MA, int MB, int KB, class Epi>
-static void launch_group(Group<Epi>& grp, uint8_t* ws, hipStream_t s) {
+static hipError_t launch_group(Group<Epi>& grp, uint8_t* ws, hipStream_t s) {
   const int32_t per_xcd = prep_group<ELEM, KB>(grp, ws, 0);
-  if (per_xcd == 0) return;
-  static const int cus = device_cus();
-  const int32_t bpx = std::min(per_xcd, std::max(1, cus / 8));
-  hipLaunchKernelGGL((gemm_v3_kernel<ELEM, MA, MB, KB, Epi>), dim3((unsigned)(8 * bpx)), dim3(NTH), 0, s, grp);
+  if (per_xcd == 0) return hipSuccess;
+  const int32_t bpx = std::min(per_xcd, std::max(1, current_device_cus() / 8));
+  LaunchStatus st;
+  st << launch_kernel(sched_clear_kernel, dim3(1), dim3(64), s, reinterpret_cast<int*>(ws));
+  st << launch_kernel(gemm_v3_kernel<ELEM, MA, MB, KB, Epi>, dim3((unsigned)(8 * bpx)), dim3(NTH), s, grp);
+  return st.e;
 }
 
 // Groups g1 then g2 in one launch (tile counters in slots 1 and 0).
 template <int E1, int MA1, int MB1, int KB1, class Epi1, int E2, int MA2, int MB2, int KB2, class Epi2>
-static void launch_dual(Group<Epi1>& g1, Group<Epi2>& g2, uint8_t* ws, hipStream_t s) {
+static hipError_t launch_dual(Group<Epi1>& g1, Group<Epi2>& g2, uint8_t* ws, hipStream_t s) {
   const int32_t p1 = prep_group<E1, KB1>(g1, ws, 1);
   const int32_t p2 = prep_group<E2, KB2>(g2, ws, 0);
   const int32_t per_xcd = std::max(p1, p2);
-  if (per_xcd == 0) return;
-  static const int cus = device_cus();
-  const int32_t bpx = std::min(per_xcd, std::max(1, cus / 8));
-  hipLaunchKernelGGL((gemm_v3_dual_kernel<E1, MA1, MB1, KB1, Epi1, E2, MA2, MB2, KB2, Epi2>),
-                     dim3((unsigned)(8 * bpx)), dim3(NTH), 0, s, g1, g2);
+  if (per_xcd == 0) return hipSuccess;
+  const int32_t bpx = std::min(per_xcd, std::max(1, current_device_cus() / 8));
+  LaunchStatus st;
+  st << launch_kernel(sched_clear_kernel, dim3(1), dim3(64), s, reinterpret_cast<int*>(ws));
+  st << launch_kernel(gemm_v3_dual_kernel<E1, MA1, MB1, KB1, Epi1, E2, MA2, MB2, KB2, Epi2>,
+                      dim3((unsigned)(8 * bpx)), dim3(NTH), s, g1, g2);
+  return st.e;
 }
 
 }  // namespace v3
@@ -1364,8 +1356,7 @@ hipError_t launch_unpack_int4(const void* src, int8_t* dst, int64_t n, hipStream
   tab.dst[0] = dst;
   tab.n16[0] = n / 16;
   const int32_t blocks = seal(tab);
-  hipLaunchKernelGGL(unpack_int4_kernel<0>, dim3(blocks), dim3(256), 0, stream, tab);
-  return hipGetLastError();
+  return launch_kernel(unpack_int4_kernel<0>, dim3(blocks), dim3(256), stream, tab);
 }
 
 // Ternary weights reach the forward GEMM as packed codes when every d_in of
@@ -1389,6 +1380,7 @@ size_t fwd_batch_workspace(int n, const LinearIO* io, int cf, size_t* offs) {
 
 hipError_t launch_fwd_batch(const BatchCfg& c, const LinearIO* io, uint8_t* ws, hipStream_t stream) {
   if (c.M == 0 || c.n == 0) return hipSuccess;
+  LaunchStatus st;
   size_t offs[kMaxBatch];
   fwd_batch_workspace(c.n, io, c.w_ternary ? CF_T2 : c.w_int4 ? CF_I4 : CF_I8, offs);
   const bool packed = c.w_ternary && fwd_packed(c.n, io);
@@ -1403,9 +1395,9 @@ hipError_t launch_fwd_batch(const BatchCfg& c, const LinearIO* io, uint8_t* ws, 
     }
     const int32_t blocks = seal(tab);
     if (c.act_e4m3)
-      hipLaunchKernelGGL(unpack_int4_kernel<1>, dim3(blocks), dim3(256), 0, stream, tab);
+      st << launch_kernel(unpack_int4_kernel<1>, dim3(blocks), dim3(256), stream, tab);
     else
-      hipLaunchKernelGGL(unpack_int4_kernel<0>, dim3(blocks), dim3(256), 0, stream, tab);
+      st << launch_kernel(unpack_int4_kernel<0>, dim3(blocks), dim3(256), stream, tab);
   } else if (c.w_ternary && !packed) {
     SegTab tab{};
     tab.n = c.n;
@@ -1416,9 +1408,9 @@ hipError_t launch_fwd_batch(const BatchCfg& c, const LinearIO* io, uint8_t* ws, 
     }
     const int32_t blocks = seal(tab);
     if (c.act_e4m3)
-      hipLaunchKernelGGL(unpack_ternary_kernel<1>, dim3(blocks), dim3(256), 0, stream, tab);
+      st << launch_kernel(unpack_ternary_kernel<1>, dim3(blocks), dim3(256), stream, tab);
     else
-      hipLaunchKernelGGL(unpack_ternary_kernel<0>, dim3(blocks), dim3(256), 0, stream, tab);
+      st << launch_kernel(unpack_ternary_kernel<0>, dim3(blocks), dim3(256), stream, tab);
   }
   Group<EpiFwd> grp{};
   grp.ng = c.n;
@@ -1439,13 +1431,13 @@ hipError_t launch_fwd_batch(const BatchCfg& c, const LinearIO* io, uint8_t* ws, 
     p.nbz = 1;
   }
   if (packed) {
-    if (c.act_e4m3) launch_group<EF8, KC, KCP, 128>(grp, ws, stream);
-    else launch_group<EI8, KC, KCP, 128>(grp, ws, stream);
+    if (c.act_e4m3) st << launch_group<EF8, KC, KCP, 128>(grp, ws, stream);
+    else st << launch_group<EI8, KC, KCP, 128>(grp, ws, stream);
   } else {
-    if (c.act_e4m3) launch_group<EF8, KC, KC, KB_FWD>(grp, ws, stream);
-    else launch_group<EI8, KC, KC, KB_FWD>(grp, ws, stream);
+    if (c.act_e4m3) st << launch_group<EF8, KC, KC, KB_FWD>(grp, ws, stream);
+    else st << launch_group<EI8, KC, KC, KB_FWD>(grp, ws, stream);
   }
-  return hipGetLastError();
+  return st.e;
 }
 
 // Backward plan for a batch in the bf16 environment: one split count for
@@ -1463,7 +1455,7 @@ BwdPlan plan_bwd_batch(int n, const LinearIO* io, int64_t M) {
   P.wj = 4;
   P.splits = 1;
   P.splits_dual = 1;
-  static const int cus = device_cus();
+  const int cus = current_device_cus();
   // a step of a 256 x 256 bf16 tile is ~2048 MFMA cycles at ~2.1 GHz, plus
   // ~2 us of per-tile prologue / epilogue; partials move at ~4 TB/s
   constexpr double kStepUs = 2048.0 / 2100.0, kTileUs = 2.0;
@@ -1511,7 +1503,7 @@ BwdPlan plan_bwd_batch(int n, const LinearIO* io, int64_t M) {
 // Fills the problems of the group and launches the pre-pass that writes its
 // B operand into the workspace.
 static void prep_dx(const BatchCfg& c, const LinearIO* io, uint8_t* ws, const BwdPlan& P,
-                    hipStream_t stream, Group<EpiScale>& grp) {
+                    hipStream_t stream, Group<EpiScale>& grp, LaunchStatus& st) {
   grp.ng = c.n;
   for (int l = 0; l < c.n; ++l) {
     Prob<EpiScale>& p = grp.p[l];
@@ -1540,7 +1532,7 @@ static void prep_dx(const BatchCfg& c, const LinearIO* io, uint8_t* ws, const Bw
       grp.p[l].B = Opnd{ws + P.q_off[l], 16 * ((io[l].d_out + 63) / 64), io[l].d_in};
     }
     tab.b0[c.n] = blocks;
-    hipLaunchKernelGGL(pack_codes_t_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, tab);
+    st << launch_kernel(pack_codes_t_kernel, dim3((unsigned)blocks), dim3(256), stream, tab);
     return;
   }
   // bf16 weights transposed (reduction contiguous), so both operands are
@@ -1560,27 +1552,28 @@ static void prep_dx(const BatchCfg& c, const LinearIO* io, uint8_t* ws, const Bw
   }
   tab.b0[c.n] = blocks;
   if (c.w_ternary)
-    hipLaunchKernelGGL(unpack_t_kernel<CF_T2>, dim3(blocks), dim3(256), 0, stream, tab);
+    st << launch_kernel(unpack_t_kernel<CF_T2>, dim3(blocks), dim3(256), stream, tab);
   else if (c.w_int4)
-    hipLaunchKernelGGL(unpack_t_kernel<CF_I4>, dim3(blocks), dim3(256), 0, stream, tab);
+    st << launch_kernel(unpack_t_kernel<CF_I4>, dim3(blocks), dim3(256), stream, tab);
   else
-    hipLaunchKernelGGL(unpack_t_kernel<CF_I8>, dim3(blocks), dim3(256), 0, stream, tab);
+    st << launch_kernel(unpack_t_kernel<CF_I8>, dim3(blocks), dim3(256), stream, tab);
 }
 
 hipError_t launch_dx_batch(const BatchCfg& c, const LinearIO* io, uint8_t* ws, const BwdPlan& P,
                            hipStream_t stream) {
   if (c.M == 0 || c.n == 0) return hipSuccess;
   Group<EpiScale> grp{};
-  prep_dx(c, io, ws, P, stream, grp);
-  if (c.w_ternary && DX_PACKED_B) launch_group<EBF16, KC, KCP, 128>(grp, ws, stream);
-  else launch_group<EBF16, KC, KC, KB_BWD>(grp, ws, stream);
-  return hipGetLastError();
+  LaunchStatus st;
+  prep_dx(c, io, ws, P, stream, grp, st);
+  if (c.w_ternary && DX_PACKED_B) st << launch_group<EBF16, KC, KCP, 128>(grp, ws, stream);
+  else st << launch_group<EBF16, KC, KC, KB_BWD>(grp, ws, stream);
+  return st.e;
 }
 
 // X~T once per distinct quantised input (the dequantising transpose
 // pre-pass); first[l] is the linear whose X~T linear l reads.
 static void prep_xt(const BatchCfg& c, const LinearIO* io, uint8_t* ws, const BwdPlan& P,
-                    hipStream_t stream, int* first) {
+                    hipStream_t stream, int* first, LaunchStatus& st) {
   DqTab tab{};
   tab.M = c.M;
   tab.Mp = xt_stride(c.M);
@@ -1603,9 +1596,9 @@ static void prep_xt(const BatchCfg& c, const LinearIO* io, uint8_t* ws, const Bw
   tab.b0[tab.n] = blocks;
   if (tab.n > 0) {
     if (c.act_e4m3)
-      hipLaunchKernelGGL(dequant_t_kernel<true>, dim3(blocks), dim3(256), 0, stream, tab);
+      st << launch_kernel(dequant_t_kernel<true>, dim3(blocks), dim3(256), stream, tab);
     else
-      hipLaunchKernelGGL(dequant_t_kernel<false>, dim3(blocks), dim3(256), 0, stream, tab);
+      st << launch_kernel(dequant_t_kernel<false>, dim3(blocks), dim3(256), stream, tab);
   }
 }
 
@@ -1634,9 +1627,9 @@ static void fill_dw(const BatchCfg& c, const LinearIO* io, uint8_t* ws, const Bw
 
 // dW into dW (one split) or into the workspace partials (several).
 static void prep_dw(const BatchCfg& c, const LinearIO* io, uint8_t* ws, const BwdPlan& P,
-                    hipStream_t stream, Group<EpiPartial>& grp) {
+                    hipStream_t stream, Group<EpiPartial>& grp, LaunchStatus& st) {
   int first[kMaxBatch];
-  prep_xt(c, io, ws, P, stream, first);
+  prep_xt(c, io, ws, P, stream, first, st);
   fill_dw(c, io, ws, P, first, grp, [&](int l) {
     const int64_t I = io[l].d_out, J = io[l].d_in;
     float* target = P.splits > 1 ? reinterpret_cast<float*>(ws + P.part_off[l]) : io[l].dW;
@@ -1648,6 +1641,7 @@ static void prep_dw(const BatchCfg& c, const LinearIO* io, uint8_t* ws, const Bw
 static hipError_t reduce_dw(const BatchCfg& c, const LinearIO* io, uint8_t* ws, const BwdPlan& P,
                             hipStream_t stream) {
   if (P.splits == 1) return hipSuccess;
+  LaunchStatus st;
   RedTab red{};
   red.n = c.n;
   red.splits = (int32_t)P.splits;
@@ -1660,18 +1654,18 @@ static hipError_t reduce_dw(const BatchCfg& c, const LinearIO* io, uint8_t* ws, 
     blocks += (int32_t)((red.n4[l] + 255) / 256);
   }
   red.b0[c.n] = blocks;
-  hipLaunchKernelGGL(split_reduce_batch_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, red);
-  return hipGetLastError();
+  st << launch_kernel(split_reduce_batch_kernel, dim3((unsigned)blocks), dim3(256), stream, red);
+  return st.e;
 }
 
 hipError_t launch_dw_batch(const BatchCfg& c, const LinearIO* io, uint8_t* ws, const BwdPlan& P,
                            hipStream_t stream) {
   if (c.n == 0) return hipSuccess;
   Group<EpiPartial> grp{};
-  prep_dw(c, io, ws, P, stream, grp);
-  launch_group<EBF16, KM, KC, KB_BWD>(grp, ws, stream);
-  const hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  LaunchStatus st;
+  prep_dw(c, io, ws, P, stream, grp, st);
+  st << launch_group<EBF16, KM, KC, KB_BWD>(grp, ws, stream);
+  if (st.e != hipSuccess) return st.e;
   return reduce_dw(c, io, ws, P, stream);
 }
 
@@ -1689,11 +1683,11 @@ hipError_t launch_dxdw_batch(const BatchCfg& c, const LinearIO* io, uint8_t* ws,
   Group<EpiPartial> gw{};
   BwdPlan Q = P;
   Q.splits = P.splits_dual;
-  prep_dx(c, io, ws, Q, stream, gx);
-  prep_dw(c, io, ws, Q, stream, gw);
-  launch_dual<EBF16, KM, KC, KB_BWD, EpiPartial, EBF16, KC, KC, KB_BWD, EpiScale>(gw, gx, ws, stream);
-  const hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  LaunchStatus st;
+  prep_dx(c, io, ws, Q, stream, gx, st);
+  prep_dw(c, io, ws, Q, stream, gw, st);
+  st << launch_dual<EBF16, KM, KC, KB_BWD, EpiPartial, EBF16, KC, KC, KB_BWD, EpiScale>(gw, gx, ws, stream);
+  if (st.e != hipSuccess) return st.e;
   return reduce_dw(c, io, ws, Q, stream);
 }
 
@@ -1701,6 +1695,7 @@ hipError_t launch_dxdw_batch(const BatchCfg& c, const LinearIO* io, uint8_t* ws,
 static hipError_t reduce_sr(const BatchCfg& c, const LinearIO* io, const SRTensor* t, uint64_t seed,
                             uint32_t step, unsigned long long* counters, uint8_t* ws,
                             const BwdPlan& P, hipStream_t stream) {
+  LaunchStatus st;
   RedSRTab red{};
   red.n = c.n;
   red.splits = (int32_t)P.splits;
@@ -1723,19 +1718,19 @@ static hipError_t reduce_sr(const BatchCfg& c, const LinearIO* io, const SRTenso
   }
   red.b0[c.n] = blocks;
   if (c.w_ternary)
-    hipLaunchKernelGGL(split_reduce_sr_kernel<CF_T2>, dim3((unsigned)blocks), dim3(256), 0, stream, red);
+    st << launch_kernel(split_reduce_sr_kernel<CF_T2>, dim3((unsigned)blocks), dim3(256), stream, red);
   else if (c.w_int4)
-    hipLaunchKernelGGL(split_reduce_sr_kernel<CF_I4>, dim3((unsigned)blocks), dim3(256), 0, stream, red);
+    st << launch_kernel(split_reduce_sr_kernel<CF_I4>, dim3((unsigned)blocks), dim3(256), stream, red);
   else
-    hipLaunchKernelGGL(split_reduce_sr_kernel<CF_I8>, dim3((unsigned)blocks), dim3(256), 0, stream, red);
-  return hipGetLastError();
+    st << launch_kernel(split_reduce_sr_kernel<CF_I8>, dim3((unsigned)blocks), dim3(256), stream, red);
+  return st.e;
 }
 
 // dW of every linear consumed by the SR update of its codes in the GEMM
 // epilogue (one split) or in the reduction of the partials (several), with
 // dX of every linear in the same launch when with_dx.
 template <int CF>
-static void launch_dw_sr_group(const BatchCfg& c, const LinearIO* io, const SRTensor* t, uint64_t seed,
+static hipError_t launch_dw_sr_group(const BatchCfg& c, const LinearIO* io, const SRTensor* t, uint64_t seed,
                                uint32_t step, unsigned long long* counters, uint8_t* ws,
                                const BwdPlan& P, const int* first, Group<EpiScale>* gx,
                                hipStream_t stream) {
@@ -1757,9 +1752,8 @@ static void launch_dw_sr_group(const BatchCfg& c, const LinearIO* io, const SRTe
     return e;
   });
   if (gx != nullptr)
-    launch_dual<EBF16, KM, KC, KB_BWD, EpiSR<CF>, EBF16, KC, KC, KB_BWD, EpiScale>(gw, *gx, ws, stream);
-  else
-    launch_group<EBF16, KM, KC, KB_BWD, EpiSR<CF>>(gw, ws, stream);
+    return launch_dual<EBF16, KM, KC, KB_BWD, EpiSR<CF>, EBF16, KC, KC, KB_BWD, EpiScale>(gw, *gx, ws, stream);
+  return launch_group<EBF16, KM, KC, KB_BWD, EpiSR<CF>>(gw, ws, stream);
 }
 
 hipError_t launch_bwd_sr_batch(const BatchCfg& c, const LinearIO* io, const SRTensor* t, uint64_t seed,
@@ -1774,15 +1768,16 @@ hipError_t launch_bwd_sr_batch(const BatchCfg& c, const LinearIO* io, const SRTe
   BwdPlan Q = P;
   Q.splits = with_dx ? P.splits_dual : P.splits;
   Group<EpiScale> gx{};
-  if (with_dx) prep_dx(c, io, ws, Q, stream, gx);
+  LaunchStatus st;
+  if (with_dx) prep_dx(c, io, ws, Q, stream, gx, st);
   int first[kMaxBatch];
-  prep_xt(c, io, ws, Q, stream, first);
+  prep_xt(c, io, ws, Q, stream, first, st);
   if (Q.splits == 1) {
     Group<EpiScale>* const pgx = with_dx ? &gx : nullptr;
-    if (c.w_ternary) launch_dw_sr_group<CF_T2>(c, io, t, seed, step, counters, ws, Q, first, pgx, stream);
-    else if (c.w_int4) launch_dw_sr_group<CF_I4>(c, io, t, seed, step, counters, ws, Q, first, pgx, stream);
-    else launch_dw_sr_group<CF_I8>(c, io, t, seed, step, counters, ws, Q, first, pgx, stream);
-    return hipGetLastError();
+    if (c.w_ternary) st << launch_dw_sr_group<CF_T2>(c, io, t, seed, step, counters, ws, Q, first, pgx, stream);
+    else if (c.w_int4) st << launch_dw_sr_group<CF_I4>(c, io, t, seed, step, counters, ws, Q, first, pgx, stream);
+    else st << launch_dw_sr_group<CF_I8>(c, io, t, seed, step, counters, ws, Q, first, pgx, stream);
+    return st.e;
   }
   Group<EpiPartial> gw{};
   fill_dw(c, io, ws, Q, first, gw, [&](int l) {
@@ -1790,11 +1785,10 @@ hipError_t launch_bwd_sr_batch(const BatchCfg& c, const LinearIO* io, const SRTe
     return EpiPartial{reinterpret_cast<float*>(ws + Q.part_off[l]), J, I * J};
   });
   if (with_dx)
-    launch_dual<EBF16, KM, KC, KB_BWD, EpiPartial, EBF16, KC, KC, KB_BWD, EpiScale>(gw, gx, ws, stream);
+    st << launch_dual<EBF16, KM, KC, KB_BWD, EpiPartial, EBF16, KC, KC, KB_BWD, EpiScale>(gw, gx, ws, stream);
   else
-    launch_group<EBF16, KM, KC, KB_BWD, EpiPartial>(gw, ws, stream);
-  const hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+    st << launch_group<EBF16, KM, KC, KB_BWD, EpiPartial>(gw, ws, stream);
+  if (st.e != hipSuccess) return st.e;
   return reduce_sr(c, io, t, seed, step, counters, ws, Q, stream);
 }
 

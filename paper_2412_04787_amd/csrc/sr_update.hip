@@ -187,19 +187,15 @@ hipError_t launch_sr_update(int cf, int n, const SRTensor* t, uint64_t seed, uin
   tab.b0[n] = tiles;
   if (tiles == 0) return hipSuccess;
   // as many blocks as fit on the device at once; each loops over tiles
-  static const int resident[3] = {
-      occupancy_blocks(reinterpret_cast<const void*>(sr_update_kernel<CF_I8, kCW>), 256),
-      occupancy_blocks(reinterpret_cast<const void*>(sr_update_kernel<CF_T2, kCW>), 256),
-      occupancy_blocks(reinterpret_cast<const void*>(sr_update_kernel<CF_I4, kCW>), 256)};
-  const int64_t cap = resident[cf];
+  const int64_t cap = occupancy_blocks(
+      cf == CF_T2 ? reinterpret_cast<const void*>(sr_update_kernel<CF_T2, kCW>)
+                  : cf == CF_I4 ? reinterpret_cast<const void*>(sr_update_kernel<CF_I4, kCW>)
+                                : reinterpret_cast<const void*>(sr_update_kernel<CF_I8, kCW>),
+      256);
   const unsigned blocks = (unsigned)(tiles < cap ? tiles : cap);
-  if (cf == CF_T2)
-    hipLaunchKernelGGL((sr_update_kernel<CF_T2, kCW>), dim3(blocks), dim3(256), 0, stream, tab, counters);
-  else if (cf == CF_I4)
-    hipLaunchKernelGGL((sr_update_kernel<CF_I4, kCW>), dim3(blocks), dim3(256), 0, stream, tab, counters);
-  else
-    hipLaunchKernelGGL((sr_update_kernel<CF_I8, kCW>), dim3(blocks), dim3(256), 0, stream, tab, counters);
-  return hipGetLastError();
+  if (cf == CF_T2) return launch_kernel(sr_update_kernel<CF_T2, kCW>, dim3(blocks), dim3(256), stream, tab, counters);
+  if (cf == CF_I4) return launch_kernel(sr_update_kernel<CF_I4, kCW>, dim3(blocks), dim3(256), stream, tab, counters);
+  return launch_kernel(sr_update_kernel<CF_I8, kCW>, dim3(blocks), dim3(256), stream, tab, counters);
 }
 
 hipError_t launch_debug_rng(uint64_t seed, uint32_t step, uint32_t tensor_id, uint64_t i0,
@@ -208,9 +204,8 @@ hipError_t launch_debug_rng(uint64_t seed, uint32_t step, uint32_t tensor_id, ui
   const int threads = 256;
   int64_t blocks = (n + threads - 1) / threads;
   if (blocks > 65536) blocks = 65536;
-  hipLaunchKernelGGL(debug_rng_kernel, dim3((unsigned)blocks), dim3(threads), 0, stream, out, i0,
-                     n, (uint32_t)seed, (uint32_t)(seed >> 32), step, tensor_id);
-  return hipGetLastError();
+  return launch_kernel(debug_rng_kernel, dim3((unsigned)blocks), dim3(threads), stream, out, i0, n,
+                       (uint32_t)seed, (uint32_t)(seed >> 32), step, tensor_id);
 }
 
 }  // namespace dqt

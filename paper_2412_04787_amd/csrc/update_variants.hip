@@ -280,23 +280,24 @@ hipError_t launch_update_variant(int cf, int n, const SRTensor* t, int mode, flo
   tab.t0[n] = tiles;
   if (tiles == 0) return hipSuccess;
   SelState* st = static_cast<SelState*>(ws);
+  LaunchStatus ls;
   if (any_sel) {
-    hipLaunchKernelGGL(sel_init_kernel, dim3((unsigned)n), dim3(256), 0, stream, tab, st);
+    ls << launch_kernel(sel_init_kernel, dim3((unsigned)n), dim3(256), stream, tab, st);
     const int shifts[3] = {20, 9, 0}, bins[3] = {2048, 2048, 512};
     for (int p = 0; p < 3; ++p) {
-      hipLaunchKernelGGL(sel_hist_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, tab, st, shifts[p],
-                         bins[p]);
-      hipLaunchKernelGGL(sel_pick_kernel, dim3((unsigned)n), dim3(256), 0, stream, tab, st, shifts[p], bins[p]);
+      ls << launch_kernel(sel_hist_kernel, dim3((unsigned)blocks), dim3(256), stream, tab, st, shifts[p],
+                          bins[p]);
+      ls << launch_kernel(sel_pick_kernel, dim3((unsigned)n), dim3(256), stream, tab, st, shifts[p], bins[p]);
     }
   }
   const unsigned grid = (unsigned)(tiles < 4096 ? tiles : 4096);
   if (cf == CF_T2)
-    hipLaunchKernelGGL(variant_update_kernel<CF_T2>, dim3(grid), dim3(256), 0, stream, tab, st, counters);
+    ls << launch_kernel(variant_update_kernel<CF_T2>, dim3(grid), dim3(256), stream, tab, st, counters);
   else if (cf == CF_I4)
-    hipLaunchKernelGGL(variant_update_kernel<CF_I4>, dim3(grid), dim3(256), 0, stream, tab, st, counters);
+    ls << launch_kernel(variant_update_kernel<CF_I4>, dim3(grid), dim3(256), stream, tab, st, counters);
   else
-    hipLaunchKernelGGL(variant_update_kernel<CF_I8>, dim3(grid), dim3(256), 0, stream, tab, st, counters);
-  return hipGetLastError();
+    ls << launch_kernel(variant_update_kernel<CF_I8>, dim3(grid), dim3(256), stream, tab, st, counters);
+  return ls.e;
 }
 
 }  // namespace dqt

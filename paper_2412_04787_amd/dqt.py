@@ -183,8 +183,8 @@ def dqt_linear_fwd(w: DqtWeight, Wq, X, M: int, act_q: int, Xq, xdq, Y, ws=None,
 
 def workspace(nbytes: int, device="cuda:0"):
     """A zero-filled device buffer of at least nbytes (16-byte aligned), or
-    None for 0.  (The GEMM calls keep tile counters in the first 256 bytes of
-    a workspace; they must start at zero and every call leaves them zero.)"""
+    None for 0.  (The library does not depend on a workspace's contents; the
+    zero fill only makes unused bytes deterministic.)"""
     if nbytes == 0:
         return None
     torch = _torch()

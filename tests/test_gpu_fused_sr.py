@@ -86,6 +86,7 @@ def test_fused_sr_matches_two_calls_and_oracle(lib, ci):
     cnt2 = torch.zeros((2,), dtype=torch.int64, device=DEV)
     cntf = torch.zeros((2,), dtype=torch.int64, device=DEV)
     seed, step = 77, 5
+    wsf.view(torch.uint8).fill_(0xFF)     # a workspace's contents on entry do not matter
     dqt.dqt_linear_bwd_batch(io2, M, a_code, bf, bf, bf, ws2)
     dqt.dqt_sr_update_batch(io2, lr, seed, step, cnt2)
     dqt.dqt_linear_bwd_sr_batch(iof, M, a_code, bf, bf, bf, lr, seed, step, cntf, wsf)

@@ -91,6 +91,8 @@ def _run_case(name, with_dx, full_oracle):
     io2, iof = dqt.linear_io(two), dqt.linear_io(fused)
     ws = dqt.workspace(max(dqt.dqt_linear_bwd_batch_workspace(io2, M),
                            dqt.dqt_linear_bwd_batch_workspace(iof, M)))
+    # the workspace's contents on entry do not matter (tile counters included)
+    ws.view(torch.uint8).fill_(0xA5)
     cnt2 = torch.zeros((2,), dtype=torch.int64, device=DEV)
     cntf = torch.zeros((2,), dtype=torch.int64, device=DEV)
     lr = wl.lr
@@ -98,8 +100,6 @@ def _run_case(name, with_dx, full_oracle):
     dqt.dqt_sr_update_batch(io2, lr, SEED, STEP, cnt2)
     dqt.dqt_linear_bwd_sr_batch(iof, M, act, bf, bf, bf, lr, SEED, STEP, cntf, ws)
     torch.cuda.synchronize()
-    # the workspace's tile counters are left at zero by every call
-    assert int(torch.count_nonzero(ws.view(torch.uint8)[:256]).item()) == 0
     assert torch.equal(cnt2, cntf), (cnt2.tolist(), cntf.tolist())
     log(f"  counters {cntf.tolist()}")
     rng = np.random.default_rng(5)
