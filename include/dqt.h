@@ -17,8 +17,9 @@
  * Conventions for every entry point:
  *  - Tensor pointers are DEVICE pointers unless marked "host".  The caller
  *    owns every buffer; the library never allocates or frees memory on these
- *    calls and holds no mutable global state, so calls on different streams
- *    or devices may run concurrently (as long as their buffers differ).
+ *    calls and holds no mutable global state (except the static scratch of
+ *    dqt_linear_fwd_batch_noalloc), so calls on different streams or devices
+ *    may run concurrently (as long as their buffers differ).
  *  - Layouts are row-major.  W is [d_out, d_in] (nn.Linear); X is [M, d_in];
  *    Y and dY are [M, d_out].  M is the number of tokens.
  *  - `stream` is a hipStream_t (NULL = the legacy default stream).  Every
@@ -236,6 +237,28 @@ size_t dqt_linear_fwd_batch_workspace(int32_t n, const dqt_linear_io* io);
 dqt_status dqt_linear_fwd_batch(int32_t n, const dqt_linear_io* io, int64_t M,
                                 int32_t act_q, int32_t y_t,
                                 void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * The forward of n linears (dqt_linear_fwd_batch) without a workspace
+ * argument, for callers that cannot allocate device memory: code under HIP
+ * graph capture, tight serving loops, harnesses that forbid allocation.  The
+ * call allocates nothing: its scratch (the tile counters, plus the operand
+ * bytes of dqt_linear_fwd_batch_workspace() for 4-bit codes or ternary rows
+ * whose d_in is not a multiple of 64) is a static device array of
+ * DQT_NOALLOC_SCRATCH_BYTES that each GPU the library runs on holds until
+ * the process ends; its address is looked up on a device's first call.
+ * Calls on one GPU share that array, so calls that overlap in time on one
+ * GPU (different streams, or threads without ordering) race and must not be
+ * made; the counters are cleared by every call on its stream.
+ *   Arguments and results: those of dqt_linear_fwd_batch.
+ *   Errors: those of dqt_linear_fwd_batch; DQT_ERR_WORKSPACE when the batch
+ *   needs more than DQT_NOALLOC_SCRATCH_BYTES of scratch (nothing is
+ *   launched); DQT_ERR_HIP when the array's address cannot be found.
+ */
+#define DQT_NOALLOC_SCRATCH_BYTES (32u << 20)
+
+dqt_status dqt_linear_fwd_batch_noalloc(int32_t n, const dqt_linear_io* io, int64_t M,
+                                        int32_t act_q, int32_t y_t, void* stream);
 
 /* Workspace bytes of dqt_linear_bwd_batch; depends only on the descriptors'
  * shapes and M. */

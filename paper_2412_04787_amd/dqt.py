@@ -24,6 +24,7 @@ EXPORTS = (
     "dqt_act_quant", "dqt_act_quant_batch", "dqt_linear_fwd_workspace", "dqt_linear_fwd", "dqt_linear_bwd_workspace",
     "dqt_linear_bwd", "dqt_linear_fwd_batch_workspace", "dqt_linear_fwd_batch",
     "dqt_linear_bwd_batch_workspace", "dqt_linear_bwd_batch", "dqt_linear_bwd_sr_batch",
+    "dqt_linear_fwd_batch_noalloc",
     "dqt_sr_update_batch", "dqt_adamw_sr_update", "dqt_adamw_sr_update_batch",
     "dqt_update_variant_workspace", "dqt_update_variant_batch",
     "dqt_sr_update", "dqt_debug_rng", "dqt_absmean_init", "dqt_pack_ternary",
@@ -84,6 +85,7 @@ _SIGS = {
     "dqt_sr_update": (_i32, [_wp, _vp, _vp, _f32, _u64, _u32, _vp, _vp]),
     "dqt_linear_fwd_batch_workspace": (ctypes.c_size_t, [_i32, _vp]),
     "dqt_linear_fwd_batch": (_i32, [_i32, _vp, _i64, _i32, _i32, _vp, ctypes.c_size_t, _vp]),
+    "dqt_linear_fwd_batch_noalloc": (_i32, [_i32, _vp, _i64, _i32, _i32, _vp]),
     "dqt_linear_bwd_batch_workspace": (ctypes.c_size_t, [_i32, _vp, _i64]),
     "dqt_linear_bwd_batch": (_i32, [_i32, _vp, _i64, _i32, _i32, _i32, _i32, _vp,
                                     ctypes.c_size_t, _vp]),
@@ -265,6 +267,16 @@ def dqt_linear_fwd_batch(io, M: int, act_q: int, y_t: int, ws=None, stream=None)
     ws_bytes = 0 if ws is None else ws.numel() * ws.element_size()
     _check("dqt_linear_fwd_batch", load().dqt_linear_fwd_batch(len(io), io, M, act_q, y_t, _ptr(ws),
                                                                ws_bytes, _stream(stream)))
+
+
+NOALLOC_SCRATCH_BYTES = 32 << 20
+
+
+def dqt_linear_fwd_batch_noalloc(io, M: int, act_q: int, y_t: int, stream=None):
+    """dqt_linear_fwd_batch with the library's static per-GPU scratch instead
+    of a workspace (the call allocates nothing)."""
+    _check("dqt_linear_fwd_batch_noalloc",
+           load().dqt_linear_fwd_batch_noalloc(len(io), io, M, act_q, y_t, _stream(stream)))
 
 
 def dqt_linear_bwd_batch_workspace(io, M: int) -> int:
