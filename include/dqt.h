@@ -293,6 +293,40 @@ dqt_status dqt_sr_update_batch(int32_t n, const dqt_linear_io* io, float lr,
                                unsigned long long* counters, void* stream);
 
 /*
+ * Direct SR update of any number of weight tensors in one launch (Sec. 3.2:
+ * Eq. 5 is applied to every weight matrix of the model at every step), with
+ * the per-tensor fractions of changed weights of Sec. 5.2 counted in the
+ * same pass.  The tensors are described by a table in device memory:
+ *   dqt_sr_table_bytes(n):  bytes of the table of n tensors (64 per tensor).
+ *   dqt_sr_table_build (host): validates entries io[0 .. n-1] (w, Wq, dW;
+ *          one code format; the checks of dqt_sr_update_batch) and writes
+ *          the table into the host buffer `table` of table_bytes bytes.  The
+ *          caller copies it to device memory; the copy stays valid for as
+ *          long as the descriptors and the Wq / dW addresses do not change,
+ *          so it is built once and reused every step.
+ *   dqt_sr_update_table: the update of every tensor of io (checked again,
+ *          as by dqt_sr_table_build), reading the tensors from `table`, the
+ *          device copy of dqt_sr_table_build(n, io); results are those of
+ *          dqt_sr_update on each tensor with its own tensor_id (the step size
+ *          fl(lr / alpha) is formed on the device by the same correctly
+ *          rounded fp32 division).
+ *          counters: NULL, or device uint64[2] (changed, non-finite; ADDED).
+ *          per_tensor: NULL, or device uint64[2 n]; entry 2 s (2 s + 1)
+ *          receives the changed (non-finite) count of tensor s (ADDED).
+ *   Errors: DQT_ERR_SHAPE (n < 1), DQT_ERR_NULL, DQT_ERR_ALIGN (16 bytes
+ *   for the table, 8 for the counters), DQT_ERR_WORKSPACE (host buffer too
+ *   small), DQT_ERR_UNSUPPORTED (mixed code formats), DQT_ERR_RANGE, and
+ *   the weight checks of dqt_sr_update.
+ */
+size_t dqt_sr_table_bytes(int32_t n);
+dqt_status dqt_sr_table_build(int32_t n, const dqt_linear_io* io, void* table,
+                              size_t table_bytes);
+dqt_status dqt_sr_update_table(int32_t n, const dqt_linear_io* io, const void* table,
+                               float lr, uint64_t seed, uint32_t step,
+                               unsigned long long* counters,
+                               unsigned long long* per_tensor, void* stream);
+
+/*
  * Analysis variants of the direct update (Sec. 5).  The paper contrasts SR
  * with a deterministic rounding that drops small updates, and intervenes in
  * the smallest 20 % of each step's updates, keeping those codes or forcing

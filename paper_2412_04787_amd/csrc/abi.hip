@@ -468,6 +468,74 @@ dqt_status dqt_sr_update_batch(int32_t n, const dqt_linear_io* io, float lr, uin
                                         static_cast<hipStream_t>(stream)));
 }
 
+// ---------------------------------------------------------- update tables
+
+namespace {
+
+// Checks of one update-table batch (any n, one code format).  Returns the
+// launch's tile count in *tiles; writes the table entries when `out` is
+// given.
+dqt_status check_table(int32_t n, const dqt_linear_io* io, float lr, int32_t* wfmt, int64_t* tiles,
+                       dqt::SRTableEntry* out) {
+  if (n < 1) return DQT_ERR_SHAPE;
+  if (io == nullptr) return DQT_ERR_NULL;
+  if (!(isfinite(lr) && lr >= 0.0f)) return DQT_ERR_RANGE;
+  *tiles = 0;
+  for (int l = 0; l < n; ++l) {
+    const dqt_status st = check_weight(io[l].w);
+    if (st != DQT_OK) return st;
+    if (l == 0) *wfmt = io[l].w->wfmt;
+    else if (io[l].w->wfmt != *wfmt) return DQT_ERR_UNSUPPORTED;
+    if (io[l].Wq == nullptr || io[l].dW == nullptr) return DQT_ERR_NULL;
+    if (!aligned16(io[l].Wq) || !aligned16(io[l].dW)) return DQT_ERR_ALIGN;
+    if (!isfinite(lr / io[l].w->alpha)) return DQT_ERR_RANGE;   // the step in grid units
+    dqt::SRTensor t;
+    t.wq = static_cast<uint8_t*>(io[l].Wq);
+    t.grad = io[l].dW;
+    t.nweights = (int64_t)io[l].w->d_out * (int64_t)io[l].w->d_in;
+    t.c = 0.0f;
+    t.qmin = io[l].w->qmin;
+    t.qmax = io[l].w->qmax;
+    t.tensor_id = io[l].w->tensor_id;
+    t.alpha = io[l].w->alpha;
+    if (out != nullptr) dqt::sr_table_entry(t, *tiles, &out[l]);
+    *tiles += dqt::sr_tiles(t.nweights);
+  }
+  return DQT_OK;
+}
+
+}  // namespace
+
+size_t dqt_sr_table_bytes(int32_t n) {
+  return n < 1 ? 0 : (size_t)n * sizeof(dqt::SRTableEntry);
+}
+
+dqt_status dqt_sr_table_build(int32_t n, const dqt_linear_io* io, void* table, size_t table_bytes) {
+  if (n < 1) return DQT_ERR_SHAPE;
+  if (table == nullptr) return DQT_ERR_NULL;
+  if (table_bytes < dqt_sr_table_bytes(n)) return DQT_ERR_WORKSPACE;
+  int32_t wfmt;
+  int64_t tiles;
+  return check_table(n, io, 0.0f, &wfmt, &tiles, static_cast<dqt::SRTableEntry*>(table));
+}
+
+dqt_status dqt_sr_update_table(int32_t n, const dqt_linear_io* io, const void* table, float lr,
+                               uint64_t seed, uint32_t step, unsigned long long* counters,
+                               unsigned long long* per_tensor, void* stream) {
+  int32_t wfmt;
+  int64_t tiles;
+  const dqt_status st = check_table(n, io, lr, &wfmt, &tiles, nullptr);
+  if (st != DQT_OK) return st;
+  if (table == nullptr) return DQT_ERR_NULL;
+  if (!aligned16(table)) return DQT_ERR_ALIGN;
+  if (counters != nullptr && (reinterpret_cast<uintptr_t>(counters) & 7u) != 0) return DQT_ERR_ALIGN;
+  if (per_tensor != nullptr && (reinterpret_cast<uintptr_t>(per_tensor) & 7u) != 0) return DQT_ERR_ALIGN;
+  return from_hip(dqt::launch_sr_update_table(code_format(wfmt), n, tiles,
+                                              static_cast<const dqt::SRTableEntry*>(table), lr, seed,
+                                              step, counters, per_tensor,
+                                              static_cast<hipStream_t>(stream)));
+}
+
 // ---------------------------------------------------------- single linears
 
 size_t dqt_linear_fwd_workspace(const dqt_weight* w) {

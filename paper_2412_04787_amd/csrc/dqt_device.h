@@ -87,6 +87,40 @@ __device__ __forceinline__ float code_to_f32(uint32_t code) {
   return (float)((int)code - 1);
 }
 
+// ---------------------------------------------------------------- LDS DMA
+using lds_u8 = __attribute__((address_space(3))) uint8_t;
+// One direct-to-LDS load per lane (global_load_lds_dwordx4: 16 bytes, or
+// global_load_lds_dword: 4 bytes); the wave's chunks land at consecutive
+// positions from the wave-uniform LDS address l (passed in M0).  Issued as
+// inline asm so that the compiler, which cannot tell which LDS bytes the
+// DMA writes, does not wait for all outstanding DMA before every later LDS
+// access; callers wait for their DMA explicitly (vmcnt) before a barrier
+// publishes it.  Nothing else in these kernels uses M0.
+__device__ __forceinline__ void dma16(const uint8_t* g, lds_u8* l) {
+  const uint32_t m0 = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)l);
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" : : "v"(g), "s"(m0) : "memory");
+}
+__device__ __forceinline__ void dma4(const uint8_t* g, lds_u8* l) {
+  const uint32_t m0 = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)l);
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dword %0, off" : : "v"(g), "s"(m0) : "memory");
+}
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+// wait until at most n (wave-uniform, 0 <= n <= N) vector memory operations
+// of this wave are outstanding
+template <int N>
+__device__ __forceinline__ void wait_vm_le(int n) {
+  if constexpr (N == 0) {
+    wait_vm<0>();
+  } else {
+    if (n >= N) wait_vm<N>();
+    else wait_vm_le<N - 1>(n);
+  }
+}
+
 // ---------------------------------------------------------------- waves
 __device__ __forceinline__ float wave_max(float v) {
 #pragma unroll

@@ -139,10 +139,32 @@ struct SRTensor {
   float c;              // fl32(lr / alpha)
   int qmin, qmax;
   uint32_t tensor_id;
+  float alpha;
 };
 // cf: code format, 0 int8, 1 ternary 2-bit, 2 int4 nibbles
 hipError_t launch_sr_update(int cf, int n, const SRTensor* t, uint64_t seed, uint32_t step,
                             unsigned long long* counters, hipStream_t stream);
+// One tensor of a device-resident update table (dqt_sr_table_build's
+// entries, 64 bytes each).
+struct SRTableEntry {
+  uint64_t wq;          // codes (device address)
+  uint64_t grad;        // dW (device address)
+  int64_t nchunks;      // weights / 8
+  int64_t tile0;        // first tile (256 chunks) of this tensor in the launch
+  float alpha;
+  int32_t qmin, qmax;
+  uint32_t tensor_id;
+  uint32_t reserved[4];
+};
+static_assert(sizeof(SRTableEntry) == 64, "table entry layout");
+// the entry of tensor t whose first tile is tile0, and a tensor's tile count
+void sr_table_entry(const SRTensor& t, int64_t tile0, SRTableEntry* e);
+int64_t sr_tiles(int64_t nweights);
+// Any number of tensors of one code format in one launch; per_tensor
+// (nullable) receives each tensor's changed / non-finite counts.
+hipError_t launch_sr_update_table(int cf, int n, int64_t tiles, const SRTableEntry* table, float lr,
+                                  uint64_t seed, uint32_t step, unsigned long long* counters,
+                                  unsigned long long* per_tensor, hipStream_t stream);
 // Analysis variants of the update (mode 0 plain SR, 1 nearest, 2 force to
 // remain, 3 force to update the bottom `frac` of |delta|).
 size_t update_variant_workspace(int n);

@@ -44,7 +44,6 @@
 namespace dqt {
 namespace v3 {
 
-using lds_u8 = __attribute__((address_space(3))) uint8_t;
 typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
 
 #ifndef GEMM_NW
@@ -128,12 +127,6 @@ __device__ __forceinline__ u32x2 tr_read(const lds_u8* base, int off) {
 __device__ __forceinline__ i32x4 join(u32x2 lo, u32x2 hi) {
   return i32x4{(int)lo[0], (int)lo[1], (int)hi[0], (int)hi[1]};
 }
-// One direct-to-LDS load of 16 bytes per lane; the wave's 64 chunks land at
-// l, l + 16, ... (l is wave-uniform, passed in M0).  Issued as inline asm so
-// that the compiler, which cannot tell which LDS bytes the DMA writes, does
-// not wait for all outstanding DMA before every later LDS access; the
-// kernel waits for its DMA explicitly (vmcnt) before the barrier that
-// publishes a stage.  Nothing else in these kernels uses M0.
 // 16 packed ternary codes (code q + 1 at bits 2k, 2k+1) -> 16 operand bytes
 // in k order, via the byte lookup `lut` (code 0, 1, 2 -> lut bytes 0, 1, 2):
 // split the four codes of every byte into four byte planes, transpose the
@@ -147,26 +140,6 @@ __device__ __forceinline__ i32x4 expand16(uint32_t x, uint32_t lut) {
   const uint32_t d2 = __builtin_amdgcn_perm(ghh, efh, 0x05040100u), d3 = __builtin_amdgcn_perm(ghh, efh, 0x07060302u);
   return i32x4{(int)__builtin_amdgcn_perm(0u, lut, d0), (int)__builtin_amdgcn_perm(0u, lut, d1),
                (int)__builtin_amdgcn_perm(0u, lut, d2), (int)__builtin_amdgcn_perm(0u, lut, d3)};
-}
-__device__ __forceinline__ void dma16(const uint8_t* g, lds_u8* l) {
-  const uint32_t m0 = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)l);
-  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" : : "v"(g), "s"(m0) : "memory");
-}
-template <int N>
-__device__ __forceinline__ void wait_vm() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
-}
-// wait until at most n (wave-uniform, 0 <= n <= N) vector memory operations
-// of this wave are outstanding
-template <int N>
-__device__ __forceinline__ void wait_vm_le(int n) {
-  if constexpr (N == 0) {
-    wait_vm<0>();
-  } else {
-    if (n >= N) wait_vm<N>();
-    else wait_vm_le<N - 1>(n);
-  }
 }
 // Barrier that keeps the compiler from moving memory accesses across it; it
 // waits for this wave's LDS accesses but not for outstanding DMA.

@@ -156,7 +156,7 @@ struct CodeFmt {
       n = __builtin_popcount((x | (x >> 1)) & 0x55555555u);
     } else if constexpr (CF == CF_I4) {
 #pragma unroll
-      for (int w = 0; w < CW / 8; ++w) {
+      for (int w = 0; w < (CW + 7) / 8; ++w) {   // (fields past CW weights are zero in both)
         const uint32_t x = a[w] ^ b[w];
         n += __builtin_popcount((x | (x >> 1) | (x >> 2) | (x >> 3)) & 0x11111111u);
       }

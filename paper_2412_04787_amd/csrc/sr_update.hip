@@ -11,126 +11,194 @@
 
 namespace dqt {
 
-constexpr int kMaxSR = kMaxBatch;
-constexpr int kChunksPerTile = 256;   // one chunk of weights per thread
-// Up to kMaxSR tensors in one launch; tensor s owns the tiles [b0[s], b0[s+1])
-// of 256 chunks each (its last tile may be partial).
-struct SRTab {
-  uint8_t* wq[kMaxSR];
-  const float* grad[kMaxSR];
-  int64_t nchunks[kMaxSR];
-  float c[kMaxSR], L[kMaxSR];
-  int qmin[kMaxSR], qmax[kMaxSR];
-  uint32_t tid[kMaxSR];
-  int64_t b0[kMaxSR + 1];
-  int32_t n;
-  uint32_t k0, k1, step;
+constexpr int kChunksPerTile = 256;   // one chunk of 8 weights per thread
+constexpr int kCW = 8;                // weights per chunk (one Philox block)
+
+// One tensor of an update launch: codes, gradient, its chunks of 8 weights
+// and the first tile (256 chunks) it owns in the launch's tile order.
+struct SRDesc {
+  uint8_t* wq;
+  const float* grad;
+  int64_t nchunks;
+  int64_t tile0;
+  float c, L;           // fl32(lr / alpha); |delta| clamp qmax - qmin + 1
+  int qmin, qmax;
+  uint32_t tid;
 };
 
-// Code words of CW weights in format CF: 2-bit ternary codes (CW / 4
-// bytes, in w[0]), nibbles (CW / 2 bytes) or int8 codes (CW bytes).
-template <int CF, int CW>
+// Tensors passed in the kernel arguments (up to kMaxBatch).
+struct SRArgTab {
+  static constexpr bool kStrided = true;
+  SRDesc d[kMaxBatch];
+  int32_t n;
+  __device__ SRDesc get(int s) const { return d[s]; }
+};
+// Tensors described by a table in device memory (any number), built on the
+// host by dqt_sr_table_build; the step size is formed per tensor from lr
+// and alpha as one correctly rounded fp32 division.
+struct SRDevTab {
+  static constexpr bool kStrided = false;
+  const SRTableEntry* e;
+  int32_t n;
+  float lr;
+  __device__ SRDesc get(int s) const {
+    // read through the constant address space: wave-uniform scalar loads,
+    // which do not count against the vector memory counter that paces the
+    // DMA pipeline
+    const auto* ce = reinterpret_cast<const __attribute__((address_space(4))) SRTableEntry*>(
+        (const __attribute__((address_space(4))) void*)e);
+    const auto& t = ce[s];
+    SRDesc d;
+    d.wq = reinterpret_cast<uint8_t*>(t.wq);
+    d.grad = reinterpret_cast<const float*>(t.grad);
+    d.nchunks = t.nchunks;
+    d.tile0 = t.tile0;
+    d.c = __fdiv_rn(lr, t.alpha);
+    d.L = (float)(t.qmax - t.qmin + 1);
+    d.qmin = t.qmin;
+    d.qmax = t.qmax;
+    d.tid = t.tensor_id;
+    return d;
+  }
+};
+
+// Code words of one chunk of 8 weights in format CF: 2-bit ternary codes
+// (2 bytes), nibbles (4 bytes) or int8 codes (8 bytes).
+template <int CF>
 struct CodeIO {
-  static constexpr int NBYTES = CF == CF_T2 ? CW / 4 : CF == CF_I4 ? CW / 2 : CW;
-  static constexpr int NWORD = NBYTES >= 4 ? NBYTES / 4 : 1;
-  __device__ static void load(const uint8_t* wq, int64_t t, uint32_t (&w)[4]) {
+  static constexpr int NBYTES = CF == CF_T2 ? 2 : CF == CF_I4 ? 4 : 8;
+  __device__ static void load(const uint8_t* wq, int64_t t, uint32_t (&w)[2]) {
     if constexpr (NBYTES == 2) {
       w[0] = reinterpret_cast<const uint16_t*>(wq)[t];
     } else if constexpr (NBYTES == 4) {
       w[0] = reinterpret_cast<const uint32_t*>(wq)[t];
-    } else if constexpr (NBYTES == 8) {
-      const uint2 v = reinterpret_cast<const uint2*>(wq)[t];
-      w[0] = v.x; w[1] = v.y;
     } else {
-      const uint4 v = reinterpret_cast<const uint4*>(wq)[t];
-      w[0] = v.x; w[1] = v.y; w[2] = v.z; w[3] = v.w;
+      const uint2 v = reinterpret_cast<const uint2*>(wq)[t];
+      w[0] = v.x;
+      w[1] = v.y;
     }
   }
   __device__ static void store(uint8_t* wq, int64_t t, const uint32_t (&w)[4]) {
     if constexpr (NBYTES == 2) reinterpret_cast<uint16_t*>(wq)[t] = (uint16_t)w[0];
     else if constexpr (NBYTES == 4) reinterpret_cast<uint32_t*>(wq)[t] = w[0];
-    else if constexpr (NBYTES == 8) reinterpret_cast<uint2*>(wq)[t] = make_uint2(w[0], w[1]);
-    else reinterpret_cast<uint4*>(wq)[t] = make_uint4(w[0], w[1], w[2], w[3]);
+    else reinterpret_cast<uint2*>(wq)[t] = make_uint2(w[0], w[1]);
   }
 };
 
-// Persistent kernel: block b takes tiles b, b + grid, ...; thread t of a tile
-// owns chunk t of CW consecutive weights (4 CW bytes of gradient, CW / 4 or
-// CW bytes of codes, so no two lanes touch the same byte).  The change and
-// non-finite counts are reduced per block and added with one atomic each.
-template <int CF, int CW>
-__global__ __launch_bounds__(256) void sr_update_kernel(const SRTab tab,
-                                                        unsigned long long* __restrict__ counters) {
-  static_assert(CW == 8 || CW == 16, "8 or 16 weights per lane");
-  using CIO = CodeIO<CF, CW>;
-  constexpr int NG = CW / 4;               // gradient f32x4 per chunk
-  constexpr int NB = CW / 8;               // Philox blocks per chunk
-  __shared__ unsigned long long red[2][256 / kWave];
-  unsigned long long changed = 0, nonfin = 0;
-  const int64_t ntiles = tab.b0[tab.n];
-  // Software pipeline: the next tile's gradient and codes are requested
-  // before the current tile is computed, so loads stay in flight meanwhile.
-  int sidx = 0;
-  f32x4 ng[NG];
-  uint32_t nw[4];
-  int64_t nt = 0;
-  int ns = 0;
-  auto fetch = [&](int64_t tl) {
-    while (sidx + 1 < tab.n && tl >= tab.b0[sidx + 1]) ++sidx;   // tiles ascend
-    ns = sidx;
-    nt = (tl - tab.b0[sidx]) * kChunksPerTile + threadIdx.x;
-    if (nt < tab.nchunks[sidx]) {
-      const f32x4* gp = reinterpret_cast<const f32x4*>(tab.grad[sidx] + nt * CW);
+// Sum of a per-lane count over the block (every thread gets it; the block
+// runs this in uniform control flow).  `red` holds one slot per wave.
+__device__ __forceinline__ uint32_t block_sum(uint32_t v, uint32_t* red) {
+  v = wave_sum_u32(v);
+  __syncthreads();                         // earlier readers of `red` are done
+  if ((threadIdx.x & (kWave - 1)) == 0) red[threadIdx.x / kWave] = v;
+  __syncthreads();
+  uint32_t t = 0;
 #pragma unroll
-      for (int u = 0; u < NG; ++u) ng[u] = __builtin_nontemporal_load(gp + u);
-      CIO::load(tab.wq[sidx], nt, nw);
+  for (int w = 0; w < 256 / kWave; ++w) t += red[w];
+  return t;
+}
+
+// Persistent streaming kernel.  Thread t of a tile owns chunk t: 32 bytes
+// of gradient and whole bytes of codes, so no two lanes touch the same byte.
+// The next tile's gradient and codes are loaded before the current tile is
+// updated.  Counts are kept per lane; the per-tensor counts are summed over
+// the block whenever the tensor changes, the totals once at the end.  (The update is bound by its vector
+// instructions -- about 176 per 8 weights, 40 of them Philox -- more than by
+// memory: the loads alone stream at about 6.3 TB/s.)
+template <int CF, class Tab>
+__global__ __launch_bounds__(256) void sr_update_kernel(const Tab tab, int64_t ntiles, uint32_t k0,
+                                                        uint32_t k1, uint32_t step,
+                                                        unsigned long long* __restrict__ counters,
+                                                        unsigned long long* __restrict__ per_tensor) {
+  using CIO = CodeIO<CF>;
+  // tiles b, b + G, ... of the launch (few tensors: the front of loads
+  // sweeps through memory together), or the contiguous range
+  // [b T / G, (b + 1) T / G) (many tensors: a block meets few boundaries)
+  const int64_t t_begin = Tab::kStrided ? (int64_t)blockIdx.x : ntiles * blockIdx.x / gridDim.x;
+  const int64_t t_end = Tab::kStrided ? ntiles : ntiles * (blockIdx.x + 1) / gridDim.x;
+  const int64_t t_inc = Tab::kStrided ? (int64_t)gridDim.x : 1;
+  if (t_begin >= t_end) return;
+  // tensor of the first tile (binary search over the tensors' first tiles)
+  int s0 = 0;
+  {
+    int lo = 0, hi = tab.n - 1;
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (tab.get(mid).tile0 <= t_begin) lo = mid;
+      else hi = mid - 1;
+    }
+    s0 = lo;
+  }
+  SRDesc dn = tab.get(s0);          // tensor of the next tile to load
+  int sn = s0;
+  f32x4 ng[2];
+  uint32_t nw[2] = {0u, 0u};
+  int64_t nt = 0;
+  int ns = s0;
+  auto fetch = [&](int64_t tl) {
+    while (tl >= dn.tile0 + (dn.nchunks + kChunksPerTile - 1) / kChunksPerTile) dn = tab.get(++sn);
+    ns = sn;
+    nt = (tl - dn.tile0) * kChunksPerTile + threadIdx.x;
+    if (nt < dn.nchunks) {
+      const f32x4* gp = reinterpret_cast<const f32x4*>(dn.grad + nt * kCW);
+      ng[0] = __builtin_nontemporal_load(gp);
+      ng[1] = __builtin_nontemporal_load(gp + 1);
+      CIO::load(dn.wq, nt, nw);
     }
   };
-  int64_t tile = blockIdx.x;
-  if (tile < ntiles) fetch(tile);
-  for (; tile < ntiles; tile += gridDim.x) {
+  SRDesc dc = tab.get(s0);          // tensor of the tile being updated
+  int sc = s0;
+  __shared__ uint32_t red[256 / kWave];
+  // counts of the current tensor (per lane), and of the tensors before it
+  uint32_t ch = 0, nf = 0, ch_done = 0, nf_done = 0;
+  // one atomic per block per tensor for the per-tensor counts (tensor
+  // changes are block-uniform: all threads work on the same tile)
+  auto flush_tensor = [&](int s_) {
+    if (per_tensor != nullptr) {
+      const uint32_t c = block_sum(ch, red), f = block_sum(nf, red);
+      if (threadIdx.x == 0) {
+        if (c) atomicAdd(per_tensor + 2 * s_, (unsigned long long)c);
+        if (f) atomicAdd(per_tensor + 2 * s_ + 1, (unsigned long long)f);
+      }
+    }
+    ch_done += ch;
+    nf_done += nf;
+    ch = nf = 0;
+  };
+  fetch(t_begin);
+  for (int64_t tile = t_begin; tile < t_end; tile += t_inc) {
     const int cs = ns;
     const int64_t t = nt;
-    f32x4 gv[NG];
-    uint32_t win[4];
-#pragma unroll
-    for (int u = 0; u < NG; ++u) gv[u] = ng[u];
-#pragma unroll
-    for (int u = 0; u < CIO::NWORD; ++u) win[u] = nw[u];
-    if (tile + gridDim.x < ntiles) fetch(tile + gridDim.x);
-    if (t >= tab.nchunks[cs]) continue;
-    SRArgs a;
-    a.c = tab.c[cs];
-    a.L = tab.L[cs];
-    a.qmin = tab.qmin[cs];
-    a.qmax = tab.qmax[cs];
-    a.k0 = tab.k0;
-    a.k1 = tab.k1;
-    a.step = tab.step;
-    a.tid = tab.tid[cs];
-    uint8_t* __restrict__ wq = tab.wq[cs];
-    uint32_t wout[4];
-    sr_chunk<CF, CW>(win, gv, (uint64_t)t * NB, a, wout, changed, nonfin);
-    CIO::store(wq, t, wout);
-  }
-  if (counters != nullptr) {
-    changed = wave_sum_u64(changed);
-    nonfin = wave_sum_u64(nonfin);
-    const int w = threadIdx.x / kWave;
-    if ((threadIdx.x & (kWave - 1)) == 0) {
-      red[0][w] = changed;
-      red[1][w] = nonfin;
+    const f32x4 gv[2] = {ng[0], ng[1]};
+    const uint32_t win[4] = {nw[0], nw[1], 0u, 0u};
+    if (tile + t_inc < t_end) fetch(tile + t_inc);
+    if (cs != sc) {
+      flush_tensor(sc);
+      sc = cs;
+      dc = tab.get(sc);
     }
-    __syncthreads();
+    if (t >= dc.nchunks) continue;
+    SRArgs a;
+    a.c = dc.c;
+    a.L = dc.L;
+    a.qmin = dc.qmin;
+    a.qmax = dc.qmax;
+    a.k0 = k0;
+    a.k1 = k1;
+    a.step = step;
+    a.tid = dc.tid;
+    uint32_t wout[4];
+    sr_chunk<CF, kCW>(win, gv, (uint64_t)t, a, wout, ch, nf);
+    CIO::store(dc.wq, t, wout);
+  }
+  flush_tensor(sc);
+  // the launch totals: one atomic per block (atomics from every wave on
+  // one address serialise and had held the update far below bandwidth)
+  if (counters != nullptr) {
+    const uint32_t c = block_sum(ch_done, red), f = block_sum(nf_done, red);
     if (threadIdx.x == 0) {
-      unsigned long long c = 0, f = 0;
-#pragma unroll
-      for (int i = 0; i < 256 / kWave; ++i) {
-        c += red[0][i];
-        f += red[1][i];
-      }
-      if (c) atomicAdd(counters + 0, c);
-      if (f) atomicAdd(counters + 1, f);
+      if (c) atomicAdd(counters, (unsigned long long)c);
+      if (f) atomicAdd(counters + 1, (unsigned long long)f);
     }
   }
 }
@@ -150,52 +218,77 @@ __global__ __launch_bounds__(256) void debug_rng_kernel(uint32_t* __restrict__ o
 
 // Blocks of `threads` threads of `fn` resident on the current device at once.
 static int occupancy_blocks(const void* fn, int threads) {
-  int dev = 0, cus = 0, per_cu = 0;
-  if (hipGetDevice(&dev) != hipSuccess ||
-      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
-    cus = 256;
+  int per_cu = 0;
   if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, threads, 0) != hipSuccess || per_cu <= 0)
     per_cu = 4;
-  return cus * per_cu;
+  return current_device_cus() * per_cu;
 }
 
-#ifndef SR_CW
-#define SR_CW 8
-#endif
-constexpr int kCW = SR_CW;   // weights per lane
+template <int CF, class Tab>
+static hipError_t launch_sr_cf(const Tab& tab, int64_t tiles, uint64_t seed, uint32_t step,
+                               unsigned long long* counters, unsigned long long* per_tensor,
+                               hipStream_t stream) {
+  const auto kern = sr_update_kernel<CF, Tab>;
+  const int64_t cap = occupancy_blocks(reinterpret_cast<const void*>(kern), 256);
+  const unsigned blocks = (unsigned)(tiles < cap ? tiles : cap);
+  return launch_kernel(kern, dim3(blocks), dim3(256), stream, tab, tiles, (uint32_t)seed,
+                       (uint32_t)(seed >> 32), step, counters, per_tensor);
+}
+
+template <class Tab>
+static hipError_t launch_sr(int cf, const Tab& tab, int64_t tiles, uint64_t seed, uint32_t step,
+                            unsigned long long* counters, unsigned long long* per_tensor,
+                            hipStream_t stream) {
+  if (tiles == 0) return hipSuccess;
+  if (cf == CF_T2) return launch_sr_cf<CF_T2>(tab, tiles, seed, step, counters, per_tensor, stream);
+  if (cf == CF_I4) return launch_sr_cf<CF_I4>(tab, tiles, seed, step, counters, per_tensor, stream);
+  return launch_sr_cf<CF_I8>(tab, tiles, seed, step, counters, per_tensor, stream);
+}
+
+static int64_t tiles_of(int64_t nweights) {
+  return (nweights / kCW + kChunksPerTile - 1) / kChunksPerTile;
+}
 
 hipError_t launch_sr_update(int cf, int n, const SRTensor* t, uint64_t seed, uint32_t step,
                             unsigned long long* counters, hipStream_t stream) {
-  SRTab tab{};
+  SRArgTab tab{};
   tab.n = n;
-  tab.k0 = (uint32_t)seed;
-  tab.k1 = (uint32_t)(seed >> 32);
-  tab.step = step;
   int64_t tiles = 0;
   for (int s = 0; s < n; ++s) {
-    tab.wq[s] = t[s].wq;
-    tab.grad[s] = t[s].grad;
-    tab.nchunks[s] = t[s].nweights / kCW;
-    tab.c[s] = t[s].c;
-    tab.L[s] = (float)(t[s].qmax - t[s].qmin + 1);
-    tab.qmin[s] = t[s].qmin;
-    tab.qmax[s] = t[s].qmax;
-    tab.tid[s] = t[s].tensor_id;
-    tab.b0[s] = tiles;
-    tiles += (tab.nchunks[s] + kChunksPerTile - 1) / kChunksPerTile;
+    SRDesc& d = tab.d[s];
+    d.wq = t[s].wq;
+    d.grad = t[s].grad;
+    d.nchunks = t[s].nweights / kCW;
+    d.tile0 = tiles;
+    d.c = t[s].c;
+    d.L = (float)(t[s].qmax - t[s].qmin + 1);
+    d.qmin = t[s].qmin;
+    d.qmax = t[s].qmax;
+    d.tid = t[s].tensor_id;
+    tiles += tiles_of(t[s].nweights);
   }
-  tab.b0[n] = tiles;
-  if (tiles == 0) return hipSuccess;
-  // as many blocks as fit on the device at once; each loops over tiles
-  const int64_t cap = occupancy_blocks(
-      cf == CF_T2 ? reinterpret_cast<const void*>(sr_update_kernel<CF_T2, kCW>)
-                  : cf == CF_I4 ? reinterpret_cast<const void*>(sr_update_kernel<CF_I4, kCW>)
-                                : reinterpret_cast<const void*>(sr_update_kernel<CF_I8, kCW>),
-      256);
-  const unsigned blocks = (unsigned)(tiles < cap ? tiles : cap);
-  if (cf == CF_T2) return launch_kernel(sr_update_kernel<CF_T2, kCW>, dim3(blocks), dim3(256), stream, tab, counters);
-  if (cf == CF_I4) return launch_kernel(sr_update_kernel<CF_I4, kCW>, dim3(blocks), dim3(256), stream, tab, counters);
-  return launch_kernel(sr_update_kernel<CF_I8, kCW>, dim3(blocks), dim3(256), stream, tab, counters);
+  return launch_sr(cf, tab, tiles, seed, step, counters, nullptr, stream);
+}
+
+void sr_table_entry(const SRTensor& t, int64_t tile0, SRTableEntry* e) {
+  *e = SRTableEntry{};
+  e->wq = reinterpret_cast<uint64_t>(t.wq);
+  e->grad = reinterpret_cast<uint64_t>(t.grad);
+  e->nchunks = t.nweights / kCW;
+  e->tile0 = tile0;
+  e->alpha = t.alpha;
+  e->qmin = t.qmin;
+  e->qmax = t.qmax;
+  e->tensor_id = t.tensor_id;
+}
+
+int64_t sr_tiles(int64_t nweights) { return tiles_of(nweights); }
+
+hipError_t launch_sr_update_table(int cf, int n, int64_t total_weights_tiles, const SRTableEntry* table,
+                                  float lr, uint64_t seed, uint32_t step, unsigned long long* counters,
+                                  unsigned long long* per_tensor, hipStream_t stream) {
+  SRDevTab tab{table, n, lr};
+  return launch_sr(cf, tab, total_weights_tiles, seed, step, counters, per_tensor, stream);
 }
 
 hipError_t launch_debug_rng(uint64_t seed, uint32_t step, uint32_t tensor_id, uint64_t i0,

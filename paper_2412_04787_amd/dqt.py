@@ -24,7 +24,8 @@ EXPORTS = (
     "dqt_act_quant", "dqt_act_quant_batch", "dqt_linear_fwd_workspace", "dqt_linear_fwd", "dqt_linear_bwd_workspace",
     "dqt_linear_bwd", "dqt_linear_fwd_batch_workspace", "dqt_linear_fwd_batch",
     "dqt_linear_bwd_batch_workspace", "dqt_linear_bwd_batch", "dqt_linear_bwd_sr_batch",
-    "dqt_linear_fwd_batch_noalloc",
+    "dqt_linear_fwd_batch_noalloc", "dqt_sr_table_bytes", "dqt_sr_table_build",
+    "dqt_sr_update_table",
     "dqt_sr_update_batch", "dqt_adamw_sr_update", "dqt_adamw_sr_update_batch",
     "dqt_update_variant_workspace", "dqt_update_variant_batch",
     "dqt_sr_update", "dqt_debug_rng", "dqt_absmean_init", "dqt_pack_ternary",
@@ -92,6 +93,9 @@ _SIGS = {
     "dqt_linear_bwd_sr_batch": (_i32, [_i32, _vp, _i64, _i32, _i32, _i32, _i32, _f32, _u64, _u32,
                                        _vp, _vp, ctypes.c_size_t, _vp]),
     "dqt_sr_update_batch": (_i32, [_i32, _vp, _f32, _u64, _u32, _vp, _vp]),
+    "dqt_sr_table_bytes": (ctypes.c_size_t, [_i32]),
+    "dqt_sr_table_build": (_i32, [_i32, _vp, _vp, ctypes.c_size_t]),
+    "dqt_sr_update_table": (_i32, [_i32, _vp, _vp, _f32, _u64, _u32, _vp, _vp, _vp]),
     "dqt_update_variant_workspace": (ctypes.c_size_t, [_i32]),
     "dqt_update_variant_batch": (_i32, [_i32, _vp, _f32, _u64, _u32, _i32, _f32, _vp, _vp,
                                         ctypes.c_size_t, _vp]),
@@ -346,6 +350,27 @@ def dqt_adamw_sr_update_batch(io, ms, vs, hp: DqtAdamW, seed: int, step: int, co
 def dqt_sr_update_batch(io, lr: float, seed: int, step: int, counters=None, stream=None):
     _check("dqt_sr_update_batch", load().dqt_sr_update_batch(len(io), io, lr, seed, step,
                                                              _ptr(counters), _stream(stream)))
+
+
+def dqt_sr_table_bytes(n: int) -> int:
+    return int(load().dqt_sr_table_bytes(n))
+
+
+def dqt_sr_table_build(io) -> np.ndarray:
+    """The update table of the entries of io, as host bytes (copy them to the
+    device once, e.g. torch.from_numpy(t).to(device))."""
+    n = len(io)
+    table = np.zeros(max(dqt_sr_table_bytes(n), 1), dtype=np.uint8)
+    _check("dqt_sr_table_build", load().dqt_sr_table_build(n, io, table.ctypes.data, table.size))
+    return table
+
+
+def dqt_sr_update_table(io, table, lr: float, seed: int, step: int, counters=None,
+                        per_tensor=None, stream=None):
+    """table: the device copy of dqt_sr_table_build(io)."""
+    _check("dqt_sr_update_table",
+           load().dqt_sr_update_table(len(io), io, _ptr(table), lr, seed, step, _ptr(counters),
+                                      _ptr(per_tensor), _stream(stream)))
 
 
 # ----------------------------------------------------------------- host helpers

@@ -282,3 +282,55 @@ def test_new_batch_entry_points_take_one_to_eight_linears():
                                         None) == dqt.DQT_ERR_SHAPE
     assert lib.dqt_update_variant_batch(1, dqt.linear_io([dict(w=_w())]), 1e-3, 0, 1, 7, 0.2, None,
                                         None, 0, None) == dqt.DQT_ERR_RANGE
+
+
+def test_sr_table_build_layout_and_checks():
+    """The update table of n tensors: 64-byte entries holding the code and
+    gradient addresses, the tensor's chunks of 8 weights, its first tile of
+    256 chunks in the launch (a running sum), alpha, the grid and the tensor
+    id; the host checks reject bad entries before anything is written to the
+    device."""
+    lib = dqt.load()
+    shapes = [(16, 16), (256, 272), (48, 80), (4096, 4096)]
+    ents = []
+    for s, (d_out, d_in) in enumerate(shapes):
+        w = _w(d_out=d_out, d_in=d_in, wfmt=dqt.DQT_I8, qmin=-127, qmax=127, alpha=0.5 + s,
+               tensor_id=9 + s)
+        ents.append(w)
+    io = dqt.linear_io([dict(w=w) for w in ents])
+    for s in range(len(ents)):
+        io[s].Wq = 0x10000 * (s + 1)
+        io[s].dW = 0x100000 * (s + 1)
+    assert dqt.dqt_sr_table_bytes(4) == 256 and dqt.dqt_sr_table_bytes(0) == 0
+    tab = dqt.dqt_sr_table_build(io)
+    rec = np.frombuffer(tab.tobytes(), dtype=np.dtype([
+        ("wq", "<u8"), ("grad", "<u8"), ("nchunks", "<i8"), ("tile0", "<i8"), ("alpha", "<f4"),
+        ("qmin", "<i4"), ("qmax", "<i4"), ("tid", "<u4"), ("pad", "<u4", 4)]))
+    tile = 0
+    for s, (d_out, d_in) in enumerate(shapes):
+        r = rec[s]
+        assert r["wq"] == 0x10000 * (s + 1) and r["grad"] == 0x100000 * (s + 1)
+        assert r["nchunks"] == d_out * d_in // 8 and r["tile0"] == tile
+        assert r["alpha"] == np.float32(0.5 + s) and (r["qmin"], r["qmax"]) == (-127, 127)
+        assert r["tid"] == 9 + s and not r["pad"].any()
+        tile += (d_out * d_in // 8 + 255) // 256
+    buf = np.zeros(256, np.uint8)
+    assert lib.dqt_sr_table_build(4, io, buf.ctypes.data, 255) == dqt.DQT_ERR_WORKSPACE
+    assert lib.dqt_sr_table_build(0, io, buf.ctypes.data, 256) == dqt.DQT_ERR_SHAPE
+    assert lib.dqt_sr_table_build(4, io, None, 256) == dqt.DQT_ERR_NULL
+    io[2].dW = 0x100008                                       # not 16-byte aligned
+    assert lib.dqt_sr_table_build(4, io, buf.ctypes.data, 256) == dqt.DQT_ERR_ALIGN
+    io[2].dW = None
+    assert lib.dqt_sr_table_build(4, io, buf.ctypes.data, 256) == dqt.DQT_ERR_NULL
+    io[2].dW = 0x300000
+    mixed = dqt.linear_io([dict(w=ents[0]), dict(w=_w(wfmt=dqt.DQT_TERNARY2))])
+    mixed[0].Wq = mixed[1].Wq = mixed[0].dW = mixed[1].dW = 0x10000
+    assert lib.dqt_sr_table_build(2, mixed, buf.ctypes.data, 256) == dqt.DQT_ERR_UNSUPPORTED
+    # the update call repeats the checks, and refuses a bad lr or table
+    assert lib.dqt_sr_update_table(4, io, 0x200000, -1.0, 0, 1, None, None, None) == \
+        dqt.DQT_ERR_RANGE
+    assert lib.dqt_sr_update_table(4, io, None, 1e-3, 0, 1, None, None, None) == dqt.DQT_ERR_NULL
+    assert lib.dqt_sr_update_table(4, io, 0x200008, 1e-3, 0, 1, None, None, None) == \
+        dqt.DQT_ERR_ALIGN
+    assert lib.dqt_sr_update_table(4, io, 0x200000, 1e-3, 0, 1, None, 0x300004, None) == \
+        dqt.DQT_ERR_ALIGN

@@ -1,0 +1,134 @@
+"""The direct SR update of many tensors in one launch (Sec. 3.2 Eq. 5 applied
+to every weight matrix of a model) through a device table: codes bit-exact
+against the oracle's update of each tensor with its own tensor id, and the
+per-tensor changed / non-finite counts (the update frequency of Sec. 5.2)
+equal to the oracle's."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import dqt_oracle as O
+from paper_2412_04787_amd import dqt, workloads as W
+
+from gpu_util import DEV, log, make_weight, weight_codes_dev, weight_codes_host
+
+pytestmark = pytest.mark.gpu
+
+SEED, STEP = 31, 7
+
+
+def _tensors(shapes, wfmt, qmin, qmax, gscale, wid, nonfinite=()):
+    """Codes, gradients and descriptors of a list of (d_out, d_in) tensors;
+    `nonfinite` lists (tensor, flat index, value) to plant in gradients."""
+    ents, host = [], []
+    for s, (d_out, d_in) in enumerate(shapes):
+        if wfmt == "ternary":
+            q = W.draw_ternary((d_out, d_in), SEED, wid, 1, s)
+        else:
+            q = W.draw_int((d_out, d_in), qmin, qmax, SEED, wid, 1, s)
+        g = W.draw_normal((d_out, d_in), gscale, SEED, wid, 2, s)
+        for (ts, idx, val) in nonfinite:
+            if ts == s:
+                g.reshape(-1)[idx] = val
+        alpha = np.float32(0.01 + 0.0005 * (s % 17))
+        w = make_weight(d_out, d_in, wfmt, qmin, qmax, alpha, tensor_id=100 + s)
+        ents.append(dict(w=w, Wq=weight_codes_dev(q, wfmt), dW=torch.from_numpy(g).to(DEV)))
+        host.append((q, g, alpha, w))
+    return ents, host
+
+
+def _check_against_oracle(ents, host, wfmt, qmin, qmax, lr, per_tensor, counters):
+    tot_c = tot_f = 0
+    pt = per_tensor.cpu().numpy().reshape(-1, 2)
+    for s, (q, g, alpha, w) in enumerate(host):
+        got = weight_codes_host(ents[s]["Wq"], wfmt, w.d_in)
+        want, nch, nnf = O.sr_update(q.ravel(), g.ravel(), lr, alpha, qmin, qmax, SEED, STEP,
+                                     w.tensor_id)
+        assert np.array_equal(got.ravel(), want), f"tensor {s} codes"
+        assert (int(pt[s, 0]), int(pt[s, 1])) == (nch, nnf), (s, pt[s].tolist(), nch, nnf)
+        tot_c += nch
+        tot_f += nnf
+    assert counters.tolist() == [tot_c, tot_f]
+
+
+def test_sr_table_168_tensors_of_a_24_layer_model(lib):
+    """24 layers x 7 linears of a scaled-down LLaMA (hidden 256, FFN 704),
+    ternary codes: 168 tensors in one launch."""
+    h, ffn = 256, 704
+    layer = [(h, h)] * 4 + [(ffn, h), (ffn, h), (h, ffn)]
+    shapes = layer * 24
+    lr = 3e-2
+    ents, host = _tensors(shapes, "ternary", -1, 1, 0.05, 61)
+    log(f"table SR: {len(shapes)} tensors, {sum(a * b for a, b in shapes)} weights")
+    io = dqt.linear_io(ents)
+    table = torch.from_numpy(dqt.dqt_sr_table_build(io)).to(DEV)
+    counters = torch.zeros((2,), dtype=torch.int64, device=DEV)
+    per_tensor = torch.zeros((2 * len(shapes),), dtype=torch.int64, device=DEV)
+    dqt.dqt_sr_update_table(io, table, lr, SEED, STEP, counters, per_tensor)
+    torch.cuda.synchronize()
+    _check_against_oracle(ents, host, "ternary", -1, 1, lr, per_tensor, counters)
+    assert counters[0].item() > 0
+
+
+@pytest.mark.parametrize("wfmt,qmin,qmax", [("i8", -127, 127), ("i4", -8, 7)])
+def test_sr_table_ragged_tiny_and_nonfinite(lib, wfmt, qmin, qmax):
+    """Tensors smaller than one tile, tensors ending mid-tile, and non-finite
+    gradients counted per tensor."""
+    shapes = [(16, 16), (48, 80), (256, 272), (16, 32), (512, 1024), (32, 16), (208, 96),
+              (16, 16)] * 3 + [(1024, 1024)]
+    nonfinite = [(1, 5, np.inf), (4, 777, np.nan), (4, 778, -np.inf), (24, 100000, np.nan)]
+    lr = 5e-2
+    ents, host = _tensors(shapes, wfmt, qmin, qmax, 0.3, 62 if wfmt == "i8" else 63, nonfinite)
+    io = dqt.linear_io(ents)
+    table = torch.from_numpy(dqt.dqt_sr_table_build(io)).to(DEV)
+    counters = torch.zeros((2,), dtype=torch.int64, device=DEV)
+    per_tensor = torch.zeros((2 * len(shapes),), dtype=torch.int64, device=DEV)
+    dqt.dqt_sr_update_table(io, table, lr, SEED, STEP, counters, per_tensor)
+    torch.cuda.synchronize()
+    _check_against_oracle(ents, host, wfmt, qmin, qmax, lr, per_tensor, counters)
+    assert counters[1].item() == 4
+
+
+def test_sr_table_matches_batch_calls(lib):
+    """300 tiny tensors in one table launch give the codes and totals of the
+    same tensors updated eight at a time by dqt_sr_update_batch; the table is
+    reused for a second step (new draws, codes moved again)."""
+    shapes = [(16, 32 * (1 + s % 5)) for s in range(300)]
+    lr = 0.2
+    ents, _ = _tensors(shapes, "ternary", -1, 1, 0.1, 64)
+    ref = [dict(e, Wq=e["Wq"].clone()) for e in ents]
+    io = dqt.linear_io(ents)
+    table = torch.from_numpy(dqt.dqt_sr_table_build(io)).to(DEV)
+    c_tab = torch.zeros((2,), dtype=torch.int64, device=DEV)
+    c_ref = torch.zeros((2,), dtype=torch.int64, device=DEV)
+    for step in (STEP, STEP + 1):
+        dqt.dqt_sr_update_table(io, table, lr, SEED, step, c_tab)
+        for k in range(0, len(ref), 8):
+            dqt.dqt_sr_update_batch(dqt.linear_io(ref[k:k + 8]), lr, SEED, step, c_ref)
+        torch.cuda.synchronize()
+        for s in range(len(shapes)):
+            assert torch.equal(ents[s]["Wq"], ref[s]["Wq"]), (step, s)
+        assert torch.equal(c_tab, c_ref), (c_tab.tolist(), c_ref.tolist())
+
+
+def test_sr_table_argument_checks(lib):
+    w = make_weight(64, 64, "ternary", -1, 1, 0.01)
+    w8 = make_weight(64, 64, "i8", -127, 127, 0.01)
+    t = torch.zeros((64 * 64,), dtype=torch.int8, device=DEV)
+    g = torch.zeros((64, 64), dtype=torch.float32, device=DEV)
+    io = dqt.linear_io([dict(w=w, Wq=t, dW=g)] * 3)
+    table = torch.from_numpy(dqt.dqt_sr_table_build(io)).to(DEV)
+    for bad_lr in (-1.0, float("nan")):
+        with pytest.raises(dqt.DqtError) as e:
+            dqt.dqt_sr_update_table(io, table, bad_lr, 0, 1)
+        assert e.value.status == dqt.DQT_ERR_RANGE
+    with pytest.raises(dqt.DqtError) as e:
+        dqt.dqt_sr_update_table(io, None, 1e-3, 0, 1)
+    assert e.value.status == dqt.DQT_ERR_NULL
+    with pytest.raises(dqt.DqtError) as e:
+        dqt.dqt_sr_update_table(dqt.linear_io([dict(w=w, Wq=t, dW=g), dict(w=w8, Wq=t, dW=g)]),
+                                table, 1e-3, 0, 1)
+    assert e.value.status == dqt.DQT_ERR_UNSUPPORTED
+    with pytest.raises(dqt.DqtError) as e:
+        dqt.dqt_sr_update_table(io, table[1:], 1e-3, 0, 1)
+    assert e.value.status == dqt.DQT_ERR_ALIGN
