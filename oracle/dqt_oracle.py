@@ -25,6 +25,7 @@ Paper map (section / equation of the DQT paper):
   * Sec. 5.2 ............... fraction of weights changed per step -> n_changed
   * Sec. 4.1 (AdamW modified with SR; reading R11) ............... -> adamw_sr_update
   * Sec. 5 (rounding without SR; forcing the smallest 20 %; R12) -> update_variant
+  * Sec. 3.2 inputs of the linears after the block's RMSNorm (R13) -> rmsnorm_act_quant
 
 Readings of points the paper leaves open (each is listed in the design doc):
   R1  SR acts in grid units: with W~ = q * alpha (alpha = 1/s, Eq. 3) and
@@ -57,13 +58,19 @@ Readings of points the paper leaves open (each is listed in the design doc):
       the weight, m and v unchanged and is counted.
   R12 Analysis variants of Sec. 5 (with alpha fixed, R3): the deterministic
       control rounds x = q + delta to the nearest grid value (ties to even)
-      instead of stochastically; "the smallest 20 % of the updates" of a step
-      are ranked per tensor by |delta| (fp32 bit patterns as unsigned
+      instead of stochastically; for the interventions on the smallest
+      fraction of a step's updates, updates are ranked per tensor by |delta| (fp32 bit patterns as unsigned
       integers, non-finite gradients ranked last): with k = floor(frac n) and
       tau the k-th smallest key, the bottom set is {key <= tau} (ties at tau
       may enlarge it).  Force-to-remain keeps the bottom codes; force-to-
       update rounds x away from q (ceil for delta > 0, floor for delta < 0),
       then clips; every other element takes the plain SR update.
+  R13 RMSNorm before the activation quantisation (the LLaMA block's norm,
+      not specified by the paper): y = x / sqrt(mean(x^2) + eps) * gamma in
+      fp32, the sum of squares in the fixed order of ``rms_sum_squares``
+      (64 lane sums over chunks of 8 elements, then a butterfly), each
+      operation one correctly rounded fp32 operation; y then goes through
+      ``act_quant``.
 """
 
 from __future__ import annotations
@@ -272,6 +279,65 @@ def act_quant(X, kind: str):
     else:
         Xq = e4m3_encode(scaled)
     return Xq, d
+
+
+# ---------------------------------------------------------------------------
+# Next row: RMSNorm followed by the activation quantisation (reading R13).
+# In a LLaMA block the inputs of the q/k/v and gate/up linears are RMSNorm
+# outputs; the paper quantises those inputs to 8 bits (Sec. 3.2).
+# ---------------------------------------------------------------------------
+
+RMS_LANES = 64      # lane partial sums of the sum of squares
+RMS_CHUNK = 8       # consecutive elements per chunk
+
+
+def rms_sum_squares(X) -> np.ndarray:
+    """Sum of squares of each row of X [M, K] (fp32 values) in the fixed
+    fp32 order of reading R13: every square is one fp32 multiply; lane l of
+    64 adds, in order, the squares of the chunks l, l + 64, l + 128, ... of
+    8 consecutive elements (each chunk's elements in order) into a sum that
+    starts at 0; then, for d = 32, 16, 8, 4, 2, 1, every lane sum becomes
+    fl(s_l + s_(l xor d)).  Returns the fp32 sums [M]."""
+    X = np.asarray(X, dtype=np.float32)
+    M, K = X.shape
+    sq = (X * X).astype(np.float32)
+    nchunk = K // RMS_CHUNK
+    lanes = np.zeros((M, RMS_LANES), dtype=np.float32)
+    # position p of lane l's sequence is element RMS_CHUNK * (l + 64 (p // 8)) + p % 8
+    per_lane = (nchunk + RMS_LANES - 1) // RMS_LANES * RMS_CHUNK
+    for p in range(per_lane):
+        chunk = np.arange(RMS_LANES) + RMS_LANES * (p // RMS_CHUNK)
+        elem = RMS_CHUNK * chunk + p % RMS_CHUNK
+        live = chunk < nchunk
+        add = np.where(live[None, :], sq[:, np.minimum(elem, K - 1)], np.float32(0))
+        lanes = np.where(live[None, :], (lanes + add).astype(np.float32), lanes)
+    idx = np.arange(RMS_LANES)
+    for d in (32, 16, 8, 4, 2, 1):
+        lanes = (lanes + lanes[:, idx ^ d]).astype(np.float32)
+    return lanes[:, 0].copy()
+
+
+def rmsnorm(X, gamma, eps):
+    """RMSNorm of each row (R13): r_m = fl(1 / fl(sqrt(fl(fl(s_m / K) +
+    eps)))) with s_m = rms_sum_squares, then y_mk = fl(fl(x_mk r_m) gamma_k);
+    every operation one correctly rounded fp32 operation.  Returns (y, r)."""
+    X = np.asarray(X, dtype=np.float32)
+    K = X.shape[1]
+    s = rms_sum_squares(X)
+    mean = (s / np.float32(K)).astype(np.float32)
+    v = (mean + np.float32(eps)).astype(np.float32)
+    with np.errstate(divide="ignore"):
+        r = (np.float32(1.0) / np.sqrt(v).astype(np.float32)).astype(np.float32)
+    y = ((X * r[:, None]).astype(np.float32) * np.asarray(gamma, dtype=np.float32)[None, :])
+    return y.astype(np.float32), r
+
+
+def rmsnorm_act_quant(X, gamma, eps, kind: str):
+    """RMSNorm, then the per-token quantisation of act_quant applied to its
+    output.  Returns (Xq, d, r, y)."""
+    y, r = rmsnorm(X, gamma, eps)
+    Xq, d = act_quant(y, kind)
+    return Xq, d, r, y
 
 
 def act_values(Xq, kind: str) -> np.ndarray:
