@@ -120,6 +120,29 @@ typedef struct {
 dqt_status dqt_act_quant(const void* X, int32_t x_t, int64_t M, int32_t K,
                          int32_t act_q, void* Xq, float* xdq, void* stream);
 
+/*
+ * RMSNorm of each token, then the per-token activation quantisation of
+ * dqt_act_quant applied to its output, in one launch: the normalised row
+ * never reaches memory.  (In a LLaMA block the q/k/v and gate/up linears
+ * take RMSNorm outputs, and Sec. 3.2 quantises the linears' inputs to 8
+ * bits; the norm itself is the block's, not the paper's.)  For each row m of
+ * X [M, K], every operation one correctly rounded fp32 operation:
+ *   s_m  = sum over k of fl(x_mk * x_mk), in this order: lane l = 0..63 adds
+ *          the squares of the chunks of 8 consecutive elements l, l + 64,
+ *          l + 128, ... (each chunk's elements in order) into a sum starting
+ *          at 0; then for d = 32, 16, 8, 4, 2, 1 every lane sum s_l becomes
+ *          s_l + s_(l xor d); s_m is the result
+ *   r_m  = 1 / sqrt(s_m / K + eps)
+ *   y_mk = (x_mk * r_m) * gamma_k
+ *   Xq, xdq: dqt_act_quant of y (act_q = DQT_I8 or DQT_FP8E4M3).
+ *   X: [M, K], x_t = DQT_F32 or DQT_BF16; gamma: [K] fp32; eps: finite, > 0.
+ *   Xq: [M, K] codes; xdq: [M] scales; rinv: NULL or [M] fp32, receives r_m
+ *   (for the norm's backward).  K a multiple of 16, M at most 2^28.
+ */
+dqt_status dqt_rmsnorm_act_quant(const void* X, int32_t x_t, const float* gamma,
+                                 float eps, int64_t M, int32_t K, int32_t act_q,
+                                 void* Xq, float* xdq, float* rinv, void* stream);
+
 /* Bytes of device workspace dqt_linear_fwd needs for this weight: the 256
  * counter bytes, plus, for ternary weights whose d_in is not a multiple of
  * 64, d_out * d_in operand bytes they are unpacked into (with d_in a

@@ -73,6 +73,20 @@ dqt_status dqt_act_quant(const void* X, int32_t x_t, int64_t M, int32_t K, int32
                                         static_cast<hipStream_t>(stream)));
 }
 
+dqt_status dqt_rmsnorm_act_quant(const void* X, int32_t x_t, const float* gamma, float eps,
+                                 int64_t M, int32_t K, int32_t act_q, void* Xq, float* xdq,
+                                 float* rinv, void* stream) {
+  if (M < 0 || M > (int64_t(1) << 28) || K < 16 || (K % 16) != 0) return DQT_ERR_SHAPE;
+  if (!is_float_type(x_t) || (act_q != DQT_I8 && act_q != DQT_FP8E4M3)) return DQT_ERR_DTYPE;
+  if (!(isfinite(eps) && eps > 0.0f)) return DQT_ERR_RANGE;
+  if (M == 0) return DQT_OK;
+  if (X == nullptr || gamma == nullptr || Xq == nullptr || xdq == nullptr) return DQT_ERR_NULL;
+  if (!aligned16(X) || !aligned16(gamma) || !aligned16(Xq) || !aligned16(xdq)) return DQT_ERR_ALIGN;
+  if (rinv != nullptr && (reinterpret_cast<uintptr_t>(rinv) & 3u) != 0) return DQT_ERR_ALIGN;
+  return from_hip(dqt::launch_rmsnorm_act_quant(X, x_t == DQT_BF16, gamma, eps, M, K, act_q == DQT_FP8E4M3,
+                                                Xq, xdq, rinv, static_cast<hipStream_t>(stream)));
+}
+
 dqt_status dqt_act_quant_batch(int32_t n, const dqt_act_io* io, int32_t x_t, int64_t M,
                                int32_t act_q, void* stream) {
   if (n < 0 || n > DQT_MAX_BATCH) return DQT_ERR_SHAPE;

@@ -114,7 +114,9 @@ __global__ __launch_bounds__(256) void adamw_sr_kernel(const AdamTab tab,
       const int q = CodeFmt<CF>::q_of(win, j);
       const float m1 = __fadd_rn(__fmul_rn(tab.b1, m), __fmul_rn(tab.ob1, g));
       const float v1 = __fadd_rn(__fmul_rn(tab.b2, v), __fmul_rn(__fmul_rn(tab.ob2, g), g));
-      const float den = __fadd_rn(__fmul_rn(__fsqrt_rn(v1), tab.k2), tab.eps);
+      // (sqrtf is the correctly rounded square root in HIP; __fsqrt_rn
+      // lowers to the one-ulp hardware approximation)
+      const float den = __fadd_rn(__fmul_rn(sqrtf(v1), tab.k2), tab.eps);
       const float u = __fdiv_rn(m1, den);
       const float d = -__fadd_rn(__fmul_rn(cu, u), __fmul_rn(tab.cd, (float)q));
       const bool keep = !__builtin_isfinite(g) || __builtin_isnan(d);

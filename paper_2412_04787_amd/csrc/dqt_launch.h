@@ -65,6 +65,11 @@ struct DwArgs {
 
 hipError_t launch_act_quant(const void* X, bool x_bf16, int64_t M, int K, bool e4m3, void* Xq,
                             float* xdq, hipStream_t stream);
+// RMSNorm (fp32, fixed summation order) then the per-token quantisation;
+// rinv (nullable) receives each row's 1 / rms.
+hipError_t launch_rmsnorm_act_quant(const void* X, bool x_bf16, const float* gamma, float eps, int64_t M,
+                                    int K, bool e4m3, void* Xq, float* xdq, float* rinv,
+                                    hipStream_t stream);
 // up to kMaxBatch inputs with the same M and dtypes in one launch
 struct ActIO {
   const void* X;        // [M, K]
