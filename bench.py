@@ -39,6 +39,8 @@ if ROOT not in sys.path:
 # MI355X published peaks
 PEAK_HBM_GBS = 8000.0
 PEAK_TFLOPS = {"bf16": 2500.0, "i8": 5000.0, "fp8": 5000.0, "f32": 157.3}
+# bytes of code storage per weight
+CODE_BYTES = {"ternary": 0.25, "i3": 0.375, "i4": 0.5, "i8": 1.0}
 
 
 def parse():
@@ -73,7 +75,8 @@ class Block:
         bf = torch.bfloat16 if wl.x_dtype == "bf16" else torch.float32
         self.act = dqt.DQT_I8 if wl.act == "i8" else dqt.DQT_FP8E4M3
         self.xt = dqt.DQT_BF16 if wl.xt == "bf16" else dqt.DQT_F32
-        wfmt = {"ternary": dqt.DQT_TERNARY2, "i4": dqt.DQT_INT4}.get(wl.wfmt, dqt.DQT_I8)
+        wfmt = {"ternary": dqt.DQT_TERNARY2, "i4": dqt.DQT_INT4, "i3": dqt.DQT_INT3}.get(wl.wfmt,
+                                                                                   dqt.DQT_I8)
         M = wl.M
         self.weights, self.codes, self.dY, self.Y, self.dX, self.dW = [], [], [], [], [], []
         for li, lin in enumerate(wl.linears):
@@ -82,7 +85,8 @@ class Block:
             if wl.init == "uniform":   # codes drawn directly; scale from W0 (qmax = 1)
                 q = qdraw
             codes = (dqt.dqt_pack_ternary(q) if wl.wfmt == "ternary"
-                     else dqt.dqt_pack_int4(q) if wl.wfmt == "i4" else q)
+                     else dqt.dqt_pack_int4(q) if wl.wfmt == "i4"
+                     else dqt.dqt_pack_int3(q) if wl.wfmt == "i3" else q)
             self.codes.append(torch.from_numpy(np.ascontiguousarray(codes)).to(dev))
             self.weights.append(dqt.weight(lin.d_out, lin.d_in, wfmt, wl.qmin, wl.qmax, alpha, li))
             dy = torch.from_numpy(W.grad_draw(wl, li)).to(bf).to(dev)
@@ -154,7 +158,7 @@ def algorithmic_units(wl):
     """Per step: flops of each GEMM stage, bytes of each streaming stage."""
     M = wl.M
     f = sum(2 * M * l.d_in * l.d_out for l in wl.linears)
-    code_b = {"ternary": 0.25, "i4": 0.5}.get(wl.wfmt, 1.0)
+    code_b = CODE_BYTES.get(wl.wfmt, 1.0)
     sr_bytes = sum((2 * code_b + 4) * l.d_in * l.d_out for l in wl.linears)
     # AdamW with SR: read g, m, v and the code; write m, v and the code
     adam_bytes = sum((2 * code_b + 20) * l.d_in * l.d_out for l in wl.linears)
@@ -251,7 +255,7 @@ def cpu_baseline(wl, tokens: int, sr_weights: int):
         "one_thread_value": flops / (gemm_one + sr_full) / 1e12,
         "one_thread_sample": f"GEMM part on the first {tok1} tokens ({t_one:.1f} s, x {wl.M / tok1:g})",
         "sr_update_gbs_one_thread": round(
-            sum((2 * {"ternary": 0.25, "i4": 0.5}.get(wl.wfmt, 1.0) + 4) * l.d_in * l.d_out
+            sum((2 * CODE_BYTES.get(wl.wfmt, 1.0) + 4) * l.d_in * l.d_out
                 for l in wl.linears) / sr_full / 1e9, 3),
     }
 

@@ -67,7 +67,8 @@ typedef enum {
   DQT_I8 = 2,         /* int8                                                 */
   DQT_FP8E4M3 = 3,    /* OCP E4M3 ("fn": bias 7, max 448, no inf)             */
   DQT_TERNARY2 = 4,   /* packed 2-bit ternary weight codes, see dqt_weight    */
-  DQT_INT4 = 5        /* packed 4-bit weight codes, see dqt_weight            */
+  DQT_INT4 = 5,       /* packed 4-bit weight codes, see dqt_weight            */
+  DQT_INT3 = 6        /* packed 3-bit weight codes, see dqt_weight            */
 } dqt_dtype;
 
 /*
@@ -85,6 +86,13 @@ typedef enum {
  *          Requires -8 <= qmin < qmax <= 7.  The forward and dX expand the
  *          nibbles to int8 or e4m3 / bf16 in the workspace; the updates work
  *          on the nibbles in place.
+ *   wfmt = DQT_INT3: the n = 3 grid of Eq. 3 (-4..3) at 3 bits per weight:
+ *          each group of 8 weights (n, 8 g .. 8 g + 7) is a 24-bit
+ *          little-endian word in bytes n * (3 d_in / 8) + 3 g .. + 2, weight
+ *          8 g + j at bits 3 j (two's complement).  Requires
+ *          -4 <= qmin < qmax <= 3.  The forward and dX expand the fields to
+ *          int8 or e4m3 / bf16 in the workspace; the updates work on the
+ *          packed bytes in place.
  *   alpha: dequantisation scale, the weight's real value is q * alpha
  *          (alpha = 1/s, Eq. 3).  Finite and > 0.  Fixed for the life of the
  *          tensor: the library never recomputes it (Sec. 3.2 skips Eq. 2-4
@@ -95,7 +103,7 @@ typedef enum {
 typedef struct {
   int32_t d_out;
   int32_t d_in;
-  int32_t wfmt;       /* dqt_dtype: DQT_TERNARY2, DQT_INT4 or DQT_I8 */
+  int32_t wfmt;       /* dqt_dtype: DQT_TERNARY2, DQT_INT3, DQT_INT4 or DQT_I8 */
   int32_t qmin;
   int32_t qmax;
   float alpha;
@@ -159,8 +167,8 @@ size_t dqt_linear_fwd_workspace(const dqt_weight* w);
  *   X:     [M, d_in] (x_t = DQT_F32/DQT_BF16), or NULL when Xq/xdq already
  *          hold this input's quantised form (several linears sharing one
  *          input quantise it once with dqt_act_quant).
- *   act_q: DQT_I8 or DQT_FP8E4M3 (e4m3 needs wfmt = DQT_TERNARY2 or DQT_INT4,
- *          whose values e4m3 holds exactly).
+ *   act_q: DQT_I8 or DQT_FP8E4M3 (e4m3 needs wfmt = DQT_TERNARY2, DQT_INT3
+ *          or DQT_INT4, whose values e4m3 holds exactly).
  *   Xq, xdq: [M, d_in] codes and [M] scales; written when X != NULL, read
  *          otherwise.  Keep them for dqt_linear_bwd.
  *   Y:     [M, d_out], y_t = DQT_F32 or DQT_BF16.  (output)
@@ -484,6 +492,13 @@ dqt_status dqt_unpack_ternary(const uint8_t* packed, int64_t rows,
  * even.  pack returns DQT_ERR_RANGE (and stops) on a value outside [-8, 7]. */
 dqt_status dqt_pack_int4(const int8_t* q, int64_t rows, int64_t cols, uint8_t* packed);
 dqt_status dqt_unpack_int4(const uint8_t* packed, int64_t rows, int64_t cols, int8_t* q);
+
+/* Host packing of codes in [-4, 3] into the DQT_INT3 layout and back.
+ * q: host int8 [rows, cols]; packed: host uint8 [rows, 3 cols / 8]; cols a
+ * multiple of 8.  pack returns DQT_ERR_RANGE (and stops) on a value outside
+ * [-4, 3]. */
+dqt_status dqt_pack_int3(const int8_t* q, int64_t rows, int64_t cols, uint8_t* packed);
+dqt_status dqt_unpack_int3(const uint8_t* packed, int64_t rows, int64_t cols, int8_t* q);
 
 /* Human-readable name of a status code (static storage). */
 const char* dqt_status_string(int32_t status);

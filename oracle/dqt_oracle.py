@@ -221,6 +221,33 @@ def unpack_int4(packed: np.ndarray, d_in: int) -> np.ndarray:
     return out.astype(np.int8)
 
 
+def pack_int3(q: np.ndarray) -> np.ndarray:
+    """Codes in [-4, 3] [rows, cols] -> 3-bit two's-complement fields, 8 per
+    3 bytes: the group of weights 8g .. 8g + 7 is the 24-bit number
+    sum_j (q_(8g+j) mod 8) 2^(3j), stored little-endian in bytes 3g .. 3g + 2."""
+    q = np.asarray(q).astype(np.int64)
+    assert q.ndim == 2 and q.shape[1] % 8 == 0 and q.min() >= -4 and q.max() <= 3
+    rows, cols = q.shape
+    fields = (q & 7).reshape(rows, cols // 8, 8)
+    word = np.zeros((rows, cols // 8), dtype=np.int64)
+    for j in range(8):
+        word += fields[:, :, j] << (3 * j)
+    out = np.empty((rows, cols // 8, 3), dtype=np.uint8)
+    for b in range(3):
+        out[:, :, b] = (word >> (8 * b)) & 0xFF
+    return out.reshape(rows, 3 * cols // 8)
+
+
+def unpack_int3(packed: np.ndarray, d_in: int) -> np.ndarray:
+    p = np.asarray(packed, dtype=np.uint8).reshape(-1, d_in // 8, 3).astype(np.int64)
+    word = p[:, :, 0] | (p[:, :, 1] << 8) | (p[:, :, 2] << 16)
+    out = np.empty((p.shape[0], d_in // 8, 8), dtype=np.int64)
+    for j in range(8):
+        f = (word >> (3 * j)) & 7
+        out[:, :, j] = np.where(f >= 4, f - 8, f)
+    return out.reshape(p.shape[0], d_in).astype(np.int8)
+
+
 def absmean(W) -> float:
     """Eq. 2: the mean absolute value over every element of the tensor (fp64)."""
     W = np.asarray(W, dtype=np.float64)
@@ -680,7 +707,7 @@ def gemm_abs_bound(A, B) -> np.ndarray:
 
 __all__ = [
     "bf16_round", "bf16_to_f32", "E4M3_VALUES", "e4m3_encode", "e4m3_decode",
-    "pack_ternary", "unpack_ternary", "absmean", "absmean_init", "act_quant",
+    "pack_ternary", "unpack_ternary", "pack_int3", "unpack_int3", "absmean", "absmean_init", "act_quant",
     "act_values", "act_dequant", "cast_out", "linear_fwd", "linear_bwd",
     "philox4x32_10", "rng_u32", "sr_step_size", "sr_update",
     "sr_change_probability", "linear_train_step", "gemm_abs_bound",

@@ -27,6 +27,8 @@ dqt_status check_weight(const dqt_weight* w) {
     if (w->qmin < -128 || w->qmax > 127 || w->qmin >= w->qmax) return DQT_ERR_RANGE;
   } else if (w->wfmt == DQT_INT4) {
     if (w->qmin < -8 || w->qmax > 7 || w->qmin >= w->qmax) return DQT_ERR_RANGE;
+  } else if (w->wfmt == DQT_INT3) {
+    if (w->qmin < -4 || w->qmax > 3 || w->qmin >= w->qmax) return DQT_ERR_RANGE;
   } else {
     return DQT_ERR_DTYPE;
   }
@@ -35,7 +37,9 @@ dqt_status check_weight(const dqt_weight* w) {
 }
 
 // code format of the update kernels: 0 int8, 1 ternary 2-bit, 2 int4 nibbles
-int code_format(int32_t wfmt) { return wfmt == DQT_TERNARY2 ? 1 : wfmt == DQT_INT4 ? 2 : 0; }
+int code_format(int32_t wfmt) {
+  return wfmt == DQT_TERNARY2 ? 1 : wfmt == DQT_INT4 ? 2 : wfmt == DQT_INT3 ? 3 : 0;
+}
 
 bool is_float_type(int32_t t) { return t == DQT_F32 || t == DQT_BF16; }
 
@@ -165,6 +169,7 @@ dqt_status dqt_linear_fwd_batch(int32_t n, const dqt_linear_io* io, int64_t M, i
   if (need > 0 && !aligned16(ws)) return DQT_ERR_ALIGN;
   dqt::BatchCfg c{n, M, wfmt == DQT_TERNARY2, act_q == DQT_FP8E4M3, y_t == DQT_BF16};
   c.w_int4 = wfmt == DQT_INT4;
+  c.w_int3 = wfmt == DQT_INT3;
   return from_hip(dqt::launch_fwd_batch(c, L, static_cast<uint8_t*>(ws), static_cast<hipStream_t>(stream)));
 }
 
@@ -221,6 +226,7 @@ dqt_status dqt_linear_bwd_batch(int32_t n, const dqt_linear_io* io, int64_t M, i
   if (both) {
     dqt::BatchCfg c{n, M, wfmt == DQT_TERNARY2, act_q == DQT_FP8E4M3, dx_t == DQT_BF16};
     c.w_int4 = wfmt == DQT_INT4;
+    c.w_int3 = wfmt == DQT_INT3;
     return from_hip(dqt::launch_dxdw_batch(c, L, wsb, P, s));
   }
   // dX for the linears that want it
@@ -235,16 +241,19 @@ dqt_status dqt_linear_bwd_batch(int32_t n, const dqt_linear_io* io, int64_t M, i
     if (dy_t == DQT_BF16) {
       dqt::BatchCfg c{nx, M, wfmt == DQT_TERNARY2, act_q == DQT_FP8E4M3, dx_t == DQT_BF16};
       c.w_int4 = wfmt == DQT_INT4;
+      c.w_int3 = wfmt == DQT_INT3;
       st = from_hip(dqt::launch_dx_batch(c, sub, wsb, Px, s));
     } else {
       for (int l = 0; l < nx && st == DQT_OK; ++l) {
         dqt::DxArgs a;
         a.dY = sub[l].dY;
         a.Wq = sub[l].Wq;
-        if (wfmt == DQT_INT4) {
-          // nibbles -> one int8 code per weight, in the weight area of the workspace
+        if (wfmt == DQT_INT4 || wfmt == DQT_INT3) {
+          // packed codes -> one int8 code per weight, in the weight area of the workspace
           int8_t* q8 = reinterpret_cast<int8_t*>(wsb + Px.q_off[l]);
-          st = from_hip(dqt::launch_unpack_int4(sub[l].Wq, q8, sub[l].d_out * sub[l].d_in, s));
+          const int64_t nwt = sub[l].d_out * sub[l].d_in;
+          st = from_hip(wfmt == DQT_INT4 ? dqt::launch_unpack_int4(sub[l].Wq, q8, nwt, s)
+                                         : dqt::launch_unpack_int3(sub[l].Wq, q8, nwt, s));
           if (st != DQT_OK) break;
           a.Wq = q8;
         }
@@ -274,6 +283,7 @@ dqt_status dqt_linear_bwd_batch(int32_t n, const dqt_linear_io* io, int64_t M, i
     if (xt_t == DQT_BF16) {
       dqt::BatchCfg c{nw, M, wfmt == DQT_TERNARY2, act_q == DQT_FP8E4M3, false};
       c.w_int4 = wfmt == DQT_INT4;
+      c.w_int3 = wfmt == DQT_INT3;
       st = from_hip(dqt::launch_dw_batch(c, sub, wsb, Pw, s));
     } else {
       for (int l = 0; l < nw && st == DQT_OK; ++l) {
@@ -342,6 +352,7 @@ dqt_status dqt_linear_bwd_sr_batch(int32_t n, const dqt_linear_io* io, int64_t M
   uint8_t* wsb = static_cast<uint8_t*>(ws);
   dqt::BatchCfg c{n, M, wfmt == DQT_TERNARY2, act_q == DQT_FP8E4M3, dx_t == DQT_BF16};
   c.w_int4 = wfmt == DQT_INT4;
+  c.w_int3 = wfmt == DQT_INT3;
   if (nx > 0 && nx < n) {
     // dX of the linears that want it first (it reads the codes before the
     // update), then dW and the update of every linear
@@ -355,6 +366,7 @@ dqt_status dqt_linear_bwd_sr_batch(int32_t n, const dqt_linear_io* io, int64_t M
       }
     dqt::BatchCfg cx{nx, M, c.w_ternary, c.act_e4m3, c.out_bf16};
     cx.w_int4 = wfmt == DQT_INT4;
+    cx.w_int3 = wfmt == DQT_INT3;
     st = from_hip(dqt::launch_dx_batch(cx, sub, wsb, Px, s));
     if (st != DQT_OK) return st;
   }
@@ -702,6 +714,42 @@ dqt_status dqt_unpack_int4(const uint8_t* packed, int64_t rows, int64_t cols, in
         const int v = (packed[r * pc + b] >> (4 * j)) & 0xF;
         q[r * cols + 2 * b + j] = (int8_t)(v >= 8 ? v - 16 : v);
       }
+  return DQT_OK;
+}
+
+dqt_status dqt_pack_int3(const int8_t* q, int64_t rows, int64_t cols, uint8_t* packed) {
+  if (q == nullptr || packed == nullptr) return DQT_ERR_NULL;
+  if (rows < 0 || cols < 0 || (cols % 8) != 0) return DQT_ERR_SHAPE;
+  const int64_t groups = cols / 8;
+  for (int64_t r = 0; r < rows; ++r)
+    for (int64_t g = 0; g < groups; ++g) {
+      uint32_t bits = 0;
+      for (int j = 0; j < 8; ++j) {
+        const int v = q[r * cols + 8 * g + j];
+        if (v < -4 || v > 3) return DQT_ERR_RANGE;
+        bits |= ((uint32_t)v & 7u) << (3 * j);
+      }
+      uint8_t* p = packed + r * (3 * groups) + 3 * g;
+      p[0] = (uint8_t)bits;
+      p[1] = (uint8_t)(bits >> 8);
+      p[2] = (uint8_t)(bits >> 16);
+    }
+  return DQT_OK;
+}
+
+dqt_status dqt_unpack_int3(const uint8_t* packed, int64_t rows, int64_t cols, int8_t* q) {
+  if (q == nullptr || packed == nullptr) return DQT_ERR_NULL;
+  if (rows < 0 || cols < 0 || (cols % 8) != 0) return DQT_ERR_SHAPE;
+  const int64_t groups = cols / 8;
+  for (int64_t r = 0; r < rows; ++r)
+    for (int64_t g = 0; g < groups; ++g) {
+      const uint8_t* p = packed + r * (3 * groups) + 3 * g;
+      const uint32_t bits = (uint32_t)p[0] | ((uint32_t)p[1] << 8) | ((uint32_t)p[2] << 16);
+      for (int j = 0; j < 8; ++j) {
+        const int v = (int)((bits >> (3 * j)) & 7u);
+        q[r * cols + 8 * g + j] = (int8_t)(v >= 4 ? v - 8 : v);
+      }
+    }
   return DQT_OK;
 }
 

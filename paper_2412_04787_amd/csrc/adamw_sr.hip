@@ -57,7 +57,7 @@ __global__ __launch_bounds__(256) void adamw_sr_kernel(const AdamTab tab,
   int sidx = 0, ns = 0;
   int64_t nt = 0;
   f32x4 ng[2], nm[2], nv[2];
-  uint32_t nw[2] = {0u, 0u};
+  uint32_t nw[4] = {0u, 0u, 0u, 0u};
   auto fetch = [&](int64_t tl) {
     while (sidx + 1 < tab.n && tl >= tab.b0[sidx + 1]) ++sidx;    // tiles ascend
     ns = sidx;
@@ -72,15 +72,7 @@ __global__ __launch_bounds__(256) void adamw_sr_kernel(const AdamTab tab,
         nm[u] = __builtin_nontemporal_load(mp + u);
         nv[u] = __builtin_nontemporal_load(vp + u);
       }
-      if constexpr (CF == CF_T2) {
-        nw[0] = reinterpret_cast<const uint16_t*>(tab.wq[sidx])[nt];
-      } else if constexpr (CF == CF_I4) {
-        nw[0] = reinterpret_cast<const uint32_t*>(tab.wq[sidx])[nt];
-      } else {
-        const uint2 w = reinterpret_cast<const uint2*>(tab.wq[sidx])[nt];
-        nw[0] = w.x;
-        nw[1] = w.y;
-      }
+      ChunkIO<CF>::load(tab.wq[sidx], nt, nw);
     }
   };
   if ((int64_t)blockIdx.x < ntiles) fetch(blockIdx.x);
@@ -131,9 +123,7 @@ __global__ __launch_bounds__(256) void adamw_sr_kernel(const AdamTab tab,
     mp[1] = mo[1];
     vp[0] = vo[0];
     vp[1] = vo[1];
-    if constexpr (CF == CF_T2) reinterpret_cast<uint16_t*>(tab.wq[s])[t] = (uint16_t)wout[0];
-    else if constexpr (CF == CF_I4) reinterpret_cast<uint32_t*>(tab.wq[s])[t] = wout[0];
-    else reinterpret_cast<uint2*>(tab.wq[s])[t] = make_uint2(wout[0], wout[1]);
+    ChunkIO<CF>::store(tab.wq[s], t, wout);
   }
   if (counters != nullptr) {
     changed = wave_sum_u64(changed);
@@ -217,10 +207,12 @@ hipError_t launch_adamw_sr(int cf, int n, const AdamTensor* t, const AdamHyper& 
   const int64_t cap = adam_resident_blocks(
       cf == CF_T2 ? reinterpret_cast<const void*>(adamw_sr_kernel<CF_T2>)
                   : cf == CF_I4 ? reinterpret_cast<const void*>(adamw_sr_kernel<CF_I4>)
+                  : cf == CF_I3 ? reinterpret_cast<const void*>(adamw_sr_kernel<CF_I3>)
                                 : reinterpret_cast<const void*>(adamw_sr_kernel<CF_I8>));
   const unsigned blocks = (unsigned)(tiles < cap ? tiles : cap);
   if (cf == CF_T2) return launch_kernel(adamw_sr_kernel<CF_T2>, dim3(blocks), dim3(256), stream, tab, counters);
   if (cf == CF_I4) return launch_kernel(adamw_sr_kernel<CF_I4>, dim3(blocks), dim3(256), stream, tab, counters);
+  if (cf == CF_I3) return launch_kernel(adamw_sr_kernel<CF_I3>, dim3(blocks), dim3(256), stream, tab, counters);
   return launch_kernel(adamw_sr_kernel<CF_I8>, dim3(blocks), dim3(256), stream, tab, counters);
 }
 

@@ -103,6 +103,7 @@ struct BatchCfg {
   int64_t M;
   bool w_ternary, act_e4m3, out_bf16;
   bool w_int4;          // 4-bit codes (two's-complement nibbles)
+  bool w_int3;          // 3-bit codes (8 weights in 3 bytes)
 };
 struct BwdPlan {
   int64_t splits;        // dW batch splits when dW runs in a launch of its own
@@ -114,6 +115,8 @@ struct BwdPlan {
 size_t fwd_batch_workspace(int n, const LinearIO* io, int cf, size_t* offs);
 // int4 codes [n] -> int8 codes (one byte per weight), n a multiple of 16
 hipError_t launch_unpack_int4(const void* src, int8_t* dst, int64_t n, hipStream_t stream);
+// int3 codes [n] -> int8 codes, n a multiple of 16
+hipError_t launch_unpack_int3(const void* src, int8_t* dst, int64_t n, hipStream_t stream);
 hipError_t launch_fwd_batch(const BatchCfg& c, const LinearIO* io, uint8_t* ws, hipStream_t stream);
 BwdPlan plan_bwd_batch(int n, const LinearIO* io, int64_t M);
 hipError_t launch_dx_batch(const BatchCfg& c, const LinearIO* io, uint8_t* ws, const BwdPlan& P,
@@ -146,7 +149,7 @@ struct SRTensor {
   uint32_t tensor_id;
   float alpha;
 };
-// cf: code format, 0 int8, 1 ternary 2-bit, 2 int4 nibbles
+// cf: code format, 0 int8, 1 ternary 2-bit, 2 int4 nibbles, 3 int3 fields
 hipError_t launch_sr_update(int cf, int n, const SRTensor* t, uint64_t seed, uint32_t step,
                             unsigned long long* counters, hipStream_t stream);
 // One tensor of a device-resident update table (dqt_sr_table_build's

@@ -651,6 +651,12 @@ __device__ __forceinline__ void gemm_v3_body(const Group<Epi>& grp, lds_u8* smem
               const uint8_t* src = ok ? epi.wq + n * epi.ldc + (k >> 1) : dummy;
               sr8[ta][tb][u][0] = *reinterpret_cast<const uint32_t*>(src);
               sr8[ta][tb][u][1] = 0;
+            } else if constexpr (Epi::kCF == CF_I3) {
+              // three bytes (k / 8 chunks of 3 bytes into the row)
+              uint32_t w[4];
+              ChunkIO<CF_I3>::load(ok ? epi.wq + n * epi.ldc : dummy, ok ? (k >> 3) : 0, w);
+              sr8[ta][tb][u][0] = w[0];
+              sr8[ta][tb][u][1] = 0;
             } else {
               const uint8_t* src = ok ? epi.wq + n * epi.ldc + k : dummy;
               const uint2 v = *reinterpret_cast<const uint2*>(src);
@@ -818,6 +824,10 @@ __device__ __forceinline__ void gemm_v3_body(const Group<Epi>& grp, lds_u8* smem
           } else if constexpr (Epi::kCF == CF_I4) {
             uint8_t* dst = ok ? epi.wq + n * epi.ldc + (k >> 1) : dummy;
             *reinterpret_cast<uint32_t*>(dst) = wout[0];
+          } else if constexpr (Epi::kCF == CF_I3) {
+            // (three single-byte stores: the vmcnt accounting above counts
+            // one per chunk, a lower bound, which only makes waits stricter)
+            ChunkIO<CF_I3>::store(ok ? epi.wq + n * epi.ldc : dummy, ok ? (k >> 3) : 0, wout);
           } else {
             uint8_t* dst = ok ? epi.wq + n * epi.ldc + k : dummy;
             *reinterpret_cast<uint2*>(dst) = make_uint2(wout[0], wout[1]);
@@ -997,6 +1007,26 @@ __global__ __launch_bounds__(256) void unpack_int4_kernel(const SegTab tab) {
   static_cast<uint4*>(tab.dst[s])[t] = make_uint4(o[0], o[1], o[2], o[3]);
 }
 
+// 3-bit codes (8 weights in 3 bytes, weight k at bits 3 (k mod 8) of its
+// group) -> one operand byte per weight (int8, or e4m3, exact for |q| <= 4),
+// same order; 16 weights (6 bytes, read as three 2-byte words) per thread.
+template <int OUT>   // 0: int8, 1: e4m3
+__global__ __launch_bounds__(256) void unpack_int3_kernel(const SegTab tab) {
+  const int s = seg_of_block(tab);
+  const int64_t t = (int64_t)(blockIdx.x - tab.b0[s]) * 256 + threadIdx.x;
+  if (t >= tab.n16[s]) return;
+  const uint16_t* src = static_cast<const uint16_t*>(tab.src[s]) + 3 * t;
+  const uint64_t bits = (uint64_t)src[0] | ((uint64_t)src[1] << 16) | ((uint64_t)src[2] << 32);
+  uint32_t o[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+  for (int e = 0; e < 16; ++e) {
+    const int q = (int)((uint32_t)(bits >> (3 * e)) << 29) >> 29;
+    const uint32_t b = OUT == 1 ? f32_to_e4m3((float)q) : ((uint32_t)q & 0xFFu);
+    o[e >> 2] |= b << (8 * (e & 3));
+  }
+  static_cast<uint4*>(tab.dst[s])[t] = make_uint4(o[0], o[1], o[2], o[3]);
+}
+
 // int8 codes -> bf16 (|q| <= 128 is exact in bf16).
 // Weights q [d_out][d_in] (packed ternary codes, or int8) -> the B operand of
 // dX with the reduction contiguous: W~T[k][n] = bf16(q[n][k]), rows of d_out
@@ -1028,6 +1058,15 @@ __global__ __launch_bounds__(256) void unpack_t_kernel(const TrTab tab) {
         const uint32_t w = *reinterpret_cast<const uint32_t*>(tab.src[s] + (int64_t)n * (d_in / 4) + k / 4);
 #pragma unroll
         for (int e = 0; e < 16; ++e) v[e] = (uint16_t)code_to_bf16_bits((w >> (2 * e)) & 3u);
+      } else if constexpr (CF == CF_I3) {
+        // 16 weights: 6 bytes at 3 k / 8 (k a multiple of 16: 2-byte aligned)
+        const uint16_t* w3 = reinterpret_cast<const uint16_t*>(tab.src[s] + (int64_t)n * (3 * d_in / 8) + 3 * k / 8);
+        const uint64_t bits = (uint64_t)w3[0] | ((uint64_t)w3[1] << 16) | ((uint64_t)w3[2] << 32);
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const float f = (float)((int)((uint32_t)(bits >> (3 * e)) << 29) >> 29);
+          v[e] = (uint16_t)(__float_as_uint(f) >> 16);   // exact: |q| <= 4
+        }
       } else if constexpr (CF == CF_I4) {
         const uint2 w2 = *reinterpret_cast<const uint2*>(tab.src[s] + (int64_t)n * (d_in / 2) + k / 2);
         const uint32_t w[2] = {w2.x, w2.y};
@@ -1203,25 +1242,28 @@ __global__ __launch_bounds__(256) void split_reduce_sr_kernel(const RedSRTab tab
     a.step = tab.step;
     a.tid = tab.tid[s];
     uint32_t win[4] = {0u, 0u, 0u, 0u}, wout[4];
-    if constexpr (CF == CF_T2) {
-      win[0] = reinterpret_cast<const uint16_t*>(tab.wq[s])[t];
-    } else if constexpr (CF == CF_I4) {
-      win[0] = reinterpret_cast<const uint32_t*>(tab.wq[s])[t];
-    } else {
-      const uint2 v = reinterpret_cast<const uint2*>(tab.wq[s])[t];
-      win[0] = v.x;
-      win[1] = v.y;
-    }
+    ChunkIO<CF>::load(tab.wq[s], t, win);
     sr_chunk<CF, 8>(win, gv, (uint64_t)t, a, wout, ch, nf);
-    if constexpr (CF == CF_T2) reinterpret_cast<uint16_t*>(tab.wq[s])[t] = (uint16_t)wout[0];
-    else if constexpr (CF == CF_I4) reinterpret_cast<uint32_t*>(tab.wq[s])[t] = wout[0];
-    else reinterpret_cast<uint2*>(tab.wq[s])[t] = make_uint2(wout[0], wout[1]);
+    ChunkIO<CF>::store(tab.wq[s], t, wout);
   }
   if (tab.counters != nullptr) {
-    const unsigned long long c = wave_sum_u64(ch), f = wave_sum_u64(nf);
+    // one atomic per block (atomics of every wave on one address serialise)
+    __shared__ uint32_t red[2][256 / kWave];
+    const uint32_t c = wave_sum_u32(ch), f = wave_sum_u32(nf);
     if ((threadIdx.x & (kWave - 1)) == 0) {
-      if (c) atomicAdd(tab.counters, c);
-      if (f) atomicAdd(tab.counters + 1, f);
+      red[0][threadIdx.x / kWave] = c;
+      red[1][threadIdx.x / kWave] = f;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      unsigned long long ct = 0, ft = 0;
+#pragma unroll
+      for (int w = 0; w < 256 / kWave; ++w) {
+        ct += red[0][w];
+        ft += red[1][w];
+      }
+      if (ct) atomicAdd(tab.counters, ct);
+      if (ft) atomicAdd(tab.counters + 1, ft);
     }
   }
 }
@@ -1321,6 +1363,17 @@ using namespace v3;
 
 static size_t align256(size_t n) { return (n + 255) / 256 * 256; }
 
+hipError_t launch_unpack_int3(const void* src, int8_t* dst, int64_t n, hipStream_t stream) {
+  if (n == 0) return hipSuccess;
+  SegTab tab{};
+  tab.n = 1;
+  tab.src[0] = src;
+  tab.dst[0] = dst;
+  tab.n16[0] = n / 16;
+  const int32_t blocks = seal(tab);
+  return launch_kernel(unpack_int3_kernel<0>, dim3(blocks), dim3(256), stream, tab);
+}
+
 hipError_t launch_unpack_int4(const void* src, int8_t* dst, int64_t n, hipStream_t stream) {
   if (n == 0) return hipSuccess;
   SegTab tab{};
@@ -1343,7 +1396,7 @@ static bool fwd_packed(int n, const LinearIO* io) {
 
 size_t fwd_batch_workspace(int n, const LinearIO* io, int cf, size_t* offs) {
   size_t total = kSchedBytes;
-  const bool unpack = (cf == CF_T2 && !fwd_packed(n, io)) || cf == CF_I4;
+  const bool unpack = (cf == CF_T2 && !fwd_packed(n, io)) || cf == CF_I4 || cf == CF_I3;
   for (int l = 0; l < n; ++l) {
     if (offs) offs[l] = total;
     if (unpack) total += align256((size_t)(io[l].d_out * io[l].d_in));
@@ -1355,10 +1408,24 @@ hipError_t launch_fwd_batch(const BatchCfg& c, const LinearIO* io, uint8_t* ws, 
   if (c.M == 0 || c.n == 0) return hipSuccess;
   LaunchStatus st;
   size_t offs[kMaxBatch];
-  fwd_batch_workspace(c.n, io, c.w_ternary ? CF_T2 : c.w_int4 ? CF_I4 : CF_I8, offs);
+  fwd_batch_workspace(c.n, io, c.w_ternary ? CF_T2 : c.w_int4 ? CF_I4 : c.w_int3 ? CF_I3 : CF_I8, offs);
   const bool packed = c.w_ternary && fwd_packed(c.n, io);
-  const bool unpacked = (c.w_ternary && !packed) || c.w_int4;   // int8 copy in the workspace
-  if (c.w_int4) {
+  // int8 (or e4m3) copy of the codes in the workspace
+  const bool unpacked = (c.w_ternary && !packed) || c.w_int4 || c.w_int3;
+  if (c.w_int3) {
+    SegTab tab{};
+    tab.n = c.n;
+    for (int l = 0; l < c.n; ++l) {
+      tab.src[l] = io[l].Wq;
+      tab.dst[l] = ws + offs[l];
+      tab.n16[l] = io[l].d_out * io[l].d_in / 16;
+    }
+    const int32_t blocks = seal(tab);
+    if (c.act_e4m3)
+      st << launch_kernel(unpack_int3_kernel<1>, dim3(blocks), dim3(256), stream, tab);
+    else
+      st << launch_kernel(unpack_int3_kernel<0>, dim3(blocks), dim3(256), stream, tab);
+  } else if (c.w_int4) {
     SegTab tab{};
     tab.n = c.n;
     for (int l = 0; l < c.n; ++l) {
@@ -1528,6 +1595,8 @@ static void prep_dx(const BatchCfg& c, const LinearIO* io, uint8_t* ws, const Bw
     st << launch_kernel(unpack_t_kernel<CF_T2>, dim3(blocks), dim3(256), stream, tab);
   else if (c.w_int4)
     st << launch_kernel(unpack_t_kernel<CF_I4>, dim3(blocks), dim3(256), stream, tab);
+  else if (c.w_int3)
+    st << launch_kernel(unpack_t_kernel<CF_I3>, dim3(blocks), dim3(256), stream, tab);
   else
     st << launch_kernel(unpack_t_kernel<CF_I8>, dim3(blocks), dim3(256), stream, tab);
 }
@@ -1694,6 +1763,8 @@ static hipError_t reduce_sr(const BatchCfg& c, const LinearIO* io, const SRTenso
     st << launch_kernel(split_reduce_sr_kernel<CF_T2>, dim3((unsigned)blocks), dim3(256), stream, red);
   else if (c.w_int4)
     st << launch_kernel(split_reduce_sr_kernel<CF_I4>, dim3((unsigned)blocks), dim3(256), stream, red);
+  else if (c.w_int3)
+    st << launch_kernel(split_reduce_sr_kernel<CF_I3>, dim3((unsigned)blocks), dim3(256), stream, red);
   else
     st << launch_kernel(split_reduce_sr_kernel<CF_I8>, dim3((unsigned)blocks), dim3(256), stream, red);
   return st.e;
@@ -1711,7 +1782,7 @@ static hipError_t launch_dw_sr_group(const BatchCfg& c, const LinearIO* io, cons
   fill_dw(c, io, ws, P, first, gw, [&](int l) {
     EpiSR<CF> e;
     e.wq = t[l].wq;
-    e.ldc = CF == CF_T2 ? io[l].d_in / 4 : CF == CF_I4 ? io[l].d_in / 2 : io[l].d_in;
+    e.ldc = io[l].d_in / 8 * chunk_code_bytes<CF>();
     e.d_in = io[l].d_in;
     e.c = t[l].c;
     e.L = (float)(t[l].qmax - t[l].qmin + 1);
@@ -1749,6 +1820,7 @@ hipError_t launch_bwd_sr_batch(const BatchCfg& c, const LinearIO* io, const SRTe
     Group<EpiScale>* const pgx = with_dx ? &gx : nullptr;
     if (c.w_ternary) st << launch_dw_sr_group<CF_T2>(c, io, t, seed, step, counters, ws, Q, first, pgx, stream);
     else if (c.w_int4) st << launch_dw_sr_group<CF_I4>(c, io, t, seed, step, counters, ws, Q, first, pgx, stream);
+    else if (c.w_int3) st << launch_dw_sr_group<CF_I3>(c, io, t, seed, step, counters, ws, Q, first, pgx, stream);
     else st << launch_dw_sr_group<CF_I8>(c, io, t, seed, step, counters, ws, Q, first, pgx, stream);
     return st.e;
   }

@@ -121,15 +121,21 @@ __device__ __forceinline__ int sr_fast(int code, float g, uint32_t P, float nc, 
 
 // Code formats of the weights: CF_I8 one byte per weight (two's complement),
 // CF_T2 2-bit ternary (code q + 1 at bits 2k of the chunk's first word),
-// CF_I4 two's-complement nibbles (weight k at bits 4 (k mod 8) of word k / 8).
+// CF_I4 two's-complement nibbles (weight k at bits 4 (k mod 8) of word k / 8),
+// CF_I3 3-bit two's-complement fields, 8 weights in 3 bytes (weight k at
+// bits 3 k of the chunk's 24-bit little-endian group).
 // A chunk's codes sit in words w[0 .. 3]; `field` is what the fast rule
 // moves (q + off, clamped to [qmin + off, qmax + off]).
-constexpr int CF_I8 = 0, CF_T2 = 1, CF_I4 = 2;
+constexpr int CF_I8 = 0, CF_T2 = 1, CF_I4 = 2, CF_I3 = 3;
+// Bytes of codes per chunk of 8 weights.
+template <int CF>
+constexpr int chunk_code_bytes() { return CF == CF_T2 ? 2 : CF == CF_I3 ? 3 : CF == CF_I4 ? 4 : 8; }
 template <int CF>
 struct CodeFmt {
   static constexpr int off = CF == CF_T2 ? 1 : 0;
   __device__ static int field(const uint32_t (&w)[4], int j) {
     if constexpr (CF == CF_T2) return (int)((w[0] >> (2 * j)) & 3u);
+    else if constexpr (CF == CF_I3) return (int)(w[0] << (29 - 3 * j)) >> 29;
     else if constexpr (CF == CF_I4) return (int)(w[j >> 3] << (28 - 4 * (j & 7))) >> 28;
     else return (int)(int8_t)(w[j >> 2] >> (8 * (j & 3)));
   }
@@ -137,12 +143,14 @@ struct CodeFmt {
   // ORs field v of weight j into zeroed words
   __device__ static void put(uint32_t (&w)[4], int j, int v) {
     if constexpr (CF == CF_T2) w[0] |= (uint32_t)v << (2 * j);
+    else if constexpr (CF == CF_I3) w[0] |= ((uint32_t)v & 7u) << (3 * j);
     else if constexpr (CF == CF_I4) w[j >> 3] |= ((uint32_t)v & 0xFu) << (4 * (j & 7));
     else w[j >> 2] |= ((uint32_t)v & 0xFFu) << (8 * (j & 3));
   }
   // replaces field j by v
   __device__ static void set(uint32_t (&w)[4], int j, int v) {
     if constexpr (CF == CF_T2) w[0] = (w[0] & ~(3u << (2 * j))) | ((uint32_t)v << (2 * j));
+    else if constexpr (CF == CF_I3) w[0] = (w[0] & ~(7u << (3 * j))) | (((uint32_t)v & 7u) << (3 * j));
     else if constexpr (CF == CF_I4)
       w[j >> 3] = (w[j >> 3] & ~(0xFu << (4 * (j & 7)))) | (((uint32_t)v & 0xFu) << (4 * (j & 7)));
     else w[j >> 2] = (w[j >> 2] & ~(0xFFu << (8 * (j & 3)))) | (((uint32_t)v & 0xFFu) << (8 * (j & 3)));
@@ -154,6 +162,9 @@ struct CodeFmt {
     if constexpr (CF == CF_T2) {
       const uint32_t x = a[0] ^ b[0];
       n = __builtin_popcount((x | (x >> 1)) & 0x55555555u);
+    } else if constexpr (CF == CF_I3) {
+      const uint32_t x = a[0] ^ b[0];
+      n = __builtin_popcount((x | (x >> 1) | (x >> 2)) & 0x00249249u);
     } else if constexpr (CF == CF_I4) {
 #pragma unroll
       for (int w = 0; w < (CW + 7) / 8; ++w) {   // (fields past CW weights are zero in both)
@@ -168,6 +179,43 @@ struct CodeFmt {
       }
     }
     return n;
+  }
+};
+
+// The codes of chunk t (8 consecutive weights, chunk_code_bytes<CF>() bytes
+// from byte t * that) of a code array, into / from words w[0 .. 1].  Lanes
+// own whole chunks, so no two lanes write one byte.  3-byte chunks are
+// moved a byte at a time (their alignment varies).
+template <int CF>
+struct ChunkIO {
+  static constexpr int NB = chunk_code_bytes<CF>();
+  __device__ static void load(const uint8_t* wq, int64_t t, uint32_t (&w)[4]) {
+    if constexpr (NB == 2) {
+      w[0] = reinterpret_cast<const uint16_t*>(wq)[t];
+    } else if constexpr (NB == 3) {
+      const uint8_t* p = wq + 3 * t;
+      w[0] = (uint32_t)p[0] | ((uint32_t)p[1] << 8) | ((uint32_t)p[2] << 16);
+    } else if constexpr (NB == 4) {
+      w[0] = reinterpret_cast<const uint32_t*>(wq)[t];
+    } else {
+      const uint2 v = reinterpret_cast<const uint2*>(wq)[t];
+      w[0] = v.x;
+      w[1] = v.y;
+    }
+  }
+  __device__ static void store(uint8_t* wq, int64_t t, const uint32_t (&w)[4]) {
+    if constexpr (NB == 2) {
+      reinterpret_cast<uint16_t*>(wq)[t] = (uint16_t)w[0];
+    } else if constexpr (NB == 3) {
+      uint8_t* p = wq + 3 * t;
+      p[0] = (uint8_t)w[0];
+      p[1] = (uint8_t)(w[0] >> 8);
+      p[2] = (uint8_t)(w[0] >> 16);
+    } else if constexpr (NB == 4) {
+      reinterpret_cast<uint32_t*>(wq)[t] = w[0];
+    } else {
+      reinterpret_cast<uint2*>(wq)[t] = make_uint2(w[0], w[1]);
+    }
   }
 };
 

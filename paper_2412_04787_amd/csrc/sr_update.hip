@@ -62,29 +62,6 @@ struct SRDevTab {
   }
 };
 
-// Code words of one chunk of 8 weights in format CF: 2-bit ternary codes
-// (2 bytes), nibbles (4 bytes) or int8 codes (8 bytes).
-template <int CF>
-struct CodeIO {
-  static constexpr int NBYTES = CF == CF_T2 ? 2 : CF == CF_I4 ? 4 : 8;
-  __device__ static void load(const uint8_t* wq, int64_t t, uint32_t (&w)[2]) {
-    if constexpr (NBYTES == 2) {
-      w[0] = reinterpret_cast<const uint16_t*>(wq)[t];
-    } else if constexpr (NBYTES == 4) {
-      w[0] = reinterpret_cast<const uint32_t*>(wq)[t];
-    } else {
-      const uint2 v = reinterpret_cast<const uint2*>(wq)[t];
-      w[0] = v.x;
-      w[1] = v.y;
-    }
-  }
-  __device__ static void store(uint8_t* wq, int64_t t, const uint32_t (&w)[4]) {
-    if constexpr (NBYTES == 2) reinterpret_cast<uint16_t*>(wq)[t] = (uint16_t)w[0];
-    else if constexpr (NBYTES == 4) reinterpret_cast<uint32_t*>(wq)[t] = w[0];
-    else reinterpret_cast<uint2*>(wq)[t] = make_uint2(w[0], w[1]);
-  }
-};
-
 // Sum of a per-lane count over the block (every thread gets it; the block
 // runs this in uniform control flow).  `red` holds one slot per wave.
 __device__ __forceinline__ uint32_t block_sum(uint32_t v, uint32_t* red) {
@@ -110,7 +87,7 @@ __global__ __launch_bounds__(256) void sr_update_kernel(const Tab tab, int64_t n
                                                         uint32_t k1, uint32_t step,
                                                         unsigned long long* __restrict__ counters,
                                                         unsigned long long* __restrict__ per_tensor) {
-  using CIO = CodeIO<CF>;
+  using CIO = ChunkIO<CF>;
   // tiles b, b + G, ... of the launch (few tensors: the front of loads
   // sweeps through memory together), or the contiguous range
   // [b T / G, (b + 1) T / G) (many tensors: a block meets few boundaries)
@@ -132,7 +109,7 @@ __global__ __launch_bounds__(256) void sr_update_kernel(const Tab tab, int64_t n
   SRDesc dn = tab.get(s0);          // tensor of the next tile to load
   int sn = s0;
   f32x4 ng[2];
-  uint32_t nw[2] = {0u, 0u};
+  uint32_t nw[4] = {0u, 0u, 0u, 0u};
   int64_t nt = 0;
   int ns = s0;
   auto fetch = [&](int64_t tl) {
@@ -242,6 +219,7 @@ static hipError_t launch_sr(int cf, const Tab& tab, int64_t tiles, uint64_t seed
   if (tiles == 0) return hipSuccess;
   if (cf == CF_T2) return launch_sr_cf<CF_T2>(tab, tiles, seed, step, counters, per_tensor, stream);
   if (cf == CF_I4) return launch_sr_cf<CF_I4>(tab, tiles, seed, step, counters, per_tensor, stream);
+  if (cf == CF_I3) return launch_sr_cf<CF_I3>(tab, tiles, seed, step, counters, per_tensor, stream);
   return launch_sr_cf<CF_I8>(tab, tiles, seed, step, counters, per_tensor, stream);
 }
 

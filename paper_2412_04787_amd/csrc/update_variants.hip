@@ -183,15 +183,7 @@ __global__ __launch_bounds__(256) void variant_update_kernel(const VarTab tab, c
     const f32x4* gp = reinterpret_cast<const f32x4*>(tab.grad[s]) + 2 * t;
     const f32x4 gv[2] = {__builtin_nontemporal_load(gp), __builtin_nontemporal_load(gp + 1)};
     uint32_t win[4] = {0u, 0u, 0u, 0u};
-    if constexpr (CF == CF_T2) {
-      win[0] = reinterpret_cast<const uint16_t*>(tab.wq[s])[t];
-    } else if constexpr (CF == CF_I4) {
-      win[0] = reinterpret_cast<const uint32_t*>(tab.wq[s])[t];
-    } else {
-      const uint2 w = reinterpret_cast<const uint2*>(tab.wq[s])[t];
-      win[0] = w.x;
-      win[1] = w.y;
-    }
+    ChunkIO<CF>::load(tab.wq[s], t, win);
     SRArgs a;
     a.c = tab.c[s];
     a.L = tab.L[s];
@@ -218,9 +210,7 @@ __global__ __launch_bounds__(256) void variant_update_kernel(const VarTab tab, c
       CodeFmt<CF>::set(wout, j, v + CodeFmt<CF>::off);
     }
     changed += CodeFmt<CF>::template changed<8>(wout, win);
-    if constexpr (CF == CF_T2) reinterpret_cast<uint16_t*>(tab.wq[s])[t] = (uint16_t)wout[0];
-    else if constexpr (CF == CF_I4) reinterpret_cast<uint32_t*>(tab.wq[s])[t] = wout[0];
-    else reinterpret_cast<uint2*>(tab.wq[s])[t] = make_uint2(wout[0], wout[1]);
+    ChunkIO<CF>::store(tab.wq[s], t, wout);
   }
   if (counters != nullptr) {
     changed = wave_sum_u64(changed);
@@ -295,6 +285,8 @@ hipError_t launch_update_variant(int cf, int n, const SRTensor* t, int mode, flo
     ls << launch_kernel(variant_update_kernel<CF_T2>, dim3(grid), dim3(256), stream, tab, st, counters);
   else if (cf == CF_I4)
     ls << launch_kernel(variant_update_kernel<CF_I4>, dim3(grid), dim3(256), stream, tab, st, counters);
+  else if (cf == CF_I3)
+    ls << launch_kernel(variant_update_kernel<CF_I3>, dim3(grid), dim3(256), stream, tab, st, counters);
   else
     ls << launch_kernel(variant_update_kernel<CF_I8>, dim3(grid), dim3(256), stream, tab, st, counters);
   return ls.e;

@@ -18,7 +18,7 @@ LIB_PATH = os.path.join(_HERE, "libdqt.so")
 DQT_OK, DQT_ERR_NULL, DQT_ERR_SHAPE, DQT_ERR_ALIGN, DQT_ERR_DTYPE = 0, 1, 2, 3, 4
 DQT_ERR_RANGE, DQT_ERR_WORKSPACE, DQT_ERR_UNSUPPORTED, DQT_ERR_HIP = 5, 6, 7, 8
 # dqt_dtype
-DQT_F32, DQT_BF16, DQT_I8, DQT_FP8E4M3, DQT_TERNARY2, DQT_INT4 = 0, 1, 2, 3, 4, 5
+DQT_F32, DQT_BF16, DQT_I8, DQT_FP8E4M3, DQT_TERNARY2, DQT_INT4, DQT_INT3 = 0, 1, 2, 3, 4, 5, 6
 
 EXPORTS = (
     "dqt_act_quant", "dqt_act_quant_batch", "dqt_linear_fwd_workspace", "dqt_linear_fwd", "dqt_linear_bwd_workspace",
@@ -29,7 +29,7 @@ EXPORTS = (
     "dqt_sr_update_batch", "dqt_adamw_sr_update", "dqt_adamw_sr_update_batch",
     "dqt_update_variant_workspace", "dqt_update_variant_batch",
     "dqt_sr_update", "dqt_debug_rng", "dqt_absmean_init", "dqt_pack_ternary",
-    "dqt_unpack_ternary", "dqt_pack_int4", "dqt_unpack_int4", "dqt_status_string", "dqt_version",
+    "dqt_unpack_ternary", "dqt_pack_int4", "dqt_unpack_int4", "dqt_pack_int3", "dqt_unpack_int3", "dqt_status_string", "dqt_version",
 )
 
 
@@ -108,6 +108,8 @@ _SIGS = {
     "dqt_unpack_ternary": (_i32, [_vp, _i64, _i64, _vp]),
     "dqt_pack_int4": (_i32, [_vp, _i64, _i64, _vp]),
     "dqt_unpack_int4": (_i32, [_vp, _i64, _i64, _vp]),
+    "dqt_pack_int3": (_i32, [_vp, _i64, _i64, _vp]),
+    "dqt_unpack_int3": (_i32, [_vp, _i64, _i64, _vp]),
     "dqt_status_string": (ctypes.c_char_p, [_i32]),
     "dqt_version": (_i32, []),
 }
@@ -405,6 +407,22 @@ def dqt_unpack_int4(packed: np.ndarray, cols: int) -> np.ndarray:
     rows = packed.shape[0]
     q = np.empty((rows, cols), dtype=np.int8)
     _check("dqt_unpack_int4", load().dqt_unpack_int4(packed.ctypes.data, rows, cols, q.ctypes.data))
+    return q
+
+
+def dqt_pack_int3(q: np.ndarray) -> np.ndarray:
+    q = np.ascontiguousarray(q, dtype=np.int8)
+    rows, cols = q.shape
+    packed = np.empty((rows, 3 * cols // 8), dtype=np.uint8)
+    _check("dqt_pack_int3", load().dqt_pack_int3(q.ctypes.data, rows, cols, packed.ctypes.data))
+    return packed
+
+
+def dqt_unpack_int3(packed: np.ndarray, cols: int) -> np.ndarray:
+    packed = np.ascontiguousarray(packed, dtype=np.uint8)
+    rows = packed.shape[0]
+    q = np.empty((rows, cols), dtype=np.int8)
+    _check("dqt_unpack_int3", load().dqt_unpack_int3(packed.ctypes.data, rows, cols, q.ctypes.data))
     return q
 
 

@@ -37,7 +37,7 @@ class Workload:
     wid: int
     M: int                      # tokens
     linears: tuple
-    wfmt: str                   # "ternary" (2-bit packed), "i4" (4-bit packed) or "i8"
+    wfmt: str                   # "ternary" (2-bit), "i3" (3-bit), "i4" (4-bit) packed, or "i8"
     qmin: int
     qmax: int
     init: str                   # "uniform": q ~ U{-1,0,1}, scale from W0
@@ -124,6 +124,13 @@ WORKLOADS = {
     "llama_h2048_int4": Workload(
         name="llama_h2048_int4", wid=5, M=16384, linears=_llama_linears(2048, 5632),
         wfmt="i4", qmin=-8, qmax=7, init="absmean", act="i8",
+        x_dtype="bf16", dy_dtype="bf16", xt="bf16", y_out="bf16", dx_out="bf16",
+        lr=3e-4),
+    # The hidden-2048 block with 3-bit weights (the n = 3 grid of Eq. 3,
+    # -4..3, 8 weights in 3 bytes).
+    "llama_h2048_int3": Workload(
+        name="llama_h2048_int3", wid=6, M=16384, linears=_llama_linears(2048, 5632),
+        wfmt="i3", qmin=-4, qmax=3, init="absmean", act="i8",
         x_dtype="bf16", dy_dtype="bf16", xt="bf16", y_out="bf16", dx_out="bf16",
         lr=3e-4),
 }

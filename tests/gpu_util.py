@@ -48,6 +48,8 @@ def weight_codes_dev(q: np.ndarray, wfmt: str):
         return torch.from_numpy(packed).to(DEV)
     if wfmt == "i4":
         return torch.from_numpy(O.pack_int4(q)).to(DEV)
+    if wfmt == "i3":
+        return torch.from_numpy(O.pack_int3(q)).to(DEV)
     return torch.from_numpy(np.ascontiguousarray(q, dtype=np.int8)).to(DEV)
 
 
@@ -57,11 +59,13 @@ def weight_codes_host(buf, wfmt: str, d_in: int) -> np.ndarray:
         return O.unpack_ternary(a, d_in)
     if wfmt == "i4":
         return O.unpack_int4(a.reshape(-1, d_in // 2), d_in)
+    if wfmt == "i3":
+        return O.unpack_int3(a.reshape(-1, 3 * d_in // 8), d_in)
     return a.astype(np.int8)
 
 
 def make_weight(d_out, d_in, wfmt, qmin, qmax, alpha, tensor_id=0):
-    code = {"ternary": dqt.DQT_TERNARY2, "i4": dqt.DQT_INT4}.get(wfmt, dqt.DQT_I8)
+    code = {"ternary": dqt.DQT_TERNARY2, "i4": dqt.DQT_INT4, "i3": dqt.DQT_INT3}.get(wfmt, dqt.DQT_I8)
     return dqt.weight(d_out, d_in, code, qmin, qmax, float(alpha), tensor_id)
 
 

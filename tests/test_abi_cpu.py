@@ -334,3 +334,21 @@ def test_sr_table_build_layout_and_checks():
         dqt.DQT_ERR_ALIGN
     assert lib.dqt_sr_update_table(4, io, 0x200000, 1e-3, 0, 1, None, 0x300004, None) == \
         dqt.DQT_ERR_ALIGN
+
+
+def test_int3_pack_matches_oracle_and_checks():
+    rng = np.random.default_rng(5)
+    q = rng.integers(-4, 4, size=(7, 48)).astype(np.int8)
+    packed = dqt.dqt_pack_int3(q)
+    assert np.array_equal(packed, O.pack_int3(q))
+    assert np.array_equal(dqt.dqt_unpack_int3(packed, 48), q)
+    with pytest.raises(dqt.DqtError) as e:
+        dqt.dqt_pack_int3(np.array([[4] + [0] * 7], np.int8))
+    assert e.value.status == dqt.DQT_ERR_RANGE
+    lib = dqt.load()
+    ok = _w(wfmt=dqt.DQT_INT3, qmin=-4, qmax=3)
+    assert lib.dqt_sr_update(ctypes.byref(ok), FAKE, None, 1e-3, 0, 1, None, None) == dqt.DQT_ERR_NULL
+    for qmin, qmax in ((-5, 3), (-4, 4), (2, 1)):
+        bad = _w(wfmt=dqt.DQT_INT3, qmin=qmin, qmax=qmax)
+        assert lib.dqt_sr_update(ctypes.byref(bad), FAKE, FAKE, 1e-3, 0, 1, None, None) == \
+            dqt.DQT_ERR_RANGE

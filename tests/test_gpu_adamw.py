@@ -25,6 +25,8 @@ CASES = [
                                               weight_decay=0.01), 17),
     (192, 160, "i4", -8, 7, 0.01, dict(lr=1e-2, beta1=0.9, beta2=0.99, eps=1e-8,
                                         weight_decay=0.05), 4),
+    (160, 208, "i3", -4, 3, 0.01, dict(lr=1e-2, beta1=0.9, beta2=0.99, eps=1e-8,
+                                        weight_decay=0.05), 6),
 ]
 
 

@@ -28,6 +28,9 @@ BATCHES = [
     # 4-bit codes: forward, dX, dW and the SR update
     (600, [(256, 128, 0), (128, 256, 1), (256, 256, 0)], "i4", -8, 7, "i8", "bf16"),
     (300, [(64, 80, 0), (80, 64, 1)], "i4", -4, 3, "i8", "f32"),
+    # 3-bit codes (8 weights in 3 bytes)
+    (600, [(256, 128, 0), (128, 256, 1), (256, 256, 0)], "i3", -4, 3, "i8", "bf16"),
+    (300, [(64, 80, 0), (80, 64, 1)], "i3", -2, 1, "e4m3", "f32"),
 ]
 
 

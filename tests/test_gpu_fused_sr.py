@@ -45,6 +45,11 @@ CASES = [
     (4096, [(256, 256, 0, True)], "i4", -4, 3, "i8", 2e-2, (0, 9, 3)),
     # 4-bit codes with e4m3 activations
     (640, [(128, 256, 0, True), (256, 128, 1, True)], "i4", -8, 7, "e4m3", 2e-2, None),
+    # 3-bit codes: ragged batch; a batch-split dW with a non-finite gradient;
+    # e4m3 activations
+    (1000, [(256, 384, 0, True), (384, 128, 1, True)], "i3", -4, 3, "i8", 2e-2, None),
+    (4096, [(256, 256, 0, True)], "i3", -4, 3, "i8", 2e-2, (0, 9, 3)),
+    (640, [(128, 256, 0, True), (256, 128, 1, True)], "i3", -4, 3, "e4m3", 2e-2, None),
 ]
 
 

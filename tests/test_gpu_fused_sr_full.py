@@ -36,7 +36,8 @@ def _block(name, with_dx):
     wl = W.WORKLOADS[name]
     M = wl.M
     act = dqt.DQT_I8 if wl.act == "i8" else dqt.DQT_FP8E4M3
-    wfmt = {"ternary": dqt.DQT_TERNARY2, "i4": dqt.DQT_INT4}.get(wl.wfmt, dqt.DQT_I8)
+    wfmt = {"ternary": dqt.DQT_TERNARY2, "i4": dqt.DQT_INT4, "i3": dqt.DQT_INT3}.get(wl.wfmt,
+                                                                                   dqt.DQT_I8)
     Xq, xdq, Xd = {}, {}, {}
     for name_in in wl.inputs:
         X = torch.from_numpy(W.input_draw(wl, name_in)).to(torch.bfloat16).to(DEV)
@@ -57,6 +58,8 @@ def _block(name, with_dx):
             codes = O.pack_ternary(q)
         elif wl.wfmt == "i4":
             codes = O.pack_int4(q)
+        elif wl.wfmt == "i3":
+            codes = O.pack_int3(q)
         else:
             codes = q
         c1 = torch.from_numpy(np.ascontiguousarray(codes)).to(DEV)
@@ -180,3 +183,8 @@ def test_fused_sr_full_llama_h4096(lib):
 def test_fused_sr_full_llama_h2048_int4(lib):
     """Hidden 2048 block with 4-bit codes -8..7."""
     _run_case("llama_h2048_int4", True, False)
+
+
+def test_fused_sr_full_llama_h2048_int3(lib):
+    """Hidden 2048 block with 3-bit codes -4..3 (8 weights in 3 bytes)."""
+    _run_case("llama_h2048_int3", True, False)

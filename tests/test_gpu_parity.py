@@ -94,6 +94,8 @@ FWD_KINDS = [  # act, wfmt, qmin, qmax, x_t, y_out
     ("i8", "i4", -8, 7, "bf16", "bf16"),
     ("i8", "i4", -4, 3, "f32", "f32"),
     ("e4m3", "i4", -8, 7, "bf16", "f32"),
+    ("i8", "i3", -4, 3, "bf16", "bf16"),
+    ("e4m3", "i3", -4, 3, "f32", "f32"),
 ]
 
 
@@ -141,6 +143,8 @@ BWD_KINDS = [  # act, wfmt, qmin, qmax, xt (= dY dtype), dx_out
     ("i8", "i4", -8, 7, "bf16", "bf16"),
     ("i8", "i4", -2, 1, "f32", "f32"),
     ("e4m3", "i4", -4, 3, "bf16", "bf16"),
+    ("i8", "i3", -4, 3, "bf16", "bf16"),
+    ("i8", "i3", -2, 1, "f32", "f32"),
 ]
 
 
@@ -209,6 +213,8 @@ SR_CASES = [  # d_out, d_in, wfmt, qmin, qmax, lr, alpha, gscale
     (1024, 1024, "ternary", -1, 1, 3e-4, 0.0159, 0.01),
     (256, 384, "i4", -8, 7, 1e-2, 2e-3, 1.0),
     (144, 48, "i4", -4, 3, 0.3, 0.02, 1.0),
+    (256, 384, "i3", -4, 3, 1e-2, 2e-3, 1.0),
+    (144, 48, "i3", -4, 3, 0.3, 0.02, 1.0),
 ]
 
 

@@ -70,7 +70,7 @@ def test_sr_table_168_tensors_of_a_24_layer_model(lib):
     assert counters[0].item() > 0
 
 
-@pytest.mark.parametrize("wfmt,qmin,qmax", [("i8", -127, 127), ("i4", -8, 7)])
+@pytest.mark.parametrize("wfmt,qmin,qmax", [("i8", -127, 127), ("i4", -8, 7), ("i3", -4, 3)])
 def test_sr_table_ragged_tiny_and_nonfinite(lib, wfmt, qmin, qmax):
     """Tensors smaller than one tile, tensors ending mid-tile, and non-finite
     gradients counted per tensor."""
@@ -78,7 +78,8 @@ def test_sr_table_ragged_tiny_and_nonfinite(lib, wfmt, qmin, qmax):
               (16, 16)] * 3 + [(1024, 1024)]
     nonfinite = [(1, 5, np.inf), (4, 777, np.nan), (4, 778, -np.inf), (24, 100000, np.nan)]
     lr = 5e-2
-    ents, host = _tensors(shapes, wfmt, qmin, qmax, 0.3, 62 if wfmt == "i8" else 63, nonfinite)
+    ents, host = _tensors(shapes, wfmt, qmin, qmax, 0.3, {"i8": 62, "i4": 63}.get(wfmt, 65),
+                          nonfinite)
     io = dqt.linear_io(ents)
     table = torch.from_numpy(dqt.dqt_sr_table_build(io)).to(DEV)
     counters = torch.zeros((2,), dtype=torch.int64, device=DEV)

@@ -21,6 +21,7 @@ SHAPES = [
     (64, 48, "i8", -8, 7, 0.05, 0.5, "ties"),          # few distinct |delta|: ties at tau
     (2048, 1024, "ternary", -1, 1, 0.01, 1e-2, "normal"),
     (96, 256, "i4", -8, 7, 0.02, 0.1, "normal"),
+    (112, 208, "i3", -4, 3, 0.02, 0.1, "normal"),
 ]
 MODES = [(dqt.DQT_UPD_SR, 0.2), (dqt.DQT_UPD_NEAREST, 0.2), (dqt.DQT_UPD_FORCE_REMAIN, 0.2),
          (dqt.DQT_UPD_FORCE_CHANGE, 0.2), (dqt.DQT_UPD_FORCE_CHANGE, 1.0),

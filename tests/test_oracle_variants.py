@@ -114,3 +114,16 @@ def test_int4_packing_layout():
     assert p.tolist() == [[0x78, 0xF1, 0xE0]]
     allv = np.arange(-8, 8).reshape(1, 16)
     assert np.array_equal(O.unpack_int4(O.pack_int4(allv), 16), allv)
+
+
+def test_int3_packing_layout():
+    """3-bit codes (the n = 3 grid of Eq. 3, -4..3): a group of 8 weights is
+    the 24-bit number sum_j (q_j mod 8) 2^(3j), little-endian.  For q = 0, 1,
+    2, 3, -4, -3, -2, -1 the fields are 0..7, so the number is 0xFAC688:
+    bytes 0x88, 0xC6, 0xFA.  Every value round-trips."""
+    q = np.array([[0, 1, 2, 3, -4, -3, -2, -1, 3, 3, 3, 3, 3, 3, 3, 3]], np.int64)
+    p = O.pack_int3(q)
+    assert p.tolist() == [[0x88, 0xC6, 0xFA, 0xDB, 0xB6, 0x6D]]   # 3 x (011 repeated) = 0x6DB6DB
+    rng = np.random.default_rng(9)
+    allv = rng.integers(-4, 4, size=(5, 64))
+    assert np.array_equal(O.unpack_int3(O.pack_int3(allv), 64), allv)
