@@ -71,6 +71,10 @@ Readings of points the paper leaves open (each is listed in the design doc):
       (64 lane sums over chunks of 8 elements, then a butterfly), each
       operation one correctly rounded fp32 operation; y then goes through
       ``act_quant``.
+  R14 The deterministic control of Sec. 5.1 read literally: absmax
+      quantisation of the updated real-valued matrix W' = W~ - lr g with a
+      new per-tensor scale alpha' = max|W'| / qmax each step (see
+      ``absmax_requant``); a non-finite g counts as 0 and is counted.
 """
 
 from __future__ import annotations
@@ -742,6 +746,35 @@ def bottom_threshold(keys, frac):
     if k <= 0:
         return None
     return np.uint32(np.sort(keys)[k - 1])
+
+
+def absmax_requant(q, g, lr, alpha, qmin: int, qmax: int):
+    """The deterministic control of Sec. 5.1 read literally (R14): the
+    updated matrix W' = W~ - lr g (W~ = q alpha) is quantised afresh with
+    Eq. 3-4's form and the maximum in place of the mean,
+      W'_i    = fl(fl(q_i alpha) - fl(lr g_i))       (g_i non-finite: g_i = 0)
+      m       = max_i |W'_i|
+      s'      = fl(qmax / m),  alpha' = fl(m / qmax)
+      q'_i    = Clip(Round(fl(W'_i s')), qmin, qmax)  (Round: ties to even)
+    with m = 0 giving s' = 0 and alpha' = alpha.  No stochastic rounding.
+    Returns (q' int64, alpha' fp32, n_changed, n_nonfinite)."""
+    q = np.asarray(q).astype(np.int64).ravel()
+    g = np.asarray(g, dtype=np.float32).ravel()
+    finite = np.isfinite(g)
+    a = np.float32(alpha)
+    w = (q.astype(np.float32) * a).astype(np.float32)
+    with np.errstate(over="ignore", invalid="ignore"):
+        u = (np.float32(lr) * np.where(finite, g, np.float32(0))).astype(np.float32)
+    wp = (w - u).astype(np.float32)
+    m = np.float32(np.max(np.abs(wp))) if wp.size else np.float32(0)
+    if m == 0:
+        s_new, alpha_new = np.float32(0), a
+    else:
+        s_new = np.float32(np.float32(qmax) / m)
+        alpha_new = np.float32(m / np.float32(qmax))
+    scaled = (wp * s_new).astype(np.float32)
+    new = np.clip(np.rint(scaled), qmin, qmax).astype(np.int64)
+    return new, alpha_new, int(np.count_nonzero(new != q)), int(np.count_nonzero(~finite))
 
 
 def update_variant(q, g, lr, alpha, qmin: int, qmax: int, seed: int, step: int, tensor_id: int,

@@ -127,3 +127,56 @@ def test_int3_packing_layout():
     rng = np.random.default_rng(9)
     allv = rng.integers(-4, 4, size=(5, 64))
     assert np.array_equal(O.unpack_int3(O.pack_int3(allv), 64), allv)
+
+
+def test_absmax_requant_hand_example():
+    """Sec. 5.1's control read literally, on a hand-computed case: alpha =
+    0.5, lr = 0.25, ternary.  W~ = q alpha = [0.5, 0, -0.5, 0.5]; lr g = [0,
+    0.25, -0.75, 1.0] (g = [0, 1, -3, 4]), so W' = [0.5, -0.25, 0.25, -0.5];
+    m = 0.5, s' = 2, alpha' = 0.5; W' s' = [1, -0.5, 0.5, -1] rounds (ties to
+    even) to [1, -0, 0, -1]."""
+    q = np.array([1, 0, -1, 1])
+    g = np.array([0.0, 1.0, -3.0, 4.0], np.float32)
+    new, alpha_new, nch, nnf = O.absmax_requant(q, g, 0.25, 0.5, -1, 1)
+    assert new.tolist() == [1, 0, 0, -1]
+    assert alpha_new == np.float32(0.5) and (nch, nnf) == (2, 0)
+
+
+def test_absmax_requant_drops_small_updates_and_rescales():
+    """The property the paper measures: an update far below the grid step
+    changes no code (SR would move a fraction of them), while one large entry
+    rescales the whole tensor and sends the rest to zero."""
+    rng = np.random.default_rng(21)
+    q = rng.integers(-1, 2, size=4096)
+    q[0] = 1                                        # max |W~| = alpha
+    alpha = np.float32(0.02)
+    g = (rng.standard_normal(4096) * 1e-3).astype(np.float32)
+    g[0] = 0.0
+    new, a2, nch, _ = O.absmax_requant(q, g, 1e-2, alpha, -1, 1)
+    assert nch == 0 and np.array_equal(new, q)      # |lr g| <= 1e-4 << alpha / 2
+    assert abs(float(a2) - float(alpha)) <= 1e-4
+    sr_new, sr_changed, _ = O.sr_update(q, g * np.float32(100.0), 1e-2, alpha, -1, 1, 0, 1, 0)
+    assert sr_changed > 0                           # SR moves some codes at a larger step
+    g2 = np.zeros(4096, np.float32)
+    g2[1] = -100.0                                  # W'_1 = q_1 alpha + 1
+    new2, a3, _, _ = O.absmax_requant(q, g2, 1e-2, alpha, -1, 1)
+    assert a3 == np.float32(np.float32(q[1] * alpha) + np.float32(1.0))
+    assert new2[1] == 1 and np.count_nonzero(new2) == 1
+
+
+def test_absmax_requant_int8_grid_matches_eq4_form():
+    """On the 8-bit grid the new codes are Eq. 4 with s' = 127 / max|W'|:
+    the entry holding the maximum maps to +-127 exactly; a non-finite
+    gradient counts as zero and is counted; an all-zero W' keeps alpha."""
+    rng = np.random.default_rng(22)
+    q = rng.integers(-127, 128, size=1000)
+    g = rng.standard_normal(1000).astype(np.float32)
+    g[5] = np.nan
+    new, a2, _, nnf = O.absmax_requant(q, g, 1e-3, 0.01, -127, 127)
+    wp = (q.astype(np.float32) * np.float32(0.01)).astype(np.float32) - \
+        (np.float32(1e-3) * np.where(np.isfinite(g), g, 0)).astype(np.float32)
+    k = int(np.argmax(np.abs(wp)))
+    assert abs(int(new[k])) == 127 and nnf == 1
+    z, az, nz, _ = O.absmax_requant(np.zeros(16, np.int64), np.zeros(16, np.float32), 1e-3,
+                                    0.25, -127, 127)
+    assert not z.any() and az == np.float32(0.25) and nz == 0
