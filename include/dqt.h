@@ -393,6 +393,29 @@ dqt_status dqt_update_variant_batch(int32_t n, const dqt_linear_io* io, float lr
                                     void* ws, size_t ws_bytes, void* stream);
 
 /*
+ * The deterministic control of Sec. 5.1 read literally: instead of the
+ * stochastic rounding of Eq. 5, the updated real-valued matrix W' = W~ -
+ * lr dW (W~ = q alpha) is absmax-quantised afresh, i.e. Eq. 3-4 with the
+ * maximum of |W'| in place of the mean, which gives the tensor a new scale
+ * every step.  Per tensor, every operation one correctly rounded fp32
+ * operation:
+ *   W'_i   = q_i alpha - lr dW_i        (a non-finite dW_i is read as 0 and
+ *                                        counted in counters[1])
+ *   m      = max_i |W'_i|;  s' = qmax / m;  alpha' = m / qmax
+ *   q'_i   = Clip(rint(W'_i s'), qmin, qmax)     (rint: ties to even)
+ * with m = 0 giving q' = 0 and alpha' = alpha.  The codes are updated in
+ * place and alpha' of tensor l is written to alpha_out[l] (device fp32 [n]);
+ * the caller adopts it (the descriptor's alpha) for the next step.
+ *   counters: NULL, or device uint64[2] (changed, non-finite; ADDED).
+ *   ws, ws_bytes: dqt_absmax_requant_workspace(n) bytes of device memory.
+ * Uses w, Wq, dW of each of the n (1..DQT_MAX_BATCH) entries of io.
+ */
+size_t dqt_absmax_requant_workspace(int32_t n);
+dqt_status dqt_absmax_requant_batch(int32_t n, const dqt_linear_io* io, float lr,
+                                    float* alpha_out, unsigned long long* counters,
+                                    void* ws, size_t ws_bytes, void* stream);
+
+/*
  * AdamW with direct stochastic rounding.  The paper trains DQT with AdamW
  * modified to round stochastically (Sec. 4.1): the optimiser's target W'
  * (Sec. 3.2) is the AdamW step with decoupled weight decay and bias

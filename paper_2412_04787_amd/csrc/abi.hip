@@ -414,6 +414,41 @@ dqt_status dqt_update_variant_batch(int32_t n, const dqt_linear_io* io, float lr
                                              counters, ws, static_cast<hipStream_t>(stream)));
 }
 
+size_t dqt_absmax_requant_workspace(int32_t n) {
+  if (n < 1 || n > DQT_MAX_BATCH) return 0;
+  return dqt::absmax_requant_workspace(n);
+}
+
+dqt_status dqt_absmax_requant_batch(int32_t n, const dqt_linear_io* io, float lr, float* alpha_out,
+                                    unsigned long long* counters, void* ws, size_t ws_bytes,
+                                    void* stream) {
+  dqt::LinearIO L[DQT_MAX_BATCH];
+  int32_t wfmt;
+  dqt_status st = check_batch(n, io, L, &wfmt);
+  if (st != DQT_OK) return st;
+  if (alpha_out == nullptr) return DQT_ERR_NULL;
+  if ((reinterpret_cast<uintptr_t>(alpha_out) & 3u) != 0) return DQT_ERR_ALIGN;
+  if (counters != nullptr && (reinterpret_cast<uintptr_t>(counters) & 7u) != 0) return DQT_ERR_ALIGN;
+  if (!(isfinite(lr) && lr >= 0.0f)) return DQT_ERR_RANGE;
+  if (ws == nullptr || ws_bytes < dqt::absmax_requant_workspace(n)) return DQT_ERR_WORKSPACE;
+  if ((reinterpret_cast<uintptr_t>(ws) & 3u) != 0) return DQT_ERR_ALIGN;
+  dqt::SRTensor t[DQT_MAX_BATCH];
+  for (int l = 0; l < n; ++l) {
+    if (io[l].Wq == nullptr || io[l].dW == nullptr) return DQT_ERR_NULL;
+    if (!aligned16(io[l].Wq) || !aligned16(io[l].dW)) return DQT_ERR_ALIGN;
+    t[l].wq = static_cast<uint8_t*>(io[l].Wq);
+    t[l].grad = io[l].dW;
+    t[l].nweights = (int64_t)io[l].w->d_out * (int64_t)io[l].w->d_in;
+    t[l].c = 0.0f;
+    t[l].qmin = io[l].w->qmin;
+    t[l].qmax = io[l].w->qmax;
+    t[l].tensor_id = io[l].w->tensor_id;
+    t[l].alpha = io[l].w->alpha;
+  }
+  return from_hip(dqt::launch_absmax_requant(code_format(wfmt), n, t, lr, alpha_out, counters, ws,
+                                             static_cast<hipStream_t>(stream)));
+}
+
 dqt_status dqt_adamw_sr_update_batch(int32_t n, const dqt_linear_io* io, float* const* m,
                                      float* const* v, const dqt_adamw* hp, uint64_t seed,
                                      uint32_t step, unsigned long long* counters, void* stream) {

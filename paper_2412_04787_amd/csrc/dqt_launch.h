@@ -179,6 +179,10 @@ size_t update_variant_workspace(int n);
 hipError_t launch_update_variant(int cf, int n, const SRTensor* t, int mode, float frac,
                                  uint64_t seed, uint32_t step, unsigned long long* counters,
                                  void* ws, hipStream_t stream);
+// The literal absmax re-quantisation control (Sec. 5.1); ws: n uint32.
+size_t absmax_requant_workspace(int n);
+hipError_t launch_absmax_requant(int cf, int n, const SRTensor* t, float lr, float* alpha_out,
+                                 unsigned long long* counters, void* ws, hipStream_t stream);
 // AdamW with SR (up to kMaxBatch tensors of one code format per launch).
 struct AdamTensor {
   uint8_t* wq;          // codes, updated in place

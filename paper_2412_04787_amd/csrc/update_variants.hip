@@ -236,6 +236,158 @@ __global__ __launch_bounds__(256) void variant_update_kernel(const VarTab tab, c
 
 }  // namespace
 
+// ------------------------------------------------------------------------
+// The deterministic control of Sec. 5.1 read literally: the updated matrix
+// W' = W~ - lr dW is absmax-quantised afresh, with a new per-tensor scale
+// alpha' = max|W'| / qmax (Eq. 3-4 with the maximum in place of the mean).
+// Two passes over each tensor: the maximum of |W'| (per block, then one
+// atomic max on its bit pattern, which orders as the value for |W'| >= 0),
+// then the new codes.
+namespace {
+
+struct AbsTab {
+  uint8_t* wq[kMaxV];
+  const float* grad[kMaxV];
+  int64_t nweights[kMaxV];
+  int64_t t0[kMaxV + 1];         // tiles of 256 chunks
+  float alpha[kMaxV], lr;
+  int qmin[kMaxV], qmax[kMaxV];
+  float* alpha_out;              // [n] device
+  uint32_t* wmax;                // [n] device, the max |W'| bits
+  int32_t n;
+};
+
+// W'_j of a chunk: fl(fl(q alpha) - fl(lr g)), a non-finite g read as 0
+template <int CF>
+__device__ __forceinline__ void wprime8(const uint32_t (&win)[4], const f32x4 (&gv)[2], float alpha,
+                                        float lr, float (&w)[8], uint32_t& nonfin) {
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const float g = gv[j >> 2][j & 3];
+    const bool fin = __builtin_isfinite(g);
+    nonfin += fin ? 0u : 1u;
+    w[j] = (float)CodeFmt<CF>::q_of(win, j) * alpha - lr * (fin ? g : 0.0f);
+  }
+}
+
+__global__ __launch_bounds__(64) void absmax_init_kernel(uint32_t* wmax, int n) {
+  for (int i = threadIdx.x; i < n; i += 64) wmax[i] = 0u;
+}
+
+template <int CF>
+__global__ __launch_bounds__(256) void absmax_max_kernel(const AbsTab tab) {
+  __shared__ uint32_t red[256 / kWave];
+  const int64_t tile = blockIdx.x;
+  const int s = seg_of(tab.t0, tab.n, tile);
+  const int64_t t = (tile - tab.t0[s]) * 256 + threadIdx.x;
+  float m = 0.0f;
+  if (t < tab.nweights[s] / 8) {
+    const f32x4* gp = reinterpret_cast<const f32x4*>(tab.grad[s]) + 2 * t;
+    const f32x4 gv[2] = {gp[0], gp[1]};
+    uint32_t win[4] = {0u, 0u, 0u, 0u}, nf = 0;
+    ChunkIO<CF>::load(tab.wq[s], t, win);
+    float w[8];
+    wprime8<CF>(win, gv, tab.alpha[s], tab.lr, w, nf);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) m = fmaxf(m, fabsf(w[j]));
+  }
+  m = wave_max(m);
+  if ((threadIdx.x & (kWave - 1)) == 0) red[threadIdx.x / kWave] = __float_as_uint(m);
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint32_t b = 0;
+#pragma unroll
+    for (int i = 0; i < 256 / kWave; ++i) b = max(b, red[i]);
+    if (b) atomicMax(tab.wmax + s, b);
+  }
+}
+
+template <int CF>
+__global__ __launch_bounds__(256) void absmax_quant_kernel(const AbsTab tab, unsigned long long* counters) {
+  __shared__ uint32_t red[2][256 / kWave];
+  const int64_t tile = blockIdx.x;
+  const int s = seg_of(tab.t0, tab.n, tile);
+  const int64_t t = (tile - tab.t0[s]) * 256 + threadIdx.x;
+  const float m = __uint_as_float(tab.wmax[s]);
+  const float qp = (float)tab.qmax[s];
+  const float sn = m > 0.0f ? __fdiv_rn(qp, m) : 0.0f;
+  if (tile == tab.t0[s] && threadIdx.x == 0) tab.alpha_out[s] = m > 0.0f ? __fdiv_rn(m, qp) : tab.alpha[s];
+  uint32_t ch = 0, nf = 0;
+  if (t < tab.nweights[s] / 8) {
+    const f32x4* gp = reinterpret_cast<const f32x4*>(tab.grad[s]) + 2 * t;
+    const f32x4 gv[2] = {gp[0], gp[1]};
+    uint32_t win[4] = {0u, 0u, 0u, 0u}, wout[4] = {0u, 0u, 0u, 0u};
+    ChunkIO<CF>::load(tab.wq[s], t, win);
+    float w[8];
+    wprime8<CF>(win, gv, tab.alpha[s], tab.lr, w, nf);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int v = (int)fminf(fmaxf(rintf(w[j] * sn), (float)tab.qmin[s]), qp);
+      CodeFmt<CF>::put(wout, j, v + CodeFmt<CF>::off);
+    }
+    ch = CodeFmt<CF>::template changed<8>(wout, win);
+    ChunkIO<CF>::store(tab.wq[s], t, wout);
+  }
+  if (counters != nullptr) {
+    const uint32_t c = wave_sum_u32(ch), f = wave_sum_u32(nf);
+    if ((threadIdx.x & (kWave - 1)) == 0) {
+      red[0][threadIdx.x / kWave] = c;
+      red[1][threadIdx.x / kWave] = f;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      unsigned long long ct = 0, ft = 0;
+#pragma unroll
+      for (int i = 0; i < 256 / kWave; ++i) {
+        ct += red[0][i];
+        ft += red[1][i];
+      }
+      if (ct) atomicAdd(counters, ct);
+      if (ft) atomicAdd(counters + 1, ft);
+    }
+  }
+}
+
+template <int CF>
+hipError_t launch_absmax_cf(const AbsTab& tab, int64_t tiles, unsigned long long* counters,
+                            hipStream_t stream) {
+  LaunchStatus ls;
+  ls << launch_kernel(absmax_init_kernel, dim3(1), dim3(64), stream, tab.wmax, (int)tab.n);
+  ls << launch_kernel(absmax_max_kernel<CF>, dim3((unsigned)tiles), dim3(256), stream, tab);
+  ls << launch_kernel(absmax_quant_kernel<CF>, dim3((unsigned)tiles), dim3(256), stream, tab, counters);
+  return ls.e;
+}
+
+}  // namespace
+
+size_t absmax_requant_workspace(int n) { return (size_t)(n > 0 ? n : 0) * 4; }
+
+hipError_t launch_absmax_requant(int cf, int n, const SRTensor* t, float lr, float* alpha_out,
+                                 unsigned long long* counters, void* ws, hipStream_t stream) {
+  AbsTab tab{};
+  tab.n = n;
+  tab.lr = lr;
+  tab.alpha_out = alpha_out;
+  tab.wmax = static_cast<uint32_t*>(ws);
+  int64_t tiles = 0;
+  for (int s = 0; s < n; ++s) {
+    tab.wq[s] = t[s].wq;
+    tab.grad[s] = t[s].grad;
+    tab.nweights[s] = t[s].nweights;
+    tab.alpha[s] = t[s].alpha;
+    tab.qmin[s] = t[s].qmin;
+    tab.qmax[s] = t[s].qmax;
+    tab.t0[s] = tiles;
+    tiles += (t[s].nweights / 8 + 255) / 256;
+  }
+  tab.t0[n] = tiles;
+  if (tiles == 0) return hipSuccess;
+  if (cf == CF_T2) return launch_absmax_cf<CF_T2>(tab, tiles, counters, stream);
+  if (cf == CF_I4) return launch_absmax_cf<CF_I4>(tab, tiles, counters, stream);
+  if (cf == CF_I3) return launch_absmax_cf<CF_I3>(tab, tiles, counters, stream);
+  return launch_absmax_cf<CF_I8>(tab, tiles, counters, stream);
+}
+
 size_t update_variant_workspace(int n) { return (size_t)n * sizeof(SelState); }
 
 hipError_t launch_update_variant(int cf, int n, const SRTensor* t, int mode, float frac,

@@ -25,7 +25,8 @@ EXPORTS = (
     "dqt_linear_bwd", "dqt_linear_fwd_batch_workspace", "dqt_linear_fwd_batch",
     "dqt_linear_bwd_batch_workspace", "dqt_linear_bwd_batch", "dqt_linear_bwd_sr_batch",
     "dqt_linear_fwd_batch_noalloc", "dqt_sr_table_bytes", "dqt_sr_table_build",
-    "dqt_sr_update_table", "dqt_rmsnorm_act_quant",
+    "dqt_sr_update_table", "dqt_rmsnorm_act_quant", "dqt_absmax_requant_workspace",
+    "dqt_absmax_requant_batch",
     "dqt_sr_update_batch", "dqt_adamw_sr_update", "dqt_adamw_sr_update_batch",
     "dqt_update_variant_workspace", "dqt_update_variant_batch",
     "dqt_sr_update", "dqt_debug_rng", "dqt_absmean_init", "dqt_pack_ternary",
@@ -98,6 +99,8 @@ _SIGS = {
     "dqt_sr_table_build": (_i32, [_i32, _vp, _vp, ctypes.c_size_t]),
     "dqt_sr_update_table": (_i32, [_i32, _vp, _vp, _f32, _u64, _u32, _vp, _vp, _vp]),
     "dqt_update_variant_workspace": (ctypes.c_size_t, [_i32]),
+    "dqt_absmax_requant_workspace": (ctypes.c_size_t, [_i32]),
+    "dqt_absmax_requant_batch": (_i32, [_i32, _vp, _f32, _vp, _vp, _vp, ctypes.c_size_t, _vp]),
     "dqt_update_variant_batch": (_i32, [_i32, _vp, _f32, _u64, _u32, _i32, _f32, _vp, _vp,
                                         ctypes.c_size_t, _vp]),
     "dqt_adamw_sr_update": (_i32, [_wp, _vp, _vp, _vp, _vp, _vp, _u64, _u32, _vp, _vp]),
@@ -325,6 +328,16 @@ def dqt_update_variant_batch(io, lr: float, seed: int, step: int, mode: int, fra
     ws_bytes = 0 if ws is None else ws.numel() * ws.element_size()
     _check("dqt_update_variant_batch",
            load().dqt_update_variant_batch(len(io), io, lr, seed, step, mode, frac, _ptr(counters),
+                                           _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def dqt_absmax_requant_batch(io, lr: float, alpha_out, counters=None, ws=None, stream=None):
+    """alpha_out: device fp32 [len(io)], receives each tensor's new scale."""
+    if ws is None:
+        ws = workspace(int(load().dqt_absmax_requant_workspace(len(io))))
+    ws_bytes = 0 if ws is None else ws.numel() * ws.element_size()
+    _check("dqt_absmax_requant_batch",
+           load().dqt_absmax_requant_batch(len(io), io, lr, _ptr(alpha_out), _ptr(counters),
                                            _ptr(ws), ws_bytes, _stream(stream)))
 
 
