@@ -461,11 +461,13 @@ dqt_status dqt_adamw_sr_update_batch(int32_t n, const dqt_linear_io* io,
 
 /*
  * Backward and direct SR update of n linears in one call (Sec. 3.2: the
- * update of Eq. 5 consumes dW of the backward), with dW never written to
- * memory: the dW product's epilogue updates the 8 codes of each group of 8
- * consecutive weights of a row as it forms their gradients (or, when the
- * dW reduction over tokens is split, the kernel that sums the partials
- * does).  The codes and counters equal those of dqt_linear_bwd_batch
+ * update of Eq. 5 consumes dW of the backward), with dW never written to the
+ * caller's memory: the dW product's epilogue updates the 8 codes of each
+ * group of 8 consecutive weights of a row as it forms their gradients; when
+ * the dW reduction over tokens is split, the kernel that sums the partials
+ * does.  With the environment variable DQT_SR_EPILOGUE=staged, dW is
+ * instead staged in the workspace and a streaming pass updates the codes
+ * (same dW bits, same codes); the workspace query reads it too.  The codes and counters equal those of dqt_linear_bwd_batch
  * writing dW followed by dqt_sr_update_batch on that dW, bit for bit; dX is
  * formed from the codes as they were before the update.
  *   io: uses w, Wq (updated in place), Xq, xdq, dY, dX of each entry; dX may

@@ -108,6 +108,8 @@ struct BatchCfg {
 struct BwdPlan {
   int64_t splits;        // dW batch splits when dW runs in a launch of its own
   int64_t splits_dual;   // ... and when it shares one launch with dX
+  bool sr_fused;         // unsplit dW: the SR update in its epilogue (else a pass over
+  bool sr_fused_dual;    //   dW staged in the workspace); alone / with dX
   int wi, wj;       // dW block tile (64 wi) x (64 wj)
   size_t q_off[kMaxBatch], xt_off[kMaxBatch], part_off[kMaxBatch];
   size_t total;

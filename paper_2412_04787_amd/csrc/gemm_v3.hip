@@ -36,6 +36,8 @@
 // Each DMA wave instruction fills 1 KB of consecutive LDS positions, so each
 // lane loads the global chunk that belongs at its position.
 #include <algorithm>
+#include <cstdlib>
+#include <cstring>
 #include <type_traits>
 
 #include "gemm_common.h"
@@ -1523,6 +1525,18 @@ BwdPlan plan_bwd_batch(int n, const LinearIO* io, int64_t M) {
                           part_bytes / 4.0e6;
     if (t_dual < best_dual * 0.999) { best_dual = t_dual; P.splits_dual = s; }
   }
+  // The SR update in the dW epilogue saves dW's store and a streaming pass
+  // over it, at the price of ~173 vector instructions per 8 weights in the
+  // dW tiles.  Measured per call it is the faster form on every LLaMA block
+  // (hidden 768, where those tiles are the launch's critical path: 288 us
+  // against 300 us staged), so it is the default; DQT_SR_EPILOGUE=staged in
+  // the environment stages dW in the workspace and updates it in a pass of
+  // its own (same dW bits, same codes), e.g. to test both forms.
+  bool fuse = true;
+  if (const char* f = getenv("DQT_SR_EPILOGUE")) fuse = strcmp(f, "staged") != 0;
+  P.sr_fused = P.splits == 1 && fuse;
+  P.sr_fused_dual = P.splits_dual == 1 && fuse;
+  const bool stage_dw = (P.splits == 1 && !P.sr_fused) || (P.splits_dual == 1 && !P.sr_fused_dual);
   size_t off = kSchedBytes;
   for (int l = 0; l < n; ++l) {
     const size_t wn = (size_t)(io[l].d_out * io[l].d_in);
@@ -1533,7 +1547,7 @@ BwdPlan plan_bwd_batch(int n, const LinearIO* io, int64_t M) {
     P.xt_off[l] = off;
     off += align256((size_t)xt_stride(M) * (size_t)io[l].d_in * 2);
     P.part_off[l] = off;
-    off += sp > 1 ? align256((size_t)sp * wn * 4) : 0;
+    off += sp > 1 ? align256((size_t)sp * wn * 4) : stage_dw ? align256(wn * 4) : 0;
   }
   P.total = off;
   return P;
@@ -1811,12 +1825,13 @@ hipError_t launch_bwd_sr_batch(const BatchCfg& c, const LinearIO* io, const SRTe
   }
   BwdPlan Q = P;
   Q.splits = with_dx ? P.splits_dual : P.splits;
+  const bool fused = with_dx ? P.sr_fused_dual : P.sr_fused;
   Group<EpiScale> gx{};
   LaunchStatus st;
   if (with_dx) prep_dx(c, io, ws, Q, stream, gx, st);
   int first[kMaxBatch];
   prep_xt(c, io, ws, Q, stream, first, st);
-  if (Q.splits == 1) {
+  if (Q.splits == 1 && fused) {
     Group<EpiScale>* const pgx = with_dx ? &gx : nullptr;
     if (c.w_ternary) st << launch_dw_sr_group<CF_T2>(c, io, t, seed, step, counters, ws, Q, first, pgx, stream);
     else if (c.w_int4) st << launch_dw_sr_group<CF_I4>(c, io, t, seed, step, counters, ws, Q, first, pgx, stream);

@@ -1,4 +1,6 @@
-"""Backward with the SR update fused into the dW product (dW never stored):
+"""Backward with the SR update fused into the backward call (dW never
+reaches the caller's memory: updated in the dW product's epilogue, or staged
+in the workspace for a streaming pass):
 the codes, the counters and dX equal those of the backward call that writes
 dW followed by the SR update call on that dW, bit for bit, and the codes
 equal the oracle's SR update (Sec. 3.2 Eq. 5) of that dW."""
@@ -53,10 +55,14 @@ CASES = [
 ]
 
 
+@pytest.mark.parametrize("mode", ["fused", "staged"])
 @pytest.mark.parametrize("ci", range(len(CASES)))
-def test_fused_sr_matches_two_calls_and_oracle(lib, ci):
+def test_fused_sr_matches_two_calls_and_oracle(lib, ci, mode, monkeypatch):
+    """mode: the update in the dW epilogue, or on dW staged in the workspace
+    (DQT_SR_EPILOGUE); a batch-split dW always updates in the reduction."""
+    monkeypatch.setenv("DQT_SR_EPILOGUE", mode)
     M, lins, wfmt, qmin, qmax, act, lr, inf_at = CASES[ci]
-    log(f"fused SR case {ci}: M={M} {lins} {wfmt} {act} lr={lr} inf_at={inf_at}")
+    log(f"fused SR case {ci} ({mode}): M={M} {lins} {wfmt} {act} lr={lr} inf_at={inf_at}")
     a_code = dqt.DQT_I8 if act == "i8" else dqt.DQT_FP8E4M3
     bf = dqt.DQT_BF16
     n_in = max(l[2] for l in lins) + 1

@@ -188,3 +188,10 @@ def test_fused_sr_full_llama_h2048_int4(lib):
 def test_fused_sr_full_llama_h2048_int3(lib):
     """Hidden 2048 block with 3-bit codes -4..3 (8 weights in 3 bytes)."""
     _run_case("llama_h2048_int3", True, False)
+
+
+def test_fused_sr_full_llama_h768_staged(lib, monkeypatch):
+    """The h768 block with dW staged in the workspace and the update run as
+    a streaming pass (DQT_SR_EPILOGUE=staged) instead of in the epilogue."""
+    monkeypatch.setenv("DQT_SR_EPILOGUE", "staged")
+    _run_case("llama_h768", True, True)
