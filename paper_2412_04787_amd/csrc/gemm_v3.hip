@@ -225,6 +225,31 @@ struct Plan {
   }
 };
 
+// Tile order within one problem: reduction split bz outermost; within a
+// split, bands of kGroupRows tile rows, and within a band column by column
+// (problems more than 8 tiles wide; narrower ones stay row-major).  An XCD
+// owns a contiguous run of this order, so the 32 tiles its compute units
+// hold at once span about 4 tile rows and 8 tile columns, where row-major
+// order would span 1-2 rows and 16-32 columns: they share more of their
+// operand panels in the XCD's L2 (12 panels per step instead of 18; hidden
+// 4096 block: forward -2 %, backward + SR -1.5 %).
+#ifndef GEMM_GROUP_ROWS
+#define GEMM_GROUP_ROWS 4
+#endif
+constexpr int kGroupRows = GEMM_GROUP_ROWS;
+__host__ __device__ __forceinline__ void tile_coords(int local, int nbx, int nby, int& bx, int& by,
+                                                     int& bz) {
+  const int per_z = nbx * nby;
+  bz = local / per_z;
+  const int r = local - bz * per_z;
+  const int gr = nbx > 8 ? kGroupRows : 1;
+  const int band = r / (gr * nbx);
+  const int in = r - band * (gr * nbx);
+  const int rows = nby - band * gr < gr ? nby - band * gr : gr;
+  by = band * gr + in % rows;
+  bx = in / rows;
+}
+
 // Tile j of XCD x's list: XCD x owns [x n / 8, (x + 1) n / 8) of every
 // problem's n tiles, problems in launch order.  False past the end.
 template <class Epi>
@@ -312,9 +337,8 @@ __device__ __forceinline__ void gemm_v3_body(const Group<Epi>& grp, lds_u8* smem
 
   auto setup = [&](int g, int local, TileState& T) {
     const Prob<Epi>& P = grp.p[g];
-    const int bx = local % P.nbx;
-    const int by = (local / P.nbx) % P.nby;
-    const int bz = local / (P.nbx * P.nby);
+    int bx, by, bz;
+    tile_coords(local, P.nbx, P.nby, bx, by, bz);
     T.g = g;
     T.i0 = (int64_t)by * TILE;
     T.j0 = (int64_t)bx * TILE;
