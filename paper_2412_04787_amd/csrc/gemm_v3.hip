@@ -421,13 +421,23 @@ __device__ __forceinline__ void gemm_v3_body(const Group<Epi>& grp, lds_u8* smem
     uint32_t pb[WJ];          // packed codes (16 per lane), expanded at use
   };
   // pk: bf16 steps from packed codes, this lane's 64 bits of each B row
-  // (sub-step kk in bits 16 kk .. 16 kk + 15, read once per step)
-  auto read_frags = [&](const lds_u8* la, const lds_u8* lb, int kk, Frags& F, const u32x2* pk) {
+  // (sub-step kk in bits 16 kk .. 16 kk + 15, read once per step).
+  // pq: 8-bit steps from packed codes, this lane's 16-byte half of each B
+  // row (64 codes, read once per step; sub-step kk in word kk).  Lane half h
+  // then takes reduction elements 64 h .. 64 h + 63 of the step, sub-step kk
+  // the 16 from 64 h + 16 kk, and its A chunks follow the same order: chunk
+  // 4 h + kk instead of 2 kk + h.  (One 16-byte read per row half is free of
+  // bank conflicts; four 4-byte reads of words 2 kk + h, all lanes at one
+  // word offset in 32-byte rows, conflicted 4-way and cost the e4m3 forward
+  // 9 %.)
+  constexpr bool kPq = MB == KCP && !kLutB;
+  auto read_frags = [&](const lds_u8* la, const lds_u8* lb, int kk, Frags& F, const u32x2* pk,
+                        const i32x4* pq) {
 #pragma unroll
     for (int t = 0; t < WI; ++t) {
       if constexpr (MA == KC) {
         const int row = wi * 32 * WI + t * 32 + frow;
-        const int c = (2 * kk + h) ^ G::swz(row);
+        const int c = (kPq ? 4 * h + kk : 2 * kk + h) ^ G::swz(row);
         F.fa[t] = *(const __attribute__((address_space(3))) i32x4*)(la + row * KB + 16 * c);
       } else {
         const int col = wi * 32 * WI + t * 32 + 16 * ch + 4 * u4;
@@ -444,10 +454,7 @@ __device__ __forceinline__ void gemm_v3_body(const Group<Epi>& grp, lds_u8* smem
 #pragma unroll
         for (int i = 0; i < 4; ++i) F.fb[t][i] = (int)code_lut[(x16 >> (4 * i)) & 0xFu];
       } else if constexpr (MB == KCP) {
-        const int row = wj * 32 * WJ + t * 32 + frow;
-        const int w = 2 * kk + h;                  // 4-byte word of the row's 32 bytes
-        const int pos = 4 * ((w >> 2) ^ ((row >> 3) & 1)) + (w & 3);
-        F.pb[t] = *(const __attribute__((address_space(3))) uint32_t*)(lb + row * PKB + 4 * pos);
+        F.pb[t] = (uint32_t)pq[t][kk];
       } else if constexpr (MB == KC) {
         const int row = wj * 32 * WJ + t * 32 + frow;
         const int c = (2 * kk + h) ^ G::swz(row);
@@ -527,21 +534,30 @@ __device__ __forceinline__ void gemm_v3_body(const Group<Epi>& grp, lds_u8* smem
         pk[t] = *(const __attribute__((address_space(3))) u32x2*)(lb + row * 16 + 8 * (h ^ ((row >> 4) & 1)));
       }
     }
+    // (the DMA stores logical 16-byte half c of row r at half c ^ ((r >> 3) & 1))
+    i32x4 pq[WJ];
+    if constexpr (kPq) {
+#pragma unroll
+      for (int t = 0; t < WJ; ++t) {
+        const int row = wj * 32 * WJ + t * 32 + frow;
+        pq[t] = *(const __attribute__((address_space(3))) i32x4*)(lb + row * PKB + 16 * (h ^ ((row >> 3) & 1)));
+      }
+    }
     Frags F0, F1;
     if constexpr (ELEM != EF8) {
-      read_frags(la, lb, 0, F0, pk);
-      read_frags(la, lb, 1, F1, pk);
+      read_frags(la, lb, 0, F0, pk, pq);
+      read_frags(la, lb, 1, F1, pk, pq);
       __builtin_amdgcn_sched_barrier(0);
       mfma1(F0);
       __builtin_amdgcn_sched_barrier(0);
       mid();
       __builtin_amdgcn_sched_barrier(0);
       if constexpr (G::NKK == 4) {
-        read_frags(la, lb, 2, F0, pk);
+        read_frags(la, lb, 2, F0, pk, pq);
         __builtin_amdgcn_sched_barrier(0);
         mfma1(F1);
         __builtin_amdgcn_sched_barrier(0);
-        read_frags(la, lb, 3, F1, pk);
+        read_frags(la, lb, 3, F1, pk, pq);
         __builtin_amdgcn_sched_barrier(0);
         mfma1(F0);
         __builtin_amdgcn_sched_barrier(0);
@@ -550,14 +566,14 @@ __device__ __forceinline__ void gemm_v3_body(const Group<Epi>& grp, lds_u8* smem
     } else {
       // (e4m3 keeps the compiler's own order: a pair of sub-steps per
       // instruction leaves no registers for a further pair in flight)
-      read_frags(la, lb, 0, F0, pk);
-      read_frags(la, lb, 1, F1, pk);
+      read_frags(la, lb, 0, F0, pk, pq);
+      read_frags(la, lb, 1, F1, pk, pq);
       if constexpr (G::NKK == 4) {
         Frags F2, F3;
-        read_frags(la, lb, 2, F2, pk);
+        read_frags(la, lb, 2, F2, pk, pq);
         mfma2(F0, F1);
         mid();
-        read_frags(la, lb, 3, F3, pk);
+        read_frags(la, lb, 3, F3, pk, pq);
         mfma2(F2, F3);
       } else {
         mfma2(F0, F1);
