@@ -100,6 +100,12 @@ __device__ __forceinline__ void dma16(const uint8_t* g, lds_u8* l) {
   const uint32_t m0 = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)l);
   asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" : : "v"(g), "s"(m0) : "memory");
 }
+// The same with the non-temporal hint: for data read once (streaming
+// kernels), which should not displace reused lines from the caches.
+__device__ __forceinline__ void dma16_nt(const uint8_t* g, lds_u8* l) {
+  const uint32_t m0 = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)l);
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off nt" : : "v"(g), "s"(m0) : "memory");
+}
 __device__ __forceinline__ void dma4(const uint8_t* g, lds_u8* l) {
   const uint32_t m0 = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)l);
   asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dword %0, off" : : "v"(g), "s"(m0) : "memory");

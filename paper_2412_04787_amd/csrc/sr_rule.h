@@ -219,6 +219,62 @@ struct ChunkIO {
   }
 };
 
+// Ternary codes, a chunk of 8 weights whose steps all satisfy |delta| < 1
+// (the usual case: the step sizes of training are a small fraction of a grid
+// step), in mask arithmetic.  With n = trunc(delta) = 0 the rule moves q one
+// step in the direction of delta iff U < T = ceil(|delta| 2^32).  Let
+// h = floor(|delta| 2^16) (exact: |delta| 2^16 = |c 2^16 g| is the rounded
+// product scaled by a power of two, and products too small for that to hold
+// give h = 0 either way).  A draw with p16 < h moves (U < 2^16 (p16 + 1) <=
+// 2^16 h <= T); one with p16 > h does not (U >= 2^16 (h + 1) >= T); p16 = h
+// is left to the full rule, which reads the secondary draw.  The moves and
+// the signs of delta become bit masks (bit j for weight j), spread to the
+// 2-bit fields, and the fields are stepped up (not past code 2) or down (not
+// below code 0) by one masked add and one masked subtract.  Returns false,
+// with nothing changed, when the chunk holds a step of 1 or more, a
+// non-finite gradient, a tie or an invalid code 3: the full rule decides it.
+template <class Count>
+__device__ __forceinline__ bool sr_chunk_t2_small(uint32_t code, const f32x4 (&gv)[2], uint4 r, float c,
+                                                  uint32_t& out, Count& changed) {
+  // x = c g 2^16 = -delta 2^16, exact (|c| < 2^100 checked by the caller)
+  const float cs = c * 65536.0f;
+  float x[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) x[j] = cs * gv[j >> 2][j & 3];
+  // largest |x| of the chunk; NaN propagates (IEEE maximum)
+  float m = __builtin_elementwise_maximum(__builtin_elementwise_maximum(fabsf(x[0]), fabsf(x[1])), fabsf(x[2]));
+  m = __builtin_elementwise_maximum(__builtin_elementwise_maximum(m, fabsf(x[3])), fabsf(x[4]));
+  m = __builtin_elementwise_maximum(__builtin_elementwise_maximum(m, fabsf(x[5])), fabsf(x[6]));
+  m = __builtin_elementwise_maximum(m, fabsf(x[7]));
+  if (!(m < 65536.0f)) return false;
+  // bit j of mv: p16 < h (p16 - h < 0, both below 2^16); bit j of up: x < 0
+  // (delta > 0); dmin = 0 iff some p16 = h
+  uint32_t mv = 0, up_dir = 0, dmin = 0xFFFFFFFFu;
+#pragma unroll
+  for (int j = 7; j >= 0; --j) {
+    const uint32_t word = (j >> 1) == 0 ? r.x : (j >> 1) == 1 ? r.y : (j >> 1) == 2 ? r.z : r.w;
+    const uint32_t p = (j & 1) ? (word >> 16) : (word & 0xFFFFu);
+    uint32_t h;
+    asm("v_cvt_u32_f32_e64 %0, |%1|" : "=v"(h) : "v"(x[j]));   // floor(|x|), |x| < 2^16
+    const uint32_t d = p - h;
+    dmin = min(dmin, d);
+    mv = __builtin_amdgcn_alignbit(mv, d, 31);
+    up_dir = __builtin_amdgcn_alignbit(up_dir, __float_as_uint(x[j]), 31);
+  }
+  if (dmin == 0u || (code & (code >> 1) & 0x5555u) != 0u) return false;
+  auto spread = [](uint32_t v) {            // bit j -> bit 2 j (8 bits)
+    v = (v | (v << 4)) & 0x0F0Fu;
+    v = (v | (v << 2)) & 0x3333u;
+    return (v | (v << 1)) & 0x5555u;
+  };
+  const uint32_t M = spread(mv), U = spread(up_dir);
+  const uint32_t up = M & U & ~(code >> 1);                        // not from code 2
+  const uint32_t dn = M & ~U & (code | (code >> 1)) & 0x5555u;    // not from code 0
+  out = code + up - dn;
+  changed += __builtin_popcount(up | dn);
+  return true;
+}
+
 // The update of one chunk of CW consecutive weights, elements
 // 8 blk .. 8 blk + CW - 1 of their tensor (CW / 8 Philox blocks): codes `win`
 // (format CF), gradients gv.  Writes the new codes to `wout` and adds the
@@ -232,6 +288,16 @@ __device__ __forceinline__ void sr_chunk(const uint32_t (&win)[4], const f32x4 (
   uint4 r[NB];
 #pragma unroll
   for (int b = 0; b < NB; ++b) r[b] = philox_block(blk + b, 0u, a.step, a.tid, a.k0, a.k1);
+  if constexpr (CF == CF_T2 && CW == 8) {
+    if (fabsf(a.c) < 0x1p100f) {
+      uint32_t o;
+      if (sr_chunk_t2_small(win[0], gv, r[0], a.c, o, changed)) {
+        wout[0] = o;
+        wout[1] = wout[2] = wout[3] = 0u;
+        return;
+      }
+    }
+  }
 
   // finite check: a product chain stays finite unless some g is inf/NaN
   // (or a product overflows, which only sends the chunk to the full rule)

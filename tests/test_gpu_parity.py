@@ -246,6 +246,41 @@ def test_sr_update_bit_exact(lib, case):
     assert int(counters[1].item()) == 2 * n_nonfinite
 
 
+def test_sr_update_ternary_small_steps_any_codes(lib):
+    """Ternary codes as raw bytes (invalid code 3 included, which the rule
+    reads as q = 2 and clips), steps |delta| < 1 on most chunks (the common
+    case of training), some chunks with |delta| >= 1 or a non-finite
+    gradient, and enough elements that draws equal to the threshold's top
+    16 bits occur: every weight against the oracle."""
+    d_out, d_in = 1024, 1024
+    n = d_out * d_in
+    rng = np.random.default_rng(2024)
+    raw = rng.integers(0, 256, size=(d_out, d_in // 4), dtype=np.uint8)
+    q = O.unpack_ternary(raw, d_in)
+    g = rng.uniform(-0.999, 0.999, size=(d_out, d_in)).astype(np.float32)
+    flat = g.reshape(-1)
+    flat[40_003::65_537] = 2.5            # |delta| >= 1 in a few chunks
+    flat[123_457] = np.nan
+    lr, alpha, seed, step, tid = 1.0, 1.0, 5, 9, 3
+    # the oracle's draws: elements whose primary draw equals the top 16 bits
+    # of floor(|delta| 2^32) take the secondary draw
+    c = O.sr_step_size(lr, alpha)
+    delta = -(c * flat)
+    u = O.rng_u32(seed, step, tid, np.arange(n, dtype=np.uint64))
+    with np.errstate(invalid="ignore"):
+        h = np.floor(np.abs(delta.astype(np.float64)) * 65536.0)
+    ties = int(np.count_nonzero((np.abs(delta) < 1) & ((u >> 16) == h)))
+    assert ties >= 3, ties
+    w = make_weight(d_out, d_in, "ternary", -1, 1, alpha, tensor_id=tid)
+    Wq = torch.from_numpy(raw.copy()).to(DEV)
+    counters = torch.zeros((2,), dtype=torch.int64, device=DEV)
+    dqt.dqt_sr_update(w, Wq, torch.from_numpy(g).to(DEV), lr, seed, step, counters)
+    got = weight_codes_host(Wq, "ternary", d_in)
+    want, n_changed, n_nonfinite = O.sr_update(q.ravel(), flat, lr, alpha, -1, 1, seed, step, tid)
+    assert np.array_equal(got.ravel(), want), np.argwhere(got.ravel() != want)[:5]
+    assert int(counters[0].item()) == n_changed and int(counters[1].item()) == n_nonfinite == 1
+
+
 def test_sr_update_without_counters_and_repeatable(lib):
     d_out, d_in = 512, 512
     q = _weights(d_out, d_in, "ternary", -1, 1, 3)
