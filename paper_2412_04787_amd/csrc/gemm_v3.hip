@@ -82,7 +82,9 @@ struct Geo {
 };
 
 
-enum Elem { EI8 = 0, EF8 = 1, EBF16 = 2 };
+// EF4B: e4m3 A with ternary B as FP4 (E2M1) values formed from the packed
+// codes in registers (B must be packed codes)
+enum Elem { EI8 = 0, EF8 = 1, EBF16 = 2, EF4B = 3 };
 enum Mode { KC = 0, KM = 1, KCP = 2 };   // KCP: K-contiguous packed ternary codes (B only)
 
 // bytes per stage: A, then B (bf16 / 8-bit operand, or packed ternary codes)
@@ -142,6 +144,21 @@ __device__ __forceinline__ i32x4 expand16(uint32_t x, uint32_t lut) {
   const uint32_t d2 = __builtin_amdgcn_perm(ghh, efh, 0x05040100u), d3 = __builtin_amdgcn_perm(ghh, efh, 0x07060302u);
   return i32x4{(int)__builtin_amdgcn_perm(0u, lut, d0), (int)__builtin_amdgcn_perm(0u, lut, d1),
                (int)__builtin_amdgcn_perm(0u, lut, d2), (int)__builtin_amdgcn_perm(0u, lut, d3)};
+}
+// 16 packed ternary codes (code q + 1 at bits 2k) -> 16 FP4 (E2M1) values,
+// value k in nibble k of the 64-bit result (low nibble of each byte first):
+// q = -1 -> 0xA (-1.0), 0 -> 0x0, +1 -> 0x2 (+1.0).  Each 8-code half: its
+// two bytes to bytes 0 and 2, their nibbles to bytes 0..3, the 2-bit codes
+// to nibbles; then nibble = (code bit 1) * 2 + (code == 0) * 0xA.
+__device__ __forceinline__ u32x2 expand16_fp4(uint32_t x) {
+  auto half = [](uint32_t v) {
+    v = (v | (v << 4)) & 0x0F0F0F0Fu;
+    const uint32_t u = v | (v << 2);             // codes at nibble bits 0-1 (bits 2-3: junk)
+    const uint32_t z = ~u & ~(u >> 1) & 0x11111111u;
+    const uint32_t w = z | (z << 2);
+    return (u & 0x22222222u) | (w << 1);
+  };
+  return u32x2{half(__builtin_amdgcn_perm(0u, x, 0x0C010C00u)), half(__builtin_amdgcn_perm(0u, x, 0x0C030C02u))};
 }
 // Barrier that keeps the compiler from moving memory accesses across it; it
 // waits for this wave's LDS accesses but not for outstanding DMA.
@@ -300,7 +317,8 @@ __device__ __forceinline__ void gemm_v3_body(const Group<Epi>& grp, lds_u8* smem
   constexpr int LPS = NL + NLB;            // DMA instructions per thread per stage (at most)
   // (measured faster for the int8 forward, dX and dW; the e4m3 forward keeps
   // the burst after the barrier)
-  constexpr bool kSplitCopies = ELEM != EF8;
+  constexpr bool kSplitCopies = ELEM != EF8 && ELEM != EF4B;
+  static_assert(ELEM != EF4B || MB == KCP, "FP4 B comes from packed ternary codes");
   // bf16 operand from packed codes: two codes (a nibble) -> two bf16 by table
   constexpr bool kLutB = MB == KCP && ELEM == EBF16;
 
@@ -497,8 +515,25 @@ __device__ __forceinline__ void gemm_v3_body(const Group<Epi>& grp, lds_u8* smem
         const i32x4 a0 = opa(F0, ta), a1 = opa(F1, ta), b0 = opb(F0, tb), b1 = opb(F1, tb);
         const i32x8 av = {a0[0], a0[1], a0[2], a0[3], a1[0], a1[1], a1[2], a1[3]};
         const i32x8 bv = {b0[0], b0[1], b0[2], b0[3], b1[0], b1[1], b1[2], b1[3]};
-        // both operands e4m3 (format 0), unit E8M0 scales (127 = 2^0)
-        acc[ta][tb] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(bv, av, acc[ta][tb], 0, 0, 0, 127, 0, 127);
+        if constexpr (ELEM == EF4B) {
+          // B as FP4 (format 4: 32 values in the first four registers), A
+          // e4m3 (format 0), unit E8M0 scales (127 = 2^0).  With FP4 the
+          // first operand's lane half h holds reduction elements 16 h ..
+          // 16 h + 15 and 32 + 16 h .. 32 + 16 h + 15 of the instruction
+          // (the e4m3 operand: 32 h .. 32 h + 31).  The A chunks cover
+          // elements 64 h' + 32 m .. + 31 of the step (m: the sub-step
+          // pair), so half h takes the codes of word 2 m + h from both lane
+          // halves: one swap of the halves' upper and lower lanes gives
+          // them (lanes 0-31 keep their word 2 m and get word 2 m of lanes
+          // 32-63, which keep word 2 m + 1 and get that of lanes 0-31).
+          const auto sw = __builtin_amdgcn_permlane32_swap(F0.pb[tb], F1.pb[tb], false, false);
+          const u32x2 f0 = expand16_fp4(sw[0]), f1 = expand16_fp4(sw[1]);
+          const i32x8 bv4 = {(int)f0[0], (int)f0[1], (int)f1[0], (int)f1[1], 0, 0, 0, 0};
+          acc[ta][tb] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(bv4, av, acc[ta][tb], 4, 0, 0, 127, 0, 127);
+        } else {
+          // both operands e4m3 (format 0), unit E8M0 scales (127 = 2^0)
+          acc[ta][tb] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(bv, av, acc[ta][tb], 0, 0, 0, 127, 0, 127);
+        }
       }
   };
   auto stage_ptr = [&](int slot) { return smem + slot * SLOTB; };
@@ -544,7 +579,7 @@ __device__ __forceinline__ void gemm_v3_body(const Group<Epi>& grp, lds_u8* smem
       }
     }
     Frags F0, F1;
-    if constexpr (ELEM != EF8) {
+    if constexpr (ELEM != EF8 && ELEM != EF4B) {
       read_frags(la, lb, 0, F0, pk, pq);
       read_frags(la, lb, 1, F1, pk, pq);
       __builtin_amdgcn_sched_barrier(0);
@@ -1399,6 +1434,11 @@ using namespace v3;
 #ifndef KB_BWD
 #define KB_BWD 128
 #endif
+// ternary weights against e4m3 activations: B as FP4 values (1) or as e4m3
+// bytes (0) in the scaled MFMA
+#ifndef FWD_FP4B
+#define FWD_FP4B 1
+#endif
 #ifndef DX_PACKED_B
 #define DX_PACKED_B 0
 #endif
@@ -1513,7 +1553,7 @@ hipError_t launch_fwd_batch(const BatchCfg& c, const LinearIO* io, uint8_t* ws, 
     p.nbz = 1;
   }
   if (packed) {
-    if (c.act_e4m3) st << launch_group<EF8, KC, KCP, 128>(grp, ws, stream);
+    if (c.act_e4m3) st << launch_group<FWD_FP4B ? EF4B : EF8, KC, KCP, 128>(grp, ws, stream);
     else st << launch_group<EI8, KC, KCP, 128>(grp, ws, stream);
   } else {
     if (c.act_e4m3) st << launch_group<EF8, KC, KC, KB_FWD>(grp, ws, stream);
