@@ -288,12 +288,123 @@ def read_traffic(kernel_class: str, workload: str):
         return None
 
 
+def model_cpu_baseline(cfg, tokens: int, sr_weights: int):
+    """The oracle on one block's seven DQT linears (the model's shapes, its
+    ternary codes and lr), extrapolated by the model's layer count.  The
+    attention, norms, embedding and LM head are not DQT linears and have no
+    oracle; the value is the DQT part's flops over that time."""
+    import dataclasses
+
+    from paper_2412_04787_amd import workloads as W
+    lin = []
+    for _, grp in cfg.linears():
+        for name, d_in, d_out in grp:
+            lin.append(W.Linear(name, d_in, d_out, "mlp_hidden" if name == "down" else
+                                "attn_out" if name == "o" else
+                                "attn_in" if name in ("q", "k", "v") else "mlp_in"))
+    wl = dataclasses.replace(W.WORKLOADS["llama_h2048"], name=f"{cfg.name} block", M=cfg.tokens,
+                             linears=tuple(lin), wfmt="ternary", qmin=-1, qmax=1, lr=cfg.lr)
+    b = cpu_baseline(wl, tokens, max(1, sr_weights))
+    L = cfg.layers
+    b["value"] /= L
+    b["one_thread_value"] /= L
+    b["step_s_all_cores"] = round(b["step_s_all_cores"] * L, 2)
+    b["step_s_one_thread"] = round(b["step_s_one_thread"] * L, 2)
+    b["sample"] = (f"per-layer extrapolation x {L} of one block's DQT linears (the model's "
+                   f"attention, norms, embedding and LM head are not DQT linears and are not "
+                   f"in the oracle); block: " + b["sample"])
+    return b
+
+
+def run_model(args):
+    """A train step of the whole model (model_step.py): forward, backward
+    with the SR update of every DQT tensor, AdamW on the dense parameters."""
+    import torch
+
+    from paper_2412_04787_amd import dqt, model_step as MS
+
+    cfg = MS.MODELS[args.workload]
+    torch.cuda.set_device(0)
+    model = MS.DQTModel(cfg)
+    flops = cfg.step_flops()
+    losses = []
+    for s in range(args.warmup):
+        tok, tgt = MS.synthetic_batch(cfg, s)
+        losses.append(float(model.train_step(tok, tgt).item()))
+        print(f"warmup step {s + 1}: loss {losses[-1]:.4f}", file=sys.stderr, flush=True)
+    batches = [MS.synthetic_batch(cfg, args.warmup + s) for s in range(args.steps)]
+    stream = torch.cuda.current_stream()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    changed = []
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    ev[0].record(stream)
+    step_losses = []
+    c0 = model.counters.clone()
+    for s in range(args.steps):
+        step_losses.append(model.train_step(*batches[s]))
+        ev[s + 1].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    per = [ev[s].elapsed_time(ev[s + 1]) for s in range(args.steps)]
+    total_ms = ev[0].elapsed_time(ev[args.steps])
+    losses += [float(x.item()) for x in step_losses]
+    changed = int((model.counters - c0)[0].item())
+    ms = total_ms / args.steps
+    pct = lambda v, q: float(np.percentile(np.asarray(v), q))
+    value = flops["total"] / (ms * 1e-3) / 1e12
+    out = {
+        "metric": "DQT model train-step TFLOP/s (fwd+bwd of the whole model, SR update of every "
+                  "DQT weight in the step)",
+        "value": round(value, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 3),
+        "ms_per_step_median": round(pct(per, 50), 3),
+        "ms_per_step_p10": round(pct(per, 10), 3),
+        "ms_per_step_p90": round(pct(per, 90), 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "i8+bf16",
+        "data": "synthetic (uniform-random token ids)",
+        "config": {
+            "workload": f"{cfg.name}: {cfg.layers}-layer LLaMA-shaped model, hidden {cfg.hidden}, "
+                        f"{cfg.heads} heads, FFN {cfg.ffn}, vocab {cfg.vocab}, RMSNorm, RoPE; "
+                        f"all {7 * cfg.layers} block linears DQT ternary (int8 activations, "
+                        f"bf16 environment); batch {cfg.batch} x seq {cfg.seq}; lr {cfg.lr}",
+            "tokens": cfg.tokens, "dqt_weights": cfg.dqt_weights,
+            "sr_update": "fused into each layer's dW product (one backward call per group of "
+                         "linears sharing an input)",
+            "parallelism": "single GPU",
+        },
+        "flops_per_step": flops,
+        "dqt_tflops_share": round(flops["dqt_linears"] / (ms * 1e-3) / 1e12, 2),
+        "losses": [round(x, 4) for x in losses],
+        "loss_expected_at_init": round(MS.initial_loss_expected(cfg), 4),
+        "weights_changed_per_step": changed / args.steps,
+        "update_fraction_per_step": round(changed / args.steps / cfg.dqt_weights, 6),
+        "wall_s_timed_region": round(wall, 3),
+        "kernel_source_hash": kernel_source_hash(),
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = model_cpu_baseline(cfg, args.cpu_tokens, args.cpu_sr_weights // 4)
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1 "
                                    "(multi-GPU sharding is described, not built)"}))
         sys.exit(2)
+    from paper_2412_04787_amd import model_step
+
+    if args.workload in model_step.MODELS:
+        run_model(args)
+        return
     import torch
 
     from paper_2412_04787_amd import dqt, workloads as W
