@@ -151,6 +151,28 @@ dqt_status dqt_rmsnorm_act_quant(const void* X, int32_t x_t, const float* gamma,
                                  float eps, int64_t M, int32_t K, int32_t act_q,
                                  void* Xq, float* xdq, float* rinv, void* stream);
 
+/*
+ * Backward of the RMSNorm in front of a group of linears, for training a
+ * model built of DQT layers (the norm is the model's, not the paper's; its
+ * forward is dqt_rmsnorm_act_quant, whose rinv this takes).  The linears' dX
+ * pass straight through the activation quantiser, so the norm's output
+ * gradient is their sum.  For each row m of X [M, K], in fp32:
+ *   dn_mk = sum over i of dY_i[m, k]          (i = 0 .. n_dy - 1 in order)
+ *   g_mk  = dn_mk gamma_k,  c_m = (sum over k of g_mk x_mk) / K
+ *   dX_mk = r_m g_mk - x_mk r_m^3 c_m         (rounded to bf16)
+ *   gpart[b, k] = sum over the rows m of block b of dn_mk x_mk r_m
+ * so that the gradient of gamma is the sum of gpart over b (the caller
+ * sums).  Block b takes rows 4 b .. 4 b + 3, then those blocks * 4 further on.
+ *   n_dy: 1 .. 4; dY: host array of n_dy device pointers to [M, K] bf16.
+ *   X: [M, K], x_t = DQT_BF16; gamma: [K] fp32; rinv: [M] fp32.
+ *   dX: [M, K] bf16 (output, aliasing no input); gpart: [blocks, K] fp32
+ *   (output); blocks: 1 .. 65536.  K: a multiple of 16, at most 8192.
+ * Errors: DQT_ERR_NULL, DQT_ERR_SHAPE, DQT_ERR_DTYPE, DQT_ERR_ALIGN.
+ */
+dqt_status dqt_rmsnorm_backward(int32_t n_dy, const void* const* dY, const void* X, int32_t x_t,
+                                const float* gamma, const float* rinv, int64_t M, int32_t K,
+                                void* dX, float* gpart, int32_t blocks, void* stream);
+
 /* Bytes of device workspace dqt_linear_fwd needs for this weight: the 256
  * counter bytes, plus, for ternary weights whose d_in is not a multiple of
  * 64, d_out * d_in operand bytes they are unpacked into (with d_in a

@@ -91,6 +91,26 @@ dqt_status dqt_rmsnorm_act_quant(const void* X, int32_t x_t, const float* gamma,
                                                 Xq, xdq, rinv, static_cast<hipStream_t>(stream)));
 }
 
+dqt_status dqt_rmsnorm_backward(int32_t n_dy, const void* const* dY, const void* X, int32_t x_t,
+                                const float* gamma, const float* rinv, int64_t M, int32_t K,
+                                void* dX, float* gpart, int32_t blocks, void* stream) {
+  if (n_dy < 1 || n_dy > dqt::kMaxNormDy) return DQT_ERR_SHAPE;
+  if (M < 0 || M > (int64_t(1) << 28) || K < 16 || (K % 16) != 0 || K > 8192) return DQT_ERR_SHAPE;
+  if (blocks < 1 || blocks > 65536) return DQT_ERR_SHAPE;
+  if (x_t != DQT_BF16) return DQT_ERR_DTYPE;
+  if (dY == nullptr || X == nullptr || gamma == nullptr || rinv == nullptr || dX == nullptr ||
+      gpart == nullptr)
+    return DQT_ERR_NULL;
+  for (int i = 0; i < n_dy; ++i) {
+    if (dY[i] == nullptr) return DQT_ERR_NULL;
+    if (!aligned16(dY[i])) return DQT_ERR_ALIGN;
+  }
+  if (!aligned16(X) || !aligned16(gamma) || !aligned16(dX) || !aligned16(gpart)) return DQT_ERR_ALIGN;
+  if ((reinterpret_cast<uintptr_t>(rinv) & 3u) != 0) return DQT_ERR_ALIGN;
+  return from_hip(dqt::launch_rmsnorm_backward(n_dy, dY, X, gamma, rinv, M, K, dX, gpart, blocks,
+                                               static_cast<hipStream_t>(stream)));
+}
+
 dqt_status dqt_act_quant_batch(int32_t n, const dqt_act_io* io, int32_t x_t, int64_t M,
                                int32_t act_q, void* stream) {
   if (n < 0 || n > DQT_MAX_BATCH) return DQT_ERR_SHAPE;

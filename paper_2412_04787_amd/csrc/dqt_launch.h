@@ -26,6 +26,17 @@ hipError_t launch_kernel(void (*k)(P...), dim3 grid, dim3 block, hipStream_t s, 
   std::tuple<std::decay_t<P>...> vals(std::forward<A>(a)...);
   return launch_argv(k, grid, block, s, vals, std::index_sequence_for<P...>{});
 }
+template <class... P, class... A>
+hipError_t launch_kernel_lds(void (*k)(P...), dim3 grid, dim3 block, size_t lds, hipStream_t s, A&&... a) {
+  static_assert(sizeof...(P) == sizeof...(A), "argument count");
+  std::tuple<std::decay_t<P>...> vals(std::forward<A>(a)...);
+  void* argv[sizeof...(P)];
+  std::apply([&](auto&... v) {
+    int i = 0;
+    ((argv[i++] = static_cast<void*>(&v)), ...);
+  }, vals);
+  return hipLaunchKernel(reinterpret_cast<const void*>(k), grid, block, argv, lds, s);
+}
 // The first error of a sequence of launches.
 struct LaunchStatus {
   hipError_t e = hipSuccess;
@@ -65,6 +76,13 @@ struct DwArgs {
 
 hipError_t launch_act_quant(const void* X, bool x_bf16, int64_t M, int K, bool e4m3, void* Xq,
                             float* xdq, hipStream_t stream);
+// Backward of the RMSNorm feeding a group of linears: dX of the norm's input
+// from the sum of up to kMaxNormDy upstream gradients (bf16), and per-block
+// partial sums of the gamma gradient, gpart [blocks, K].
+constexpr int kMaxNormDy = 4;
+hipError_t launch_rmsnorm_backward(int n_dy, const void* const* dY, const void* X, const float* gamma,
+                                   const float* rinv, int64_t M, int K, void* dX, float* gpart,
+                                   int blocks, hipStream_t stream);
 // RMSNorm (fp32, fixed summation order) then the per-token quantisation;
 // rinv (nullable) receives each row's 1 / rms.
 hipError_t launch_rmsnorm_act_quant(const void* X, bool x_bf16, const float* gamma, float eps, int64_t M,

@@ -25,7 +25,7 @@ EXPORTS = (
     "dqt_linear_bwd", "dqt_linear_fwd_batch_workspace", "dqt_linear_fwd_batch",
     "dqt_linear_bwd_batch_workspace", "dqt_linear_bwd_batch", "dqt_linear_bwd_sr_batch",
     "dqt_linear_fwd_batch_noalloc", "dqt_sr_table_bytes", "dqt_sr_table_build",
-    "dqt_sr_update_table", "dqt_rmsnorm_act_quant", "dqt_absmax_requant_workspace",
+    "dqt_sr_update_table", "dqt_rmsnorm_act_quant", "dqt_rmsnorm_backward", "dqt_absmax_requant_workspace",
     "dqt_absmax_requant_batch",
     "dqt_sr_update_batch", "dqt_adamw_sr_update", "dqt_adamw_sr_update_batch",
     "dqt_update_variant_workspace", "dqt_update_variant_batch",
@@ -79,6 +79,7 @@ _SIGS = {
     "dqt_act_quant": (_i32, [_vp, _i32, _i64, _i32, _i32, _vp, _vp, _vp]),
     "dqt_act_quant_batch": (_i32, [_i32, _vp, _i32, _i64, _i32, _vp]),
     "dqt_rmsnorm_act_quant": (_i32, [_vp, _i32, _vp, _f32, _i64, _i32, _i32, _vp, _vp, _vp, _vp]),
+    "dqt_rmsnorm_backward": (_i32, [_i32, _vp, _vp, _i32, _vp, _vp, _i64, _i32, _vp, _vp, _i32, _vp]),
     "dqt_linear_fwd_workspace": (ctypes.c_size_t, [_wp]),
     "dqt_linear_fwd": (_i32, [_wp, _vp, _vp, _i32, _i64, _i32, _vp, _vp, _vp, _i32, _vp,
                               ctypes.c_size_t, _vp]),
@@ -182,6 +183,16 @@ def dqt_rmsnorm_act_quant(X, gamma, eps: float, act_q: int, Xq, xdq, rinv=None, 
     _check("dqt_rmsnorm_act_quant",
            load().dqt_rmsnorm_act_quant(_ptr(X), dtype_code(X), _ptr(gamma), eps, M, K, act_q,
                                         _ptr(Xq), _ptr(xdq), _ptr(rinv), _stream(stream)))
+
+
+def dqt_rmsnorm_backward(dYs, X, gamma, rinv, dX, gpart, stream=None):
+    """dYs: list of 1..4 [M, K] bf16 tensors; gpart: [blocks, K] fp32."""
+    M, K = X.shape
+    ptrs = (ctypes.c_void_p * len(dYs))(*[t.data_ptr() for t in dYs])
+    _check("dqt_rmsnorm_backward",
+           load().dqt_rmsnorm_backward(len(dYs), ptrs, _ptr(X), dtype_code(X), _ptr(gamma),
+                                       _ptr(rinv), M, K, _ptr(dX), _ptr(gpart), gpart.shape[0],
+                                       _stream(stream)))
 
 
 def dqt_linear_fwd_workspace(w: DqtWeight) -> int:

@@ -89,6 +89,10 @@ MODELS = {
 }
 
 
+# blocks of the norm backward (each one sums the gamma gradient of its rows)
+MS_NORM_BLOCKS = 1024
+
+
 def _pack_ternary_dev(q):
     """int8 codes {-1, 0, 1} [d_out, d_in] -> packed bytes [d_out, d_in / 4]:
     code q + 1 of weight k at bits 2 (k mod 4) of byte k / 4."""
@@ -181,19 +185,22 @@ class _DQTGroupFn:
                                             dqt.DQT_BF16, m.cfg.lr, m.cfg.seed, m.step_no,
                                             m.counters,
                                             m.workspace(dqt.dqt_linear_bwd_batch_workspace(io, T)))
-                dn = dXs[0].float()
-                for d in dXs[1:]:
-                    dn += d.float()
                 if not ctx.has_gamma:
+                    if len(dXs) == 1:
+                        return dXs[0], None, None
+                    dn = dXs[0].float()
+                    for d in dXs[1:]:
+                        dn += d.float()
                     return dn.to(torch.bfloat16), None, None
-                # RMSNorm backward: y = x r gamma, r = (mean(x^2) + eps)^(-1/2)
+                # the norm's backward (y = x r gamma, r = (mean(x^2) + eps)^(-1/2))
+                # on the sum of the linears' dX, in one kernel; the gamma
+                # gradient from its per-block partial sums
                 x, gamma, rinv = saved[2], saved[3], saved[4]
-                xf = x.float()
-                r = rinv[:, None]
-                g = dn * gamma
-                dx = r * g - xf * (r * r * r) * ((g * xf).sum(-1, keepdim=True) / x.shape[1])
-                dgamma = (dn * xf * r).sum(0)
-                return dx.to(torch.bfloat16), dgamma, None
+                dx = torch.empty_like(x)
+                gpart = torch.empty((MS_NORM_BLOCKS, x.shape[1]), dtype=torch.float32,
+                                    device=x.device)
+                dqt.dqt_rmsnorm_backward(dXs, x, gamma, rinv, dx, gpart)
+                return dx, gpart.sum(0), None
 
         cls._cls = Fn
         return Fn
