@@ -270,8 +270,12 @@ def kernel_source_hash() -> str:
 
 
 def read_traffic(kernel_class: str, workload: str):
-    """HBM bytes per launch from the committed rocprofv3 counter summary, if it
-    was taken on the current kernel sources; else None."""
+    """Bytes per launch that the L2 caches fetched from and wrote to memory
+    (FETCH_SIZE + WRITE_SIZE, scaled by a plain copy of known size), from the
+    committed rocprofv3 counter summary, if it was taken on the current
+    kernel sources; else None.  The counters see the last-level cache (MALL)
+    and HBM alike, so on a block whose data fits the 256 MB MALL this is an
+    upper bound of the HBM bytes."""
     path = os.path.join(ROOT, "profiles", f"{kernel_class}_{workload}_counters.txt")
     if not os.path.exists(path):
         return None
@@ -283,7 +287,7 @@ def read_traffic(kernel_class: str, workload: str):
     if vals.get("kernel_source_hash") != kernel_source_hash():
         return None
     try:
-        return float(vals["hbm_bytes_per_launch"])
+        return float(vals["fetch_write_bytes_per_launch"])
     except (KeyError, ValueError):
         return None
 
