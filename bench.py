@@ -310,8 +310,7 @@ def model_cpu_baseline(cfg, tokens: int, sr_weights: int):
                              linears=tuple(lin), wfmt="ternary", qmin=-1, qmax=1, lr=cfg.lr)
     b = cpu_baseline(wl, tokens, max(1, sr_weights))
     L = cfg.layers
-    b["value"] /= L
-    b["one_thread_value"] /= L
+    # every layer has the block's flops and its time: the rate is the block's
     b["step_s_all_cores"] = round(b["step_s_all_cores"] * L, 2)
     b["step_s_one_thread"] = round(b["step_s_one_thread"] * L, 2)
     b["sample"] = (f"per-layer extrapolation x {L} of one block's DQT linears (the model's "
