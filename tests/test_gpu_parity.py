@@ -83,7 +83,8 @@ def test_act_quant_batch_matches_oracle(lib, x_t, act):
 
 # -------------------------------------------------------------- forward
 
-FWD_SHAPES = [(1, 16, 16), (300, 272, 400), (512, 256, 256), (129, 48, 144), (1000, 1024, 208)]
+FWD_SHAPES = [(1, 16, 16), (300, 272, 400), (512, 256, 256), (129, 48, 144), (1000, 1024, 208),
+              (257, 320, 96)]   # d_in 320: packed codes with a half step at the end
 FWD_KINDS = [  # act, wfmt, qmin, qmax, x_t, y_out
     ("i8", "ternary", -1, 1, "f32", "f32"),
     ("i8", "ternary", -1, 1, "bf16", "bf16"),
