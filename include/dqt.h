@@ -173,11 +173,15 @@ dqt_status dqt_rmsnorm_backward(int32_t n_dy, const void* const* dY, const void*
                                 const float* gamma, const float* rinv, int64_t M, int32_t K,
                                 void* dX, float* gpart, int32_t blocks, void* stream);
 
-/* Bytes of device workspace dqt_linear_fwd needs for this weight: the 256
- * counter bytes, plus, for ternary weights whose d_in is not a multiple of
- * 64, d_out * d_in operand bytes they are unpacked into (with d_in a
- * multiple of 64 the packed codes feed the matrix cores directly).  Depends
- * only on the descriptor. */
+/* Bytes of device workspace for the fastest form of dqt_linear_fwd on this
+ * weight: the 256 counter bytes, plus, for ternary, 3-bit and 4-bit codes,
+ * d_out * d_in bytes the codes are expanded into (int8 or e4m3 bytes, or
+ * FP4 E2M1 values at half a byte each for ternary codes against e4m3
+ * activations).  Ternary codes with d_in a multiple of 64 also run from the
+ * packed codes, expanded in registers, with the 256 counter bytes alone: a
+ * smaller workspace than this selects that form (same results for int8
+ * activations, bit for bit; within the e4m3 forward's tolerance otherwise).
+ * Depends only on the descriptor. */
 size_t dqt_linear_fwd_workspace(const dqt_weight* w);
 
 /*
@@ -194,8 +198,10 @@ size_t dqt_linear_fwd_workspace(const dqt_weight* w);
  *   Xq, xdq: [M, d_in] codes and [M] scales; written when X != NULL, read
  *          otherwise.  Keep them for dqt_linear_bwd.
  *   Y:     [M, d_out], y_t = DQT_F32 or DQT_BF16.  (output)
- *   ws, ws_bytes: device workspace of at least dqt_linear_fwd_workspace()
- *          bytes (may be NULL when that is 0).
+ *   ws, ws_bytes: device workspace of dqt_linear_fwd_workspace() bytes, or
+ *          of at least the 256 counter bytes for ternary codes with d_in a
+ *          multiple of 64 (see dqt_linear_fwd_workspace); DQT_ERR_WORKSPACE
+ *          when smaller.
  */
 dqt_status dqt_linear_fwd(const dqt_weight* w, const void* Wq,
                           const void* X, int32_t x_t, int64_t M, int32_t act_q,
@@ -281,8 +287,9 @@ typedef struct {
   float* dW;            /* weight gradient [d_out, d_in] fp32, or NULL to skip */
 } dqt_linear_io;
 
-/* Workspace bytes of dqt_linear_fwd_batch (0 if none); depends only on the
- * descriptors. */
+/* Workspace bytes of the fastest form of dqt_linear_fwd_batch (see
+ * dqt_linear_fwd_workspace: the sum over the linears, counters once);
+ * depends only on the descriptors. */
 size_t dqt_linear_fwd_batch_workspace(int32_t n, const dqt_linear_io* io);
 
 /* Forward of n linears (see dqt_linear_fwd; inputs already quantised).
@@ -296,17 +303,19 @@ dqt_status dqt_linear_fwd_batch(int32_t n, const dqt_linear_io* io, int64_t M,
  * argument, for callers that cannot allocate device memory: code under HIP
  * graph capture, tight serving loops, harnesses that forbid allocation.  The
  * call allocates nothing: its scratch (the tile counters, plus the operand
- * bytes of dqt_linear_fwd_batch_workspace() for 4-bit codes or ternary rows
- * whose d_in is not a multiple of 64) is a static device array of
+ * bytes of dqt_linear_fwd_batch_workspace() when they fit; ternary codes
+ * whose expansion does not fit run from the packed codes) is a static device
+ * array of
  * DQT_NOALLOC_SCRATCH_BYTES that each GPU the library runs on holds until
  * the process ends; its address is looked up on a device's first call.
  * Calls on one GPU share that array, so calls that overlap in time on one
  * GPU (different streams, or threads without ordering) race and must not be
  * made; the counters are cleared by every call on its stream.
  *   Arguments and results: those of dqt_linear_fwd_batch.
- *   Errors: those of dqt_linear_fwd_batch; DQT_ERR_WORKSPACE when the batch
- *   needs more than DQT_NOALLOC_SCRATCH_BYTES of scratch (nothing is
- *   launched); DQT_ERR_HIP when the array's address cannot be found.
+ *   Errors: those of dqt_linear_fwd_batch; DQT_ERR_WORKSPACE when the
+ *   smallest workspace of the batch exceeds DQT_NOALLOC_SCRATCH_BYTES
+ *   (nothing is launched); DQT_ERR_HIP when the array's address cannot be
+ *   found.
  */
 #define DQT_NOALLOC_SCRATCH_BYTES (32u << 20)
 

@@ -159,6 +159,19 @@ dqt_status check_batch(int32_t n, const dqt_linear_io* io, dqt::LinearIO* L, int
 
 }  // namespace
 
+namespace {
+
+// The smallest workspace a forward batch accepts (the packed form of ternary
+// codes needs only the counters); 0 for a batch the checks refuse.
+size_t fwd_batch_workspace_least(int32_t n, const dqt_linear_io* io) {
+  dqt::LinearIO L[DQT_MAX_BATCH];
+  int32_t wfmt;
+  if (check_batch(n, io, L, &wfmt) != DQT_OK) return 0;
+  return dqt::fwd_batch_workspace_min(n, L, code_format(wfmt));
+}
+
+}  // namespace
+
 size_t dqt_linear_fwd_batch_workspace(int32_t n, const dqt_linear_io* io) {
   dqt::LinearIO L[DQT_MAX_BATCH];
   int32_t wfmt;
@@ -184,13 +197,14 @@ dqt_status dqt_linear_fwd_batch(int32_t n, const dqt_linear_io* io, int64_t M, i
     if (!aligned16(io[l].Wq) || !aligned16(io[l].Xq) || !aligned16(io[l].xdq) || !aligned16(io[l].Y))
       return DQT_ERR_ALIGN;
   }
-  const size_t need = dqt::fwd_batch_workspace(n, L, code_format(wfmt), nullptr);
+  const size_t need = dqt::fwd_batch_workspace_min(n, L, code_format(wfmt));
   if (need > 0 && (ws == nullptr || ws_bytes < need)) return DQT_ERR_WORKSPACE;
   if (need > 0 && !aligned16(ws)) return DQT_ERR_ALIGN;
   dqt::BatchCfg c{n, M, wfmt == DQT_TERNARY2, act_q == DQT_FP8E4M3, y_t == DQT_BF16};
   c.w_int4 = wfmt == DQT_INT4;
   c.w_int3 = wfmt == DQT_INT3;
-  return from_hip(dqt::launch_fwd_batch(c, L, static_cast<uint8_t*>(ws), static_cast<hipStream_t>(stream)));
+  return from_hip(dqt::launch_fwd_batch(c, L, static_cast<uint8_t*>(ws), ws == nullptr ? 0 : ws_bytes,
+                                        static_cast<hipStream_t>(stream)));
 }
 
 size_t dqt_linear_bwd_batch_workspace(int32_t n, const dqt_linear_io* io, int64_t M) {
@@ -640,7 +654,14 @@ dqt_status dqt_linear_fwd(const dqt_weight* w, const void* Wq, const void* X, in
   if (!aligned16(Wq) || !aligned16(Xq) || !aligned16(xdq) || !aligned16(Y) ||
       (X != nullptr && !aligned16(X)))
     return DQT_ERR_ALIGN;
-  const size_t need = dqt_linear_fwd_workspace(w);
+  dqt_linear_io io{};
+  io.w = w;
+  io.Wq = const_cast<void*>(Wq);
+  io.Xq = Xq;
+  io.xdq = xdq;
+  io.Y = Y;
+  // refused before the quantisation is launched
+  const size_t need = fwd_batch_workspace_least(1, &io);
   if (need > 0 && (ws == nullptr || ws_bytes < need)) return DQT_ERR_WORKSPACE;
   if (need > 0 && !aligned16(ws)) return DQT_ERR_ALIGN;
   if (X != nullptr) {
@@ -648,12 +669,6 @@ dqt_status dqt_linear_fwd(const dqt_weight* w, const void* Wq, const void* X, in
                                         xdq, static_cast<hipStream_t>(stream)));
     if (st != DQT_OK) return st;
   }
-  dqt_linear_io io{};
-  io.w = w;
-  io.Wq = const_cast<void*>(Wq);
-  io.Xq = Xq;
-  io.xdq = xdq;
-  io.Y = Y;
   return dqt_linear_fwd_batch(1, &io, M, act_q, y_t, ws, ws_bytes, stream);
 }
 

@@ -133,11 +133,13 @@ struct BwdPlan {
   size_t total;
 };
 size_t fwd_batch_workspace(int n, const LinearIO* io, int cf, size_t* offs);
+size_t fwd_batch_workspace_min(int n, const LinearIO* io, int cf);
 // int4 codes [n] -> int8 codes (one byte per weight), n a multiple of 16
 hipError_t launch_unpack_int4(const void* src, int8_t* dst, int64_t n, hipStream_t stream);
 // int3 codes [n] -> int8 codes, n a multiple of 16
 hipError_t launch_unpack_int3(const void* src, int8_t* dst, int64_t n, hipStream_t stream);
-hipError_t launch_fwd_batch(const BatchCfg& c, const LinearIO* io, uint8_t* ws, hipStream_t stream);
+hipError_t launch_fwd_batch(const BatchCfg& c, const LinearIO* io, uint8_t* ws, size_t ws_bytes,
+                           hipStream_t stream);
 BwdPlan plan_bwd_batch(int n, const LinearIO* io, int64_t M);
 hipError_t launch_dx_batch(const BatchCfg& c, const LinearIO* io, uint8_t* ws, const BwdPlan& P,
                            hipStream_t stream);

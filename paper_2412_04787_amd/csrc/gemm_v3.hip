@@ -85,11 +85,16 @@ struct Geo {
 // EF4B: e4m3 A with ternary B as FP4 (E2M1) values formed from the packed
 // codes in registers (B must be packed codes)
 enum Elem { EI8 = 0, EF8 = 1, EBF16 = 2, EF4B = 3 };
-enum Mode { KC = 0, KM = 1, KCP = 2 };   // KCP: K-contiguous packed ternary codes (B only)
+// KCP: K-contiguous packed ternary codes (B only); KF4: K-contiguous FP4
+// (E2M1) values, two per byte (B only, with e4m3 A), expanded from the codes
+// by a pass into the workspace
+enum Mode { KC = 0, KM = 1, KCP = 2, KF4 = 3 };
 
 // bytes per stage: A, then B (bf16 / 8-bit operand, or packed ternary codes)
 template <int MB, int KB, int EB>
-constexpr int slot_bytes() { return Geo<KB>::OPB + (MB == KCP ? TILE * pkb<KB, EB>() : Geo<KB>::OPB); }
+constexpr int slot_bytes() {
+  return Geo<KB>::OPB + (MB == KCP ? TILE * pkb<KB, EB>() : MB == KF4 ? TILE * KB / 2 : Geo<KB>::OPB);
+}
 
 
 // Global operand: base of element (row 0, reduction 0), row stride in bytes,
@@ -188,7 +193,7 @@ struct Plan {
   static constexpr int PK = pkb<KB, EB>();
   static constexpr int CH = TILE * PK / 16;   // packed 16-byte chunks per stage
   // packed codes: all threads (32-byte rows), or the first CH threads (16-byte rows)
-  static constexpr int NL = MODE == KCP ? (CH >= NTD ? CH / NTD : 1) : G::NL;
+  static constexpr int NL = MODE == KCP ? (CH >= NTD ? CH / NTD : 1) : MODE == KF4 ? G::NL / 2 : G::NL;
   // K-major: a thread's chunks cover two reduction rows, k and k + KSTEP,
   // when one wave instruction's 8 rows repeat within a region (4 waves)
   static constexpr int KSTEP = MODE == KM && NTD < G::KR * 8 ? NTD / 8 : 0;
@@ -216,6 +221,16 @@ struct Plan {
         g[q] = o.p + gr * o.ld + r_begin / 4 + 16 * c;
         back = r_begin / 4 + 16 * c;
         rk = 64 * c;
+      } else if constexpr (MODE == KF4) {
+        // rows of KB / 2 bytes (4 chunks of 32 values), chunk c of row r at
+        // position c ^ ((r >> 2) & 3): conflict-free 16-byte reads
+        const int row = p >> 2;
+        const int c = (p & 3) ^ ((row >> 2) & 3);
+        int64_t gr = row0 + row;
+        if (gr > o.n - 1) gr = o.n - 1;
+        g[q] = o.p + gr * o.ld + r_begin / 2 + 16 * c;
+        back = r_begin / 2 + 16 * c;
+        rk = 32 * c;
       } else if constexpr (MODE == KC) {
         const int row = p / G::CPR;
         const int c = (p % G::CPR) ^ G::swz(row);   // logical chunk (same for every q)
@@ -238,7 +253,7 @@ struct Plan {
         }
       }
     }
-    inc = MODE == KC ? KB : MODE == KCP ? PK : G::KR * o.ld;
+    inc = MODE == KC ? KB : MODE == KCP ? PK : MODE == KF4 ? KB / 2 : G::KR * o.ld;
   }
 };
 
@@ -318,7 +333,8 @@ __device__ __forceinline__ void gemm_v3_body(const Group<Epi>& grp, lds_u8* smem
   // (measured faster for the int8 forward, dX and dW; the e4m3 forward keeps
   // the burst after the barrier)
   constexpr bool kSplitCopies = ELEM != EF8 && ELEM != EF4B;
-  static_assert(ELEM != EF4B || MB == KCP, "FP4 B comes from packed ternary codes");
+  static_assert(ELEM != EF4B || MB == KCP || MB == KF4, "FP4 B comes from ternary codes");
+  static_assert(MB != KF4 || (ELEM == EF4B && KB == 128), "KF4 holds FP4 B of 128-element steps");
   // bf16 operand from packed codes: two codes (a nibble) -> two bf16 by table
   constexpr bool kLutB = MB == KCP && ELEM == EBF16;
 
@@ -417,7 +433,9 @@ __device__ __forceinline__ void gemm_v3_body(const Group<Epi>& grp, lds_u8* smem
 #pragma unroll
     for (int q = 0; q < NL; ++q)
       if (rbase + pa.rk_of(q) >= T.rlen) *(__attribute__((address_space(3))) i32x4*)(la + (q * NTD + dtid) * 16) = z;
-    if constexpr (MB != KCP)
+    // (packed codes and FP4 values past the end need no zeroing: they meet
+    // zeroed A, and neither holds a NaN or an infinity)
+    if constexpr (MB != KCP && MB != KF4)
 #pragma unroll
       for (int q = 0; q < NL; ++q)
         if (rbase + pb.rk_of(q) >= T.rlen) *(__attribute__((address_space(3))) i32x4*)(lb + (q * NTD + dtid) * 16) = z;
@@ -473,6 +491,15 @@ __device__ __forceinline__ void gemm_v3_body(const Group<Epi>& grp, lds_u8* smem
         for (int i = 0; i < 4; ++i) F.fb[t][i] = (int)code_lut[(x16 >> (4 * i)) & 0xFu];
       } else if constexpr (MB == KCP) {
         F.pb[t] = (uint32_t)pq[t][kk];
+      } else if constexpr (MB == KF4) {
+        // the FP4 operand of sub-step pair m = kk / 2 (read with its even
+        // sub-step): lane half h takes the row's 32 values from 64 m + 32 h,
+        // which are the elements its e4m3 partner lanes pair them with
+        if ((kk & 1) == 0) {
+          const int row = wj * 32 * WJ + t * 32 + frow;
+          const int c = (kk + h) ^ ((row >> 2) & 3);
+          F.fb[t] = *(const __attribute__((address_space(3))) i32x4*)(lb + row * (KB / 2) + 16 * c);
+        }
       } else if constexpr (MB == KC) {
         const int row = wj * 32 * WJ + t * 32 + frow;
         const int c = (2 * kk + h) ^ G::swz(row);
@@ -490,7 +517,7 @@ __device__ __forceinline__ void gemm_v3_body(const Group<Epi>& grp, lds_u8* smem
   auto opb = [&](const Frags& F, int t) {
     if constexpr (kLutB) return F.fb[t];
     else if constexpr (MB == KCP) return expand16(F.pb[t], ELEM == EF8 ? 0x003800B8u : 0x000100FFu);
-    else return MB == KC ? F.fb[t] : join(F.kb[t][0], F.kb[t][1]);
+    else return MB == KC || MB == KF4 ? F.fb[t] : join(F.kb[t][0], F.kb[t][1]);
   };
   // MFMAs of one sub-step (int8 / bf16), or of two sub-steps (e4m3, whose
   // instruction reduces 64 elements: sub-step pairs (0, 1) and (2, 3)).
@@ -515,7 +542,12 @@ __device__ __forceinline__ void gemm_v3_body(const Group<Epi>& grp, lds_u8* smem
         const i32x4 a0 = opa(F0, ta), a1 = opa(F1, ta), b0 = opb(F0, tb), b1 = opb(F1, tb);
         const i32x8 av = {a0[0], a0[1], a0[2], a0[3], a1[0], a1[1], a1[2], a1[3]};
         const i32x8 bv = {b0[0], b0[1], b0[2], b0[3], b1[0], b1[1], b1[2], b1[3]};
-        if constexpr (ELEM == EF4B) {
+        if constexpr (ELEM == EF4B && MB == KF4) {
+          // FP4 B from the workspace, already in the instruction's order
+          const i32x4 f = F0.fb[tb];
+          const i32x8 bv4 = {f[0], f[1], f[2], f[3], 0, 0, 0, 0};
+          acc[ta][tb] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(bv4, av, acc[ta][tb], 4, 0, 0, 127, 0, 127);
+        } else if constexpr (ELEM == EF4B) {
           // B as FP4 (format 4: 32 values in the first four registers), A
           // e4m3 (format 0), unit E8M0 scales (127 = 2^0).  With FP4 the
           // first operand's lane half h holds reduction elements 16 h ..
@@ -1064,6 +1096,17 @@ __global__ __launch_bounds__(256) void unpack_ternary_kernel(const SegTab tab) {
   static_cast<uint4*>(tab.dst[s])[t] = make_uint4(o[0], o[1], o[2], o[3]);
 }
 
+// Packed ternary codes -> FP4 (E2M1) values, two per byte in weight order
+// (weight k in the low nibble of byte k / 2 when k is even): the B operand of
+// the e4m3 forward.  16 weights per thread.
+__global__ __launch_bounds__(256) void expand_fp4_kernel(const SegTab tab) {
+  const int s = seg_of_block(tab);
+  const int64_t t = (int64_t)(blockIdx.x - tab.b0[s]) * 256 + threadIdx.x;
+  if (t >= tab.n16[s]) return;
+  const u32x2 v = expand16_fp4(static_cast<const uint32_t*>(tab.src[s])[t]);
+  static_cast<uint2*>(tab.dst[s])[t] = make_uint2(v[0], v[1]);
+}
+
 // int4 codes (two's-complement nibbles, weight k at bits 4 (k mod 2) of byte
 // k / 2) -> one operand byte per weight (int8, or e4m3, exact for |q| <= 8),
 // same order; 16 weights per thread.
@@ -1476,24 +1519,42 @@ static bool fwd_packed(int n, const LinearIO* io) {
   return true;
 }
 
+// Forward workspace: the tile counters, then per linear the operand bytes
+// its codes are expanded into (one byte per weight; FP4 uses half).  Ternary
+// codes with d_in a multiple of 64 can also run straight from the packed
+// codes, expanded in registers, with the counters alone: that form needs
+// only fwd_batch_workspace_min, the expanded one (measured faster: the
+// expansion in the main loop costs more than a pass and the extra copies)
+// is taken whenever the workspace holds it.
 size_t fwd_batch_workspace(int n, const LinearIO* io, int cf, size_t* offs) {
   size_t total = kSchedBytes;
-  const bool unpack = (cf == CF_T2 && !fwd_packed(n, io)) || cf == CF_I4 || cf == CF_I3;
+  const bool unpack = cf == CF_T2 || cf == CF_I4 || cf == CF_I3;
   for (int l = 0; l < n; ++l) {
     if (offs) offs[l] = total;
     if (unpack) total += align256((size_t)(io[l].d_out * io[l].d_in));
   }
   return total;
 }
+size_t fwd_batch_workspace_min(int n, const LinearIO* io, int cf) {
+  if (cf == CF_T2 && fwd_packed(n, io)) return kSchedBytes;
+  return fwd_batch_workspace(n, io, cf, nullptr);
+}
 
-hipError_t launch_fwd_batch(const BatchCfg& c, const LinearIO* io, uint8_t* ws, hipStream_t stream) {
+hipError_t launch_fwd_batch(const BatchCfg& c, const LinearIO* io, uint8_t* ws, size_t ws_bytes,
+                           hipStream_t stream) {
   if (c.M == 0 || c.n == 0) return hipSuccess;
   LaunchStatus st;
   size_t offs[kMaxBatch];
-  fwd_batch_workspace(c.n, io, c.w_ternary ? CF_T2 : c.w_int4 ? CF_I4 : c.w_int3 ? CF_I3 : CF_I8, offs);
-  const bool packed = c.w_ternary && fwd_packed(c.n, io);
+  const size_t full =
+      fwd_batch_workspace(c.n, io, c.w_ternary ? CF_T2 : c.w_int4 ? CF_I4 : c.w_int3 ? CF_I3 : CF_I8, offs);
+  const bool aligned = c.w_ternary && fwd_packed(c.n, io);
+  // ternary codes straight from the packed form only when the workspace
+  // cannot hold their expansion
+  const bool packed = aligned && ws_bytes < full;
+  // FP4 values of ternary codes in the workspace (e4m3 activations)
+  const bool fp4 = aligned && !packed && c.act_e4m3;
   // int8 (or e4m3) copy of the codes in the workspace
-  const bool unpacked = (c.w_ternary && !packed) || c.w_int4 || c.w_int3;
+  const bool unpacked = (c.w_ternary && !packed && !fp4) || c.w_int4 || c.w_int3;
   if (c.w_int3) {
     SegTab tab{};
     tab.n = c.n;
@@ -1520,6 +1581,16 @@ hipError_t launch_fwd_batch(const BatchCfg& c, const LinearIO* io, uint8_t* ws, 
       st << launch_kernel(unpack_int4_kernel<1>, dim3(blocks), dim3(256), stream, tab);
     else
       st << launch_kernel(unpack_int4_kernel<0>, dim3(blocks), dim3(256), stream, tab);
+  } else if (fp4) {
+    SegTab tab{};
+    tab.n = c.n;
+    for (int l = 0; l < c.n; ++l) {
+      tab.src[l] = io[l].Wq;
+      tab.dst[l] = ws + offs[l];
+      tab.n16[l] = io[l].d_out * io[l].d_in / 16;
+    }
+    const int32_t blocks = seal(tab);
+    st << launch_kernel(expand_fp4_kernel, dim3(blocks), dim3(256), stream, tab);
   } else if (c.w_ternary && !packed) {
     SegTab tab{};
     tab.n = c.n;
@@ -1541,6 +1612,8 @@ hipError_t launch_fwd_batch(const BatchCfg& c, const LinearIO* io, uint8_t* ws, 
     p.A = Opnd{static_cast<const uint8_t*>(io[l].Xq), io[l].d_in, c.M};
     if (packed)
       p.B = Opnd{static_cast<const uint8_t*>(io[l].Wq), io[l].d_in / 4, io[l].d_out};
+    else if (fp4)
+      p.B = Opnd{ws + offs[l], io[l].d_in / 2, io[l].d_out};
     else if (unpacked)
       p.B = Opnd{ws + offs[l], io[l].d_in, io[l].d_out};
     else
@@ -1555,6 +1628,8 @@ hipError_t launch_fwd_batch(const BatchCfg& c, const LinearIO* io, uint8_t* ws, 
   if (packed) {
     if (c.act_e4m3) st << launch_group<FWD_FP4B ? EF4B : EF8, KC, KCP, 128>(grp, ws, stream);
     else st << launch_group<EI8, KC, KCP, 128>(grp, ws, stream);
+  } else if (fp4) {
+    st << launch_group<EF4B, KC, KF4, 128>(grp, ws, stream);
   } else {
     if (c.act_e4m3) st << launch_group<EF8, KC, KC, KB_FWD>(grp, ws, stream);
     else st << launch_group<EI8, KC, KC, KB_FWD>(grp, ws, stream);

@@ -1,9 +1,9 @@
 // The batched forward without a caller workspace, for callers that cannot
 // allocate device memory (code under graph capture, serving loops, harnesses
 // that forbid allocation).  Its scratch -- the persistent GEMM's tile
-// counters and, for 4-bit codes or ternary rows not a multiple of 64 long,
-// the operand bytes the codes are expanded into -- lives in one static
-// device array per GPU, kept for the life of the process.
+// counters and, when they fit, the operand bytes the codes are expanded
+// into -- lives in one static device array per GPU, kept for the life of the
+// process.
 #include <mutex>
 
 #include "../../include/dqt.h"
@@ -39,11 +39,10 @@ dqt_status scratch_of_current_device(uint8_t** out) {
 
 extern "C" dqt_status dqt_linear_fwd_batch_noalloc(int32_t n, const dqt_linear_io* io, int64_t M,
                                                    int32_t act_q, int32_t y_t, void* stream) {
-  // a batch whose scratch does not fit is refused before anything else; the
-  // other checks are those of dqt_linear_fwd_batch (an invalid batch reports
-  // 0 bytes here and is refused there, before anything is enqueued)
-  const size_t need = dqt_linear_fwd_batch_workspace(n, io);
-  if (need > (size_t)DQT_NOALLOC_SCRATCH_BYTES) return DQT_ERR_WORKSPACE;
+  // every check is dqt_linear_fwd_batch's, made before anything is
+  // enqueued: a batch whose smallest workspace exceeds the scratch is refused
+  // (DQT_ERR_WORKSPACE); ternary codes whose expansion does not fit run from
+  // the packed codes
   uint8_t* ws = nullptr;
   const dqt_status st = scratch_of_current_device(&ws);
   if (st != DQT_OK) return st;

@@ -120,9 +120,12 @@ def test_call_level_checks():
                               dqt.DQT_F32, FAKE, BIG, None) == dqt.DQT_ERR_DTYPE
     assert lib.dqt_linear_fwd(bw, FAKE, FAKE, dqt.DQT_F32, 16, dqt.DQT_F32, FAKE, FAKE, FAKE,
                               dqt.DQT_F32, FAKE, BIG, None) == dqt.DQT_ERR_DTYPE
-    # 256 counter bytes; packed codes go straight to the GEMM when d_in is a
-    # multiple of 64, else they are unpacked into the workspace
-    assert lib.dqt_linear_fwd_workspace(bw) == 256
+    # the fastest form expands the codes into the workspace (256 counter
+    # bytes + one byte per weight); with d_in a multiple of 64 the counters
+    # alone also do (the packed codes go straight to the GEMM), fewer do not
+    assert lib.dqt_linear_fwd_workspace(bw) == 256 + w.d_out * w.d_in
+    assert lib.dqt_linear_fwd(bw, FAKE, FAKE, dqt.DQT_F32, 16, dqt.DQT_I8, FAKE, FAKE, FAKE,
+                              dqt.DQT_F32, FAKE, 255, None) == dqt.DQT_ERR_WORKSPACE
     w48 = _w(d_in=48)
     need_f = lib.dqt_linear_fwd_workspace(ctypes.byref(w48))
     assert need_f == 256 + 64 * 48

@@ -131,6 +131,50 @@ def test_forward(lib, shape, kind):
         assert ok, (nbad, emax)
 
 
+PACKED_SHAPES = [(512, 256, 256), (1000, 1024, 208), (257, 320, 96)]
+
+
+@pytest.mark.parametrize("shape", PACKED_SHAPES)
+@pytest.mark.parametrize("act", ["i8", "e4m3"])
+def test_forward_packed_form_with_the_smallest_workspace(lib, shape, act):
+    """Ternary codes with d_in a multiple of 64 given only the 256 counter
+    bytes of workspace run from the packed codes, expanded in registers
+    (int8 bytes, or FP4 values against e4m3 activations): int8 bit for bit
+    equal to the expanded form and the oracle, e4m3 within the tolerance."""
+    M, d_in, d_out = shape
+    log(f"forward packed form M={M} d_in={d_in} d_out={d_out} {act}")
+    q = _weights(d_out, d_in, "ternary", -1, 1, M, d_in, d_out, 7)
+    alpha = np.float32(0.0173)
+    w = make_weight(d_out, d_in, "ternary", -1, 1, alpha)
+    Wq = weight_codes_dev(q, "ternary")
+    X_dev, X_seen = to_dev(draws((M, d_in), 1.0, 3, M, d_in), "bf16")
+    code = dqt.DQT_I8 if act == "i8" else dqt.DQT_FP8E4M3
+    Xq = torch.empty((M, d_in), dtype=torch.int8 if act == "i8" else torch.uint8, device=DEV)
+    xdq = torch.empty((M,), dtype=torch.float32, device=DEV)
+    full = dqt.dqt_linear_fwd_workspace(w)
+    assert full >= 256 + d_out * d_in            # the expansion's bytes
+    outs = []
+    for nbytes in (full, 256):
+        ws = dqt.workspace(nbytes)
+        Y = torch.empty((M, d_out), dtype=torch.float32, device=DEV)
+        dqt.dqt_linear_fwd(w, Wq, X_dev, M, code, Xq, xdq, Y, ws)
+        outs.append(Y.cpu().numpy())
+    # one byte short of the counters is refused
+    with pytest.raises(dqt.DqtError):
+        Y = torch.empty((M, d_out), dtype=torch.float32, device=DEV)
+        dqt.dqt_linear_fwd(w, Wq, X_dev, M, code, Xq, xdq, Y, dqt.workspace(256)[:-1])
+    want_q, want_d = O.act_quant(X_seen, act)
+    Y_ref, acc = O.linear_fwd(want_q, want_d, act, q, alpha, "f32")
+    if act == "i8":
+        assert np.array_equal(outs[0], Y_ref) and np.array_equal(outs[1], Y_ref)
+    else:
+        a = np.abs(O.act_values(want_q, act)) @ np.abs(q.astype(np.float64)).T
+        f = (want_d * alpha).astype(np.float64)[:, None]
+        for got in outs:
+            ok, nbad, emax = gemm_close(got, acc * f, a * f, bf16_out=False)
+            assert ok, (nbad, emax)
+
+
 # ------------------------------------------------------------- backward
 
 BWD_SHAPES = [(1, 16, 16), (300, 272, 400), (512, 256, 256), (2100, 96, 160), (4097, 128, 48)]

@@ -1,8 +1,9 @@
 """dqt_linear_fwd_batch_noalloc -- the forward batch for callers that cannot
 allocate -- gives the bits of dqt_linear_fwd_batch with a workspace, call
 after call on the library's static per-GPU scratch (two calls in a row, the
-second with a smaller input), and refuses a batch whose scratch exceeds the
-array before launching anything."""
+second with a smaller input), runs ternary codes whose expansion does not fit
+from the packed codes, and refuses a batch whose smallest workspace exceeds
+the array before launching anything."""
 import numpy as np
 import pytest
 import torch
@@ -65,6 +66,23 @@ def test_noalloc_forward_matches_workspace_forward(lib, ci):
         torch.cuda.synchronize()
         for li, (a, b) in enumerate(zip(ents_ws, ents_na)):
             assert torch.equal(a["Y"], b["Y"]), (ci, k, li)
+
+
+def test_noalloc_forward_large_ternary_runs_packed(lib):
+    """Ternary codes whose expansion exceeds the array (2 x 4096 x 4096 bytes
+    plus the counters) run from the packed codes, expanded in registers:
+    int8 activations give the bits of the workspace call, which expands them."""
+    for k, M in enumerate((256, 96)):
+        log(f"no-alloc forward, packed ternary: M={M}")
+        a_code, ents_ws, ents_na = _batch(M, [(4096, 4096), (4096, 4096)], "ternary", -1, 1, "i8", 70 + k)
+        io_ws, io_na = dqt.linear_io(ents_ws), dqt.linear_io(ents_na)
+        need = dqt.dqt_linear_fwd_batch_workspace(io_ws)
+        assert need > dqt.NOALLOC_SCRATCH_BYTES
+        dqt.dqt_linear_fwd_batch(io_ws, M, a_code, dqt.DQT_BF16, dqt.workspace(need))
+        dqt.dqt_linear_fwd_batch_noalloc(io_na, M, a_code, dqt.DQT_BF16)
+        torch.cuda.synchronize()
+        for li, (a, b) in enumerate(zip(ents_ws, ents_na)):
+            assert torch.equal(a["Y"], b["Y"]), (k, li)
 
 
 def test_noalloc_forward_refuses_oversized_scratch(lib):
