@@ -269,13 +269,14 @@ def kernel_source_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def read_traffic(kernel_class: str, workload: str):
+def read_traffic(kernel_class: str, workload: str, kernel_only: bool = False):
     """Bytes per launch that the L2 caches fetched from and wrote to memory
     (FETCH_SIZE + WRITE_SIZE, scaled by a plain copy of known size), from the
     committed rocprofv3 counter summary, if it was taken on the current
-    kernel sources; else None.  The counters see the last-level cache (MALL)
-    and HBM alike, so on a block whose data fits the 256 MB MALL this is an
-    upper bound of the HBM bytes."""
+    kernel sources; else None.  kernel_only: the GEMM kernel's own bytes,
+    without the passes of its call.  The counters see the last-level cache
+    (MALL) and HBM alike, so on a block whose data fits the 256 MB MALL this
+    is an upper bound of the HBM bytes."""
     path = os.path.join(ROOT, "profiles", f"{kernel_class}_{workload}_counters.txt")
     if not os.path.exists(path):
         return None
@@ -287,7 +288,7 @@ def read_traffic(kernel_class: str, workload: str):
     if vals.get("kernel_source_hash") != kernel_source_hash():
         return None
     try:
-        return float(vals["fetch_write_bytes_per_launch"])
+        return float(vals["gemm_kernel_fetch_write_bytes" if kernel_only else "fetch_write_bytes_per_launch"])
     except (KeyError, ValueError):
         return None
 
@@ -556,11 +557,33 @@ def main():
             entry.update({"gbs": round(gbs, 1), "frac_hbm": round(gbs / PEAK_HBM_GBS, 4)})
         breakdown[kind] = entry
 
-    # the dominant call of the step: its share of the step is the largest;
-    # each such call is one GEMM launch (plus the tile-counter clear)
+    # the dominant call of the step: its share of the step is the largest.
+    # A GEMM call is its GEMM kernel launch plus passes around it (operand
+    # expansion or transposition, the tile-counter clear); the roofline is the
+    # GEMM kernel's own: the library's launch timer brackets each GEMM kernel
+    # launch with HIP events on the call's stream, here over `steps` calls of
+    # the dominant kind issued back to back.
     dom = max(step_kinds, key=lambda k: per_kind[k]["median"])
-    dom_avg_ms = per_kind[dom]["mean"]
+    dom_call_ms = per_kind[dom]["mean"]
     dom_units = units[dom]
+    kernel_ms, launches = None, 0
+    if dom in gemm_dtype:
+        def only_dom(k, fn):
+            if k == dom:
+                fn()
+        cap = 8 * args.steps
+        torch.cuda.synchronize()
+        dqt.dqt_launch_timer_start(cap)
+        try:
+            for r in range(args.steps):
+                run_step(blk, dqt, 3000 + r, None, only_dom, split_bwd=dom in ("bwd_dx", "bwd_dw"),
+                         sr="fused" if dom == "bwd_sr" else "separate")
+            torch.cuda.synchronize()
+        finally:
+            launch_ms, launches = dqt.dqt_launch_timer_stop(cap)
+        if launches > 0 and launches % args.steps == 0:
+            kernel_ms = sum(launch_ms) / args.steps
+    dom_avg_ms = kernel_ms if kernel_ms is not None else dom_call_ms
     if dom in gemm_dtype:
         achieved = dom_units / (dom_avg_ms * 1e-3) / 1e12
         peak = PEAK_TFLOPS[gemm_dtype[dom]]
@@ -569,10 +592,14 @@ def main():
         achieved = dom_units / (dom_avg_ms * 1e-3) / 1e9
         peak = PEAK_HBM_GBS
         roof = {"bound": "hbm", "unit": "GB/s"}
-    traffic = read_traffic(dom, wl.name)
+    traffic = read_traffic(dom, wl.name, kernel_only=kernel_ms is not None)
     roof.update({"achieved": round(achieved, 2), "peak": peak,
                  "frac": round(achieved / peak, 4), "traffic": traffic, "kernel": dom,
-                 "avg_launch_ms": round(dom_avg_ms, 5), "units_per_launch": dom_units})
+                 "avg_launch_ms": round(dom_avg_ms, 5), "units_per_launch": dom_units,
+                 "timing": ("GEMM kernel launches (library launch timer)" if kernel_ms is not None
+                            else "whole call"),
+                 "gemm_launches_per_call": launches // args.steps if kernel_ms is not None else None,
+                 "call_ms": round(dom_call_ms, 5)})
 
     sr = breakdown.get("sr")
     mfma_frac = sum(units[k] / (PEAK_TFLOPS[gemm_dtype[k]] * 1e12)

@@ -556,6 +556,30 @@ dqt_status dqt_unpack_int4(const uint8_t* packed, int64_t rows, int64_t cols, in
 dqt_status dqt_pack_int3(const int8_t* q, int64_t rows, int64_t cols, uint8_t* packed);
 dqt_status dqt_unpack_int3(const uint8_t* packed, int64_t rows, int64_t cols, int8_t* q);
 
+/* ------------------------------------------------------------ measurement
+ * Launch timer: the durations of the library's GEMM kernel launches (the
+ * forward, dX and dW products, alone or in one launch), without the passes
+ * around them, for a caller that measures a kernel against its roofline.
+ * Not for graph capture: the events are recorded when a launch is issued.
+ *
+ *   dqt_launch_timer_start(max_launches): creates 2 * max_launches events
+ *          (1 <= max_launches <= DQT_LAUNCH_TIMER_MAX; else DQT_ERR_SHAPE) on
+ *          the current device; from then on every GEMM kernel launch, in
+ *          issue order, is bracketed by the next pair, recorded on the call's
+ *          stream, until max_launches are taken (later launches run
+ *          untimed).  One timer per process: DQT_ERR_UNSUPPORTED while one
+ *          runs.  Timed launches must run on the device current at start.
+ *   dqt_launch_timer_stop(ms, max, count): waits for the recorded pairs,
+ *          writes the first min(max, *count) durations (milliseconds, host
+ *          float[max]) to ms, the number of timed launches to *count, and
+ *          frees the events.  DQT_ERR_UNSUPPORTED when no timer runs;
+ *          DQT_ERR_NULL / DQT_ERR_SHAPE for bad arguments (the timer keeps
+ *          running); DQT_ERR_HIP if an event fails (the events are freed).
+ */
+#define DQT_LAUNCH_TIMER_MAX 65536
+dqt_status dqt_launch_timer_start(int32_t max_launches);
+dqt_status dqt_launch_timer_stop(float* ms, int32_t max, int32_t* count);
+
 /* Human-readable name of a status code (static storage). */
 const char* dqt_status_string(int32_t status);
 

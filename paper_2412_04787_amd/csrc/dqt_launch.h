@@ -46,6 +46,22 @@ struct LaunchStatus {
   }
 };
 
+// Launch timer (measurement only): while one runs, every GEMM kernel launch
+// is bracketed by a pair of events recorded on its stream, one pair per
+// launch up to the timer's capacity; launches beyond it are not timed.
+// begin gives the pair's slot, or -1 when no timer runs or it is full.
+hipError_t launch_timer_begin(hipStream_t s, int* slot);
+hipError_t launch_timer_end(int slot, hipStream_t s);
+template <class F>
+hipError_t timed_launch(hipStream_t s, F&& launch) {
+  int slot = -1;
+  hipError_t e = launch_timer_begin(s, &slot);
+  if (e != hipSuccess) return e;
+  e = launch();
+  const hipError_t e2 = launch_timer_end(slot, s);
+  return e != hipSuccess ? e : e2;
+}
+
 // Compute units of the current device, queried on every call (nothing is
 // cached across calls or devices).
 inline int current_device_cus() {

@@ -238,12 +238,16 @@ hipError_t launch_dx_f32(const DxArgs& a, hipStream_t stream) {
   ContigSrc ya{static_cast<const uint8_t*>(a.dY), R * 4, I, R * 4};
   if (a.w_ternary) {
     QTernarySrc qb{static_cast<const uint8_t*>(a.Wq), J / 4, R, J};
-    return launch_kernel(gemm_f32_kernel<ContigStager, TransF32Stager<QTernarySrc>, ContigSrc, QTernarySrc, EpiScale>,
-                         grid, block, stream, ya, qb, epi, I, J, R, R);
+    return timed_launch(stream, [&] {
+      return launch_kernel(gemm_f32_kernel<ContigStager, TransF32Stager<QTernarySrc>, ContigSrc, QTernarySrc, EpiScale>,
+                           grid, block, stream, ya, qb, epi, I, J, R, R);
+    });
   } else {
     QInt8Src qb{static_cast<const int8_t*>(a.Wq), J, R, J};
-    return launch_kernel(gemm_f32_kernel<ContigStager, TransF32Stager<QInt8Src>, ContigSrc, QInt8Src, EpiScale>,
-                         grid, block, stream, ya, qb, epi, I, J, R, R);
+    return timed_launch(stream, [&] {
+      return launch_kernel(gemm_f32_kernel<ContigStager, TransF32Stager<QInt8Src>, ContigSrc, QInt8Src, EpiScale>,
+                           grid, block, stream, ya, qb, epi, I, J, R, R);
+    });
   }
 }
 
@@ -269,12 +273,16 @@ hipError_t launch_dw_f32(const DwArgs& a, hipStream_t stream) {
   hipError_t e;
   if (a.act_e4m3) {
     XtSrc<true> xb{static_cast<const uint8_t*>(a.Xq), a.xdq, J, R, J};
-    e = launch_kernel(gemm_f32_kernel<TransF32Stager<DyF32Src>, TransF32Stager<XtSrc<true>>, DyF32Src, XtSrc<true>, EpiPartial>,
-                      grid, block, stream, ya, xb, epi, I, J, R, len);
+    e = timed_launch(stream, [&] {
+      return launch_kernel(gemm_f32_kernel<TransF32Stager<DyF32Src>, TransF32Stager<XtSrc<true>>, DyF32Src, XtSrc<true>, EpiPartial>,
+                           grid, block, stream, ya, xb, epi, I, J, R, len);
+    });
   } else {
     XtSrc<false> xb{static_cast<const uint8_t*>(a.Xq), a.xdq, J, R, J};
-    e = launch_kernel(gemm_f32_kernel<TransF32Stager<DyF32Src>, TransF32Stager<XtSrc<false>>, DyF32Src, XtSrc<false>, EpiPartial>,
-                      grid, block, stream, ya, xb, epi, I, J, R, len);
+    e = timed_launch(stream, [&] {
+      return launch_kernel(gemm_f32_kernel<TransF32Stager<DyF32Src>, TransF32Stager<XtSrc<false>>, DyF32Src, XtSrc<false>, EpiPartial>,
+                           grid, block, stream, ya, xb, epi, I, J, R, len);
+    });
   }
   if (e != hipSuccess || splits == 1) return e;
   return launch_split_reduce(a.ws, (int)splits, I * J, a.dW, stream);

@@ -1445,7 +1445,9 @@ static hipError_t launch_group(Group<Epi>& grp, uint8_t* ws, hipStream_t s) {
   const int32_t bpx = std::min(per_xcd, std::max(1, current_device_cus() / 8));
   LaunchStatus st;
   st << launch_kernel(sched_clear_kernel, dim3(1), dim3(64), s, reinterpret_cast<int*>(ws));
-  st << launch_kernel(gemm_v3_kernel<ELEM, MA, MB, KB, Epi>, dim3((unsigned)(8 * bpx)), dim3(NTH), s, grp);
+  st << timed_launch(s, [&] {
+    return launch_kernel(gemm_v3_kernel<ELEM, MA, MB, KB, Epi>, dim3((unsigned)(8 * bpx)), dim3(NTH), s, grp);
+  });
   return st.e;
 }
 
@@ -1459,8 +1461,10 @@ static hipError_t launch_dual(Group<Epi1>& g1, Group<Epi2>& g2, uint8_t* ws, hip
   const int32_t bpx = std::min(per_xcd, std::max(1, current_device_cus() / 8));
   LaunchStatus st;
   st << launch_kernel(sched_clear_kernel, dim3(1), dim3(64), s, reinterpret_cast<int*>(ws));
-  st << launch_kernel(gemm_v3_dual_kernel<E1, MA1, MB1, KB1, Epi1, E2, MA2, MB2, KB2, Epi2>,
-                      dim3((unsigned)(8 * bpx)), dim3(NTH), s, g1, g2);
+  st << timed_launch(s, [&] {
+    return launch_kernel(gemm_v3_dual_kernel<E1, MA1, MB1, KB1, Epi1, E2, MA2, MB2, KB2, Epi2>,
+                         dim3((unsigned)(8 * bpx)), dim3(NTH), s, g1, g2);
+  });
   return st.e;
 }
 

@@ -30,7 +30,8 @@ EXPORTS = (
     "dqt_sr_update_batch", "dqt_adamw_sr_update", "dqt_adamw_sr_update_batch",
     "dqt_update_variant_workspace", "dqt_update_variant_batch",
     "dqt_sr_update", "dqt_debug_rng", "dqt_absmean_init", "dqt_pack_ternary",
-    "dqt_unpack_ternary", "dqt_pack_int4", "dqt_unpack_int4", "dqt_pack_int3", "dqt_unpack_int3", "dqt_status_string", "dqt_version",
+    "dqt_unpack_ternary", "dqt_pack_int4", "dqt_unpack_int4", "dqt_pack_int3", "dqt_unpack_int3", "dqt_launch_timer_start", "dqt_launch_timer_stop",
+    "dqt_status_string", "dqt_version",
 )
 
 
@@ -114,6 +115,8 @@ _SIGS = {
     "dqt_unpack_int4": (_i32, [_vp, _i64, _i64, _vp]),
     "dqt_pack_int3": (_i32, [_vp, _i64, _i64, _vp]),
     "dqt_unpack_int3": (_i32, [_vp, _i64, _i64, _vp]),
+    "dqt_launch_timer_start": (_i32, [_i32]),
+    "dqt_launch_timer_stop": (_i32, [_vp, _i32, _vp]),
     "dqt_status_string": (ctypes.c_char_p, [_i32]),
     "dqt_version": (_i32, []),
 }
@@ -245,6 +248,19 @@ def dqt_sr_update(w: DqtWeight, Wq, dW, lr: float, seed: int, step: int, counter
 def dqt_debug_rng(seed: int, step: int, tensor_id: int, i0: int, out, stream=None):
     _check("dqt_debug_rng", load().dqt_debug_rng(seed, step, tensor_id, i0, out.numel(),
                                                  _ptr(out), _stream(stream)))
+
+
+def dqt_launch_timer_start(max_launches: int):
+    _check("dqt_launch_timer_start", load().dqt_launch_timer_start(max_launches))
+
+
+def dqt_launch_timer_stop(max_launches: int):
+    """Durations (ms) of the GEMM kernel launches timed since the start, in
+    issue order, and how many launches were timed."""
+    ms = (ctypes.c_float * max(1, max_launches))()
+    count = ctypes.c_int32(0)
+    _check("dqt_launch_timer_stop", load().dqt_launch_timer_stop(ms, max_launches, ctypes.byref(count)))
+    return [float(ms[k]) for k in range(min(count.value, max_launches))], count.value
 
 
 # ----------------------------------------------------------------- batches

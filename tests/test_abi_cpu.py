@@ -355,3 +355,15 @@ def test_int3_pack_matches_oracle_and_checks():
         bad = _w(wfmt=dqt.DQT_INT3, qmin=qmin, qmax=qmax)
         assert lib.dqt_sr_update(ctypes.byref(bad), FAKE, FAKE, 1e-3, 0, 1, None, None) == \
             dqt.DQT_ERR_RANGE
+
+
+def test_launch_timer_argument_checks():
+    """The launch timer refuses bad capacities and a stop without a start
+    (neither touches a device)."""
+    lib = dqt.load()
+    assert lib.dqt_launch_timer_start(0) == 2                 # DQT_ERR_SHAPE
+    assert lib.dqt_launch_timer_start(65537) == 2
+    count = ctypes.c_int32(-1)
+    ms = (ctypes.c_float * 4)()
+    assert lib.dqt_launch_timer_stop(ms, 4, ctypes.byref(count)) == 7   # DQT_ERR_UNSUPPORTED
+    assert count.value == -1
