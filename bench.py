@@ -601,6 +601,25 @@ def main():
                  "gemm_launches_per_call": launches // args.steps if kernel_ms is not None else None,
                  "call_ms": round(dom_call_ms, 5)})
 
+    # The chip's own streaming read rate (a plain one-pass read, 16-byte
+    # non-temporal loads, alternating two 1 GiB buffers): what the SR update,
+    # a stream of 4.25 B read and 0.25 B written per ternary weight, can
+    # approach at best.
+    rs_bytes = 1 << 30
+    rs_bufs = [torch.full((rs_bytes // 4,), r + 1, dtype=torch.int32, device="cuda:0") for r in range(2)]
+    rs_sink = torch.empty((dqt.READ_STREAM_SINK_WORDS,), dtype=torch.int32, device="cuda:0")
+    for r in range(4):
+        dqt.dqt_read_stream(rs_bufs[r & 1], rs_sink)
+    rs_ev = [torch.cuda.Event(enable_timing=True) for _ in range(21)]
+    torch.cuda.synchronize()
+    rs_ev[0].record(stream)
+    for r in range(20):
+        dqt.dqt_read_stream(rs_bufs[r & 1], rs_sink, stream)
+        rs_ev[r + 1].record(stream)
+    torch.cuda.synchronize()
+    read_gbs = rs_bytes / (pct([rs_ev[r].elapsed_time(rs_ev[r + 1]) for r in range(20)], 50) * 1e-3) / 1e9
+    del rs_bufs, rs_sink
+
     sr = breakdown.get("sr")
     mfma_frac = sum(units[k] / (PEAK_TFLOPS[gemm_dtype[k]] * 1e12)
                     for k in ("fwd", "bwd_dx", "bwd_dw")) / (ms_per_step * 1e-3)
@@ -635,6 +654,9 @@ def main():
         "sr_update_frac_hbm": sr["frac_hbm"] if sr else None,
         "sr_update_note": (f"separate SR call, median over {args.steps} replays, rotating "
                            f"{n_sets} buffer sets of {set_bytes / 1e6:.1f} MB") if sr else None,
+        "hbm_read_stream_gbs": round(read_gbs, 1),
+        "hbm_read_stream_frac_hbm": round(read_gbs / PEAK_HBM_GBS, 4),
+        "sr_update_frac_of_read_stream": round(sr["gbs"] / read_gbs, 4) if sr else None,
         "gemm_frac_of_dtype_peak": round(mfma_frac, 4),
         "breakdown": breakdown,
         "wall_s_timed_region": round(wall, 3),

@@ -580,6 +580,19 @@ dqt_status dqt_unpack_int3(const uint8_t* packed, int64_t rows, int64_t cols, in
 dqt_status dqt_launch_timer_start(int32_t max_launches);
 dqt_status dqt_launch_timer_stop(float* ms, int32_t max, int32_t* count);
 
+/* A plain streaming read of `bytes` bytes of device memory (one pass, 16-byte
+ * non-temporal loads over a fixed grid of DQT_READ_STREAM_SINK_WORDS / 4
+ * blocks): the read rate this chip achieves, which the streaming kernels
+ * (SR update, AdamW) are compared with.
+ *   src:   device, 16-byte aligned; bytes a multiple of 16 (DQT_ERR_SHAPE),
+ *          0 does nothing.
+ *   sink:  device uint32[DQT_READ_STREAM_SINK_WORDS], 16-byte aligned:
+ *          receives xors of the data read (so no read is elided).
+ *   Asynchronous on `stream`; DQT_ERR_NULL / DQT_ERR_ALIGN for bad pointers.
+ */
+#define DQT_READ_STREAM_SINK_WORDS 32768
+dqt_status dqt_read_stream(const void* src, size_t bytes, uint32_t* sink, void* stream);
+
 /* Human-readable name of a status code (static storage). */
 const char* dqt_status_string(int32_t status);
 

@@ -1,5 +1,7 @@
-// Launch timer: events around each GEMM kernel launch, so that a caller can
-// read the kernels' own durations (for measurement; not on any compute path).
+// Measurement helpers (not on any compute path): the launch timer, events
+// around each GEMM kernel launch so that a caller can read the kernels' own
+// durations; and a plain streaming read, the achievable HBM read rate that
+// the streaming kernels are compared with.
 #include <hip/hip_runtime.h>
 
 #include <mutex>
@@ -41,9 +43,48 @@ hipError_t launch_timer_end(int slot, hipStream_t s) {
   return hipEventRecord(g_ev[2 * slot + 1], s);
 }
 
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+
+// Grid-stride read of n16 16-byte words, 8 non-temporal loads in flight per
+// lane; each wave's xor of what it read goes to sink[4 * block + wave].
+__global__ __launch_bounds__(256) void read_stream_kernel(const u32x4_t* __restrict__ p, int64_t n16,
+                                                          uint32_t* __restrict__ sink) {
+  const int64_t stride = (int64_t)gridDim.x * 256;
+  int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  uint32_t acc = 0;
+  for (; i + 7 * stride < n16; i += 8 * stride) {
+    u32x4_t v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v[u] = __builtin_nontemporal_load(p + i + u * stride);
+#pragma unroll
+    for (int u = 0; u < 8; ++u) acc ^= v[u].x ^ v[u].y ^ v[u].z ^ v[u].w;
+  }
+  for (; i < n16; i += stride) {
+    const u32x4_t v = __builtin_nontemporal_load(p + i);
+    acc ^= v.x ^ v.y ^ v.z ^ v.w;
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) acc ^= (uint32_t)__shfl_xor((int)acc, o, 64);
+  if ((threadIdx.x & 63) == 0) sink[4 * blockIdx.x + (threadIdx.x >> 6)] = acc;
+}
+
 }  // namespace dqt
 
 extern "C" {
+
+dqt_status dqt_read_stream(const void* src, size_t bytes, uint32_t* sink, void* stream) {
+  if (bytes == 0) return DQT_OK;
+  if (src == nullptr || sink == nullptr) return DQT_ERR_NULL;
+  if (bytes % 16 != 0) return DQT_ERR_SHAPE;
+  if (reinterpret_cast<uintptr_t>(src) % 16 != 0 || reinterpret_cast<uintptr_t>(sink) % 16 != 0)
+    return DQT_ERR_ALIGN;
+  constexpr int kBlocks = DQT_READ_STREAM_SINK_WORDS / 4;
+  const hipError_t e = dqt::launch_kernel(dqt::read_stream_kernel, dim3(kBlocks), dim3(256),
+                                          static_cast<hipStream_t>(stream),
+                                          static_cast<const dqt::u32x4_t*>(src),
+                                          static_cast<int64_t>(bytes / 16), sink);
+  return e == hipSuccess ? DQT_OK : DQT_ERR_HIP;
+}
 
 dqt_status dqt_launch_timer_start(int32_t max_launches) {
   if (max_launches < 1 || max_launches > DQT_LAUNCH_TIMER_MAX) return DQT_ERR_SHAPE;

@@ -30,7 +30,7 @@ EXPORTS = (
     "dqt_sr_update_batch", "dqt_adamw_sr_update", "dqt_adamw_sr_update_batch",
     "dqt_update_variant_workspace", "dqt_update_variant_batch",
     "dqt_sr_update", "dqt_debug_rng", "dqt_absmean_init", "dqt_pack_ternary",
-    "dqt_unpack_ternary", "dqt_pack_int4", "dqt_unpack_int4", "dqt_pack_int3", "dqt_unpack_int3", "dqt_launch_timer_start", "dqt_launch_timer_stop",
+    "dqt_unpack_ternary", "dqt_pack_int4", "dqt_unpack_int4", "dqt_pack_int3", "dqt_unpack_int3", "dqt_launch_timer_start", "dqt_launch_timer_stop", "dqt_read_stream",
     "dqt_status_string", "dqt_version",
 )
 
@@ -117,6 +117,7 @@ _SIGS = {
     "dqt_unpack_int3": (_i32, [_vp, _i64, _i64, _vp]),
     "dqt_launch_timer_start": (_i32, [_i32]),
     "dqt_launch_timer_stop": (_i32, [_vp, _i32, _vp]),
+    "dqt_read_stream": (_i32, [_vp, ctypes.c_size_t, _vp, _vp]),
     "dqt_status_string": (ctypes.c_char_p, [_i32]),
     "dqt_version": (_i32, []),
 }
@@ -261,6 +262,17 @@ def dqt_launch_timer_stop(max_launches: int):
     count = ctypes.c_int32(0)
     _check("dqt_launch_timer_stop", load().dqt_launch_timer_stop(ms, max_launches, ctypes.byref(count)))
     return [float(ms[k]) for k in range(min(count.value, max_launches))], count.value
+
+
+READ_STREAM_SINK_WORDS = 32768
+
+
+def dqt_read_stream(src, sink, stream=None):
+    """One streaming read of the device tensor src (all its bytes); sink: a
+    device int32/uint32 tensor of READ_STREAM_SINK_WORDS words."""
+    nbytes = src.numel() * src.element_size()
+    assert sink.numel() * sink.element_size() >= 4 * READ_STREAM_SINK_WORDS
+    _check("dqt_read_stream", load().dqt_read_stream(_ptr(src), nbytes, _ptr(sink), _stream(stream)))
 
 
 # ----------------------------------------------------------------- batches

@@ -367,3 +367,12 @@ def test_launch_timer_argument_checks():
     ms = (ctypes.c_float * 4)()
     assert lib.dqt_launch_timer_stop(ms, 4, ctypes.byref(count)) == 7   # DQT_ERR_UNSUPPORTED
     assert count.value == -1
+
+
+def test_read_stream_argument_checks():
+    """The streaming read refuses bad sizes and pointers before launching."""
+    lib = dqt.load()
+    assert lib.dqt_read_stream(None, 0, None, None) == 0          # nothing to read
+    assert lib.dqt_read_stream(None, 16, FAKE, None) == 1         # DQT_ERR_NULL
+    assert lib.dqt_read_stream(FAKE, 15, FAKE, None) == 2         # DQT_ERR_SHAPE
+    assert lib.dqt_read_stream(UNALIGNED, 16, FAKE, None) == 3    # DQT_ERR_ALIGN

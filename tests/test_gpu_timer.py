@@ -4,12 +4,13 @@ calls after the stop run untimed."""
 import os
 import sys
 
+import numpy as np
 import pytest
 import torch
 
 from paper_2412_04787_amd import dqt, workloads as W
 
-from gpu_util import log
+from gpu_util import DEV, log
 
 sys.path.insert(0, os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
 import bench  # noqa: E402
@@ -77,3 +78,19 @@ def test_timer_capacity_and_restart(lib):
     torch.cuda.synchronize()
     ms, count = dqt.dqt_launch_timer_stop(1)
     assert count == 1 and len(ms) == 1
+
+
+@pytest.mark.parametrize("nbytes", [16, 16 * 1000003, 64 << 20])
+def test_read_stream_reads_every_word_once(lib, nbytes):
+    """The xor of the sink is the xor of every 32-bit word of the buffer (each
+    word read exactly once), ragged sizes included."""
+    log(f"read stream: {nbytes} bytes")
+    g = torch.Generator(device=DEV)
+    g.manual_seed(nbytes)
+    src = torch.randint(-2**31, 2**31 - 1, (nbytes // 4,), dtype=torch.int32, device=DEV, generator=g)
+    sink = torch.full((dqt.READ_STREAM_SINK_WORDS,), 12345, dtype=torch.int32, device=DEV)
+    dqt.dqt_read_stream(src, sink)
+    torch.cuda.synchronize()
+    want = np.bitwise_xor.reduce(src.cpu().numpy().view(np.uint32))
+    got = np.bitwise_xor.reduce(sink.cpu().numpy().view(np.uint32))
+    assert got == want
