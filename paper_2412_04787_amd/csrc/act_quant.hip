@@ -62,20 +62,11 @@ __device__ __forceinline__ void quantise_store(const float (&v)[E], float inv, u
   uint32_t out[E / 4];
 #pragma unroll
   for (int w = 0; w < E / 4; ++w) {
-    uint32_t word = 0;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const float s = v[4 * w + i] * inv;
-      uint32_t b;
-      if constexpr (E4M3) {
-        b = f32_to_e4m3(s);
-      } else {
-        const float r = fminf(fmaxf(rintf(s), -128.0f), 127.0f);
-        b = (uint32_t)(int)r & 0xFFu;
-      }
-      word |= b << (8 * i);
+    if constexpr (E4M3) {
+      out[w] = f32x4_to_e4m3x4(v[4 * w] * inv, v[4 * w + 1] * inv, v[4 * w + 2] * inv, v[4 * w + 3] * inv);
+    } else {
+      out[w] = f32x4_to_i8x4(v[4 * w] * inv, v[4 * w + 1] * inv, v[4 * w + 2] * inv, v[4 * w + 3] * inv);
     }
-    out[w] = word;
   }
   if constexpr (E == 8) {
     *reinterpret_cast<uint2*>(dst) = make_uint2(out[0], out[1]);

@@ -54,6 +54,27 @@ __device__ __forceinline__ uint32_t f32_to_e4m3(float v) {
   return code | sign;
 }
 
+// Four fp32 values -> four OCP e4m3 bytes (value i in byte i), each equal to
+// f32_to_e4m3 of the value: the hardware conversion (round to nearest even;
+// equal to f32_to_e4m3 for every fp32 of magnitude below 449, all bit
+// patterns compared on the GPU) after |v| is clamped to 448 with v's sign,
+// which gives f32_to_e4m3's saturation of large values and of NaN.
+__device__ __forceinline__ float e4m3_sat(float v) { return copysignf(fminf(fabsf(v), 448.0f), v); }
+__device__ __forceinline__ uint32_t f32x4_to_e4m3x4(float a, float b, float c, float d) {
+  int w = __builtin_amdgcn_cvt_pk_fp8_f32(e4m3_sat(a), e4m3_sat(b), 0, false);
+  w = __builtin_amdgcn_cvt_pk_fp8_f32(e4m3_sat(c), e4m3_sat(d), w, true);
+  return (uint32_t)w;
+}
+
+// Four fp32 values -> four int8 codes clip(round(v), -128, 127) (value i in
+// byte i; round to nearest even; NaN gives -128 like fmaxf): after the clip,
+// adding 1.5 * 2^23 rounds to an integer to nearest even and leaves it, in
+// two's complement, in the low byte of the sum's bits.
+__device__ __forceinline__ uint32_t f32x4_to_i8x4(float a, float b, float c, float d) {
+  auto q = [](float v) { return __float_as_uint(fminf(fmaxf(v, -128.0f), 127.0f) + 12582912.0f); };
+  return (q(a) & 0xFFu) | ((q(b) & 0xFFu) << 8) | ((q(c) & 0xFFu) << 16) | (q(d) << 24);
+}
+
 // E4M3 byte -> fp32 (exact).  NaN codes are not produced by this library.
 __device__ __forceinline__ float e4m3_to_f32(uint32_t c) {
   const uint32_t e = (c >> 3) & 0xFu, m = c & 7u;

@@ -98,17 +98,16 @@ __global__ __launch_bounds__(kRows * kWave) void rmsnorm_quant_kernel(const TX* 
     const float4 g0 = *reinterpret_cast<const float4*>(gamma + 8 * c);
     const float4 g1 = *reinterpret_cast<const float4*>(gamma + 8 * c + 4);
     const float g[8] = {g0.x, g0.y, g0.z, g0.w, g1.x, g1.y, g1.z, g1.w};
-    uint32_t w[2] = {0u, 0u};
+    float q[8];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const float q = ((v[j] * r) * g[j]) * inv;
-      uint32_t b;
-      if constexpr (E4M3) {
-        b = f32_to_e4m3(q);
-      } else {
-        b = (uint32_t)(int)fminf(fmaxf(rintf(q), -128.0f), 127.0f) & 0xFFu;
-      }
-      w[j >> 2] |= b << (8 * (j & 3));
+    for (int j = 0; j < 8; ++j) q[j] = ((v[j] * r) * g[j]) * inv;
+    uint32_t w[2];
+    if constexpr (E4M3) {
+      w[0] = f32x4_to_e4m3x4(q[0], q[1], q[2], q[3]);
+      w[1] = f32x4_to_e4m3x4(q[4], q[5], q[6], q[7]);
+    } else {
+      w[0] = f32x4_to_i8x4(q[0], q[1], q[2], q[3]);
+      w[1] = f32x4_to_i8x4(q[4], q[5], q[6], q[7]);
     }
     *reinterpret_cast<uint2*>(qr + 8 * c) = make_uint2(w[0], w[1]);
   }
