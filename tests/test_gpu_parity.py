@@ -56,6 +56,46 @@ def test_act_quant_bit_exact(lib, M, K, x_t, act):
     assert np.array_equal(Xq.cpu().numpy(), want_q.view(np.uint8))
 
 
+def _rounding_cases(act):
+    """fp32 values at unit scale: every code's value, the midpoints between
+    neighbouring codes (the ties), one ulp either side of each, tiny and
+    subnormal values, both signs."""
+    if act == "e4m3":
+        grid = np.array(sorted({float(O.act_values(np.array([c], dtype=np.uint8), "e4m3")[0])
+                                for c in range(0x7F)}), dtype=np.float64)
+    else:
+        grid = np.arange(-128.0, 128.0)
+    grid = np.abs(grid) if act == "e4m3" else grid
+    mids = (grid[:-1] + grid[1:]) / 2
+    v = np.concatenate([grid, mids]).astype(np.float32)
+    v = np.concatenate([v, np.nextafter(v, np.float32(np.inf)), np.nextafter(v, np.float32(-np.inf)),
+                        np.float32([1e-30, 1e-40, 2.0 ** -10, 2.0 ** -11, 3 * 2.0 ** -11])])
+    v = np.concatenate([v, -v])
+    top = np.float32(448.0 if act == "e4m3" else 127.0)
+    return v[np.abs(v) <= top], top
+
+
+@pytest.mark.parametrize("act", ["i8", "e4m3"])
+def test_act_quant_rounding_at_every_tie(lib, act):
+    """Rows whose absmax is the format's largest value quantise at scale 1
+    exactly, so each code is the rounding of the value itself: every tie
+    between neighbouring codes and its neighbours against the oracle."""
+    v, top = _rounding_cases(act)
+    K = 512
+    rows = (v.size + K - 2) // (K - 1)
+    X = np.zeros((rows, K), dtype=np.float32)
+    X[:, 0] = top                                  # absmax of every row
+    X[:, 1:].flat[:v.size] = v
+    X_dev, X_seen = to_dev(X, "f32")
+    assert np.array_equal(X_seen, X)
+    Xq = torch.empty((rows, K), dtype=torch.uint8, device=DEV)
+    xdq = torch.empty((rows,), dtype=torch.float32, device=DEV)
+    dqt.dqt_act_quant(X_dev, act_code(act), Xq, xdq)
+    want_q, want_d = O.act_quant(X_seen, act)
+    assert np.array_equal(xdq.cpu().numpy(), want_d)
+    assert np.array_equal(Xq.cpu().numpy(), want_q.view(np.uint8))
+
+
 @pytest.mark.parametrize("x_t", ["f32", "bf16"])
 @pytest.mark.parametrize("act", ["i8", "e4m3"])
 def test_act_quant_batch_matches_oracle(lib, x_t, act):
