@@ -154,6 +154,23 @@ def run_step(blk, dqt, step, stream, rec, split_bwd=False, sr="separate"):
                                               stream))
 
 
+def gemm_min_bytes(wl):
+    """Per GEMM call kind, the bytes it moves at the least: each operand read
+    once and each output written once (quantised inputs once per distinct
+    input; the fused call reads and writes the codes instead of writing dW)."""
+    M = wl.M
+    cb = CODE_BYTES.get(wl.wfmt, 1.0)
+    size = {"f32": 4, "bf16": 2}
+    xq = sum(M * wl.input_width(n) for n in wl.inputs) + 4 * M * len(wl.inputs)
+    y = sum(M * l.d_out * size[wl.y_out] for l in wl.linears)
+    dy = sum(M * l.d_out * size[wl.dy_dtype] for l in wl.linears)
+    dx = sum(M * l.d_in * size[wl.dx_out] for l in wl.linears)
+    codes = cb * wl.n_weights
+    dw = 4 * wl.n_weights
+    return {"fwd": xq + codes + y, "bwd_dx": dy + codes + dx, "bwd_dw": dy + xq + dw,
+            "bwd": dy + xq + codes + dx + dw, "bwd_sr": dy + xq + 2 * codes + dx}
+
+
 def algorithmic_units(wl):
     """Per step: flops of each GEMM stage, bytes of each streaming stage."""
     M = wl.M
@@ -541,6 +558,7 @@ def main():
                   "bwd_dx": "bf16" if wl.dy_dtype == "bf16" else "f32",
                   "bwd_dw": "bf16" if wl.xt == "bf16" else "f32"}
     breakdown = {}
+    min_bytes = gemm_min_bytes(wl)
     for kind, tk in per_kind.items():
         t = tk["median"]
         u = units[kind]
@@ -550,8 +568,13 @@ def main():
             entry["buffer_sets_rotated"] = tk["calls"]
         if kind in gemm_dtype:
             tf = u / (t * 1e-3) / 1e12
+            # the call's roofline bound: max(flops at the dtype's peak, least
+            # bytes at 8 TB/s)
+            bound_ms = max(u / (PEAK_TFLOPS[gemm_dtype[kind]] * 1e12),
+                           min_bytes[kind] / (PEAK_HBM_GBS * 1e9)) * 1e3
             entry.update({"tflops": round(tf, 1), "dtype": gemm_dtype[kind],
-                          "frac_peak": round(tf / PEAK_TFLOPS[gemm_dtype[kind]], 4)})
+                          "frac_peak": round(tf / PEAK_TFLOPS[gemm_dtype[kind]], 4),
+                          "bound_ms": round(bound_ms, 4), "frac_of_bound": round(bound_ms / t, 4)})
         else:
             gbs = u / (t * 1e-3) / 1e9
             entry.update({"gbs": round(gbs, 1), "frac_hbm": round(gbs / PEAK_HBM_GBS, 4)})
