@@ -127,6 +127,12 @@ __device__ __forceinline__ int sr_fast(int code, float g, uint32_t P, float nc, 
 // A chunk's codes sit in words w[0 .. 3]; `field` is what the fast rule
 // moves (q + off, clamped to [qmin + off, qmax + off]).
 constexpr int CF_I8 = 0, CF_T2 = 1, CF_I4 = 2, CF_I3 = 3;
+// small steps of 4-bit and 3-bit codes in lane arithmetic (1), or each
+// weight by the fast rule (0; int8 codes always: their bytes extract in one
+// instruction, and the lane form measured 9 % slower for them)
+#ifndef SR_INT_SMALL
+#define SR_INT_SMALL 1
+#endif
 // Bytes of codes per chunk of 8 weights.
 template <int CF>
 constexpr int chunk_code_bytes() { return CF == CF_T2 ? 2 : CF == CF_I3 ? 3 : CF == CF_I4 ? 4 : 8; }
@@ -233,9 +239,12 @@ struct ChunkIO {
 // below code 0) by one masked add and one masked subtract.  Returns false,
 // with nothing changed, when the chunk holds a step of 1 or more, a
 // non-finite gradient, a tie or an invalid code 3: the full rule decides it.
-template <class Count>
-__device__ __forceinline__ bool sr_chunk_t2_small(uint32_t code, const f32x4 (&gv)[2], uint4 r, float c,
-                                                  uint32_t& out, Count& changed) {
+// The moves of a chunk of 8 weights whose steps all satisfy |delta| < 1, as
+// bit masks (bit j for weight j): mv, the weights that move one step; up,
+// those whose delta is positive.  False when some |delta| >= 1, a gradient
+// is not finite or a draw ties (p16 = h).
+__device__ __forceinline__ bool small_moves(const f32x4 (&gv)[2], uint4 r, float c, uint32_t& mv,
+                                            uint32_t& up) {
   // x = c g 2^16 = -delta 2^16, exact (|c| < 2^100 checked by the caller)
   const float cs = c * 65536.0f;
   float x[8];
@@ -249,7 +258,9 @@ __device__ __forceinline__ bool sr_chunk_t2_small(uint32_t code, const f32x4 (&g
   if (!(m < 65536.0f)) return false;
   // bit j of mv: p16 < h (p16 - h < 0, both below 2^16); bit j of up: x < 0
   // (delta > 0); dmin = 0 iff some p16 = h
-  uint32_t mv = 0, up_dir = 0, dmin = 0xFFFFFFFFu;
+  uint32_t dmin = 0xFFFFFFFFu;
+  mv = 0;
+  up = 0;
 #pragma unroll
   for (int j = 7; j >= 0; --j) {
     const uint32_t word = (j >> 1) == 0 ? r.x : (j >> 1) == 1 ? r.y : (j >> 1) == 2 ? r.z : r.w;
@@ -259,9 +270,16 @@ __device__ __forceinline__ bool sr_chunk_t2_small(uint32_t code, const f32x4 (&g
     const uint32_t d = p - h;
     dmin = min(dmin, d);
     mv = __builtin_amdgcn_alignbit(mv, d, 31);
-    up_dir = __builtin_amdgcn_alignbit(up_dir, __float_as_uint(x[j]), 31);
+    up = __builtin_amdgcn_alignbit(up, __float_as_uint(x[j]), 31);
   }
-  if (dmin == 0u || (code & (code >> 1) & 0x5555u) != 0u) return false;
+  return dmin != 0u;
+}
+
+template <class Count>
+__device__ __forceinline__ bool sr_chunk_t2_small(uint32_t code, const f32x4 (&gv)[2], uint4 r, float c,
+                                                  uint32_t& out, Count& changed) {
+  uint32_t mv, up_dir;
+  if (!small_moves(gv, r, c, mv, up_dir) || (code & (code >> 1) & 0x5555u) != 0u) return false;
   auto spread = [](uint32_t v) {            // bit j -> bit 2 j (8 bits)
     v = (v | (v << 4)) & 0x0F0Fu;
     v = (v | (v << 2)) & 0x3333u;
@@ -272,6 +290,87 @@ __device__ __forceinline__ bool sr_chunk_t2_small(uint32_t code, const f32x4 (&g
   const uint32_t dn = M & ~U & (code | (code >> 1)) & 0x5555u;    // not from code 0
   out = code + up - dn;
   changed += __builtin_popcount(up | dn);
+  return true;
+}
+
+// The same for two's-complement codes of B = 4 or 3 bits (CF_I4: one word
+// of eight nibbles; CF_I3: eight 3-bit fields in the low 24 bits).  Codes
+// are offset to u = q + 2^(B-1) (`bias`) and the fields of even and odd
+// weights split into two words whose lanes have room above each field (8-
+// and 6-bit lanes), so that sums carry no
+// further than their own lane: a field is nonzero iff field + (2^(w-1) - 1)
+// sets the lane's top bit (w the lane width), u > H iff u + 2^(w-1) - 1 - H
+// does, and u < L iff u + 2^(w-1) - L does not.  A moving weight steps up
+// unless at qmax, down unless at qmin, by one masked add and one masked
+// subtract per lane word.  False (nothing changed) when the moves are not
+// all small (small_moves) or a code lies outside [qmin, qmax], which the
+// full rule clamps.
+template <int CF>
+struct SwarFmt;
+template <>
+struct SwarFmt<CF_I4> {   // lanes of 8 bits; words: even nibbles, odd nibbles
+  static constexpr int W = 8, bias = 8;
+  static constexpr uint32_t rep = 0x01010101u, off = 0x88888888u, lmask = 0x0F0F0F0Fu;
+  __device__ static void split(const uint32_t (&w)[4], uint32_t (&x)[2]) {
+    const uint32_t o = w[0] ^ off;
+    x[0] = o & lmask;
+    x[1] = (o >> 4) & lmask;
+  }
+  __device__ static uint32_t lanes(uint32_t v, int l) {   // bits l, l + 2, l + 4, l + 6 -> 0, 8, 16, 24
+    return (((v >> l) & 0x55u) * 0x41041u) & rep;
+  }
+  __device__ static void join(const uint32_t (&x)[2], uint32_t (&w)[4]) {
+    w[0] = (x[0] | (x[1] << 4)) ^ off;
+    w[1] = w[2] = w[3] = 0u;
+  }
+};
+template <>
+struct SwarFmt<CF_I3> {   // lanes of 6 bits; words: even fields, odd fields
+  static constexpr int W = 6, bias = 4;
+  static constexpr uint32_t rep = 0x00041041u, off = 0x00924924u, lmask = 0x001C71C7u;
+  __device__ static void split(const uint32_t (&w)[4], uint32_t (&x)[2]) {
+    const uint32_t o = w[0] ^ off;
+    x[0] = o & lmask;
+    x[1] = (o >> 3) & lmask;
+  }
+  __device__ static uint32_t lanes(uint32_t v, int l) {   // bits l, l + 2, l + 4, l + 6 -> 0, 6, 12, 18
+    const uint32_t b = v >> l;
+    return (b & 1u) | ((b & 4u) << 4) | ((b & 0x10u) << 8) | ((b & 0x40u) << 12);
+  }
+  __device__ static void join(const uint32_t (&x)[2], uint32_t (&w)[4]) {
+    w[0] = (x[0] | (x[1] << 3)) ^ off;
+    w[1] = w[2] = w[3] = 0u;
+  }
+};
+
+template <int CF, class Count>
+__device__ __forceinline__ bool sr_chunk_int_small(const uint32_t (&win)[4], const f32x4 (&gv)[2], uint4 r,
+                                                   const SRArgs& a, uint32_t (&wout)[4], Count& changed) {
+  using S = SwarFmt<CF>;
+  uint32_t mv, up_dir;
+  if (!small_moves(gv, r, a.c, mv, up_dir)) return false;
+  constexpr uint32_t half = 1u << (S::W - 1);             // a lane's top bit
+  constexpr uint32_t top = S::rep * half;
+  const uint32_t lo = (uint32_t)(a.qmin + S::bias), hi = (uint32_t)(a.qmax + S::bias);
+  uint32_t x[2];
+  S::split(win, x);
+  uint32_t bad = 0;
+#pragma unroll
+  for (int l = 0; l < 2; ++l)
+    bad |= (x[l] + S::rep * (half - 1u - hi)) | ~(x[l] + S::rep * (half - lo));
+  if ((bad & top) != 0u) return false;
+  uint32_t moved = 0;
+#pragma unroll
+  for (int l = 0; l < 2; ++l) {
+    const uint32_t m = S::lanes(mv, l), u = S::lanes(up_dir, l);
+    const uint32_t not_hi = (((x[l] ^ (S::rep * hi)) + S::rep * (half - 1u)) & top) >> (S::W - 1);
+    const uint32_t not_lo = (((x[l] ^ (S::rep * lo)) + S::rep * (half - 1u)) & top) >> (S::W - 1);
+    const uint32_t up = m & u & not_hi, dn = m & ~u & not_lo;
+    x[l] = x[l] + up - dn;
+    moved += __builtin_popcount(up | dn);
+  }
+  S::join(x, wout);
+  changed += moved;
   return true;
 }
 
@@ -297,6 +396,8 @@ __device__ __forceinline__ void sr_chunk(const uint32_t (&win)[4], const f32x4 (
         return;
       }
     }
+  } else if constexpr (CW == 8 && SR_INT_SMALL && (CF == CF_I4 || CF == CF_I3)) {
+    if (fabsf(a.c) < 0x1p100f && sr_chunk_int_small<CF>(win, gv, r[0], a, wout, changed)) return;
   }
 
   // finite check: a product chain stays finite unless some g is inf/NaN

@@ -366,6 +366,44 @@ def test_sr_update_ternary_small_steps_any_codes(lib):
     assert int(counters[0].item()) == n_changed and int(counters[1].item()) == n_nonfinite == 1
 
 
+@pytest.mark.parametrize("wfmt,qmin,qmax", [("i4", -8, 7), ("i4", -4, 3), ("i4", -1, 1),
+                                             ("i3", -4, 3), ("i3", -2, 1)])
+def test_sr_update_packed_small_steps(lib, wfmt, qmin, qmax):
+    """4-bit and 3-bit codes, steps |delta| < 1 on most chunks (the lane
+    arithmetic of small steps), codes mostly at the grid's edges, a few
+    outside the grid (which the rule clips, on any step), some chunks with
+    |delta| >= 1 or a non-finite gradient, and draws equal to the
+    threshold's top 16 bits: every weight and both counts against the
+    oracle."""
+    d_out, d_in = 1024, 1024
+    n = d_out * d_in
+    rng = np.random.default_rng(7 + qmax)
+    lo_f, hi_f = (-8, 7) if wfmt == "i4" else (-4, 3)
+    q = rng.choice([qmin, qmax, qmin + 1, qmax - 1], size=(d_out, d_in)).astype(np.int8)
+    q = np.clip(q, qmin, qmax).astype(np.int8)
+    q.reshape(-1)[::4099] = rng.integers(lo_f, hi_f + 1, size=q.reshape(-1)[::4099].shape)  # off-grid too
+    g = rng.uniform(-0.999, 0.999, size=(d_out, d_in)).astype(np.float32)
+    flat = g.reshape(-1)
+    flat[40_003::65_537] = 2.5            # |delta| >= 1 in a few chunks
+    flat[123_457] = np.nan
+    lr, alpha, seed, step, tid = 1.0, 1.0, 11, 2, 4
+    c = O.sr_step_size(lr, alpha)
+    delta = -(c * flat)
+    u = O.rng_u32(seed, step, tid, np.arange(n, dtype=np.uint64))
+    with np.errstate(invalid="ignore"):
+        h = np.floor(np.abs(delta.astype(np.float64)) * 65536.0)
+    assert int(np.count_nonzero((np.abs(delta) < 1) & ((u >> 16) == h))) >= 3
+    assert np.count_nonzero((q < qmin) | (q > qmax)) > 0 or (qmin, qmax) == (lo_f, hi_f)
+    w = make_weight(d_out, d_in, wfmt, qmin, qmax, alpha, tensor_id=tid)
+    Wq = weight_codes_dev(q, wfmt)
+    counters = torch.zeros((2,), dtype=torch.int64, device=DEV)
+    dqt.dqt_sr_update(w, Wq, torch.from_numpy(g).to(DEV), lr, seed, step, counters)
+    got = weight_codes_host(Wq, wfmt, d_in)
+    want, n_changed, n_nonfinite = O.sr_update(q.ravel(), flat, lr, alpha, qmin, qmax, seed, step, tid)
+    assert np.array_equal(got.ravel(), want), np.argwhere(got.ravel() != want)[:5]
+    assert int(counters[0].item()) == n_changed and int(counters[1].item()) == n_nonfinite == 1
+
+
 def test_sr_update_without_counters_and_repeatable(lib):
     d_out, d_in = 512, 512
     q = _weights(d_out, d_in, "ternary", -1, 1, 3)
