@@ -181,8 +181,11 @@ def algorithmic_units(wl):
     adam_bytes = sum((2 * code_b + 20) * l.d_in * l.d_out for l in wl.linears)
     xb = 2 if wl.x_dtype == "bf16" else 4
     act_bytes = sum(M * wl.input_width(n) * (xb + 1) + 4 * M for n in wl.inputs)
+    # force-to-update of the smallest 20 %: three selection passes over the
+    # gradient (4 B per weight each), then the update
+    upd_bytes = sr_bytes + 3 * 4 * wl.n_weights
     return {"fwd": f, "bwd": 2 * f, "bwd_sr": 2 * f, "bwd_dx": f, "bwd_dw": f, "sr": sr_bytes,
-            "act_quant": act_bytes, "adamw_sr": adam_bytes, "upd_force": sr_bytes}
+            "act_quant": act_bytes, "adamw_sr": adam_bytes, "upd_force": upd_bytes}
 
 
 def _oracle_slab(O, W, wl, tokens):
