@@ -124,7 +124,9 @@ def test_act_quant_batch_matches_oracle(lib, x_t, act):
 # -------------------------------------------------------------- forward
 
 FWD_SHAPES = [(1, 16, 16), (300, 272, 400), (512, 256, 256), (129, 48, 144), (1000, 1024, 208),
-              (257, 320, 96)]   # d_in 320: packed codes with a half step at the end
+              (257, 320, 96),   # d_in 320: packed codes with a half step at the end
+              (70, 64, 80),     # d_in 64: the whole reduction one half step
+              (1, 128, 16)]     # one token, one step
 FWD_KINDS = [  # act, wfmt, qmin, qmax, x_t, y_out
     ("i8", "ternary", -1, 1, "f32", "f32"),
     ("i8", "ternary", -1, 1, "bf16", "bf16"),
@@ -171,7 +173,7 @@ def test_forward(lib, shape, kind):
         assert ok, (nbad, emax)
 
 
-PACKED_SHAPES = [(512, 256, 256), (1000, 1024, 208), (257, 320, 96)]
+PACKED_SHAPES = [(512, 256, 256), (1000, 1024, 208), (257, 320, 96), (70, 64, 80), (1, 128, 16)]
 
 
 @pytest.mark.parametrize("shape", PACKED_SHAPES)
