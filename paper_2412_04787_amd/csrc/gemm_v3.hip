@@ -1222,6 +1222,56 @@ __global__ __launch_bounds__(256) void unpack_t_kernel(const TrTab tab) {
   }
 }
 
+// Ternary codes -> W~T as unpack_t_kernel, one block per strip of 64 rows x
+// 512 reduction elements: the strip's codes (whole 128-byte lines of each
+// row) come into LDS in one pass, eight loads in flight per thread, then its
+// eight 64 x 64 tiles are transposed through LDS in turn.  (One block per
+// tile read 16 bytes of each row's line and fetched about 4 times the code
+// bytes.)
+__global__ __launch_bounds__(256) void unpack_t2_strip_kernel(const TrTab tab) {
+  int s = 0;
+  while (s + 1 < tab.n && (int)blockIdx.x >= tab.b0[s + 1]) ++s;
+  const int strip = (int)blockIdx.x - tab.b0[s];
+  const int n0 = (strip % tab.tn[s]) * 64, ks0 = (strip / tab.tn[s]) * 512;
+  const int d_out = tab.d_out[s], d_in = tab.d_in[s];
+  __shared__ uint32_t codes[64][33];                                 // [row][word of 16 codes]
+  __shared__ __attribute__((aligned(16))) uint16_t t_lds[64][72];   // [k][n]
+  const int t = threadIdx.x;
+  {
+    // thread t: row n0 + t / 4, words 8 (t mod 4) .. + 7 of the strip
+    const int row = t >> 2, n = n0 + row;
+    const int wrow = d_in / 16;                       // words of a row
+    const uint32_t* src = reinterpret_cast<const uint32_t*>(tab.src[s]) + (int64_t)n * wrow;
+    uint32_t w[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int kw = ks0 / 16 + 8 * (t & 3) + e;
+      w[e] = (n < d_out && kw < wrow) ? src[kw] : 0u;
+    }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) codes[row][8 * (t & 3) + e] = w[e];
+  }
+  __syncthreads();
+  const int nl = t >> 2, kl = (t & 3) * 16;
+  for (int j = 0; j < 8; ++j) {
+    const int k0 = ks0 + 64 * j;
+    if (k0 >= d_in) break;                            // (uniform)
+    const uint32_t w = codes[nl][4 * j + (t & 3)];
+#pragma unroll
+    for (int e = 0; e < 16; ++e) t_lds[kl + e][nl] = (uint16_t)code_to_bf16_bits((w >> (2 * e)) & 3u);
+    __syncthreads();
+#pragma unroll
+    for (int c = t; c < 64 * 8; c += 256) {
+      const int kr = c >> 3, ch = c & 7;
+      const int k = k0 + kr, n = n0 + ch * 8;
+      if (k < d_in && n < d_out)
+        *reinterpret_cast<uint4*>(tab.dst[s] + (int64_t)k * d_out + n) =
+            *reinterpret_cast<const uint4*>(&t_lds[kr][ch * 8]);
+    }
+    __syncthreads();
+  }
+}
+
 // X~T[k, m] = bf16(fl(value(Xq[m, k]) * xdq[m])): the dequantised
 // activations transposed (the reduction of dW, over tokens, contiguous).
 // One 64 x 64 tile per block, transposed through LDS.
@@ -1488,6 +1538,9 @@ using namespace v3;
 #endif
 #ifndef DX_PACKED_B
 #define DX_PACKED_B 0
+#endif
+#ifndef UNPACK_T2_STRIP
+#define UNPACK_T2_STRIP 1
 #endif
 
 static size_t align256(size_t n) { return (n + 255) / 256 * 256; }
@@ -1760,11 +1813,15 @@ static void prep_dx(const BatchCfg& c, const LinearIO* io, uint8_t* ws, const Bw
     tab.d_in[l] = (int32_t)io[l].d_in;
     tab.tn[l] = (int32_t)((io[l].d_out + 63) / 64);
     tab.b0[l] = blocks;
-    blocks += tab.tn[l] * (int32_t)((io[l].d_in + 63) / 64);
+    // ternary: strips of 512 reduction elements; else 64 x 64 tiles
+    const int kspan = c.w_ternary && UNPACK_T2_STRIP ? 512 : 64;
+    blocks += tab.tn[l] * (int32_t)((io[l].d_in + kspan - 1) / kspan);
     grp.p[l].B = Opnd{ws + P.q_off[l], io[l].d_out * 2, io[l].d_in};
   }
   tab.b0[c.n] = blocks;
-  if (c.w_ternary)
+  if (c.w_ternary && UNPACK_T2_STRIP)
+    st << launch_kernel(unpack_t2_strip_kernel, dim3(blocks), dim3(256), stream, tab);
+  else if (c.w_ternary)
     st << launch_kernel(unpack_t_kernel<CF_T2>, dim3(blocks), dim3(256), stream, tab);
   else if (c.w_int4)
     st << launch_kernel(unpack_t_kernel<CF_I4>, dim3(blocks), dim3(256), stream, tab);
