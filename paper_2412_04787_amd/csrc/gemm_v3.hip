@@ -1098,13 +1098,18 @@ __global__ __launch_bounds__(256) void unpack_ternary_kernel(const SegTab tab) {
 
 // Packed ternary codes -> FP4 (E2M1) values, two per byte in weight order
 // (weight k in the low nibble of byte k / 2 when k is even): the B operand of
-// the e4m3 forward.  16 weights per thread.
+// the e4m3 forward.  64 weights per thread (16 bytes in, 32 out: with 16
+// weights a thread the pass was held by the few bytes each had in flight);
+// n16 a multiple of 4.
 __global__ __launch_bounds__(256) void expand_fp4_kernel(const SegTab tab) {
   const int s = seg_of_block(tab);
   const int64_t t = (int64_t)(blockIdx.x - tab.b0[s]) * 256 + threadIdx.x;
-  if (t >= tab.n16[s]) return;
-  const u32x2 v = expand16_fp4(static_cast<const uint32_t*>(tab.src[s])[t]);
-  static_cast<uint2*>(tab.dst[s])[t] = make_uint2(v[0], v[1]);
+  if (t >= tab.n16[s] / 4) return;
+  const uint4 w = static_cast<const uint4*>(tab.src[s])[t];
+  const u32x2 a = expand16_fp4(w.x), b = expand16_fp4(w.y), c = expand16_fp4(w.z), d = expand16_fp4(w.w);
+  uint4* const dst = static_cast<uint4*>(tab.dst[s]) + 2 * t;
+  dst[0] = make_uint4(a[0], a[1], b[0], b[1]);
+  dst[1] = make_uint4(c[0], c[1], d[0], d[1]);
 }
 
 // int4 codes (two's-complement nibbles, weight k at bits 4 (k mod 2) of byte
@@ -1644,9 +1649,15 @@ hipError_t launch_fwd_batch(const BatchCfg& c, const LinearIO* io, uint8_t* ws, 
     for (int l = 0; l < c.n; ++l) {
       tab.src[l] = io[l].Wq;
       tab.dst[l] = ws + offs[l];
-      tab.n16[l] = io[l].d_out * io[l].d_in / 16;
+      tab.n16[l] = io[l].d_out * io[l].d_in / 16;   // a multiple of 4 (d_in of 64)
     }
-    const int32_t blocks = seal(tab);
+    // one thread per 4 chunks
+    int32_t blocks = 0;
+    for (int l = 0; l < c.n; ++l) {
+      tab.b0[l] = blocks;
+      blocks += (int32_t)((tab.n16[l] / 4 + 255) / 256);
+    }
+    tab.b0[c.n] = blocks;
     st << launch_kernel(expand_fp4_kernel, dim3(blocks), dim3(256), stream, tab);
   } else if (c.w_ternary && !packed) {
     SegTab tab{};
