@@ -1081,19 +1081,34 @@ __global__ __launch_bounds__(256) void pack_codes_t_kernel(const TpTab tab) {
 
 // Packed ternary codes -> one operand byte (int8 or e4m3) per weight, same
 // [d_out][d_in] row-major order.
-template <int OUT>   // 0: int8, 1: e4m3
-__global__ __launch_bounds__(256) void unpack_ternary_kernel(const SegTab tab) {
-  const int s = seg_of_block(tab);
-  const int64_t t = (int64_t)(blockIdx.x - tab.b0[s]) * 256 + threadIdx.x;
-  if (t >= tab.n16[s]) return;
-  const uint32_t w = static_cast<const uint32_t*>(tab.src[s])[t];
+// Four chunks of 16 weights per thread (16 bytes in, 64 out), the last
+// thread of a tensor whatever chunks remain.
+template <int OUT>
+__device__ __forceinline__ uint4 unpack16_ternary(uint32_t w) {
   uint32_t o[4];
 #pragma unroll
   for (int b = 0; b < 4; ++b) {
     const uint32_t sp = spread_codes((w >> (8 * b)) & 0xFFu);
     o[b] = OUT == 1 ? codes_to_e4m3x4(sp) : codes_to_i8x4(sp);
   }
-  static_cast<uint4*>(tab.dst[s])[t] = make_uint4(o[0], o[1], o[2], o[3]);
+  return make_uint4(o[0], o[1], o[2], o[3]);
+}
+template <int OUT>   // 0: int8, 1: e4m3
+__global__ __launch_bounds__(256) void unpack_ternary_kernel(const SegTab tab) {
+  const int s = seg_of_block(tab);
+  const int64_t t = (int64_t)(blockIdx.x - tab.b0[s]) * 256 + threadIdx.x;
+  const int64_t g0 = 4 * t, n16 = tab.n16[s];
+  if (g0 >= n16) return;
+  uint4* const dst = static_cast<uint4*>(tab.dst[s]);
+  if (g0 + 4 <= n16) {
+    const uint4 w = static_cast<const uint4*>(tab.src[s])[t];
+    dst[g0] = unpack16_ternary<OUT>(w.x);
+    dst[g0 + 1] = unpack16_ternary<OUT>(w.y);
+    dst[g0 + 2] = unpack16_ternary<OUT>(w.z);
+    dst[g0 + 3] = unpack16_ternary<OUT>(w.w);
+  } else {
+    for (int64_t g = g0; g < n16; ++g) dst[g] = unpack16_ternary<OUT>(static_cast<const uint32_t*>(tab.src[s])[g]);
+  }
 }
 
 // Packed ternary codes -> FP4 (E2M1) values, two per byte in weight order
@@ -1667,7 +1682,13 @@ hipError_t launch_fwd_batch(const BatchCfg& c, const LinearIO* io, uint8_t* ws, 
       tab.dst[l] = ws + offs[l];
       tab.n16[l] = io[l].d_out * io[l].d_in / 16;
     }
-    const int32_t blocks = seal(tab);
+    // one thread per 4 chunks
+    int32_t blocks = 0;
+    for (int l = 0; l < c.n; ++l) {
+      tab.b0[l] = blocks;
+      blocks += (int32_t)(((tab.n16[l] + 3) / 4 + 255) / 256);
+    }
+    tab.b0[c.n] = blocks;
     if (c.act_e4m3)
       st << launch_kernel(unpack_ternary_kernel<1>, dim3(blocks), dim3(256), stream, tab);
     else
