@@ -27,7 +27,7 @@ Paper map (section / equation of the DQT paper):
   * Sec. 5 (rounding without SR; forcing the smallest 20 %; R12) -> update_variant
   * Sec. 3.2 inputs of the linears after the block's RMSNorm (R13) -> rmsnorm_act_quant
 
-Readings of points the paper leaves open (each is listed in the design doc):
+Readings of points the paper leaves open:
   R1  SR acts in grid units: with W~ = q * alpha (alpha = 1/s, Eq. 3) and
       W' = W~ - lr * grad, the updated code is SR(W' / alpha).  This is what
       the worked example of Sec. 5 (a value -1 + 0.02 goes to 0 with
