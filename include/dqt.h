@@ -18,8 +18,10 @@
  *  - Tensor pointers are DEVICE pointers unless marked "host".  The caller
  *    owns every buffer; the library never allocates or frees memory on these
  *    calls and holds no mutable global state (except the static scratch of
- *    dqt_linear_fwd_batch_noalloc), so calls on different streams or devices
- *    may run concurrently (as long as their buffers differ).
+ *    dqt_linear_fwd_batch_noalloc, and the launch timer while one runs: it
+ *    creates and frees its events at start and stop), so calls on different
+ *    streams or devices may run concurrently (as long as their buffers
+ *    differ).
  *  - Layouts are row-major.  W is [d_out, d_in] (nn.Linear); X is [M, d_in];
  *    Y and dY are [M, d_out].  M is the number of tokens.
  *  - `stream` is a hipStream_t (NULL = the legacy default stream).  Every
