@@ -1544,7 +1544,9 @@ using namespace v3;
 
 // reduction bytes per step of the unpacked 8-bit forward and of the bf16
 // backward products (128: full lines, two stages; 64: half lines, four
-// stages in flight -- measured equal on the LLaMA-block shapes)
+// stages in flight: 9-11 % slower for the int8 forward on the LLaMA-block
+// shapes; the backward's SR epilogue needs a whole 64 KB stage for its
+// staging)
 #ifndef KB_FWD
 #define KB_FWD 128
 #endif
