@@ -17,6 +17,8 @@
 // weight).
 #include <math.h>
 
+#include <algorithm>
+
 #include "sr_rule.h"
 
 namespace dqt {
@@ -25,8 +27,11 @@ namespace {
 
 constexpr int kMaxV = kMaxBatch;
 constexpr int kHistBins = 2048;
-constexpr int kChunksPerThread = 4;               // 8 weights per chunk
-constexpr int kElemsPerBlock = 256 * 8 * kChunksPerThread;
+// A selection block takes 256 threads x `chunks` chunks of 8 weights, chunks
+// a multiple of 4 from 4 to 32 chosen by the host for at least ~1024 blocks:
+// more weights a block spread its histogram's clearing and flushing (h4096
+// block, force-to-update call: 1010 us at 4 chunks, 725 us at 32).
+constexpr int kMinChunks = 4, kMaxChunks = 32;
 
 // Radix-select state of one tensor (in the caller's workspace).
 struct SelState {
@@ -38,7 +43,8 @@ struct VarTab {
   uint8_t* wq[kMaxV];
   const float* grad[kMaxV];
   int64_t nweights[kMaxV];
-  int64_t b0[kMaxV + 1];         // blocks of kElemsPerBlock weights (selection passes)
+  int64_t b0[kMaxV + 1];         // blocks of 2048 `chunks` chunks (selection passes)
+  int32_t chunks;                // chunks of 8 weights per thread (selection passes)
   int64_t t0[kMaxV + 1];         // tiles of 256 chunks (update)
   float c[kMaxV], L[kMaxV];
   int qmin[kMaxV], qmax[kMaxV];
@@ -71,7 +77,7 @@ __global__ __launch_bounds__(256) void sel_init_kernel(const VarTab tab, SelStat
 }
 
 // Histogram of bits [shift, shift + nbits) of the keys that match the bits
-// chosen so far.  One block per kElemsPerBlock weights of one tensor.
+// chosen so far.  One block per 2048 chunks of 8 weights of one tensor.
 __global__ __launch_bounds__(256) void sel_hist_kernel(const VarTab tab, SelState* __restrict__ st,
                                                        int shift, int nbins) {
   __shared__ uint32_t h[kHistBins];
@@ -81,19 +87,25 @@ __global__ __launch_bounds__(256) void sel_hist_kernel(const VarTab tab, SelStat
   const SelState& S = st[s];
   const uint32_t prefix = S.prefix, mask = S.mask;
   if (tab.k[s] != 0) {
-    const int64_t base = (int64_t)(blockIdx.x - tab.b0[s]) * kElemsPerBlock;
+    const int chunks = tab.chunks;
+    const int64_t nw = tab.nweights[s];
+    const int64_t base = (int64_t)(blockIdx.x - tab.b0[s]) * (2048 * (int64_t)chunks);
     const float c = tab.c[s];
     const f32x4* g4 = reinterpret_cast<const f32x4*>(tab.grad[s]);
+    for (int u0 = 0; u0 < chunks; u0 += 4) {
+      if (base + (int64_t)u0 * 2048 >= nw) break;          // (block-uniform)
+      // four chunks' loads in flight
 #pragma unroll
-    for (int u = 0; u < kChunksPerThread; ++u) {
-      const int64_t e0 = base + ((int64_t)u * 256 + threadIdx.x) * 8;
-      if (e0 >= tab.nweights[s]) break;
-      const f32x4 a = g4[e0 / 4], b = g4[e0 / 4 + 1];
-      const float g[8] = {a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+      for (int du = 0; du < 4; ++du) {
+        const int64_t e0 = base + ((int64_t)(u0 + du) * 256 + threadIdx.x) * 8;
+        if (e0 >= nw) break;
+        const f32x4 a = g4[e0 / 4], b = g4[e0 / 4 + 1];
+        const float g[8] = {a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const uint32_t key = delta_key(g[j], c);
-        if ((key & mask) == prefix) atomicAdd(&h[(key >> shift) & (uint32_t)(nbins - 1)], 1u);
+        for (int j = 0; j < 8; ++j) {
+          const uint32_t key = delta_key(g[j], c);
+          if ((key & mask) == prefix) atomicAdd(&h[(key >> shift) & (uint32_t)(nbins - 1)], 1u);
+        }
       }
     }
   }
@@ -401,6 +413,10 @@ hipError_t launch_update_variant(int cf, int n, const SRTensor* t, int mode, flo
   tab.step = step;
   int64_t blocks = 0, tiles = 0;
   bool any_sel = false;
+  int64_t total = 0;
+  for (int s = 0; s < n; ++s) total += t[s].nweights;
+  tab.chunks = (int32_t)std::max<int64_t>(kMinChunks, std::min<int64_t>(kMaxChunks, total / (2048 * 1024) / 4 * 4));
+  const int64_t per_block = 2048 * (int64_t)tab.chunks;
   for (int s = 0; s < n; ++s) {
     tab.wq[s] = t[s].wq;
     tab.grad[s] = t[s].grad;
@@ -414,7 +430,7 @@ hipError_t launch_update_variant(int cf, int n, const SRTensor* t, int mode, flo
     tab.k[s] = (uint32_t)kk;
     any_sel |= tab.k[s] != 0;
     tab.b0[s] = blocks;
-    blocks += (t[s].nweights + kElemsPerBlock - 1) / kElemsPerBlock;
+    blocks += (t[s].nweights + per_block - 1) / per_block;
     tab.t0[s] = tiles;
     tiles += (t[s].nweights / 8 + 255) / 256;
   }

@@ -83,3 +83,33 @@ def test_update_variant_batch_equals_singles(lib):
     assert torch.equal(c1, c2)
     for e, s in zip(ents, singles):
         assert torch.equal(e["Wq"], s["Wq"])
+
+
+@pytest.mark.parametrize("mode", [dqt.DQT_UPD_FORCE_CHANGE, dqt.DQT_UPD_FORCE_REMAIN])
+def test_update_variant_large_batch_equals_singles(lib, mode):
+    """A batch of 17.8 M weights takes 8 chunks of 8 weights per thread in its
+    selection passes (a single 8.4 M-weight tensor takes 4), the last block of
+    a tensor partly empty: codes and counts equal those of the single calls,
+    whose selection the small cases above pin to the oracle."""
+    shapes = [(2048, 4096), (2048, 4096), (1040, 1024)]
+    log(f"variant large batch mode {mode}: {shapes}")
+    ents, singles = [], []
+    for li, (d_out, d_in) in enumerate(shapes):
+        q = torch.from_numpy(W.draw_ternary((d_out, d_in), SEED, 70, li))
+        w = make_weight(d_out, d_in, "ternary", -1, 1, 0.01, tensor_id=li)
+        g = torch.randn((d_out, d_in), generator=torch.Generator().manual_seed(li), dtype=torch.float32) * 1e-2
+        g = g.to(DEV)
+        ents.append(dict(w=w, Wq=weight_codes_dev(q.numpy(), "ternary"), dW=g))
+        singles.append(dict(w=w, Wq=weight_codes_dev(q.numpy(), "ternary"), dW=g))
+    c1 = torch.zeros((2,), dtype=torch.int64, device=DEV)
+    c2 = torch.zeros((2,), dtype=torch.int64, device=DEV)
+    ws = dqt.workspace(dqt.dqt_update_variant_workspace(len(shapes)))
+    dqt.dqt_update_variant_batch(dqt.linear_io(ents), 1e-2, 5, 3, mode, 0.2, c1, ws)
+    ws1 = dqt.workspace(dqt.dqt_update_variant_workspace(1))
+    for s in singles:
+        dqt.dqt_update_variant_batch(dqt.linear_io([s]), 1e-2, 5, 3, mode, 0.2, c2, ws1)
+    torch.cuda.synchronize()
+    for a, b in zip(ents, singles):
+        assert torch.equal(a["Wq"], b["Wq"])
+    assert torch.equal(c1, c2)
+    assert int(c1[0].item()) > 0
