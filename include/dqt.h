@@ -307,9 +307,8 @@ dqt_status dqt_linear_fwd_batch(int32_t n, const dqt_linear_io* io, int64_t M,
  * call allocates nothing: its scratch (the tile counters, plus the operand
  * bytes of dqt_linear_fwd_batch_workspace() when they fit; ternary codes
  * whose expansion does not fit run from the packed codes) is a static device
- * array of
- * DQT_NOALLOC_SCRATCH_BYTES that each GPU the library runs on holds until
- * the process ends; its address is looked up on a device's first call.
+ * array of DQT_NOALLOC_SCRATCH_BYTES that each GPU the library runs on holds
+ * until the process ends; its address is looked up on a device's first call.
  * Calls on one GPU share that array, so calls that overlap in time on one
  * GPU (different streams, or threads without ordering) race and must not be
  * made; the counters are cleared by every call on its stream.
