@@ -75,6 +75,9 @@ typedef enum {
 
 /*
  * Weight descriptor (Sec. 3.2).
+ *   d_out, d_in: multiples of 16, 16 <= d_out, 16 <= d_in <= 65536 (the
+ *          int8 forward's int32 sums stay exact: |acc| <= 128 * 128 * 65536
+ *          = 2^30); else DQT_ERR_SHAPE.
  *   wfmt = DQT_TERNARY2: q in {-1, 0, 1}; weight (n, k) is stored as the
  *          2-bit code q + 1 in byte n * (d_in / 4) + k / 4, bit offset
  *          2 * (k % 4).  Code 3 is never written and must not appear.

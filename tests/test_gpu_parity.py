@@ -260,6 +260,49 @@ def test_backward(lib, shape, kind):
     assert ok, ("dW", nbad, emax)
 
 
+@pytest.mark.parametrize("act,wfmt,qmin,qmax", [("i8", "i8", -128, 127), ("e4m3", "ternary", -1, 1)])
+def test_maximum_reduction_length(lib, act, wfmt, qmin, qmax):
+    """d_in = 65536, the largest the library takes: the forward (one token's
+    int32 sum at 127 * 128 * 65536 for int8 codes, exact), dX, dW and the SR
+    update of the same weights against the oracle."""
+    M, d_in, d_out = 40, 65536, 32
+    log(f"maximum d_in: M={M} d_in={d_in} d_out={d_out} {act} {wfmt}")
+    q = _weights(d_out, d_in, wfmt, qmin, qmax, M, d_in, d_out, 11)
+    q[0, :] = qmin                                  # the largest |sum| of row 0 of Y
+    alpha = np.float32(0.0137)
+    w = make_weight(d_out, d_in, wfmt, qmin, qmax, alpha, tensor_id=2)
+    Wq = weight_codes_dev(q, wfmt)
+    X = draws((M, d_in), 1.0, 12, M, d_in)
+    X[0, :] = -1.0
+    X_dev, X_seen = to_dev(X, "bf16")
+    Xq, xdq, Y = run_fwd(w, Wq, X_dev, act, "f32")
+    want_q, want_d = O.act_quant(X_seen, act)
+    Y_ref, acc = O.linear_fwd(want_q, want_d, act, q, alpha, "f32")
+    if act == "i8":
+        assert int(np.max(np.abs(acc))) == 127 * 128 * 65536
+        assert np.array_equal(Y.cpu().numpy(), Y_ref)
+    else:
+        a = np.abs(O.act_values(want_q, act)) @ np.abs(q.astype(np.float64)).T
+        f = (want_d * alpha).astype(np.float64)[:, None]
+        ok, nbad, emax = gemm_close(Y.cpu().numpy(), acc * f, a * f, bf16_out=False)
+        assert ok, (nbad, emax)
+    dY_dev, dY_seen = to_dev(draws((M, d_out), 1e-2, 13, M, d_out), "bf16")
+    dX, dW = run_bwd(w, Wq, Xq, act, xdq, dY_dev, "bf16", "f32")
+    _, _, dX64, dW64 = O.linear_bwd(dY_seen, q, alpha, want_q, want_d, act, "bf16", "f32")
+    bx = float(alpha) * O.gemm_abs_bound(dY_seen, q.astype(np.float64))
+    ok, nbad, emax = gemm_close(dX.cpu().numpy(), dX64, bx)
+    assert ok, ("dX", nbad, emax)
+    bw = O.gemm_abs_bound(dY_seen.T, O.act_dequant(want_q, want_d, act, "bf16"))
+    ok, nbad, emax = gemm_close(dW.cpu().numpy(), dW64, bw)
+    assert ok, ("dW", nbad, emax)
+    counters = torch.zeros((2,), dtype=torch.int64, device=DEV)
+    dqt.dqt_sr_update(w, Wq, dW, 3e-3, 9, 1, counters)
+    g = dW.cpu().numpy()
+    want, n_changed, n_nonfinite = O.sr_update(q.ravel(), g.ravel(), 3e-3, alpha, qmin, qmax, 9, 1, 2)
+    assert np.array_equal(weight_codes_host(Wq, wfmt, d_in).ravel(), want)
+    assert int(counters[0].item()) == n_changed and int(counters[1].item()) == n_nonfinite
+
+
 def test_backward_empty_tokens_writes_zero_dw(lib):
     w = make_weight(48, 32, "ternary", -1, 1, 0.01)
     Wq = weight_codes_dev(np.zeros((48, 32), np.int8), "ternary")
