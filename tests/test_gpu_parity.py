@@ -449,6 +449,24 @@ def test_sr_update_packed_small_steps(lib, wfmt, qmin, qmax):
     assert int(counters[0].item()) == n_changed and int(counters[1].item()) == n_nonfinite == 1
 
 
+@pytest.mark.parametrize("wfmt,qmin,qmax", [("ternary", -1, 1), ("i4", -8, 7), ("i3", -4, 3), ("i8", -128, 127)])
+def test_sr_update_degenerate_steps_change_nothing(lib, wfmt, qmin, qmax):
+    """lr = 0 with any gradient, and any lr with a zero gradient (both signs
+    of zero): every code stays, nothing is counted."""
+    d_out, d_in = 256, 512
+    q = _weights(d_out, d_in, wfmt, qmin, qmax, 31)
+    w = make_weight(d_out, d_in, wfmt, qmin, qmax, 0.01, tensor_id=1)
+    g = draws((d_out, d_in), 1.0, 32, d_out, d_in)
+    zero = np.zeros_like(g)
+    zero.reshape(-1)[1::2] = -0.0
+    for lr, grad in ((0.0, g), (0.5, zero)):
+        Wq = weight_codes_dev(q, wfmt)
+        counters = torch.zeros((2,), dtype=torch.int64, device=DEV)
+        dqt.dqt_sr_update(w, Wq, torch.from_numpy(grad).to(DEV), lr, 3, 7, counters)
+        assert np.array_equal(weight_codes_host(Wq, wfmt, d_in), q)
+        assert counters.tolist() == [0, 0]
+
+
 def test_sr_update_without_counters_and_repeatable(lib):
     d_out, d_in = 512, 512
     q = _weights(d_out, d_in, "ternary", -1, 1, 3)

@@ -212,3 +212,17 @@ def test_step_size_is_lr_over_alpha_in_fp32():
     c = O.sr_step_size(3e-4, 0.0123)
     assert c == np.float32(np.float32(3e-4) / np.float32(0.0123))
     assert c.dtype == np.float32
+
+
+def test_zero_step_changes_nothing():
+    """lr = 0, or a zero gradient of either sign: Eq. 5 leaves W' = W~, which
+    lies on the grid, so SR returns every code unchanged whatever the draws."""
+    rng = np.random.default_rng(5)
+    q = rng.integers(-8, 8, size=4096).astype(np.int64)
+    g = rng.standard_normal(4096).astype(np.float32)
+    out, n_changed, n_nonfinite = O.sr_update(q, g, 0.0, 0.01, -8, 7, 3, 7, 1)
+    assert np.array_equal(out, q) and n_changed == 0 and n_nonfinite == 0
+    z = np.zeros(4096, np.float32)
+    z[1::2] = -0.0
+    out, n_changed, _ = O.sr_update(q, z, 0.5, 0.01, -8, 7, 3, 7, 1)
+    assert np.array_equal(out, q) and n_changed == 0
