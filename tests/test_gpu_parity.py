@@ -467,6 +467,30 @@ def test_sr_update_degenerate_steps_change_nothing(lib, wfmt, qmin, qmax):
         assert counters.tolist() == [0, 0]
 
 
+@pytest.mark.parametrize("wfmt,qmin,qmax", [("ternary", -1, 1), ("i4", -4, 3), ("i8", -127, 127)])
+def test_sr_update_overflowing_step(lib, wfmt, qmin, qmax):
+    """lr / alpha near the top of fp32 (c = 5e37, past the 2^100 bound of
+    the small-step paths): c g overflows to an infinite step for about half
+    of the gradients (|g| > 6.8) and is finite but far beyond the grid for
+    the rest; every code saturates toward its step's sign (the gradients are
+    finite, so nothing counts as non-finite), and zero gradients stay put."""
+    d_out, d_in = 128, 256
+    alpha = np.float32(2e-38)                    # the smallest normal fp32 is 1.18e-38
+    q = _weights(d_out, d_in, wfmt, qmin, qmax, 41)
+    w = make_weight(d_out, d_in, wfmt, qmin, qmax, alpha, tensor_id=6)
+    g = draws((d_out, d_in), 10.0, 42, d_out, d_in)
+    g.reshape(-1)[::7] = 0.0
+    c = O.sr_step_size(1.0, alpha)
+    with np.errstate(over="ignore"):
+        assert np.count_nonzero(np.isinf(c * g)) > g.size // 4
+    Wq = weight_codes_dev(q, wfmt)
+    counters = torch.zeros((2,), dtype=torch.int64, device=DEV)
+    dqt.dqt_sr_update(w, Wq, torch.from_numpy(g).to(DEV), 1.0, 8, 2, counters)
+    want, n_changed, n_nonfinite = O.sr_update(q.ravel(), g.ravel(), 1.0, alpha, qmin, qmax, 8, 2, 6)
+    assert np.array_equal(weight_codes_host(Wq, wfmt, d_in).ravel(), want)
+    assert counters.tolist() == [n_changed, n_nonfinite] and n_nonfinite == 0
+
+
 def test_sr_update_without_counters_and_repeatable(lib):
     d_out, d_in = 512, 512
     q = _weights(d_out, d_in, "ternary", -1, 1, 3)
