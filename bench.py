@@ -281,11 +281,14 @@ def cpu_baseline(wl, tokens: int, sr_weights: int):
 
 
 def kernel_source_hash() -> str:
+    """Hash of what the kernels are built from: the HIP sources and the build
+    script (its compiler flags)."""
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2412_04787_amd", "csrc")
     for f in sorted(os.listdir(csrc)):
         if f.endswith((".hip", ".h")):
             h.update(open(os.path.join(csrc, f), "rb").read())
+    h.update(open(os.path.join(ROOT, "paper_2412_04787_amd", "build_lib.py"), "rb").read())
     return h.hexdigest()[:16]
 
 

@@ -61,7 +61,8 @@ def test_traffic_read_only_from_a_profile_of_the_current_sources(tmp_path, monke
     prof = tmp_path / "profiles"
     prof.mkdir()
     (tmp_path / "paper_2412_04787_amd").mkdir()
-    os.symlink(os.path.join(ROOT, "paper_2412_04787_amd", "csrc"), tmp_path / "paper_2412_04787_amd" / "csrc")
+    for f in ("csrc", "build_lib.py"):
+        os.symlink(os.path.join(ROOT, "paper_2412_04787_amd", f), tmp_path / "paper_2412_04787_amd" / f)
     monkeypatch.setattr(bench, "ROOT", str(tmp_path))
     h = bench.kernel_source_hash()
     body = "# comment = 1\nkernel_source_hash = {}\nfetch_write_bytes_per_launch = 1234\n" \
