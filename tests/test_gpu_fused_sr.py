@@ -150,3 +150,39 @@ def test_fused_sr_argument_checks(lib):
     dqt.dqt_linear_bwd_sr_batch(io, 0, dqt.DQT_I8, bf, bf, bf, 1e-3, 0, 1, None, ws)
     torch.cuda.synchronize()
     assert torch.equal(before, t)
+
+
+def test_fused_sr_is_deterministic_at_block_size(lib):
+    """The step's fused call on the hidden-768 block (M = 8192, seven
+    linears, several dW tiles per compute unit) twice from the same codes:
+    codes, dX and counts identical bit for bit (fixed reduction orders, no
+    atomics in any value)."""
+    import os
+    import sys
+    sys.path.insert(0, os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
+    import bench
+    log("fused backward + SR determinism: llama_h768")
+    blk = bench.Block(W.WORKLOADS["llama_h768"], torch, dqt, W)
+
+    def only(kind):
+        def rec(k, fn):
+            if k == kind:
+                fn()
+        return rec
+    bench.run_step(blk, dqt, 1, None, only("act_quant"))
+    bench.run_step(blk, dqt, 1, None, only("fwd"))
+    torch.cuda.synchronize()
+    codes0 = [c.clone() for c in blk.codes]
+    outs = []
+    for _ in range(2):
+        for c, c0 in zip(blk.codes, codes0):
+            c.copy_(c0)
+        blk.counters.zero_()
+        bench.run_step(blk, dqt, 5, None, only("bwd_sr"), sr="fused")
+        torch.cuda.synchronize()
+        outs.append(([c.clone() for c in blk.codes], [x.clone() for x in blk.dX], blk.counters.clone()))
+    (ca, xa, na), (cb, xb, nb) = outs
+    assert all(torch.equal(a, b) for a, b in zip(ca, cb))
+    assert all(torch.equal(a, b) for a, b in zip(xa, xb))
+    assert torch.equal(na, nb) and int(na[0].item()) > 0
+    assert any(not torch.equal(a, b) for a, b in zip(ca, codes0))
