@@ -18,6 +18,7 @@ template <> struct AccT<Mfma::I8> { using type = i32x16; };
 struct EpiFwd {          // y = fl(fl(acc) * fl(xdq[i] * alpha))
   void* y; int64_t ld; bool bf16; const float* xdq; float alpha;
   static constexpr bool kRowScale = true;
+  static constexpr bool kTrans = false;
   static constexpr bool kSR = false;
   static constexpr bool kTern = false;
   static constexpr int kCF = 0;
@@ -40,6 +41,7 @@ struct EpiFwd {          // y = fl(fl(acc) * fl(xdq[i] * alpha))
 struct EpiScale {        // y = fl(alpha * acc)
   void* y; int64_t ld; bool bf16; float alpha;
   static constexpr bool kRowScale = false;
+  static constexpr bool kTrans = false;
   static constexpr bool kSR = false;
   static constexpr bool kTern = false;
   static constexpr int kCF = 0;
@@ -60,6 +62,7 @@ struct EpiScale {        // y = fl(alpha * acc)
 struct EpiPartial {      // fp32 partial sums, one slab per split
   float* y; int64_t ld; int64_t slab;
   static constexpr bool kRowScale = false;
+  static constexpr bool kTrans = false;
   static constexpr bool kSR = false;
   static constexpr bool kTern = false;
   static constexpr int kCF = 0;
@@ -80,7 +83,12 @@ struct EpiPartial {      // fp32 partial sums, one slab per split
 // a row goes through the direct SR update of its 8 codes (Sec. 3.2 Eq. 5)
 // and dW itself is never stored.  CF: code format, 0 int8 codes (8 bytes
 // per 8 weights), 1 2-bit ternary codes (2 bytes), 2 int4 nibbles (4 bytes).
-template <int CF>
+// TR: the product is formed transposed, dW^T = X~^T dY (rows d_in, columns
+// d_out), with the MFMA operands swapped so that each lane still holds four
+// consecutive weights of a row of dW; the transposing LDS reads of dY's
+// tiles then fall on the wave's two column blocks instead of its four row
+// blocks.
+template <int CF, bool TR = false>
 struct EpiSR {
   uint8_t* wq;          // codes [d_out][d_in], updated in place
   int64_t ldc;          // bytes per code row (d_in / 4, d_in / 2 or d_in)
@@ -90,6 +98,7 @@ struct EpiSR {
   uint32_t k0, k1, step, tid;   // Philox key (seed), step, tensor id
   unsigned long long* counters; // nullable: changed, non-finite (accumulated)
   static constexpr bool kRowScale = false;
+  static constexpr bool kTrans = TR;
   static constexpr bool kSR = true;
   static constexpr bool kTern = CF == 1;
   static constexpr int kCF = CF;

@@ -528,6 +528,10 @@ __device__ __forceinline__ void gemm_v3_body(const Group<Epi>& grp, lds_u8* smem
       for (int tb = 0; tb < WJ; ++tb) {
         if constexpr (ELEM == EI8)
           acc[ta][tb] = __builtin_amdgcn_mfma_i32_32x32x32_i8(opb(F, tb), opa(F, ta), acc[ta][tb], 0, 0, 0);
+        else if constexpr (Epi::kTrans)   // lanes hold four consecutive rows of one column
+          acc[ta][tb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, opa(F, ta)),
+                                                                __builtin_bit_cast(bf16x8, opb(F, tb)),
+                                                                acc[ta][tb], 0, 0, 0);
         else
           acc[ta][tb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, opb(F, tb)),
                                                                 __builtin_bit_cast(bf16x8, opa(F, ta)),
@@ -738,9 +742,17 @@ __device__ __forceinline__ void gemm_v3_body(const Group<Epi>& grp, lds_u8* smem
     [[maybe_unused]] uint32_t srt[Epi::kSR ? WI : 1][Epi::kSR ? WJ : 1];
     [[maybe_unused]] uint32_t sr8[Epi::kSR && !Epi::kTern ? WI : 1][Epi::kSR && !Epi::kTern ? WJ : 1][2][2];
     auto sr_pos = [&](int ta, int tb, int u, int64_t& n, int64_t& k) {
-      n = i0 + wi * 32 * WI + ta * 32 + sr_r + 16 * u;
-      k = j0 + wj * 32 * WJ + tb * 32 + 8 * sr_c;
-      return n < I && k < J;
+      if constexpr (Epi::kTrans) {
+        // block (ta, tb) of dW^T holds dW rows j0 + .. + 32 tb (d_out) and
+        // columns i0 + .. + 32 ta (d_in), laid out as a block of dW
+        n = j0 + wj * 32 * WJ + tb * 32 + sr_r + 16 * u;
+        k = i0 + wi * 32 * WI + ta * 32 + 8 * sr_c;
+        return n < J && k < I;
+      } else {
+        n = i0 + wi * 32 * WI + ta * 32 + sr_r + 16 * u;
+        k = j0 + wj * 32 * WJ + tb * 32 + 8 * sr_c;
+        return n < I && k < J;
+      }
     };
     if constexpr (Epi::kSR) {
 #pragma unroll
@@ -1561,6 +1573,11 @@ using namespace v3;
 #ifndef DX_PACKED_B
 #define DX_PACKED_B 0
 #endif
+// dW with the SR update formed transposed (X~^T dY, EpiSR<CF, true>): 1, or
+// as dY^T X~ (0)
+#ifndef DW_TRANS
+#define DW_TRANS 1
+#endif
 #ifndef UNPACK_T2_STRIP
 #define UNPACK_T2_STRIP 1
 #endif
@@ -2042,9 +2059,10 @@ static hipError_t launch_dw_sr_group(const BatchCfg& c, const LinearIO* io, cons
                                uint32_t step, unsigned long long* counters, uint8_t* ws,
                                const BwdPlan& P, const int* first, Group<EpiScale>* gx,
                                hipStream_t stream) {
-  Group<EpiSR<CF>> gw{};
+  constexpr bool TR = DW_TRANS != 0;
+  Group<EpiSR<CF, TR>> gw{};
   fill_dw(c, io, ws, P, first, gw, [&](int l) {
-    EpiSR<CF> e;
+    EpiSR<CF, TR> e;
     e.wq = t[l].wq;
     e.ldc = io[l].d_in / 8 * chunk_code_bytes<CF>();
     e.d_in = io[l].d_in;
@@ -2059,9 +2077,25 @@ static hipError_t launch_dw_sr_group(const BatchCfg& c, const LinearIO* io, cons
     e.counters = counters;
     return e;
   });
-  if (gx != nullptr)
-    return launch_dual<EBF16, KM, KC, KB_BWD, EpiSR<CF>, EBF16, KC, KC, KB_BWD, EpiScale>(gw, *gx, ws, stream);
-  return launch_group<EBF16, KM, KC, KB_BWD, EpiSR<CF>>(gw, ws, stream);
+  if constexpr (TR) {
+    // dW^T = X~^T dY: X~^T [d_in][Mp] (K-contiguous) as the first operand,
+    // dY [M][d_out] (K-major) as the second
+    for (int l = 0; l < c.n; ++l) {
+      Prob<EpiSR<CF, TR>>& p = gw.p[l];
+      const int64_t I = io[l].d_in, J = io[l].d_out;
+      p.A = Opnd{ws + P.xt_off[first[l]], xt_stride(c.M) * 2, I};
+      p.B = Opnd{static_cast<const uint8_t*>(io[l].dY), J * 2, J};
+      p.I = I;
+      p.J = J;
+    }
+    if (gx != nullptr)
+      return launch_dual<EBF16, KC, KM, KB_BWD, EpiSR<CF, TR>, EBF16, KC, KC, KB_BWD, EpiScale>(gw, *gx, ws, stream);
+    return launch_group<EBF16, KC, KM, KB_BWD, EpiSR<CF, TR>>(gw, ws, stream);
+  } else {
+    if (gx != nullptr)
+      return launch_dual<EBF16, KM, KC, KB_BWD, EpiSR<CF>, EBF16, KC, KC, KB_BWD, EpiScale>(gw, *gx, ws, stream);
+    return launch_group<EBF16, KM, KC, KB_BWD, EpiSR<CF>>(gw, ws, stream);
+  }
 }
 
 hipError_t launch_bwd_sr_batch(const BatchCfg& c, const LinearIO* io, const SRTensor* t, uint64_t seed,
