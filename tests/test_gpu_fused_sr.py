@@ -42,6 +42,11 @@ CASES = [
     (640, [(128, 128, 0, True), (128, 256, 0, True), (128, 64, 0, True), (256, 128, 1, True),
            (64, 128, 2, True), (128, 192, 0, True), (256, 64, 1, False), (64, 64, 2, True)],
      "ternary", -1, 1, "i8", 1e-2, None),
+    # widths that are not multiples of 32 (partial 32-wide blocks of dW in
+    # both directions), a token count that is not a multiple of 64
+    (300, [(80, 48, 0, True), (48, 272, 1, True), (208, 80, 2, False)], "ternary", -1, 1, "i8",
+     5e-3, None),
+    (200, [(16, 96, 0, True), (272, 16, 1, True)], "i8", -127, 127, "e4m3", 5e-3, None),
     # 4-bit codes (ragged batch, dX for all; and a batch-split dW)
     (1000, [(256, 384, 0, True), (384, 128, 1, True)], "i4", -8, 7, "i8", 2e-2, None),
     (4096, [(256, 256, 0, True)], "i4", -4, 3, "i8", 2e-2, (0, 9, 3)),
