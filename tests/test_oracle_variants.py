@@ -99,6 +99,21 @@ def test_outside_the_bottom_set_is_the_plain_update(mode):
     assert nch == int(np.count_nonzero(new != q))
 
 
+def test_non_finite_gradients_are_never_among_the_smallest_updates():
+    """The bottom-20 % threshold with non-finite gradients present equals the
+    k-th smallest |fl32(c g)| over the finite elements (k = floor(0.2 n) of
+    all n): a non-finite gradient ranks above every finite one."""
+    q, g = _case(30000, 6, -127, 127, scale=0.05)
+    g[[3, 400, 29999]] = [np.inf, -np.inf, np.nan]
+    lr, alpha = 1e-2, 0.004
+    c = np.float32(np.float32(lr) / np.float32(alpha))
+    fin = np.isfinite(g)
+    mags = np.sort(np.abs((c * g[fin]).astype(np.float32)))
+    k = int(np.floor(np.float64(np.float32(0.2)) * g.size))
+    tau = O.bottom_threshold(O.delta_keys(g, lr, alpha), 0.2)
+    assert tau == mags[k - 1].view(np.uint32)
+
+
 def test_frac_zero_is_the_plain_update():
     q, g = _case(5000, 4)
     a, *_ = O.update_variant(q, g, 1e-2, 0.01, -1, 1, 3, 3, 3, O.UPD_FORCE_CHANGE, 0.0)
